@@ -1,0 +1,23 @@
+"""CPU oracle for one Speculative Pipeline Decoding step (float64, numpy).
+
+TEST INFRASTRUCTURE ONLY: only tests/, the smoke check and the benchmark's CPU-baseline leg may
+import it. It shares no code with the GPU path; both draw their inputs from the `synth` module.
+
+Pins (what ties each function to something other than itself) are in tests/test_oracle_*.py:
+  model.rms_norm, model.silu, model.attend   -> torch.nn.functional routines, closed forms
+  model.rope                                 -> complex-rotation form, norm and relative-position
+                                                invariants
+  model.decoder_layer / ar_greedy            -> the transformers Llama implementation of the same
+                                                architecture; brute-force forward_full
+  spd.SPDOracle.step                         -> n=1 equals plain greedy decode; brute-force
+                                                recomputation of every in-flight state; lossless
+                                                greedy stream; staircase of Eq. steady-g/warmup-g;
+                                                worked indices of Figure 1; closed forms for
+                                                special weights
+  spd.simulate_steps                         -> exact step counts of the oracle under forced masks
+Parity unpinned: the PDM's draft quality (it has random weights); only its definition is pinned.
+"""
+from .model import (LayerCache, Model, ar_greedy, argmax_first, attend, decoder_layer, embed,
+                    forward_full, lm_logits, rms_norm, rope, rope_angles, round_bf16, silu)
+from .spd import (ACCEPT, NONE, REJECT, SPDOracle, StepResult, eligible_anchors, l_max, run_spd,
+                  simulate_steps, stage_bounds)

@@ -1,0 +1,286 @@
+"""Oracle, part 2: one Speculative Pipeline Decoding step, in float64 on the CPU.
+
+TEST INFRASTRUCTURE ONLY (see oracle/model.py).
+
+What it follows:
+  * Token-level pipeline (Section 3.1): the L layers form n contiguous stages; each step advances
+    every in-flight token of one sequence through one stage. Boundaries beta_s = floor(s*L/n)
+    (the uniform split of Section 4.1 extended to n not dividing L).
+  * Depth staircase (Eq. steady-g and Eq. warmup-g): a token at depth k has completed k stages.
+    Pre-step, the a in-flight tokens at positions c..c+a-1 have depths a-1..0; positions < c are
+    complete (depth n).
+  * Multi-depth feature aggregation (Eq. depth-to-type and Eq. agg-main) with the anchor set
+    B = (beta_0, ..., beta_{n-1}) (the stage inputs) and one projection W_in of width n*d:
+    f(k) = min(k, n-1) anchors are eligible at depth k, and FC_{f(k)} is W_in applied to the
+    concatenation of the eligible anchors with the ineligible blocks set to zero. No bias and no
+    normalisation before the concatenation.
+  * Pre-step schedule (Section 3.3): the PDM reads only features present before the step, so it
+    runs concurrently with the stage compute; its L_s decoder layers run causally over the feature
+    sequence; rows < c are final (their PDM KV rows persist), rows c..c+a-1 are recomputed each
+    step. The draft is the argmax of the shared LM head over the PDM's last row after its own
+    final RMSNorm (gain 1).
+  * Streaming greedy verification and rollback (Section 3.4): when the pipeline is full (a = n)
+    the oldest token exits; its logits judge the next in-flight token. Accept: the draft enters
+    stage 1. Reject: caches keep the committed prefix only, in-flight work is dropped, and the
+    target's own argmax is reseeded at depth 0. With n = 1 the judged token is this step's own
+    draft, so the step is ordinary greedy decoding. While a < n (warm-up or refill) nothing exits
+    and the draft is pushed unconditionally.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Callable, Dict, List, Optional, Sequence
+
+import numpy as np
+
+import synth
+from .model import (LayerCache, Model, argmax_first, decoder_layer, embed, lm_logits, new_caches)
+
+NONE, ACCEPT, REJECT = 0, 1, 2
+
+
+def stage_bounds(n_layers: int, n: int) -> List[int]:
+    """beta_0 = 0 < beta_1 < ... < beta_n = L, with beta_s = floor(s * L / n)."""
+    assert 1 <= n <= n_layers
+    return [s * n_layers // n for s in range(n + 1)]
+
+
+def l_max(k: int, n_layers: int, n: int) -> float:
+    """Deepest layer available to a token that has completed k stages (Eq. before depth-to-type)."""
+    return min(n_layers, k * n_layers / n)
+
+
+def eligible_anchors(k: int, anchors: Sequence[int], n_layers: int, n: int) -> int:
+    """f(k) = max{i : b_i <= l_max(k)} (Eq. depth-to-type)."""
+    lm = l_max(k, n_layers, n)
+    return max(i for i, b in enumerate(anchors) if b <= lm)
+
+
+@dataclasses.dataclass
+class StepResult:
+    decision: int
+    target_argmax: int  # y (or -1 when nothing exited)
+    draft: int  # the token the PDM proposed (after any forced override)
+    pdm_draft: int  # the PDM's own argmax
+    exited_pos: int
+    verified_pos: int
+    verified_token: int
+    c: int
+    a: int
+    exit_logits: Optional[np.ndarray] = None
+    pdm_logits: Optional[np.ndarray] = None
+    pdm_hidden: Optional[Dict[int, np.ndarray]] = None
+    depths: Optional[Dict[int, int]] = None  # pre-step depth of every row the PDM read
+
+
+class SPDOracle:
+    """SPD state for one sequence: target KV per layer, PDM KV per PDM layer, in-flight tokens."""
+
+    def __init__(self, model: Model, n: Optional[int] = None, pdm_layers: Optional[int] = None):
+        model = model.for_width(model.shape.n_stages if n is None else n, pdm_layers)
+        sh = model.shape
+        self.m = model
+        self.sh = sh
+        self.n = sh.n_stages
+        self.ls = sh.pdm_layers
+        self.L = sh.n_layers
+        self.beta = stage_bounds(self.L, self.n)
+        self.anchor_layers = self.beta[: self.n]  # B = stage inputs
+        self.caches = new_caches(sh, self.L)
+        self.pdm_caches = new_caches(sh, self.ls)
+        self.toks: List[int] = []
+        self.hidden: Dict[int, np.ndarray] = {}  # in-flight residual streams by position
+        self.anch: Dict[int, List[np.ndarray]] = {}  # in-flight anchors by position
+        self.c = 0
+        self.a = 0
+        self.prompt_len = 0
+        self.steps = 0
+        self.verified = 0  # N: prefill token + one per exit
+
+    # ------------------------------------------------------------------ PDM pieces
+    def w_in(self) -> np.ndarray:
+        w = self.m.w("pdm.in")
+        assert w.shape == (self.sh.d_model, self.n * self.sh.d_model)
+        return w
+
+    def feature(self, anchors: List[np.ndarray], k: int) -> np.ndarray:
+        """g^k = FC_{f(k)}(Concat(H^{b_0..b_f(k)})): W_in over the eligible anchors, zeros elsewhere."""
+        d = self.sh.d_model
+        f = eligible_anchors(k, self.anchor_layers, self.L, self.n)
+        z = np.zeros(self.n * d)
+        for j in range(f + 1):
+            z[j * d:(j + 1) * d] = anchors[j]
+        return self.w_in() @ z
+
+    def pdm_row(self, g: np.ndarray, pos: int) -> np.ndarray:
+        h = g
+        for i in range(self.ls):
+            h = decoder_layer(self.sh, self.m.layer(i, "pdm.layer"), h, pos, self.pdm_caches[i])
+        return h
+
+    # ------------------------------------------------------------------ prefill
+    def prefill(self, prompt) -> int:
+        """Process the prompt through the target (keeping the anchors), build the PDM KV over it
+        with full-depth features, and place the target's first token in flight at depth 0."""
+        prompt = [int(t) for t in prompt]
+        P = len(prompt)
+        assert P >= 1
+        h = None
+        for p, t in enumerate(prompt):
+            h, kept = self._run_stage_range(embed(self.m, t), p, 0, self.n, capture=True)
+            self.pdm_row(self.feature(kept, self.n), p)
+        x = argmax_first(lm_logits(self.m, h))
+        self.toks = prompt + [x]
+        self.prompt_len = P
+        self.c = P
+        self._push(x, P)
+        self.a = 1
+        self.steps = 0
+        self.verified = 1
+        return x
+
+    def _run_stage_range(self, h, pos, s0, s1, capture=False, anchors=None):
+        """Run stages s0..s1-1 on one token; anchors[j] := H^{beta_j} as each stage completes."""
+        kept = list(anchors) if anchors is not None else [h.copy()]
+        for s in range(s0, s1):
+            for l in range(self.beta[s], self.beta[s + 1]):
+                h = decoder_layer(self.sh, self.m.layer(l), h, pos, self.caches[l])
+            if s + 1 <= self.n - 1:
+                if len(kept) == s + 1:
+                    kept.append(h.copy())
+                else:
+                    kept[s + 1] = h.copy()
+        return (h, kept) if capture else h
+
+    def _push(self, tok: int, pos: int) -> None:
+        e = embed(self.m, tok)
+        self.hidden[pos] = e.copy()
+        self.anch[pos] = [e.copy()]
+
+    # ------------------------------------------------------------------ one step
+    def depth(self, pos: int) -> int:
+        return self.a - 1 - (pos - self.c) if pos >= self.c else self.n
+
+    def step(self, forced_draft: Optional[int] = None, want_logits: bool = False) -> StepResult:
+        c, a, n = self.c, self.a, self.n
+        depths = {q: self.depth(q) for q in range(0, c + a)}
+
+        # --- PDM on pre-step features: rows c..c+a-1 rewritten, rows < c kept
+        for pc in self.pdm_caches:
+            pc.truncate(c)
+        pdm_h = {}
+        for i in range(a):
+            q = c + i
+            g = self.feature(self.anch[q], a - 1 - i)
+            pdm_h[q] = self.pdm_row(g, q)
+        pdm_lg = lm_logits(self.m, pdm_h[c + a - 1], "pdm.norm")
+        pdm_draft = argmax_first(pdm_lg)
+        draft = pdm_draft if forced_draft is None else int(forced_draft)
+
+        # --- target: the token at depth s runs stage s
+        for i in range(a):
+            q = c + i
+            s = a - 1 - i
+            h, kept = self._run_stage_range(self.hidden[q], q, s, s + 1, capture=True, anchors=self.anch[q])
+            self.hidden[q] = h
+            self.anch[q] = kept
+
+        self.steps += 1
+        res = StepResult(NONE, -1, draft, pdm_draft, -1, -1, -1, 0, 0, depths=depths,
+                         pdm_hidden=pdm_h)
+        if want_logits:
+            res.pdm_logits = pdm_lg
+        if a == n:
+            lg = lm_logits(self.m, self.hidden[c])
+            y = argmax_first(lg)
+            succ = self.toks[c + 1] if n >= 2 else draft
+            res.target_argmax, res.exited_pos, res.verified_pos, res.verified_token = y, c, c + 1, y
+            if want_logits:
+                res.exit_logits = lg
+            del self.hidden[c], self.anch[c]
+            self.c = c + 1
+            self.verified += 1
+            if succ == y:
+                res.decision = ACCEPT
+                q = c + a  # the draft's position
+                self._set_tok(q, draft)
+                self._push(draft, q)
+            else:
+                res.decision = REJECT
+                self._truncate_to(self.c)
+                self._set_tok(self.c, y)
+                self._push(y, self.c)
+                self.a = 1
+        else:
+            q = c + a
+            self._set_tok(q, draft)
+            self._push(draft, q)
+            self.a = a + 1
+        res.c, res.a = self.c, self.a
+        return res
+
+    def _set_tok(self, q: int, t: int) -> None:
+        if q < len(self.toks):
+            self.toks[q] = t
+            del self.toks[q + 1:]
+        else:
+            assert q == len(self.toks)
+            self.toks.append(t)
+
+    def _truncate_to(self, keep: int) -> None:
+        for cch in self.caches:
+            cch.truncate(min(cch.n, keep))
+        for pc in self.pdm_caches:
+            pc.truncate(min(pc.n, keep))
+        for q in [q for q in self.hidden if q >= keep]:
+            del self.hidden[q], self.anch[q]
+        del self.toks[keep:]
+
+    def rollback(self, keep_len: int, reseed: int) -> None:
+        """Keep positions < keep_len in every cache, drop in-flight work, reseed at keep_len."""
+        assert self.prompt_len <= keep_len <= self.c
+        self.c = keep_len
+        self._truncate_to(keep_len)
+        self._set_tok(keep_len, int(reseed))
+        self._push(int(reseed), keep_len)
+        self.a = 1
+
+    # ------------------------------------------------------------------ views
+    def generated(self) -> List[int]:
+        """Verified tokens after the prompt: positions prompt_len..c (tok[c] is always verified)."""
+        return self.toks[self.prompt_len: self.c + 1]
+
+    def kv_lengths(self) -> List[int]:
+        return [cc.n for cc in self.caches]
+
+    def alpha(self) -> float:
+        """Step acceptance ratio N/K (Section 4.2), N counting generated tokens."""
+        return self.verified / max(1, self.steps)
+
+
+def run_spd(model: Model, prompt, n_tokens: int, n: Optional[int] = None,
+            draft_for: Optional[Callable[[int], Optional[int]]] = None, max_steps: int = 100000):
+    """Run SPD until n_tokens generated tokens are verified. draft_for(position) may force drafts.
+
+    Returns (oracle, list of StepResult)."""
+    o = SPDOracle(model, n=n)
+    o.prefill(prompt)
+    results = []
+    while o.verified < n_tokens and len(results) < max_steps:
+        q = o.c + o.a
+        fd = draft_for(q) if draft_for is not None else None
+        results.append(o.step(forced_draft=fd))
+    return o, results
+
+
+def simulate_steps(n: int, n_tokens: int, accept_at: Callable[[int], bool], prompt_len: int) -> int:
+    """Step count from the pipeline's timing alone: the first exit is n steps after prefill; after
+    an exit verifying position q the next exit comes 1 step later if q was accepted, n if not."""
+    if n_tokens <= 1:
+        return 0
+    t, verified, q = n, 2, prompt_len + 1  # the exit at step n verifies position prompt_len+1
+    while verified < n_tokens:
+        t += 1 if accept_at(q) else n
+        q += 1
+        verified += 1
+    return t
