@@ -1,0 +1,215 @@
+/*
+ * spd.h — C ABI of the single-GPU Speculative Pipeline Decoding (SPD) step for MI355X (gfx950).
+ *
+ * The calls follow the method's statement of decoding: a prompt is processed (prefill), then each
+ * pipeline step advances every in-flight token of one sequence through one stage of the target
+ * (Section 3.1, token-level pipeline), while the Pipeline Draft Module drafts the next token from
+ * pre-step multi-depth features (Sections 3.2-3.3, Eq. input-seq, Eq. agg-main); when the pipeline
+ * is full the oldest token exits and its logits verify the next in-flight token, with rollback on
+ * a mismatch (Section 3.4).
+ *
+ * Conventions shared by every entry point:
+ *   - Ownership: the caller owns all device memory (weights, workspace) and both streams; they must
+ *     outlive the handle. The library never frees caller memory and allocates only small host
+ *     buffers (pinned result staging) and two events per handle.
+ *   - Pointers marked "device" are HIP device addresses on the current device; "host" pointers are
+ *     ordinary host memory. hipStream_t arguments are passed as void*.
+ *   - Errors: every call returns spd_status; no C++ exception crosses the ABI. SPD_E_INVAL: bad
+ *     argument; SPD_E_STATE: call not legal in the handle's state; SPD_E_CAPACITY: max_tokens or the
+ *     workspace is too small; SPD_E_HIP: a HIP call failed (spd_last_error() has the message). On
+ *     SPD_E_INVAL, SPD_E_STATE and SPD_E_CAPACITY the handle is unchanged.
+ *   - Threads: one handle is used by one host thread at a time.
+ */
+#ifndef SPD_H
+#define SPD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum spd_status {
+  SPD_OK = 0,
+  SPD_E_INVAL = 1,
+  SPD_E_STATE = 2,
+  SPD_E_CAPACITY = 3,
+  SPD_E_HIP = 4
+} spd_status;
+
+/* Storage type of weights (norm gains are always fp32) and of the KV caches. */
+typedef enum spd_dtype { SPD_F32 = 0, SPD_BF16 = 1 } spd_dtype;
+
+/* Outcome of one step (Section 3.4): NONE while the pipeline is filling (no token exits),
+ * ACCEPT when the exiting token's greedy successor equals the in-flight token behind it,
+ * REJECT otherwise (caches roll back to the committed prefix and the target's token is reseeded). */
+typedef enum spd_decision { SPD_NONE = 0, SPD_ACCEPT = 1, SPD_REJECT = 2 } spd_decision;
+
+/* Model and run configuration. The target is a pre-norm dense decoder with grouped-query attention,
+ * rotate-half RoPE, RMSNorm and a SwiGLU MLP, no biases, untied embedding and LM head. Limits:
+ * d_model, n_q_heads*head_dim and ffn_dim are multiples of 8; head_dim is 64 or 128;
+ * n_q_heads = G * n_kv_heads with G in {1, 2, 4, 8}; 1 <= n_stages <= min(8, n_layers);
+ * 1 <= pdm_layers <= 4; page_size is 16. */
+typedef struct spd_config {
+  int32_t n_layers;      /* L */
+  int32_t d_model;       /* d */
+  int32_t n_q_heads;     /* Hq */
+  int32_t n_kv_heads;    /* Hkv */
+  int32_t head_dim;      /* dh */
+  int32_t ffn_dim;       /* F */
+  int32_t vocab;         /* V */
+  float rms_eps;         /* RMSNorm epsilon */
+  float rope_base;       /* RoPE base: theta_j = base^(-2j/dh) */
+  int32_t dtype;         /* spd_dtype */
+  int32_t n_stages;      /* SPD width n: stage s holds layers [floor(sL/n), floor((s+1)L/n)) */
+  int32_t pdm_layers;    /* L_s, decoder layers of the PDM */
+  int32_t page_size;     /* KV page, in tokens */
+  int32_t max_tokens;    /* capacity in positions: prompt + generated + n */
+  int32_t auto_rollback; /* 1: spd_step applies the rollback of a REJECT itself (needed for
+                            spd_run_steps); 0: a REJECT leaves the handle waiting for spd_rollback */
+  int32_t attn_chunk;    /* keys per attention split, a multiple of page_size; 0 picks it from
+                            max_tokens. Results depend on it, so compare runs with equal values. */
+  uint64_t page_seed;    /* 0: physical KV pages are handed out in order; else in an order
+                            shuffled with this seed (exercises the page table) */
+} spd_config;
+
+/* One decoder layer's weights, all device pointers, row-major [out x in]:
+ * attn_norm, mlp_norm: fp32 [d]; wq: [Hq*dh x d]; wk, wv: [Hkv*dh x d]; wo: [d x Hq*dh];
+ * wg, wu: [F x d]; wd: [d x F]. Matrices are in the config's dtype, 16-byte aligned. */
+typedef struct spd_layer_weights {
+  const void* attn_norm;
+  const void* wq;
+  const void* wk;
+  const void* wv;
+  const void* wo;
+  const void* mlp_norm;
+  const void* wg;
+  const void* wu;
+  const void* wd;
+} spd_layer_weights;
+
+/* All weights. `layers` and `pdm_layers` are HOST arrays (n_layers and pdm_layers entries) of device
+ * pointers; they are copied during spd_init. embed, lm_head: [V x d]; final_norm, pdm_norm: fp32 [d];
+ * pdm_in: [d x n*d], the PDM's feature projection (Eq. agg-main): column block j multiplies the
+ * anchor H^{beta_j} (the input of stage j). The PDM shares the target's lm_head. */
+typedef struct spd_weights {
+  const void* embed;
+  const spd_layer_weights* layers;
+  const void* final_norm;
+  const void* lm_head;
+  const void* pdm_in;
+  const spd_layer_weights* pdm_layers;
+  const void* pdm_norm;
+} spd_weights;
+
+/* Result of one step. Positions are 0-based. committed_len = c, the number of positions that have
+ * passed all L layers; inflight = a, tokens in the pipeline at positions c..c+a-1. */
+typedef struct spd_step_result {
+  int32_t decision;       /* spd_decision */
+  int32_t target_argmax;  /* y: greedy successor of the exiting token, -1 if none exited */
+  int32_t draft;          /* token pushed at depth 0 (the PDM's draft unless forced); -1 on REJECT */
+  int32_t pdm_draft;      /* the PDM's own argmax */
+  int32_t exited_pos;     /* position that left the last stage, -1 if none */
+  int32_t verified_pos;   /* position judged this step, -1 if none */
+  int32_t verified_token; /* token now committed at verified_pos (equals target_argmax) */
+  int32_t committed_len;  /* c after the step */
+  int32_t inflight;       /* a after the step (0 while a rollback is pending) */
+  int32_t step_index;     /* steps taken since prefill, counting this one */
+} spd_step_result;
+
+typedef struct spd_handle spd_handle;
+
+/* Bytes of device workspace spd_init needs for cfg (KV pools, page table, RoPE table, in-flight
+ * activations and scratch). Host-only: touches no GPU. */
+spd_status spd_workspace_size(const spd_config* cfg, size_t* bytes);
+
+/* Stage boundaries beta_0..beta_n (host array of n_stages+1 ints), beta_s = floor(s*L/n)
+ * (Section 3.1 uniform split, Section 4.1). Host-only. */
+spd_status spd_stage_bounds(const spd_config* cfg, int32_t* beta);
+
+/* Bind weights and workspace, build the tables (RoPE cos/sin in double precision rounded to fp32,
+ * page table, layer table) and return a handle. workspace: device, >= spd_workspace_size bytes,
+ * 256-byte aligned. main_stream runs the stage compute, pdm_stream the draft module (they must
+ * differ; both default priority). */
+spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace, size_t ws_bytes,
+                    void* main_stream, void* pdm_stream, spd_handle** out);
+
+/* Process the prompt (host int32[len], ids in [0, V)) through the target, keeping the stage-input
+ * hidden states as PDM anchors, build the PDM KV over the prompt with full-depth features, and
+ * place the target's greedy token x_len in flight at depth 0. Writes x_len to *first_token.
+ * Legal once, right after spd_init. Synchronous. */
+spd_status spd_prefill(spd_handle* h, const int32_t* prompt, int32_t len, int32_t* first_token);
+
+/* One pipeline step (Section 3.1-3.4): PDM on pdm_stream over pre-step features, every active
+ * stage on main_stream, exit + greedy verify when the pipeline is full. forced_draft (host, may be
+ * NULL) replaces the PDM's draft for this step; the PDM still runs. Synchronous: returns after the
+ * result is on the host. SPD_E_STATE before prefill or while a rollback is pending. */
+spd_status spd_step(spd_handle* h, const int32_t* forced_draft, spd_step_result* out);
+
+/* Keep positions < keep_len in every target and PDM cache, drop all in-flight work and put
+ * reseed_token in flight at position keep_len, depth 0 (Section 3.4 with keep_len = t-n+1).
+ * Requires prompt_len <= keep_len <= c and 0 <= reseed_token < V. */
+spd_status spd_rollback(spd_handle* h, int32_t keep_len, int32_t reseed_token);
+
+/* Per-position draft override table used by spd_step and spd_run_steps: for each position
+ * first_pos+i with table[i] >= 0 the draft pushed at that position is table[i]. table: host. */
+spd_status spd_set_forced_drafts(spd_handle* h, const int32_t* table, int32_t first_pos, int32_t len);
+spd_status spd_clear_forced_drafts(spd_handle* h);
+
+/* Enqueue `count` steps without host synchronisation (needs auto_rollback = 1). If log is not
+ * NULL (host, count entries) the call waits and fills it with each step's result; otherwise it
+ * returns once the work is enqueued and spd_sync() waits. */
+spd_status spd_run_steps(spd_handle* h, int32_t count, spd_step_result* log);
+
+/* Wait for all enqueued work; if last is not NULL store the latest step result there. */
+spd_status spd_sync(spd_handle* h, spd_step_result* last);
+
+/* Debug and parity reads (synchronous; host destination). what:
+ *   SPD_DBG_RESID:       n*d fp32, in-flight residual streams; position q lives in row q mod n
+ *   SPD_DBG_ANCHORS:     n*n*d fp32, [row q mod n][anchor j][d], anchor j = H^{beta_j}
+ *   SPD_DBG_PDM_HIDDEN:  8*d fp32, the PDM's output rows of the last step (row i = position c+i)
+ *   SPD_DBG_EXIT_LOGITS: V fp32, target logits of the last exiting token (needs spd_set_debug)
+ *   SPD_DBG_PDM_LOGITS:  V fp32, the PDM's logits of the last step (needs spd_set_debug)
+ *   SPD_DBG_TOKENS:      max_tokens int32, token id per position
+ *   SPD_DBG_STATE:       4 int32: c, a, prompt_len, steps
+ * bytes must equal the size listed. */
+enum {
+  SPD_DBG_RESID = 1,
+  SPD_DBG_ANCHORS = 2,
+  SPD_DBG_PDM_HIDDEN = 3,
+  SPD_DBG_EXIT_LOGITS = 4,
+  SPD_DBG_PDM_LOGITS = 5,
+  SPD_DBG_TOKENS = 6,
+  SPD_DBG_STATE = 7
+};
+spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes);
+
+/* Copy K and V of positions [pos0, pos0+count) of one layer (pdm = 0: target layer, 1: PDM layer)
+ * to host arrays [count x Hkv x dh] in the config's dtype. */
+spd_status spd_read_kv(spd_handle* h, int32_t pdm, int32_t layer, int32_t pos0, int32_t count,
+                       void* host_k, void* host_v);
+
+/* 1: every LM-head pass also writes its full logits (for SPD_DBG_*_LOGITS). */
+spd_status spd_set_debug(spd_handle* h, int32_t on);
+
+/* Kernel timing for roofline measurements. kernel selects one launch class of the stage compute on
+ * main_stream (SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD; 0 turns timing
+ * off). While on, every launch of that class is bracketed by two HIP events on main_stream.
+ * spd_kernel_timing waits for the stream, returns the summed event time in milliseconds and the
+ * number of timed launches, and clears both. */
+enum { SPD_K_QKV = 1, SPD_K_ATTN = 2, SPD_K_OPROJ = 3, SPD_K_GATEUP = 4, SPD_K_DOWN = 5, SPD_K_HEAD = 6 };
+spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel);
+spd_status spd_kernel_timing(spd_handle* h, double* total_ms, int32_t* launches);
+
+/* Release the handle's events and host buffers (not the caller's memory). NULL is ignored. */
+void spd_destroy(spd_handle* h);
+
+const char* spd_status_str(spd_status s);
+/* Message of the last failure on this handle ("" if none); NULL handle: last spd_init failure. */
+const char* spd_last_error(const spd_handle* h);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPD_H */

@@ -1,0 +1,719 @@
+// Host side of the C ABI: argument checks, workspace carving, tables, and the launch sequence of
+// prefill and of one pipeline step on the caller's two streams.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <random>
+#include <string>
+#include <vector>
+
+#include "spd.h"
+#include "spd_dev.h"
+
+using namespace spd;
+
+namespace {
+
+thread_local std::string g_init_error;
+
+enum HState { H_INIT = 0, H_READY = 1, H_PENDING = 2 };
+
+struct Layout {
+  size_t kv, pkv, pt, rope, state, tok, forced, log, resid, anch, pdmx, pfx, pfanch, dbg, lay;
+  size_t q[2], ao[2], act[2], part[2], cnt[2], hpv[2], hpi[2], hcnt[2];
+  size_t total;
+  int num_pages, chunk, max_splits, head_tiles;
+  size_t kv_layer_bytes;
+};
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+spd_status check_config(const spd_config* c, std::string* why) {
+  auto bad = [&](const char* m) {
+    if (why) *why = m;
+    return SPD_E_INVAL;
+  };
+  if (!c) return bad("config is NULL");
+  if (c->n_layers < 1 || c->d_model < 8 || c->n_q_heads < 1 || c->n_kv_heads < 1 || c->ffn_dim < 8 ||
+      c->vocab < 1)
+    return bad("dimensions must be positive");
+  if (c->head_dim != 64 && c->head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (c->n_q_heads % c->n_kv_heads) return bad("n_q_heads must be a multiple of n_kv_heads");
+  const int G = c->n_q_heads / c->n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return bad("n_q_heads / n_kv_heads must be 1, 2, 4 or 8");
+  if (c->d_model % 8 || c->ffn_dim % 8 || (c->n_q_heads * c->head_dim) % 8)
+    return bad("d_model, ffn_dim and n_q_heads*head_dim must be multiples of 8");
+  if (c->dtype != SPD_F32 && c->dtype != SPD_BF16) return bad("dtype must be SPD_F32 or SPD_BF16");
+  if (c->n_stages < 1 || c->n_stages > kMaxStages || c->n_stages > c->n_layers)
+    return bad("n_stages must be in [1, min(8, n_layers)]");
+  if (c->pdm_layers < 1 || c->pdm_layers > kMaxPdmLayers) return bad("pdm_layers must be in [1, 4]");
+  if (c->page_size != 16) return bad("page_size must be 16");
+  if (c->max_tokens < c->n_stages + 2) return bad("max_tokens too small");
+  if (c->max_tokens > (1 << 20)) return bad("max_tokens too large");
+  if (c->attn_chunk < 0 || (c->attn_chunk && (c->attn_chunk % c->page_size)))
+    return bad("attn_chunk must be 0 or a multiple of page_size");
+  if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return bad("rms_eps must be > 0 and rope_base > 1");
+  if (c->auto_rollback != 0 && c->auto_rollback != 1) return bad("auto_rollback must be 0 or 1");
+  return SPD_OK;
+}
+
+Layout make_layout(const spd_config& c) {
+  Layout L{};
+  const size_t esz = c.dtype == SPD_BF16 ? 2 : 4;
+  const int n = c.n_stages, d = c.d_model, dh = c.head_dim, hkv = c.n_kv_heads;
+  const int qdim = c.n_q_heads * dh;
+  const int G = c.n_q_heads / hkv;
+  L.num_pages = (c.max_tokens + c.page_size - 1) / c.page_size;
+  L.chunk = c.attn_chunk ? c.attn_chunk : (c.max_tokens <= 4096 ? 64 : (c.max_tokens <= 16384 ? 128 : 256));
+  L.max_splits = (c.max_tokens + L.chunk - 1) / L.chunk;
+  L.head_tiles = (c.vocab + 15) / 16;
+  L.kv_layer_bytes = (size_t)L.num_pages * 2 * hkv * c.page_size * dh * esz;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o = align_up(o + bytes, 256);
+    return at;
+  };
+  L.kv = take(L.kv_layer_bytes * c.n_layers);
+  L.pkv = take(L.kv_layer_bytes * c.pdm_layers);
+  L.pt = take(sizeof(int32_t) * L.num_pages);
+  L.rope = take(sizeof(float) * 2 * (size_t)c.max_tokens * (dh / 2));
+  L.state = take(sizeof(DevState));
+  L.tok = take(sizeof(int32_t) * (c.max_tokens + 8));
+  L.forced = take(sizeof(int32_t) * (c.max_tokens + 8));
+  L.log = take(sizeof(spd_step_result) * kLogCap);
+  L.resid = take(sizeof(float) * n * d);
+  L.anch = take(sizeof(float) * n * n * d);
+  L.pdmx = take(sizeof(float) * kMaxRows * d);
+  L.pfx = take(sizeof(float) * kMaxRows * d);
+  L.pfanch = take(sizeof(float) * kMaxRows * n * d);
+  L.dbg = take(sizeof(float) * 2 * (size_t)c.vocab);
+  L.lay = take(sizeof(LayerDesc) * (c.n_layers + c.pdm_layers));
+  const size_t part_floats = (size_t)64 * hkv * L.max_splits * (dh + 2);
+  (void)G;
+  for (int s = 0; s < 2; s++) {
+    L.q[s] = take(sizeof(float) * kMaxRows * qdim);
+    L.ao[s] = take(sizeof(float) * kMaxRows * qdim);
+    L.act[s] = take(sizeof(float) * kMaxRows * (size_t)c.ffn_dim);
+    L.part[s] = take(sizeof(float) * part_floats);
+    L.cnt[s] = take(sizeof(int32_t) * kMaxStages * hkv);
+    L.hpv[s] = take(sizeof(float) * L.head_tiles);
+    L.hpi[s] = take(sizeof(int32_t) * L.head_tiles);
+    L.hcnt[s] = take(sizeof(int32_t) * 64);
+  }
+  L.total = o;
+  return L;
+}
+
+void stage_bounds(int L, int n, int* beta) {
+  for (int s = 0; s <= n; s++) beta[s] = (int)((long long)s * L / n);
+}
+
+}  // namespace
+
+struct spd_handle {
+  spd_config cfg;
+  Layout lay;
+  Ctx ctx;
+  int dev = 0;
+  int bf16 = 0;
+  int J = 0;  // layer slots per step = longest stage
+  hipStream_t main = nullptr, pdm = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  char* ws = nullptr;
+  int hstate = H_INIT;
+  int c = 0, a = 0, prompt_len = 0;
+  int unsynced = 0;     // steps were enqueued since the host last read c and a
+  long long bound = 0;  // upper bound of c + a (each step raises c + a by at most one)
+  spd_step_result* pinned = nullptr;  // [kLogCap + 1]
+  std::vector<int32_t> page_table;
+  std::string err;
+  // kernel timing
+  int timed_kernel = 0;
+  std::vector<hipEvent_t> tev;  // pool, pairs
+  size_t tev_used = 0;
+};
+
+#define HIPC(expr)                                                              \
+  do {                                                                          \
+    hipError_t e_ = (expr);                                                     \
+    if (e_ != hipSuccess) {                                                     \
+      h->err = std::string(#expr) + ": " + hipGetErrorString(e_);               \
+      return SPD_E_HIP;                                                         \
+    }                                                                           \
+  } while (0)
+
+static spd_status launch_check(spd_handle* h, const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    h->err = std::string("launch ") + what + ": " + hipGetErrorString(e);
+    return SPD_E_HIP;
+  }
+  return SPD_OK;
+}
+
+// Event pair around one launch when that launch class is being timed (main stream only).
+struct TimedLaunch {
+  spd_handle* h;
+  hipStream_t s;
+  bool on;
+  size_t idx;
+  TimedLaunch(spd_handle* hh, hipStream_t ss, int kind) : h(hh), s(ss), on(false), idx(0) {
+    if (!h || h->timed_kernel != kind || s != h->main) return;
+    if (h->tev_used + 2 > h->tev.size()) {
+      for (int i = 0; i < 64; i++) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return;
+        h->tev.push_back(e);
+      }
+    }
+    idx = h->tev_used;
+    h->tev_used += 2;
+    on = hipEventRecord(h->tev[idx], s) == hipSuccess;
+  }
+  ~TimedLaunch() {
+    if (on) (void)hipEventRecord(h->tev[idx + 1], s);
+  }
+};
+
+template <typename WT>
+static void enqueue_layer(const Ctx& C, const Rows& r, hipStream_t s, spd_handle* h = nullptr) {
+  { TimedLaunch t(h, s, SPD_K_QKV); Launch<WT>::qkv(C, r, s); }
+  { TimedLaunch t(h, s, SPD_K_ATTN); Launch<WT>::attn(C, r, s); }
+  { TimedLaunch t(h, s, SPD_K_OPROJ); Launch<WT>::oproj(C, r, s); }
+  { TimedLaunch t(h, s, SPD_K_GATEUP); Launch<WT>::gateup(C, r, s); }
+  { TimedLaunch t(h, s, SPD_K_DOWN); Launch<WT>::down(C, r, s); }
+}
+
+static Rows rows_block(int layer, int nrows, int pos0, float* x, float* anch, int cap, int set) {
+  Rows r;
+  r.kind = 1;
+  r.slot = 0;
+  r.layer = layer;
+  r.nrows = nrows;
+  r.pos0 = pos0;
+  r.x = x;
+  r.anch = anch;
+  r.cap = cap;
+  r.set = set;
+  return r;
+}
+
+template <typename WT>
+static spd_status enqueue_step(spd_handle* h, int forced_override) {
+  const Ctx& C = h->ctx;
+  HIPC(hipEventRecord(h->ev_fork, h->main));
+  HIPC(hipStreamWaitEvent(h->pdm, h->ev_fork, 0));
+  // Pipeline Draft Module on its own stream: pre-step features only (Section 3.3)
+  Launch<WT>::pdm_fc(C, 0, 0, h->pdm);
+  for (int i = 0; i < h->cfg.pdm_layers; i++)
+    enqueue_layer<WT>(C, rows_block(h->cfg.n_layers + i, -1, -1, C.pdm_x, nullptr, -1, 1), h->pdm);
+  Launch<WT>::head(C, 1, 0, h->pdm);
+  HIPC(hipEventRecord(h->ev_join, h->pdm));
+  // every active stage advances its token by one layer per slot (Section 3.1)
+  for (int j = 0; j < h->J; j++) {
+    Rows r;
+    r.kind = 0;
+    r.slot = j;
+    r.layer = 0;
+    r.nrows = 1;
+    r.pos0 = 0;
+    r.x = nullptr;
+    r.anch = nullptr;
+    r.cap = -1;
+    r.set = 0;
+    enqueue_layer<WT>(C, r, h->main, h);
+  }
+  {
+    TimedLaunch t(h, h->main, SPD_K_HEAD);
+    Launch<WT>::head(C, 0, 0, h->main);  // exit row, only when the pipeline is full
+  }
+  HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
+  launch_verify(C, forced_override, h->cfg.auto_rollback, h->main, h->bf16);
+  return launch_check(h, "step");
+}
+
+template <typename WT>
+static spd_status enqueue_prefill(spd_handle* h, int len) {
+  const Ctx& C = h->ctx;
+  const int n = h->cfg.n_stages, L = h->cfg.n_layers;
+  for (int t0 = 0; t0 < len; t0 += kMaxRows) {
+    const int rc = std::min(kMaxRows, len - t0);
+    Launch<WT>::embed_rows(C, t0, rc, h->main);
+    for (int l = 0; l < L; l++) {
+      int cap = -1;
+      for (int s = 0; s + 1 <= n - 1; s++)
+        if (l + 1 == C.beta[s + 1]) cap = s + 1;
+      enqueue_layer<WT>(C, rows_block(l, rc, t0, C.pf_x, C.pf_anch, cap, 0), h->main);
+    }
+    // PDM KV over the prompt: every prompt row has full depth
+    Launch<WT>::pdm_fc(C, 1, rc, h->main);
+    for (int i = 0; i < h->cfg.pdm_layers; i++)
+      enqueue_layer<WT>(C, rows_block(L + i, rc, t0, C.pdm_x, nullptr, -1, 1), h->main);
+    if (t0 + rc == len) Launch<WT>::head(C, 2, rc - 1, h->main);
+    spd_status st = launch_check(h, "prefill");
+    if (st != SPD_OK) return st;
+  }
+  launch_reseed(C, len, -1, len, h->main, h->bf16);
+  return launch_check(h, "prefill reseed");
+}
+
+extern "C" {
+
+const char* spd_status_str(spd_status s) {
+  switch (s) {
+    case SPD_OK: return "SPD_OK";
+    case SPD_E_INVAL: return "SPD_E_INVAL: invalid argument";
+    case SPD_E_STATE: return "SPD_E_STATE: call not legal in this state";
+    case SPD_E_CAPACITY: return "SPD_E_CAPACITY: capacity exceeded";
+    case SPD_E_HIP: return "SPD_E_HIP: HIP runtime error";
+  }
+  return "unknown spd_status";
+}
+
+const char* spd_last_error(const spd_handle* h) { return h ? h->err.c_str() : g_init_error.c_str(); }
+
+spd_status spd_workspace_size(const spd_config* cfg, size_t* bytes) {
+  if (!bytes) return SPD_E_INVAL;
+  spd_status st = check_config(cfg, &g_init_error);
+  if (st != SPD_OK) return st;
+  *bytes = make_layout(*cfg).total;
+  return SPD_OK;
+}
+
+spd_status spd_stage_bounds(const spd_config* cfg, int32_t* beta) {
+  if (!beta) return SPD_E_INVAL;
+  spd_status st = check_config(cfg, &g_init_error);
+  if (st != SPD_OK) return st;
+  stage_bounds(cfg->n_layers, cfg->n_stages, beta);
+  return SPD_OK;
+}
+
+static bool layer_ok(const spd_layer_weights& l) {
+  return l.attn_norm && l.wq && l.wk && l.wv && l.wo && l.mlp_norm && l.wg && l.wu && l.wd;
+}
+
+spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace, size_t ws_bytes,
+                    void* main_stream, void* pdm_stream, spd_handle** out) {
+  g_init_error.clear();
+  if (!out) return SPD_E_INVAL;
+  *out = nullptr;
+  spd_status st = check_config(cfg, &g_init_error);
+  if (st != SPD_OK) return st;
+  if (!w || !w->embed || !w->layers || !w->final_norm || !w->lm_head || !w->pdm_in || !w->pdm_layers ||
+      !w->pdm_norm) {
+    g_init_error = "weights: NULL pointer";
+    return SPD_E_INVAL;
+  }
+  for (int l = 0; l < cfg->n_layers; l++)
+    if (!layer_ok(w->layers[l])) {
+      g_init_error = "weights: NULL layer pointer";
+      return SPD_E_INVAL;
+    }
+  for (int l = 0; l < cfg->pdm_layers; l++)
+    if (!layer_ok(w->pdm_layers[l])) {
+      g_init_error = "weights: NULL PDM layer pointer";
+      return SPD_E_INVAL;
+    }
+  if (!workspace || ((uintptr_t)workspace & 255)) {
+    g_init_error = "workspace must be non-NULL and 256-byte aligned";
+    return SPD_E_INVAL;
+  }
+  if (!main_stream || !pdm_stream || main_stream == pdm_stream) {
+    g_init_error = "main_stream and pdm_stream must be two distinct non-default streams";
+    return SPD_E_INVAL;
+  }
+  const Layout lay = make_layout(*cfg);
+  if (ws_bytes < lay.total) {
+    g_init_error = "workspace too small";
+    return SPD_E_CAPACITY;
+  }
+  spd_handle* h = new (std::nothrow) spd_handle();
+  if (!h) return SPD_E_CAPACITY;
+  h->cfg = *cfg;
+  h->lay = lay;
+  h->bf16 = cfg->dtype == SPD_BF16;
+  h->main = (hipStream_t)main_stream;
+  h->pdm = (hipStream_t)pdm_stream;
+  h->ws = (char*)workspace;
+  auto fail = [&](spd_status s) {
+    g_init_error = h->err;
+    spd_destroy(h);
+    return s;
+  };
+#define HIPI(expr)                                                  \
+  do {                                                              \
+    hipError_t e_ = (expr);                                         \
+    if (e_ != hipSuccess) {                                         \
+      h->err = std::string(#expr) + ": " + hipGetErrorString(e_);   \
+      return fail(SPD_E_HIP);                                       \
+    }                                                               \
+  } while (0)
+  HIPI(hipGetDevice(&h->dev));
+  HIPI(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming));
+  HIPI(hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming));
+  HIPI(hipHostMalloc((void**)&h->pinned, sizeof(spd_step_result) * (kLogCap + 1), hipHostMallocDefault));
+
+  const spd_config& c = *cfg;
+  Ctx& C = h->ctx;
+  std::memset(&C, 0, sizeof(C));
+  C.d = c.d_model;
+  C.hq = c.n_q_heads;
+  C.hkv = c.n_kv_heads;
+  C.dh = c.head_dim;
+  C.qdim = c.n_q_heads * c.head_dim;
+  C.kvdim = c.n_kv_heads * c.head_dim;
+  C.F = c.ffn_dim;
+  C.V = c.vocab;
+  C.L = c.n_layers;
+  C.n = c.n_stages;
+  C.ls = c.pdm_layers;
+  C.page = c.page_size;
+  C.chunk = lay.chunk;
+  C.max_pages = lay.num_pages;
+  C.max_splits = lay.max_splits;
+  C.max_tokens = c.max_tokens;
+  C.G = c.n_q_heads / c.n_kv_heads;
+  C.eps = c.rms_eps;
+  C.scale = (float)(1.0 / std::sqrt((double)c.head_dim));
+  stage_bounds(c.n_layers, c.n_stages, C.beta);
+  h->J = 0;
+  for (int s = 0; s < c.n_stages; s++) h->J = std::max(h->J, C.beta[s + 1] - C.beta[s]);
+  char* ws = h->ws;
+  C.lay = (const LayerDesc*)(ws + lay.lay);
+  C.embed = w->embed;
+  C.lm_head = w->lm_head;
+  C.w_in = w->pdm_in;
+  C.final_norm = (const float*)w->final_norm;
+  C.pdm_norm = (const float*)w->pdm_norm;
+  C.page_table = (const int32_t*)(ws + lay.pt);
+  C.rope = (const float2*)(ws + lay.rope);
+  C.st = (DevState*)(ws + lay.state);
+  C.tok = (int32_t*)(ws + lay.tok);
+  C.forced = (int32_t*)(ws + lay.forced);
+  C.log = (spd_step_result*)(ws + lay.log);
+  C.resid = (float*)(ws + lay.resid);
+  C.anchors = (float*)(ws + lay.anch);
+  C.pdm_x = (float*)(ws + lay.pdmx);
+  C.pf_x = (float*)(ws + lay.pfx);
+  C.pf_anch = (float*)(ws + lay.pfanch);
+  C.dbg_logits = (float*)(ws + lay.dbg);
+  C.debug = 0;
+  for (int s = 0; s < 2; s++) {
+    BufSet& B = C.b[s];
+    B.q = (float*)(ws + lay.q[s]);
+    B.ao = (float*)(ws + lay.ao[s]);
+    B.act = (float*)(ws + lay.act[s]);
+    B.part = (float*)(ws + lay.part[s]);
+    B.cnt = (int32_t*)(ws + lay.cnt[s]);
+    B.hpart_v = (float*)(ws + lay.hpv[s]);
+    B.hpart_i = (int32_t*)(ws + lay.hpi[s]);
+    B.hcnt = (int32_t*)(ws + lay.hcnt[s]);
+  }
+
+  // layer table
+  std::vector<LayerDesc> ld(c.n_layers + c.pdm_layers);
+  for (int l = 0; l < c.n_layers + c.pdm_layers; l++) {
+    const bool pdm = l >= c.n_layers;
+    const spd_layer_weights& s = pdm ? w->pdm_layers[l - c.n_layers] : w->layers[l];
+    LayerDesc& d = ld[l];
+    d.wq = s.wq;
+    d.wk = s.wk;
+    d.wv = s.wv;
+    d.wo = s.wo;
+    d.wg = s.wg;
+    d.wu = s.wu;
+    d.wd = s.wd;
+    d.attn_norm = (const float*)s.attn_norm;
+    d.mlp_norm = (const float*)s.mlp_norm;
+    d.kv = pdm ? (void*)(ws + lay.pkv + lay.kv_layer_bytes * (l - c.n_layers))
+               : (void*)(ws + lay.kv + lay.kv_layer_bytes * l);
+  }
+  // RoPE table: angle pos * base^(-2j/dh) and its cos/sin in double precision, rounded to fp32
+  const int half = c.head_dim / 2;
+  std::vector<float> rope((size_t)c.max_tokens * half * 2);
+  for (int j = 0; j < half; j++) {
+    const double inv = std::pow((double)c.rope_base, -2.0 * j / c.head_dim);
+    for (int p = 0; p < c.max_tokens; p++) {
+      const double ang = (double)p * inv;
+      rope[((size_t)p * half + j) * 2] = (float)std::cos(ang);
+      rope[((size_t)p * half + j) * 2 + 1] = (float)std::sin(ang);
+    }
+  }
+  // page table: logical page i -> physical page, in order or seeded-shuffled
+  h->page_table.resize(lay.num_pages);
+  for (int i = 0; i < lay.num_pages; i++) h->page_table[i] = i;
+  if (c.page_seed) {
+    std::mt19937_64 rng(c.page_seed);
+    for (int i = lay.num_pages - 1; i > 0; i--) {
+      const int j = (int)(rng() % (uint64_t)(i + 1));
+      std::swap(h->page_table[i], h->page_table[j]);
+    }
+  }
+  HIPI(hipMemcpyAsync(ws + lay.lay, ld.data(), sizeof(LayerDesc) * ld.size(), hipMemcpyHostToDevice, h->main));
+  HIPI(hipMemcpyAsync(ws + lay.rope, rope.data(), sizeof(float) * rope.size(), hipMemcpyHostToDevice, h->main));
+  HIPI(hipMemcpyAsync(ws + lay.pt, h->page_table.data(), sizeof(int32_t) * lay.num_pages, hipMemcpyHostToDevice,
+                      h->main));
+  HIPI(hipMemsetAsync(ws + lay.state, 0, sizeof(DevState), h->main));
+  HIPI(hipMemsetAsync(ws + lay.tok, 0, sizeof(int32_t) * (c.max_tokens + 8), h->main));
+  HIPI(hipMemsetAsync(ws + lay.forced, 0xff, sizeof(int32_t) * (c.max_tokens + 8), h->main));
+  for (int s = 0; s < 2; s++) {
+    HIPI(hipMemsetAsync(ws + lay.cnt[s], 0, sizeof(int32_t) * kMaxStages * c.n_kv_heads, h->main));
+    HIPI(hipMemsetAsync(ws + lay.hcnt[s], 0, sizeof(int32_t) * 64, h->main));
+  }
+  HIPI(hipStreamSynchronize(h->main));
+#undef HIPI
+  *out = h;
+  return SPD_OK;
+}
+
+spd_status spd_set_debug(spd_handle* h, int32_t on) {
+  if (!h) return SPD_E_INVAL;
+  h->ctx.debug = on ? 1 : 0;
+  return SPD_OK;
+}
+
+static spd_status fetch_state(spd_handle* h) {
+  HIPC(hipMemcpyAsync(h->pinned, &h->ctx.st->res, sizeof(spd_step_result), hipMemcpyDeviceToHost, h->main));
+  HIPC(hipStreamSynchronize(h->main));
+  const spd_step_result& r = h->pinned[0];
+  h->c = r.committed_len;
+  h->a = r.inflight;
+  h->bound = (long long)h->c + h->a;
+  h->unsynced = 0;
+  return SPD_OK;
+}
+
+static spd_status ensure_synced(spd_handle* h) {
+  if (!h->unsynced) return SPD_OK;
+  HIPC(hipStreamSynchronize(h->pdm));
+  return fetch_state(h);
+}
+
+spd_status spd_prefill(spd_handle* h, const int32_t* prompt, int32_t len, int32_t* first_token) {
+  if (!h || !prompt || len < 1) return SPD_E_INVAL;
+  if (h->hstate != H_INIT) return SPD_E_STATE;
+  if (len + h->cfg.n_stages + 1 > h->cfg.max_tokens) return SPD_E_CAPACITY;
+  for (int i = 0; i < len; i++)
+    if (prompt[i] < 0 || prompt[i] >= h->cfg.vocab) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipMemcpyAsync(h->ctx.tok, prompt, sizeof(int32_t) * len, hipMemcpyHostToDevice, h->main));
+  spd_status st = h->bf16 ? enqueue_prefill<uint16_t>(h, len) : enqueue_prefill<float>(h, len);
+  if (st != SPD_OK) return st;
+  int32_t y = 0;
+  HIPC(hipMemcpyAsync(&h->pinned[0].target_argmax, &h->ctx.st->y, sizeof(int32_t), hipMemcpyDeviceToHost, h->main));
+  HIPC(hipStreamSynchronize(h->main));
+  y = h->pinned[0].target_argmax;
+  h->c = len;
+  h->a = 1;
+  h->bound = len + 1;
+  h->prompt_len = len;
+  h->hstate = H_READY;
+  if (first_token) *first_token = y;
+  return SPD_OK;
+}
+
+spd_status spd_step(spd_handle* h, const int32_t* forced_draft, spd_step_result* out) {
+  if (!h) return SPD_E_INVAL;
+  if (h->hstate != H_READY) return SPD_E_STATE;
+  if (forced_draft && (*forced_draft < 0 || *forced_draft >= h->cfg.vocab)) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  spd_status sy = ensure_synced(h);
+  if (sy != SPD_OK) return sy;
+  if (h->c + h->a >= h->cfg.max_tokens) return SPD_E_CAPACITY;
+  spd_status st = h->bf16 ? enqueue_step<uint16_t>(h, forced_draft ? *forced_draft : -1)
+                          : enqueue_step<float>(h, forced_draft ? *forced_draft : -1);
+  if (st != SPD_OK) return st;
+  st = fetch_state(h);
+  if (st != SPD_OK) return st;
+  const spd_step_result r = h->pinned[0];
+  if (r.decision == SPD_REJECT && !h->cfg.auto_rollback) h->hstate = H_PENDING;
+  if (out) *out = r;
+  return SPD_OK;
+}
+
+spd_status spd_run_steps(spd_handle* h, int32_t count, spd_step_result* log) {
+  if (!h || count < 0) return SPD_E_INVAL;
+  if (h->hstate != H_READY || !h->cfg.auto_rollback) return SPD_E_STATE;
+  if (count > kLogCap && log) return SPD_E_INVAL;
+  if (h->bound + count > h->cfg.max_tokens) return SPD_E_CAPACITY;
+  HIPC(hipSetDevice(h->dev));
+  for (int i = 0; i < count; i++) {
+    spd_status st = h->bf16 ? enqueue_step<uint16_t>(h, -1) : enqueue_step<float>(h, -1);
+    if (st != SPD_OK) return st;
+  }
+  h->bound += count;
+  h->unsynced = 1;
+  if (log) {
+    spd_status st = fetch_state(h);
+    if (st != SPD_OK) return st;
+    const int last = h->pinned[0].step_index;
+    // copy the ring entries of the last `count` steps
+    for (int i = 0; i < count; i++) {
+      const int idx = (last - count + i) % kLogCap;
+      HIPC(hipMemcpyAsync(&h->pinned[1 + i % kLogCap], h->ctx.log + idx, sizeof(spd_step_result),
+                          hipMemcpyDeviceToHost, h->main));
+    }
+    HIPC(hipStreamSynchronize(h->main));
+    for (int i = 0; i < count; i++) log[i] = h->pinned[1 + i % kLogCap];
+  }
+  return SPD_OK;
+}
+
+spd_status spd_sync(spd_handle* h, spd_step_result* last) {
+  if (!h) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->pdm));
+  if (h->hstate == H_INIT) {
+    HIPC(hipStreamSynchronize(h->main));
+    return SPD_OK;
+  }
+  spd_status st = fetch_state(h);
+  if (st != SPD_OK) return st;
+  if (last) *last = h->pinned[0];
+  return SPD_OK;
+}
+
+spd_status spd_rollback(spd_handle* h, int32_t keep_len, int32_t reseed_token) {
+  if (!h) return SPD_E_INVAL;
+  if (h->hstate == H_INIT) return SPD_E_STATE;
+  if (reseed_token < 0 || reseed_token >= h->cfg.vocab) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  spd_status sy = ensure_synced(h);
+  if (sy != SPD_OK) return sy;
+  if (keep_len < h->prompt_len || keep_len > h->c) return SPD_E_INVAL;
+  if (keep_len + 1 >= h->cfg.max_tokens) return SPD_E_CAPACITY;
+  HIPC(hipStreamSynchronize(h->pdm));
+  launch_reseed(h->ctx, keep_len, reseed_token, -1, h->main, h->bf16);
+  spd_status st = launch_check(h, "rollback");
+  if (st != SPD_OK) return st;
+  HIPC(hipStreamSynchronize(h->main));
+  h->c = keep_len;
+  h->a = 1;
+  h->bound = keep_len + 1;
+  h->hstate = H_READY;
+  return SPD_OK;
+}
+
+spd_status spd_set_forced_drafts(spd_handle* h, const int32_t* table, int32_t first_pos, int32_t len) {
+  if (!h || (!table && len > 0) || first_pos < 0 || len < 0) return SPD_E_INVAL;
+  if ((long long)first_pos + len > h->cfg.max_tokens) return SPD_E_CAPACITY;
+  for (int i = 0; i < len; i++)
+    if (table[i] >= h->cfg.vocab) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->main));
+  if (len) HIPC(hipMemcpy(h->ctx.forced + first_pos, table, sizeof(int32_t) * len, hipMemcpyHostToDevice));
+  return SPD_OK;
+}
+
+spd_status spd_clear_forced_drafts(spd_handle* h) {
+  if (!h) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->main));
+  HIPC(hipMemset(h->ctx.forced, 0xff, sizeof(int32_t) * (h->cfg.max_tokens + 8)));
+  return SPD_OK;
+}
+
+spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes) {
+  if (!h || !host) return SPD_E_INVAL;
+  const spd_config& c = h->cfg;
+  const void* src = nullptr;
+  size_t need = 0;
+  switch (what) {
+    case SPD_DBG_RESID: src = h->ctx.resid; need = sizeof(float) * c.n_stages * c.d_model; break;
+    case SPD_DBG_ANCHORS: src = h->ctx.anchors; need = sizeof(float) * c.n_stages * c.n_stages * c.d_model; break;
+    case SPD_DBG_PDM_HIDDEN: src = h->ctx.pdm_x; need = sizeof(float) * kMaxRows * c.d_model; break;
+    case SPD_DBG_EXIT_LOGITS: src = h->ctx.dbg_logits; need = sizeof(float) * c.vocab; break;
+    case SPD_DBG_PDM_LOGITS: src = h->ctx.dbg_logits + c.vocab; need = sizeof(float) * c.vocab; break;
+    case SPD_DBG_TOKENS: src = h->ctx.tok; need = sizeof(int32_t) * c.max_tokens; break;
+    case SPD_DBG_STATE: src = nullptr; need = sizeof(int32_t) * 4; break;
+    default: return SPD_E_INVAL;
+  }
+  if (bytes != need) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->pdm));
+  HIPC(hipStreamSynchronize(h->main));
+  if (what == SPD_DBG_STATE) {
+    DevState s;
+    HIPC(hipMemcpy(&s, h->ctx.st, sizeof(DevState), hipMemcpyDeviceToHost));
+    int32_t* o = (int32_t*)host;
+    o[0] = s.c;
+    o[1] = s.a;
+    o[2] = s.prompt_len;
+    o[3] = s.nsteps;
+    return SPD_OK;
+  }
+  HIPC(hipMemcpy(host, src, need, hipMemcpyDeviceToHost));
+  return SPD_OK;
+}
+
+spd_status spd_read_kv(spd_handle* h, int32_t pdm, int32_t layer, int32_t pos0, int32_t count, void* host_k,
+                       void* host_v) {
+  if (!h || !host_k || !host_v || count < 0 || pos0 < 0) return SPD_E_INVAL;
+  const spd_config& c = h->cfg;
+  if (layer < 0 || layer >= (pdm ? c.pdm_layers : c.n_layers)) return SPD_E_INVAL;
+  if ((long long)pos0 + count > c.max_tokens) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->pdm));
+  HIPC(hipStreamSynchronize(h->main));
+  const size_t esz = h->bf16 ? 2 : 4;
+  const int P = c.page_size, hkv = c.n_kv_heads, dh = c.head_dim;
+  const size_t page_bytes = (size_t)2 * hkv * P * dh * esz;
+  const char* base = h->ws + (pdm ? h->lay.pkv : h->lay.kv) + h->lay.kv_layer_bytes * layer;
+  std::vector<char> pg(page_bytes);
+  int cur = -1;
+  for (int p = pos0; p < pos0 + count; p++) {
+    const int lp = p / P;
+    if (lp != cur) {
+      HIPC(hipMemcpy(pg.data(), base + (size_t)h->page_table[lp] * page_bytes, page_bytes, hipMemcpyDeviceToHost));
+      cur = lp;
+    }
+    for (int g = 0; g < hkv; g++) {
+      const size_t ko = ((size_t)g * P + (p % P)) * dh * esz;
+      const size_t vo = ko + (size_t)hkv * P * dh * esz;
+      const size_t oo = ((size_t)(p - pos0) * hkv + g) * dh * esz;
+      std::memcpy((char*)host_k + oo, pg.data() + ko, dh * esz);
+      std::memcpy((char*)host_v + oo, pg.data() + vo, dh * esz);
+    }
+  }
+  return SPD_OK;
+}
+
+spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel) {
+  if (!h || kernel < 0 || kernel > SPD_K_HEAD) return SPD_E_INVAL;
+  h->timed_kernel = kernel;
+  return SPD_OK;
+}
+
+spd_status spd_kernel_timing(spd_handle* h, double* total_ms, int32_t* launches) {
+  if (!h || !total_ms || !launches) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->main));
+  double tot = 0.0;
+  for (size_t i = 0; i + 1 < h->tev_used; i += 2) {
+    float ms = 0.f;
+    HIPC(hipEventElapsedTime(&ms, h->tev[i], h->tev[i + 1]));
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = (int32_t)(h->tev_used / 2);
+  h->tev_used = 0;
+  return SPD_OK;
+}
+
+void spd_destroy(spd_handle* h) {
+  if (!h) return;
+  for (hipEvent_t e : h->tev) (void)hipEventDestroy(e);
+  if (h->main) (void)hipStreamSynchronize(h->main);
+  if (h->pdm) (void)hipStreamSynchronize(h->pdm);
+  if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
+  if (h->ev_join) (void)hipEventDestroy(h->ev_join);
+  if (h->pinned) (void)hipHostFree(h->pinned);
+  delete h;
+}
+
+}  // extern "C"

@@ -1,0 +1,124 @@
+// Internal layout shared by the host runtime and the gfx950 kernels. Not part of the C ABI.
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+#include "spd.h"
+
+namespace spd {
+
+constexpr int kMaxStages = 8;   // n
+constexpr int kMaxRows = 8;     // rows of one row-block launch (PDM rows, prefill chunk)
+constexpr int kMaxPdmLayers = 4;
+constexpr int kWG = 256;        // threads per workgroup in every kernel
+constexpr int kLogCap = 4096;   // step log ring
+
+// One decoder layer as the kernels see it. KV pool of the layer: [pages][2][Hkv][page][dh].
+struct LayerDesc {
+  const void* wq;
+  const void* wk;
+  const void* wv;
+  const void* wo;
+  const void* wg;
+  const void* wu;
+  const void* wd;
+  const float* attn_norm;
+  const float* mlp_norm;
+  void* kv;
+};
+
+// Device-resident decoding state; every kernel of a step reads the pre-step c and a from here and
+// only the verify kernel (last in the step) changes them.
+struct DevState {
+  int32_t c;           // positions that have passed all layers
+  int32_t a;           // in-flight tokens, positions c..c+a-1 (0 while a rollback is pending)
+  int32_t prompt_len;
+  int32_t pending;     // 1: a REJECT waits for spd_rollback
+  int32_t nsteps;
+  int32_t y;           // target argmax of this step's exiting token
+  int32_t pdm_draft;   // PDM argmax of this step
+  int32_t pad0;
+  spd_step_result res; // last step
+  int32_t pad1[6];
+};
+
+// Scratch of one compute stream. The target path and the PDM each own one, so the two streams
+// never share scratch.
+struct BufSet {
+  float* q;         // [8][Hq*dh] rotated queries (row index = group for stage launches)
+  float* ao;        // [8][Hq*dh] attention outputs
+  float* act;       // [8][F] SwiGLU activations
+  float* part;      // attention split partials
+  int32_t* cnt;     // attention combine counters [8 * Hkv], zero between launches
+  float* hpart_v;   // LM-head partial maxima [tiles][2]
+  int32_t* hpart_i; // LM-head partial argmax [tiles][2]
+  int32_t* hcnt;    // LM-head combine counter
+};
+
+struct Ctx {
+  // shapes
+  int d, hq, hkv, dh, qdim, kvdim, F, V, L, n, ls, page, chunk, max_pages, max_splits, max_tokens;
+  int G;            // query heads per KV head
+  float eps, scale; // RMSNorm eps, 1/sqrt(dh)
+  int beta[kMaxStages + 1];
+  // weights and tables
+  const LayerDesc* lay;   // [L + ls]: target layers then PDM layers
+  const void* embed;
+  const void* lm_head;
+  const void* w_in;
+  const float* final_norm;
+  const float* pdm_norm;
+  const int32_t* page_table;
+  const float2* rope;     // [max_tokens][dh/2] (cos, sin)
+  // state
+  DevState* st;
+  int32_t* tok;           // [max_tokens + 8]
+  int32_t* forced;        // [max_tokens + 8], -1 = no override
+  spd_step_result* log;   // [kLogCap]
+  // activations
+  float* resid;     // [n][d] in-flight residual streams, row q mod n
+  float* anchors;   // [n][n][d] row q mod n, anchor j
+  float* pdm_x;     // [8][d] PDM residual rows
+  float* pf_x;      // [8][d] prefill chunk residual rows
+  float* pf_anch;   // [8][n][d] prefill chunk anchors
+  float* dbg_logits;// [2][V]
+  int debug;
+  BufSet b[2];      // 0: target stream, 1: PDM stream
+};
+
+// Which rows a launch works on.
+//   kind 0 (stage launch): group g = stage s, one row: the token at depth s, position c+a-1-s,
+//            layer beta_s + slot (inactive if s >= a or the stage has fewer layers).
+//   kind 1 (row block): one group of `nrows` rows at positions pos0+i through layer `layer`;
+//            nrows < 0 means "a" and pos0 < 0 means "c" read from the device state (PDM step).
+struct Rows {
+  int kind;
+  int slot;
+  int layer;    // index into Ctx::lay
+  int nrows;
+  int pos0;
+  float* x;     // kind 1: residual rows [nrows][d]
+  float* anch;  // kind 1: anchor capture base [rows][n][d] (null: none)
+  int cap;      // kind 1: anchor index to capture after this layer (-1: none)
+  int set;      // scratch set
+};
+
+// Launchers (spd_kernels.hip). All are asynchronous on `stream`.
+template <typename WT>
+struct Launch {
+  static void qkv(const Ctx& c, const Rows& r, void* stream);
+  static void attn(const Ctx& c, const Rows& r, void* stream);
+  static void oproj(const Ctx& c, const Rows& r, void* stream);
+  static void gateup(const Ctx& c, const Rows& r, void* stream);
+  static void down(const Ctx& c, const Rows& r, void* stream);
+  // PDM feature projection; prefill = 1: nrows rows of pf_anch at full depth.
+  static void pdm_fc(const Ctx& c, int prefill, int nrows, void* stream);
+  // LM head + argmax. src: 0 = target exit row (skipped unless a == n), 1 = PDM last row,
+  // 2 = prefill row `row` of pf_x. Writes st->y (src 0, 2) or st->pdm_draft (src 1).
+  static void head(const Ctx& c, int src, int row, void* stream);
+  static void embed_rows(const Ctx& c, int t0, int nrows, void* stream);
+};
+void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* stream, int bf16);
+void launch_reseed(const Ctx& c, int keep, int tok, int prompt_len, void* stream, int bf16);
+
+}  // namespace spd

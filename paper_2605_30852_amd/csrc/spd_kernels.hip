@@ -1,0 +1,1044 @@
+// gfx950 kernels of one SPD pipeline step.
+//
+// The step is HBM-bound: each stage multiplies its own layer's weights by one activation vector, so
+// every launch below streams weight rows once with 16-byte coalesced loads, keeps activations in
+// fp32 (staged in LDS), reduces each row across a 64-lane wavefront in a fixed butterfly order and
+// groups all active stages (or all rows of a row block) into one launch per sublayer.
+//
+// Determinism: a row's result depends only on its weights, its input vector and (for attention) its
+// KV length: the lane-to-column map, the FMA order, the butterfly and the split size never depend
+// on how many stages share a launch. That makes a token's arithmetic identical whether it runs in an
+// n-stage SPD step or in plain decoding (n = 1), which the lossless check relies on.
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "spd_dev.h"
+
+namespace spd {
+
+// ------------------------------------------------------------------------------------------ types
+template <typename T>
+struct Elt;
+template <>
+struct Elt<float> {
+  static constexpr int VE = 4;  // elements per 16-byte load
+};
+template <>
+struct Elt<uint16_t> {
+  static constexpr int VE = 8;
+};
+
+__device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+
+__device__ __forceinline__ uint16_t f2bf(float f) {  // round to nearest even (finite inputs)
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ void unpack16(const uint4& v, float* o);
+template <>
+__device__ __forceinline__ void unpack16<float>(const uint4& v, float* o) {
+  o[0] = __uint_as_float(v.x);
+  o[1] = __uint_as_float(v.y);
+  o[2] = __uint_as_float(v.z);
+  o[3] = __uint_as_float(v.w);
+}
+template <>
+__device__ __forceinline__ void unpack16<uint16_t>(const uint4& v, float* o) {
+  o[0] = bf_lo(v.x);
+  o[1] = bf_hi(v.x);
+  o[2] = bf_lo(v.y);
+  o[3] = bf_hi(v.y);
+  o[4] = bf_lo(v.z);
+  o[5] = bf_hi(v.z);
+  o[6] = bf_lo(v.w);
+  o[7] = bf_hi(v.w);
+}
+
+template <typename T>
+__device__ __forceinline__ float ld1(const T* p, size_t i);
+template <>
+__device__ __forceinline__ float ld1<float>(const float* p, size_t i) { return p[i]; }
+template <>
+__device__ __forceinline__ float ld1<uint16_t>(const uint16_t* p, size_t i) {
+  return __uint_as_float(((uint32_t)p[i]) << 16);
+}
+
+template <typename T>
+__device__ __forceinline__ void st1(T* p, size_t i, float v);
+template <>
+__device__ __forceinline__ void st1<float>(float* p, size_t i, float v) { p[i] = v; }
+template <>
+__device__ __forceinline__ void st1<uint16_t>(uint16_t* p, size_t i, float v) { p[i] = f2bf(v); }
+
+// ------------------------------------------------------------------------------------ reductions
+__device__ __forceinline__ float wave_sum(float v) {
+  // xor butterfly: every lane ends with the same, order-fixed total (fp add is commutative)
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  return v;
+}
+
+// ------------------------------------------------------------------------------- row resolution
+struct Grp {
+  int active;
+  int layer;
+  int nrows;
+  int pos0;
+  int s;      // stage (kind 0) or -1
+  int brow0;  // first scratch row of this group
+  float* x;   // residual rows: row i at x + i*xstride
+  int xstride;
+};
+
+__device__ __forceinline__ Grp resolve(const Ctx& C, const Rows& R, int g) {
+  Grp r;
+  r.active = 1;
+  if (R.kind == 0) {
+    const int a = C.st->a, c = C.st->c;
+    r.s = g;
+    if (g >= a || C.beta[g] + R.slot >= C.beta[g + 1]) {
+      r.active = 0;
+      return r;
+    }
+    r.layer = C.beta[g] + R.slot;
+    r.nrows = 1;
+    r.pos0 = c + a - 1 - g;
+    r.brow0 = g;
+    r.x = C.resid + (size_t)(r.pos0 % C.n) * C.d;
+    r.xstride = C.d;
+  } else {
+    r.s = -1;
+    r.layer = R.layer;
+    r.nrows = R.nrows >= 0 ? R.nrows : C.st->a;
+    r.pos0 = R.pos0 >= 0 ? R.pos0 : C.st->c;
+    r.brow0 = 0;
+    r.x = R.x;
+    r.xstride = C.d;
+    if (r.nrows <= 0) r.active = 0;
+  }
+  return r;
+}
+
+__device__ __forceinline__ size_t kv_off(const Ctx& C, int pos, int kvh, int j) {
+  // [page][2][Hkv][page_size][dh]; returns the K element offset (V is + Hkv*page*dh)
+  const int pg = C.page_table[pos / C.page];
+  return (size_t)pg * (2 * C.hkv * C.page * C.dh) + ((size_t)kvh * C.page + (pos % C.page)) * C.dh + j;
+}
+
+// --------------------------------------------------------------------------------- GEMV building
+// LDS layout of one staged activation chunk. For bf16 weights lane l multiplies columns
+// 8l..8l+7 of each 512-column block; the chunk is stored so that the lane's first four and last
+// four values are two conflict-free 16-byte LDS reads.
+template <int VE>
+__device__ __forceinline__ int xidx(int k) {
+  if constexpr (VE == 8) {
+    const int blk = k >> 9, w = k & 511, l = w >> 3, e = w & 7;
+    return (blk << 9) + ((e >> 2) << 8) + (l << 2) + (e & 3);
+  } else {
+    return k;
+  }
+}
+
+// acc[v][r] += W[row r][cols of this lane] . x[v][same cols], over one staged chunk.
+template <typename WT, int NV, int RL>
+__device__ __forceinline__ void accum_chunk(const WT* const (&wr)[RL], int K, int kc0, int kl_pad,
+                                            const float* lds, int KC, int nrows,
+                                            float (&acc)[NV][RL], int lane) {
+  constexpr int VE = Elt<WT>::VE;
+  constexpr int BLK = 64 * VE;
+#pragma unroll 2
+  for (int b = 0; b < kl_pad; b += BLK) {
+    const int col = kc0 + b + lane * VE;
+    uint4 w[RL];
+#pragma unroll
+    for (int r = 0; r < RL; r++) {
+      if (wr[r] != nullptr && col < K)
+        w[r] = *reinterpret_cast<const uint4*>(wr[r] + col);
+      else
+        w[r] = make_uint4(0u, 0u, 0u, 0u);
+    }
+    float wf[RL][VE];
+#pragma unroll
+    for (int r = 0; r < RL; r++) unpack16<WT>(w[r], wf[r]);
+#pragma unroll
+    for (int v = 0; v < NV; v++) {
+      if (v < nrows) {
+        float x[VE];
+        const float* xb = lds + v * KC + b;
+        const float4 x0 = *reinterpret_cast<const float4*>(xb + lane * 4);
+        x[0] = x0.x;
+        x[1] = x0.y;
+        x[2] = x0.z;
+        x[3] = x0.w;
+        if constexpr (VE == 8) {
+          const float4 x1 = *reinterpret_cast<const float4*>(xb + 256 + lane * 4);
+          x[4] = x1.x;
+          x[5] = x1.y;
+          x[6] = x1.z;
+          x[7] = x1.w;
+        }
+#pragma unroll
+        for (int r = 0; r < RL; r++) {
+#pragma unroll
+          for (int e = 0; e < VE; e++) acc[v][r] = fmaf(wf[r][e], x[e], acc[v][r]);
+        }
+      }
+    }
+  }
+}
+
+// Source of the activation vectors a GEMV multiplies.
+enum XSrc {
+  XS_NORM_RESID = 0,  // rmsnorm(residual row) * gain: gain applied while staging, 1/rms at the end
+  XS_PLAIN = 1,       // a scratch row, as is
+  XS_ANCHORS = 2      // PDM feature input: concatenated eligible anchors, zeros for the rest
+};
+
+struct XSpec {
+  int src = 0;
+  const float* gain;           // XS_NORM_RESID
+  const float* row[kMaxRows];  // activation row v
+  int nelig[kMaxRows];         // XS_ANCHORS: eligible length (f+1)*d per row
+};
+
+// Stage chunk [kc0, kc0+kl) of every row into LDS (zero padded to kl_pad); accumulate sum of
+// squares per row in ss (per-thread partials) when normalising.
+template <int VE, int NV>
+__device__ __forceinline__ void stage_chunk(const XSpec& xs, int nrows, int kc0, int kl, int kl_pad,
+                                            float* lds, int KC, float (&ss)[NV]) {
+#pragma unroll
+  for (int v = 0; v < NV; v++) {
+    if (v >= nrows) continue;
+    const float* row = xs.row[v];
+    const int nel = xs.nelig[v];
+    for (int k = threadIdx.x; k < kl_pad; k += kWG) {
+      float val = 0.f;
+      const int gk = kc0 + k;
+      if (k < kl) {
+        if (xs.src == XS_ANCHORS) {
+          val = gk < nel ? row[gk] : 0.f;
+        } else {
+          val = row[gk];
+          if (xs.src == XS_NORM_RESID) {
+            ss[v] = fmaf(val, val, ss[v]);
+            val *= xs.gain[gk];
+          }
+        }
+      }
+      lds[v * KC + xidx<VE>(k)] = val;
+    }
+  }
+}
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+// Run the full K loop for one tile: stage chunks, accumulate, reduce over the wave, and scale
+// by 1/rms for normalised inputs. On return every lane of a wave holds the wave's row results.
+template <typename WT, int NV, int RL>
+__device__ __forceinline__ void gemv_tile(const WT* const (&wr)[RL], int K, const XSpec& xs, int nrows,
+                                          float eps, float* lds, int KC, float (&acc)[NV][RL]) {
+  constexpr int VE = Elt<WT>::VE;
+  constexpr int BLK = 64 * VE;
+  __shared__ float red[4];
+  const int lane = threadIdx.x & 63;
+  float ss[NV];
+#pragma unroll
+  for (int v = 0; v < NV; v++) {
+    ss[v] = 0.f;
+#pragma unroll
+    for (int r = 0; r < RL; r++) acc[v][r] = 0.f;
+  }
+  for (int kc0 = 0; kc0 < K; kc0 += KC) {
+    const int kl = min(KC, K - kc0);
+    const int kl_pad = (kl + BLK - 1) / BLK * BLK;
+    __syncthreads();
+    stage_chunk<VE, NV>(xs, nrows, kc0, kl, kl_pad, lds, KC, ss);
+    __syncthreads();
+    accum_chunk<WT, NV, RL>(wr, K, kc0, kl_pad, lds, KC, nrows, acc, lane);
+  }
+#pragma unroll
+  for (int v = 0; v < NV; v++) {
+#pragma unroll
+    for (int r = 0; r < RL; r++) acc[v][r] = wave_sum(acc[v][r]);
+  }
+  if (xs.src == XS_NORM_RESID) {
+#pragma unroll
+    for (int v = 0; v < NV; v++) {
+      const float tot = block_sum(ss[v], red);  // every workgroup reduces in the same order
+      const float sc = 1.0f / sqrtf(tot / (float)K + eps);
+#pragma unroll
+      for (int r = 0; r < RL; r++) acc[v][r] *= sc;
+    }
+  }
+}
+
+// Staged activation floats per row and chunk (multiples of every block width, so that the
+// per-lane accumulation order does not depend on the chunking). LDS stays at 48 KB or less.
+constexpr int kChunkCap1 = 12288;
+constexpr int kChunkCapN = 1536;
+
+template <int NV>
+__device__ __forceinline__ int chunk_floats(int K, int blk) {
+  const int kp = (K + blk - 1) / blk * blk;
+  const int cap = (NV == 1 ? kChunkCap1 : kChunkCapN);
+  return kp < cap ? kp : cap;
+}
+
+// ------------------------------------------------------------------ QKV + RoPE + KV append
+// Tile = 8 RoPE pairs of one head: wave w holds rows (2w, 2w+1) of the pair block and their
+// partners half a head away, so the rotation happens in registers right after the reduction.
+template <typename WT, int NV>
+__global__ __launch_bounds__(kWG) void k_qkv(Ctx C, Rows R) {
+  extern __shared__ float lds[];
+  const Grp gr = resolve(C, R, blockIdx.y);
+  if (!gr.active) return;
+  const LayerDesc& Ld = C.lay[gr.layer];
+  const int dh = C.dh, half = dh >> 1, tph = dh >> 4;
+  const int head = blockIdx.x / tph, pb = blockIdx.x % tph;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const WT* W;
+  int hrow;  // head index within its matrix
+  int kind;  // 0 q, 1 k, 2 v
+  if (head < C.hq) {
+    W = (const WT*)Ld.wq;
+    hrow = head;
+    kind = 0;
+  } else if (head < C.hq + C.hkv) {
+    W = (const WT*)Ld.wk;
+    hrow = head - C.hq;
+    kind = 1;
+  } else {
+    W = (const WT*)Ld.wv;
+    hrow = head - C.hq - C.hkv;
+    kind = 2;
+  }
+  const int j0 = pb * 8 + 2 * w;  // pair indices j0, j0+1 (< half)
+  const WT* wr[4];
+  wr[0] = W + (size_t)(hrow * dh + j0) * C.d;
+  wr[1] = W + (size_t)(hrow * dh + j0 + 1) * C.d;
+  wr[2] = W + (size_t)(hrow * dh + j0 + half) * C.d;
+  wr[3] = W + (size_t)(hrow * dh + j0 + half + 1) * C.d;
+  XSpec xs;
+  xs.src = XS_NORM_RESID;
+  xs.gain = Ld.attn_norm;
+  for (int v = 0; v < NV; v++) xs.row[v] = gr.x + (size_t)v * gr.xstride;
+  const int KC = chunk_floats<NV>(C.d, 64 * Elt<WT>::VE);
+  float acc[NV][4];
+  gemv_tile<WT, NV, 4>(wr, C.d, xs, gr.nrows, C.eps, lds, KC, acc);
+  float* qbuf = C.b[R.set].q;
+#pragma unroll
+  for (int v = 0; v < NV; v++) {
+#pragma unroll
+    for (int p = 0; p < 2; p++) {
+      if (lane == v * 2 + p && v < gr.nrows) {
+        const int pos = gr.pos0 + v;
+        const int j = j0 + p;
+        float lo = acc[v][p], hi = acc[v][p + 2];
+        if (kind != 2) {
+          const float2 cs = C.rope[(size_t)pos * half + j];
+          const float rlo = lo * cs.x - hi * cs.y;
+          const float rhi = hi * cs.x + lo * cs.y;
+          lo = rlo;
+          hi = rhi;
+        }
+        if (kind == 0) {
+          float* qo = qbuf + (size_t)(gr.brow0 + v) * C.qdim + hrow * dh;
+          qo[j] = lo;
+          qo[j + half] = hi;
+        } else {
+          WT* kv = (WT*)Ld.kv;
+          const size_t off = kv_off(C, pos, hrow, j) + (kind == 2 ? (size_t)C.hkv * C.page * dh : 0);
+          st1<WT>(kv, off, lo);
+          st1<WT>(kv, off + half, hi);
+        }
+      }
+    }
+  }
+}
+
+// --------------------------------------------------------------- O-proj / down-proj + residual
+// Tile = 16 output rows (4 per wave). MODE 0: o-proj (input = attention output, K = Hq*dh);
+// MODE 1: down-proj (input = SwiGLU activation, K = F), which also captures the stage output as
+// the next PDM anchor when this is a stage's last layer.
+template <typename WT, int NV, int MODE>
+__global__ __launch_bounds__(kWG) void k_proj_add(Ctx C, Rows R) {
+  extern __shared__ float lds[];
+  const Grp gr = resolve(C, R, blockIdx.y);
+  if (!gr.active) return;
+  const LayerDesc& Ld = C.lay[gr.layer];
+  const int K = MODE == 0 ? C.qdim : C.F;
+  const WT* W = (const WT*)(MODE == 0 ? Ld.wo : Ld.wd);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m0 = blockIdx.x * 16 + w * 4;
+  const WT* wr[4];
+#pragma unroll
+  for (int r = 0; r < 4; r++) wr[r] = (m0 + r < C.d) ? W + (size_t)(m0 + r) * K : nullptr;
+  XSpec xs;
+  xs.src = XS_PLAIN;
+  xs.gain = nullptr;
+  {
+    const float* b0 = (MODE == 0 ? C.b[R.set].ao : C.b[R.set].act) + (size_t)gr.brow0 * K;
+    for (int v = 0; v < NV; v++) xs.row[v] = b0 + (size_t)v * K;
+  }
+  const int KC = chunk_floats<NV>(K, 64 * Elt<WT>::VE);
+  float acc[NV][4];
+  gemv_tile<WT, NV, 4>(wr, K, xs, gr.nrows, 0.f, lds, KC, acc);
+  // anchor capture target
+  float* cap = nullptr;
+  size_t cap_stride = 0;
+  if (MODE == 1) {
+    if (R.kind == 0) {
+      const int s = gr.s;
+      if (gr.layer + 1 == C.beta[s + 1] && s + 1 <= C.n - 1) {
+        cap = C.anchors + ((size_t)(gr.pos0 % C.n) * C.n + (s + 1)) * C.d;
+      }
+    } else if (R.anch != nullptr && R.cap >= 0) {
+      cap = R.anch + (size_t)R.cap * C.d;
+      cap_stride = (size_t)C.n * C.d;
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < NV; v++) {
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+      if (lane == v * 4 + r && v < gr.nrows && m0 + r < C.d) {
+        float* xo = gr.x + (size_t)v * gr.xstride;
+        const float nv = xo[m0 + r] + acc[v][r];
+        xo[m0 + r] = nv;
+        if (cap != nullptr) cap[(size_t)v * cap_stride + m0 + r] = nv;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------------- gate/up + SwiGLU
+// Tile = 8 outputs (2 per wave); each wave streams the gate and up rows of its outputs together.
+template <typename WT, int NV>
+__global__ __launch_bounds__(kWG) void k_gateup(Ctx C, Rows R) {
+  extern __shared__ float lds[];
+  const Grp gr = resolve(C, R, blockIdx.y);
+  if (!gr.active) return;
+  const LayerDesc& Ld = C.lay[gr.layer];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m0 = blockIdx.x * 8 + w * 2;
+  const WT* Wg = (const WT*)Ld.wg;
+  const WT* Wu = (const WT*)Ld.wu;
+  const WT* wr[4];
+  wr[0] = (m0 < C.F) ? Wg + (size_t)m0 * C.d : nullptr;
+  wr[1] = (m0 + 1 < C.F) ? Wg + (size_t)(m0 + 1) * C.d : nullptr;
+  wr[2] = (m0 < C.F) ? Wu + (size_t)m0 * C.d : nullptr;
+  wr[3] = (m0 + 1 < C.F) ? Wu + (size_t)(m0 + 1) * C.d : nullptr;
+  XSpec xs;
+  xs.src = XS_NORM_RESID;
+  xs.gain = Ld.mlp_norm;
+  for (int v = 0; v < NV; v++) xs.row[v] = gr.x + (size_t)v * gr.xstride;
+  const int KC = chunk_floats<NV>(C.d, 64 * Elt<WT>::VE);
+  float acc[NV][4];
+  gemv_tile<WT, NV, 4>(wr, C.d, xs, gr.nrows, C.eps, lds, KC, acc);
+  float* act = C.b[R.set].act;
+#pragma unroll
+  for (int v = 0; v < NV; v++) {
+#pragma unroll
+    for (int p = 0; p < 2; p++) {
+      if (lane == v * 2 + p && v < gr.nrows && m0 + p < C.F) {
+        const float g = acc[v][p], u = acc[v][p + 2];
+        act[(size_t)(gr.brow0 + v) * C.F + m0 + p] = g / (1.0f + expf(-g)) * u;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------- PDM feature projection
+// g_q = W_in . [H^{beta_0}; ...; H^{beta_f}; 0 ...] for the rows the PDM runs (Eq. agg-main with
+// one projection whose column block j serves anchor j). prefill = 1: rows of the prefill chunk
+// at full depth; else the a in-flight rows, row i at depth a-1-i.
+template <typename WT>
+__global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_arg) {
+  extern __shared__ float lds[];
+  constexpr int NV = kMaxRows;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int K = C.n * C.d;
+  int nrows;
+  XSpec xs;
+  xs.src = XS_ANCHORS;
+  xs.gain = nullptr;
+  if (prefill) {
+    nrows = nrows_arg;
+    for (int i = 0; i < kMaxRows; i++) {
+      xs.row[i] = C.pf_anch + (size_t)i * C.n * C.d;
+      xs.nelig[i] = K;
+    }
+  } else {
+    const int c = C.st->c, a = C.st->a;
+    nrows = a;
+    for (int i = 0; i < kMaxRows; i++) {
+      // in-flight position c+i keeps its anchors in ring row (c+i) mod n
+      xs.row[i] = C.anchors + (size_t)((c + i) % C.n) * C.n * C.d;
+      const int depth = a - 1 - i;
+      const int f = depth < C.n - 1 ? depth : C.n - 1;
+      xs.nelig[i] = (f + 1) * C.d;
+    }
+  }
+  if (nrows <= 0) return;
+  const int m0 = blockIdx.x * 16 + w * 4;
+  const WT* W = (const WT*)C.w_in;
+  const WT* wr[4];
+#pragma unroll
+  for (int r = 0; r < 4; r++) wr[r] = (m0 + r < C.d) ? W + (size_t)(m0 + r) * K : nullptr;
+  const int KC = chunk_floats<NV>(K, 64 * Elt<WT>::VE);
+  float acc[NV][4];
+  gemv_tile<WT, NV, 4>(wr, K, xs, nrows, 0.f, lds, KC, acc);
+  float* out = C.pdm_x;
+#pragma unroll
+  for (int v = 0; v < NV; v++) {
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+      if (lane == v * 4 + r && v < nrows && m0 + r < C.d) out[(size_t)v * C.d + m0 + r] = acc[v][r];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------- LM head + argmax
+// Tile = 16 vocabulary rows. Each workgroup keeps its best (value, index) with the lowest index
+// winning ties; the last workgroup to finish reduces the partials. The (value desc, index asc)
+// order is total, so the winner does not depend on the reduction order.
+__device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
+  return v > bv || (v == bv && i < bi);
+}
+
+template <typename WT>
+__global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row, int set) {
+  extern __shared__ float lds[];
+  __shared__ float s_v[4];
+  __shared__ int s_i[4];
+  __shared__ int s_last;
+  const float* x;
+  const float* gain;
+  int* dst;
+  if (src == 0) {
+    const int a = C.st->a, c = C.st->c;
+    if (a != C.n) return;  // nothing exits while the pipeline fills
+    x = C.resid + (size_t)(c % C.n) * C.d;
+    gain = C.final_norm;
+    dst = &C.st->y;
+  } else if (src == 1) {
+    x = C.pdm_x + (size_t)(C.st->a - 1) * C.d;
+    gain = C.pdm_norm;
+    dst = &C.st->pdm_draft;
+  } else {
+    x = C.pf_x + (size_t)row * C.d;
+    gain = C.final_norm;
+    dst = &C.st->y;
+  }
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int m0 = blockIdx.x * 16 + w * 4;
+  const WT* W = (const WT*)C.lm_head;
+  const WT* wr[4];
+#pragma unroll
+  for (int r = 0; r < 4; r++) wr[r] = (m0 + r < C.V) ? W + (size_t)(m0 + r) * C.d : nullptr;
+  XSpec xs;
+  xs.src = XS_NORM_RESID;
+  xs.gain = gain;
+  xs.row[0] = x;
+  const int KC = chunk_floats<1>(C.d, 64 * Elt<WT>::VE);
+  float acc[1][4];
+  gemv_tile<WT, 1, 4>(wr, C.d, xs, 1, C.eps, lds, KC, acc);
+  if (C.debug && lane < 4 && m0 + lane < C.V) {
+    float val = acc[0][0];
+#pragma unroll
+    for (int r = 1; r < 4; r++)
+      if (lane == r) val = acc[0][r];
+    C.dbg_logits[(size_t)(src == 1 ? 1 : 0) * C.V + m0 + lane] = val;
+  }
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+#pragma unroll
+  for (int r = 0; r < 4; r++) {
+    if (m0 + r < C.V && better(acc[0][r], m0 + r, bv, bi)) {
+      bv = acc[0][r];
+      bi = m0 + r;
+    }
+  }
+  if (lane == 0) {
+    s_v[w] = bv;
+    s_i[w] = bi;
+  }
+  __syncthreads();
+  const BufSet& B = C.b[set];
+  if (threadIdx.x == 0) {
+    float v = s_v[0];
+    int i = s_i[0];
+    for (int k = 1; k < 4; k++)
+      if (better(s_v[k], s_i[k], v, i)) {
+        v = s_v[k];
+        i = s_i[k];
+      }
+    B.hpart_v[blockIdx.x] = v;
+    B.hpart_i[blockIdx.x] = i;
+    __threadfence();
+    const int t = atomicAdd(B.hcnt, 1);
+    s_last = (t == (int)gridDim.x - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  float v = -INFINITY;
+  int i = 0x7fffffff;
+  for (int k = threadIdx.x; k < (int)gridDim.x; k += kWG) {
+    const float pv = B.hpart_v[k];
+    const int pi = B.hpart_i[k];
+    if (better(pv, pi, v, i)) {
+      v = pv;
+      i = pi;
+    }
+  }
+  // block argmax: wave butterfly then the 4 wave winners
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    const float ov = __shfl_xor(v, m, 64);
+    const int oi = __shfl_xor(i, m, 64);
+    if (better(ov, oi, v, i)) {
+      v = ov;
+      i = oi;
+    }
+  }
+  __syncthreads();
+  if (lane == 0) {
+    s_v[w] = v;
+    s_i[w] = i;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float fv = s_v[0];
+    int fi = s_i[0];
+    for (int k = 1; k < 4; k++)
+      if (better(s_v[k], s_i[k], fv, fi)) {
+        fv = s_v[k];
+        fi = s_i[k];
+      }
+    *dst = (fi >= 0 && fi < C.V) ? fi : 0;  // all-NaN logits cannot leave an out-of-range id
+    atomicExch(B.hcnt, 0);
+  }
+}
+
+// ------------------------------------------------------------------------------- attention
+// Ragged paged GQA decode attention. Grid: x = key split (chunk keys each), y = KV head, z = group.
+// A group's rows sit at positions pos0..pos0+nrows-1; row i attends to keys [0, pos0+i]. The split
+// count is ceil(keys / chunk), a function of the length only. With one split the workgroup writes
+// the output; otherwise each split writes (m, l, o) and the last split to finish combines them in
+// split order.
+template <typename KVT, int MAXQ, int DH>
+__global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
+  constexpr int PASS = 64;  // keys per pass
+  constexpr int dh = DH;
+  __shared__ float qs[MAXQ * DH];
+  __shared__ float sc[MAXQ * PASS];
+  __shared__ float s_m[MAXQ], s_l[MAXQ], s_al[MAXQ];
+  __shared__ int s_last;
+  const Grp gr = resolve(C, R, blockIdx.z);
+  if (!gr.active) return;
+  const int g = blockIdx.y, split = blockIdx.x;
+  const int G = C.G;
+  const int nkeys = gr.pos0 + gr.nrows;
+  const int nsplit = (nkeys + C.chunk - 1) / C.chunk;
+  if (split >= nsplit) return;
+  const int k0 = split * C.chunk, k1 = min(nkeys, k0 + C.chunk);
+  const int nq = gr.nrows * G;
+  const LayerDesc& Ld = C.lay[gr.layer];
+  const KVT* kvb = (const KVT*)Ld.kv;
+  const size_t voff = (size_t)C.hkv * C.page * dh;
+  const BufSet& B = C.b[R.set];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+
+  // queries (already rotated), pre-scaled by 1/sqrt(dh)
+  for (int e = tid; e < nq * dh; e += kWG) {
+    const int qi = e / dh, dd = e % dh;
+    const int i = qi / G, h = g * G + (qi % G);
+    qs[qi * dh + dd] = B.q[(size_t)(gr.brow0 + i) * C.qdim + h * dh + dd] * C.scale;
+  }
+  for (int qi = tid; qi < MAXQ; qi += kWG) {
+    s_m[qi] = -INFINITY;
+    s_l[qi] = 0.f;
+  }
+  // output accumulators: thread -> (query group qg, dim pair dp)
+  constexpr int npair = DH >> 1;
+  constexpr int NG = kWG / npair;  // 4 (dh 128) or 8 (dh 64)
+  const int dp = tid % npair, qg = tid / npair;
+  constexpr int MAXU = (MAXQ + NG - 1) / NG;
+  float o0[MAXU], o1[MAXU];
+#pragma unroll
+  for (int u = 0; u < MAXU; u++) {
+    o0[u] = 0.f;
+    o1[u] = 0.f;
+  }
+  __syncthreads();
+
+  constexpr int NE = DH >> 2;  // dims per thread in the score phase
+  for (int kp = k0; kp < k1; kp += PASS) {
+    const int nk = min(PASS, k1 - kp);
+    // scores: thread -> (key kk, quarter qq)
+    {
+      const int kk = tid >> 2, qq = tid & 3;
+      float kr[NE];
+      if (kk < nk) {
+        const KVT* kptr = kvb + kv_off(C, kp + kk, g, qq * NE);
+        const uint4* k4 = reinterpret_cast<const uint4*>(kptr);
+        constexpr int VE = Elt<KVT>::VE;
+#pragma unroll
+        for (int c4 = 0; c4 < NE / VE; c4++) unpack16<KVT>(k4[c4], kr + c4 * VE);
+      } else {
+#pragma unroll
+        for (int e = 0; e < NE; e++) kr[e] = 0.f;
+      }
+      for (int qi = 0; qi < nq; qi++) {
+        float dsum = 0.f;
+        const float* qv = qs + qi * dh + qq * NE;
+#pragma unroll
+        for (int e = 0; e < NE; e += 4) {
+          const float4 q4 = *reinterpret_cast<const float4*>(qv + e);
+          dsum = fmaf(q4.x, kr[e], dsum);
+          dsum = fmaf(q4.y, kr[e + 1], dsum);
+          dsum = fmaf(q4.z, kr[e + 2], dsum);
+          dsum = fmaf(q4.w, kr[e + 3], dsum);
+        }
+        dsum += __shfl_xor(dsum, 1, 64);
+        dsum += __shfl_xor(dsum, 2, 64);
+        if (qq == 0 && kk < nk) {
+          const int lim = gr.pos0 + qi / G;
+          sc[qi * PASS + kk] = (kp + kk <= lim) ? dsum : -INFINITY;
+        }
+      }
+    }
+    __syncthreads();
+    // online softmax update per query vector (one wave per query vector)
+    for (int qi = w; qi < nq; qi += 4) {
+      const float s = lane < nk ? sc[qi * PASS + lane] : -INFINITY;
+      const float mx = wave_max(s);
+      const float mo = s_m[qi];
+      const float mn = fmaxf(mo, mx);
+      const float p = (s == -INFINITY) ? 0.f : expf(s - mn);
+      if (lane < nk) sc[qi * PASS + lane] = p;
+      const float ps = wave_sum(p);
+      if (lane == 0) {
+        const float al = (mo == -INFINITY) ? 0.f : expf(mo - mn);
+        s_al[qi] = al;
+        s_l[qi] = s_l[qi] * al + ps;
+        s_m[qi] = mn;
+      }
+    }
+    __syncthreads();
+    // o = o * alpha + P V
+#pragma unroll
+    for (int u = 0; u < MAXU; u++) {
+      const int qi = qg + u * NG;
+      if (qi < nq) {
+        const float al = s_al[qi];
+        o0[u] *= al;
+        o1[u] *= al;
+      }
+    }
+    for (int kk = 0; kk < nk; kk++) {
+      const size_t off = kv_off(C, kp + kk, g, 2 * dp) + voff;
+      const float v0 = ld1<KVT>(kvb, off), v1 = ld1<KVT>(kvb, off + 1);
+#pragma unroll
+      for (int u = 0; u < MAXU; u++) {
+        const int qi = qg + u * NG;
+        if (qi < nq) {
+          const float p = sc[qi * PASS + kk];
+          o0[u] = fmaf(p, v0, o0[u]);
+          o1[u] = fmaf(p, v1, o1[u]);
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  const int RS = MAXQ * (dh + 2);  // partial record: o[MAXQ][dh], m[MAXQ], l[MAXQ]
+  const int cidx = blockIdx.z * C.hkv + g;
+  if (nsplit == 1) {
+#pragma unroll
+    for (int u = 0; u < MAXU; u++) {
+      const int qi = qg + u * NG;
+      if (qi < nq) {
+        const int i = qi / G, h = g * G + (qi % G);
+        const float inv = 1.0f / s_l[qi];
+        float* out = B.ao + (size_t)(gr.brow0 + i) * C.qdim + h * dh + 2 * dp;
+        out[0] = o0[u] * inv;
+        out[1] = o1[u] * inv;
+      }
+    }
+    return;
+  }
+  float* rec = B.part + ((size_t)cidx * C.max_splits + split) * RS;
+#pragma unroll
+  for (int u = 0; u < MAXU; u++) {
+    const int qi = qg + u * NG;
+    if (qi < nq) {
+      rec[qi * dh + 2 * dp] = o0[u];
+      rec[qi * dh + 2 * dp + 1] = o1[u];
+    }
+  }
+  for (int qi = tid; qi < nq; qi += kWG) {
+    rec[MAXQ * dh + qi] = s_m[qi];
+    rec[MAXQ * dh + MAXQ + qi] = s_l[qi];
+  }
+  __threadfence();  // each thread publishes its own partial writes at device scope
+  __syncthreads();
+  if (tid == 0) {
+    const int t = atomicAdd(&B.cnt[cidx], 1);
+    s_last = (t == nsplit - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  const float* base = B.part + (size_t)cidx * C.max_splits * RS;
+#pragma unroll
+  for (int u = 0; u < MAXU; u++) {
+    const int qi = qg + u * NG;
+    if (qi < nq) {
+      float M = -INFINITY;
+      for (int s = 0; s < nsplit; s++) M = fmaxf(M, base[(size_t)s * RS + MAXQ * dh + qi]);
+      float Ls = 0.f, A0 = 0.f, A1 = 0.f;
+      for (int s = 0; s < nsplit; s++) {
+        const float* r = base + (size_t)s * RS;
+        const float ms = r[MAXQ * dh + qi];
+        const float f = (ms == -INFINITY) ? 0.f : expf(ms - M);
+        Ls = fmaf(r[MAXQ * dh + MAXQ + qi], f, Ls);
+        A0 = fmaf(r[qi * dh + 2 * dp], f, A0);
+        A1 = fmaf(r[qi * dh + 2 * dp + 1], f, A1);
+      }
+      const int i = qi / G, h = g * G + (qi % G);
+      const float inv = 1.0f / Ls;
+      float* out = B.ao + (size_t)(gr.brow0 + i) * C.qdim + h * dh + 2 * dp;
+      out[0] = A0 * inv;
+      out[1] = A1 * inv;
+    }
+  }
+  if (tid == 0) atomicExch(&B.cnt[cidx], 0);
+}
+
+// ------------------------------------------------------------------------- embedding / state
+template <typename WT>
+__device__ __forceinline__ void push_embedding(const Ctx& C, int tok, float* dst0, float* dst1) {
+  const WT* E = (const WT*)C.embed + (size_t)tok * C.d;
+  for (int k = threadIdx.x; k < C.d; k += kWG) {
+    const float v = ld1<WT>(E, k);
+    dst0[k] = v;
+    if (dst1) dst1[k] = v;
+  }
+}
+
+template <typename WT>
+__global__ __launch_bounds__(kWG) void k_embed_rows(Ctx C, int t0, int nrows) {
+  const int i = blockIdx.x;
+  if (i >= nrows) return;
+  const int tok = C.tok[t0 + i];
+  push_embedding<WT>(C, tok, C.pf_x + (size_t)i * C.d, C.pf_anch + (size_t)i * C.n * C.d);
+}
+
+// Greedy streaming verification (Section 3.4) and the pipeline state update; single workgroup,
+// last kernel of a step.
+template <typename WT>
+__global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int auto_rb) {
+  __shared__ int s_tok, s_pos;
+  DevState* st = C.st;
+  if (threadIdx.x == 0) {
+    const int c = st->c, a = st->a, n = C.n;
+    const int pd = st->pdm_draft;
+    const int dpos = c + a;
+    int fd = forced_override;
+    if (fd < 0 && dpos < C.max_tokens) fd = C.forced[dpos];
+    const int draft = fd >= 0 ? fd : pd;
+    spd_step_result r;
+    r.decision = SPD_NONE;
+    r.target_argmax = -1;
+    r.draft = draft;
+    r.pdm_draft = pd;
+    r.exited_pos = -1;
+    r.verified_pos = -1;
+    r.verified_token = -1;
+    int ptok = -1, ppos = -1;
+    if (a == n) {
+      const int y = st->y;
+      const int succ = n >= 2 ? C.tok[c + 1] : draft;
+      r.target_argmax = y;
+      r.exited_pos = c;
+      r.verified_pos = c + 1;
+      r.verified_token = y;
+      st->c = c + 1;
+      if (succ == y) {
+        r.decision = SPD_ACCEPT;
+        C.tok[c + a] = draft;
+        ptok = draft;
+        ppos = c + a;
+      } else {
+        r.decision = SPD_REJECT;
+        r.draft = -1;
+        C.tok[c + 1] = y;
+        if (auto_rb) {
+          st->a = 1;
+          ptok = y;
+          ppos = c + 1;
+        } else {
+          st->a = 0;
+          st->pending = 1;
+        }
+      }
+    } else {
+      st->a = a + 1;
+      C.tok[c + a] = draft;
+      ptok = draft;
+      ppos = c + a;
+    }
+    r.committed_len = st->c;
+    r.inflight = st->a;
+    r.step_index = ++st->nsteps;
+    st->res = r;
+    C.log[(r.step_index - 1) % kLogCap] = r;
+    s_tok = ptok;
+    s_pos = ppos;
+  }
+  __syncthreads();
+  if (s_tok >= 0) {
+    const int row = s_pos % C.n;
+    push_embedding<WT>(C, s_tok, C.resid + (size_t)row * C.d, C.anchors + (size_t)row * C.n * C.d);
+  }
+}
+
+// Rollback / first placement: c := keep, one token in flight at position keep (tok < 0: the value
+// the last LM-head pass left in st->y).
+template <typename WT>
+__global__ __launch_bounds__(kWG) void k_reseed(Ctx C, int keep, int tok, int prompt_len) {
+  __shared__ int s_tok;
+  DevState* st = C.st;
+  if (threadIdx.x == 0) {
+    const int t = tok >= 0 ? tok : st->y;
+    st->c = keep;
+    st->a = 1;
+    st->pending = 0;
+    if (prompt_len >= 0) {
+      st->prompt_len = prompt_len;
+      st->nsteps = 0;
+    }
+    C.tok[keep] = t;
+    s_tok = t;
+  }
+  __syncthreads();
+  const int row = keep % C.n;
+  push_embedding<WT>(C, s_tok, C.resid + (size_t)row * C.d, C.anchors + (size_t)row * C.n * C.d);
+}
+
+// -------------------------------------------------------------------------------- launchers
+static inline hipStream_t S(void* s) { return (hipStream_t)s; }
+
+template <typename WT>
+static inline size_t gemv_lds(int K, int nv) {
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  const int kp = (K + BLK - 1) / BLK * BLK;
+  const int cap = nv == 1 ? kChunkCap1 : kChunkCapN;
+  return (size_t)nv * (kp < cap ? kp : cap) * sizeof(float);
+}
+
+template <typename WT>
+void Launch<WT>::qkv(const Ctx& c, const Rows& r, void* s) {
+  const dim3 grid((c.hq + 2 * c.hkv) * (c.dh / 16), r.kind == 0 ? c.n : 1);
+  if (r.kind == 0)
+    hipLaunchKernelGGL((k_qkv<WT, 1>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, r);
+  else
+    hipLaunchKernelGGL((k_qkv<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
+}
+
+template <typename WT>
+void Launch<WT>::oproj(const Ctx& c, const Rows& r, void* s) {
+  const dim3 grid((c.d + 15) / 16, r.kind == 0 ? c.n : 1);
+  if (r.kind == 0)
+    hipLaunchKernelGGL((k_proj_add<WT, 1, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, 1), S(s), c, r);
+  else
+    hipLaunchKernelGGL((k_proj_add<WT, kMaxRows, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, kMaxRows), S(s), c, r);
+}
+
+template <typename WT>
+void Launch<WT>::down(const Ctx& c, const Rows& r, void* s) {
+  const dim3 grid((c.d + 15) / 16, r.kind == 0 ? c.n : 1);
+  if (r.kind == 0)
+    hipLaunchKernelGGL((k_proj_add<WT, 1, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, 1), S(s), c, r);
+  else
+    hipLaunchKernelGGL((k_proj_add<WT, kMaxRows, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, kMaxRows), S(s), c, r);
+}
+
+template <typename WT>
+void Launch<WT>::gateup(const Ctx& c, const Rows& r, void* s) {
+  const dim3 grid((c.F + 7) / 8, r.kind == 0 ? c.n : 1);
+  if (r.kind == 0)
+    hipLaunchKernelGGL((k_gateup<WT, 1>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, r);
+  else
+    hipLaunchKernelGGL((k_gateup<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
+}
+
+template <typename WT>
+void Launch<WT>::attn(const Ctx& c, const Rows& r, void* s) {
+  const dim3 grid(c.max_splits, c.hkv, r.kind == 0 ? c.n : 1);
+  if (c.dh == 128) {
+    if (r.kind == 0)
+      hipLaunchKernelGGL((k_attn<WT, 8, 128>), grid, dim3(kWG), 0, S(s), c, r);
+    else
+      hipLaunchKernelGGL((k_attn<WT, 64, 128>), grid, dim3(kWG), 0, S(s), c, r);
+  } else {
+    if (r.kind == 0)
+      hipLaunchKernelGGL((k_attn<WT, 8, 64>), grid, dim3(kWG), 0, S(s), c, r);
+    else
+      hipLaunchKernelGGL((k_attn<WT, 64, 64>), grid, dim3(kWG), 0, S(s), c, r);
+  }
+}
+
+template <typename WT>
+void Launch<WT>::pdm_fc(const Ctx& c, int prefill, int nrows, void* s) {
+  const dim3 grid((c.d + 15) / 16);
+  hipLaunchKernelGGL((k_pdm_fc<WT>), grid, dim3(kWG), gemv_lds<WT>(c.n * c.d, kMaxRows), S(s), c, prefill, nrows);
+}
+
+template <typename WT>
+void Launch<WT>::head(const Ctx& c, int src, int row, void* s) {
+  const dim3 grid((c.V + 15) / 16);
+  hipLaunchKernelGGL((k_head<WT>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, src, row, src == 1 ? 1 : 0);
+}
+
+template <typename WT>
+void Launch<WT>::embed_rows(const Ctx& c, int t0, int nrows, void* s) {
+  hipLaunchKernelGGL((k_embed_rows<WT>), dim3(nrows), dim3(kWG), 0, S(s), c, t0, nrows);
+}
+
+template struct Launch<float>;
+template struct Launch<uint16_t>;
+
+void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* s, int bf16) {
+  if (bf16)
+    hipLaunchKernelGGL((k_verify<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
+  else
+    hipLaunchKernelGGL((k_verify<float>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
+}
+
+void launch_reseed(const Ctx& c, int keep, int tok, int prompt_len, void* s, int bf16) {
+  if (bf16)
+    hipLaunchKernelGGL((k_reseed<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
+  else
+    hipLaunchKernelGGL((k_reseed<float>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
+}
+
+}  // namespace spd

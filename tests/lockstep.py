@@ -1,0 +1,125 @@
+"""Run the HIP path (through the C ABI) and the CPU oracle side by side and compare every step.
+
+Tolerances (float results): hidden states relative L2 <= 2e-2; logits max abs <= 5e-2; top-1 tokens
+identical unless the oracle's top-2 margin is below 1e-2, in which case the two runs may part ways
+and the comparison stops there (both choices are correct)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+from oracle import model as om
+from oracle import spd as osp
+
+REL_HIDDEN = 2e-2
+ABS_LOGIT = 5e-2
+TIE_MARGIN = 1e-2
+
+
+def rel_l2(a, b) -> float:
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30))
+
+
+def margin(logits) -> float:
+    top = np.sort(np.asarray(logits))[-2:]
+    return float(top[1] - top[0])
+
+
+class NearTie(Exception):
+    pass
+
+
+def compare_state(eng, ora, tag, worst):
+    """In-flight residual streams and anchors of every in-flight position."""
+    res = eng.resid()
+    anch = eng.anchors()
+    n = ora.n
+    for q in range(ora.c, ora.c + ora.a):
+        r = rel_l2(res[q % n], ora.hidden[q])
+        worst["hidden"] = max(worst["hidden"], r)
+        assert r <= REL_HIDDEN, f"{tag}: hidden state of position {q} rel L2 {r:.3e}"
+        for j, an in enumerate(ora.anch[q]):
+            r = rel_l2(anch[q % n][j], an)
+            worst["hidden"] = max(worst["hidden"], r)
+            assert r <= REL_HIDDEN, f"{tag}: anchor {j} of position {q} rel L2 {r:.3e}"
+
+
+def run_lockstep(eng, model, prompt, n_steps, draft_for=None, check_pdm=True, log=None):
+    """eng: paper_2605_30852_amd.engine.Engine with debug on. Returns worst errors seen."""
+    ora = osp.SPDOracle(model, n=eng.n)
+    worst = {"hidden": 0.0, "logit": 0.0, "pdm_hidden": 0.0, "pdm_logit": 0.0, "steps": 0, "near_tie": 0}
+    eng.spd_set_debug(True)
+    xg = eng.spd_prefill(prompt)
+    # the oracle's first token and its margin
+    xo = ora.prefill(prompt)
+    if xg != xo:
+        lg = om.lm_logits(ora.m, _last_prompt_hidden(ora, model, prompt))
+        if margin(lg) < TIE_MARGIN:
+            worst["near_tie"] = 1
+            return worst
+        raise AssertionError(f"prefill token {xg} != oracle {xo}")
+    compare_state(eng, ora, "prefill", worst)
+    for i in range(n_steps):
+        q = ora.c + ora.a
+        fd = draft_for(q) if draft_for is not None else None
+        rg = eng.spd_step(fd)
+        ro = ora.step(forced_draft=fd, want_logits=True)
+        tag = f"step {i} (c={ro.c} a={ro.a})"
+        # PDM: hidden rows and logits
+        if check_pdm:
+            ph = eng.pdm_hidden()
+            c0 = min(ro.pdm_hidden)
+            for qq, h in ro.pdm_hidden.items():
+                r = rel_l2(ph[qq - c0], h)
+                worst["pdm_hidden"] = max(worst["pdm_hidden"], r)
+                assert r <= REL_HIDDEN, f"{tag}: PDM row {qq} rel L2 {r:.3e}"
+            pl = eng.pdm_logits()
+            e = float(np.max(np.abs(pl - ro.pdm_logits)))
+            worst["pdm_logit"] = max(worst["pdm_logit"], e)
+            assert e <= ABS_LOGIT, f"{tag}: PDM logits max abs {e:.3e}"
+            if rg.pdm_draft != ro.pdm_draft:
+                if margin(ro.pdm_logits) >= TIE_MARGIN:
+                    raise AssertionError(f"{tag}: PDM draft {rg.pdm_draft} != oracle {ro.pdm_draft}")
+                worst["near_tie"] = 1
+                break
+        if ro.exit_logits is not None:
+            el = eng.exit_logits()
+            e = float(np.max(np.abs(el - ro.exit_logits)))
+            worst["logit"] = max(worst["logit"], e)
+            assert e <= ABS_LOGIT, f"{tag}: exit logits max abs {e:.3e}"
+            if rg.target_argmax != ro.target_argmax:
+                if margin(ro.exit_logits) >= TIE_MARGIN:
+                    raise AssertionError(f"{tag}: target argmax {rg.target_argmax} != {ro.target_argmax}")
+                worst["near_tie"] = 1
+                break
+        assert rg.decision == ro.decision, f"{tag}: decision {rg.decision} != {ro.decision}"
+        assert (rg.committed_len, rg.inflight) == (ro.c, ro.a), f"{tag}: (c, a) differ"
+        if ro.decision != osp.NONE:
+            assert (rg.exited_pos, rg.verified_pos, rg.verified_token) == \
+                   (ro.exited_pos, ro.verified_pos, ro.verified_token), tag
+        compare_state(eng, ora, tag, worst)
+        worst["steps"] += 1
+        if log is not None:
+            log.append((rg.as_dict(), ro.decision))
+    toks = eng.tokens()
+    if not worst["near_tie"]:
+        assert list(toks[: ora.c + 1]) == ora.toks[: ora.c + 1]
+    print("lockstep worst:", worst, file=sys.stderr)
+    return worst
+
+
+def _last_prompt_hidden(ora, model, prompt):
+    full = om.forward_full(model, prompt, layers_out=[model.shape.n_layers])
+    return full[model.shape.n_layers][-1]
+
+
+def forced_table(ref, mask, prompt_len, vocab):
+    """draft override by position: the reference token where the mask bit is set, a wrong one else."""
+    table = {}
+    for i, t in enumerate(ref):
+        q = prompt_len + i
+        table[q] = int(t) if mask[q] else int((t + 1) % vocab)
+    return table

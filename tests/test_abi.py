@@ -1,0 +1,83 @@
+"""The C-ABI library loads, exports every entry point include/spd.h declares, and its host-only
+calls (sizes, stage bounds, argument checks) behave without a GPU."""
+import os
+import re
+
+import pytest
+
+import synth
+from paper_2605_30852_amd import binding as B
+from paper_2605_30852_amd.engine import make_config
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    src = open(os.path.join(ROOT, "include", "spd.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(spd_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.lib()
+    names = declared_symbols()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), f"{n} is declared in include/spd.h but not exported"
+    assert set(names) == set(B.EXPORTS)
+
+
+def test_status_strings():
+    assert B.status_str(B.SPD_OK) == "SPD_OK"
+    for s in (B.SPD_E_INVAL, B.SPD_E_STATE, B.SPD_E_CAPACITY, B.SPD_E_HIP):
+        assert B.status_str(s).startswith("SPD_E_")
+
+
+@pytest.mark.parametrize("L,n", [(36, 4), (36, 8), (36, 6), (4, 3), (4, 1), (5, 5)])
+def test_stage_bounds_match_uniform_split(L, n):
+    cfg = make_config(synth.TINY.with_(n_layers=L), 128, n=n)
+    assert B.spd_stage_bounds(cfg) == [s * L // n for s in range(n + 1)]
+
+
+def test_workspace_size_accounts_for_the_kv_pools():
+    cfg = make_config(synth.B4, 2304)
+    ws = B.spd_workspace_size(cfg)
+    kv = 36 * (2304 // 16) * 2 * 8 * 16 * 128 * 2
+    assert kv < ws < kv + 200 * 2**20
+    # the long-context workload: 32k positions of bf16 KV for 36 layers + 2 PDM layers
+    cfg5 = make_config(synth.B9_LONG, 32768 + 520)
+    assert B.spd_workspace_size(cfg5) > 38 * 33288 * 4096
+
+
+@pytest.mark.parametrize("field,value", [
+    ("head_dim", 96), ("n_kv_heads", 3), ("n_stages", 0), ("n_stages", 9), ("pdm_layers", 0),
+    ("page_size", 32), ("dtype", 7), ("d_model", 260), ("ffn_dim", 1001), ("max_tokens", 2),
+    ("attn_chunk", 20), ("rms_eps", 0.0),
+])
+def test_invalid_configs_are_rejected(field, value):
+    cfg = make_config(synth.TINY, 128)
+    setattr(cfg, field, value)
+    with pytest.raises(B.SPDError) as e:
+        B.spd_workspace_size(cfg)
+    assert e.value.status == B.SPD_E_INVAL
+
+
+def test_n_larger_than_layers_rejected():
+    cfg = make_config(synth.TINY, 128, n=5)  # tiny has 4 layers
+    with pytest.raises(B.SPDError):
+        B.spd_stage_bounds(cfg)
+
+
+def test_init_rejects_null_arguments_before_touching_the_gpu():
+    import ctypes as ct
+    cfg = make_config(synth.TINY, 128)
+    w = B.spd_weights()  # all NULL
+    h = ct.c_void_p(0)
+    st = B.lib().spd_init(ct.byref(cfg), ct.byref(w), ct.c_void_p(0), 0, ct.c_void_p(1), ct.c_void_p(2),
+                          ct.byref(h))
+    assert st == B.SPD_E_INVAL and h.value is None
+    assert "NULL" in B.lib().spd_last_error(None).decode()
+    # every call checks its handle
+    assert B.lib().spd_step(None, None, None) == B.SPD_E_INVAL
+    assert B.lib().spd_rollback(None, 0, 0) == B.SPD_E_INVAL
+    assert B.lib().spd_prefill(None, None, 0, None) == B.SPD_E_INVAL

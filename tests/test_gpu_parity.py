@@ -1,0 +1,195 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, step by step, and the lossless
+greedy invariant of the GPU path itself (SPD token ids and decisions bit-exact against the GPU's
+plain greedy decode, i.e. the same library at n = 1)."""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import model as om
+from oracle import spd as osp
+from tests.lockstep import forced_table, run_lockstep
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+SEED = 11
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def tiny_w():
+    from paper_2605_30852_amd.engine import DeviceWeights
+    return DeviceWeights(synth.TINY, SEED)
+
+
+@pytest.fixture(scope="module")
+def mid_w():
+    from paper_2605_30852_amd.engine import DeviceWeights
+    return DeviceWeights(synth.MID, SEED)
+
+
+def _engine(w, n, max_tokens=160, **kw):
+    from paper_2605_30852_amd.engine import Engine
+    return Engine(w, max_tokens=max_tokens, n=n, page_seed=kw.pop("page_seed", 5), **kw)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4])
+def test_tiny_fp32_lockstep_forced(tiny_w, n):
+    _say(f"[tiny lockstep forced n={n}]")
+    sh = synth.TINY
+    model = om.Model(sh, SEED)
+    prompt = synth.prompt(sh, SEED, 37)  # 37 rows: several 8-row prefill chunks and a ragged tail
+    ref = om.ar_greedy(model, prompt, 30)
+    mask = synth.accept_mask(0.7, SEED, 200)
+    tab = forced_table(ref, mask, len(prompt), sh.vocab)
+    eng = _engine(tiny_w, n)
+    w = run_lockstep(eng, model, prompt, 24, draft_for=lambda q: tab.get(q))
+    eng.close()
+    assert w["steps"] >= 10 or w["near_tie"]
+    assert w["hidden"] < 1e-4  # fp32 weights and KV: only summation order differs
+
+
+@pytest.mark.parametrize("n", [2])
+def test_tiny_fp32_lockstep_natural_drafts(tiny_w, n):
+    _say(f"[tiny lockstep natural n={n}]")
+    sh = synth.TINY
+    model = om.Model(sh, SEED)
+    prompt = synth.prompt(sh, SEED, 20)
+    eng = _engine(tiny_w, n)
+    w = run_lockstep(eng, model, prompt, 16)
+    eng.close()
+    assert w["steps"] >= 8 or w["near_tie"]
+
+
+@pytest.mark.parametrize("n", [1, 3])
+def test_mid_bf16_lockstep(mid_w, n):
+    """bf16 weights and KV, ragged FFN (1000) and vocabulary (3001), chunked attention splits."""
+    _say(f"[mid lockstep n={n}]")
+    sh = synth.MID
+    model = om.Model(sh, SEED)
+    prompt = synth.prompt(sh, SEED, 75)
+    ref = om.ar_greedy(model, prompt, 24)
+    mask = synth.accept_mask(0.6, SEED + 1, 300)
+    tab = forced_table(ref, mask, len(prompt), sh.vocab)
+    eng = _engine(mid_w, n, max_tokens=200, attn_chunk=32)
+    w = run_lockstep(eng, model, prompt, 20, draft_for=lambda q: tab.get(q))
+    eng.close()
+    assert w["steps"] >= 8 or w["near_tie"]
+
+
+def _gpu_stream(w, n, prompt, steps, table=None, max_tokens=400, **kw):
+    eng = _engine(w, n, max_tokens=max_tokens, **kw)
+    first = eng.spd_prefill(prompt)
+    if table is not None:
+        base = len(prompt)
+        arr = np.full(len(table) + 8, -1, dtype=np.int32)
+        for q, t in table.items():
+            arr[q - base] = t
+        eng.spd_set_forced_drafts(arr, base)
+    res = [eng.spd_step().as_dict() for _ in range(steps)]
+    toks = eng.tokens()
+    c = res[-1]["committed_len"]
+    eng.close()
+    return first, list(toks[len(prompt): c + 1]), res
+
+
+@pytest.mark.parametrize("which", ["tiny", "mid"])
+@pytest.mark.parametrize("p", [None, 0.7, 1.0])
+def test_lossless_gpu_spd_equals_gpu_greedy(tiny_w, mid_w, which, p):
+    """Token ids and decisions of the GPU's own SPD run are bit-exact against the GPU's plain greedy
+    decode (n = 1 through the same library), for natural and forced drafts."""
+    w = tiny_w if which == "tiny" else mid_w
+    sh = w.shape
+    prompt = synth.prompt(sh, SEED + 3, 29)
+    _say(f"[lossless {which} p={p}] AR reference")
+    first, ar, _ = _gpu_stream(w, 1, prompt, 40, max_tokens=200)
+    for n in (2, 3, 4):
+        _say(f"[lossless {which} p={p}] n={n}")
+        table = None
+        mask = None
+        if p is not None:
+            mask = synth.accept_mask(p, SEED + n, 400)
+            table = forced_table([first] + ar, mask, len(prompt), sh.vocab)
+        f2, toks, res = _gpu_stream(w, n, prompt, 40, table, max_tokens=200)
+        assert f2 == first
+        m = len(toks)
+        assert m >= 2
+        assert toks == ([first] + ar)[:m], f"n={n}: SPD stream differs from greedy"
+        if p is not None:
+            for r in res:
+                if r["decision"] != 0:
+                    assert r["decision"] == (1 if mask[r["verified_pos"]] else 2)
+            K = osp.simulate_steps(n, m, lambda q: bool(mask[q]), len(prompt))
+            assert len(res) >= K
+
+
+def test_run_steps_matches_step_by_step(mid_w):
+    _say("[run_steps]")
+    sh = mid_w.shape
+    prompt = synth.prompt(sh, SEED + 4, 40)
+    first, ar, _ = _gpu_stream(mid_w, 1, prompt, 30, max_tokens=200)
+    mask = synth.accept_mask(0.7, 99, 400)
+    table = forced_table([first] + ar, mask, len(prompt), sh.vocab)
+    _, toks_a, res_a = _gpu_stream(mid_w, 3, prompt, 24, table, max_tokens=200)
+    eng = _engine(mid_w, 3, max_tokens=200)
+    eng.spd_prefill(prompt)
+    arr = np.full(len(table) + 8, -1, dtype=np.int32)
+    for q, t in table.items():
+        arr[q - len(prompt)] = t
+    eng.spd_set_forced_drafts(arr, len(prompt))
+    log = eng.spd_run_steps(24, want_log=True)
+    assert [r["decision"] for r in log] == [r["decision"] for r in res_a]
+    assert [r["committed_len"] for r in log] == [r["committed_len"] for r in res_a]
+    eng.close()
+
+
+def test_rollback_api_and_state_errors(tiny_w):
+    """spd_rollback to an earlier length continues like the oracle does after the same rollback;
+    illegal call orders return SPD_E_STATE."""
+    from paper_2605_30852_amd import binding as B
+    sh = synth.TINY
+    model = om.Model(sh, SEED)
+    prompt = synth.prompt(sh, SEED + 5, 16)
+    eng = _engine(tiny_w, 2, auto_rollback=False)
+    with pytest.raises(B.SPDError) as e:
+        eng.spd_step()
+    assert e.value.status == B.SPD_E_STATE
+    ora = osp.SPDOracle(model, n=2)
+    assert eng.spd_prefill(prompt) == ora.prefill(prompt)
+    with pytest.raises(B.SPDError) as e:
+        eng.spd_prefill(prompt)
+    assert e.value.status == B.SPD_E_STATE
+    # natural drafts with random weights reject: the handle then waits for spd_rollback
+    pending = False
+    for _ in range(6):
+        r = eng.spd_step()
+        ro = ora.step()
+        assert r.decision == ro.decision
+        if r.decision == B.SPD_REJECT:
+            pending = True
+            with pytest.raises(B.SPDError) as e:
+                eng.spd_step()
+            assert e.value.status == B.SPD_E_STATE
+            eng.spd_rollback(r.committed_len, r.target_argmax)
+    assert pending
+    # explicit rollback to an earlier length with another token
+    keep = ora.c - 1
+    with pytest.raises(B.SPDError):
+        eng.spd_rollback(len(prompt) - 1, 3)  # below the prompt
+    eng.spd_rollback(keep, 17)
+    ora.rollback(keep, 17)
+    eng.spd_set_debug(True)
+    for _ in range(4):
+        r = eng.spd_step()
+        ro = ora.step()
+        if r.decision == B.SPD_REJECT:
+            eng.spd_rollback(r.committed_len, r.target_argmax)
+        res = eng.resid()
+        for q in range(ora.c, ora.c + ora.a):
+            assert np.linalg.norm(res[q % 2] - ora.hidden[q]) <= 2e-2 * np.linalg.norm(ora.hidden[q])
+    eng.close()
