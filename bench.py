@@ -58,6 +58,7 @@ def cpu_baseline(sh, n, ctx, seed):
     cache = om.LayerCache(sh.n_kv_heads, sh.head_dim, ctx + 8)
     cache.k[:ctx] = rng.standard_normal((ctx, sh.n_kv_heads, sh.head_dim))
     cache.v[:ctx] = rng.standard_normal((ctx, sh.n_kv_heads, sh.head_dim))
+    cache.n = ctx
     lw = model.layer(0)
     h = rng.standard_normal(sh.d_model)
     reps = 4
@@ -108,6 +109,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ar", action="store_true", help="skip the plain greedy tokens/s line")
+    ap.add_argument("--no-graph", action="store_true", help="issue every launch instead of replaying the step graph")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the SPD step here is the single-GPU stage-batched "
@@ -140,6 +142,7 @@ def main():
     # plain greedy decoding (n = 1 through the same library): reference tokens and AR tokens/s
     t0 = time.time()
     ar = Engine(weights, max_tokens=max_tokens, n=1)
+    ar.spd_set_graph(not args.no_graph)
     first = ar.spd_prefill(prompt)
     log(f"[bench] AR prefill {P} tokens in {time.time() - t0:.1f}s")
     n_ref = W + 2 * K + 2 * n + 8
@@ -156,6 +159,7 @@ def main():
 
     # SPD handle, all drafts forced to the greedy tokens: every step after the fill is a full step
     eng = Engine(weights, max_tokens=max_tokens, n=n)
+    eng.spd_set_graph(not args.no_graph)
     f2 = eng.spd_prefill(prompt)
     assert f2 == first
     eng.spd_set_forced_drafts(ref.astype(np.int32), P)
@@ -243,6 +247,7 @@ def main():
         "vs_baseline": None,
         "dtype": sh.dtype,
         "data": "synthetic (seeded N(0,0.02) weights, uniform-random prompt)",
+        "graph": not args.no_graph,
         "config": {"workload": f"{sh.name}-class dense decoder, SPD width n={n}, PDM {sh.pdm_layers} layer, "
                                f"{P}-token prompt, steady-state full-pipeline steps",
                    "n": n, "layers": sh.n_layers, "d_model": sh.d_model, "prompt": P,

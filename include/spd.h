@@ -190,6 +190,11 @@ spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes)
 spd_status spd_read_kv(spd_handle* h, int32_t pdm, int32_t layer, int32_t pos0, int32_t count,
                        void* host_k, void* host_v);
 
+/* 1: steps without a per-call draft override replay a HIP graph of the step (both streams, captured
+ * on first use) instead of issuing each launch; 0 (default): issue the launches. The step's launch
+ * sequence does not depend on host state, so one capture serves every step. */
+spd_status spd_set_graph(spd_handle* h, int32_t on);
+
 /* 1: every LM-head pass also writes its full logits (for SPD_DBG_*_LOGITS). */
 spd_status spd_set_debug(spd_handle* h, int32_t on);
 

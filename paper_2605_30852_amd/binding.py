@@ -57,7 +57,7 @@ EXPORTS = [
     "spd_workspace_size", "spd_stage_bounds", "spd_init", "spd_prefill", "spd_step", "spd_rollback",
     "spd_set_forced_drafts", "spd_clear_forced_drafts", "spd_run_steps", "spd_sync", "spd_read_debug",
     "spd_read_kv", "spd_set_debug", "spd_destroy", "spd_status_str", "spd_last_error",
-    "spd_set_kernel_timing", "spd_kernel_timing",
+    "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -94,6 +94,7 @@ def lib() -> ct.CDLL:
             "spd_read_kv": (I, [P, I, I, I, I, P, P]),
             "spd_set_debug": (I, [P, I]),
             "spd_set_kernel_timing": (I, [P, I]),
+            "spd_set_graph": (I, [P, I]),
             "spd_kernel_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
             "spd_destroy": (None, [P]),
             "spd_status_str": (ct.c_char_p, [I]),
@@ -211,6 +212,10 @@ def spd_kernel_timing(h: int):
     n = ct.c_int32(0)
     _check("spd_kernel_timing", lib().spd_kernel_timing(h, ct.byref(ms), ct.byref(n)), h)
     return ms.value, n.value
+
+
+def spd_set_graph(h: int, on: bool) -> None:
+    _check("spd_set_graph", lib().spd_set_graph(h, 1 if on else 0), h)
 
 
 def spd_destroy(h: int) -> None:

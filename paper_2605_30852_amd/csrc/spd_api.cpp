@@ -24,7 +24,7 @@ enum HState { H_INIT = 0, H_READY = 1, H_PENDING = 2 };
 
 struct Layout {
   size_t kv, pkv, pt, rope, state, tok, forced, log, resid, anch, pdmx, pfx, pfanch, dbg, lay;
-  size_t q[2], ao[2], act[2], part[2], cnt[2], hpv[2], hpi[2], hcnt[2];
+  size_t q[2], ao[2], act[2], part[2], cnt[2], hpv[2], hpi[2];
   size_t total;
   int num_pages, chunk, max_splits, head_tiles;
   size_t kv_layer_bytes;
@@ -68,9 +68,14 @@ Layout make_layout(const spd_config& c) {
   const int qdim = c.n_q_heads * dh;
   const int G = c.n_q_heads / hkv;
   L.num_pages = (c.max_tokens + c.page_size - 1) / c.page_size;
-  L.chunk = c.attn_chunk ? c.attn_chunk : (c.max_tokens <= 4096 ? 64 : (c.max_tokens <= 16384 ? 128 : 256));
+  // about 40 splits at full capacity, 64..2048 keys each: enough workgroups for the short
+  // contexts, few partials for the long ones
+  {
+    int ch = (c.max_tokens / 40 + 63) / 64 * 64;
+    L.chunk = c.attn_chunk ? c.attn_chunk : std::min(2048, std::max(64, ch));
+  }
   L.max_splits = (c.max_tokens + L.chunk - 1) / L.chunk;
-  L.head_tiles = (c.vocab + 15) / 16;
+  L.head_tiles = (c.vocab + 63) / 64;
   L.kv_layer_bytes = (size_t)L.num_pages * 2 * hkv * c.page_size * dh * esz;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -103,7 +108,6 @@ Layout make_layout(const spd_config& c) {
     L.cnt[s] = take(sizeof(int32_t) * kMaxStages * hkv);
     L.hpv[s] = take(sizeof(float) * L.head_tiles);
     L.hpi[s] = take(sizeof(int32_t) * L.head_tiles);
-    L.hcnt[s] = take(sizeof(int32_t) * 64);
   }
   L.total = o;
   return L;
@@ -132,6 +136,9 @@ struct spd_handle {
   spd_step_result* pinned = nullptr;  // [kLogCap + 1]
   std::vector<int32_t> page_table;
   std::string err;
+  // step graph (fork/join of both streams captured once, replayed per step)
+  int use_graph = 0;
+  hipGraphExec_t gexec = nullptr;
   // kernel timing
   int timed_kernel = 0;
   std::vector<hipEvent_t> tev;  // pool, pairs
@@ -412,7 +419,6 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
     B.cnt = (int32_t*)(ws + lay.cnt[s]);
     B.hpart_v = (float*)(ws + lay.hpv[s]);
     B.hpart_i = (int32_t*)(ws + lay.hpi[s]);
-    B.hcnt = (int32_t*)(ws + lay.hcnt[s]);
   }
 
   // layer table
@@ -461,19 +467,20 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   HIPI(hipMemsetAsync(ws + lay.state, 0, sizeof(DevState), h->main));
   HIPI(hipMemsetAsync(ws + lay.tok, 0, sizeof(int32_t) * (c.max_tokens + 8), h->main));
   HIPI(hipMemsetAsync(ws + lay.forced, 0xff, sizeof(int32_t) * (c.max_tokens + 8), h->main));
-  for (int s = 0; s < 2; s++) {
-    HIPI(hipMemsetAsync(ws + lay.cnt[s], 0, sizeof(int32_t) * kMaxStages * c.n_kv_heads, h->main));
-    HIPI(hipMemsetAsync(ws + lay.hcnt[s], 0, sizeof(int32_t) * 64, h->main));
-  }
+  for (int s = 0; s < 2; s++) HIPI(hipMemsetAsync(ws + lay.cnt[s], 0, sizeof(int32_t) * kMaxStages * c.n_kv_heads, h->main));
   HIPI(hipStreamSynchronize(h->main));
 #undef HIPI
   *out = h;
   return SPD_OK;
 }
 
+static void drop_graph(spd_handle* h);
+static spd_status run_one_step(spd_handle* h, int forced_override);
+
 spd_status spd_set_debug(spd_handle* h, int32_t on) {
   if (!h) return SPD_E_INVAL;
   h->ctx.debug = on ? 1 : 0;
+  drop_graph(h);  // kernel arguments changed
   return SPD_OK;
 }
 
@@ -525,14 +532,52 @@ spd_status spd_step(spd_handle* h, const int32_t* forced_draft, spd_step_result*
   spd_status sy = ensure_synced(h);
   if (sy != SPD_OK) return sy;
   if (h->c + h->a >= h->cfg.max_tokens) return SPD_E_CAPACITY;
-  spd_status st = h->bf16 ? enqueue_step<uint16_t>(h, forced_draft ? *forced_draft : -1)
-                          : enqueue_step<float>(h, forced_draft ? *forced_draft : -1);
+  spd_status st = run_one_step(h, forced_draft ? *forced_draft : -1);
   if (st != SPD_OK) return st;
   st = fetch_state(h);
   if (st != SPD_OK) return st;
   const spd_step_result r = h->pinned[0];
   if (r.decision == SPD_REJECT && !h->cfg.auto_rollback) h->hstate = H_PENDING;
   if (out) *out = r;
+  return SPD_OK;
+}
+
+static void drop_graph(spd_handle* h) {
+  if (h->gexec) (void)hipGraphExecDestroy(h->gexec);
+  h->gexec = nullptr;
+}
+
+// One step: a replay of the captured step graph when graph mode is on (and no per-step override or
+// kernel timing is active), else the launches themselves.
+static spd_status run_one_step(spd_handle* h, int forced_override) {
+  const bool graph = h->use_graph && forced_override < 0 && h->timed_kernel == 0;
+  if (!graph) return h->bf16 ? enqueue_step<uint16_t>(h, forced_override) : enqueue_step<float>(h, forced_override);
+  if (!h->gexec) {
+    hipGraph_t g = nullptr;
+    HIPC(hipStreamBeginCapture(h->main, hipStreamCaptureModeRelaxed));
+    spd_status st = h->bf16 ? enqueue_step<uint16_t>(h, -1) : enqueue_step<float>(h, -1);
+    hipError_t e = hipStreamEndCapture(h->main, &g);
+    if (st != SPD_OK) return st;
+    if (e != hipSuccess) {
+      h->err = std::string("hipStreamEndCapture: ") + hipGetErrorString(e);
+      return SPD_E_HIP;
+    }
+    e = hipGraphInstantiate(&h->gexec, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (e != hipSuccess) {
+      h->gexec = nullptr;
+      h->err = std::string("hipGraphInstantiate: ") + hipGetErrorString(e);
+      return SPD_E_HIP;
+    }
+  }
+  HIPC(hipGraphLaunch(h->gexec, h->main));
+  return SPD_OK;
+}
+
+spd_status spd_set_graph(spd_handle* h, int32_t on) {
+  if (!h) return SPD_E_INVAL;
+  h->use_graph = on ? 1 : 0;
+  if (!on) drop_graph(h);
   return SPD_OK;
 }
 
@@ -543,7 +588,7 @@ spd_status spd_run_steps(spd_handle* h, int32_t count, spd_step_result* log) {
   if (h->bound + count > h->cfg.max_tokens) return SPD_E_CAPACITY;
   HIPC(hipSetDevice(h->dev));
   for (int i = 0; i < count; i++) {
-    spd_status st = h->bf16 ? enqueue_step<uint16_t>(h, -1) : enqueue_step<float>(h, -1);
+    spd_status st = run_one_step(h, -1);
     if (st != SPD_OK) return st;
   }
   h->bound += count;
@@ -707,6 +752,7 @@ spd_status spd_kernel_timing(spd_handle* h, double* total_ms, int32_t* launches)
 
 void spd_destroy(spd_handle* h) {
   if (!h) return;
+  drop_graph(h);
   for (hipEvent_t e : h->tev) (void)hipEventDestroy(e);
   if (h->main) (void)hipStreamSynchronize(h->main);
   if (h->pdm) (void)hipStreamSynchronize(h->pdm);

@@ -49,10 +49,9 @@ struct BufSet {
   float* ao;        // [8][Hq*dh] attention outputs
   float* act;       // [8][F] SwiGLU activations
   float* part;      // attention split partials
-  int32_t* cnt;     // attention combine counters [8 * Hkv], zero between launches
-  float* hpart_v;   // LM-head partial maxima [tiles][2]
-  int32_t* hpart_i; // LM-head partial argmax [tiles][2]
-  int32_t* hcnt;    // LM-head combine counter
+  int32_t* cnt;     // per (stage, KV head) split tickets of the decode attention; zero at rest
+  float* hpart_v;   // LM-head per-tile maxima [tiles]
+  int32_t* hpart_i; // LM-head per-tile argmax [tiles]
 };
 
 struct Ctx {

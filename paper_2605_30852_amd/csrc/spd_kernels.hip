@@ -58,6 +58,15 @@ __device__ __forceinline__ void unpack16<uint16_t>(const uint4& v, float* o) {
   o[7] = bf_hi(v.w);
 }
 
+// 16-byte load through the global address space (the pointers come from tables in memory, so
+// the compiler cannot infer it and would otherwise emit flat loads).
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const v4u gv4u;
+__device__ __forceinline__ uint4 ldg16(const void* p) {
+  const v4u v = *(gv4u*)(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 template <typename T>
 __device__ __forceinline__ float ld1(const T* p, size_t i);
 template <>
@@ -162,7 +171,7 @@ __device__ __forceinline__ void accum_chunk(const WT* const (&wr)[RL], int K, in
 #pragma unroll
     for (int r = 0; r < RL; r++) {
       if (wr[r] != nullptr && col < K)
-        w[r] = *reinterpret_cast<const uint4*>(wr[r] + col);
+        w[r] = ldg16(wr[r] + col);
       else
         w[r] = make_uint4(0u, 0u, 0u, 0u);
     }
@@ -515,9 +524,11 @@ __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_ar
 }
 
 // ---------------------------------------------------------------------------- LM head + argmax
-// Tile = 16 vocabulary rows. Each workgroup keeps its best (value, index) with the lowest index
-// winning ties; the last workgroup to finish reduces the partials. The (value desc, index asc)
-// order is total, so the winner does not depend on the reduction order.
+constexpr int kHeadRowsPerWave = 16;  // 64 vocabulary rows per workgroup
+
+// Tile = 64 vocabulary rows. Each workgroup writes its best (value, index), the lowest index
+// winning ties; the single-workgroup kernel that follows on the stream reduces the partials. The
+// (value desc, index asc) order is total, so the winner does not depend on the reduction order.
 __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
@@ -527,52 +538,60 @@ __global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row, int set) 
   extern __shared__ float lds[];
   __shared__ float s_v[4];
   __shared__ int s_i[4];
-  __shared__ int s_last;
+  __shared__ float red[4];
   const float* x;
   const float* gain;
-  int* dst;
   if (src == 0) {
     const int a = C.st->a, c = C.st->c;
     if (a != C.n) return;  // nothing exits while the pipeline fills
     x = C.resid + (size_t)(c % C.n) * C.d;
     gain = C.final_norm;
-    dst = &C.st->y;
   } else if (src == 1) {
     x = C.pdm_x + (size_t)(C.st->a - 1) * C.d;
     gain = C.pdm_norm;
-    dst = &C.st->pdm_draft;
   } else {
     x = C.pf_x + (size_t)row * C.d;
     gain = C.final_norm;
-    dst = &C.st->y;
   }
+  constexpr int VE = Elt<WT>::VE;
+  constexpr int BLK = 64 * VE;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int m0 = blockIdx.x * 16 + w * 4;
-  const WT* W = (const WT*)C.lm_head;
-  const WT* wr[4];
-#pragma unroll
-  for (int r = 0; r < 4; r++) wr[r] = (m0 + r < C.V) ? W + (size_t)(m0 + r) * C.d : nullptr;
+  // stage rmsnorm-gain input once (d fits one chunk), then stream 4 groups of 4 rows per wave
   XSpec xs;
   xs.src = XS_NORM_RESID;
   xs.gain = gain;
   xs.row[0] = x;
-  const int KC = chunk_floats<1>(C.d, 64 * Elt<WT>::VE);
-  float acc[1][4];
-  gemv_tile<WT, 1, 4>(wr, C.d, xs, 1, C.eps, lds, KC, acc);
-  if (C.debug && lane < 4 && m0 + lane < C.V) {
-    float val = acc[0][0];
-#pragma unroll
-    for (int r = 1; r < 4; r++)
-      if (lane == r) val = acc[0][r];
-    C.dbg_logits[(size_t)(src == 1 ? 1 : 0) * C.V + m0 + lane] = val;
-  }
+  const int KC = chunk_floats<1>(C.d, BLK);
+  const int kl_pad = (C.d + BLK - 1) / BLK * BLK;
+  float ss[1] = {0.f};
+  stage_chunk<VE, 1>(xs, 1, 0, C.d, kl_pad, lds, KC, ss);
+  const float tot = block_sum(ss[0], red);  // includes the barrier that publishes the staged row
+  const float scl = 1.0f / sqrtf(tot / (float)C.d + C.eps);
+  const WT* W = (const WT*)C.lm_head;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
+  for (int rg = 0; rg < kHeadRowsPerWave / 4; rg++) {
+    const int m0 = blockIdx.x * (4 * kHeadRowsPerWave) + w * kHeadRowsPerWave + rg * 4;
+    const WT* wr[4];
 #pragma unroll
-  for (int r = 0; r < 4; r++) {
-    if (m0 + r < C.V && better(acc[0][r], m0 + r, bv, bi)) {
-      bv = acc[0][r];
-      bi = m0 + r;
+    for (int r = 0; r < 4; r++) wr[r] = (m0 + r < C.V) ? W + (size_t)(m0 + r) * C.d : nullptr;
+    float acc[1][4] = {{0.f, 0.f, 0.f, 0.f}};
+    accum_chunk<WT, 1, 4>(wr, C.d, 0, kl_pad, lds, KC, 1, acc, lane);
+#pragma unroll
+    for (int r = 0; r < 4; r++) acc[0][r] = wave_sum(acc[0][r]) * scl;
+    if (C.debug && lane < 4 && m0 + lane < C.V) {
+      float val = acc[0][0];
+#pragma unroll
+      for (int r = 1; r < 4; r++)
+        if (lane == r) val = acc[0][r];
+      C.dbg_logits[(size_t)(src == 1 ? 1 : 0) * C.V + m0 + lane] = val;
+    }
+#pragma unroll
+    for (int r = 0; r < 4; r++) {
+      if (m0 + r < C.V && better(acc[0][r], m0 + r, bv, bi)) {
+        bv = acc[0][r];
+        bi = m0 + r;
+      }
     }
   }
   if (lane == 0) {
@@ -580,7 +599,6 @@ __global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row, int set) 
     s_i[w] = bi;
   }
   __syncthreads();
-  const BufSet& B = C.b[set];
   if (threadIdx.x == 0) {
     float v = s_v[0];
     int i = s_i[0];
@@ -589,18 +607,22 @@ __global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row, int set) 
         v = s_v[k];
         i = s_i[k];
       }
-    B.hpart_v[blockIdx.x] = v;
-    B.hpart_i[blockIdx.x] = i;
-    __threadfence();
-    const int t = atomicAdd(B.hcnt, 1);
-    s_last = (t == (int)gridDim.x - 1);
+    C.b[set].hpart_v[blockIdx.x] = v;
+    C.b[set].hpart_i[blockIdx.x] = i;
   }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
+}
+
+// Argmax over the LM head's per-tile partials (one workgroup; the next kernel on the stream, so
+// the kernel boundary orders the partial writes). Every thread returns the winner, which is
+// clamped into [0, V) so that all-NaN logits cannot produce an out-of-range id.
+__device__ int reduce_head(const BufSet& B, int tiles, int V) {
+  __shared__ float r_v[4];
+  __shared__ int r_i[4];
+  __shared__ int r_out;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   float v = -INFINITY;
   int i = 0x7fffffff;
-  for (int k = threadIdx.x; k < (int)gridDim.x; k += kWG) {
+  for (int k = threadIdx.x; k < tiles; k += kWG) {
     const float pv = B.hpart_v[k];
     const int pi = B.hpart_i[k];
     if (better(pv, pi, v, i)) {
@@ -608,7 +630,6 @@ __global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row, int set) 
       i = pi;
     }
   }
-  // block argmax: wave butterfly then the 4 wave winners
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
     const float ov = __shfl_xor(v, m, 64);
@@ -620,37 +641,55 @@ __global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row, int set) 
   }
   __syncthreads();
   if (lane == 0) {
-    s_v[w] = v;
-    s_i[w] = i;
+    r_v[w] = v;
+    r_i[w] = i;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    float fv = s_v[0];
-    int fi = s_i[0];
+    float fv = r_v[0];
+    int fi = r_i[0];
     for (int k = 1; k < 4; k++)
-      if (better(s_v[k], s_i[k], fv, fi)) {
-        fv = s_v[k];
-        fi = s_i[k];
+      if (better(r_v[k], r_i[k], fv, fi)) {
+        fv = r_v[k];
+        fi = r_i[k];
       }
-    *dst = (fi >= 0 && fi < C.V) ? fi : 0;  // all-NaN logits cannot leave an out-of-range id
-    atomicExch(B.hcnt, 0);
+    r_out = (fi >= 0 && fi < V) ? fi : 0;
   }
+  __syncthreads();
+  return r_out;
 }
 
 // ------------------------------------------------------------------------------- attention
 // Ragged paged GQA decode attention. Grid: x = key split (chunk keys each), y = KV head, z = group.
 // A group's rows sit at positions pos0..pos0+nrows-1; row i attends to keys [0, pos0+i]. The split
 // count is ceil(keys / chunk), a function of the length only. With one split the workgroup writes
-// the output; otherwise each split writes (m, l, o) and the last split to finish combines them in
-// split order.
+// the output; otherwise each split writes (o, m, l) and k_attn_combine merges them in split order.
+// LDS (dynamic): queries [MAXQ][DH] fp32, scores [MAXQ][PASS] fp32, V tile [PASS][DH] in the KV type.
+template <int MAXQ>
+struct AttnShape {
+  static constexpr int PASS = MAXQ <= 8 ? 64 : 32;  // keys per pass
+  static constexpr int TPK = kWG / PASS;             // threads per key in the score phase
+};
+
+template <typename KVT, int MAXQ, int DH>
+constexpr size_t attn_lds() {
+  return (size_t)MAXQ * DH * 4 + (size_t)MAXQ * AttnShape<MAXQ>::PASS * 4 +
+         (size_t)AttnShape<MAXQ>::PASS * DH * sizeof(KVT) + (size_t)3 * MAXQ * 4;
+}
+
 template <typename KVT, int MAXQ, int DH>
 __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
-  constexpr int PASS = 64;  // keys per pass
-  constexpr int dh = DH;
-  __shared__ float qs[MAXQ * DH];
-  __shared__ float sc[MAXQ * PASS];
-  __shared__ float s_m[MAXQ], s_l[MAXQ], s_al[MAXQ];
-  __shared__ int s_last;
+  constexpr int PASS = AttnShape<MAXQ>::PASS;
+  constexpr int TPK = AttnShape<MAXQ>::TPK;
+  constexpr int NE = DH / TPK;  // dims per thread in the score phase
+  constexpr int VE = Elt<KVT>::VE;
+  extern __shared__ float smem[];
+  float* qs = smem;                       // [MAXQ][DH]
+  float* sc = qs + MAXQ * DH;             // [MAXQ][PASS]
+  KVT* vs = (KVT*)(sc + MAXQ * PASS);     // [PASS][DH]
+  float* s_m = (float*)(vs + PASS * DH);  // [MAXQ]
+  float* s_l = s_m + MAXQ;
+  float* s_al = s_l + MAXQ;
   const Grp gr = resolve(C, R, blockIdx.z);
   if (!gr.active) return;
   const int g = blockIdx.y, split = blockIdx.x;
@@ -662,15 +701,15 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
   const int nq = gr.nrows * G;
   const LayerDesc& Ld = C.lay[gr.layer];
   const KVT* kvb = (const KVT*)Ld.kv;
-  const size_t voff = (size_t)C.hkv * C.page * dh;
+  const size_t voff = (size_t)C.hkv * C.page * DH;
   const BufSet& B = C.b[R.set];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
 
   // queries (already rotated), pre-scaled by 1/sqrt(dh)
-  for (int e = tid; e < nq * dh; e += kWG) {
-    const int qi = e / dh, dd = e % dh;
+  for (int e = tid; e < nq * DH; e += kWG) {
+    const int qi = e / DH, dd = e % DH;
     const int i = qi / G, h = g * G + (qi % G);
-    qs[qi * dh + dd] = B.q[(size_t)(gr.brow0 + i) * C.qdim + h * dh + dd] * C.scale;
+    qs[qi * DH + dd] = B.q[(size_t)(gr.brow0 + i) * C.qdim + h * DH + dd] * C.scale;
   }
   for (int qi = tid; qi < MAXQ; qi += kWG) {
     s_m[qi] = -INFINITY;
@@ -689,17 +728,21 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
   }
   __syncthreads();
 
-  constexpr int NE = DH >> 2;  // dims per thread in the score phase
+  constexpr int VCH = DH * (int)sizeof(KVT) / 16;  // 16-byte chunks per V row
   for (int kp = k0; kp < k1; kp += PASS) {
     const int nk = min(PASS, k1 - kp);
-    // scores: thread -> (key kk, quarter qq)
+    // V tile -> LDS, 16-byte loads (a page holds 16 consecutive keys of one head contiguously)
+    for (int e = tid; e < nk * VCH; e += kWG) {
+      const int kk = e / VCH, ch = e % VCH;
+      const uint4* src = reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + kk, g, 0) + voff) + ch;
+      reinterpret_cast<uint4*>(vs + kk * DH)[ch] = *src;
+    }
+    // scores: thread -> (key kk, part qq of the head dimension)
     {
-      const int kk = tid >> 2, qq = tid & 3;
+      const int kk = tid / TPK, qq = tid % TPK;
       float kr[NE];
       if (kk < nk) {
-        const KVT* kptr = kvb + kv_off(C, kp + kk, g, qq * NE);
-        const uint4* k4 = reinterpret_cast<const uint4*>(kptr);
-        constexpr int VE = Elt<KVT>::VE;
+        const uint4* k4 = reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + kk, g, qq * NE));
 #pragma unroll
         for (int c4 = 0; c4 < NE / VE; c4++) unpack16<KVT>(k4[c4], kr + c4 * VE);
       } else {
@@ -708,7 +751,7 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
       }
       for (int qi = 0; qi < nq; qi++) {
         float dsum = 0.f;
-        const float* qv = qs + qi * dh + qq * NE;
+        const float* qv = qs + qi * DH + qq * NE;
 #pragma unroll
         for (int e = 0; e < NE; e += 4) {
           const float4 q4 = *reinterpret_cast<const float4*>(qv + e);
@@ -717,8 +760,8 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
           dsum = fmaf(q4.z, kr[e + 2], dsum);
           dsum = fmaf(q4.w, kr[e + 3], dsum);
         }
-        dsum += __shfl_xor(dsum, 1, 64);
-        dsum += __shfl_xor(dsum, 2, 64);
+#pragma unroll
+        for (int m = 1; m < TPK; m <<= 1) dsum += __shfl_xor(dsum, m, 64);
         if (qq == 0 && kk < nk) {
           const int lim = gr.pos0 + qi / G;
           sc[qi * PASS + kk] = (kp + kk <= lim) ? dsum : -INFINITY;
@@ -728,11 +771,11 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
     __syncthreads();
     // online softmax update per query vector (one wave per query vector)
     for (int qi = w; qi < nq; qi += 4) {
-      const float s = lane < nk ? sc[qi * PASS + lane] : -INFINITY;
-      const float mx = wave_max(s);
+      const float sv = lane < nk ? sc[qi * PASS + lane] : -INFINITY;
+      const float mx = wave_max(sv);
       const float mo = s_m[qi];
       const float mn = fmaxf(mo, mx);
-      const float p = (s == -INFINITY) ? 0.f : expf(s - mn);
+      const float p = (sv == -INFINITY) ? 0.f : expf(sv - mn);
       if (lane < nk) sc[qi * PASS + lane] = p;
       const float ps = wave_sum(p);
       if (lane == 0) {
@@ -754,8 +797,8 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
       }
     }
     for (int kk = 0; kk < nk; kk++) {
-      const size_t off = kv_off(C, kp + kk, g, 2 * dp) + voff;
-      const float v0 = ld1<KVT>(kvb, off), v1 = ld1<KVT>(kvb, off + 1);
+      const float v0 = ld1<KVT>(vs, (size_t)kk * DH + 2 * dp);
+      const float v1 = ld1<KVT>(vs, (size_t)kk * DH + 2 * dp + 1);
 #pragma unroll
       for (int u = 0; u < MAXU; u++) {
         const int qi = qg + u * NG;
@@ -769,8 +812,6 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
     __syncthreads();
   }
 
-  const int RS = MAXQ * (dh + 2);  // partial record: o[MAXQ][dh], m[MAXQ], l[MAXQ]
-  const int cidx = blockIdx.z * C.hkv + g;
   if (nsplit == 1) {
 #pragma unroll
     for (int u = 0; u < MAXU; u++) {
@@ -778,59 +819,266 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
       if (qi < nq) {
         const int i = qi / G, h = g * G + (qi % G);
         const float inv = 1.0f / s_l[qi];
-        float* out = B.ao + (size_t)(gr.brow0 + i) * C.qdim + h * dh + 2 * dp;
+        float* out = B.ao + (size_t)(gr.brow0 + i) * C.qdim + h * DH + 2 * dp;
         out[0] = o0[u] * inv;
         out[1] = o1[u] * inv;
       }
     }
     return;
   }
+  constexpr int RS = MAXQ * (DH + 2);  // partial record: o[MAXQ][DH], m[MAXQ], l[MAXQ]
+  const int cidx = blockIdx.z * C.hkv + g;
   float* rec = B.part + ((size_t)cidx * C.max_splits + split) * RS;
 #pragma unroll
   for (int u = 0; u < MAXU; u++) {
     const int qi = qg + u * NG;
     if (qi < nq) {
-      rec[qi * dh + 2 * dp] = o0[u];
-      rec[qi * dh + 2 * dp + 1] = o1[u];
+      rec[qi * DH + 2 * dp] = o0[u];
+      rec[qi * DH + 2 * dp + 1] = o1[u];
     }
   }
   for (int qi = tid; qi < nq; qi += kWG) {
-    rec[MAXQ * dh + qi] = s_m[qi];
-    rec[MAXQ * dh + MAXQ + qi] = s_l[qi];
+    rec[MAXQ * DH + qi] = s_m[qi];
+    rec[MAXQ * DH + MAXQ + qi] = s_l[qi];
   }
-  __threadfence();  // each thread publishes its own partial writes at device scope
+}
+
+// Device-coherent scalar accesses for data handed between workgroups of one launch: agent-scope
+// atomic stores and loads are issued with device scope (written through to, and read from, the
+// level every XCD shares), so no L2 writeback fence is needed; a producer waits for its own
+// stores (s_waitcnt) before it signals.
+__device__ __forceinline__ void st_dev(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_dev(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void wait_own_stores() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// Decode attention of the stage launches: one query row per stage, G query heads per KV head.
+// Grid: x = split (chunk keys), y = KV head, z = stage. Each 64-key pass issues its K loads
+// (registers) and V loads (LDS tile) together; the last split to finish of each (stage, KV head)
+// merges the partial (o, m, l) records in split order and writes the output.
+template <typename KVT, int DH>
+__global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
+  constexpr int PASS = 64, TPK = 4, NE = DH / TPK, VE = Elt<KVT>::VE;
+  constexpr int MAXQ = 8;
+  __shared__ float qs[MAXQ * DH];
+  __shared__ float sc[MAXQ * PASS];
+  __shared__ __align__(16) KVT vs[PASS * DH];
+  __shared__ float s_m[MAXQ], s_l[MAXQ], s_al[MAXQ];
+  __shared__ int s_last;
+  const Grp gr = resolve(C, R, blockIdx.z);
+  if (!gr.active) return;
+  const int g = blockIdx.y, split = blockIdx.x;
+  const int G = C.G;
+  const int nkeys = gr.pos0 + 1;
+  const int nsplit = (nkeys + C.chunk - 1) / C.chunk;
+  if (split >= nsplit) return;
+  const int k0 = split * C.chunk, k1 = min(nkeys, k0 + C.chunk);
+  const LayerDesc& Ld = C.lay[gr.layer];
+  const KVT* kvb = (const KVT*)Ld.kv;
+  const size_t voff = (size_t)C.hkv * C.page * DH;
+  const BufSet& B = C.b[R.set];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  for (int e = tid; e < G * DH; e += kWG) {
+    const int qi = e / DH, dd = e % DH;
+    qs[qi * DH + dd] = B.q[(size_t)gr.brow0 * C.qdim + (g * G + qi) * DH + dd] * C.scale;
+  }
+  if (tid < MAXQ) {
+    s_m[tid] = -INFINITY;
+    s_l[tid] = 0.f;
+  }
+  constexpr int npair = DH >> 1;
+  constexpr int NG = kWG / npair;
+  constexpr int MAXU = (MAXQ + NG - 1) / NG;
+  const int dp = tid % npair, qg = tid / npair;
+  float o0[MAXU], o1[MAXU];
+#pragma unroll
+  for (int u = 0; u < MAXU; u++) o0[u] = o1[u] = 0.f;
+  constexpr int VCH = DH * (int)sizeof(KVT) / 16;  // 16-byte chunks per V row
+  constexpr int VPT = PASS * VCH / kWG;              // V chunks per thread per pass
+  for (int kp = k0; kp < k1; kp += PASS) {
+    const int nk = min(PASS, k1 - kp);
+    const int kk = tid / TPK, qq = tid % TPK;
+    // issue this pass's K (registers) and V (LDS) loads together
+    // loads are unconditional (rows past the chunk end re-read its last key) so that they stay in
+    // registers; only valid keys are used
+    uint4 kraw[NE / VE];
+    {
+      const uint4* k4 = reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + min(kk, nk - 1), g, qq * NE));
+#pragma unroll
+      for (int c4 = 0; c4 < NE / VE; c4++) kraw[c4] = ldg16(k4 + c4);
+    }
+    uint4 vraw[VPT];
+#pragma unroll
+    for (int i = 0; i < VPT; i++) {
+      const int e = tid + i * kWG, vk = e / VCH, ch = e % VCH;
+      vraw[i] = ldg16(reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + min(vk, nk - 1), g, 0) + voff) + ch);
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; i++) {  // rows past the chunk end hold copies and are never read
+      const int e = tid + i * kWG, vk = e / VCH, ch = e % VCH;
+      reinterpret_cast<uint4*>(vs + vk * DH)[ch] = vraw[i];
+    }
+    __syncthreads();  // q staged (first pass), V tile written
+    float kr[NE];
+#pragma unroll
+    for (int c4 = 0; c4 < NE / VE; c4++) unpack16<KVT>(kraw[c4], kr + c4 * VE);
+    for (int qi = 0; qi < G; qi++) {
+      float dsum = 0.f;
+      const float* qv = qs + qi * DH + qq * NE;
+#pragma unroll
+      for (int e = 0; e < NE; e += 4) {
+        const float4 q4 = *reinterpret_cast<const float4*>(qv + e);
+        dsum = fmaf(q4.x, kr[e], dsum);
+        dsum = fmaf(q4.y, kr[e + 1], dsum);
+        dsum = fmaf(q4.z, kr[e + 2], dsum);
+        dsum = fmaf(q4.w, kr[e + 3], dsum);
+      }
+      dsum += __shfl_xor(dsum, 1, 64);
+      dsum += __shfl_xor(dsum, 2, 64);
+      if (qq == 0 && kk < nk) sc[qi * PASS + kk] = dsum;
+    }
+    __syncthreads();
+    for (int qi = w; qi < G; qi += 4) {
+      const float sv = lane < nk ? sc[qi * PASS + lane] : -INFINITY;
+      const float mx = wave_max(sv);
+      const float mo = s_m[qi];
+      const float mn = fmaxf(mo, mx);
+      const float p = lane < nk ? expf(sv - mn) : 0.f;
+      if (lane < nk) sc[qi * PASS + lane] = p;
+      const float ps = wave_sum(p);
+      if (lane == 0) {
+        const float al = (mo == -INFINITY) ? 0.f : expf(mo - mn);
+        s_al[qi] = al;
+        s_l[qi] = s_l[qi] * al + ps;
+        s_m[qi] = mn;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < MAXU; u++) {
+      const int qi = qg + u * NG;
+      if (qi < G) {
+        const float al = s_al[qi];
+        o0[u] *= al;
+        o1[u] *= al;
+      }
+    }
+    for (int k2 = 0; k2 < nk; k2++) {
+      const float v0 = ld1<KVT>(vs, (size_t)k2 * DH + 2 * dp);
+      const float v1 = ld1<KVT>(vs, (size_t)k2 * DH + 2 * dp + 1);
+#pragma unroll
+      for (int u = 0; u < MAXU; u++) {
+        const int qi = qg + u * NG;
+        if (qi < G) {
+          const float p = sc[qi * PASS + k2];
+          o0[u] = fmaf(p, v0, o0[u]);
+          o1[u] = fmaf(p, v1, o1[u]);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  float* out = B.ao + (size_t)gr.brow0 * C.qdim + g * G * DH;
+  if (nsplit == 1) {
+#pragma unroll
+    for (int u = 0; u < MAXU; u++) {
+      const int qi = qg + u * NG;
+      if (qi < G) {
+        const float inv = 1.0f / s_l[qi];
+        out[qi * DH + 2 * dp] = o0[u] * inv;
+        out[qi * DH + 2 * dp + 1] = o1[u] * inv;
+      }
+    }
+    return;
+  }
+  constexpr int RS = MAXQ * (DH + 2);
+  const int cidx = blockIdx.z * C.hkv + g;
+  float* rec = B.part + ((size_t)cidx * C.max_splits + split) * RS;
+#pragma unroll
+  for (int u = 0; u < MAXU; u++) {
+    const int qi = qg + u * NG;
+    if (qi < G) {
+      st_dev(rec + qi * DH + 2 * dp, o0[u]);
+      st_dev(rec + qi * DH + 2 * dp + 1, o1[u]);
+    }
+  }
+  if (tid < G) {
+    st_dev(rec + MAXQ * DH + tid, s_m[tid]);
+    st_dev(rec + MAXQ * DH + MAXQ + tid, s_l[tid]);
+  }
+  wait_own_stores();
   __syncthreads();
   if (tid == 0) {
-    const int t = atomicAdd(&B.cnt[cidx], 1);
+    const int t = __hip_atomic_fetch_add(&cnt[cidx], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     s_last = (t == nsplit - 1);
   }
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
   const float* base = B.part + (size_t)cidx * C.max_splits * RS;
 #pragma unroll
   for (int u = 0; u < MAXU; u++) {
     const int qi = qg + u * NG;
-    if (qi < nq) {
+    if (qi < G) {
       float M = -INFINITY;
-      for (int s = 0; s < nsplit; s++) M = fmaxf(M, base[(size_t)s * RS + MAXQ * dh + qi]);
+      for (int sp = 0; sp < nsplit; sp++) M = fmaxf(M, ld_dev(base + (size_t)sp * RS + MAXQ * DH + qi));
       float Ls = 0.f, A0 = 0.f, A1 = 0.f;
-      for (int s = 0; s < nsplit; s++) {
-        const float* r = base + (size_t)s * RS;
-        const float ms = r[MAXQ * dh + qi];
-        const float f = (ms == -INFINITY) ? 0.f : expf(ms - M);
-        Ls = fmaf(r[MAXQ * dh + MAXQ + qi], f, Ls);
-        A0 = fmaf(r[qi * dh + 2 * dp], f, A0);
-        A1 = fmaf(r[qi * dh + 2 * dp + 1], f, A1);
+      for (int sp = 0; sp < nsplit; sp++) {
+        const float* r = base + (size_t)sp * RS;
+        const float f = expf(ld_dev(r + MAXQ * DH + qi) - M);  // every split has >= 1 key
+        Ls = fmaf(ld_dev(r + MAXQ * DH + MAXQ + qi), f, Ls);
+        A0 = fmaf(ld_dev(r + qi * DH + 2 * dp), f, A0);
+        A1 = fmaf(ld_dev(r + qi * DH + 2 * dp + 1), f, A1);
       }
-      const int i = qi / G, h = g * G + (qi % G);
       const float inv = 1.0f / Ls;
-      float* out = B.ao + (size_t)(gr.brow0 + i) * C.qdim + h * dh + 2 * dp;
-      out[0] = A0 * inv;
-      out[1] = A1 * inv;
+      out[qi * DH + 2 * dp] = A0 * inv;
+      out[qi * DH + 2 * dp + 1] = A1 * inv;
     }
   }
-  if (tid == 0) atomicExch(&B.cnt[cidx], 0);
+  if (tid == 0) __hip_atomic_store(&cnt[cidx], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Merge the splits of each (group, KV head) in split order. Grid: x = KV head, y = group.
+template <int MAXQ, int DH>
+__global__ __launch_bounds__(kWG) void k_attn_combine(Ctx C, Rows R) {
+  const Grp gr = resolve(C, R, blockIdx.y);
+  if (!gr.active) return;
+  const int g = blockIdx.x;
+  const int nkeys = gr.pos0 + gr.nrows;
+  const int nsplit = (nkeys + C.chunk - 1) / C.chunk;
+  if (nsplit == 1) return;  // the attention kernel wrote the output itself
+  const int G = C.G, nq = gr.nrows * G;
+  constexpr int RS = MAXQ * (DH + 2);
+  constexpr int npair = DH >> 1;
+  constexpr int NG = kWG / npair;
+  const int tid = threadIdx.x, dp = tid % npair, qg = tid / npair;
+  const BufSet& B = C.b[R.set];
+  const int cidx = blockIdx.y * C.hkv + g;
+  const float* base = B.part + (size_t)cidx * C.max_splits * RS;
+  for (int qi = qg; qi < nq; qi += NG) {
+    float M = -INFINITY;
+    for (int sp = 0; sp < nsplit; sp++) M = fmaxf(M, base[(size_t)sp * RS + MAXQ * DH + qi]);
+    float Ls = 0.f, A0 = 0.f, A1 = 0.f;
+    for (int sp = 0; sp < nsplit; sp++) {
+      const float* r = base + (size_t)sp * RS;
+      const float ms = r[MAXQ * DH + qi];
+      const float f = (ms == -INFINITY) ? 0.f : expf(ms - M);
+      Ls = fmaf(r[MAXQ * DH + MAXQ + qi], f, Ls);
+      A0 = fmaf(r[qi * DH + 2 * dp], f, A0);
+      A1 = fmaf(r[qi * DH + 2 * dp + 1], f, A1);
+    }
+    const int i = qi / G, h = g * G + (qi % G);
+    const float inv = 1.0f / Ls;
+    float* out = B.ao + (size_t)(gr.brow0 + i) * C.qdim + h * DH + 2 * dp;
+    out[0] = A0 * inv;
+    out[1] = A1 * inv;
+  }
 }
 
 // ------------------------------------------------------------------------- embedding / state
@@ -858,9 +1106,14 @@ template <typename WT>
 __global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int auto_rb) {
   __shared__ int s_tok, s_pos;
   DevState* st = C.st;
+  const int tiles = (C.V + 4 * kHeadRowsPerWave - 1) / (4 * kHeadRowsPerWave);
+  const int y_all = (st->a == C.n) ? reduce_head(C.b[0], tiles, C.V) : -1;
+  const int pd_all = reduce_head(C.b[1], tiles, C.V);
   if (threadIdx.x == 0) {
     const int c = st->c, a = st->a, n = C.n;
-    const int pd = st->pdm_draft;
+    const int pd = pd_all;
+    st->pdm_draft = pd;
+    st->y = y_all;
     const int dpos = c + a;
     int fd = forced_override;
     if (fd < 0 && dpos < C.max_tokens) fd = C.forced[dpos];
@@ -875,7 +1128,7 @@ __global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int 
     r.verified_token = -1;
     int ptok = -1, ppos = -1;
     if (a == n) {
-      const int y = st->y;
+      const int y = y_all;
       const int succ = n >= 2 ? C.tok[c + 1] : draft;
       r.target_argmax = y;
       r.exited_pos = c;
@@ -927,8 +1180,10 @@ template <typename WT>
 __global__ __launch_bounds__(kWG) void k_reseed(Ctx C, int keep, int tok, int prompt_len) {
   __shared__ int s_tok;
   DevState* st = C.st;
+  const int yv = tok >= 0 ? tok : reduce_head(C.b[0], (C.V + 4 * kHeadRowsPerWave - 1) / (4 * kHeadRowsPerWave), C.V);
   if (threadIdx.x == 0) {
-    const int t = tok >= 0 ? tok : st->y;
+    const int t = yv;
+    if (tok < 0) st->y = t;
     st->c = keep;
     st->a = 1;
     st->pending = 0;
@@ -991,20 +1246,28 @@ void Launch<WT>::gateup(const Ctx& c, const Rows& r, void* s) {
     hipLaunchKernelGGL((k_gateup<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
 }
 
+template <typename WT, int MAXQ, int DH>
+static void attn_launch(const Ctx& c, const Rows& r, void* s) {
+  const dim3 grid(c.max_splits, c.hkv, r.kind == 0 ? c.n : 1);
+  hipLaunchKernelGGL((k_attn<WT, MAXQ, DH>), grid, dim3(kWG), (attn_lds<WT, MAXQ, DH>()), S(s), c, r);
+  const dim3 cgrid(c.hkv, r.kind == 0 ? c.n : 1);
+  hipLaunchKernelGGL((k_attn_combine<MAXQ, DH>), cgrid, dim3(kWG), 0, S(s), c, r);
+}
+
 template <typename WT>
 void Launch<WT>::attn(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid(c.max_splits, c.hkv, r.kind == 0 ? c.n : 1);
-  if (c.dh == 128) {
-    if (r.kind == 0)
-      hipLaunchKernelGGL((k_attn<WT, 8, 128>), grid, dim3(kWG), 0, S(s), c, r);
+  if (r.kind == 0) {
+    const dim3 grid(c.max_splits, c.hkv, c.n);
+    if (c.dh == 128)
+      hipLaunchKernelGGL((k_attn_dec<WT, 128>), grid, dim3(kWG), 0, S(s), c, r, c.b[r.set].cnt);
     else
-      hipLaunchKernelGGL((k_attn<WT, 64, 128>), grid, dim3(kWG), 0, S(s), c, r);
-  } else {
-    if (r.kind == 0)
-      hipLaunchKernelGGL((k_attn<WT, 8, 64>), grid, dim3(kWG), 0, S(s), c, r);
-    else
-      hipLaunchKernelGGL((k_attn<WT, 64, 64>), grid, dim3(kWG), 0, S(s), c, r);
+      hipLaunchKernelGGL((k_attn_dec<WT, 64>), grid, dim3(kWG), 0, S(s), c, r, c.b[r.set].cnt);
+    return;
   }
+  if (c.dh == 128)
+    attn_launch<WT, 64, 128>(c, r, s);
+  else
+    attn_launch<WT, 64, 64>(c, r, s);
 }
 
 template <typename WT>
@@ -1015,7 +1278,7 @@ void Launch<WT>::pdm_fc(const Ctx& c, int prefill, int nrows, void* s) {
 
 template <typename WT>
 void Launch<WT>::head(const Ctx& c, int src, int row, void* s) {
-  const dim3 grid((c.V + 15) / 16);
+  const dim3 grid((c.V + 4 * kHeadRowsPerWave - 1) / (4 * kHeadRowsPerWave));
   hipLaunchKernelGGL((k_head<WT>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, src, row, src == 1 ? 1 : 0);
 }
 

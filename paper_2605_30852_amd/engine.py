@@ -151,6 +151,9 @@ class Engine:
     def spd_sync(self):
         return B.spd_sync(self.h)
 
+    def spd_set_graph(self, on: bool) -> None:
+        B.spd_set_graph(self.h, on)
+
     def spd_set_debug(self, on: bool) -> None:
         B.spd_set_debug(self.h, on)
 

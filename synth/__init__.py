@@ -100,7 +100,7 @@ B9 = ModelShape("9b", 36, 4096, 32, 8, 128, 12288, 151936, "bf16", n_stages=4, p
 B9_LONG = B9.with_(name="9b-long", n_stages=8, pdm_layers=2)
 # A mid-size bf16 model for parity: several GEMV/attention tiles per launch and ragged tails
 # (ffn 1000 and vocab 3001 are not multiples of any tile height).
-MID = ModelShape("mid", 6, 384, 6, 2, 64, 1000, 3001, "bf16", n_stages=3, pdm_layers=1)
+MID = ModelShape("mid", 6, 384, 8, 2, 64, 1000, 3001, "bf16", n_stages=3, pdm_layers=1)
 
 WORKLOADS = {
     "tiny": dict(shape=TINY, prompt_len=64, steps=32, p_accept=None),
