@@ -46,8 +46,37 @@ def step_bytes(sh, n, ls, c, esz, pdm_head=True):
     return target, pdm
 
 
-def cpu_baseline(sh, n, ctx, seed):
-    """Time the float64 CPU oracle on a bounded sample of the same step and scale it to a step."""
+def layer_bytes(sh, esz):
+    d, F, qd, kvd = sh.d_model, sh.ffn_dim, sh.q_dim, sh.kv_dim
+    return (qd * d + 2 * kvd * d + d * qd + 3 * F * d) * esz + 2 * d * 4
+
+
+def launch_bytes(sh, n, c, esz):
+    """Algorithmic bytes of one steady-state launch of each stage-batched kernel class (all n stages
+    active), starting the step with c committed positions: weights once, activations in and out."""
+    d, F, qd, kvd, V = sh.d_model, sh.ffn_dim, sh.q_dim, sh.kv_dim, sh.vocab
+    L = sh.n_layers
+    beta = [s * L // n for s in range(n + 1)]
+    # attention of slot 0 (every stage has a layer in slot 0): stage s reads c + n - s keys
+    attn = sum((c + n - s) * 2 * kvd * esz + qd * 4 * 2 for s in range(n))
+    return {
+        "qkv": n * ((qd + 2 * kvd) * d * esz + 2 * d * 4 + qd * 4 + 2 * kvd * esz),
+        "attn": attn,
+        "oproj": n * (d * qd * esz + qd * 4 + 2 * d * 4),
+        "gateup": n * (2 * F * d * esz + 2 * d * 4 + F * 4),
+        "down": n * (d * F * esz + F * 4 + 2 * d * 4),
+        "head": V * d * esz + 2 * d * 4,
+        "_beta": beta,
+    }
+
+
+def cpu_baseline(sh, n, ctx, seed, budget_s=12.0):
+    """Time the float64 CPU oracle on a bounded sample of the same step and scale it to one step.
+
+    The sample: oracle.model.decoder_layer on one layer of the workload at context ctx (a stage layer
+    and a PDM layer cost the same), oracle.model.lm_logits over the full vocabulary, and the PDM
+    feature projection SPDOracle.feature on n anchors. A full-pipeline oracle step runs L target
+    layers, n rows through each PDM layer, n feature projections and two LM heads."""
     import numpy as np
     from threadpoolctl import threadpool_info
     from oracle import model as om
@@ -61,40 +90,42 @@ def cpu_baseline(sh, n, ctx, seed):
     cache.n = ctx
     lw = model.layer(0)
     h = rng.standard_normal(sh.d_model)
-    reps = 4
-    om.decoder_layer(sh, lw, h, ctx, cache)  # warm
-    cache.truncate(ctx)
-    t0 = time.perf_counter()
-    for _ in range(reps):
+
+    def timed(fn, share):
+        fn()  # warm (draws the weights)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            fn()
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= share * budget_s or reps >= 200:
+                return el / reps, reps
+
+    def one_layer():
         om.decoder_layer(sh, lw, h, ctx, cache)
         cache.truncate(ctx)
-    t_layer = (time.perf_counter() - t0) / reps
-    model.w("lm_head")
-    t0 = time.perf_counter()
-    for _ in range(2):
-        om.lm_logits(model, h)
-    t_head = (time.perf_counter() - t0) / 2
+
+    t_layer, r_layer = timed(one_layer, 0.5)
+    t_head, r_head = timed(lambda: om.lm_logits(model, h), 0.3)
     o = osp.SPDOracle.__new__(osp.SPDOracle)
     o.m, o.sh, o.n, o.L = model, sh, n, sh.n_layers
     o.anchor_layers = osp.stage_bounds(sh.n_layers, n)[:n]
     anchors = [rng.standard_normal(sh.d_model) for _ in range(n)]
-    o.feature(anchors, n)  # draws W_in
-    t0 = time.perf_counter()
-    for _ in range(2):
-        o.feature(anchors, n)
-    t_fc = (time.perf_counter() - t0) / 2
-    step = sh.n_layers * t_layer + sh.pdm_layers * n * t_layer / n + t_fc + 2 * t_head
+    t_fc, r_fc = timed(lambda: o.feature(anchors, n), 0.2)
+    step = (sh.n_layers + n * sh.pdm_layers) * t_layer + n * t_fc + 2 * t_head
     threads = 0
     for info in threadpool_info():
         if info.get("user_api") == "blas":
             threads = max(threads, int(info.get("num_threads", 0)))
     return {
-        "value": 1e6 * step, "unit": "us/step", "cores": threads or len(os.sched_getaffinity(0)),
+        "value": round(1e6 * step, 1), "unit": "us/step", "cores": threads or len(os.sched_getaffinity(0)),
         "kind": "oracle",
-        "sample": (f"float64 oracle: decoder_layer on one {sh.name} layer at context {ctx} x{reps}, "
-                   f"LM head x2, PDM feature projection x2; scaled to {sh.n_layers} target layers + "
-                   f"{sh.pdm_layers} PDM layer + projection + 2 LM heads per step"),
-        "per_layer_s": t_layer, "head_s": t_head,
+        "sample": (f"float64 oracle on the host: decoder_layer of one {sh.name} layer at context {ctx} "
+                   f"x{r_layer}, lm_logits over {sh.vocab} tokens x{r_head}, PDM feature projection "
+                   f"({n}*{sh.d_model} -> {sh.d_model}) x{r_fc}; scaled to one full-pipeline step = "
+                   f"{sh.n_layers} target layers + {n} rows x {sh.pdm_layers} PDM layer(s) + {n} "
+                   f"projections + 2 LM heads"),
+        "per_layer_s": round(t_layer, 5), "head_s": round(t_head, 5), "fc_s": round(t_fc, 5),
     }
 
 
@@ -108,8 +139,9 @@ def main():
     ap.add_argument("--prompt", type=int, default=None)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-ar", action="store_true", help="skip the plain greedy tokens/s line")
     ap.add_argument("--no-graph", action="store_true", help="issue every launch instead of replaying the step graph")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device copy (the known-size kernel for HBM counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the SPD step here is the single-GPU stage-batched "
@@ -130,7 +162,22 @@ def main():
     P = args.prompt or wl["prompt_len"]
     K, W = args.steps, args.warmup
     esz = 2 if sh.dtype == "bf16" else 4
-    max_tokens = P + W + 2 * K + 4 * n + 64
+    K_GU, K_CLS, K_SPAN = 64, 16, 64
+    # greedy reference long enough for every forced-accept phase below
+    n_ref = W + K + K_GU + 5 * K_CLS + K_SPAN + 2 * n + 16
+    # capacity and attention split size depend on the workload only (not on --steps), so that a
+    # profiled run with fewer steps launches exactly the kernels the timed run launches
+    max_tokens = P + max(1024, n_ref + 4 * n + 64)
+    attn_chunk = max(64, (P // 16 + 63) // 64 * 64)
+
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] copy calibration: 3 x 1 GiB device copies")
+        del src, dst
 
     t0 = time.time()
     log(f"[bench] generating and uploading {sh.name} weights ({sh.param_bytes() / 1e9:.2f} GB)")
@@ -141,11 +188,10 @@ def main():
 
     # plain greedy decoding (n = 1 through the same library): reference tokens and AR tokens/s
     t0 = time.time()
-    ar = Engine(weights, max_tokens=max_tokens, n=1)
+    ar = Engine(weights, max_tokens=max_tokens, n=1, attn_chunk=attn_chunk)
     ar.spd_set_graph(not args.no_graph)
     first = ar.spd_prefill(prompt)
     log(f"[bench] AR prefill {P} tokens in {time.time() - t0:.1f}s")
-    n_ref = W + 2 * K + 2 * n + 8
     torch.cuda.synchronize()
     ta = time.perf_counter()
     ar.spd_run_steps(n_ref)
@@ -158,10 +204,12 @@ def main():
     log(f"[bench] AR: {n_ref} tokens, {1e6 * ar_s / n_ref:.1f} us/token")
 
     # SPD handle, all drafts forced to the greedy tokens: every step after the fill is a full step
-    eng = Engine(weights, max_tokens=max_tokens, n=n)
+    t0 = time.time()
+    eng = Engine(weights, max_tokens=max_tokens, n=n, attn_chunk=attn_chunk)
     eng.spd_set_graph(not args.no_graph)
     f2 = eng.spd_prefill(prompt)
     assert f2 == first
+    log(f"[bench] SPD prefill {P} tokens in {time.time() - t0:.1f}s")
     eng.spd_set_forced_drafts(ref.astype(np.int32), P)
     eng.spd_run_steps(W)
     c0, a0, _, _ = eng.state()
@@ -169,7 +217,7 @@ def main():
     torch.cuda.synchronize()
     ts = time.perf_counter()
     eng.spd_run_steps(K)
-    last = eng.spd_sync()
+    eng.spd_sync()
     torch.cuda.synchronize()
     el = time.perf_counter() - ts
     c1, a1, _, _ = eng.state()
@@ -177,35 +225,49 @@ def main():
     toks = eng.tokens()[P: c1 + 1]
     assert np.array_equal(toks, ref[: len(toks)]), "SPD stream differs from greedy decoding"
     us_step = 1e6 * el / K
-    tgt_b, pdm_b = step_bytes(sh, n, sh.pdm_layers, (c0 + c1) // 2, esz)
+    c_mid = (c0 + c1) // 2
+    tgt_b, pdm_b = step_bytes(sh, n, sh.pdm_layers, c_mid, esz)
     bytes_step = tgt_b + pdm_b
     gbs = bytes_step / (us_step * 1e-6) / 1e9
-    log(f"[bench] SPD n={n}: {us_step:.1f} us/step, {bytes_step / 1e9:.3f} GB/step, {gbs:.0f} GB/s")
+    log(f"[bench] SPD n={n}: {us_step:.1f} us/step, {bytes_step / 1e9:.3f} GB/step, {gbs:.0f} GB/s "
+        f"({100 * gbs / PEAK_HBM_GBS:.1f}% of {PEAK_HBM_GBS:.0f})")
 
-    # dominant kernel: grouped gate/up + SwiGLU over the n stages, HIP events on the main stream
-    B.spd_set_kernel_timing(eng.h, B.SPD_K_GATEUP)
-    Kt = min(K, 64)
-    eng.spd_run_steps(Kt)
-    eng.spd_sync()
-    ms, launches = B.spd_kernel_timing(eng.h)
-    B.spd_set_kernel_timing(eng.h, 0)
-    gu_bytes = n * (2 * sh.ffn_dim * sh.d_model * esz + sh.d_model * 4 + sh.ffn_dim * 4)
-    gu_s = ms * 1e-3 / max(1, launches)
-    gu_gbs = gu_bytes / gu_s / 1e9
-    # all kernels' share for the log
-    shares = {}
-    for kname, kid in (("qkv", B.SPD_K_QKV), ("attn", B.SPD_K_ATTN), ("oproj", B.SPD_K_OPROJ),
-                       ("down", B.SPD_K_DOWN), ("head", B.SPD_K_HEAD)):
+    # per-kernel HIP-event timing on the main stream, steady state (every step accepts)
+    def time_class(kid, steps):
         B.spd_set_kernel_timing(eng.h, kid)
-        eng.spd_run_steps(8)
+        ca, _, _, _ = eng.state()
+        eng.spd_run_steps(steps)
         eng.spd_sync()
-        kms, kl = B.spd_kernel_timing(eng.h)
-        shares[kname] = {"us_per_launch": 1e3 * kms / max(1, kl), "launches_per_step": kl / 8}
-    B.spd_set_kernel_timing(eng.h, 0)
-    shares["gateup"] = {"us_per_launch": 1e6 * gu_s, "launches_per_step": launches / Kt}
-    log(f"[bench] gate/up: {1e6 * gu_s:.1f} us/launch, {gu_gbs:.0f} GB/s; kernels {shares}")
+        ms, nl = B.spd_kernel_timing(eng.h)
+        B.spd_set_kernel_timing(eng.h, 0)
+        cb, ab, _, _ = eng.state()
+        assert cb - ca == steps and ab == n, "kernel timing left the steady state"
+        return ms, nl, (ca + cb) // 2
 
-    # tokens/s at a seeded Bernoulli(0.7) acceptance pattern (rollback, refill exercised)
+    kernels = {}
+    classes = (("qkv", B.SPD_K_QKV), ("attn", B.SPD_K_ATTN), ("oproj", B.SPD_K_OPROJ),
+               ("gateup", B.SPD_K_GATEUP), ("down", B.SPD_K_DOWN), ("head", B.SPD_K_HEAD))
+    for kname, kid in classes:
+        steps = K_GU if kname == "gateup" else K_CLS
+        ms, nl, cm = time_class(kid, steps)
+        lb = launch_bytes(sh, n, cm, esz)[kname]
+        us = 1e3 * ms / max(1, nl)
+        kernels[kname] = {"us_per_launch": round(us, 2), "launches_per_step": nl / steps,
+                          "bytes_per_launch": int(lb), "GBps": round(lb / (us * 1e-6) / 1e9, 1)}
+    log(f"[bench] kernels: {kernels}")
+    gu = kernels["gateup"]
+
+    # PDM overlap: step start -> end of the stage compute (main) and -> end of the PDM (side stream)
+    B.spd_set_kernel_timing(eng.h, B.SPD_K_SPANS)
+    eng.spd_run_steps(K_SPAN)
+    st_ms, pd_ms, late_ms, ns = B.spd_span_timing(eng.h)
+    B.spd_set_kernel_timing(eng.h, 0)
+    spans = {"stage_us": round(1e3 * st_ms / ns, 1), "pdm_us": round(1e3 * pd_ms / ns, 1),
+             "verify_wait_us": round(1e3 * late_ms / ns, 2), "steps": ns,
+             "pdm_hidden": late_ms == 0.0}
+    log(f"[bench] spans: {spans}")
+
+    # tokens/s at a seeded Bernoulli acceptance pattern (rollback and refill exercised)
     p = wl.get("p_accept") or 0.7
     eng.spd_rollback(P, int(first))
     mask = synth.accept_mask(p, args.seed, max_tokens)
@@ -215,18 +277,22 @@ def main():
         table[i] = ref[i] if mask[q] else (ref[i] + 1) % sh.vocab
     eng.spd_clear_forced_drafts()
     eng.spd_set_forced_drafts(table, P)
-    Kp = K
     torch.cuda.synchronize()
     ts = time.perf_counter()
-    logp = eng.spd_run_steps(Kp, want_log=True)
+    logp = eng.spd_run_steps(K, want_log=True)
     elp = time.perf_counter() - ts
     committed = logp[-1]["committed_len"] - P
     spd_tok_s = committed / elp
-    alpha = committed / Kp
+    alpha = committed / K
     toks = eng.tokens()[P: logp[-1]["committed_len"] + 1]
     assert np.array_equal(toks, ref[: len(toks)]), "SPD stream differs from greedy decoding (p run)"
+    for r in logp:
+        if r["decision"] != B.SPD_NONE:
+            assert r["decision"] == (B.SPD_ACCEPT if mask[r["verified_pos"]] else B.SPD_REJECT)
     log(f"[bench] p={p}: alpha={alpha:.3f}, {spd_tok_s:.0f} tok/s (AR {ar_tok_s:.0f} tok/s)")
     eng.close()
+    del weights
+    torch.cuda.empty_cache()
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -246,25 +312,47 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": sh.dtype,
-        "data": "synthetic (seeded N(0,0.02) weights, uniform-random prompt)",
-        "graph": not args.no_graph,
-        "config": {"workload": f"{sh.name}-class dense decoder, SPD width n={n}, PDM {sh.pdm_layers} layer, "
-                               f"{P}-token prompt, steady-state full-pipeline steps",
-                   "n": n, "layers": sh.n_layers, "d_model": sh.d_model, "prompt": P,
-                   "pdm_layers": sh.pdm_layers, "global_batch": 1, "seq_len": P, "parallelism": "none"},
+        "data": "synthetic (seeded N(0,0.02) weights, uniform-random prompt, drafts forced to greedy tokens)",
+        "config": {"workload": f"{sh.name}-class dense decoder ({sh.n_layers} layers, d {sh.d_model}, "
+                               f"{sh.n_q_heads}/{sh.n_kv_heads} heads of {sh.head_dim}, FFN {sh.ffn_dim}, "
+                               f"vocab {sh.vocab}), SPD width n={n}, {sh.pdm_layers}-layer PDM, "
+                               f"{P}-token prompt, batch 1, steady-state full-pipeline steps",
+                   "n": n, "prompt": P, "pdm_layers": sh.pdm_layers, "batch": 1,
+                   "max_tokens": max_tokens, "attn_chunk": attn_chunk,
+                   "step_graph": not args.no_graph},
         "bytes_per_step": int(bytes_step),
         "step_GBps": round(gbs, 1),
         "step_roofline_frac": round(gbs / PEAK_HBM_GBS, 4),
-        "roofline": {"bound": "hbm", "achieved": round(gu_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(gu_gbs / PEAK_HBM_GBS, 4), "traffic": None,
-                     "kernel": "k_gateup (grouped gate/up GEMV + SwiGLU over n stages)",
-                     "bytes_per_launch": gu_bytes, "us_per_launch": round(1e6 * gu_s, 2)},
-        "kernels": shares,
+        "roofline": {"bound": "hbm", "achieved": gu["GBps"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gu["GBps"] / PEAK_HBM_GBS, 4), "traffic": traffic_from_profile(),
+                     "kernel": "k_gateup<bf16,1>: grouped gate/up GEMV + SwiGLU over the n stages",
+                     "bytes_per_launch": gu["bytes_per_launch"], "us_per_launch": gu["us_per_launch"]},
+        "kernels": kernels,
+        "pdm_overlap": spans,
         "tokens_per_s": {"spd_forced_p": p, "alpha": round(alpha, 4), "spd": round(spd_tok_s, 1),
                          "ar_same_gpu": round(ar_tok_s, 1)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def traffic_from_profile():
+    """HBM bytes per launch of the dominant kernel from committed rocprofv3 counter runs, or None
+    when the counters were taken on other kernel sources than the ones built now."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "gateup_4b_n4_traffic.txt")
+    src = os.path.join(ROOT, "paper_2605_30852_amd", "csrc", "spd_kernels.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if kv.get("kernels_sha256") != digest or "hbm_bytes_per_launch" not in kv:
+        return None
+    return int(float(kv["hbm_bytes_per_launch"]))
 
 
 if __name__ == "__main__":

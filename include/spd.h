@@ -203,9 +203,19 @@ spd_status spd_set_debug(spd_handle* h, int32_t on);
  * off). While on, every launch of that class is bracketed by two HIP events on main_stream.
  * spd_kernel_timing waits for the stream, returns the summed event time in milliseconds and the
  * number of timed launches, and clears both. */
-enum { SPD_K_QKV = 1, SPD_K_ATTN = 2, SPD_K_OPROJ = 3, SPD_K_GATEUP = 4, SPD_K_DOWN = 5, SPD_K_HEAD = 6 };
+enum { SPD_K_QKV = 1, SPD_K_ATTN = 2, SPD_K_OPROJ = 3, SPD_K_GATEUP = 4, SPD_K_DOWN = 5, SPD_K_HEAD = 6,
+       SPD_K_SPANS = 7 };
 spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel);
 spd_status spd_kernel_timing(spd_handle* h, double* total_ms, int32_t* launches);
+
+/* Overlap of the draft module with the stage compute (Section 3.3: drafting must finish within the
+ * pipeline step). With spd_set_kernel_timing(h, SPD_K_SPANS) every step records three HIP events: the
+ * step's start on main_stream, the end of the PDM's work on pdm_stream, and the end of the stage
+ * compute plus exit LM head on main_stream (the point where verification waits for the draft).
+ * spd_span_timing waits for both streams and returns, summed over the timed steps: stage_ms (start to
+ * end of stage compute), pdm_ms (start to end of the PDM), late_ms (the sum of max(0, pdm end - stage
+ * end), i.e. time the verification waited for the draft), and the number of steps; then clears them. */
+spd_status spd_span_timing(spd_handle* h, double* stage_ms, double* pdm_ms, double* late_ms, int32_t* steps);
 
 /* Release the handle's events and host buffers (not the caller's memory). NULL is ignored. */
 void spd_destroy(spd_handle* h);

@@ -15,9 +15,11 @@ Pins (what ties each function to something other than itself) are in tests/test_
                                                 worked indices of Figure 1; closed forms for
                                                 special weights
   spd.simulate_steps                         -> exact step counts of the oracle under forced masks
+  spd.speedup_*                              -> Table 3's printed speedups (tests/golden/)
 Parity unpinned: the PDM's draft quality (it has random weights); only its definition is pinned.
 """
 from .model import (LayerCache, Model, ar_greedy, argmax_first, attend, decoder_layer, embed,
                     forward_full, lm_logits, rms_norm, rope, rope_angles, round_bf16, silu)
 from .spd import (ACCEPT, NONE, REJECT, SPDOracle, StepResult, eligible_anchors, l_max, run_spd,
-                  simulate_steps, stage_bounds)
+                  simulate_steps, speedup_serial_draft, speedup_zero_cost, stage_bounds,
+                  step_acceptance)

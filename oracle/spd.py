@@ -284,3 +284,22 @@ def simulate_steps(n: int, n_tokens: int, accept_at: Callable[[int], bool], prom
         q += 1
         verified += 1
     return t
+
+
+# ----------------------------------------------------------------------------- accounting (Sec. 4.2)
+def step_acceptance(n_tokens: int, n_steps: int) -> float:
+    """alpha = N / K: generated tokens per executed pipeline step."""
+    return n_tokens / n_steps
+
+
+def speedup_zero_cost(alpha: float, n: int) -> float:
+    """Eq. s0-spd: each step advances n stage tokens at 1/n of a full forward, so S0 = alpha * n."""
+    return alpha * n
+
+
+def speedup_serial_draft(s0: float, n_layers: int, draft_layers: int, draft_calls: int) -> float:
+    """Eq. s-eagle: when drafting is not hidden, every step also pays draft_calls passes of an
+    L_s-layer drafter, measured in target layers: S = S0 * L / (L_s * draft_calls + L). For PPSD and
+    the post-step ablation draft_calls = n; for EAGLE-3 it is the draft length k."""
+    return s0 * n_layers / (draft_layers * draft_calls + n_layers)
+

@@ -17,7 +17,7 @@ SPD_F32, SPD_BF16 = 0, 1
 SPD_NONE, SPD_ACCEPT, SPD_REJECT = 0, 1, 2
 SPD_DBG_RESID, SPD_DBG_ANCHORS, SPD_DBG_PDM_HIDDEN = 1, 2, 3
 SPD_DBG_EXIT_LOGITS, SPD_DBG_PDM_LOGITS, SPD_DBG_TOKENS, SPD_DBG_STATE = 4, 5, 6, 7
-SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD = 1, 2, 3, 4, 5, 6
+SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD, SPD_K_SPANS = 1, 2, 3, 4, 5, 6, 7
 
 
 class spd_config(ct.Structure):
@@ -57,7 +57,7 @@ EXPORTS = [
     "spd_workspace_size", "spd_stage_bounds", "spd_init", "spd_prefill", "spd_step", "spd_rollback",
     "spd_set_forced_drafts", "spd_clear_forced_drafts", "spd_run_steps", "spd_sync", "spd_read_debug",
     "spd_read_kv", "spd_set_debug", "spd_destroy", "spd_status_str", "spd_last_error",
-    "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph",
+    "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -96,6 +96,8 @@ def lib() -> ct.CDLL:
             "spd_set_kernel_timing": (I, [P, I]),
             "spd_set_graph": (I, [P, I]),
             "spd_kernel_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
+            "spd_span_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_double),
+                                    ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
             "spd_destroy": (None, [P]),
             "spd_status_str": (ct.c_char_p, [I]),
             "spd_last_error": (ct.c_char_p, [P]),
@@ -212,6 +214,14 @@ def spd_kernel_timing(h: int):
     n = ct.c_int32(0)
     _check("spd_kernel_timing", lib().spd_kernel_timing(h, ct.byref(ms), ct.byref(n)), h)
     return ms.value, n.value
+
+
+def spd_span_timing(h: int):
+    """(stage_ms, pdm_ms, late_ms, steps), sums over the steps timed with SPD_K_SPANS."""
+    st, pd, late = ct.c_double(0.0), ct.c_double(0.0), ct.c_double(0.0)
+    n = ct.c_int32(0)
+    _check("spd_span_timing", lib().spd_span_timing(h, ct.byref(st), ct.byref(pd), ct.byref(late), ct.byref(n)), h)
+    return st.value, pd.value, late.value, n.value
 
 
 def spd_set_graph(h: int, on: bool) -> None:

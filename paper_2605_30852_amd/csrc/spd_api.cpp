@@ -56,6 +56,8 @@ spd_status check_config(const spd_config* c, std::string* why) {
   if (c->max_tokens > (1 << 20)) return bad("max_tokens too large");
   if (c->attn_chunk < 0 || (c->attn_chunk && (c->attn_chunk % c->page_size)))
     return bad("attn_chunk must be 0 or a multiple of page_size");
+  if (c->attn_chunk && (c->max_tokens + c->attn_chunk - 1) / c->attn_chunk > kMaxSplits)
+    return bad("attn_chunk too small: max_tokens / attn_chunk must not exceed 64 key splits");
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return bad("rms_eps must be > 0 and rope_base > 1");
   if (c->auto_rollback != 0 && c->auto_rollback != 1) return bad("auto_rollback must be 0 or 1");
   return SPD_OK;
@@ -68,11 +70,11 @@ Layout make_layout(const spd_config& c) {
   const int qdim = c.n_q_heads * dh;
   const int G = c.n_q_heads / hkv;
   L.num_pages = (c.max_tokens + c.page_size - 1) / c.page_size;
-  // about 40 splits at full capacity, 64..2048 keys each: enough workgroups for the short
-  // contexts, few partials for the long ones
+  // about 40 key splits at full capacity, at least 64 keys each: enough workgroups for the short
+  // contexts, few partials for the long ones (never more than kMaxSplits)
   {
-    int ch = (c.max_tokens / 40 + 63) / 64 * 64;
-    L.chunk = c.attn_chunk ? c.attn_chunk : std::min(2048, std::max(64, ch));
+    const int ch = ((c.max_tokens + 39) / 40 + 63) / 64 * 64;
+    L.chunk = c.attn_chunk ? c.attn_chunk : std::max(64, ch);
   }
   L.max_splits = (c.max_tokens + L.chunk - 1) / L.chunk;
   L.head_tiles = (c.vocab + 63) / 64;
@@ -143,6 +145,8 @@ struct spd_handle {
   int timed_kernel = 0;
   std::vector<hipEvent_t> tev;  // pool, pairs
   size_t tev_used = 0;
+  std::vector<hipEvent_t> sev;  // span events, triples (start, pdm end, stage end)
+  size_t sev_used = 0;
 };
 
 #define HIPC(expr)                                                              \
@@ -210,9 +214,26 @@ static Rows rows_block(int layer, int nrows, int pos0, float* x, float* anch, in
   return r;
 }
 
+// Three timing events of one step when SPD_K_SPANS timing is on (nullptr otherwise).
+static hipEvent_t* span_events(spd_handle* h) {
+  if (h->timed_kernel != SPD_K_SPANS) return nullptr;
+  if (h->sev_used + 3 > h->sev.size()) {
+    for (int i = 0; i < 96; i++) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      h->sev.push_back(e);
+    }
+  }
+  hipEvent_t* ev = h->sev.data() + h->sev_used;
+  h->sev_used += 3;
+  return ev;
+}
+
 template <typename WT>
 static spd_status enqueue_step(spd_handle* h, int forced_override) {
   const Ctx& C = h->ctx;
+  hipEvent_t* sp = span_events(h);
+  if (sp) HIPC(hipEventRecord(sp[0], h->main));
   HIPC(hipEventRecord(h->ev_fork, h->main));
   HIPC(hipStreamWaitEvent(h->pdm, h->ev_fork, 0));
   // Pipeline Draft Module on its own stream: pre-step features only (Section 3.3)
@@ -220,6 +241,7 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
   for (int i = 0; i < h->cfg.pdm_layers; i++)
     enqueue_layer<WT>(C, rows_block(h->cfg.n_layers + i, -1, -1, C.pdm_x, nullptr, -1, 1), h->pdm);
   Launch<WT>::head(C, 1, 0, h->pdm);
+  if (sp) HIPC(hipEventRecord(sp[1], h->pdm));
   HIPC(hipEventRecord(h->ev_join, h->pdm));
   // every active stage advances its token by one layer per slot (Section 3.1)
   for (int j = 0; j < h->J; j++) {
@@ -239,6 +261,7 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     TimedLaunch t(h, h->main, SPD_K_HEAD);
     Launch<WT>::head(C, 0, 0, h->main);  // exit row, only when the pipeline is full
   }
+  if (sp) HIPC(hipEventRecord(sp[2], h->main));
   HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
   launch_verify(C, forced_override, h->cfg.auto_rollback, h->main, h->bf16);
   return launch_check(h, "step");
@@ -729,7 +752,7 @@ spd_status spd_read_kv(spd_handle* h, int32_t pdm, int32_t layer, int32_t pos0, 
 }
 
 spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel) {
-  if (!h || kernel < 0 || kernel > SPD_K_HEAD) return SPD_E_INVAL;
+  if (!h || kernel < 0 || kernel > SPD_K_SPANS) return SPD_E_INVAL;
   h->timed_kernel = kernel;
   return SPD_OK;
 }
@@ -750,10 +773,33 @@ spd_status spd_kernel_timing(spd_handle* h, double* total_ms, int32_t* launches)
   return SPD_OK;
 }
 
+spd_status spd_span_timing(spd_handle* h, double* stage_ms, double* pdm_ms, double* late_ms, int32_t* steps) {
+  if (!h || !stage_ms || !pdm_ms || !late_ms || !steps) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->pdm));
+  HIPC(hipStreamSynchronize(h->main));
+  double st = 0.0, pd = 0.0, late = 0.0;
+  for (size_t i = 0; i + 3 <= h->sev_used; i += 3) {
+    float a = 0.f, b = 0.f;
+    HIPC(hipEventElapsedTime(&a, h->sev[i], h->sev[i + 2]));
+    HIPC(hipEventElapsedTime(&b, h->sev[i], h->sev[i + 1]));
+    st += a;
+    pd += b;
+    late += b > a ? (double)(b - a) : 0.0;
+  }
+  *stage_ms = st;
+  *pdm_ms = pd;
+  *late_ms = late;
+  *steps = (int32_t)(h->sev_used / 3);
+  h->sev_used = 0;
+  return SPD_OK;
+}
+
 void spd_destroy(spd_handle* h) {
   if (!h) return;
   drop_graph(h);
   for (hipEvent_t e : h->tev) (void)hipEventDestroy(e);
+  for (hipEvent_t e : h->sev) (void)hipEventDestroy(e);
   if (h->main) (void)hipStreamSynchronize(h->main);
   if (h->pdm) (void)hipStreamSynchronize(h->pdm);
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);

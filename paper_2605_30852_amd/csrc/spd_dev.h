@@ -12,6 +12,7 @@ constexpr int kMaxRows = 8;     // rows of one row-block launch (PDM rows, prefi
 constexpr int kMaxPdmLayers = 4;
 constexpr int kWG = 256;        // threads per workgroup in every kernel
 constexpr int kLogCap = 4096;   // step log ring
+constexpr int kMaxSplits = 64;  // attention key splits per (row, KV head)
 
 // One decoder layer as the kernels see it. KV pool of the layer: [pages][2][Hkv][page][dh].
 struct LayerDesc {

@@ -859,18 +859,31 @@ __device__ __forceinline__ void wait_own_stores() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+__device__ __forceinline__ float2 ld_dev2(const float* p) {  // p 8-byte aligned
+  const unsigned long long u =
+      __hip_atomic_load((unsigned long long*)const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)u), __uint_as_float((uint32_t)(u >> 32)));
+}
+
 // Decode attention of the stage launches: one query row per stage, G query heads per KV head.
-// Grid: x = split (chunk keys), y = KV head, z = stage. Each 64-key pass issues its K loads
-// (registers) and V loads (LDS tile) together; the last split to finish of each (stage, KV head)
-// merges the partial (o, m, l) records in split order and writes the output.
+// Grid: x = split (chunk keys), y = KV head, z = stage. The K (registers) and V (LDS tile) loads of
+// the next 64-key pass are issued before the current pass is computed. The last split to finish of
+// each (stage, KV head) merges the partial (o, m, l) records: all (m, l) pairs are read at once, the
+// split weights exp(m - M) / L go to LDS, and the partial outputs are summed in split order with
+// their loads issued eight at a time.
 template <typename KVT, int DH>
 __global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
   constexpr int PASS = 64, TPK = 4, NE = DH / TPK, VE = Elt<KVT>::VE;
   constexpr int MAXQ = 8;
+  constexpr int KCH = NE / VE;                       // 16-byte K chunks per thread
+  constexpr int VCH = DH * (int)sizeof(KVT) / 16;    // 16-byte chunks per V row
+  constexpr int VPT = PASS * VCH / kWG;              // V chunks per thread per pass
   __shared__ float qs[MAXQ * DH];
   __shared__ float sc[MAXQ * PASS];
   __shared__ __align__(16) KVT vs[PASS * DH];
   __shared__ float s_m[MAXQ], s_l[MAXQ], s_al[MAXQ];
+  __shared__ float s_pw[kMaxSplits * MAXQ];  // merge: m of each split, then its weight
+  __shared__ float s_pl[kMaxSplits * MAXQ];
   __shared__ int s_last;
   const Grp gr = resolve(C, R, blockIdx.z);
   if (!gr.active) return;
@@ -885,6 +898,22 @@ __global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
   const size_t voff = (size_t)C.hkv * C.page * DH;
   const BufSet& B = C.b[R.set];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int kk = tid / TPK, qq = tid % TPK;
+  // loads of one pass: rows past the chunk end re-read its last key so that every load is in
+  // bounds; only valid keys are used
+  uint4 kraw[KCH], vraw[VPT];
+  auto issue = [&](int kp) {
+    const int nk = min(PASS, k1 - kp);
+    const uint4* k4 = reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + min(kk, nk - 1), g, qq * NE));
+#pragma unroll
+    for (int c4 = 0; c4 < KCH; c4++) kraw[c4] = ldg16(k4 + c4);
+#pragma unroll
+    for (int i = 0; i < VPT; i++) {
+      const int e = tid + i * kWG, vk = e / VCH, ch = e % VCH;
+      vraw[i] = ldg16(reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + min(vk, nk - 1), g, 0) + voff) + ch);
+    }
+  };
+  issue(k0);
   for (int e = tid; e < G * DH; e += kWG) {
     const int qi = e / DH, dd = e % DH;
     qs[qi * DH + dd] = B.q[(size_t)gr.brow0 * C.qdim + (g * G + qi) * DH + dd] * C.scale;
@@ -900,35 +929,18 @@ __global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
   float o0[MAXU], o1[MAXU];
 #pragma unroll
   for (int u = 0; u < MAXU; u++) o0[u] = o1[u] = 0.f;
-  constexpr int VCH = DH * (int)sizeof(KVT) / 16;  // 16-byte chunks per V row
-  constexpr int VPT = PASS * VCH / kWG;              // V chunks per thread per pass
   for (int kp = k0; kp < k1; kp += PASS) {
     const int nk = min(PASS, k1 - kp);
-    const int kk = tid / TPK, qq = tid % TPK;
-    // issue this pass's K (registers) and V (LDS) loads together
-    // loads are unconditional (rows past the chunk end re-read its last key) so that they stay in
-    // registers; only valid keys are used
-    uint4 kraw[NE / VE];
-    {
-      const uint4* k4 = reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + min(kk, nk - 1), g, qq * NE));
-#pragma unroll
-      for (int c4 = 0; c4 < NE / VE; c4++) kraw[c4] = ldg16(k4 + c4);
-    }
-    uint4 vraw[VPT];
-#pragma unroll
-    for (int i = 0; i < VPT; i++) {
-      const int e = tid + i * kWG, vk = e / VCH, ch = e % VCH;
-      vraw[i] = ldg16(reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + min(vk, nk - 1), g, 0) + voff) + ch);
-    }
 #pragma unroll
     for (int i = 0; i < VPT; i++) {  // rows past the chunk end hold copies and are never read
       const int e = tid + i * kWG, vk = e / VCH, ch = e % VCH;
       reinterpret_cast<uint4*>(vs + vk * DH)[ch] = vraw[i];
     }
-    __syncthreads();  // q staged (first pass), V tile written
     float kr[NE];
 #pragma unroll
-    for (int c4 = 0; c4 < NE / VE; c4++) unpack16<KVT>(kraw[c4], kr + c4 * VE);
+    for (int c4 = 0; c4 < KCH; c4++) unpack16<KVT>(kraw[c4], kr + c4 * VE);
+    if (kp + PASS < k1) issue(kp + PASS);
+    __syncthreads();  // q staged (first pass), V tile written
     for (int qi = 0; qi < G; qi++) {
       float dsum = 0.f;
       const float* qv = qs + qi * DH + qq * NE;
@@ -1022,23 +1034,47 @@ __global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
   __syncthreads();
   if (!s_last) return;
   const float* base = B.part + (size_t)cidx * C.max_splits * RS;
+  for (int e = tid; e < nsplit * G; e += kWG) {  // every split has >= 1 key, so m is finite
+    const int sp = e / G, qi = e % G;
+    s_pw[sp * MAXQ + qi] = ld_dev(base + (size_t)sp * RS + MAXQ * DH + qi);
+    s_pl[sp * MAXQ + qi] = ld_dev(base + (size_t)sp * RS + MAXQ * DH + MAXQ + qi);
+  }
+  __syncthreads();
+  if (tid < G) {  // split order, fixed
+    float M = -INFINITY;
+    for (int sp = 0; sp < nsplit; sp++) M = fmaxf(M, s_pw[sp * MAXQ + tid]);
+    float Ls = 0.f;
+    for (int sp = 0; sp < nsplit; sp++) Ls = fmaf(s_pl[sp * MAXQ + tid], expf(s_pw[sp * MAXQ + tid] - M), Ls);
+    s_m[tid] = M;
+    s_l[tid] = 1.0f / Ls;
+  }
+  __syncthreads();
+  for (int e = tid; e < nsplit * G; e += kWG) {
+    const int sp = e / G, qi = e % G;
+    s_pw[sp * MAXQ + qi] = expf(s_pw[sp * MAXQ + qi] - s_m[qi]) * s_l[qi];
+  }
+  __syncthreads();
 #pragma unroll
   for (int u = 0; u < MAXU; u++) {
     const int qi = qg + u * NG;
     if (qi < G) {
-      float M = -INFINITY;
-      for (int sp = 0; sp < nsplit; sp++) M = fmaxf(M, ld_dev(base + (size_t)sp * RS + MAXQ * DH + qi));
-      float Ls = 0.f, A0 = 0.f, A1 = 0.f;
-      for (int sp = 0; sp < nsplit; sp++) {
-        const float* r = base + (size_t)sp * RS;
-        const float f = expf(ld_dev(r + MAXQ * DH + qi) - M);  // every split has >= 1 key
-        Ls = fmaf(ld_dev(r + MAXQ * DH + MAXQ + qi), f, Ls);
-        A0 = fmaf(ld_dev(r + qi * DH + 2 * dp), f, A0);
-        A1 = fmaf(ld_dev(r + qi * DH + 2 * dp + 1), f, A1);
+      float A0 = 0.f, A1 = 0.f;
+      for (int sp0 = 0; sp0 < nsplit; sp0 += 8) {
+        float2 v[8];
+#pragma unroll
+        for (int j = 0; j < 8; j++)
+          v[j] = sp0 + j < nsplit ? ld_dev2(base + (size_t)(sp0 + j) * RS + qi * DH + 2 * dp) : make_float2(0.f, 0.f);
+#pragma unroll
+        for (int j = 0; j < 8; j++) {
+          if (sp0 + j < nsplit) {
+            const float f = s_pw[(sp0 + j) * MAXQ + qi];
+            A0 = fmaf(v[j].x, f, A0);
+            A1 = fmaf(v[j].y, f, A1);
+          }
+        }
       }
-      const float inv = 1.0f / Ls;
-      out[qi * DH + 2 * dp] = A0 * inv;
-      out[qi * DH + 2 * dp + 1] = A1 * inv;
+      out[qi * DH + 2 * dp] = A0;
+      out[qi * DH + 2 * dp + 1] = A1;
     }
   }
   if (tid == 0) __hip_atomic_store(&cnt[cidx], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -62,6 +62,17 @@ def test_invalid_configs_are_rejected(field, value):
     assert e.value.status == B.SPD_E_INVAL
 
 
+def test_attention_split_count_is_bounded():
+    cfg = make_config(synth.TINY, 128, attn_chunk=16)  # 8 splits
+    assert B.spd_workspace_size(cfg) > 0
+    cfg = make_config(synth.TINY, 2048, attn_chunk=16)  # 128 splits > 64
+    with pytest.raises(B.SPDError) as e:
+        B.spd_workspace_size(cfg)
+    assert e.value.status == B.SPD_E_INVAL
+    # the default split size keeps the count at about 40 for any capacity
+    assert B.spd_workspace_size(make_config(synth.B4, 1 << 20)) > 0
+
+
 def test_n_larger_than_layers_rejected():
     cfg = make_config(synth.TINY, 128, n=5)  # tiny has 4 layers
     with pytest.raises(B.SPDError):
