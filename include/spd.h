@@ -72,6 +72,10 @@ typedef struct spd_config {
                             max_tokens. Results depend on it, so compare runs with equal values. */
   uint64_t page_seed;    /* 0: physical KV pages are handed out in order; else in an order
                             shuffled with this seed (exercises the page table) */
+  int32_t fused_head;    /* 1: the draft module's LM head shares the exit token's pass over the
+                            vocabulary (one two-row pass on main_stream after the draft module's
+                            layers join); 0: the draft module runs its own pass on pdm_stream.
+                            Both give the same draft. */
 } spd_config;
 
 /* One decoder layer's weights, all device pointers, row-major [out x in]:
@@ -200,12 +204,15 @@ spd_status spd_set_debug(spd_handle* h, int32_t on);
 
 /* Kernel timing for roofline measurements. kernel selects one launch class of the stage compute on
  * main_stream (SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD; 0 turns timing
- * off). While on, every launch of that class is bracketed by two HIP events on main_stream.
- * spd_kernel_timing waits for the stream, returns the summed event time in milliseconds and the
+ * off). While on, steps issue their launches (no graph replay) and every launch of that class in layer
+ * slot >= first_slot (the exit head counts as the slot after the last) hands two HIP events to its own
+ * dispatch, which records the kernel's start and end on main_stream. A first_slot past the draft
+ * module's span times the kernel without the side stream competing for memory bandwidth.
+ * spd_kernel_timing waits for the stream, returns the summed kernel time in milliseconds and the
  * number of timed launches, and clears both. */
 enum { SPD_K_QKV = 1, SPD_K_ATTN = 2, SPD_K_OPROJ = 3, SPD_K_GATEUP = 4, SPD_K_DOWN = 5, SPD_K_HEAD = 6,
        SPD_K_SPANS = 7 };
-spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel);
+spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel, int32_t first_slot);
 spd_status spd_kernel_timing(spd_handle* h, double* total_ms, int32_t* launches);
 
 /* Overlap of the draft module with the stage compute (Section 3.3: drafting must finish within the

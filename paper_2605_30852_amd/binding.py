@@ -27,7 +27,7 @@ class spd_config(ct.Structure):
         ("vocab", ct.c_int32), ("rms_eps", ct.c_float), ("rope_base", ct.c_float),
         ("dtype", ct.c_int32), ("n_stages", ct.c_int32), ("pdm_layers", ct.c_int32),
         ("page_size", ct.c_int32), ("max_tokens", ct.c_int32), ("auto_rollback", ct.c_int32),
-        ("attn_chunk", ct.c_int32), ("page_seed", ct.c_uint64),
+        ("attn_chunk", ct.c_int32), ("page_seed", ct.c_uint64), ("fused_head", ct.c_int32),
     ]
 
 
@@ -93,7 +93,7 @@ def lib() -> ct.CDLL:
             "spd_read_debug": (I, [P, I, P, ct.c_size_t]),
             "spd_read_kv": (I, [P, I, I, I, I, P, P]),
             "spd_set_debug": (I, [P, I]),
-            "spd_set_kernel_timing": (I, [P, I]),
+            "spd_set_kernel_timing": (I, [P, I, I]),
             "spd_set_graph": (I, [P, I]),
             "spd_kernel_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
             "spd_span_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_double),
@@ -205,8 +205,8 @@ def spd_set_debug(h: int, on: bool) -> None:
     _check("spd_set_debug", lib().spd_set_debug(h, 1 if on else 0), h)
 
 
-def spd_set_kernel_timing(h: int, kernel: int) -> None:
-    _check("spd_set_kernel_timing", lib().spd_set_kernel_timing(h, int(kernel)), h)
+def spd_set_kernel_timing(h: int, kernel: int, first_slot: int = 0) -> None:
+    _check("spd_set_kernel_timing", lib().spd_set_kernel_timing(h, int(kernel), int(first_slot)), h)
 
 
 def spd_kernel_timing(h: int):

@@ -60,6 +60,8 @@ spd_status check_config(const spd_config* c, std::string* why) {
     return bad("attn_chunk too small: max_tokens / attn_chunk must not exceed 64 key splits");
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return bad("rms_eps must be > 0 and rope_base > 1");
   if (c->auto_rollback != 0 && c->auto_rollback != 1) return bad("auto_rollback must be 0 or 1");
+  if (c->fused_head != 0 && c->fused_head != 1) return bad("fused_head must be 0 or 1");
+  if (c->d_model > 8192) return bad("d_model must be at most 8192");
   return SPD_OK;
 }
 
@@ -77,7 +79,7 @@ Layout make_layout(const spd_config& c) {
     L.chunk = c.attn_chunk ? c.attn_chunk : std::max(64, ch);
   }
   L.max_splits = (c.max_tokens + L.chunk - 1) / L.chunk;
-  L.head_tiles = (c.vocab + 63) / 64;
+  L.head_tiles = (c.vocab + kHeadRows - 1) / kHeadRows;
   L.kv_layer_bytes = (size_t)L.num_pages * 2 * hkv * c.page_size * dh * esz;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -137,12 +139,15 @@ struct spd_handle {
   long long bound = 0;  // upper bound of c + a (each step raises c + a by at most one)
   spd_step_result* pinned = nullptr;  // [kLogCap + 1]
   std::vector<int32_t> page_table;
+  std::vector<LayerDesc> layer_desc;  // host copy of the layer table
   std::string err;
   // step graph (fork/join of both streams captured once, replayed per step)
   int use_graph = 0;
   hipGraphExec_t gexec = nullptr;
   // kernel timing
   int timed_kernel = 0;
+  int timed_first_slot = 0;
+  int cur_slot = 0;  // layer slot being enqueued (J for the exit head)
   std::vector<hipEvent_t> tev;  // pool, pairs
   size_t tev_used = 0;
   std::vector<hipEvent_t> sev;  // span events, triples (start, pdm end, stage end)
@@ -167,14 +172,12 @@ static spd_status launch_check(spd_handle* h, const char* what) {
   return SPD_OK;
 }
 
-// Event pair around one launch when that launch class is being timed (main stream only).
+// Kernel timing of one launch when that launch class is being timed (main stream only): the launch
+// inside the scope hands an event pair to its dispatch, which records the kernel's own start and end.
 struct TimedLaunch {
-  spd_handle* h;
-  hipStream_t s;
   bool on;
-  size_t idx;
-  TimedLaunch(spd_handle* hh, hipStream_t ss, int kind) : h(hh), s(ss), on(false), idx(0) {
-    if (!h || h->timed_kernel != kind || s != h->main) return;
+  TimedLaunch(spd_handle* h, hipStream_t s, int kind) : on(false) {
+    if (!h || h->timed_kernel != kind || s != h->main || h->cur_slot < h->timed_first_slot) return;
     if (h->tev_used + 2 > h->tev.size()) {
       for (int i = 0; i < 64; i++) {
         hipEvent_t e;
@@ -182,12 +185,13 @@ struct TimedLaunch {
         h->tev.push_back(e);
       }
     }
-    idx = h->tev_used;
+    const size_t idx = h->tev_used;
     h->tev_used += 2;
-    on = hipEventRecord(h->tev[idx], s) == hipSuccess;
+    set_launch_events(h->tev[idx], h->tev[idx + 1]);
+    on = true;
   }
   ~TimedLaunch() {
-    if (on) (void)hipEventRecord(h->tev[idx + 1], s);
+    if (on) set_launch_events(nullptr, nullptr);
   }
 };
 
@@ -202,6 +206,7 @@ static void enqueue_layer(const Ctx& C, const Rows& r, hipStream_t s, spd_handle
 
 static Rows rows_block(int layer, int nrows, int pos0, float* x, float* anch, int cap, int set) {
   Rows r;
+  std::memset(&r, 0, sizeof(Rows));
   r.kind = 1;
   r.slot = 0;
   r.layer = layer;
@@ -240,12 +245,16 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
   Launch<WT>::pdm_fc(C, 0, 0, h->pdm);
   for (int i = 0; i < h->cfg.pdm_layers; i++)
     enqueue_layer<WT>(C, rows_block(h->cfg.n_layers + i, -1, -1, C.pdm_x, nullptr, -1, 1), h->pdm);
-  Launch<WT>::head(C, 1, 0, h->pdm);
+  const bool fused = h->cfg.fused_head != 0;
+  h->cur_slot = 0;
+  if (!fused) Launch<WT>::head(C, 1, 0, h->pdm);
   if (sp) HIPC(hipEventRecord(sp[1], h->pdm));
   HIPC(hipEventRecord(h->ev_join, h->pdm));
   // every active stage advances its token by one layer per slot (Section 3.1)
   for (int j = 0; j < h->J; j++) {
+    h->cur_slot = j;
     Rows r;
+    std::memset(&r, 0, sizeof(Rows));
     r.kind = 0;
     r.slot = j;
     r.layer = 0;
@@ -255,14 +264,30 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     r.anch = nullptr;
     r.cap = -1;
     r.set = 0;
+    for (int st = 0; st < kMaxStages; st++) {
+      const int l = st < h->cfg.n_stages ? C.beta[st] + j : -1;
+      if (l >= 0 && l < C.beta[st + 1])
+        r.ld[st] = h->layer_desc[l];
+      else
+        std::memset(&r.ld[st], 0, sizeof(LayerDesc));
+    }
     enqueue_layer<WT>(C, r, h->main, h);
   }
-  {
+  h->cur_slot = h->J;
+  if (fused) {
+    // one pass over the vocabulary for the exit row and the draft module's last row
+    if (sp) HIPC(hipEventRecord(sp[2], h->main));
+    HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
     TimedLaunch t(h, h->main, SPD_K_HEAD);
-    Launch<WT>::head(C, 0, 0, h->main);  // exit row, only when the pipeline is full
+    Launch<WT>::head(C, 3, 0, h->main);
+  } else {
+    {
+      TimedLaunch t(h, h->main, SPD_K_HEAD);
+      Launch<WT>::head(C, 0, 0, h->main);  // exit row, only when the pipeline is full
+    }
+    if (sp) HIPC(hipEventRecord(sp[2], h->main));
+    HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
   }
-  if (sp) HIPC(hipEventRecord(sp[2], h->main));
-  HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
   launch_verify(C, forced_override, h->cfg.auto_rollback, h->main, h->bf16);
   return launch_check(h, "step");
 }
@@ -483,6 +508,7 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
       std::swap(h->page_table[i], h->page_table[j]);
     }
   }
+  h->layer_desc = ld;
   HIPI(hipMemcpyAsync(ws + lay.lay, ld.data(), sizeof(LayerDesc) * ld.size(), hipMemcpyHostToDevice, h->main));
   HIPI(hipMemcpyAsync(ws + lay.rope, rope.data(), sizeof(float) * rope.size(), hipMemcpyHostToDevice, h->main));
   HIPI(hipMemcpyAsync(ws + lay.pt, h->page_table.data(), sizeof(int32_t) * lay.num_pages, hipMemcpyHostToDevice,
@@ -751,9 +777,10 @@ spd_status spd_read_kv(spd_handle* h, int32_t pdm, int32_t layer, int32_t pos0, 
   return SPD_OK;
 }
 
-spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel) {
-  if (!h || kernel < 0 || kernel > SPD_K_SPANS) return SPD_E_INVAL;
+spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel, int32_t first_slot) {
+  if (!h || kernel < 0 || kernel > SPD_K_SPANS || first_slot < 0) return SPD_E_INVAL;
   h->timed_kernel = kernel;
+  h->timed_first_slot = first_slot;
   return SPD_OK;
 }
 

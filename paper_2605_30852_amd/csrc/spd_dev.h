@@ -13,6 +13,7 @@ constexpr int kMaxPdmLayers = 4;
 constexpr int kWG = 256;        // threads per workgroup in every kernel
 constexpr int kLogCap = 4096;   // step log ring
 constexpr int kMaxSplits = 64;  // attention key splits per (row, KV head)
+constexpr int kHeadRows = 32;   // LM-head vocabulary rows per workgroup (one argmax partial each)
 
 // One decoder layer as the kernels see it. KV pool of the layer: [pages][2][Hkv][page][dh].
 struct LayerDesc {
@@ -94,13 +95,16 @@ struct Ctx {
 struct Rows {
   int kind;
   int slot;
-  int layer;    // index into Ctx::lay
+  int layer;    // kind 1: index into Ctx::lay
   int nrows;
   int pos0;
   float* x;     // kind 1: residual rows [nrows][d]
   float* anch;  // kind 1: anchor capture base [rows][n][d] (null: none)
   int cap;      // kind 1: anchor index to capture after this layer (-1: none)
   int set;      // scratch set
+  // kind 0: layer beta_s + slot of every stage s, passed with the launch so that weight loads need
+  // no table lookup (all pointers null for a stage with no layer in this slot)
+  LayerDesc ld[kMaxStages];
 };
 
 // Launchers (spd_kernels.hip). All are asynchronous on `stream`.
@@ -113,12 +117,16 @@ struct Launch {
   static void down(const Ctx& c, const Rows& r, void* stream);
   // PDM feature projection; prefill = 1: nrows rows of pf_anch at full depth.
   static void pdm_fc(const Ctx& c, int prefill, int nrows, void* stream);
-  // LM head + argmax. src: 0 = target exit row (skipped unless a == n), 1 = PDM last row,
-  // 2 = prefill row `row` of pf_x. Writes st->y (src 0, 2) or st->pdm_draft (src 1).
+  // LM head + argmax partials. src: 0 = target exit row (skipped unless a == n), 1 = PDM last row,
+  // 2 = prefill row `row` of pf_x, 3 = exit row and PDM row in one pass. The kernel that follows
+  // (verify / reseed) reduces the partials.
   static void head(const Ctx& c, int src, int row, void* stream);
   static void embed_rows(const Ctx& c, int t0, int nrows, void* stream);
 };
 void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* stream, int bf16);
+// Events (hipEvent_t) that the next launches of this host thread record at their own start and end;
+// nullptr turns it off.
+void set_launch_events(void* start, void* stop);
 void launch_reseed(const Ctx& c, int keep, int tok, int prompt_len, void* stream, int bf16);
 
 }  // namespace spd

@@ -9,6 +9,7 @@
 // KV length: the lane-to-column map, the FMA order, the butterfly and the split size never depend
 // on how many stages share a launch. That makes a token's arithmetic identical whether it runs in an
 // n-stage SPD step or in plain decoding (n = 1), which the lossless check relies on.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -76,6 +77,17 @@ __device__ __forceinline__ float ld1<uint16_t>(const uint16_t* p, size_t i) {
   return __uint_as_float(((uint32_t)p[i]) << 16);
 }
 
+// Two consecutive elements (4- or 8-byte aligned) as floats.
+template <typename T>
+__device__ __forceinline__ float2 ld2(const T* p);
+template <>
+__device__ __forceinline__ float2 ld2<float>(const float* p) { return *reinterpret_cast<const float2*>(p); }
+template <>
+__device__ __forceinline__ float2 ld2<uint16_t>(const uint16_t* p) {
+  const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
+  return make_float2(bf_lo(u), bf_hi(u));
+}
+
 template <typename T>
 __device__ __forceinline__ void st1(T* p, size_t i, float v);
 template <>
@@ -99,7 +111,7 @@ __device__ __forceinline__ float wave_max(float v) {
 // ------------------------------------------------------------------------------- row resolution
 struct Grp {
   int active;
-  int layer;
+  int layer;  // target or PDM layer index
   int nrows;
   int pos0;
   int s;      // stage (kind 0) or -1
@@ -118,7 +130,7 @@ __device__ __forceinline__ Grp resolve(const Ctx& C, const Rows& R, int g) {
       r.active = 0;
       return r;
     }
-    r.layer = C.beta[g] + R.slot;
+    r.layer = C.beta[g] + R.slot;  // (its weights come from R.ld[g])
     r.nrows = 1;
     r.pos0 = c + a - 1 - g;
     r.brow0 = g;
@@ -135,6 +147,12 @@ __device__ __forceinline__ Grp resolve(const Ctx& C, const Rows& R, int g) {
     if (r.nrows <= 0) r.active = 0;
   }
   return r;
+}
+
+// The layer a group runs: from the launch's own arguments for stage launches, from the device table
+// for row blocks.
+__device__ __forceinline__ LayerDesc layer_of(const Ctx& C, const Rows& R, const Grp& gr) {
+  return R.kind == 0 ? R.ld[gr.s] : C.lay[gr.layer];
 }
 
 __device__ __forceinline__ size_t kv_off(const Ctx& C, int pos, int kvh, int j) {
@@ -157,48 +175,67 @@ __device__ __forceinline__ int xidx(int k) {
   }
 }
 
-// acc[v][r] += W[row r][cols of this lane] . x[v][same cols], over one staged chunk.
-template <typename WT, int NV, int RL>
-__device__ __forceinline__ void accum_chunk(const WT* const (&wr)[RL], int K, int kc0, int kl_pad,
-                                            const float* lds, int KC, int nrows,
-                                            float (&acc)[NV][RL], int lane) {
+// Weight blocks loaded at once per row: a wave keeps RL rows x kU blocks of 16-byte loads in flight.
+constexpr int kU = 5;
+
+// Load blocks [blk, min(blk + kU, blk_end)) of every row (block b = columns b*64*VE + lane*VE + 0..VE-1);
+// rows that are nullptr or blocks past blk_end load zeros. K is a multiple of VE, so a load that starts
+// inside the row ends inside it.
+template <typename WT, int RL>
+__device__ __forceinline__ void load_blocks(const WT* const (&wr)[RL], int K, int blk, int blk_end, int lane,
+                                            uint4 (&w)[RL][kU]) {
   constexpr int VE = Elt<WT>::VE;
   constexpr int BLK = 64 * VE;
-#pragma unroll 2
-  for (int b = 0; b < kl_pad; b += BLK) {
-    const int col = kc0 + b + lane * VE;
-    uint4 w[RL];
+#pragma unroll
+  for (int u = 0; u < kU; u++) {
 #pragma unroll
     for (int r = 0; r < RL; r++) {
-      if (wr[r] != nullptr && col < K)
-        w[r] = ldg16(wr[r] + col);
-      else
-        w[r] = make_uint4(0u, 0u, 0u, 0u);
+      const int col = (blk + u) * BLK + lane * VE;
+      w[r][u] = (wr[r] != nullptr && blk + u < blk_end && col < K) ? ldg16(wr[r] + col) : make_uint4(0u, 0u, 0u, 0u);
     }
-    float wf[RL][VE];
+  }
+}
+
+// acc[v][r] += W[row r] . x[v] over staged blocks [0, nbk) of the chunk in LDS (block b of the chunk is
+// global block blk0 + b). The first kU blocks must already be in w (prefetched by the caller); later
+// groups are loaded here. Per lane the FMA order is: blocks in order, then the VE columns in order.
+template <typename WT, int NV, int RL>
+__device__ __forceinline__ void accum_blocks(const WT* const (&wr)[RL], int K, int blk0, int nbk, const float* lds,
+                                             int KC, int nrows, float (&acc)[NV][RL], uint4 (&w)[RL][kU],
+                                             int lane) {
+  constexpr int VE = Elt<WT>::VE;
+  constexpr int BLK = 64 * VE;
+  for (int b = 0; b < nbk; b += kU) {
+    if (b > 0) load_blocks<WT, RL>(wr, K, blk0 + b, blk0 + nbk, lane, w);
 #pragma unroll
-    for (int r = 0; r < RL; r++) unpack16<WT>(w[r], wf[r]);
+    for (int u = 0; u < kU; u++) {
+      if (b + u < nbk) {
+        float wf[RL][VE];
 #pragma unroll
-    for (int v = 0; v < NV; v++) {
-      if (v < nrows) {
-        float x[VE];
-        const float* xb = lds + v * KC + b;
-        const float4 x0 = *reinterpret_cast<const float4*>(xb + lane * 4);
-        x[0] = x0.x;
-        x[1] = x0.y;
-        x[2] = x0.z;
-        x[3] = x0.w;
-        if constexpr (VE == 8) {
-          const float4 x1 = *reinterpret_cast<const float4*>(xb + 256 + lane * 4);
-          x[4] = x1.x;
-          x[5] = x1.y;
-          x[6] = x1.z;
-          x[7] = x1.w;
-        }
+        for (int r = 0; r < RL; r++) unpack16<WT>(w[r][u], wf[r]);
 #pragma unroll
-        for (int r = 0; r < RL; r++) {
+        for (int v = 0; v < NV; v++) {
+          if (v < nrows) {
+            float x[VE];
+            const float* xb = lds + v * KC + (b + u) * BLK;
+            const float4 x0 = *reinterpret_cast<const float4*>(xb + lane * 4);
+            x[0] = x0.x;
+            x[1] = x0.y;
+            x[2] = x0.z;
+            x[3] = x0.w;
+            if constexpr (VE == 8) {
+              const float4 x1 = *reinterpret_cast<const float4*>(xb + 256 + lane * 4);
+              x[4] = x1.x;
+              x[5] = x1.y;
+              x[6] = x1.z;
+              x[7] = x1.w;
+            }
 #pragma unroll
-          for (int e = 0; e < VE; e++) acc[v][r] = fmaf(wf[r][e], x[e], acc[v][r]);
+            for (int r = 0; r < RL; r++) {
+#pragma unroll
+              for (int e = 0; e < VE; e++) acc[v][r] = fmaf(wf[r][e], x[e], acc[v][r]);
+            }
+          }
         }
       }
     }
@@ -214,36 +251,53 @@ enum XSrc {
 
 struct XSpec {
   int src = 0;
-  const float* gain;           // XS_NORM_RESID
-  const float* row[kMaxRows];  // activation row v
+  const float* gain[kMaxRows];  // XS_NORM_RESID: gain of row v
+  const float* row[kMaxRows];  // activation row v (16-byte aligned)
   int nelig[kMaxRows];         // XS_ANCHORS: eligible length (f+1)*d per row
 };
 
-// Stage chunk [kc0, kc0+kl) of every row into LDS (zero padded to kl_pad); accumulate sum of
-// squares per row in ss (per-thread partials) when normalising.
+// Stage chunk [kc0, kc0+kl) of every row into LDS (zero padded to kl_pad) with 16-byte loads, all of a
+// thread's loads of a round issued before its LDS stores; accumulate the sum of squares per row in ss
+// (per-thread partials) when normalising. kl, kc0 and every nelig are multiples of 4.
 template <int VE, int NV>
-__device__ __forceinline__ void stage_chunk(const XSpec& xs, int nrows, int kc0, int kl, int kl_pad,
-                                            float* lds, int KC, float (&ss)[NV]) {
+__device__ __forceinline__ void stage_chunk(const XSpec& xs, int nrows, int kc0, int kl, int kl_pad, float* lds,
+                                            int KC, float (&ss)[NV]) {
+  constexpr int RND = 4;
+  const int n4 = kl_pad >> 2;
 #pragma unroll
   for (int v = 0; v < NV; v++) {
     if (v >= nrows) continue;
     const float* row = xs.row[v];
-    const int nel = xs.nelig[v];
-    for (int k = threadIdx.x; k < kl_pad; k += kWG) {
-      float val = 0.f;
-      const int gk = kc0 + k;
-      if (k < kl) {
-        if (xs.src == XS_ANCHORS) {
-          val = gk < nel ? row[gk] : 0.f;
-        } else {
-          val = row[gk];
+    const int nel = xs.src == XS_ANCHORS ? xs.nelig[v] : 0x7fffffff;
+    for (int k40 = threadIdx.x; k40 < n4; k40 += kWG * RND) {
+      float4 xv[RND], gv[RND];
+#pragma unroll
+      for (int j = 0; j < RND; j++) {
+        const int k = (k40 + j * kWG) * 4;
+        const int gk = kc0 + k;
+        const bool ok = k < kl && gk < nel;
+        xv[j] = ok ? *reinterpret_cast<const float4*>(row + gk) : make_float4(0.f, 0.f, 0.f, 0.f);
+        if (xs.src == XS_NORM_RESID)
+          gv[j] = ok ? *reinterpret_cast<const float4*>(xs.gain[v] + gk) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int j = 0; j < RND; j++) {
+        const int k4 = k40 + j * kWG;
+        if (k4 < n4) {
+          float4 val = xv[j];
           if (xs.src == XS_NORM_RESID) {
-            ss[v] = fmaf(val, val, ss[v]);
-            val *= xs.gain[gk];
+            ss[v] = fmaf(val.x, val.x, ss[v]);
+            ss[v] = fmaf(val.y, val.y, ss[v]);
+            ss[v] = fmaf(val.z, val.z, ss[v]);
+            ss[v] = fmaf(val.w, val.w, ss[v]);
+            val.x *= gv[j].x;
+            val.y *= gv[j].y;
+            val.z *= gv[j].z;
+            val.w *= gv[j].w;
           }
+          *reinterpret_cast<float4*>(lds + v * KC + xidx<VE>(k4 * 4)) = val;
         }
       }
-      lds[v * KC + xidx<VE>(k)] = val;
     }
   }
 }
@@ -257,8 +311,22 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-// Run the full K loop for one tile: stage chunks, accumulate, reduce over the wave, and scale
-// by 1/rms for normalised inputs. On return every lane of a wave holds the wave's row results.
+// Staged activation floats per row and chunk (multiples of every block width, so that the
+// per-lane accumulation order does not depend on the chunking). LDS stays at 48 KB or less.
+constexpr int kChunkCap1 = 12288;
+constexpr int kChunkCapN = 1536;
+
+template <int NV>
+__device__ __forceinline__ int chunk_floats(int K, int blk) {
+  const int kp = (K + blk - 1) / blk * blk;
+  const int cap = (NV == 1 ? kChunkCap1 : kChunkCapN);
+  return kp < cap ? kp : cap;
+}
+
+// One GEMV tile: RL weight rows per wave against NV activation rows. The first weight blocks are
+// requested before the activations are staged (they do not depend on them), then every chunk is
+// staged and consumed. On return every lane of a wave holds the wave's row results, scaled by 1/rms
+// for normalised inputs.
 template <typename WT, int NV, int RL>
 __device__ __forceinline__ void gemv_tile(const WT* const (&wr)[RL], int K, const XSpec& xs, int nrows,
                                           float eps, float* lds, int KC, float (&acc)[NV][RL]) {
@@ -273,13 +341,22 @@ __device__ __forceinline__ void gemv_tile(const WT* const (&wr)[RL], int K, cons
 #pragma unroll
     for (int r = 0; r < RL; r++) acc[v][r] = 0.f;
   }
+  uint4 w[RL][kU];
+  {
+    const int kl0 = min(KC, K);
+    load_blocks<WT, RL>(wr, K, 0, (kl0 + BLK - 1) / BLK, lane, w);
+  }
   for (int kc0 = 0; kc0 < K; kc0 += KC) {
     const int kl = min(KC, K - kc0);
     const int kl_pad = (kl + BLK - 1) / BLK * BLK;
-    __syncthreads();
+    const int blk0 = kc0 / BLK, nbk = kl_pad / BLK;
+    if (kc0 > 0) {
+      __syncthreads();  // every wave is done with the previous chunk
+      load_blocks<WT, RL>(wr, K, blk0, blk0 + nbk, lane, w);
+    }
     stage_chunk<VE, NV>(xs, nrows, kc0, kl, kl_pad, lds, KC, ss);
     __syncthreads();
-    accum_chunk<WT, NV, RL>(wr, K, kc0, kl_pad, lds, KC, nrows, acc, lane);
+    accum_blocks<WT, NV, RL>(wr, K, blk0, nbk, lds, KC, nrows, acc, w, lane);
   }
 #pragma unroll
   for (int v = 0; v < NV; v++) {
@@ -297,28 +374,16 @@ __device__ __forceinline__ void gemv_tile(const WT* const (&wr)[RL], int K, cons
   }
 }
 
-// Staged activation floats per row and chunk (multiples of every block width, so that the
-// per-lane accumulation order does not depend on the chunking). LDS stays at 48 KB or less.
-constexpr int kChunkCap1 = 12288;
-constexpr int kChunkCapN = 1536;
-
-template <int NV>
-__device__ __forceinline__ int chunk_floats(int K, int blk) {
-  const int kp = (K + blk - 1) / blk * blk;
-  const int cap = (NV == 1 ? kChunkCap1 : kChunkCapN);
-  return kp < cap ? kp : cap;
-}
-
 // ------------------------------------------------------------------ QKV + RoPE + KV append
-// Tile = 8 RoPE pairs of one head: wave w holds rows (2w, 2w+1) of the pair block and their
-// partners half a head away, so the rotation happens in registers right after the reduction.
+// Tile = 4 RoPE pairs of one head: wave w holds row j = 4*tile + w and its partner j + dh/2, so the
+// rotation happens in registers right after the reduction.
 template <typename WT, int NV>
 __global__ __launch_bounds__(kWG) void k_qkv(Ctx C, Rows R) {
   extern __shared__ float lds[];
   const Grp gr = resolve(C, R, blockIdx.y);
   if (!gr.active) return;
-  const LayerDesc& Ld = C.lay[gr.layer];
-  const int dh = C.dh, half = dh >> 1, tph = dh >> 4;
+  const LayerDesc Ld = layer_of(C, R, gr);
+  const int dh = C.dh, half = dh >> 1, tph = half >> 2;
   const int head = blockIdx.x / tph, pb = blockIdx.x % tph;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const WT* W;
@@ -337,52 +402,48 @@ __global__ __launch_bounds__(kWG) void k_qkv(Ctx C, Rows R) {
     hrow = head - C.hq - C.hkv;
     kind = 2;
   }
-  const int j0 = pb * 8 + 2 * w;  // pair indices j0, j0+1 (< half)
-  const WT* wr[4];
-  wr[0] = W + (size_t)(hrow * dh + j0) * C.d;
-  wr[1] = W + (size_t)(hrow * dh + j0 + 1) * C.d;
-  wr[2] = W + (size_t)(hrow * dh + j0 + half) * C.d;
-  wr[3] = W + (size_t)(hrow * dh + j0 + half + 1) * C.d;
+  const int j = pb * 4 + w;  // pair index (< half)
+  const WT* wr[2];
+  wr[0] = W + (size_t)(hrow * dh + j) * C.d;
+  wr[1] = W + (size_t)(hrow * dh + j + half) * C.d;
   XSpec xs;
   xs.src = XS_NORM_RESID;
-  xs.gain = Ld.attn_norm;
-  for (int v = 0; v < NV; v++) xs.row[v] = gr.x + (size_t)v * gr.xstride;
+  for (int v = 0; v < NV; v++) {
+    xs.row[v] = gr.x + (size_t)v * gr.xstride;
+    xs.gain[v] = Ld.attn_norm;
+  }
   const int KC = chunk_floats<NV>(C.d, 64 * Elt<WT>::VE);
-  float acc[NV][4];
-  gemv_tile<WT, NV, 4>(wr, C.d, xs, gr.nrows, C.eps, lds, KC, acc);
+  float acc[NV][2];
+  gemv_tile<WT, NV, 2>(wr, C.d, xs, gr.nrows, C.eps, lds, KC, acc);
   float* qbuf = C.b[R.set].q;
 #pragma unroll
   for (int v = 0; v < NV; v++) {
-#pragma unroll
-    for (int p = 0; p < 2; p++) {
-      if (lane == v * 2 + p && v < gr.nrows) {
-        const int pos = gr.pos0 + v;
-        const int j = j0 + p;
-        float lo = acc[v][p], hi = acc[v][p + 2];
-        if (kind != 2) {
-          const float2 cs = C.rope[(size_t)pos * half + j];
-          const float rlo = lo * cs.x - hi * cs.y;
-          const float rhi = hi * cs.x + lo * cs.y;
-          lo = rlo;
-          hi = rhi;
-        }
-        if (kind == 0) {
-          float* qo = qbuf + (size_t)(gr.brow0 + v) * C.qdim + hrow * dh;
-          qo[j] = lo;
-          qo[j + half] = hi;
-        } else {
-          WT* kv = (WT*)Ld.kv;
-          const size_t off = kv_off(C, pos, hrow, j) + (kind == 2 ? (size_t)C.hkv * C.page * dh : 0);
-          st1<WT>(kv, off, lo);
-          st1<WT>(kv, off + half, hi);
-        }
+    if (lane == v && v < gr.nrows) {
+      const int pos = gr.pos0 + v;
+      float lo = acc[v][0], hi = acc[v][1];
+      if (kind != 2) {
+        const float2 cs = C.rope[(size_t)pos * half + j];
+        const float rlo = lo * cs.x - hi * cs.y;
+        const float rhi = hi * cs.x + lo * cs.y;
+        lo = rlo;
+        hi = rhi;
+      }
+      if (kind == 0) {
+        float* qo = qbuf + (size_t)(gr.brow0 + v) * C.qdim + hrow * dh;
+        qo[j] = lo;
+        qo[j + half] = hi;
+      } else {
+        WT* kv = (WT*)Ld.kv;
+        const size_t off = kv_off(C, pos, hrow, j) + (kind == 2 ? (size_t)C.hkv * C.page * dh : 0);
+        st1<WT>(kv, off, lo);
+        st1<WT>(kv, off + half, hi);
       }
     }
   }
 }
 
 // --------------------------------------------------------------- O-proj / down-proj + residual
-// Tile = 16 output rows (4 per wave). MODE 0: o-proj (input = attention output, K = Hq*dh);
+// Tile = 8 output rows (2 per wave). MODE 0: o-proj (input = attention output, K = Hq*dh);
 // MODE 1: down-proj (input = SwiGLU activation, K = F), which also captures the stage output as
 // the next PDM anchor when this is a stage's last layer.
 template <typename WT, int NV, int MODE>
@@ -390,24 +451,23 @@ __global__ __launch_bounds__(kWG) void k_proj_add(Ctx C, Rows R) {
   extern __shared__ float lds[];
   const Grp gr = resolve(C, R, blockIdx.y);
   if (!gr.active) return;
-  const LayerDesc& Ld = C.lay[gr.layer];
+  const LayerDesc Ld = layer_of(C, R, gr);
   const int K = MODE == 0 ? C.qdim : C.F;
   const WT* W = (const WT*)(MODE == 0 ? Ld.wo : Ld.wd);
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int m0 = blockIdx.x * 16 + w * 4;
-  const WT* wr[4];
+  const int m0 = blockIdx.x * 8 + w * 2;
+  const WT* wr[2];
 #pragma unroll
-  for (int r = 0; r < 4; r++) wr[r] = (m0 + r < C.d) ? W + (size_t)(m0 + r) * K : nullptr;
+  for (int r = 0; r < 2; r++) wr[r] = (m0 + r < C.d) ? W + (size_t)(m0 + r) * K : nullptr;
   XSpec xs;
   xs.src = XS_PLAIN;
-  xs.gain = nullptr;
   {
     const float* b0 = (MODE == 0 ? C.b[R.set].ao : C.b[R.set].act) + (size_t)gr.brow0 * K;
     for (int v = 0; v < NV; v++) xs.row[v] = b0 + (size_t)v * K;
   }
   const int KC = chunk_floats<NV>(K, 64 * Elt<WT>::VE);
-  float acc[NV][4];
-  gemv_tile<WT, NV, 4>(wr, K, xs, gr.nrows, 0.f, lds, KC, acc);
+  float acc[NV][2];
+  gemv_tile<WT, NV, 2>(wr, K, xs, gr.nrows, 0.f, lds, KC, acc);
   // anchor capture target
   float* cap = nullptr;
   size_t cap_stride = 0;
@@ -425,8 +485,8 @@ __global__ __launch_bounds__(kWG) void k_proj_add(Ctx C, Rows R) {
 #pragma unroll
   for (int v = 0; v < NV; v++) {
 #pragma unroll
-    for (int r = 0; r < 4; r++) {
-      if (lane == v * 4 + r && v < gr.nrows && m0 + r < C.d) {
+    for (int r = 0; r < 2; r++) {
+      if (lane == v * 2 + r && v < gr.nrows && m0 + r < C.d) {
         float* xo = gr.x + (size_t)v * gr.xstride;
         const float nv = xo[m0 + r] + acc[v][r];
         xo[m0 + r] = nv;
@@ -437,38 +497,33 @@ __global__ __launch_bounds__(kWG) void k_proj_add(Ctx C, Rows R) {
 }
 
 // ------------------------------------------------------------------------- gate/up + SwiGLU
-// Tile = 8 outputs (2 per wave); each wave streams the gate and up rows of its outputs together.
+// Tile = 4 outputs (1 per wave); each wave streams the gate and up rows of its output together.
 template <typename WT, int NV>
 __global__ __launch_bounds__(kWG) void k_gateup(Ctx C, Rows R) {
   extern __shared__ float lds[];
   const Grp gr = resolve(C, R, blockIdx.y);
   if (!gr.active) return;
-  const LayerDesc& Ld = C.lay[gr.layer];
+  const LayerDesc Ld = layer_of(C, R, gr);
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int m0 = blockIdx.x * 8 + w * 2;
-  const WT* Wg = (const WT*)Ld.wg;
-  const WT* Wu = (const WT*)Ld.wu;
-  const WT* wr[4];
-  wr[0] = (m0 < C.F) ? Wg + (size_t)m0 * C.d : nullptr;
-  wr[1] = (m0 + 1 < C.F) ? Wg + (size_t)(m0 + 1) * C.d : nullptr;
-  wr[2] = (m0 < C.F) ? Wu + (size_t)m0 * C.d : nullptr;
-  wr[3] = (m0 + 1 < C.F) ? Wu + (size_t)(m0 + 1) * C.d : nullptr;
+  const int m = blockIdx.x * 4 + w;
+  const WT* wr[2];
+  wr[0] = (m < C.F) ? (const WT*)Ld.wg + (size_t)m * C.d : nullptr;
+  wr[1] = (m < C.F) ? (const WT*)Ld.wu + (size_t)m * C.d : nullptr;
   XSpec xs;
   xs.src = XS_NORM_RESID;
-  xs.gain = Ld.mlp_norm;
-  for (int v = 0; v < NV; v++) xs.row[v] = gr.x + (size_t)v * gr.xstride;
+  for (int v = 0; v < NV; v++) {
+    xs.row[v] = gr.x + (size_t)v * gr.xstride;
+    xs.gain[v] = Ld.mlp_norm;
+  }
   const int KC = chunk_floats<NV>(C.d, 64 * Elt<WT>::VE);
-  float acc[NV][4];
-  gemv_tile<WT, NV, 4>(wr, C.d, xs, gr.nrows, C.eps, lds, KC, acc);
+  float acc[NV][2];
+  gemv_tile<WT, NV, 2>(wr, C.d, xs, gr.nrows, C.eps, lds, KC, acc);
   float* act = C.b[R.set].act;
 #pragma unroll
   for (int v = 0; v < NV; v++) {
-#pragma unroll
-    for (int p = 0; p < 2; p++) {
-      if (lane == v * 2 + p && v < gr.nrows && m0 + p < C.F) {
-        const float g = acc[v][p], u = acc[v][p + 2];
-        act[(size_t)(gr.brow0 + v) * C.F + m0 + p] = g / (1.0f + expf(-g)) * u;
-      }
+    if (lane == v && v < gr.nrows && m < C.F) {
+      const float g = acc[v][0], u = acc[v][1];
+      act[(size_t)(gr.brow0 + v) * C.F + m] = g / (1.0f + expf(-g)) * u;
     }
   }
 }
@@ -476,7 +531,7 @@ __global__ __launch_bounds__(kWG) void k_gateup(Ctx C, Rows R) {
 // ---------------------------------------------------------------------- PDM feature projection
 // g_q = W_in . [H^{beta_0}; ...; H^{beta_f}; 0 ...] for the rows the PDM runs (Eq. agg-main with
 // one projection whose column block j serves anchor j). prefill = 1: rows of the prefill chunk
-// at full depth; else the a in-flight rows, row i at depth a-1-i.
+// at full depth; else the a in-flight rows, row i at depth a-1-i. Tile = 8 outputs (2 per wave).
 template <typename WT>
 __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_arg) {
   extern __shared__ float lds[];
@@ -486,7 +541,6 @@ __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_ar
   int nrows;
   XSpec xs;
   xs.src = XS_ANCHORS;
-  xs.gain = nullptr;
   if (prefill) {
     nrows = nrows_arg;
     for (int i = 0; i < kMaxRows; i++) {
@@ -505,110 +559,147 @@ __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_ar
     }
   }
   if (nrows <= 0) return;
-  const int m0 = blockIdx.x * 16 + w * 4;
+  const int m0 = blockIdx.x * 8 + w * 2;
   const WT* W = (const WT*)C.w_in;
-  const WT* wr[4];
+  const WT* wr[2];
 #pragma unroll
-  for (int r = 0; r < 4; r++) wr[r] = (m0 + r < C.d) ? W + (size_t)(m0 + r) * K : nullptr;
+  for (int r = 0; r < 2; r++) wr[r] = (m0 + r < C.d) ? W + (size_t)(m0 + r) * K : nullptr;
   const int KC = chunk_floats<NV>(K, 64 * Elt<WT>::VE);
-  float acc[NV][4];
-  gemv_tile<WT, NV, 4>(wr, K, xs, nrows, 0.f, lds, KC, acc);
+  float acc[NV][2];
+  gemv_tile<WT, NV, 2>(wr, K, xs, nrows, 0.f, lds, KC, acc);
   float* out = C.pdm_x;
 #pragma unroll
   for (int v = 0; v < NV; v++) {
 #pragma unroll
-    for (int r = 0; r < 4; r++) {
-      if (lane == v * 4 + r && v < nrows && m0 + r < C.d) out[(size_t)v * C.d + m0 + r] = acc[v][r];
+    for (int r = 0; r < 2; r++) {
+      if (lane == v * 2 + r && v < nrows && m0 + r < C.d) out[(size_t)v * C.d + m0 + r] = acc[v][r];
     }
   }
 }
 
 // ---------------------------------------------------------------------------- LM head + argmax
-constexpr int kHeadRowsPerWave = 16;  // 64 vocabulary rows per workgroup
-
-// Tile = 64 vocabulary rows. Each workgroup writes its best (value, index), the lowest index
-// winning ties; the single-workgroup kernel that follows on the stream reduces the partials. The
-// (value desc, index asc) order is total, so the winner does not depend on the reduction order.
+// Tile = kHeadRows vocabulary rows, kHeadRows/4 per wave in pairs. Each workgroup writes its best
+// (value, index), the lowest index winning ties; the single-workgroup kernel that follows on the
+// stream reduces the partials. The (value desc, index asc) order is total, so the winner does not
+// depend on the reduction order.
 __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
 
-template <typename WT>
-__global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row, int set) {
+// Rows of one LM-head pass. src 0: the exit row (skipped unless a == n); 1: the PDM's last row;
+// 2: prefill row `row`; 3: the exit row and the PDM's last row together (rows 0 and 1), one pass over
+// W_lm serving both heads. Row results go to the partials of set 0 (target) or set 1 (PDM).
+template <typename WT, int NV>
+__global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row) {
   extern __shared__ float lds[];
-  __shared__ float s_v[4];
-  __shared__ int s_i[4];
+  __shared__ float s_v[NV][4];
+  __shared__ int s_i[NV][4];
   __shared__ float red[4];
-  const float* x;
-  const float* gain;
+  constexpr int RPW = kHeadRows / 4;  // rows per wave
+  const int a = C.st->a, c = C.st->c;
+  XSpec xs;
+  xs.src = XS_NORM_RESID;
+  int set[NV];
   if (src == 0) {
-    const int a = C.st->a, c = C.st->c;
     if (a != C.n) return;  // nothing exits while the pipeline fills
-    x = C.resid + (size_t)(c % C.n) * C.d;
-    gain = C.final_norm;
+    xs.row[0] = C.resid + (size_t)(c % C.n) * C.d;
+    xs.gain[0] = C.final_norm;
+    set[0] = 0;
   } else if (src == 1) {
-    x = C.pdm_x + (size_t)(C.st->a - 1) * C.d;
-    gain = C.pdm_norm;
+    xs.row[0] = C.pdm_x + (size_t)(a - 1) * C.d;
+    xs.gain[0] = C.pdm_norm;
+    set[0] = 1;
+  } else if (src == 2) {
+    xs.row[0] = C.pf_x + (size_t)row * C.d;
+    xs.gain[0] = C.final_norm;
+    set[0] = 0;
   } else {
-    x = C.pf_x + (size_t)row * C.d;
-    gain = C.final_norm;
+    // while the pipeline fills the exit row is computed but unused (its partials are not read)
+    xs.row[0] = C.resid + (size_t)(c % C.n) * C.d;
+    xs.gain[0] = C.final_norm;
+    set[0] = 0;
+    xs.row[NV - 1] = C.pdm_x + (size_t)(a - 1) * C.d;
+    xs.gain[NV - 1] = C.pdm_norm;
+    set[NV - 1] = 1;
   }
   constexpr int VE = Elt<WT>::VE;
   constexpr int BLK = 64 * VE;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  // stage rmsnorm-gain input once (d fits one chunk), then stream 4 groups of 4 rows per wave
-  XSpec xs;
-  xs.src = XS_NORM_RESID;
-  xs.gain = gain;
-  xs.row[0] = x;
-  const int KC = chunk_floats<1>(C.d, BLK);
-  const int kl_pad = (C.d + BLK - 1) / BLK * BLK;
-  float ss[1] = {0.f};
-  stage_chunk<VE, 1>(xs, 1, 0, C.d, kl_pad, lds, KC, ss);
-  const float tot = block_sum(ss[0], red);  // includes the barrier that publishes the staged row
-  const float scl = 1.0f / sqrtf(tot / (float)C.d + C.eps);
   const WT* W = (const WT*)C.lm_head;
-  float bv = -INFINITY;
-  int bi = 0x7fffffff;
-  for (int rg = 0; rg < kHeadRowsPerWave / 4; rg++) {
-    const int m0 = blockIdx.x * (4 * kHeadRowsPerWave) + w * kHeadRowsPerWave + rg * 4;
-    const WT* wr[4];
+  const int mw = blockIdx.x * kHeadRows + w * RPW;  // first row of this wave
+  const int kl_pad = (C.d + BLK - 1) / BLK * BLK;  // d fits one chunk (d <= 8192)
+  const int nbk = kl_pad / BLK;
+  auto rows_of = [&](int m0, const WT* (&wr)[2]) {
 #pragma unroll
-    for (int r = 0; r < 4; r++) wr[r] = (m0 + r < C.V) ? W + (size_t)(m0 + r) * C.d : nullptr;
-    float acc[1][4] = {{0.f, 0.f, 0.f, 0.f}};
-    accum_chunk<WT, 1, 4>(wr, C.d, 0, kl_pad, lds, KC, 1, acc, lane);
+    for (int r = 0; r < 2; r++) wr[r] = (m0 + r < C.V) ? W + (size_t)(m0 + r) * C.d : nullptr;
+  };
+  uint4 wv[2][kU];
+  {
+    const WT* wr[2];
+    rows_of(mw, wr);
+    load_blocks<WT, 2>(wr, C.d, 0, nbk, lane, wv);  // weights first, then the activations
+  }
+  float ss[NV];
 #pragma unroll
-    for (int r = 0; r < 4; r++) acc[0][r] = wave_sum(acc[0][r]) * scl;
-    if (C.debug && lane < 4 && m0 + lane < C.V) {
-      float val = acc[0][0];
+  for (int v = 0; v < NV; v++) ss[v] = 0.f;
+  stage_chunk<VE, NV>(xs, NV, 0, C.d, kl_pad, lds, kl_pad, ss);
+  float scl[NV];
 #pragma unroll
-      for (int r = 1; r < 4; r++)
-        if (lane == r) val = acc[0][r];
-      C.dbg_logits[(size_t)(src == 1 ? 1 : 0) * C.V + m0 + lane] = val;
-    }
+  for (int v = 0; v < NV; v++) {
+    const float tot = block_sum(ss[v], red);  // includes the barrier that publishes the staged rows
+    scl[v] = 1.0f / sqrtf(tot / (float)C.d + C.eps);
+  }
+  float bv[NV];
+  int bi[NV];
 #pragma unroll
-    for (int r = 0; r < 4; r++) {
-      if (m0 + r < C.V && better(acc[0][r], m0 + r, bv, bi)) {
-        bv = acc[0][r];
-        bi = m0 + r;
+  for (int v = 0; v < NV; v++) {
+    bv[v] = -INFINITY;
+    bi[v] = 0x7fffffff;
+  }
+  const bool dbg_row0 = C.debug && (src != 0 && src != 3 ? true : a == C.n);
+  for (int rg = 0; rg < RPW / 2; rg++) {
+    const int m0 = mw + rg * 2;
+    const WT* wr[2];
+    rows_of(m0, wr);
+    if (rg > 0) load_blocks<WT, 2>(wr, C.d, 0, nbk, lane, wv);
+    float acc[NV][2];
+#pragma unroll
+    for (int v = 0; v < NV; v++) acc[v][0] = acc[v][1] = 0.f;
+    accum_blocks<WT, NV, 2>(wr, C.d, 0, nbk, lds, kl_pad, NV, acc, wv, lane);
+#pragma unroll
+    for (int v = 0; v < NV; v++) {
+#pragma unroll
+      for (int r = 0; r < 2; r++) acc[v][r] = wave_sum(acc[v][r]) * scl[v];
+      if (C.debug && (v > 0 || dbg_row0) && lane < 2 && m0 + lane < C.V)
+        C.dbg_logits[(size_t)set[v] * C.V + m0 + lane] = lane == 0 ? acc[v][0] : acc[v][1];
+#pragma unroll
+      for (int r = 0; r < 2; r++) {
+        if (m0 + r < C.V && better(acc[v][r], m0 + r, bv[v], bi[v])) {
+          bv[v] = acc[v][r];
+          bi[v] = m0 + r;
+        }
       }
     }
   }
   if (lane == 0) {
-    s_v[w] = bv;
-    s_i[w] = bi;
+#pragma unroll
+    for (int v = 0; v < NV; v++) {
+      s_v[v][w] = bv[v];
+      s_i[v][w] = bi[v];
+    }
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    float v = s_v[0];
-    int i = s_i[0];
+  if (threadIdx.x < NV) {
+    const int v = threadIdx.x;
+    float fv = s_v[v][0];
+    int fi = s_i[v][0];
     for (int k = 1; k < 4; k++)
-      if (better(s_v[k], s_i[k], v, i)) {
-        v = s_v[k];
-        i = s_i[k];
+      if (better(s_v[v][k], s_i[v][k], fv, fi)) {
+        fv = s_v[v][k];
+        fi = s_i[v][k];
       }
-    C.b[set].hpart_v[blockIdx.x] = v;
-    C.b[set].hpart_i[blockIdx.x] = i;
+    C.b[set[v]].hpart_v[blockIdx.x] = fv;
+    C.b[set[v]].hpart_i[blockIdx.x] = fi;
   }
 }
 
@@ -622,12 +713,21 @@ __device__ int reduce_head(const BufSet& B, int tiles, int V) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   float v = -INFINITY;
   int i = 0x7fffffff;
-  for (int k = threadIdx.x; k < tiles; k += kWG) {
-    const float pv = B.hpart_v[k];
-    const int pi = B.hpart_i[k];
-    if (better(pv, pi, v, i)) {
-      v = pv;
-      i = pi;
+  for (int k0 = threadIdx.x; k0 < tiles; k0 += kWG * 4) {
+    float pv[4];
+    int pi[4];
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      const int k = k0 + j * kWG;
+      pv[j] = k < tiles ? B.hpart_v[k] : -INFINITY;
+      pi[j] = k < tiles ? B.hpart_i[k] : 0x7fffffff;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+      if (better(pv[j], pi[j], v, i)) {
+        v = pv[j];
+        i = pi[j];
+      }
     }
   }
 #pragma unroll
@@ -699,7 +799,7 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
   if (split >= nsplit) return;
   const int k0 = split * C.chunk, k1 = min(nkeys, k0 + C.chunk);
   const int nq = gr.nrows * G;
-  const LayerDesc& Ld = C.lay[gr.layer];
+  const LayerDesc Ld = layer_of(C, R, gr);
   const KVT* kvb = (const KVT*)Ld.kv;
   const size_t voff = (size_t)C.hkv * C.page * DH;
   const BufSet& B = C.b[R.set];
@@ -866,18 +966,18 @@ __device__ __forceinline__ float2 ld_dev2(const float* p) {  // p 8-byte aligned
 }
 
 // Decode attention of the stage launches: one query row per stage, G query heads per KV head.
-// Grid: x = split (chunk keys), y = KV head, z = stage. The K (registers) and V (LDS tile) loads of
-// the next 64-key pass are issued before the current pass is computed. The last split to finish of
-// each (stage, KV head) merges the partial (o, m, l) records: all (m, l) pairs are read at once, the
-// split weights exp(m - M) / L go to LDS, and the partial outputs are summed in split order with
-// their loads issued eight at a time.
+// Grid: x = split (chunk keys), y = KV head, z = stage. Thread t owns key t/4 of a 64-key pass and a
+// quarter of its head dimension, for K (registers) and V (LDS tile) alike, so one page-table lookup
+// serves both. The device state, the layer's KV base and the first pass's page are requested together
+// at entry (none depends on another); the next pass's loads are issued before the current pass is
+// computed. The last split to finish of each (stage, KV head) merges the partial (o, m, l) records:
+// all (m, l) pairs are read at once, the split weights exp(m - M) / L go to LDS, and the partial
+// outputs are summed in split order with their loads issued eight at a time.
 template <typename KVT, int DH>
 __global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
   constexpr int PASS = 64, TPK = 4, NE = DH / TPK, VE = Elt<KVT>::VE;
   constexpr int MAXQ = 8;
-  constexpr int KCH = NE / VE;                       // 16-byte K chunks per thread
-  constexpr int VCH = DH * (int)sizeof(KVT) / 16;    // 16-byte chunks per V row
-  constexpr int VPT = PASS * VCH / kWG;              // V chunks per thread per pass
+  constexpr int KCH = NE / VE;  // 16-byte chunks per thread for K and for V
   __shared__ float qs[MAXQ * DH];
   __shared__ float sc[MAXQ * PASS];
   __shared__ __align__(16) KVT vs[PASS * DH];
@@ -885,38 +985,41 @@ __global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
   __shared__ float s_pw[kMaxSplits * MAXQ];  // merge: m of each split, then its weight
   __shared__ float s_pl[kMaxSplits * MAXQ];
   __shared__ int s_last;
-  const Grp gr = resolve(C, R, blockIdx.z);
-  if (!gr.active) return;
-  const int g = blockIdx.y, split = blockIdx.x;
-  const int G = C.G;
-  const int nkeys = gr.pos0 + 1;
-  const int nsplit = (nkeys + C.chunk - 1) / C.chunk;
-  if (split >= nsplit) return;
-  const int k0 = split * C.chunk, k1 = min(nkeys, k0 + C.chunk);
-  const LayerDesc& Ld = C.lay[gr.layer];
-  const KVT* kvb = (const KVT*)Ld.kv;
-  const size_t voff = (size_t)C.hkv * C.page * DH;
-  const BufSet& B = C.b[R.set];
+  const int s = blockIdx.z, g = blockIdx.y, split = blockIdx.x;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int kk = tid / TPK, qq = tid % TPK;
-  // loads of one pass: rows past the chunk end re-read its last key so that every load is in
-  // bounds; only valid keys are used
-  uint4 kraw[KCH], vraw[VPT];
-  auto issue = [&](int kp) {
-    const int nk = min(PASS, k1 - kp);
-    const uint4* k4 = reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + min(kk, nk - 1), g, qq * NE));
+  const int k0 = split * C.chunk;
+  // independent requests first: state, layer KV base, page of this thread's first key
+  const int st_a = C.st->a, st_c = C.st->c;
+  const int layer = C.beta[s] + R.slot;
+  const KVT* kvb = (const KVT*)R.ld[s].kv;
+  int pg = C.page_table[min((k0 + kk) / C.page, C.max_pages - 1)];
+  if (s >= st_a || layer >= C.beta[s + 1]) return;  // stage idle in this slot
+  const int pos0 = st_c + st_a - 1 - s;             // the stage's token; it attends to keys [0, pos0]
+  const int nkeys = pos0 + 1;
+  const int nsplit = (nkeys + C.chunk - 1) / C.chunk;
+  if (split >= nsplit) return;
+  const int k1 = min(nkeys, k0 + C.chunk);
+  const int G = C.G;
+  const size_t page_elems = (size_t)2 * C.hkv * C.page * DH;
+  const size_t head_off = ((size_t)g * C.page) * DH;
+  const size_t voff = (size_t)C.hkv * C.page * DH;
+  const BufSet& B = C.b[R.set];
+  uint4 kraw[KCH], vraw[KCH];
+  auto issue = [&](int kp, int page) {
+    const int key = kp + kk;
+    if (key < k1) {
+      const KVT* base = kvb + (size_t)page * page_elems + head_off + (size_t)(key % C.page) * DH + qq * NE;
 #pragma unroll
-    for (int c4 = 0; c4 < KCH; c4++) kraw[c4] = ldg16(k4 + c4);
+      for (int c4 = 0; c4 < KCH; c4++) kraw[c4] = ldg16(reinterpret_cast<const uint4*>(base) + c4);
 #pragma unroll
-    for (int i = 0; i < VPT; i++) {
-      const int e = tid + i * kWG, vk = e / VCH, ch = e % VCH;
-      vraw[i] = ldg16(reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + min(vk, nk - 1), g, 0) + voff) + ch);
+      for (int c4 = 0; c4 < KCH; c4++) vraw[c4] = ldg16(reinterpret_cast<const uint4*>(base + voff) + c4);
     }
   };
-  issue(k0);
+  issue(k0, pg);
   for (int e = tid; e < G * DH; e += kWG) {
     const int qi = e / DH, dd = e % DH;
-    qs[qi * DH + dd] = B.q[(size_t)gr.brow0 * C.qdim + (g * G + qi) * DH + dd] * C.scale;
+    qs[qi * DH + dd] = B.q[(size_t)s * C.qdim + (g * G + qi) * DH + dd] * C.scale;
   }
   if (tid < MAXQ) {
     s_m[tid] = -INFINITY;
@@ -931,26 +1034,30 @@ __global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
   for (int u = 0; u < MAXU; u++) o0[u] = o1[u] = 0.f;
   for (int kp = k0; kp < k1; kp += PASS) {
     const int nk = min(PASS, k1 - kp);
-#pragma unroll
-    for (int i = 0; i < VPT; i++) {  // rows past the chunk end hold copies and are never read
-      const int e = tid + i * kWG, vk = e / VCH, ch = e % VCH;
-      reinterpret_cast<uint4*>(vs + vk * DH)[ch] = vraw[i];
-    }
     float kr[NE];
+    if (kk < nk) {
 #pragma unroll
-    for (int c4 = 0; c4 < KCH; c4++) unpack16<KVT>(kraw[c4], kr + c4 * VE);
-    if (kp + PASS < k1) issue(kp + PASS);
+      for (int c4 = 0; c4 < KCH; c4++) reinterpret_cast<uint4*>(vs + kk * DH + qq * NE)[c4] = vraw[c4];
+#pragma unroll
+      for (int c4 = 0; c4 < KCH; c4++) unpack16<KVT>(kraw[c4], kr + c4 * VE);
+    }
+    if (kp + PASS < k1) {
+      const int nkey = kp + PASS + kk;
+      issue(kp + PASS, C.page_table[min(nkey, k1 - 1) / C.page]);
+    }
     __syncthreads();  // q staged (first pass), V tile written
     for (int qi = 0; qi < G; qi++) {
       float dsum = 0.f;
-      const float* qv = qs + qi * DH + qq * NE;
+      if (kk < nk) {
+        const float* qv = qs + qi * DH + qq * NE;
 #pragma unroll
-      for (int e = 0; e < NE; e += 4) {
-        const float4 q4 = *reinterpret_cast<const float4*>(qv + e);
-        dsum = fmaf(q4.x, kr[e], dsum);
-        dsum = fmaf(q4.y, kr[e + 1], dsum);
-        dsum = fmaf(q4.z, kr[e + 2], dsum);
-        dsum = fmaf(q4.w, kr[e + 3], dsum);
+        for (int e = 0; e < NE; e += 4) {
+          const float4 q4 = *reinterpret_cast<const float4*>(qv + e);
+          dsum = fmaf(q4.x, kr[e], dsum);
+          dsum = fmaf(q4.y, kr[e + 1], dsum);
+          dsum = fmaf(q4.z, kr[e + 2], dsum);
+          dsum = fmaf(q4.w, kr[e + 3], dsum);
+        }
       }
       dsum += __shfl_xor(dsum, 1, 64);
       dsum += __shfl_xor(dsum, 2, 64);
@@ -982,22 +1089,32 @@ __global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
         o1[u] *= al;
       }
     }
-    for (int k2 = 0; k2 < nk; k2++) {
-      const float v0 = ld1<KVT>(vs, (size_t)k2 * DH + 2 * dp);
-      const float v1 = ld1<KVT>(vs, (size_t)k2 * DH + 2 * dp + 1);
+    // P.V: eight keys' V pairs and probabilities are read from LDS together (rows >= nk of the
+    // tile hold stale values and are skipped), then accumulated in key order
+    for (int k2 = 0; k2 < nk; k2 += 8) {
+      float2 vv[8];
+#pragma unroll
+      for (int j = 0; j < 8; j++) vv[j] = ld2<KVT>(vs + (size_t)(k2 + j) * DH + 2 * dp);
 #pragma unroll
       for (int u = 0; u < MAXU; u++) {
         const int qi = qg + u * NG;
         if (qi < G) {
-          const float p = sc[qi * PASS + k2];
-          o0[u] = fmaf(p, v0, o0[u]);
-          o1[u] = fmaf(p, v1, o1[u]);
+          float pp[8];
+#pragma unroll
+          for (int j = 0; j < 8; j++) pp[j] = sc[qi * PASS + k2 + j];
+#pragma unroll
+          for (int j = 0; j < 8; j++) {
+            if (k2 + j < nk) {
+              o0[u] = fmaf(pp[j], vv[j].x, o0[u]);
+              o1[u] = fmaf(pp[j], vv[j].y, o1[u]);
+            }
+          }
         }
       }
     }
     __syncthreads();
   }
-  float* out = B.ao + (size_t)gr.brow0 * C.qdim + g * G * DH;
+  float* out = B.ao + (size_t)s * C.qdim + g * G * DH;
   if (nsplit == 1) {
 #pragma unroll
     for (int u = 0; u < MAXU; u++) {
@@ -1011,7 +1128,7 @@ __global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
     return;
   }
   constexpr int RS = MAXQ * (DH + 2);
-  const int cidx = blockIdx.z * C.hkv + g;
+  const int cidx = s * C.hkv + g;
   float* rec = B.part + ((size_t)cidx * C.max_splits + split) * RS;
 #pragma unroll
   for (int u = 0; u < MAXU; u++) {
@@ -1142,7 +1259,7 @@ template <typename WT>
 __global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int auto_rb) {
   __shared__ int s_tok, s_pos;
   DevState* st = C.st;
-  const int tiles = (C.V + 4 * kHeadRowsPerWave - 1) / (4 * kHeadRowsPerWave);
+  const int tiles = (C.V + kHeadRows - 1) / kHeadRows;
   const int y_all = (st->a == C.n) ? reduce_head(C.b[0], tiles, C.V) : -1;
   const int pd_all = reduce_head(C.b[1], tiles, C.V);
   if (threadIdx.x == 0) {
@@ -1216,7 +1333,7 @@ template <typename WT>
 __global__ __launch_bounds__(kWG) void k_reseed(Ctx C, int keep, int tok, int prompt_len) {
   __shared__ int s_tok;
   DevState* st = C.st;
-  const int yv = tok >= 0 ? tok : reduce_head(C.b[0], (C.V + 4 * kHeadRowsPerWave - 1) / (4 * kHeadRowsPerWave), C.V);
+  const int yv = tok >= 0 ? tok : reduce_head(C.b[0], (C.V + kHeadRows - 1) / kHeadRows, C.V);
   if (threadIdx.x == 0) {
     const int t = yv;
     if (tok < 0) st->y = t;
@@ -1238,6 +1355,22 @@ __global__ __launch_bounds__(kWG) void k_reseed(Ctx C, int keep, int tok, int pr
 // -------------------------------------------------------------------------------- launchers
 static inline hipStream_t S(void* s) { return (hipStream_t)s; }
 
+// Timing events for the next launches of this host thread (null: plain launches). A timed launch
+// hands the events to the dispatch itself, so they hold the kernel's own start and end times.
+static thread_local hipEvent_t t_ev_start = nullptr, t_ev_stop = nullptr;
+void set_launch_events(void* start, void* stop) {
+  t_ev_start = (hipEvent_t)start;
+  t_ev_stop = (hipEvent_t)stop;
+}
+
+template <typename F, typename... Args>
+static void launch_k(F kernel, dim3 grid, dim3 block, size_t shmem, hipStream_t s, Args... args) {
+  if (t_ev_start != nullptr)
+    hipExtLaunchKernelGGL(kernel, grid, block, (std::uint32_t)shmem, s, t_ev_start, t_ev_stop, 0u, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+}
+
 template <typename WT>
 static inline size_t gemv_lds(int K, int nv) {
   constexpr int BLK = 64 * Elt<WT>::VE;
@@ -1248,46 +1381,46 @@ static inline size_t gemv_lds(int K, int nv) {
 
 template <typename WT>
 void Launch<WT>::qkv(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid((c.hq + 2 * c.hkv) * (c.dh / 16), r.kind == 0 ? c.n : 1);
+  const dim3 grid((c.hq + 2 * c.hkv) * (c.dh / 8), r.kind == 0 ? c.n : 1);
   if (r.kind == 0)
-    hipLaunchKernelGGL((k_qkv<WT, 1>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, r);
+    launch_k((k_qkv<WT, 1>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, r);
   else
-    hipLaunchKernelGGL((k_qkv<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
+    launch_k((k_qkv<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::oproj(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid((c.d + 15) / 16, r.kind == 0 ? c.n : 1);
+  const dim3 grid((c.d + 7) / 8, r.kind == 0 ? c.n : 1);
   if (r.kind == 0)
-    hipLaunchKernelGGL((k_proj_add<WT, 1, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, 1), S(s), c, r);
+    launch_k((k_proj_add<WT, 1, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, 1), S(s), c, r);
   else
-    hipLaunchKernelGGL((k_proj_add<WT, kMaxRows, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, kMaxRows), S(s), c, r);
+    launch_k((k_proj_add<WT, kMaxRows, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, kMaxRows), S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::down(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid((c.d + 15) / 16, r.kind == 0 ? c.n : 1);
+  const dim3 grid((c.d + 7) / 8, r.kind == 0 ? c.n : 1);
   if (r.kind == 0)
-    hipLaunchKernelGGL((k_proj_add<WT, 1, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, 1), S(s), c, r);
+    launch_k((k_proj_add<WT, 1, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, 1), S(s), c, r);
   else
-    hipLaunchKernelGGL((k_proj_add<WT, kMaxRows, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, kMaxRows), S(s), c, r);
+    launch_k((k_proj_add<WT, kMaxRows, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, kMaxRows), S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::gateup(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid((c.F + 7) / 8, r.kind == 0 ? c.n : 1);
+  const dim3 grid((c.F + 3) / 4, r.kind == 0 ? c.n : 1);
   if (r.kind == 0)
-    hipLaunchKernelGGL((k_gateup<WT, 1>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, r);
+    launch_k((k_gateup<WT, 1>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, r);
   else
-    hipLaunchKernelGGL((k_gateup<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
+    launch_k((k_gateup<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
 }
 
 template <typename WT, int MAXQ, int DH>
 static void attn_launch(const Ctx& c, const Rows& r, void* s) {
   const dim3 grid(c.max_splits, c.hkv, r.kind == 0 ? c.n : 1);
-  hipLaunchKernelGGL((k_attn<WT, MAXQ, DH>), grid, dim3(kWG), (attn_lds<WT, MAXQ, DH>()), S(s), c, r);
+  launch_k((k_attn<WT, MAXQ, DH>), grid, dim3(kWG), (attn_lds<WT, MAXQ, DH>()), S(s), c, r);
   const dim3 cgrid(c.hkv, r.kind == 0 ? c.n : 1);
-  hipLaunchKernelGGL((k_attn_combine<MAXQ, DH>), cgrid, dim3(kWG), 0, S(s), c, r);
+  launch_k((k_attn_combine<MAXQ, DH>), cgrid, dim3(kWG), 0, S(s), c, r);
 }
 
 template <typename WT>
@@ -1295,9 +1428,9 @@ void Launch<WT>::attn(const Ctx& c, const Rows& r, void* s) {
   if (r.kind == 0) {
     const dim3 grid(c.max_splits, c.hkv, c.n);
     if (c.dh == 128)
-      hipLaunchKernelGGL((k_attn_dec<WT, 128>), grid, dim3(kWG), 0, S(s), c, r, c.b[r.set].cnt);
+      launch_k((k_attn_dec<WT, 128>), grid, dim3(kWG), 0, S(s), c, r, c.b[r.set].cnt);
     else
-      hipLaunchKernelGGL((k_attn_dec<WT, 64>), grid, dim3(kWG), 0, S(s), c, r, c.b[r.set].cnt);
+      launch_k((k_attn_dec<WT, 64>), grid, dim3(kWG), 0, S(s), c, r, c.b[r.set].cnt);
     return;
   }
   if (c.dh == 128)
@@ -1308,19 +1441,24 @@ void Launch<WT>::attn(const Ctx& c, const Rows& r, void* s) {
 
 template <typename WT>
 void Launch<WT>::pdm_fc(const Ctx& c, int prefill, int nrows, void* s) {
-  const dim3 grid((c.d + 15) / 16);
-  hipLaunchKernelGGL((k_pdm_fc<WT>), grid, dim3(kWG), gemv_lds<WT>(c.n * c.d, kMaxRows), S(s), c, prefill, nrows);
+  const dim3 grid((c.d + 7) / 8);
+  launch_k((k_pdm_fc<WT>), grid, dim3(kWG), gemv_lds<WT>(c.n * c.d, kMaxRows), S(s), c, prefill, nrows);
 }
 
 template <typename WT>
 void Launch<WT>::head(const Ctx& c, int src, int row, void* s) {
-  const dim3 grid((c.V + 4 * kHeadRowsPerWave - 1) / (4 * kHeadRowsPerWave));
-  hipLaunchKernelGGL((k_head<WT>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, src, row, src == 1 ? 1 : 0);
+  const dim3 grid((c.V + kHeadRows - 1) / kHeadRows);
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  const size_t kl_pad = (size_t)(c.d + BLK - 1) / BLK * BLK;
+  if (src == 3)
+    launch_k((k_head<WT, 2>), grid, dim3(kWG), 2 * kl_pad * sizeof(float), S(s), c, src, row);
+  else
+    launch_k((k_head<WT, 1>), grid, dim3(kWG), kl_pad * sizeof(float), S(s), c, src, row);
 }
 
 template <typename WT>
 void Launch<WT>::embed_rows(const Ctx& c, int t0, int nrows, void* s) {
-  hipLaunchKernelGGL((k_embed_rows<WT>), dim3(nrows), dim3(kWG), 0, S(s), c, t0, nrows);
+  launch_k((k_embed_rows<WT>), dim3(nrows), dim3(kWG), 0, S(s), c, t0, nrows);
 }
 
 template struct Launch<float>;
@@ -1328,16 +1466,16 @@ template struct Launch<uint16_t>;
 
 void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* s, int bf16) {
   if (bf16)
-    hipLaunchKernelGGL((k_verify<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
+    launch_k((k_verify<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
   else
-    hipLaunchKernelGGL((k_verify<float>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
+    launch_k((k_verify<float>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
 }
 
 void launch_reseed(const Ctx& c, int keep, int tok, int prompt_len, void* s, int bf16) {
   if (bf16)
-    hipLaunchKernelGGL((k_reseed<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
+    launch_k((k_reseed<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
   else
-    hipLaunchKernelGGL((k_reseed<float>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
+    launch_k((k_reseed<float>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
 }
 
 }  // namespace spd

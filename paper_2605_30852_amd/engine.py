@@ -16,7 +16,7 @@ from . import binding as B
 
 def make_config(shape: synth.ModelShape, max_tokens: int, n: Optional[int] = None,
                 pdm_layers: Optional[int] = None, auto_rollback: bool = True, attn_chunk: int = 0,
-                page_seed: int = 0) -> B.spd_config:
+                page_seed: int = 0, fused_head: bool = True) -> B.spd_config:
     c = B.spd_config()
     c.n_layers = shape.n_layers
     c.d_model = shape.d_model
@@ -35,6 +35,7 @@ def make_config(shape: synth.ModelShape, max_tokens: int, n: Optional[int] = Non
     c.auto_rollback = 1 if auto_rollback else 0
     c.attn_chunk = attn_chunk
     c.page_seed = page_seed
+    c.fused_head = 1 if fused_head else 0
     return c
 
 
@@ -107,14 +108,14 @@ class Engine:
 
     def __init__(self, weights: DeviceWeights, max_tokens: int, n: Optional[int] = None,
                  pdm_layers: Optional[int] = None, auto_rollback: bool = True, attn_chunk: int = 0,
-                 page_seed: int = 0, device="cuda"):
+                 page_seed: int = 0, fused_head: bool = True, device="cuda"):
         if not torch.cuda.is_available():
             raise RuntimeError("Engine needs a GPU: the SPD step has no CPU path")
         n = weights.shape.n_stages if n is None else n
         self.w = weights.pdm_for_width(n, pdm_layers, device)
         self.shape = self.w.shape
         self.cfg = make_config(self.shape, max_tokens, n=n, auto_rollback=auto_rollback,
-                               attn_chunk=attn_chunk, page_seed=page_seed)
+                               attn_chunk=attn_chunk, page_seed=page_seed, fused_head=fused_head)
         self.n = n
         nbytes = B.spd_workspace_size(self.cfg)
         self.ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)

@@ -54,29 +54,30 @@ def test_tiny_fp32_lockstep_forced(tiny_w, n):
     assert w["hidden"] < 1e-4  # fp32 weights and KV: only summation order differs
 
 
-@pytest.mark.parametrize("n", [2])
-def test_tiny_fp32_lockstep_natural_drafts(tiny_w, n):
-    _say(f"[tiny lockstep natural n={n}]")
+@pytest.mark.parametrize("n,fused", [(2, True), (2, False)])
+def test_tiny_fp32_lockstep_natural_drafts(tiny_w, n, fused):
+    _say(f"[tiny lockstep natural n={n} fused_head={fused}]")
     sh = synth.TINY
     model = om.Model(sh, SEED)
     prompt = synth.prompt(sh, SEED, 20)
-    eng = _engine(tiny_w, n)
+    eng = _engine(tiny_w, n, fused_head=fused)
     w = run_lockstep(eng, model, prompt, 16)
     eng.close()
     assert w["steps"] >= 8 or w["near_tie"]
 
 
-@pytest.mark.parametrize("n", [1, 3])
-def test_mid_bf16_lockstep(mid_w, n):
-    """bf16 weights and KV, ragged FFN (1000) and vocabulary (3001), chunked attention splits."""
-    _say(f"[mid lockstep n={n}]")
+@pytest.mark.parametrize("n,fused", [(1, True), (3, True), (3, False)])
+def test_mid_bf16_lockstep(mid_w, n, fused):
+    """bf16 weights and KV, ragged FFN (1000) and vocabulary (3001), chunked attention splits; the
+    draft module's LM head fused with the exit pass or run as its own pass."""
+    _say(f"[mid lockstep n={n} fused_head={fused}]")
     sh = synth.MID
     model = om.Model(sh, SEED)
     prompt = synth.prompt(sh, SEED, 75)
     ref = om.ar_greedy(model, prompt, 24)
     mask = synth.accept_mask(0.6, SEED + 1, 300)
     tab = forced_table(ref, mask, len(prompt), sh.vocab)
-    eng = _engine(mid_w, n, max_tokens=200, attn_chunk=32)
+    eng = _engine(mid_w, n, max_tokens=200, attn_chunk=32, fused_head=fused)
     w = run_lockstep(eng, model, prompt, 20, draft_for=lambda q: tab.get(q))
     eng.close()
     assert w["steps"] >= 8 or w["near_tie"]
