@@ -51,6 +51,20 @@ def layer_bytes(sh, esz):
     return (qd * d + 2 * kvd * d + d * qd + 3 * F * d) * esz + 2 * d * 4
 
 
+def step_kernel_bytes(sh, n, c, esz):
+    """Algorithmic bytes of one steady-state persistent step launch (all n stages active, the step
+    starting with c committed positions): every layer's weights and norm gains once, each stage's KV
+    read over its own length, the new K/V written, and the activations each sublayer reads and writes
+    (per stage and layer: x in/out for the two norms and two residual adds, q, attention output and
+    the SwiGLU activation, all fp32)."""
+    d, F, qd, kvd, L = sh.d_model, sh.ffn_dim, sh.q_dim, sh.kv_dim, sh.n_layers
+    kv_tok = 2 * kvd * esz
+    beta = [s * L // n for s in range(n + 1)]
+    kv_read = sum((beta[s + 1] - beta[s]) * (c + n - s) * kv_tok for s in range(n))
+    act = L * 4 * (6 * d + 2 * qd + 2 * F)
+    return L * layer_bytes(sh, esz) + kv_read + L * kv_tok + act
+
+
 def launch_bytes(sh, n, c, esz):
     """Algorithmic bytes of one steady-state launch of each stage-batched kernel class (all n stages
     active), starting the step with c committed positions: weights once, activations in and out."""
@@ -66,6 +80,7 @@ def launch_bytes(sh, n, c, esz):
         "gateup": n * (2 * F * d * esz + 2 * d * 4 + F * 4),
         "down": n * (d * F * esz + F * 4 + 2 * d * 4),
         "head": V * d * esz + 2 * d * 4,  # one pass; the fused form adds only a second activation row
+        "step": step_kernel_bytes(sh, n, c, esz),
         "_beta": beta,
     }
 
@@ -142,6 +157,11 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="issue every launch instead of replaying the step graph")
     ap.add_argument("--separate-head", action="store_true",
                     help="the draft module runs its own LM-head pass on its stream instead of sharing the exit pass")
+    ap.add_argument("--step-mode", type=int, default=2, choices=[0, 1, 2, 3],
+                    help="stage compute: 0 five launches per layer slot covering all stages, 1 one persistent "
+                         "launch per step, 2 (default) one stream per stage, 3 skewed launches, each mixing "
+                         "independent sublayers of different stages")
+    ap.add_argument("--step-grid", type=int, default=0, help="workgroups of the persistent step launch (0: default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (the known-size kernel for HBM counter scaling)")
     args = ap.parse_args()
@@ -191,7 +211,9 @@ def main():
     # plain greedy decoding (n = 1 through the same library): reference tokens and AR tokens/s
     t0 = time.time()
     fused = not args.separate_head
+    mode = args.step_mode
     ar = Engine(weights, max_tokens=max_tokens, n=1, attn_chunk=attn_chunk, fused_head=fused)
+    ar.spd_set_step_kernel(mode, args.step_grid)
     ar.spd_set_graph(not args.no_graph)
     first = ar.spd_prefill(prompt)
     log(f"[bench] AR prefill {P} tokens in {time.time() - t0:.1f}s")
@@ -209,6 +231,7 @@ def main():
     # SPD handle, all drafts forced to the greedy tokens: every step after the fill is a full step
     t0 = time.time()
     eng = Engine(weights, max_tokens=max_tokens, n=n, attn_chunk=attn_chunk, fused_head=fused)
+    eng.spd_set_step_kernel(mode, args.step_grid)
     eng.spd_set_graph(not args.no_graph)
     f2 = eng.spd_prefill(prompt)
     assert f2 == first
@@ -235,13 +258,14 @@ def main():
     log(f"[bench] SPD n={n}: {us_step:.1f} us/step, {bytes_step / 1e9:.3f} GB/step, {gbs:.0f} GB/s "
         f"({100 * gbs / PEAK_HBM_GBS:.1f}% of {PEAK_HBM_GBS:.0f})")
 
-    # per-kernel HIP-event timing on the main stream, steady state (every step accepts)
-    # launches of the slots after the draft module's span (it ends within the first slots), so that
-    # a kernel is timed without the side stream sharing HBM, as a profiler's serialised trace sees it
-    first_slot = (L_slots := max(sh.n_layers // n + (1 if sh.n_layers % n else 0), 1)) // 2
+    # per-kernel HIP-event timing on the main stream, steady state (every step accepts). With
+    # sublayer launches only the slots after the draft module's span are timed, so that a kernel is
+    # timed without the side stream sharing HBM; the persistent launch covers the whole step.
+    L_slots = max(sh.n_layers // n + (1 if sh.n_layers % n else 0), 1)
+    first_slot = L_slots // 2 if mode in (0, 2) else 0
 
     def time_class(kid, steps):
-        B.spd_set_kernel_timing(eng.h, kid, first_slot)
+        B.spd_set_kernel_timing(eng.h, kid, first_slot if kid != B.SPD_K_HEAD else 0)
         ca, _, _, _ = eng.state()
         eng.spd_run_steps(steps)
         eng.spd_sync()
@@ -249,20 +273,34 @@ def main():
         B.spd_set_kernel_timing(eng.h, 0)
         cb, ab, _, _ = eng.state()
         assert cb - ca == steps and ab == n, "kernel timing left the steady state"
+        assert nl > 0, "no launch of the timed class"
         return ms, nl, (ca + cb) // 2
 
     kernels = {}
-    classes = (("qkv", B.SPD_K_QKV), ("attn", B.SPD_K_ATTN), ("oproj", B.SPD_K_OPROJ),
-               ("gateup", B.SPD_K_GATEUP), ("down", B.SPD_K_DOWN), ("head", B.SPD_K_HEAD))
+    if mode == 1:
+        classes = (("step", B.SPD_K_STEP), ("head", B.SPD_K_HEAD))
+        dominant = "step"
+    elif mode == 3:
+        classes = (("mix", B.SPD_K_MIX), ("head", B.SPD_K_HEAD))
+        dominant = "mix"
+    else:
+        classes = (("qkv", B.SPD_K_QKV), ("attn", B.SPD_K_ATTN), ("oproj", B.SPD_K_OPROJ),
+                   ("gateup", B.SPD_K_GATEUP), ("down", B.SPD_K_DOWN), ("head", B.SPD_K_HEAD))
+        dominant = "gateup"
     for kname, kid in classes:
-        steps = K_GU if kname == "gateup" else K_CLS
+        steps = K_GU if kname == dominant else K_CLS
         ms, nl, cm = time_class(kid, steps)
-        lb = launch_bytes(sh, n, cm, esz)[kname]
+        if kname == "mix":  # the launches of a step together stream what one persistent launch does
+            lb = launch_bytes(sh, n, cm, esz)["step"] / (nl / steps)
+        else:
+            lb = launch_bytes(sh, n, cm, esz)[kname]
+        if mode == 2 and kname not in ("head", "step"):
+            lb = lb / n  # each launch covers one stage
         us = 1e3 * ms / max(1, nl)
         kernels[kname] = {"us_per_launch": round(us, 2), "timed_launches_per_step": nl / steps,
                           "bytes_per_launch": int(lb), "GBps": round(lb / (us * 1e-6) / 1e9, 1)}
     log(f"[bench] kernels: {kernels}")
-    gu = kernels["gateup"]
+    dk = kernels[dominant]
 
     # PDM overlap: step start -> end of the stage compute (main) and -> end of the PDM (side stream)
     B.spd_set_kernel_timing(eng.h, B.SPD_K_SPANS)
@@ -327,14 +365,23 @@ def main():
                    "n": n, "prompt": P, "pdm_layers": sh.pdm_layers, "batch": 1,
                    "max_tokens": max_tokens, "attn_chunk": attn_chunk,
                    "lm_head": "one two-row pass shared by exit and draft" if fused else "separate passes",
-                   "step_graph": not args.no_graph},
+                   "step_graph": not args.no_graph,
+                   "stage_compute": {0: "five launches per layer slot covering all stages",
+                                     1: "one persistent launch per step",
+                                     2: "one stream per stage, five launches per layer slot",
+                                     3: "skewed schedule: 5J+n-1 launches, launch L runs sublayer L-s of stage s"}[mode],
+                   "step_grid": args.step_grid or None},
         "bytes_per_step": int(bytes_step),
         "step_GBps": round(gbs, 1),
         "step_roofline_frac": round(gbs / PEAK_HBM_GBS, 4),
-        "roofline": {"bound": "hbm", "achieved": gu["GBps"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(gu["GBps"] / PEAK_HBM_GBS, 4), "traffic": traffic_from_profile(),
-                     "kernel": "k_gateup<bf16,1>: grouped gate/up GEMV + SwiGLU over the n stages",
-                     "bytes_per_launch": gu["bytes_per_launch"], "us_per_launch": gu["us_per_launch"],
+        "roofline": {"bound": "hbm", "achieved": dk["GBps"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(dk["GBps"] / PEAK_HBM_GBS, 4), "traffic": traffic_from_profile(dominant),
+                     "kernel": {0: "k_sgemv gate/up: grouped gate/up GEMV + SwiGLU over the n stages",
+                                1: "k_step: the persistent launch running every layer slot of all n stages",
+                                2: "k_sgemv gate/up of one stage (stage streams run concurrently)",
+                                3: "k_mix: the skewed launches of the stage compute (all layers' weights and KV; "
+                                   "bytes and time summed over the launches of a step)"}[mode],
+                     "bytes_per_launch": dk["bytes_per_launch"], "us_per_launch": dk["us_per_launch"],
                      "timing": f"dispatch-recorded HIP events on the main stream, layer slots >= {first_slot} of "
                                f"{L_slots}, {K_GU} steady-state steps"},
         "kernels": kernels,
@@ -346,12 +393,13 @@ def main():
     print(json.dumps(out), flush=True)
 
 
-def traffic_from_profile():
+def traffic_from_profile(dominant):
     """HBM bytes per launch of the dominant kernel from committed rocprofv3 counter runs, or None
     when the counters were taken on other kernel sources than the ones built now."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "gateup_4b_n4_traffic.txt")
-    src = os.path.join(ROOT, "paper_2605_30852_amd", "csrc", "spd_kernels.hip")
+    path = os.path.join(ROOT, "profiles", f"{dominant}_4b_n4_traffic.txt")
+    src = os.path.join(ROOT, "paper_2605_30852_amd", "csrc",
+                       "spd_step.hip" if dominant == "step" else "spd_kernels.hip")
     if not os.path.exists(path):
         return None
     kv = {}

@@ -177,7 +177,12 @@ spd_status spd_sync(spd_handle* h, spd_step_result* last);
  *   SPD_DBG_PDM_LOGITS:  V fp32, the PDM's logits of the last step (needs spd_set_debug)
  *   SPD_DBG_TOKENS:      max_tokens int32, token id per position
  *   SPD_DBG_STATE:       4 int32: c, a, prompt_len, steps
- * bytes must equal the size listed. */
+ *   SPD_DBG_STEP_ITEMS:  nitems uint32, the persistent step launch's tile of each ticket:
+ *                        phase p = item >> 19 (layer slot p / 5, sublayer p % 5 in the order QKV,
+ *                        attention, O-proj, gate/up, down), stage (item >> 16) & 7, tile item & 0xffff
+ *   SPD_DBG_STEP_TRACE:  nitems x 4 uint64 wall-clock stamps per ticket of the last traced step
+ *                        (spd_set_step_trace): start, inputs ready, input staged, end (0: not reached)
+ * bytes must equal the size listed (nitems from spd_step_plan_info). */
 enum {
   SPD_DBG_RESID = 1,
   SPD_DBG_ANCHORS = 2,
@@ -185,7 +190,9 @@ enum {
   SPD_DBG_EXIT_LOGITS = 4,
   SPD_DBG_PDM_LOGITS = 5,
   SPD_DBG_TOKENS = 6,
-  SPD_DBG_STATE = 7
+  SPD_DBG_STATE = 7,
+  SPD_DBG_STEP_ITEMS = 8,
+  SPD_DBG_STEP_TRACE = 9
 };
 spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes);
 
@@ -199,19 +206,52 @@ spd_status spd_read_kv(spd_handle* h, int32_t pdm, int32_t layer, int32_t pos0, 
  * sequence does not depend on host state, so one capture serves every step. */
 spd_status spd_set_graph(spd_handle* h, int32_t on);
 
+/* How the stage compute of a step is launched (Section 3.1: every active stage advances its token by
+ * one stage). All modes give bit-identical results (the per-row arithmetic is the same).
+ *   mode 0: five launches per layer slot (QKV, attention, O-proj, gate/up, down) on main_stream, each
+ *           covering all stages.
+ *   mode 1: one persistent launch per step runs every layer slot of every stage; its `grid`
+ *           workgroups (0: 512) take tiles from a ticket counter in a fixed order and each tile waits
+ *           (bounded) only for the previous sublayer of its own stage. skew orders the tiles: 0 keeps
+ *           the stages' sublayers in lockstep, k > 0 staggers stage s by k*s sublayers, -1 keeps the
+ *           current order. If a wait ever timed out, the next call that reads the step result returns
+ *           SPD_E_HIP.
+ *   mode 2 (default): stage s runs its own chain of five launches per layer slot on its own stream
+ *           (the library's, default priority), forked from and joined to main_stream, so that one
+ *           stage's attention and launch tails can overlap the other stages' weight streaming.
+ *   mode 3: a skewed schedule on main_stream: launch L runs sublayer L - s (in the order
+ *           QKV, attention, O-proj, gate/up, down of each layer slot) of every stage s, 5J + n - 1
+ *           launches per step. The parts of a launch belong to different stages and are independent,
+ *           so one stage's latency-bound attention runs under the others' weight streaming and every
+ *           launch streams several stages' worth of weights.
+ * In modes 0, 2 and 3 `grid` sets the workgroups of one sublayer launch, or of the weight-streaming
+ * parts of one mixed launch (0: the default): each stages its input vector once and its waves stream
+ * their weight rows back to back.
+ * SPD_K_STEP times the persistent launch, SPD_K_MIX the launches of mode 3; the per-sublayer timing
+ * classes time modes 0 and 2. */
+spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t skew);
+
+/* Tracing of the persistent step launch: while on, every tile records four wall-clock stamps (for
+ * SPD_DBG_STEP_TRACE; each step overwrites them). Costs a few stores per tile. */
+spd_status spd_set_step_trace(spd_handle* h, int32_t on);
+
+/* info (host, 8 int32): number of tickets of one step, layer slots J, tiles per stage of QKV,
+ * attention, O-proj, gate/up and down, and the wall-clock rate of the trace stamps in kHz. */
+spd_status spd_step_plan_info(spd_handle* h, int32_t* info);
+
 /* 1: every LM-head pass also writes its full logits (for SPD_DBG_*_LOGITS). */
 spd_status spd_set_debug(spd_handle* h, int32_t on);
 
 /* Kernel timing for roofline measurements. kernel selects one launch class of the stage compute on
- * main_stream (SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD; 0 turns timing
- * off). While on, steps issue their launches (no graph replay) and every launch of that class in layer
+ * main_stream (SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN in step-kernel mode 0;
+ * SPD_K_STEP, the persistent launch, in mode 1; SPD_K_HEAD; 0 turns timing off). While on, steps issue their launches (no graph replay) and every launch of that class in layer
  * slot >= first_slot (the exit head counts as the slot after the last) hands two HIP events to its own
  * dispatch, which records the kernel's start and end on main_stream. A first_slot past the draft
  * module's span times the kernel without the side stream competing for memory bandwidth.
  * spd_kernel_timing waits for the stream, returns the summed kernel time in milliseconds and the
  * number of timed launches, and clears both. */
 enum { SPD_K_QKV = 1, SPD_K_ATTN = 2, SPD_K_OPROJ = 3, SPD_K_GATEUP = 4, SPD_K_DOWN = 5, SPD_K_HEAD = 6,
-       SPD_K_SPANS = 7 };
+       SPD_K_SPANS = 7, SPD_K_STEP = 8, SPD_K_MIX = 9 };
 spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel, int32_t first_slot);
 spd_status spd_kernel_timing(spd_handle* h, double* total_ms, int32_t* launches);
 

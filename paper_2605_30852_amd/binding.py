@@ -17,7 +17,9 @@ SPD_F32, SPD_BF16 = 0, 1
 SPD_NONE, SPD_ACCEPT, SPD_REJECT = 0, 1, 2
 SPD_DBG_RESID, SPD_DBG_ANCHORS, SPD_DBG_PDM_HIDDEN = 1, 2, 3
 SPD_DBG_EXIT_LOGITS, SPD_DBG_PDM_LOGITS, SPD_DBG_TOKENS, SPD_DBG_STATE = 4, 5, 6, 7
-SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD, SPD_K_SPANS = 1, 2, 3, 4, 5, 6, 7
+SPD_DBG_STEP_ITEMS, SPD_DBG_STEP_TRACE = 8, 9
+SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD, SPD_K_SPANS, SPD_K_STEP = 1, 2, 3, 4, 5, 6, 7, 8
+SPD_K_MIX = 9
 
 
 class spd_config(ct.Structure):
@@ -57,7 +59,8 @@ EXPORTS = [
     "spd_workspace_size", "spd_stage_bounds", "spd_init", "spd_prefill", "spd_step", "spd_rollback",
     "spd_set_forced_drafts", "spd_clear_forced_drafts", "spd_run_steps", "spd_sync", "spd_read_debug",
     "spd_read_kv", "spd_set_debug", "spd_destroy", "spd_status_str", "spd_last_error",
-    "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing",
+    "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing", "spd_set_step_kernel",
+    "spd_set_step_trace", "spd_step_plan_info",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -95,6 +98,9 @@ def lib() -> ct.CDLL:
             "spd_set_debug": (I, [P, I]),
             "spd_set_kernel_timing": (I, [P, I, I]),
             "spd_set_graph": (I, [P, I]),
+            "spd_set_step_kernel": (I, [P, I, I, I]),
+            "spd_set_step_trace": (I, [P, I]),
+            "spd_step_plan_info": (I, [P, ct.POINTER(ct.c_int32)]),
             "spd_kernel_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
             "spd_span_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_double),
                                     ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
@@ -226,6 +232,29 @@ def spd_span_timing(h: int):
 
 def spd_set_graph(h: int, on: bool) -> None:
     _check("spd_set_graph", lib().spd_set_graph(h, 1 if on else 0), h)
+
+
+def spd_set_step_kernel(h: int, mode: int, grid: int = 0, skew: int = -1) -> None:
+    _check("spd_set_step_kernel", lib().spd_set_step_kernel(h, int(mode), int(grid), int(skew)), h)
+
+
+def spd_set_step_trace(h: int, on: bool) -> None:
+    _check("spd_set_step_trace", lib().spd_set_step_trace(h, 1 if on else 0), h)
+
+
+def spd_step_plan_info(h: int) -> dict:
+    info = (ct.c_int32 * 8)()
+    _check("spd_step_plan_info", lib().spd_step_plan_info(h, info), h)
+    return {"nitems": info[0], "J": info[1], "tiles": list(info[2:7]), "clock_khz": info[7]}
+
+
+def spd_step_trace(h: int) -> dict:
+    """The last traced step: tile items and their wall-clock stamps (see SPD_DBG_STEP_TRACE)."""
+    info = spd_step_plan_info(h)
+    n = info["nitems"]
+    items = spd_read_debug(h, SPD_DBG_STEP_ITEMS, n, np.uint32)
+    stamps = spd_read_debug(h, SPD_DBG_STEP_TRACE, 4 * n, np.uint64).reshape(n, 4)
+    return {"items": items, "stamps": stamps, **info}
 
 
 def spd_destroy(h: int) -> None:

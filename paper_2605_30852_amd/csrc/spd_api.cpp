@@ -24,9 +24,11 @@ enum HState { H_INIT = 0, H_READY = 1, H_PENDING = 2 };
 
 struct Layout {
   size_t kv, pkv, pt, rope, state, tok, forced, log, resid, anch, pdmx, pfx, pfanch, dbg, lay;
-  size_t q[2], ao[2], act[2], part[2], cnt[2], hpv[2], hpi[2];
+  size_t q[2], ao[2], act[2], part[2], cnt[2], hkey[2];
+  size_t items, sync, dctx, trace;
   size_t total;
-  int num_pages, chunk, max_splits, head_tiles;
+  int num_pages, chunk, max_splits, J, nitems, nsync;
+  int tiles[5];
   size_t kv_layer_bytes;
 };
 
@@ -79,7 +81,18 @@ Layout make_layout(const spd_config& c) {
     L.chunk = c.attn_chunk ? c.attn_chunk : std::max(64, ch);
   }
   L.max_splits = (c.max_tokens + L.chunk - 1) / L.chunk;
-  L.head_tiles = (c.vocab + kHeadRows - 1) / kHeadRows;
+  // persistent step kernel: tiles per stage per sublayer, and the ticket table of one step
+  L.J = 0;
+  for (int s = 0; s < n; s++)
+    L.J = std::max(L.J, (int)((long long)(s + 1) * c.n_layers / n) - (int)((long long)s * c.n_layers / n));
+  L.tiles[SK_QKV] = (c.n_q_heads + 2 * hkv) * (dh / 2 / kQPairs);
+  L.tiles[SK_ATTN] = hkv * L.max_splits;
+  L.tiles[SK_OPROJ] = (d + kORows - 1) / kORows;
+  L.tiles[SK_GATEUP] = (c.ffn_dim + kGOut - 1) / kGOut;
+  L.tiles[SK_DOWN] = (d + kDRows - 1) / kDRows;
+  L.nitems = 0;
+  for (int k = 0; k < 5; k++) L.nitems += L.J * n * L.tiles[k];
+  L.nsync = (2 + 5 * L.J * n) * kSyncStride;
   L.kv_layer_bytes = (size_t)L.num_pages * 2 * hkv * c.page_size * dh * esz;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -110,15 +123,35 @@ Layout make_layout(const spd_config& c) {
     L.act[s] = take(sizeof(float) * kMaxRows * (size_t)c.ffn_dim);
     L.part[s] = take(sizeof(float) * part_floats);
     L.cnt[s] = take(sizeof(int32_t) * kMaxStages * hkv);
-    L.hpv[s] = take(sizeof(float) * L.head_tiles);
-    L.hpi[s] = take(sizeof(int32_t) * L.head_tiles);
+    L.hkey[s] = take(sizeof(unsigned long long));
   }
+  L.items = take(sizeof(uint32_t) * (size_t)L.nitems);
+  L.sync = take(sizeof(int32_t) * (size_t)L.nsync);
+  L.dctx = take(sizeof(Ctx));
+  L.trace = take(sizeof(unsigned long long) * 4 * (size_t)L.nitems);
   L.total = o;
   return L;
 }
 
 void stage_bounds(int L, int n, int* beta) {
   for (int s = 0; s <= n; s++) beta[s] = (int)((long long)s * L / n);
+}
+
+// Ticket order of the persistent step kernel. Super-phase P holds phase P - skew*s of every stage s
+// (stage by stage); skew 0 keeps the stages in lockstep, skew k > 0 staggers them by k sublayers so
+// that one stage's latency-bound sublayer (attention) overlaps other stages' weight streaming. In
+// every order a tile comes after the whole previous phase of its stage, which is all it waits for.
+std::vector<uint32_t> step_items(const Layout& L, int n, int skew) {
+  std::vector<uint32_t> v;
+  v.reserve(L.nitems);
+  const int NP = 5 * L.J;
+  for (int P = 0; P < NP + skew * (n - 1); P++)
+    for (int s = 0; s < n; s++) {
+      const int p = P - skew * s;
+      if (p < 0 || p >= NP) continue;
+      for (int t = 0; t < L.tiles[p % 5]; t++) v.push_back(step_item(p, s, t));
+    }
+  return v;
 }
 
 }  // namespace
@@ -132,6 +165,9 @@ struct spd_handle {
   int J = 0;  // layer slots per step = longest stage
   hipStream_t main = nullptr, pdm = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  // step-kernel mode 2: one stream and one completion event per stage (default priority)
+  hipStream_t sst[kMaxStages] = {};
+  hipEvent_t ev_st[kMaxStages] = {};
   char* ws = nullptr;
   int hstate = H_INIT;
   int c = 0, a = 0, prompt_len = 0;
@@ -143,6 +179,11 @@ struct spd_handle {
   std::string err;
   // step graph (fork/join of both streams captured once, replayed per step)
   int use_graph = 0;
+  // stage compute: 0 = five launches per layer slot, 1 = one persistent launch per step, 2 = one
+  // stream per stage
+  int step_mode = kStepModeDefault;
+  int step_grid = kStepGridDefault;
+  int step_skew = kStepSkewDefault;
   hipGraphExec_t gexec = nullptr;
   // kernel timing
   int timed_kernel = 0;
@@ -177,7 +218,10 @@ static spd_status launch_check(spd_handle* h, const char* what) {
 struct TimedLaunch {
   bool on;
   TimedLaunch(spd_handle* h, hipStream_t s, int kind) : on(false) {
-    if (!h || h->timed_kernel != kind || s != h->main || h->cur_slot < h->timed_first_slot) return;
+    if (!h || h->timed_kernel != kind || h->cur_slot < h->timed_first_slot) return;
+    bool ours = s == h->main;
+    for (int st = 0; st < kMaxStages; st++) ours = ours || (h->sst[st] != nullptr && s == h->sst[st]);
+    if (!ours) return;
     if (h->tev_used + 2 > h->tev.size()) {
       for (int i = 0; i < 64; i++) {
         hipEvent_t e;
@@ -251,27 +295,112 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
   if (sp) HIPC(hipEventRecord(sp[1], h->pdm));
   HIPC(hipEventRecord(h->ev_join, h->pdm));
   // every active stage advances its token by one layer per slot (Section 3.1)
-  for (int j = 0; j < h->J; j++) {
-    h->cur_slot = j;
-    Rows r;
-    std::memset(&r, 0, sizeof(Rows));
-    r.kind = 0;
-    r.slot = j;
-    r.layer = 0;
-    r.nrows = 1;
-    r.pos0 = 0;
-    r.x = nullptr;
-    r.anch = nullptr;
-    r.cap = -1;
-    r.set = 0;
-    for (int st = 0; st < kMaxStages; st++) {
-      const int l = st < h->cfg.n_stages ? C.beta[st] + j : -1;
-      if (l >= 0 && l < C.beta[st + 1])
-        r.ld[st] = h->layer_desc[l];
-      else
-        std::memset(&r.ld[st], 0, sizeof(LayerDesc));
+  if (h->step_mode == 1) {
+    h->cur_slot = 0;
+    TimedLaunch t(h, h->main, SPD_K_STEP);
+    launch_step(C, (const Ctx*)(h->ws + h->lay.dctx), h->step_grid, h->main, h->bf16);
+  } else if (h->step_mode == 3) {
+    // skewed schedule: launch L runs sublayer L - s of every stage s (Section 3.1's stages advance
+    // independently within a step), so each launch mixes independent sublayers of different stages
+    const int n = h->cfg.n_stages, NP = 5 * h->J;
+    const size_t esz = h->bf16 ? 2 : 4;
+    const int total = C.stream_wgs > 0 ? C.stream_wgs : kStreamWGs;
+    for (int L = 0; L < NP + n - 1; L++) {
+      MixLaunch m;
+      std::memset(&m, 0, sizeof(m));
+      struct G { int kind, s, slot; double bytes; int npairs; };
+      std::vector<G> gem;
+      int wg = 0;
+      for (int pass = 0; pass < 2; pass++) {  // attention parts first, then the weight-streaming ones
+        for (int st = 0; st < n; st++) {
+          const int p = L - st;
+          if (p < 0 || p >= NP) continue;
+          const int slot = p / 5, kind = p % 5, layer = C.beta[st] + slot;
+          if (layer >= C.beta[st + 1]) continue;
+          if ((kind == SK_ATTN) != (pass == 0)) continue;
+          if (kind == SK_ATTN) {
+            MixPart& P = m.p[m.nparts++];
+            P.kind = kind;
+            P.stage = st;
+            P.slot = slot;
+            P.ld = h->layer_desc[layer];
+            P.wg0 = wg;
+            P.nwg = C.hkv * C.max_splits;
+            wg += P.nwg;
+          } else {
+            G g;
+            g.kind = kind;
+            g.s = st;
+            g.slot = slot;
+            const double d = C.d, F = C.F, qd = C.qdim;
+            g.bytes = kind == SK_QKV ? (C.hq + 2 * C.hkv) * C.dh * d : kind == SK_OPROJ ? d * qd
+                      : kind == SK_GATEUP ? 2 * F * d : d * F;
+            g.npairs = kind == SK_QKV ? (C.hq + 2 * C.hkv) * (C.dh / 2) : kind == SK_GATEUP ? C.F : (C.d + 1) / 2;
+            gem.push_back(g);
+          }
+        }
+      }
+      double tot = 0;
+      for (const G& g : gem) tot += g.bytes;
+      for (const G& g : gem) {
+        int nwg = (int)std::lround(total * g.bytes / tot);
+        nwg = std::max(nwg, (g.npairs + 255) / 256);  // a wave streams at most 64 pairs
+        nwg = std::min(nwg, (g.npairs + 3) / 4);
+        nwg = std::max(nwg, 1);
+        MixPart& P = m.p[m.nparts++];
+        P.kind = g.kind;
+        P.stage = g.s;
+        P.slot = g.slot;
+        P.ld = h->layer_desc[C.beta[g.s] + g.slot];
+        P.wg0 = wg;
+        P.nwg = nwg;
+        wg += nwg;
+      }
+      if (m.nparts == 0) continue;
+      h->cur_slot = L / 5;
+      TimedLaunch t(h, h->main, SPD_K_MIX);
+      Launch<WT>::mix(C, m, wg, h->main);
     }
-    enqueue_layer<WT>(C, r, h->main, h);
+    (void)esz;
+  } else {
+    // mode 0: every launch covers all stages, on main_stream. mode 2: stage s runs its own chain of
+    // launches on its own stream, forked from and joined to main_stream, so that one stage's
+    // latency-bound attention and launch tails overlap the other stages' weight streaming.
+    const int n = h->cfg.n_stages;
+    const int groups = h->step_mode == 2 ? n : 1;
+    for (int gi = 0; gi < groups; gi++) {
+      hipStream_t s = h->main;
+      if (h->step_mode == 2) {
+        s = h->sst[gi];
+        HIPC(hipStreamWaitEvent(s, h->ev_fork, 0));
+      }
+      for (int j = 0; j < h->J; j++) {
+        h->cur_slot = j;
+        Rows r;
+        std::memset(&r, 0, sizeof(Rows));
+        r.kind = 0;
+        r.slot = j;
+        r.stage0 = h->step_mode == 2 ? gi : 0;
+        r.nst = h->step_mode == 2 ? 1 : n;
+        r.nrows = 1;
+        r.cap = -1;
+        bool any = false;
+        for (int st = 0; st < kMaxStages; st++) {
+          const int l = (st >= r.stage0 && st < r.stage0 + r.nst) ? C.beta[st] + j : -1;
+          if (l >= 0 && l < C.beta[st + 1]) {
+            r.ld[st] = h->layer_desc[l];
+            any = true;
+          } else {
+            std::memset(&r.ld[st], 0, sizeof(LayerDesc));
+          }
+        }
+        if (any) enqueue_layer<WT>(C, r, s, h);
+      }
+      if (h->step_mode == 2) {
+        HIPC(hipEventRecord(h->ev_st[gi], s));
+        HIPC(hipStreamWaitEvent(h->main, h->ev_st[gi], 0));
+      }
+    }
   }
   h->cur_slot = h->J;
   if (fused) {
@@ -411,6 +540,10 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   HIPI(hipGetDevice(&h->dev));
   HIPI(hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming));
   HIPI(hipEventCreateWithFlags(&h->ev_join, hipEventDisableTiming));
+  for (int st = 0; st < cfg->n_stages; st++) {
+    HIPI(hipStreamCreateWithFlags(&h->sst[st], hipStreamNonBlocking));
+    HIPI(hipEventCreateWithFlags(&h->ev_st[st], hipEventDisableTiming));
+  }
   HIPI(hipHostMalloc((void**)&h->pinned, sizeof(spd_step_result) * (kLogCap + 1), hipHostMallocDefault));
 
   const spd_config& c = *cfg;
@@ -465,9 +598,15 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
     B.act = (float*)(ws + lay.act[s]);
     B.part = (float*)(ws + lay.part[s]);
     B.cnt = (int32_t*)(ws + lay.cnt[s]);
-    B.hpart_v = (float*)(ws + lay.hpv[s]);
-    B.hpart_i = (int32_t*)(ws + lay.hpi[s]);
+    B.hkey = (unsigned long long*)(ws + lay.hkey[s]);
   }
+  C.plan.items = (const uint32_t*)(ws + lay.items);
+  C.plan.nitems = lay.nitems;
+  C.plan.sync = (int32_t*)(ws + lay.sync);
+  C.plan.nsync = lay.nsync;
+  for (int k = 0; k < 5; k++) C.plan.tiles[k] = lay.tiles[k];
+  C.plan.trace = nullptr;
+  const std::vector<uint32_t> items = step_items(lay, c.n_stages, kStepSkewDefault);
 
   // layer table
   std::vector<LayerDesc> ld(c.n_layers + c.pdm_layers);
@@ -517,6 +656,11 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   HIPI(hipMemsetAsync(ws + lay.tok, 0, sizeof(int32_t) * (c.max_tokens + 8), h->main));
   HIPI(hipMemsetAsync(ws + lay.forced, 0xff, sizeof(int32_t) * (c.max_tokens + 8), h->main));
   for (int s = 0; s < 2; s++) HIPI(hipMemsetAsync(ws + lay.cnt[s], 0, sizeof(int32_t) * kMaxStages * c.n_kv_heads, h->main));
+  for (int s = 0; s < 2; s++) HIPI(hipMemsetAsync(ws + lay.hkey[s], 0, sizeof(unsigned long long), h->main));
+  HIPI(hipMemcpyAsync(ws + lay.items, items.data(), sizeof(uint32_t) * items.size(), hipMemcpyHostToDevice, h->main));
+  HIPI(hipMemsetAsync(ws + lay.sync, 0, sizeof(int32_t) * lay.nsync, h->main));
+  // the persistent step kernel reads the context from device memory
+  HIPI(hipMemcpyAsync(ws + lay.dctx, &C, sizeof(Ctx), hipMemcpyHostToDevice, h->main));
   HIPI(hipStreamSynchronize(h->main));
 #undef HIPI
   *out = h;
@@ -526,16 +670,67 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
 static void drop_graph(spd_handle* h);
 static spd_status run_one_step(spd_handle* h, int forced_override);
 
+spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t skew) {
+  if (!h || mode < 0 || mode > 3 || grid < 0 || grid > 65535 || skew < -1 || skew > 16) return SPD_E_INVAL;
+  h->step_mode = mode;
+  if (mode == 1)
+    h->step_grid = grid ? grid : kStepGridDefault;
+  else
+    h->ctx.stream_wgs = grid;  // 0: default
+  if (skew >= 0 && skew != h->step_skew) {
+    HIPC(hipSetDevice(h->dev));
+    HIPC(hipStreamSynchronize(h->pdm));
+    HIPC(hipStreamSynchronize(h->main));
+    const std::vector<uint32_t> items = step_items(h->lay, h->cfg.n_stages, skew);
+    HIPC(hipMemcpy(h->ws + h->lay.items, items.data(), sizeof(uint32_t) * items.size(), hipMemcpyHostToDevice));
+    h->step_skew = skew;
+  }
+  drop_graph(h);  // the captured launches change
+  return SPD_OK;
+}
+
+spd_status spd_set_step_trace(spd_handle* h, int32_t on) {
+  if (!h) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->pdm));
+  HIPC(hipStreamSynchronize(h->main));
+  h->ctx.plan.trace = on ? (unsigned long long*)(h->ws + h->lay.trace) : nullptr;
+  if (on) HIPC(hipMemset(h->ws + h->lay.trace, 0, sizeof(unsigned long long) * 4 * (size_t)h->lay.nitems));
+  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
+  drop_graph(h);
+  return SPD_OK;
+}
+
+spd_status spd_step_plan_info(spd_handle* h, int32_t* info) {
+  if (!h || !info) return SPD_E_INVAL;
+  info[0] = h->lay.nitems;
+  info[1] = h->lay.J;
+  for (int k = 0; k < 5; k++) info[2 + k] = h->lay.tiles[k];
+  int khz = 0;
+  HIPC(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->dev));
+  info[7] = khz;
+  return SPD_OK;
+}
+
 spd_status spd_set_debug(spd_handle* h, int32_t on) {
   if (!h) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->pdm));
+  HIPC(hipStreamSynchronize(h->main));
   h->ctx.debug = on ? 1 : 0;
+  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
   drop_graph(h);  // kernel arguments changed
   return SPD_OK;
 }
 
 static spd_status fetch_state(spd_handle* h) {
   HIPC(hipMemcpyAsync(h->pinned, &h->ctx.st->res, sizeof(spd_step_result), hipMemcpyDeviceToHost, h->main));
+  HIPC(hipMemcpyAsync(&h->pinned[1].decision, &h->ctx.st->err, sizeof(int32_t), hipMemcpyDeviceToHost, h->main));
   HIPC(hipStreamSynchronize(h->main));
+  if (h->pinned[1].decision != 0) {
+    h->err = "step kernel: a dependency wait timed out; the step's results are invalid";
+    return SPD_E_HIP;
+  }
   const spd_step_result& r = h->pinned[0];
   h->c = r.committed_len;
   h->a = r.inflight;
@@ -725,6 +920,11 @@ spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes)
     case SPD_DBG_PDM_LOGITS: src = h->ctx.dbg_logits + c.vocab; need = sizeof(float) * c.vocab; break;
     case SPD_DBG_TOKENS: src = h->ctx.tok; need = sizeof(int32_t) * c.max_tokens; break;
     case SPD_DBG_STATE: src = nullptr; need = sizeof(int32_t) * 4; break;
+    case SPD_DBG_STEP_ITEMS: src = h->ctx.plan.items; need = sizeof(uint32_t) * (size_t)h->lay.nitems; break;
+    case SPD_DBG_STEP_TRACE:
+      src = h->ws + h->lay.trace;
+      need = sizeof(unsigned long long) * 4 * (size_t)h->lay.nitems;
+      break;
     default: return SPD_E_INVAL;
   }
   if (bytes != need) return SPD_E_INVAL;
@@ -778,7 +978,7 @@ spd_status spd_read_kv(spd_handle* h, int32_t pdm, int32_t layer, int32_t pos0, 
 }
 
 spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel, int32_t first_slot) {
-  if (!h || kernel < 0 || kernel > SPD_K_SPANS || first_slot < 0) return SPD_E_INVAL;
+  if (!h || kernel < 0 || kernel > SPD_K_MIX || first_slot < 0) return SPD_E_INVAL;
   h->timed_kernel = kernel;
   h->timed_first_slot = first_slot;
   return SPD_OK;
@@ -829,6 +1029,11 @@ void spd_destroy(spd_handle* h) {
   for (hipEvent_t e : h->sev) (void)hipEventDestroy(e);
   if (h->main) (void)hipStreamSynchronize(h->main);
   if (h->pdm) (void)hipStreamSynchronize(h->pdm);
+  for (int st = 0; st < kMaxStages; st++) {
+    if (h->sst[st]) (void)hipStreamSynchronize(h->sst[st]);
+    if (h->ev_st[st]) (void)hipEventDestroy(h->ev_st[st]);
+    if (h->sst[st]) (void)hipStreamDestroy(h->sst[st]);
+  }
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_join) (void)hipEventDestroy(h->ev_join);
   if (h->pinned) (void)hipHostFree(h->pinned);

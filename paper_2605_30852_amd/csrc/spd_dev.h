@@ -39,7 +39,7 @@ struct DevState {
   int32_t nsteps;
   int32_t y;           // target argmax of this step's exiting token
   int32_t pdm_draft;   // PDM argmax of this step
-  int32_t pad0;
+  int32_t err;         // sticky: a dependency wait of the step kernel timed out
   spd_step_result res; // last step
   int32_t pad1[6];
 };
@@ -52,8 +52,41 @@ struct BufSet {
   float* act;       // [8][F] SwiGLU activations
   float* part;      // attention split partials
   int32_t* cnt;     // per (stage, KV head) split tickets of the decode attention; zero at rest
-  float* hpart_v;   // LM-head per-tile maxima [tiles]
-  int32_t* hpart_i; // LM-head per-tile argmax [tiles]
+  // LM-head argmax of this stream's row: the maximum over the vocabulary of a 64-bit key that
+  // orders (logit descending, index ascending); zero at rest (reset by its reader)
+  unsigned long long* hkey;
+};
+
+// Work items of the persistent step kernel. One step is 5J phases (layer slot j = p / 5, sublayer
+// p % 5); every active stage has a fixed number of tiles per phase. An item is (phase, stage, tile).
+enum StepKind { SK_QKV = 0, SK_ATTN = 1, SK_OPROJ = 2, SK_GATEUP = 3, SK_DOWN = 4 };
+constexpr int kQPairs = 16;  // QKV item: 16 RoPE pairs of one head (32 weight rows, 4 pairs per wave)
+constexpr int kORows = 16;   // O-proj item: 16 rows (2 row pairs per wave)
+constexpr int kGOut = 16;    // gate/up item: 16 outputs = 32 weight rows (4 per wave)
+constexpr int kDRows = 8;    // down item: 8 rows (1 row pair per wave)
+constexpr int kStepGridDefault = 512;
+constexpr int kStepSkewDefault = 0;
+constexpr int kStepModeDefault = 2;
+constexpr int kStreamWGs = 768;  // workgroups of one streaming stage launch (all its stages)
+__host__ __device__ inline uint32_t step_item(int p, int s, int t) {
+  return ((uint32_t)p << 19) | ((uint32_t)s << 16) | (uint32_t)t;
+}
+
+// Counters of the persistent step kernel, each on its own 128-byte line so that polls of one do not
+// contend with atomics on another: the ticket counter, the timeout flag, and per (phase, stage) the
+// number of finished units.
+constexpr int kSyncStride = 32;  // ints per line
+__host__ __device__ inline int sync_ticket() { return 0; }
+__host__ __device__ inline int sync_err() { return kSyncStride; }
+__host__ __device__ inline int sync_done(int p, int s, int n) { return (2 + p * n + s) * kSyncStride; }
+
+struct StepPlan {
+  const uint32_t* items;  // ticket -> item
+  int nitems;
+  int* sync;              // counters (sync_ticket, sync_err, sync_done)
+  int nsync;              // ints in sync ((2 + 5J*n) * kSyncStride)
+  int tiles[5];           // tiles per stage per sublayer kind (attention: Hkv * max_splits)
+  unsigned long long* trace;  // null, or per ticket 4 wall-clock stamps: start, inputs ready, staged, end
 };
 
 struct Ctx {
@@ -85,16 +118,20 @@ struct Ctx {
   float* dbg_logits;// [2][V]
   int debug;
   BufSet b[2];      // 0: target stream, 1: PDM stream
+  StepPlan plan;    // persistent step kernel
+  int stream_wgs;   // workgroups of one streaming stage launch (all its stages)
 };
 
 // Which rows a launch works on.
-//   kind 0 (stage launch): group g = stage s, one row: the token at depth s, position c+a-1-s,
+//   kind 0 (stage launch): group g = stage s = stage0 + g, one row: the token at depth s, position c+a-1-s,
 //            layer beta_s + slot (inactive if s >= a or the stage has fewer layers).
 //   kind 1 (row block): one group of `nrows` rows at positions pos0+i through layer `layer`;
 //            nrows < 0 means "a" and pos0 < 0 means "c" read from the device state (PDM step).
 struct Rows {
   int kind;
   int slot;
+  int stage0;   // kind 0: group g of the launch is stage stage0 + g
+  int nst;      // kind 0: stages in the launch (grid y, or z for attention)
   int layer;    // kind 1: index into Ctx::lay
   int nrows;
   int pos0;
@@ -105,6 +142,21 @@ struct Rows {
   // kind 0: layer beta_s + slot of every stage s, passed with the launch so that weight loads need
   // no table lookup (all pointers null for a stage with no layer in this slot)
   LayerDesc ld[kMaxStages];
+};
+
+// One launch of the skewed schedule (step-kernel mode 3): part i is sublayer `kind` (StepKind) of
+// stage `stage` in layer slot `slot`, on workgroups [wg0, wg0 + nwg) of the launch.
+struct MixPart {
+  int kind;
+  int stage;
+  int slot;
+  int wg0;
+  int nwg;
+  LayerDesc ld;
+};
+struct MixLaunch {
+  int nparts;
+  MixPart p[kMaxStages];
 };
 
 // Launchers (spd_kernels.hip). All are asynchronous on `stream`.
@@ -122,8 +174,14 @@ struct Launch {
   // (verify / reseed) reduces the partials.
   static void head(const Ctx& c, int src, int row, void* stream);
   static void embed_rows(const Ctx& c, int t0, int nrows, void* stream);
+  // one launch of the skewed schedule, nwg workgroups
+  static void mix(const Ctx& c, const MixLaunch& m, int nwg, void* stream);
 };
 void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* stream, int bf16);
+// Every layer slot of every active stage of one step in one persistent launch (spd_step.hip).
+// dev_ctx: a device copy of c.
+void launch_step(const Ctx& c, const Ctx* dev_ctx, int grid, void* stream, int bf16);
+size_t step_lds_bytes(const Ctx& c, int bf16);
 // Events (hipEvent_t) that the next launches of this host thread record at their own start and end;
 // nullptr turns it off.
 void set_launch_events(void* start, void* stop);

@@ -10,103 +10,16 @@
 // on how many stages share a launch. That makes a token's arithmetic identical whether it runs in an
 // n-stage SPD step or in plain decoding (n = 1), which the lossless check relies on.
 #include <hip/hip_ext.h>
+#include <algorithm>
 #include <hip/hip_runtime.h>
 #include <math.h>
 
 #include "spd_dev.h"
+#include "spd_devfn.h"
+#include "spd_gemv.h"
+#include "spd_attn.h"
 
 namespace spd {
-
-// ------------------------------------------------------------------------------------------ types
-template <typename T>
-struct Elt;
-template <>
-struct Elt<float> {
-  static constexpr int VE = 4;  // elements per 16-byte load
-};
-template <>
-struct Elt<uint16_t> {
-  static constexpr int VE = 8;
-};
-
-__device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
-__device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
-
-__device__ __forceinline__ uint16_t f2bf(float f) {  // round to nearest even (finite inputs)
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-template <typename T>
-__device__ __forceinline__ void unpack16(const uint4& v, float* o);
-template <>
-__device__ __forceinline__ void unpack16<float>(const uint4& v, float* o) {
-  o[0] = __uint_as_float(v.x);
-  o[1] = __uint_as_float(v.y);
-  o[2] = __uint_as_float(v.z);
-  o[3] = __uint_as_float(v.w);
-}
-template <>
-__device__ __forceinline__ void unpack16<uint16_t>(const uint4& v, float* o) {
-  o[0] = bf_lo(v.x);
-  o[1] = bf_hi(v.x);
-  o[2] = bf_lo(v.y);
-  o[3] = bf_hi(v.y);
-  o[4] = bf_lo(v.z);
-  o[5] = bf_hi(v.z);
-  o[6] = bf_lo(v.w);
-  o[7] = bf_hi(v.w);
-}
-
-// 16-byte load through the global address space (the pointers come from tables in memory, so
-// the compiler cannot infer it and would otherwise emit flat loads).
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(1))) const v4u gv4u;
-__device__ __forceinline__ uint4 ldg16(const void* p) {
-  const v4u v = *(gv4u*)(p);
-  return make_uint4(v.x, v.y, v.z, v.w);
-}
-
-template <typename T>
-__device__ __forceinline__ float ld1(const T* p, size_t i);
-template <>
-__device__ __forceinline__ float ld1<float>(const float* p, size_t i) { return p[i]; }
-template <>
-__device__ __forceinline__ float ld1<uint16_t>(const uint16_t* p, size_t i) {
-  return __uint_as_float(((uint32_t)p[i]) << 16);
-}
-
-// Two consecutive elements (4- or 8-byte aligned) as floats.
-template <typename T>
-__device__ __forceinline__ float2 ld2(const T* p);
-template <>
-__device__ __forceinline__ float2 ld2<float>(const float* p) { return *reinterpret_cast<const float2*>(p); }
-template <>
-__device__ __forceinline__ float2 ld2<uint16_t>(const uint16_t* p) {
-  const uint32_t u = *reinterpret_cast<const uint32_t*>(p);
-  return make_float2(bf_lo(u), bf_hi(u));
-}
-
-template <typename T>
-__device__ __forceinline__ void st1(T* p, size_t i, float v);
-template <>
-__device__ __forceinline__ void st1<float>(float* p, size_t i, float v) { p[i] = v; }
-template <>
-__device__ __forceinline__ void st1<uint16_t>(uint16_t* p, size_t i, float v) { p[i] = f2bf(v); }
-
-// ------------------------------------------------------------------------------------ reductions
-__device__ __forceinline__ float wave_sum(float v) {
-  // xor butterfly: every lane ends with the same, order-fixed total (fp add is commutative)
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
-}
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
-  return v;
-}
 
 // ------------------------------------------------------------------------------- row resolution
 struct Grp {
@@ -125,6 +38,7 @@ __device__ __forceinline__ Grp resolve(const Ctx& C, const Rows& R, int g) {
   r.active = 1;
   if (R.kind == 0) {
     const int a = C.st->a, c = C.st->c;
+    g += R.stage0;
     r.s = g;
     if (g >= a || C.beta[g] + R.slot >= C.beta[g + 1]) {
       r.active = 0;
@@ -155,28 +69,8 @@ __device__ __forceinline__ LayerDesc layer_of(const Ctx& C, const Rows& R, const
   return R.kind == 0 ? R.ld[gr.s] : C.lay[gr.layer];
 }
 
-__device__ __forceinline__ size_t kv_off(const Ctx& C, int pos, int kvh, int j) {
-  // [page][2][Hkv][page_size][dh]; returns the K element offset (V is + Hkv*page*dh)
-  const int pg = C.page_table[pos / C.page];
-  return (size_t)pg * (2 * C.hkv * C.page * C.dh) + ((size_t)kvh * C.page + (pos % C.page)) * C.dh + j;
-}
 
 // --------------------------------------------------------------------------------- GEMV building
-// LDS layout of one staged activation chunk. For bf16 weights lane l multiplies columns
-// 8l..8l+7 of each 512-column block; the chunk is stored so that the lane's first four and last
-// four values are two conflict-free 16-byte LDS reads.
-template <int VE>
-__device__ __forceinline__ int xidx(int k) {
-  if constexpr (VE == 8) {
-    const int blk = k >> 9, w = k & 511, l = w >> 3, e = w & 7;
-    return (blk << 9) + ((e >> 2) << 8) + (l << 2) + (e & 3);
-  } else {
-    return k;
-  }
-}
-
-// Weight blocks loaded at once per row: a wave keeps RL rows x kU blocks of 16-byte loads in flight.
-constexpr int kU = 5;
 
 // Load blocks [blk, min(blk + kU, blk_end)) of every row (block b = columns b*64*VE + lane*VE + 0..VE-1);
 // rows that are nullptr or blocks past blk_end load zeros. K is a multiple of VE, so a load that starts
@@ -302,14 +196,6 @@ __device__ __forceinline__ void stage_chunk(const XSpec& xs, int nrows, int kc0,
   }
 }
 
-__device__ __forceinline__ float block_sum(float v, float* red) {
-  v = wave_sum(v);
-  const int w = threadIdx.x >> 6;
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0) red[w] = v;
-  __syncthreads();
-  return (red[0] + red[1]) + (red[2] + red[3]);
-}
 
 // Staged activation floats per row and chunk (multiples of every block width, so that the
 // per-lane accumulation order does not depend on the chunking). LDS stays at 48 KB or less.
@@ -379,7 +265,7 @@ __device__ __forceinline__ void gemv_tile(const WT* const (&wr)[RL], int K, cons
 // rotation happens in registers right after the reduction.
 template <typename WT, int NV>
 __global__ __launch_bounds__(kWG) void k_qkv(Ctx C, Rows R) {
-  extern __shared__ float lds[];
+  extern __shared__ __align__(16) float lds[];
   const Grp gr = resolve(C, R, blockIdx.y);
   if (!gr.active) return;
   const LayerDesc Ld = layer_of(C, R, gr);
@@ -448,7 +334,7 @@ __global__ __launch_bounds__(kWG) void k_qkv(Ctx C, Rows R) {
 // the next PDM anchor when this is a stage's last layer.
 template <typename WT, int NV, int MODE>
 __global__ __launch_bounds__(kWG) void k_proj_add(Ctx C, Rows R) {
-  extern __shared__ float lds[];
+  extern __shared__ __align__(16) float lds[];
   const Grp gr = resolve(C, R, blockIdx.y);
   if (!gr.active) return;
   const LayerDesc Ld = layer_of(C, R, gr);
@@ -500,7 +386,7 @@ __global__ __launch_bounds__(kWG) void k_proj_add(Ctx C, Rows R) {
 // Tile = 4 outputs (1 per wave); each wave streams the gate and up rows of its output together.
 template <typename WT, int NV>
 __global__ __launch_bounds__(kWG) void k_gateup(Ctx C, Rows R) {
-  extern __shared__ float lds[];
+  extern __shared__ __align__(16) float lds[];
   const Grp gr = resolve(C, R, blockIdx.y);
   if (!gr.active) return;
   const LayerDesc Ld = layer_of(C, R, gr);
@@ -528,13 +414,133 @@ __global__ __launch_bounds__(kWG) void k_gateup(Ctx C, Rows R) {
   }
 }
 
+// ------------------------------------------------------------- streaming stage-launch GEMVs
+// One launch of a sublayer for the stages of a stage launch (grid y = stage). The launch holds a few
+// workgroups per CU; each stages the stage's input vector into LDS once (with RMSNorm for QKV and
+// gate/up) and its waves then stream their row pairs back to back: wave w of workgroup b takes pairs
+// b*4+w, b*4+w+NW, ... (NW = waves per stage), loading two units ahead across pair boundaries.
+// Values an epilogue needs from memory (RoPE cos/sin, residual entries, the token's KV page) are
+// loaded before the stream, one pair per lane, and handed over by lane shuffles, so no epilogue load
+// makes a wave wait for its own weight stream. Pairs: QKV (j, j + dh/2) of one head (RoPE partners),
+// gate/up (gate m, up m), O-proj and down (2m, 2m + 1).
+enum SKind { SG_QKV = 0, SG_OPROJ = 2, SG_GATEUP = 3, SG_DOWN = 4 };
+
+// Workgroup bx of nbx working on one stage's sublayer (gr: the stage's row, Ld: its layer, set: the
+// scratch set).
+template <typename WT, int KIND>
+__device__ __forceinline__ void sgemv_part(const Ctx& C, const Grp& gr, const LayerDesc& Ld, int set, int bx,
+                                           int nbx) {
+  extern __shared__ __align__(16) float lds[];
+  __shared__ float red[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int NW = nbx * 4, wv = bx * 4 + w;
+  const int d = C.d, dh = C.dh, half = C.dh >> 1;
+  const int K = KIND == SG_OPROJ ? C.qdim : (KIND == SG_DOWN ? C.F : d);
+  const int npairs = KIND == SG_QKV ? (C.hq + 2 * C.hkv) * half : (KIND == SG_GATEUP ? C.F : (d + 1) / 2);
+  const int count = wv < npairs ? (npairs - 1 - wv) / NW + 1 : 0;  // at most 64 (the host sizes the grid)
+  const int pos = gr.pos0;
+  float* x = gr.x;
+  auto rowptr = [&](int i, int which) -> const WT* {
+    const int q = wv + i * NW;
+    if (KIND == SG_QKV) {
+      const int head = q / half, j = q - head * half;
+      const WT* W = head < C.hq ? (const WT*)Ld.wq : (head < C.hq + C.hkv ? (const WT*)Ld.wk : (const WT*)Ld.wv);
+      const int hrow = head < C.hq ? head : (head < C.hq + C.hkv ? head - C.hq : head - C.hq - C.hkv);
+      return W + (size_t)(hrow * dh + j + which * half) * d;
+    } else if (KIND == SG_GATEUP) {
+      return (which ? (const WT*)Ld.wu : (const WT*)Ld.wg) + (size_t)q * d;
+    } else {
+      const int m = 2 * q + which;
+      const WT* W = (const WT*)(KIND == SG_OPROJ ? Ld.wo : Ld.wd);
+      return m < d ? W + (size_t)m * K : (const WT*)nullptr;
+    }
+  };
+  uint4 bA[2][kU], bB[2][kU];
+  stream_prefetch<WT>(rowptr, count, K, lane, bA, bB);
+  // per-pair values for the epilogue, lane i holding pair i's
+  float2 pv = make_float2(0.f, 0.f);
+  int page = 0;
+  if (KIND == SG_QKV) {
+    if (lane < count) {
+      const int q = wv + lane * NW, j = q % half;
+      pv = C.rope[(size_t)pos * half + j];
+    }
+    page = C.page_table[pos / C.page];
+  } else if (KIND == SG_OPROJ || KIND == SG_DOWN) {
+    if (lane < count) {
+      const int m = 2 * (wv + lane * NW);
+      pv.x = x[m];
+      pv.y = m + 1 < d ? x[m + 1] : 0.f;
+    }
+  }
+  float sc = 1.f;
+  if (KIND == SG_QKV || KIND == SG_GATEUP) {
+    const float ss = stage_vec<Elt<WT>::VE, false>(x, KIND == SG_QKV ? Ld.attn_norm : Ld.mlp_norm, d, lds, red);
+    sc = 1.0f / sqrtf(ss / (float)d + C.eps);
+  } else {
+    stage_vec<Elt<WT>::VE, false>((KIND == SG_OPROJ ? C.b[set].ao : C.b[set].act) + (size_t)gr.brow0 * K,
+                                  nullptr, K, lds, red);
+  }
+  float* cap = nullptr;
+  if (KIND == SG_DOWN && gr.layer + 1 == C.beta[gr.s + 1] && gr.s + 1 <= C.n - 1)
+    cap = C.anchors + ((size_t)(pos % C.n) * C.n + (gr.s + 1)) * d;
+  auto done = [&](int i, float s0, float s1) {
+    const float2 v = make_float2(__shfl(pv.x, i, 64), __shfl(pv.y, i, 64));
+    if (lane != 0) return;
+    const int q = wv + i * NW;
+    if (KIND == SG_QKV) {
+      const int head = q / half, j = q - head * half;
+      float lo = s0 * sc, hi = s1 * sc;
+      if (head < C.hq + C.hkv) {  // q and k are rotated at the token's own position
+        const float rlo = lo * v.x - hi * v.y;
+        const float rhi = hi * v.x + lo * v.y;
+        lo = rlo;
+        hi = rhi;
+      }
+      if (head < C.hq) {
+        float* qo = C.b[set].q + (size_t)gr.brow0 * C.qdim + head * dh;
+        qo[j] = lo;
+        qo[j + half] = hi;
+      } else {
+        const int hk = head < C.hq + C.hkv ? head - C.hq : head - C.hq - C.hkv;
+        WT* kv = (WT*)Ld.kv;
+        const size_t off = (size_t)page * (2 * C.hkv * C.page * dh) + ((size_t)hk * C.page + (pos % C.page)) * dh + j +
+                           (head < C.hq + C.hkv ? 0 : (size_t)C.hkv * C.page * dh);
+        st1<WT>(kv, off, lo);
+        st1<WT>(kv, off + half, hi);
+      }
+    } else if (KIND == SG_GATEUP) {
+      const float g = s0 * sc, u = s1 * sc;
+      C.b[set].act[(size_t)gr.brow0 * C.F + q] = g / (1.0f + expf(-g)) * u;
+    } else {
+      const int m = 2 * q;
+      const float n0 = v.x + s0;
+      x[m] = n0;
+      if (cap != nullptr) cap[m] = n0;
+      if (m + 1 < d) {
+        const float n1 = v.y + s1;
+        x[m + 1] = n1;
+        if (cap != nullptr) cap[m + 1] = n1;
+      }
+    }
+  };
+  stream_run<WT>(rowptr, done, count, K, lane, lds, bA, bB);
+}
+
+template <typename WT, int KIND>
+__global__ __launch_bounds__(kWG) void k_sgemv(Ctx C, Rows R) {
+  const Grp gr = resolve(C, R, blockIdx.y);
+  if (!gr.active) return;
+  sgemv_part<WT, KIND>(C, gr, R.ld[gr.s], R.set, blockIdx.x, gridDim.x);  // stage launches carry their layers
+}
+
 // ---------------------------------------------------------------------- PDM feature projection
 // g_q = W_in . [H^{beta_0}; ...; H^{beta_f}; 0 ...] for the rows the PDM runs (Eq. agg-main with
 // one projection whose column block j serves anchor j). prefill = 1: rows of the prefill chunk
 // at full depth; else the a in-flight rows, row i at depth a-1-i. Tile = 8 outputs (2 per wave).
 template <typename WT>
 __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_arg) {
-  extern __shared__ float lds[];
+  extern __shared__ __align__(16) float lds[];
   constexpr int NV = kMaxRows;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int K = C.n * C.d;
@@ -582,16 +588,13 @@ __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_ar
 // (value, index), the lowest index winning ties; the single-workgroup kernel that follows on the
 // stream reduces the partials. The (value desc, index asc) order is total, so the winner does not
 // depend on the reduction order.
-__device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
-  return v > bv || (v == bv && i < bi);
-}
 
 // Rows of one LM-head pass. src 0: the exit row (skipped unless a == n); 1: the PDM's last row;
 // 2: prefill row `row`; 3: the exit row and the PDM's last row together (rows 0 and 1), one pass over
 // W_lm serving both heads. Row results go to the partials of set 0 (target) or set 1 (PDM).
 template <typename WT, int NV>
 __global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row) {
-  extern __shared__ float lds[];
+  extern __shared__ __align__(16) float lds[];
   __shared__ float s_v[NV][4];
   __shared__ int s_i[NV][4];
   __shared__ float red[4];
@@ -698,65 +701,15 @@ __global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row) {
         fv = s_v[v][k];
         fi = s_i[v][k];
       }
-    C.b[set[v]].hpart_v[blockIdx.x] = fv;
-    C.b[set[v]].hpart_i[blockIdx.x] = fi;
+    // the maximum is order-independent, so the result does not depend on which tile lands last
+    __hip_atomic_fetch_max(C.b[set[v]].hkey, argmax_key(fv, fi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
-// Argmax over the LM head's per-tile partials (one workgroup; the next kernel on the stream, so
-// the kernel boundary orders the partial writes). Every thread returns the winner, which is
-// clamped into [0, V) so that all-NaN logits cannot produce an out-of-range id.
-__device__ int reduce_head(const BufSet& B, int tiles, int V) {
-  __shared__ float r_v[4];
-  __shared__ int r_i[4];
-  __shared__ int r_out;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float v = -INFINITY;
-  int i = 0x7fffffff;
-  for (int k0 = threadIdx.x; k0 < tiles; k0 += kWG * 4) {
-    float pv[4];
-    int pi[4];
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-      const int k = k0 + j * kWG;
-      pv[j] = k < tiles ? B.hpart_v[k] : -INFINITY;
-      pi[j] = k < tiles ? B.hpart_i[k] : 0x7fffffff;
-    }
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-      if (better(pv[j], pi[j], v, i)) {
-        v = pv[j];
-        i = pi[j];
-      }
-    }
-  }
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    const float ov = __shfl_xor(v, m, 64);
-    const int oi = __shfl_xor(i, m, 64);
-    if (better(ov, oi, v, i)) {
-      v = ov;
-      i = oi;
-    }
-  }
-  __syncthreads();
-  if (lane == 0) {
-    r_v[w] = v;
-    r_i[w] = i;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float fv = r_v[0];
-    int fi = r_i[0];
-    for (int k = 1; k < 4; k++)
-      if (better(r_v[k], r_i[k], fv, fi)) {
-        fv = r_v[k];
-        fi = r_i[k];
-      }
-    r_out = (fi >= 0 && fi < V) ? fi : 0;
-  }
-  __syncthreads();
-  return r_out;
+// The LM-head argmax of one stream's row, read (and reset to zero for the next pass) by the single
+// workgroup that follows the head on the stream.
+__device__ __forceinline__ int take_head(const BufSet& B, int V) {
+  return argmax_index(*B.hkey, V);
 }
 
 // ------------------------------------------------------------------------------- attention
@@ -783,7 +736,7 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
   constexpr int TPK = AttnShape<MAXQ>::TPK;
   constexpr int NE = DH / TPK;  // dims per thread in the score phase
   constexpr int VE = Elt<KVT>::VE;
-  extern __shared__ float smem[];
+  extern __shared__ __align__(16) float smem[];
   float* qs = smem;                       // [MAXQ][DH]
   float* sc = qs + MAXQ * DH;             // [MAXQ][PASS]
   KVT* vs = (KVT*)(sc + MAXQ * PASS);     // [PASS][DH]
@@ -943,258 +896,64 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
   }
 }
 
-// Device-coherent scalar accesses for data handed between workgroups of one launch: agent-scope
-// atomic stores and loads are issued with device scope (written through to, and read from, the
-// level every XCD shares), so no L2 writeback fence is needed; a producer waits for its own
-// stores (s_waitcnt) before it signals.
-__device__ __forceinline__ void st_dev(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_dev(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void wait_own_stores() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
 
-__device__ __forceinline__ float2 ld_dev2(const float* p) {  // p 8-byte aligned
-  const unsigned long long u =
-      __hip_atomic_load((unsigned long long*)const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return make_float2(__uint_as_float((uint32_t)u), __uint_as_float((uint32_t)(u >> 32)));
-}
-
-// Decode attention of the stage launches: one query row per stage, G query heads per KV head.
-// Grid: x = split (chunk keys), y = KV head, z = stage. Thread t owns key t/4 of a 64-key pass and a
-// quarter of its head dimension, for K (registers) and V (LDS tile) alike, so one page-table lookup
-// serves both. The device state, the layer's KV base and the first pass's page are requested together
-// at entry (none depends on another); the next pass's loads are issued before the current pass is
-// computed. The last split to finish of each (stage, KV head) merges the partial (o, m, l) records:
-// all (m, l) pairs are read at once, the split weights exp(m - M) / L go to LDS, and the partial
-// outputs are summed in split order with their loads issued eight at a time.
+// Decode attention of a stage launch. Grid: x = key split, y = KV head, z = stage of the launch.
+// The page of this thread's first key and the device state are requested together at entry; the
+// split itself is attn_split (shared with the persistent step kernel).
 template <typename KVT, int DH>
-__global__ __launch_bounds__(kWG) void k_attn_dec(Ctx C, Rows R, int* cnt) {
-  constexpr int PASS = 64, TPK = 4, NE = DH / TPK, VE = Elt<KVT>::VE;
-  constexpr int MAXQ = 8;
-  constexpr int KCH = NE / VE;  // 16-byte chunks per thread for K and for V
-  __shared__ float qs[MAXQ * DH];
-  __shared__ float sc[MAXQ * PASS];
-  __shared__ __align__(16) KVT vs[PASS * DH];
-  __shared__ float s_m[MAXQ], s_l[MAXQ], s_al[MAXQ];
-  __shared__ float s_pw[kMaxSplits * MAXQ];  // merge: m of each split, then its weight
-  __shared__ float s_pl[kMaxSplits * MAXQ];
-  __shared__ int s_last;
-  const int s = blockIdx.z, g = blockIdx.y, split = blockIdx.x;
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  const int kk = tid / TPK, qq = tid % TPK;
+__device__ __forceinline__ void attn_part(const Ctx& C, int s, int slot, const KVT* kv, int set, int g, int split) {
+  extern __shared__ __align__(16) float lds[];
   const int k0 = split * C.chunk;
-  // independent requests first: state, layer KV base, page of this thread's first key
+  const int page0 = C.page_table[min((k0 + (int)threadIdx.x / kAttnTPK) / C.page, C.max_pages - 1)];
   const int st_a = C.st->a, st_c = C.st->c;
-  const int layer = C.beta[s] + R.slot;
-  const KVT* kvb = (const KVT*)R.ld[s].kv;
-  int pg = C.page_table[min((k0 + kk) / C.page, C.max_pages - 1)];
+  const int layer = C.beta[s] + slot;
   if (s >= st_a || layer >= C.beta[s + 1]) return;  // stage idle in this slot
   const int pos0 = st_c + st_a - 1 - s;             // the stage's token; it attends to keys [0, pos0]
-  const int nkeys = pos0 + 1;
-  const int nsplit = (nkeys + C.chunk - 1) / C.chunk;
+  const int nsplit = (pos0 + C.chunk) / C.chunk;
   if (split >= nsplit) return;
-  const int k1 = min(nkeys, k0 + C.chunk);
-  const int G = C.G;
-  const size_t page_elems = (size_t)2 * C.hkv * C.page * DH;
-  const size_t head_off = ((size_t)g * C.page) * DH;
-  const size_t voff = (size_t)C.hkv * C.page * DH;
-  const BufSet& B = C.b[R.set];
-  uint4 kraw[KCH], vraw[KCH];
-  auto issue = [&](int kp, int page) {
-    const int key = kp + kk;
-    if (key < k1) {
-      const KVT* base = kvb + (size_t)page * page_elems + head_off + (size_t)(key % C.page) * DH + qq * NE;
-#pragma unroll
-      for (int c4 = 0; c4 < KCH; c4++) kraw[c4] = ldg16(reinterpret_cast<const uint4*>(base) + c4);
-#pragma unroll
-      for (int c4 = 0; c4 < KCH; c4++) vraw[c4] = ldg16(reinterpret_cast<const uint4*>(base + voff) + c4);
-    }
-  };
-  issue(k0, pg);
-  for (int e = tid; e < G * DH; e += kWG) {
-    const int qi = e / DH, dd = e % DH;
-    qs[qi * DH + dd] = B.q[(size_t)s * C.qdim + (g * G + qi) * DH + dd] * C.scale;
-  }
-  if (tid < MAXQ) {
-    s_m[tid] = -INFINITY;
-    s_l[tid] = 0.f;
-  }
-  constexpr int npair = DH >> 1;
-  constexpr int NG = kWG / npair;
-  constexpr int MAXU = (MAXQ + NG - 1) / NG;
-  const int dp = tid % npair, qg = tid / npair;
-  float o0[MAXU], o1[MAXU];
-#pragma unroll
-  for (int u = 0; u < MAXU; u++) o0[u] = o1[u] = 0.f;
-  for (int kp = k0; kp < k1; kp += PASS) {
-    const int nk = min(PASS, k1 - kp);
-    float kr[NE];
-    if (kk < nk) {
-#pragma unroll
-      for (int c4 = 0; c4 < KCH; c4++) reinterpret_cast<uint4*>(vs + kk * DH + qq * NE)[c4] = vraw[c4];
-#pragma unroll
-      for (int c4 = 0; c4 < KCH; c4++) unpack16<KVT>(kraw[c4], kr + c4 * VE);
-    }
-    if (kp + PASS < k1) {
-      const int nkey = kp + PASS + kk;
-      issue(kp + PASS, C.page_table[min(nkey, k1 - 1) / C.page]);
-    }
-    __syncthreads();  // q staged (first pass), V tile written
-    for (int qi = 0; qi < G; qi++) {
-      float dsum = 0.f;
-      if (kk < nk) {
-        const float* qv = qs + qi * DH + qq * NE;
-#pragma unroll
-        for (int e = 0; e < NE; e += 4) {
-          const float4 q4 = *reinterpret_cast<const float4*>(qv + e);
-          dsum = fmaf(q4.x, kr[e], dsum);
-          dsum = fmaf(q4.y, kr[e + 1], dsum);
-          dsum = fmaf(q4.z, kr[e + 2], dsum);
-          dsum = fmaf(q4.w, kr[e + 3], dsum);
-        }
-      }
-      dsum += __shfl_xor(dsum, 1, 64);
-      dsum += __shfl_xor(dsum, 2, 64);
-      if (qq == 0 && kk < nk) sc[qi * PASS + kk] = dsum;
-    }
-    __syncthreads();
-    for (int qi = w; qi < G; qi += 4) {
-      const float sv = lane < nk ? sc[qi * PASS + lane] : -INFINITY;
-      const float mx = wave_max(sv);
-      const float mo = s_m[qi];
-      const float mn = fmaxf(mo, mx);
-      const float p = lane < nk ? expf(sv - mn) : 0.f;
-      if (lane < nk) sc[qi * PASS + lane] = p;
-      const float ps = wave_sum(p);
-      if (lane == 0) {
-        const float al = (mo == -INFINITY) ? 0.f : expf(mo - mn);
-        s_al[qi] = al;
-        s_l[qi] = s_l[qi] * al + ps;
-        s_m[qi] = mn;
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < MAXU; u++) {
-      const int qi = qg + u * NG;
-      if (qi < G) {
-        const float al = s_al[qi];
-        o0[u] *= al;
-        o1[u] *= al;
-      }
-    }
-    // P.V: eight keys' V pairs and probabilities are read from LDS together (rows >= nk of the
-    // tile hold stale values and are skipped), then accumulated in key order
-    for (int k2 = 0; k2 < nk; k2 += 8) {
-      float2 vv[8];
-#pragma unroll
-      for (int j = 0; j < 8; j++) vv[j] = ld2<KVT>(vs + (size_t)(k2 + j) * DH + 2 * dp);
-#pragma unroll
-      for (int u = 0; u < MAXU; u++) {
-        const int qi = qg + u * NG;
-        if (qi < G) {
-          float pp[8];
-#pragma unroll
-          for (int j = 0; j < 8; j++) pp[j] = sc[qi * PASS + k2 + j];
-#pragma unroll
-          for (int j = 0; j < 8; j++) {
-            if (k2 + j < nk) {
-              o0[u] = fmaf(pp[j], vv[j].x, o0[u]);
-              o1[u] = fmaf(pp[j], vv[j].y, o1[u]);
-            }
-          }
-        }
-      }
-    }
-    __syncthreads();
-  }
-  float* out = B.ao + (size_t)s * C.qdim + g * G * DH;
-  if (nsplit == 1) {
-#pragma unroll
-    for (int u = 0; u < MAXU; u++) {
-      const int qi = qg + u * NG;
-      if (qi < G) {
-        const float inv = 1.0f / s_l[qi];
-        out[qi * DH + 2 * dp] = o0[u] * inv;
-        out[qi * DH + 2 * dp + 1] = o1[u] * inv;
-      }
-    }
+  const int k1 = min(pos0 + 1, k0 + C.chunk);
+  const BufSet& B = C.b[set];
+  const int cidx = s * C.hkv + g;
+  constexpr int RS = kAttnMaxQ * (DH + 2);
+  attn_split<KVT, DH, false>(C, kv, B.q + (size_t)s * C.qdim + g * C.G * DH, B.ao + (size_t)s * C.qdim + g * C.G * DH,
+                             B.part + (size_t)cidx * C.max_splits * RS, B.cnt + cidx, g, split, nsplit, k0, k1, pos0,
+                             page0, lds);
+}
+
+template <typename KVT, int DH>
+__global__ __launch_bounds__(kWG) void k_attn_stage(Ctx C, Rows R) {
+  const int s = R.stage0 + blockIdx.z;
+  attn_part<KVT, DH>(C, s, R.slot, (const KVT*)R.ld[s].kv, R.set, blockIdx.y, blockIdx.x);
+}
+
+// ---------------------------------------------------------------------------- mixed launches
+// One launch of the skewed schedule: up to n independent parts, part i being sublayer kind of
+// stage s in layer slot `slot`, on workgroups [wg0, wg0 + nwg). Parts never depend on each other
+// (different stages), so a latency-bound part (attention) runs under the weight streaming of the
+// others, and every launch streams several stages' worth of weights.
+template <typename WT, int DH>
+__global__ __launch_bounds__(kWG) void k_mix(Ctx C, MixLaunch M) {
+  int i = 0;
+  while (i + 1 < M.nparts && (int)blockIdx.x >= M.p[i + 1].wg0) i++;
+  const MixPart& P = M.p[i];
+  const int b = blockIdx.x - P.wg0;
+  if (P.kind == SK_ATTN) {
+    attn_part<WT, DH>(C, P.stage, P.slot, (const WT*)P.ld.kv, 0, b / C.max_splits, b % C.max_splits);
     return;
   }
-  constexpr int RS = MAXQ * (DH + 2);
-  const int cidx = s * C.hkv + g;
-  float* rec = B.part + ((size_t)cidx * C.max_splits + split) * RS;
-#pragma unroll
-  for (int u = 0; u < MAXU; u++) {
-    const int qi = qg + u * NG;
-    if (qi < G) {
-      st_dev(rec + qi * DH + 2 * dp, o0[u]);
-      st_dev(rec + qi * DH + 2 * dp + 1, o1[u]);
-    }
+  Rows R;
+  R.kind = 0;
+  R.slot = P.slot;
+  R.stage0 = P.stage;
+  R.nst = 1;
+  const Grp gr = resolve(C, R, 0);
+  if (!gr.active) return;
+  switch (P.kind) {
+    case SK_QKV: sgemv_part<WT, SG_QKV>(C, gr, P.ld, 0, b, P.nwg); break;
+    case SK_OPROJ: sgemv_part<WT, SG_OPROJ>(C, gr, P.ld, 0, b, P.nwg); break;
+    case SK_GATEUP: sgemv_part<WT, SG_GATEUP>(C, gr, P.ld, 0, b, P.nwg); break;
+    default: sgemv_part<WT, SG_DOWN>(C, gr, P.ld, 0, b, P.nwg); break;
   }
-  if (tid < G) {
-    st_dev(rec + MAXQ * DH + tid, s_m[tid]);
-    st_dev(rec + MAXQ * DH + MAXQ + tid, s_l[tid]);
-  }
-  wait_own_stores();
-  __syncthreads();
-  if (tid == 0) {
-    const int t = __hip_atomic_fetch_add(&cnt[cidx], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (t == nsplit - 1);
-  }
-  __syncthreads();
-  if (!s_last) return;
-  const float* base = B.part + (size_t)cidx * C.max_splits * RS;
-  for (int e = tid; e < nsplit * G; e += kWG) {  // every split has >= 1 key, so m is finite
-    const int sp = e / G, qi = e % G;
-    s_pw[sp * MAXQ + qi] = ld_dev(base + (size_t)sp * RS + MAXQ * DH + qi);
-    s_pl[sp * MAXQ + qi] = ld_dev(base + (size_t)sp * RS + MAXQ * DH + MAXQ + qi);
-  }
-  __syncthreads();
-  if (tid < G) {  // split order, fixed
-    float M = -INFINITY;
-    for (int sp = 0; sp < nsplit; sp++) M = fmaxf(M, s_pw[sp * MAXQ + tid]);
-    float Ls = 0.f;
-    for (int sp = 0; sp < nsplit; sp++) Ls = fmaf(s_pl[sp * MAXQ + tid], expf(s_pw[sp * MAXQ + tid] - M), Ls);
-    s_m[tid] = M;
-    s_l[tid] = 1.0f / Ls;
-  }
-  __syncthreads();
-  for (int e = tid; e < nsplit * G; e += kWG) {
-    const int sp = e / G, qi = e % G;
-    s_pw[sp * MAXQ + qi] = expf(s_pw[sp * MAXQ + qi] - s_m[qi]) * s_l[qi];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int u = 0; u < MAXU; u++) {
-    const int qi = qg + u * NG;
-    if (qi < G) {
-      float A0 = 0.f, A1 = 0.f;
-      for (int sp0 = 0; sp0 < nsplit; sp0 += 8) {
-        float2 v[8];
-#pragma unroll
-        for (int j = 0; j < 8; j++)
-          v[j] = sp0 + j < nsplit ? ld_dev2(base + (size_t)(sp0 + j) * RS + qi * DH + 2 * dp) : make_float2(0.f, 0.f);
-#pragma unroll
-        for (int j = 0; j < 8; j++) {
-          if (sp0 + j < nsplit) {
-            const float f = s_pw[(sp0 + j) * MAXQ + qi];
-            A0 = fmaf(v[j].x, f, A0);
-            A1 = fmaf(v[j].y, f, A1);
-          }
-        }
-      }
-      out[qi * DH + 2 * dp] = A0;
-      out[qi * DH + 2 * dp + 1] = A1;
-    }
-  }
-  if (tid == 0) __hip_atomic_store(&cnt[cidx], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Merge the splits of each (group, KV head) in split order. Grid: x = KV head, y = group.
@@ -1253,16 +1012,27 @@ __global__ __launch_bounds__(kWG) void k_embed_rows(Ctx C, int t0, int nrows) {
   push_embedding<WT>(C, tok, C.pf_x + (size_t)i * C.d, C.pf_anch + (size_t)i * C.n * C.d);
 }
 
+// Zero what the next step's kernels count from: both argmax keys and the step kernel's ticket,
+// timeout flag and per-(phase, stage) counters. Plain stores: the next launch sees them.
+__device__ __forceinline__ void reset_step_sync(const Ctx& C) {
+  if (threadIdx.x < 2) *C.b[threadIdx.x].hkey = 0ull;
+  if (C.plan.sync != nullptr)
+    for (int i = threadIdx.x; i < C.plan.nsync; i += kWG) C.plan.sync[i] = 0;
+}
+
 // Greedy streaming verification (Section 3.4) and the pipeline state update; single workgroup,
 // last kernel of a step.
 template <typename WT>
 __global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int auto_rb) {
   __shared__ int s_tok, s_pos;
   DevState* st = C.st;
-  const int tiles = (C.V + kHeadRows - 1) / kHeadRows;
-  const int y_all = (st->a == C.n) ? reduce_head(C.b[0], tiles, C.V) : -1;
-  const int pd_all = reduce_head(C.b[1], tiles, C.V);
+  const int y_all = (st->a == C.n) ? take_head(C.b[0], C.V) : -1;
+  const int pd_all = take_head(C.b[1], C.V);
+  const int step_err = C.plan.sync != nullptr ? C.plan.sync[sync_err()] : 0;
+  __syncthreads();  // every thread has read the argmax keys and the timeout flag
+  reset_step_sync(C);
   if (threadIdx.x == 0) {
+    if (step_err) st->err = 1;
     const int c = st->c, a = st->a, n = C.n;
     const int pd = pd_all;
     st->pdm_draft = pd;
@@ -1333,7 +1103,9 @@ template <typename WT>
 __global__ __launch_bounds__(kWG) void k_reseed(Ctx C, int keep, int tok, int prompt_len) {
   __shared__ int s_tok;
   DevState* st = C.st;
-  const int yv = tok >= 0 ? tok : reduce_head(C.b[0], (C.V + kHeadRows - 1) / kHeadRows, C.V);
+  const int yv = tok >= 0 ? tok : take_head(C.b[0], C.V);
+  __syncthreads();  // every thread has read the argmax key
+  reset_step_sync(C);
   if (threadIdx.x == 0) {
     const int t = yv;
     if (tok < 0) st->y = t;
@@ -1362,13 +1134,9 @@ void set_launch_events(void* start, void* stop) {
   t_ev_start = (hipEvent_t)start;
   t_ev_stop = (hipEvent_t)stop;
 }
-
-template <typename F, typename... Args>
-static void launch_k(F kernel, dim3 grid, dim3 block, size_t shmem, hipStream_t s, Args... args) {
-  if (t_ev_start != nullptr)
-    hipExtLaunchKernelGGL(kernel, grid, block, (std::uint32_t)shmem, s, t_ev_start, t_ev_stop, 0u, args...);
-  else
-    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+void current_launch_events(hipEvent_t* start, hipEvent_t* stop) {
+  *start = t_ev_start;
+  *stop = t_ev_stop;
 }
 
 template <typename WT>
@@ -1379,58 +1147,82 @@ static inline size_t gemv_lds(int K, int nv) {
   return (size_t)nv * (kp < cap ? kp : cap) * sizeof(float);
 }
 
+// Workgroups per stage of a streaming stage launch: about c.stream_wgs (default kStreamWGs) in all, at least enough that no
+// wave streams more than 64 pairs (its epilogue values live one per lane), at most one per 4 pairs.
+static inline int stream_grid(const Ctx& c, int npairs, int nst) {
+  const int total = c.stream_wgs > 0 ? c.stream_wgs : kStreamWGs;
+  int wx = (total + nst - 1) / nst;
+  wx = std::max(wx, (npairs + 255) / 256);
+  wx = std::min(wx, (npairs + 3) / 4);
+  return std::max(wx, 1);
+}
+
+template <typename WT>
+static inline size_t stream_lds(int K) {
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  return (size_t)(K + BLK - 1) / BLK * BLK * sizeof(float);
+}
+
 template <typename WT>
 void Launch<WT>::qkv(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid((c.hq + 2 * c.hkv) * (c.dh / 8), r.kind == 0 ? c.n : 1);
-  if (r.kind == 0)
-    launch_k((k_qkv<WT, 1>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, r);
-  else
-    launch_k((k_qkv<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
+  if (r.kind == 0) {
+    const int np = (c.hq + 2 * c.hkv) * (c.dh / 2);
+    launch_timed((k_sgemv<WT, SG_QKV>), dim3(stream_grid(c, np, r.nst), r.nst), dim3(kWG), stream_lds<WT>(c.d), S(s), c, r);
+    return;
+  }
+  const dim3 grid((c.hq + 2 * c.hkv) * (c.dh / 8), 1);
+  launch_timed((k_qkv<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::oproj(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid((c.d + 7) / 8, r.kind == 0 ? c.n : 1);
-  if (r.kind == 0)
-    launch_k((k_proj_add<WT, 1, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, 1), S(s), c, r);
-  else
-    launch_k((k_proj_add<WT, kMaxRows, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, kMaxRows), S(s), c, r);
+  if (r.kind == 0) {
+    launch_timed((k_sgemv<WT, SG_OPROJ>), dim3(stream_grid(c, (c.d + 1) / 2, r.nst), r.nst), dim3(kWG),
+                 stream_lds<WT>(c.qdim), S(s), c, r);
+    return;
+  }
+  const dim3 grid((c.d + 7) / 8, 1);
+  launch_timed((k_proj_add<WT, kMaxRows, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, kMaxRows), S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::down(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid((c.d + 7) / 8, r.kind == 0 ? c.n : 1);
-  if (r.kind == 0)
-    launch_k((k_proj_add<WT, 1, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, 1), S(s), c, r);
-  else
-    launch_k((k_proj_add<WT, kMaxRows, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, kMaxRows), S(s), c, r);
+  if (r.kind == 0) {
+    launch_timed((k_sgemv<WT, SG_DOWN>), dim3(stream_grid(c, (c.d + 1) / 2, r.nst), r.nst), dim3(kWG),
+                 stream_lds<WT>(c.F), S(s), c, r);
+    return;
+  }
+  const dim3 grid((c.d + 7) / 8, 1);
+  launch_timed((k_proj_add<WT, kMaxRows, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, kMaxRows), S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::gateup(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid((c.F + 3) / 4, r.kind == 0 ? c.n : 1);
-  if (r.kind == 0)
-    launch_k((k_gateup<WT, 1>), grid, dim3(kWG), gemv_lds<WT>(c.d, 1), S(s), c, r);
-  else
-    launch_k((k_gateup<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
+  if (r.kind == 0) {
+    launch_timed((k_sgemv<WT, SG_GATEUP>), dim3(stream_grid(c, c.F, r.nst), r.nst), dim3(kWG), stream_lds<WT>(c.d),
+                 S(s), c, r);
+    return;
+  }
+  const dim3 grid((c.F + 3) / 4, 1);
+  launch_timed((k_gateup<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
 }
 
 template <typename WT, int MAXQ, int DH>
 static void attn_launch(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid(c.max_splits, c.hkv, r.kind == 0 ? c.n : 1);
-  launch_k((k_attn<WT, MAXQ, DH>), grid, dim3(kWG), (attn_lds<WT, MAXQ, DH>()), S(s), c, r);
-  const dim3 cgrid(c.hkv, r.kind == 0 ? c.n : 1);
-  launch_k((k_attn_combine<MAXQ, DH>), cgrid, dim3(kWG), 0, S(s), c, r);
+  const dim3 grid(c.max_splits, c.hkv, r.kind == 0 ? r.nst : 1);
+  launch_timed((k_attn<WT, MAXQ, DH>), grid, dim3(kWG), (attn_lds<WT, MAXQ, DH>()), S(s), c, r);
+  const dim3 cgrid(c.hkv, r.kind == 0 ? r.nst : 1);
+  launch_timed((k_attn_combine<MAXQ, DH>), cgrid, dim3(kWG), 0, S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::attn(const Ctx& c, const Rows& r, void* s) {
   if (r.kind == 0) {
-    const dim3 grid(c.max_splits, c.hkv, c.n);
+    const dim3 grid(c.max_splits, c.hkv, r.nst);
     if (c.dh == 128)
-      launch_k((k_attn_dec<WT, 128>), grid, dim3(kWG), 0, S(s), c, r, c.b[r.set].cnt);
+      launch_timed((k_attn_stage<WT, 128>), grid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
     else
-      launch_k((k_attn_dec<WT, 64>), grid, dim3(kWG), 0, S(s), c, r, c.b[r.set].cnt);
+      launch_timed((k_attn_stage<WT, 64>), grid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
     return;
   }
   if (c.dh == 128)
@@ -1440,9 +1232,24 @@ void Launch<WT>::attn(const Ctx& c, const Rows& r, void* s) {
 }
 
 template <typename WT>
+void Launch<WT>::mix(const Ctx& c, const MixLaunch& m, int nwg, void* s) {
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  int kmax = std::max(std::max(c.d, c.qdim), c.F);
+  kmax = (kmax + BLK - 1) / BLK * BLK;
+  size_t shm = (size_t)kmax * sizeof(float);
+  if (c.dh == 128) {
+    shm = std::max(shm, attn_split_lds<WT, 128>());
+    launch_timed((k_mix<WT, 128>), dim3(nwg), dim3(kWG), shm, S(s), c, m);
+  } else {
+    shm = std::max(shm, attn_split_lds<WT, 64>());
+    launch_timed((k_mix<WT, 64>), dim3(nwg), dim3(kWG), shm, S(s), c, m);
+  }
+}
+
+template <typename WT>
 void Launch<WT>::pdm_fc(const Ctx& c, int prefill, int nrows, void* s) {
   const dim3 grid((c.d + 7) / 8);
-  launch_k((k_pdm_fc<WT>), grid, dim3(kWG), gemv_lds<WT>(c.n * c.d, kMaxRows), S(s), c, prefill, nrows);
+  launch_timed((k_pdm_fc<WT>), grid, dim3(kWG), gemv_lds<WT>(c.n * c.d, kMaxRows), S(s), c, prefill, nrows);
 }
 
 template <typename WT>
@@ -1451,14 +1258,14 @@ void Launch<WT>::head(const Ctx& c, int src, int row, void* s) {
   constexpr int BLK = 64 * Elt<WT>::VE;
   const size_t kl_pad = (size_t)(c.d + BLK - 1) / BLK * BLK;
   if (src == 3)
-    launch_k((k_head<WT, 2>), grid, dim3(kWG), 2 * kl_pad * sizeof(float), S(s), c, src, row);
+    launch_timed((k_head<WT, 2>), grid, dim3(kWG), 2 * kl_pad * sizeof(float), S(s), c, src, row);
   else
-    launch_k((k_head<WT, 1>), grid, dim3(kWG), kl_pad * sizeof(float), S(s), c, src, row);
+    launch_timed((k_head<WT, 1>), grid, dim3(kWG), kl_pad * sizeof(float), S(s), c, src, row);
 }
 
 template <typename WT>
 void Launch<WT>::embed_rows(const Ctx& c, int t0, int nrows, void* s) {
-  launch_k((k_embed_rows<WT>), dim3(nrows), dim3(kWG), 0, S(s), c, t0, nrows);
+  launch_timed((k_embed_rows<WT>), dim3(nrows), dim3(kWG), 0, S(s), c, t0, nrows);
 }
 
 template struct Launch<float>;
@@ -1466,16 +1273,16 @@ template struct Launch<uint16_t>;
 
 void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* s, int bf16) {
   if (bf16)
-    launch_k((k_verify<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
+    launch_timed((k_verify<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
   else
-    launch_k((k_verify<float>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
+    launch_timed((k_verify<float>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
 }
 
 void launch_reseed(const Ctx& c, int keep, int tok, int prompt_len, void* s, int bf16) {
   if (bf16)
-    launch_k((k_reseed<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
+    launch_timed((k_reseed<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
   else
-    launch_k((k_reseed<float>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
+    launch_timed((k_reseed<float>), dim3(1), dim3(kWG), 0, S(s), c, keep, tok, prompt_len);
 }
 
 }  // namespace spd

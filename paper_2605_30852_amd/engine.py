@@ -155,6 +155,9 @@ class Engine:
     def spd_set_graph(self, on: bool) -> None:
         B.spd_set_graph(self.h, on)
 
+    def spd_set_step_kernel(self, mode: int, grid: int = 0, skew: int = -1) -> None:
+        B.spd_set_step_kernel(self.h, mode, grid, skew)
+
     def spd_set_debug(self, on: bool) -> None:
         B.spd_set_debug(self.h, on)
 

@@ -227,3 +227,74 @@ def test_graph_replay_matches_eager(mid_w):
     assert np.array_equal(engs[0].tokens(), engs[1].tokens())
     for e in engs:
         e.close()
+
+
+@pytest.mark.parametrize("which,n,mode,grid,skew", [
+    ("mid", 3, 1, 0, 0), ("mid", 3, 1, 1, 0), ("mid", 3, 1, 37, 1), ("mid", 1, 1, 5, 0), ("tiny", 2, 1, 0, 2),
+    ("tiny", 4, 1, 3, 1), ("mid", 3, 2, 0, -1), ("tiny", 4, 2, 0, -1), ("mid", 1, 2, 0, -1),
+    ("mid", 3, 3, 0, -1), ("mid", 3, 3, 7, -1), ("tiny", 4, 3, 0, -1), ("tiny", 3, 3, 0, -1), ("mid", 1, 3, 0, -1)])
+def test_step_modes_bit_identical_to_sublayer_launches(tiny_w, mid_w, which, n, mode, grid, skew):
+    """Every way of launching the stage compute gives the same bits as five launches per layer slot
+    covering all stages: decisions, tokens, in-flight residual streams and anchors after every step.
+    Mode 1 is the persistent step kernel (tiles taken from a ticket counter, data handed between
+    workgroups inside the launch; small grids make few workgroups walk the whole tile order, grid 1
+    strictly in ticket order, with the stages in lockstep or staggered); mode 2 runs each stage's
+    launches on its own stream; mode 3 is the skewed schedule of mixed launches (grid 7: few
+    workgroups per weight-streaming part)."""
+    _say(f"[step mode {mode} vs sublayer launches {which} n={n} grid={grid} skew={skew}]")
+    w = tiny_w if which == "tiny" else mid_w
+    sh = w.shape
+    prompt = synth.prompt(sh, SEED + 7, 41)
+    first, ar, _ = _gpu_stream(w, 1, prompt, 30, max_tokens=200)
+    mask = synth.accept_mask(0.6, 321 + n, 400)
+    table = forced_table(ar, mask, len(prompt), sh.vocab)
+    arr = np.full(len(table) + 8, -1, dtype=np.int32)
+    for q, t in table.items():
+        arr[q - len(prompt)] = t
+    engs = []
+    for m in (0, mode):
+        e = _engine(w, n, max_tokens=200, attn_chunk=32)
+        e.spd_set_step_kernel(m, grid if m == 1 else 0, skew if m == 1 else -1)
+        assert e.spd_prefill(prompt) == first
+        e.spd_set_forced_drafts(arr, len(prompt))
+        engs.append(e)
+    for i in range(18):
+        logs = [e.spd_run_steps(1, want_log=True) for e in engs]
+        assert logs[0] == logs[1], f"step {i}: {logs}"
+        c, a, _, _ = engs[0].state()
+        assert engs[1].state()[:2] == (c, a)
+        r0, r1 = engs[0].resid(), engs[1].resid()
+        an0, an1 = engs[0].anchors(), engs[1].anchors()
+        # only rows of in-flight tokens hold data (the rest of the workspace is uninitialised), and a
+        # token at depth k has anchors 0..k
+        for q in range(c, c + a):
+            k = c + a - 1 - q
+            assert np.array_equal(r0[q % n], r1[q % n]), f"step {i}: residual stream of position {q} differs"
+            assert np.array_equal(an0[q % n, : min(k, n - 1) + 1], an1[q % n, : min(k, n - 1) + 1]), \
+                f"step {i}: anchors of position {q} differ"
+    assert np.array_equal(engs[0].tokens(), engs[1].tokens())
+    for e in engs:
+        e.close()
+
+
+@pytest.mark.parametrize("chunk", [256, 384])
+def test_multi_pass_attention_splits(mid_w, chunk):
+    """Key splits longer than one 128-key pass (online softmax across passes inside a split, the
+    next pass's keys loaded while the current one is computed): oracle parity and the lossless
+    invariant against the GPU's plain greedy decode with the same split size."""
+    _say(f"[multi-pass attention chunk={chunk}]")
+    sh = synth.MID
+    model = om.Model(sh, SEED)
+    prompt = synth.prompt(sh, SEED + 8, 300)  # 300+ keys: splits of 2-3 passes and a ragged last split
+    ref = om.ar_greedy(model, prompt, 16)
+    mask = synth.accept_mask(0.6, SEED + 9, 600)
+    tab = forced_table(ref, mask, len(prompt), sh.vocab)
+    eng = _engine(mid_w, 3, max_tokens=400, attn_chunk=chunk)
+    w = run_lockstep(eng, model, prompt, 12, draft_for=lambda q: tab.get(q))
+    eng.close()
+    assert w["steps"] >= 6 or w["near_tie"]
+    first, ar, _ = _gpu_stream(mid_w, 1, prompt, 20, max_tokens=400, attn_chunk=chunk)
+    table = forced_table(ar, mask, len(prompt), sh.vocab)
+    f2, toks, res = _gpu_stream(mid_w, 3, prompt, 20, table, max_tokens=400, attn_chunk=chunk)
+    assert f2 == first
+    assert toks == ar[: len(toks)], "SPD stream differs from greedy decoding"
