@@ -220,10 +220,12 @@ def ar_greedy(model: Model, prompt, n_new: int, return_logits: bool = False):
     return (out, logs) if return_logits else out
 
 
-def forward_full(model: Model, tokens, layers_out=None) -> Dict[int, np.ndarray]:
+def forward_full(model: Model, tokens, layers_out=None, free_layers: bool = False) -> Dict[int, np.ndarray]:
     """Brute force without any cache: full causal attention over all rows at every layer.
 
-    Returns {l: H^l [T, d]} for l in layers_out (default: every l in 0..L)."""
+    Returns {l: H^l [T, d]} for l in layers_out (default: every l in 0..L). free_layers drops each
+    layer's weights once the layer is done (same arithmetic; for full-size models, whose float64
+    weights do not all fit in memory at once)."""
     sh = model.shape
     L, dh = sh.n_layers, sh.head_dim
     T = len(tokens)
@@ -255,4 +257,7 @@ def forward_full(model: Model, tokens, layers_out=None) -> Dict[int, np.ndarray]
         H = H + (silu(U @ lw["wg"].T) * (U @ lw["wu"].T)) @ lw["wd"].T
         if (l + 1) in layers_out:
             res[l + 1] = H.copy()
+        if free_layers:
+            del lw
+            model.drop(f"layer.{l}.")
     return res

@@ -1,0 +1,97 @@
+"""Parity at the full 4B-class size (36 layers, d 2560, 32/8 heads of 128, FFN 9728, vocabulary 151936,
+bf16 weights and KV, SPD width n = 4, one-layer draft module) in the launch configuration the benchmark
+times: stage compute on one stream per stage, every step replayed from the captured step graph, the
+exit and draft LM heads sharing one pass over the vocabulary.
+
+The prompt is short so that the float64 oracle can recompute every sampled output one by one: the GPU's
+in-flight residual streams and PDM anchors after each step, and the exit token's full-vocabulary logits,
+against the oracle's cache-free forward pass over the same tokens. Drafts are forced to the GPU's own
+plain greedy decode (n = 1) so that every step after the fill accepts and a token exits each step.
+Tolerances: hidden states rel L2 <= 2e-2, logits max abs <= 5e-2, top-1 identical unless the oracle's
+top-2 margin is below 1e-2."""
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import model as om
+from oracle import spd as osp
+from tests.lockstep import ABS_LOGIT, REL_HIDDEN, TIE_MARGIN, margin, rel_l2
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def test_fullsize_4b_step_parity():
+    from paper_2605_30852_amd.engine import DeviceWeights, Engine
+
+    sh = synth.B4
+    n, L, P, seed = sh.n_stages, sh.n_layers, 20, 0
+    prompt = synth.prompt(sh, seed, P)
+    chunk = max(64, (P // 16 + 63) // 64 * 64)  # the benchmark's split size for this prompt length
+    t0 = time.time()
+    _say("[fullsize 4b] uploading weights")
+    W = DeviceWeights(sh, seed, threads=16)
+    ar = Engine(W, max_tokens=P + 64, n=1, attn_chunk=chunk)
+    ar.spd_set_graph(True)
+    first = ar.spd_prefill(prompt)
+    ar.spd_run_steps(12)
+    ar.spd_sync()
+    ref = ar.tokens()[P:P + 13].astype(np.int32)
+    ar.close()
+    assert ref[0] == first
+    eng = Engine(W, max_tokens=P + 64, n=n, attn_chunk=chunk)
+    eng.spd_set_graph(True)
+    eng.spd_set_debug(True)
+    assert eng.spd_prefill(prompt) == first
+    eng.spd_set_forced_drafts(ref, P)
+    snaps = []
+    for i in range(8):
+        r = eng.spd_run_steps(1, want_log=True)[0]
+        c, a, _, _ = eng.state()
+        snaps.append((r, c, a, eng.resid().copy(), eng.anchors().copy(),
+                      eng.exit_logits().copy() if r["decision"] != 0 else None))
+    eng.close()
+    del W
+    torch.cuda.empty_cache()
+    _say(f"[fullsize 4b] GPU done in {time.time() - t0:.0f}s; oracle forward over the same tokens")
+    last = max(c + a for _, c, a, _, _, _ in snaps)
+    tokens = np.concatenate([prompt, ref[: last - P]])
+    model = om.Model(sh, seed)
+    beta = osp.stage_bounds(L, n)
+    full = om.forward_full(model, tokens, free_layers=True)
+    _say(f"[fullsize 4b] oracle done in {time.time() - t0:.0f}s")
+
+    lg = om.lm_logits(model, full[L][P - 1])
+    if om.argmax_first(lg) != first:
+        assert margin(lg) < TIE_MARGIN, f"prefill token {first} != oracle {om.argmax_first(lg)}"
+        return
+    worst_h, worst_l, exits = 0.0, 0.0, 0
+    for i, (r, c, a, res, anch, el) in enumerate(snaps):
+        for q in range(c, c + a):
+            k = c + a - 1 - q  # stages completed: the row holds H^{beta_k}
+            e = rel_l2(res[q % n], full[beta[k]][q])
+            worst_h = max(worst_h, e)
+            assert e <= REL_HIDDEN, f"step {i}: residual of position {q} (depth {k}) rel L2 {e:.3e}"
+            for j in range(min(k, n - 1) + 1):
+                e = rel_l2(anch[q % n][j], full[beta[j]][q])
+                worst_h = max(worst_h, e)
+                assert e <= REL_HIDDEN, f"step {i}: anchor {j} of position {q} rel L2 {e:.3e}"
+        if el is not None:
+            exits += 1
+            assert r["decision"] == osp.ACCEPT
+            lo = om.lm_logits(model, full[L][r["exited_pos"]])
+            e = float(np.max(np.abs(el - lo)))
+            worst_l = max(worst_l, e)
+            assert e <= ABS_LOGIT, f"step {i}: exit logits max abs {e:.3e}"
+            if r["target_argmax"] != om.argmax_first(lo):
+                assert margin(lo) < TIE_MARGIN, f"step {i}: target argmax differs"
+                break
+    _say(f"[fullsize 4b] worst hidden rel L2 {worst_h:.2e}, worst logit abs {worst_l:.2e}, {exits} exits")
+    assert exits >= 4
