@@ -157,11 +157,13 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="issue every launch instead of replaying the step graph")
     ap.add_argument("--separate-head", action="store_true",
                     help="the draft module runs its own LM-head pass on its stream instead of sharing the exit pass")
-    ap.add_argument("--step-mode", type=int, default=2, choices=[0, 1, 2, 3],
+    ap.add_argument("--step-mode", type=int, default=2, choices=[0, 1, 2, 3, 4],
                     help="stage compute: 0 five launches per layer slot covering all stages, 1 one persistent "
                          "launch per step, 2 (default) one stream per stage, 3 skewed launches, each mixing "
-                         "independent sublayers of different stages")
+                         "independent sublayers of different stages, 4 one persistent launch with a group of "
+                         "workgroups per stage")
     ap.add_argument("--step-grid", type=int, default=0, help="workgroups of the persistent step launch (0: default)")
+    ap.add_argument("--attn-chunk", type=int, default=0, help="keys per attention split (0: the workload's default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (the known-size kernel for HBM counter scaling)")
     args = ap.parse_args()
@@ -190,7 +192,7 @@ def main():
     # capacity and attention split size depend on the workload only (not on --steps), so that a
     # profiled run with fewer steps launches exactly the kernels the timed run launches
     max_tokens = P + max(1024, n_ref + 4 * n + 64)
-    attn_chunk = max(64, (P // 16 + 63) // 64 * 64)
+    attn_chunk = args.attn_chunk or max(64, (P // 16 + 63) // 64 * 64)
 
     if args.copy_calibration:
         src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
@@ -277,7 +279,7 @@ def main():
         return ms, nl, (ca + cb) // 2
 
     kernels = {}
-    if mode == 1:
+    if mode in (1, 4):
         classes = (("step", B.SPD_K_STEP), ("head", B.SPD_K_HEAD))
         dominant = "step"
     elif mode == 3:
@@ -369,7 +371,8 @@ def main():
                    "stage_compute": {0: "five launches per layer slot covering all stages",
                                      1: "one persistent launch per step",
                                      2: "one stream per stage, five launches per layer slot",
-                                     3: "skewed schedule: 5J+n-1 launches, launch L runs sublayer L-s of stage s"}[mode],
+                                     3: "skewed schedule: 5J+n-1 launches, launch L runs sublayer L-s of stage s",
+                                     4: "one persistent launch per step, a group of workgroups per stage"}[mode],
                    "step_grid": args.step_grid or None},
         "bytes_per_step": int(bytes_step),
         "step_GBps": round(gbs, 1),
@@ -380,7 +383,9 @@ def main():
                                 1: "k_step: the persistent launch running every layer slot of all n stages",
                                 2: "k_sgemv gate/up of one stage (stage streams run concurrently)",
                                 3: "k_mix: the skewed launches of the stage compute (all layers' weights and KV; "
-                                   "bytes and time summed over the launches of a step)"}[mode],
+                                   "bytes and time summed over the launches of a step)",
+                                4: "k_pstep: the persistent launch running every layer slot of all n stages, "
+                                   "one group of workgroups per stage"}[mode],
                      "bytes_per_launch": dk["bytes_per_launch"], "us_per_launch": dk["us_per_launch"],
                      "timing": f"dispatch-recorded HIP events on the main stream, layer slots >= {first_slot} of "
                                f"{L_slots}, {K_GU} steady-state steps"},

@@ -180,9 +180,12 @@ spd_status spd_sync(spd_handle* h, spd_step_result* last);
  *   SPD_DBG_STEP_ITEMS:  nitems uint32, the persistent step launch's tile of each ticket:
  *                        phase p = item >> 19 (layer slot p / 5, sublayer p % 5 in the order QKV,
  *                        attention, O-proj, gate/up, down), stage (item >> 16) & 7, tile item & 0xffff
- *   SPD_DBG_STEP_TRACE:  nitems x 4 uint64 wall-clock stamps per ticket of the last traced step
- *                        (spd_set_step_trace): start, inputs ready, input staged, end (0: not reached)
- * bytes must equal the size listed (nitems from spd_step_plan_info). */
+ *   SPD_DBG_STEP_TRACE:  ntrace uint64 wall-clock stamps of the last traced step (spd_set_step_trace;
+ *                        0: not reached). Ticket-queue kernel: 4 per ticket (start, inputs ready, input
+ *                        staged, end) in the first 4*nitems. Grouped kernel: 3 per workgroup and sublayer
+ *                        (wait start, wait end, end) at ((workgroup * 5J) + sublayer) * 3; workgroups
+ *                        whose stamps would not fit record none.
+ * bytes must equal the size listed (nitems and ntrace from spd_step_plan_info). */
 enum {
   SPD_DBG_RESID = 1,
   SPD_DBG_ANCHORS = 2,
@@ -224,10 +227,16 @@ spd_status spd_set_graph(spd_handle* h, int32_t on);
  *           launches per step. The parts of a launch belong to different stages and are independent,
  *           so one stage's latency-bound attention runs under the others' weight streaming and every
  *           launch streams several stages' worth of weights.
+ *   mode 4: one persistent launch per step in which every active stage has its own group of
+ *           workgroups (`grid` in all, 0: 512, at most what the GPU holds at once); a group walks its
+ *           stage's sublayers in order, each workgroup streaming a contiguous share of each sublayer
+ *           and waiting (bounded) for its group only before reading what the previous sublayer wrote,
+ *           with its first weights for that sublayer already requested. Stages never wait for each
+ *           other. SPD_E_INVAL if the GPU cannot hold enough workgroups for the configuration.
  * In modes 0, 2 and 3 `grid` sets the workgroups of one sublayer launch, or of the weight-streaming
  * parts of one mixed launch (0: the default): each stages its input vector once and its waves stream
  * their weight rows back to back.
- * SPD_K_STEP times the persistent launch, SPD_K_MIX the launches of mode 3; the per-sublayer timing
+ * SPD_K_STEP times the persistent launch (modes 1 and 4), SPD_K_MIX the launches of mode 3; the per-sublayer timing
  * classes time modes 0 and 2. */
 spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t skew);
 
@@ -235,8 +244,9 @@ spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_
  * SPD_DBG_STEP_TRACE; each step overwrites them). Costs a few stores per tile. */
 spd_status spd_set_step_trace(spd_handle* h, int32_t on);
 
-/* info (host, 8 int32): number of tickets of one step, layer slots J, tiles per stage of QKV,
- * attention, O-proj, gate/up and down, and the wall-clock rate of the trace stamps in kHz. */
+/* info (host, 10 int32): number of tickets of one step, layer slots J, tiles per stage of QKV,
+ * attention, O-proj, gate/up and down, the wall-clock rate of the trace stamps in kHz, the stamps the
+ * trace buffer holds (ntrace) and the grouped kernel's grid (0 until mode 4 is chosen). */
 spd_status spd_step_plan_info(spd_handle* h, int32_t* info);
 
 /* 1: every LM-head pass also writes its full logits (for SPD_DBG_*_LOGITS). */

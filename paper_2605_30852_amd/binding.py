@@ -243,9 +243,10 @@ def spd_set_step_trace(h: int, on: bool) -> None:
 
 
 def spd_step_plan_info(h: int) -> dict:
-    info = (ct.c_int32 * 8)()
+    info = (ct.c_int32 * 10)()
     _check("spd_step_plan_info", lib().spd_step_plan_info(h, info), h)
-    return {"nitems": info[0], "J": info[1], "tiles": list(info[2:7]), "clock_khz": info[7]}
+    return {"nitems": info[0], "J": info[1], "tiles": list(info[2:7]), "clock_khz": info[7],
+            "ntrace": info[8], "pstep_grid": info[9]}
 
 
 def spd_step_trace(h: int) -> dict:
@@ -253,8 +254,9 @@ def spd_step_trace(h: int) -> dict:
     info = spd_step_plan_info(h)
     n = info["nitems"]
     items = spd_read_debug(h, SPD_DBG_STEP_ITEMS, n, np.uint32)
-    stamps = spd_read_debug(h, SPD_DBG_STEP_TRACE, 4 * n, np.uint64).reshape(n, 4)
-    return {"items": items, "stamps": stamps, **info}
+    raw = spd_read_debug(h, SPD_DBG_STEP_TRACE, info["ntrace"], np.uint64)
+    stamps = raw[: 4 * n].reshape(n, 4)
+    return {"items": items, "stamps": stamps, "raw": raw, **info}
 
 
 def spd_destroy(h: int) -> None:

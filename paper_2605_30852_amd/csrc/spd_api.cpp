@@ -27,7 +27,7 @@ struct Layout {
   size_t q[2], ao[2], act[2], part[2], cnt[2], hkey[2];
   size_t items, sync, dctx, trace;
   size_t total;
-  int num_pages, chunk, max_splits, J, nitems, nsync;
+  int num_pages, chunk, max_splits, J, nitems, nsync, ntrace;
   int tiles[5];
   size_t kv_layer_bytes;
 };
@@ -92,7 +92,7 @@ Layout make_layout(const spd_config& c) {
   L.tiles[SK_DOWN] = (d + kDRows - 1) / kDRows;
   L.nitems = 0;
   for (int k = 0; k < 5; k++) L.nitems += L.J * n * L.tiles[k];
-  L.nsync = (2 + 5 * L.J * n) * kSyncStride;
+  L.nsync = (2 + std::max(5 * L.J * n, kMaxStages * kBarParts)) * kSyncStride;
   L.kv_layer_bytes = (size_t)L.num_pages * 2 * hkv * c.page_size * dh * esz;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -128,7 +128,8 @@ Layout make_layout(const spd_config& c) {
   L.items = take(sizeof(uint32_t) * (size_t)L.nitems);
   L.sync = take(sizeof(int32_t) * (size_t)L.nsync);
   L.dctx = take(sizeof(Ctx));
-  L.trace = take(sizeof(unsigned long long) * 4 * (size_t)L.nitems);
+  L.ntrace = std::max(4 * L.nitems, 2048 * 5 * L.J * 3);
+  L.trace = take(sizeof(unsigned long long) * (size_t)L.ntrace);
   L.total = o;
   return L;
 }
@@ -184,6 +185,7 @@ struct spd_handle {
   int step_mode = kStepModeDefault;
   int step_grid = kStepGridDefault;
   int step_skew = kStepSkewDefault;
+  int pstep_grid = 0;  // mode 4: workgroups, at most what the GPU holds at once
   hipGraphExec_t gexec = nullptr;
   // kernel timing
   int timed_kernel = 0;
@@ -299,6 +301,10 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     h->cur_slot = 0;
     TimedLaunch t(h, h->main, SPD_K_STEP);
     launch_step(C, (const Ctx*)(h->ws + h->lay.dctx), h->step_grid, h->main, h->bf16);
+  } else if (h->step_mode == 4) {
+    h->cur_slot = 0;
+    TimedLaunch t(h, h->main, SPD_K_STEP);
+    Launch<WT>::pstep(C, (const Ctx*)(h->ws + h->lay.dctx), h->pstep_grid, h->main);
   } else if (h->step_mode == 3) {
     // skewed schedule: launch L runs sublayer L - s of every stage s (Section 3.1's stages advance
     // independently within a step), so each launch mixes independent sublayers of different stages
@@ -571,6 +577,7 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   stage_bounds(c.n_layers, c.n_stages, C.beta);
   h->J = 0;
   for (int s = 0; s < c.n_stages; s++) h->J = std::max(h->J, C.beta[s + 1] - C.beta[s]);
+  C.J = h->J;
   char* ws = h->ws;
   C.lay = (const LayerDesc*)(ws + lay.lay);
   C.embed = w->embed;
@@ -606,6 +613,7 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   C.plan.nsync = lay.nsync;
   for (int k = 0; k < 5; k++) C.plan.tiles[k] = lay.tiles[k];
   C.plan.trace = nullptr;
+  C.plan.ntrace = lay.ntrace;
   const std::vector<uint32_t> items = step_items(lay, c.n_stages, kStepSkewDefault);
 
   // layer table
@@ -670,12 +678,40 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
 static void drop_graph(spd_handle* h);
 static spd_status run_one_step(spd_handle* h, int forced_override);
 
+// Workgroups of the grouped persistent step kernel: the requested number (0: kStepGridDefault),
+// at most what the GPU holds at once (its per-stage waits need every workgroup resident), and at least
+// enough per stage that no wave streams more than 64 row pairs.
+static spd_status size_pstep(spd_handle* h, int grid) {
+  const Ctx& C = h->ctx;
+  int per_cu = 0, cus = 0;
+  const void* fn = h->bf16 ? Launch<uint16_t>::pstep_fn(C) : Launch<float>::pstep_fn(C);
+  const size_t lds = h->bf16 ? Launch<uint16_t>::pstep_lds(C) : Launch<float>::pstep_lds(C);
+  HIPC(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kWG, lds));
+  HIPC(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->dev));
+  const int cap = per_cu * cus;
+  int g = std::min(grid > 0 ? grid : kStepGridDefault, cap);
+  const int npmax = std::max(std::max(C.F, (C.hq + 2 * C.hkv) * (C.dh / 2)), (C.d + 1) / 2);
+  const int need = h->cfg.n_stages * ((npmax + 255) / 256);
+  if (g < need) {
+    h->err = "grouped step kernel: the GPU holds " + std::to_string(cap) + " workgroups, " + std::to_string(need) +
+             " are needed";
+    return SPD_E_INVAL;
+  }
+  h->pstep_grid = g;
+  return SPD_OK;
+}
+
 spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t skew) {
-  if (!h || mode < 0 || mode > 3 || grid < 0 || grid > 65535 || skew < -1 || skew > 16) return SPD_E_INVAL;
+  if (!h || mode < 0 || mode > 4 || grid < 0 || grid > 65535 || skew < -1 || skew > 16) return SPD_E_INVAL;
+  if (mode == 4) {
+    HIPC(hipSetDevice(h->dev));
+    spd_status st = size_pstep(h, grid);
+    if (st != SPD_OK) return st;
+  }
   h->step_mode = mode;
   if (mode == 1)
     h->step_grid = grid ? grid : kStepGridDefault;
-  else
+  else if (mode != 4)
     h->ctx.stream_wgs = grid;  // 0: default
   if (skew >= 0 && skew != h->step_skew) {
     HIPC(hipSetDevice(h->dev));
@@ -695,7 +731,7 @@ spd_status spd_set_step_trace(spd_handle* h, int32_t on) {
   HIPC(hipStreamSynchronize(h->pdm));
   HIPC(hipStreamSynchronize(h->main));
   h->ctx.plan.trace = on ? (unsigned long long*)(h->ws + h->lay.trace) : nullptr;
-  if (on) HIPC(hipMemset(h->ws + h->lay.trace, 0, sizeof(unsigned long long) * 4 * (size_t)h->lay.nitems));
+  if (on) HIPC(hipMemset(h->ws + h->lay.trace, 0, sizeof(unsigned long long) * (size_t)h->lay.ntrace));
   HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
   drop_graph(h);
   return SPD_OK;
@@ -709,6 +745,8 @@ spd_status spd_step_plan_info(spd_handle* h, int32_t* info) {
   int khz = 0;
   HIPC(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->dev));
   info[7] = khz;
+  info[8] = h->lay.ntrace;
+  info[9] = h->pstep_grid;
   return SPD_OK;
 }
 
@@ -923,7 +961,7 @@ spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes)
     case SPD_DBG_STEP_ITEMS: src = h->ctx.plan.items; need = sizeof(uint32_t) * (size_t)h->lay.nitems; break;
     case SPD_DBG_STEP_TRACE:
       src = h->ws + h->lay.trace;
-      need = sizeof(unsigned long long) * 4 * (size_t)h->lay.nitems;
+      need = sizeof(unsigned long long) * (size_t)h->lay.ntrace;
       break;
     default: return SPD_E_INVAL;
   }

@@ -79,6 +79,9 @@ constexpr int kSyncStride = 32;  // ints per line
 __host__ __device__ inline int sync_ticket() { return 0; }
 __host__ __device__ inline int sync_err() { return kSyncStride; }
 __host__ __device__ inline int sync_done(int p, int s, int n) { return (2 + p * n + s) * kSyncStride; }
+// grouped persistent kernel: stage s's arrival counters, kBarParts of them (one line each)
+constexpr int kBarParts = 8;
+__host__ __device__ inline int sync_bar(int s) { return (2 + s * kBarParts) * kSyncStride; }
 
 struct StepPlan {
   const uint32_t* items;  // ticket -> item
@@ -87,6 +90,8 @@ struct StepPlan {
   int nsync;              // ints in sync ((2 + 5J*n) * kSyncStride)
   int tiles[5];           // tiles per stage per sublayer kind (attention: Hkv * max_splits)
   unsigned long long* trace;  // null, or per ticket 4 wall-clock stamps: start, inputs ready, staged, end
+                              // (grouped kernel: per workgroup and sublayer 3 stamps: wait start, wait end, end)
+  int ntrace;                 // stamps the trace buffer holds
 };
 
 struct Ctx {
@@ -120,6 +125,7 @@ struct Ctx {
   BufSet b[2];      // 0: target stream, 1: PDM stream
   StepPlan plan;    // persistent step kernel
   int stream_wgs;   // workgroups of one streaming stage launch (all its stages)
+  int J;            // layer slots per step (longest stage)
 };
 
 // Which rows a launch works on.
@@ -176,6 +182,10 @@ struct Launch {
   static void embed_rows(const Ctx& c, int t0, int nrows, void* stream);
   // one launch of the skewed schedule, nwg workgroups
   static void mix(const Ctx& c, const MixLaunch& m, int nwg, void* stream);
+  // the grouped persistent step kernel (dev_ctx: a device copy of c), its LDS bytes and function
+  static void pstep(const Ctx& c, const Ctx* dev_ctx, int grid, void* stream);
+  static size_t pstep_lds(const Ctx& c);
+  static const void* pstep_fn(const Ctx& c);
 };
 void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* stream, int bf16);
 // Every layer slot of every active stage of one step in one persistent launch (spd_step.hip).

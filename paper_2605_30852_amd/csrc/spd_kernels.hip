@@ -426,10 +426,12 @@ __global__ __launch_bounds__(kWG) void k_gateup(Ctx C, Rows R) {
 enum SKind { SG_QKV = 0, SG_OPROJ = 2, SG_GATEUP = 3, SG_DOWN = 4 };
 
 // Workgroup bx of nbx working on one stage's sublayer (gr: the stage's row, Ld: its layer, set: the
-// scratch set).
-template <typename WT, int KIND>
+// scratch set). wait_inputs runs after the first weight units are requested and before anything the
+// previous sublayer wrote is read. COH: the inputs were written, and the outputs are read, by other
+// workgroups of the same launch (device-scope loads and stores).
+template <typename WT, int KIND, bool COH, typename WaitFn>
 __device__ __forceinline__ void sgemv_part(const Ctx& C, const Grp& gr, const LayerDesc& Ld, int set, int bx,
-                                           int nbx) {
+                                           int nbx, const WaitFn& wait_inputs) {
   extern __shared__ __align__(16) float lds[];
   __shared__ float red[4];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -466,20 +468,22 @@ __device__ __forceinline__ void sgemv_part(const Ctx& C, const Grp& gr, const La
       pv = C.rope[(size_t)pos * half + j];
     }
     page = C.page_table[pos / C.page];
-  } else if (KIND == SG_OPROJ || KIND == SG_DOWN) {
+  }
+  wait_inputs();
+  if (KIND == SG_OPROJ || KIND == SG_DOWN) {
     if (lane < count) {
       const int m = 2 * (wv + lane * NW);
-      pv.x = x[m];
-      pv.y = m + 1 < d ? x[m + 1] : 0.f;
+      pv.x = COH ? ld_dev(x + m) : x[m];
+      pv.y = m + 1 < d ? (COH ? ld_dev(x + m + 1) : x[m + 1]) : 0.f;
     }
   }
   float sc = 1.f;
   if (KIND == SG_QKV || KIND == SG_GATEUP) {
-    const float ss = stage_vec<Elt<WT>::VE, false>(x, KIND == SG_QKV ? Ld.attn_norm : Ld.mlp_norm, d, lds, red);
+    const float ss = stage_vec<Elt<WT>::VE, COH>(x, KIND == SG_QKV ? Ld.attn_norm : Ld.mlp_norm, d, lds, red);
     sc = 1.0f / sqrtf(ss / (float)d + C.eps);
   } else {
-    stage_vec<Elt<WT>::VE, false>((KIND == SG_OPROJ ? C.b[set].ao : C.b[set].act) + (size_t)gr.brow0 * K,
-                                  nullptr, K, lds, red);
+    stage_vec<Elt<WT>::VE, COH>((KIND == SG_OPROJ ? C.b[set].ao : C.b[set].act) + (size_t)gr.brow0 * K,
+                                nullptr, K, lds, red);
   }
   float* cap = nullptr;
   if (KIND == SG_DOWN && gr.layer + 1 == C.beta[gr.s + 1] && gr.s + 1 <= C.n - 1)
@@ -499,27 +503,47 @@ __device__ __forceinline__ void sgemv_part(const Ctx& C, const Grp& gr, const La
       }
       if (head < C.hq) {
         float* qo = C.b[set].q + (size_t)gr.brow0 * C.qdim + head * dh;
-        qo[j] = lo;
-        qo[j + half] = hi;
+        if (COH) {
+          st_dev(qo + j, lo);
+          st_dev(qo + j + half, hi);
+        } else {
+          qo[j] = lo;
+          qo[j + half] = hi;
+        }
       } else {
         const int hk = head < C.hq + C.hkv ? head - C.hq : head - C.hq - C.hkv;
         WT* kv = (WT*)Ld.kv;
         const size_t off = (size_t)page * (2 * C.hkv * C.page * dh) + ((size_t)hk * C.page + (pos % C.page)) * dh + j +
                            (head < C.hq + C.hkv ? 0 : (size_t)C.hkv * C.page * dh);
-        st1<WT>(kv, off, lo);
-        st1<WT>(kv, off + half, hi);
+        if (COH) {
+          st_kv_dev<WT>(kv + off, lo);
+          st_kv_dev<WT>(kv + off + half, hi);
+        } else {
+          st1<WT>(kv, off, lo);
+          st1<WT>(kv, off + half, hi);
+        }
       }
     } else if (KIND == SG_GATEUP) {
       const float g = s0 * sc, u = s1 * sc;
-      C.b[set].act[(size_t)gr.brow0 * C.F + q] = g / (1.0f + expf(-g)) * u;
+      float* ao = C.b[set].act + (size_t)gr.brow0 * C.F + q;
+      if (COH)
+        st_dev(ao, g / (1.0f + expf(-g)) * u);
+      else
+        *ao = g / (1.0f + expf(-g)) * u;
     } else {
       const int m = 2 * q;
       const float n0 = v.x + s0;
-      x[m] = n0;
+      if (COH)
+        st_dev(x + m, n0);
+      else
+        x[m] = n0;
       if (cap != nullptr) cap[m] = n0;
       if (m + 1 < d) {
         const float n1 = v.y + s1;
-        x[m + 1] = n1;
+        if (COH)
+          st_dev(x + m + 1, n1);
+        else
+          x[m + 1] = n1;
         if (cap != nullptr) cap[m + 1] = n1;
       }
     }
@@ -531,7 +555,7 @@ template <typename WT, int KIND>
 __global__ __launch_bounds__(kWG) void k_sgemv(Ctx C, Rows R) {
   const Grp gr = resolve(C, R, blockIdx.y);
   if (!gr.active) return;
-  sgemv_part<WT, KIND>(C, gr, R.ld[gr.s], R.set, blockIdx.x, gridDim.x);  // stage launches carry their layers
+  sgemv_part<WT, KIND, false>(C, gr, R.ld[gr.s], R.set, blockIdx.x, gridDim.x, [] {});  // stage launches carry their layers
 }
 
 // ---------------------------------------------------------------------- PDM feature projection
@@ -949,10 +973,116 @@ __global__ __launch_bounds__(kWG) void k_mix(Ctx C, MixLaunch M) {
   const Grp gr = resolve(C, R, 0);
   if (!gr.active) return;
   switch (P.kind) {
-    case SK_QKV: sgemv_part<WT, SG_QKV>(C, gr, P.ld, 0, b, P.nwg); break;
-    case SK_OPROJ: sgemv_part<WT, SG_OPROJ>(C, gr, P.ld, 0, b, P.nwg); break;
-    case SK_GATEUP: sgemv_part<WT, SG_GATEUP>(C, gr, P.ld, 0, b, P.nwg); break;
-    default: sgemv_part<WT, SG_DOWN>(C, gr, P.ld, 0, b, P.nwg); break;
+    case SK_QKV: sgemv_part<WT, SG_QKV, false>(C, gr, P.ld, 0, b, P.nwg, [] {}); break;
+    case SK_OPROJ: sgemv_part<WT, SG_OPROJ, false>(C, gr, P.ld, 0, b, P.nwg, [] {}); break;
+    case SK_GATEUP: sgemv_part<WT, SG_GATEUP, false>(C, gr, P.ld, 0, b, P.nwg, [] {}); break;
+    default: sgemv_part<WT, SG_DOWN, false>(C, gr, P.ld, 0, b, P.nwg, [] {}); break;
+  }
+}
+
+// ----------------------------------------------------------------- grouped persistent step kernel
+// Every layer slot of every active stage in one launch, each active stage on its own group of
+// workgroups (workgroup b works for stage b mod a). A group walks its stage's sublayers in order; a
+// workgroup streams a contiguous share of each sublayer's weight rows (or of its attention splits)
+// and then counts itself on the stage's counter. Before it reads anything the previous sublayer
+// wrote, it waits until every workgroup of its group has counted that sublayer, but its first
+// weight units for the sublayer are requested before that wait, so the stream goes on while it
+// waits. Stages never wait for each other, so one stage's attention and waits overlap the other
+// stages' weight streaming. Values handed between workgroups use device-scope stores and loads.
+//
+// The per-stage waits need every workgroup of the launch to be resident at once: the host sizes the
+// grid to what the GPU holds, and every wait is bounded (a timeout raises the launch's flag, which
+// the host reports, and lets the grid drain).
+// One attention tile of the grouped kernel, kept out of line: it runs a few times per workgroup and
+// step, and inlining it would add its registers to the weight-streaming sublayers'.
+template <typename WT, int DH>
+__device__ __noinline__ void pstep_attn_tile(const Ctx& C, const void* kv, int s, int g, int split, int nsplit,
+                                             int pos0) {
+  extern __shared__ __align__(16) float lds[];
+  constexpr int RS = kAttnMaxQ * (DH + 2);
+  const int k0 = split * C.chunk, k1 = min(pos0 + 1, k0 + C.chunk);
+  const int page0 = C.page_table[min((k0 + (int)threadIdx.x / kAttnTPK) / C.page, C.max_pages - 1)];
+  const int cidx = s * C.hkv + g;
+  const BufSet& B = C.b[0];
+  attn_split<WT, DH, true>(C, (const WT*)kv, B.q + (size_t)s * C.qdim + g * C.G * DH,
+                           B.ao + (size_t)s * C.qdim + g * C.G * DH, B.part + (size_t)cidx * C.max_splits * RS,
+                           B.cnt + cidx, g, split, nsplit, k0, k1, pos0, page0, lds);
+}
+
+// The weight-streaming sublayers of the grouped kernel, each out of line for the same reason.
+template <typename WT, int KIND>
+__device__ __noinline__ void pstep_gemv(const Ctx& C, const Grp& gr, const LayerDesc& Ld, int bx, int nb, int* sync,
+                                        int bar, int target, unsigned long long* tr) {
+  sgemv_part<WT, KIND, true>(C, gr, Ld, 0, bx, nb, [&] {
+    if (tr != nullptr && threadIdx.x == 0) tr[0] = (unsigned long long)wall_clock64();
+    if (threadIdx.x == 0 && target > 0) wait_count_sum(sync, bar, kBarParts, target);
+    __syncthreads();
+    if (tr != nullptr && threadIdx.x == 0) tr[1] = (unsigned long long)wall_clock64();
+  });
+}
+
+template <typename WT, int DH>
+__global__ __launch_bounds__(kWG, 3) void k_pstep(const Ctx* __restrict__ Cp) {
+  extern __shared__ __align__(16) float lds[];
+  const Ctx& C = *Cp;
+  const int a = C.st->a, c = C.st->c;  // pre-step state; only the verify kernel changes it
+  if (a <= 0) return;
+  const int s = blockIdx.x % a, bx = blockIdx.x / a;
+  const int nb = ((int)gridDim.x - 1 - s) / a + 1;  // workgroups of this stage's group
+  int* sync = C.plan.sync;
+  const int bar = sync_bar(s);
+  int phase = 0;  // sublayers this group has finished
+  // tracing: per workgroup and sublayer, wall-clock stamps at wait start, wait end and sublayer end
+  auto trp = [&](int ph) -> unsigned long long* {
+    const size_t at = ((size_t)blockIdx.x * 5 * C.J + ph) * 3;
+    return C.plan.trace != nullptr && at + 3 <= (size_t)C.plan.ntrace ? C.plan.trace + at : nullptr;
+  };
+  auto arrive = [&]() {
+    wait_own_stores();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      __hip_atomic_fetch_add(sync + bar + (bx % kBarParts) * kSyncStride, 1, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+      unsigned long long* t = trp(phase);
+      if (t != nullptr) t[2] = (unsigned long long)wall_clock64();
+    }
+    phase++;
+  };
+  auto wait_prev = [&]() {
+    unsigned long long* t = trp(phase);
+    if (t != nullptr && threadIdx.x == 0) t[0] = (unsigned long long)wall_clock64();
+    if (threadIdx.x == 0 && phase > 0) wait_count_sum(sync, bar, kBarParts, phase * nb);
+    __syncthreads();
+    if (t != nullptr && threadIdx.x == 0) t[1] = (unsigned long long)wall_clock64();
+  };
+  Rows R;
+  R.kind = 0;
+  R.stage0 = s;
+  R.nst = 1;
+  for (int j = 0; j < C.J; j++) {
+    R.slot = j;
+    const Grp gr = resolve(C, R, 0);
+    if (!gr.active) break;  // a shorter stage has no layer in this slot
+    const LayerDesc& Ld = C.lay[gr.layer];
+    pstep_gemv<WT, SG_QKV>(C, gr, Ld, bx, nb, sync, bar, phase * nb, trp(phase));
+    arrive();
+    {  // attention: the stage's (KV head, split) tiles, shared out over the group
+      const int pos0 = gr.pos0;
+      const int nsplit = (pos0 + C.chunk) / C.chunk;
+      const int ntile = C.hkv * nsplit;
+      wait_prev();
+      for (int t = bx; t < ntile; t += nb) {
+        pstep_attn_tile<WT, DH>(C, Ld.kv, s, t / nsplit, t % nsplit, nsplit, pos0);
+        __syncthreads();  // LDS free for the next tile
+      }
+      arrive();
+    }
+    pstep_gemv<WT, SG_OPROJ>(C, gr, Ld, bx, nb, sync, bar, phase * nb, trp(phase));
+    arrive();
+    pstep_gemv<WT, SG_GATEUP>(C, gr, Ld, bx, nb, sync, bar, phase * nb, trp(phase));
+    arrive();
+    pstep_gemv<WT, SG_DOWN>(C, gr, Ld, bx, nb, sync, bar, phase * nb, trp(phase));
+    arrive();
   }
 }
 
@@ -1244,6 +1374,28 @@ void Launch<WT>::mix(const Ctx& c, const MixLaunch& m, int nwg, void* s) {
     shm = std::max(shm, attn_split_lds<WT, 64>());
     launch_timed((k_mix<WT, 64>), dim3(nwg), dim3(kWG), shm, S(s), c, m);
   }
+}
+
+template <typename WT>
+size_t Launch<WT>::pstep_lds(const Ctx& c) {
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  int kmax = std::max(std::max(c.d, c.qdim), c.F);
+  kmax = (kmax + BLK - 1) / BLK * BLK;
+  const size_t attn = c.dh == 128 ? attn_split_lds<WT, 128>() : attn_split_lds<WT, 64>();
+  return std::max((size_t)kmax * sizeof(float), attn);
+}
+
+template <typename WT>
+const void* Launch<WT>::pstep_fn(const Ctx& c) {
+  return c.dh == 128 ? (const void*)k_pstep<WT, 128> : (const void*)k_pstep<WT, 64>;
+}
+
+template <typename WT>
+void Launch<WT>::pstep(const Ctx& c, const Ctx* dev_ctx, int grid, void* s) {
+  if (c.dh == 128)
+    launch_timed((k_pstep<WT, 128>), dim3(grid), dim3(kWG), pstep_lds(c), S(s), dev_ctx);
+  else
+    launch_timed((k_pstep<WT, 64>), dim3(grid), dim3(kWG), pstep_lds(c), S(s), dev_ctx);
 }
 
 template <typename WT>

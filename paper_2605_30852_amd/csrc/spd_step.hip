@@ -36,36 +36,6 @@ namespace spd {
 
 namespace {
 
-constexpr int kSpinLimit = 1 << 20;  // polls of one dependency wait (roughly a second) before giving up
-
-__device__ __forceinline__ int ld_dev_i(const int* p) {
-  return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-template <typename T>
-__device__ __forceinline__ void st_kv_dev(T* p, float v);
-template <>
-__device__ __forceinline__ void st_kv_dev<float>(float* p, float v) {
-  st_dev(p, v);
-}
-template <>
-__device__ __forceinline__ void st_kv_dev<uint16_t>(uint16_t* p, float v) {
-  __hip_atomic_store(p, f2bf(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Thread 0: wait until the counter reaches target (bounded, see the file comment). The timeout flag
-// is looked at every 64 polls only, to keep polls off its line.
-__device__ __noinline__ void wait_count(int* sync, int idx, int target) {
-  int spins = 0;
-  while (ld_dev_i(sync + idx) < target) {
-    ++spins;
-    if ((spins & 63) == 0 && ld_dev_i(sync + sync_err()) != 0) return;
-    if (spins > kSpinLimit) {
-      __hip_atomic_store(sync + sync_err(), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return;
-    }
-    __builtin_amdgcn_s_sleep(2);
-  }
-}
 
 // Trace stamp `which` of a ticket (thread 0; tracing on only).
 __device__ __forceinline__ void stamp(const Ctx& C, int ticket, int which) {
