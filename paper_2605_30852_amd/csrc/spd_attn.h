@@ -1,30 +1,53 @@
 // Decode attention of one stage's token over one KV head's paged cache, one key split per workgroup
-// (the stage launches, the mixed launches and the persistent step kernel share it, so all compute the
-// same bits).
+// (the stage launches, the mixed launches and the persistent step kernels share it, so all compute
+// the same bits).
 //
 // The token at position pos0 attends to keys 0..pos0 of its own layer (Section 3.1: each stage's
 // token reads the cache of the layer it is on). Its G query heads share KV head g (grouped-query
-// attention). A split covers keys [k0, k1) in passes of 64 keys: thread t owns key t/4 of a pass and
-// a quarter of its head dimension, for K (registers) and V (LDS tile) alike, so one page-table lookup
-// serves both, and the next pass's keys are requested before the current pass is computed. Softmax
-// is online across passes; the split ends with its (o, m, l). With one split the workgroup writes the
-// output; otherwise the split that finishes last (a ticket per stage and head) merges every split in
-// split order: all (m, l) pairs are read at once, the split weights exp(m - M) / L go to LDS, and the
-// partial outputs are summed in split order with their loads issued eight at a time. The split size is
-// a function of the configuration only, so a token's result never depends on how many stages run.
+// attention). A split covers keys [k0, k1) in rounds of 64 keys, 16 per wave, and the waves never
+// wait for each other inside the split:
+//   * lane l of a wave owns key l/4 of the wave's 16 and a quarter of the head dimension, for K and V
+//     alike (one page-table lookup serves both); a round's loads are issued two rounds ahead and the
+//     page of the round after is requested before them, so no wait for a page ever waits for K or V;
+//   * scores are dot products over the quarter, summed across the four lanes of a key with DPP; the
+//     lanes of a key then split the heads between them (head h on lane h mod 4), so the online
+//     softmax of a head is a 16-lane max and sum;
+//   * P.V goes through a wave-private LDS tile: lane l accumulates one head's slice of dimensions over
+//     the wave's keys in key order.
+// Each wave keeps its own running (m, l, o); the four are combined in wave order at the end of the
+// split (one barrier). With one split the workgroup writes the output; otherwise the split that
+// finishes last (a ticket per stage and head) merges every split in split order, its loads for up to
+// 16 splits issued at once. The split size is a function of the configuration only, so a token's
+// result never depends on how many stages run.
 #pragma once
 #include "spd_devfn.h"
 
 namespace spd {
 
-constexpr int kAttnTPK = 4;                // threads per key
-constexpr int kAttnPass = kWG / kAttnTPK;  // keys per pass
-constexpr int kAttnMaxQ = 8;               // query heads per KV head
+constexpr int kAttnTPK = 4;                   // lanes per key
+constexpr int kAttnWaveKeys = 64 / kAttnTPK;  // keys per wave per round
+constexpr int kAttnPass = kWG / kAttnTPK;     // keys per round
+constexpr int kAttnMaxQ = 8;                  // query heads per KV head
+constexpr int kAttnMergeBatch = 16;           // splits whose records the merge loads at once
+
+// LDS: pre-scaled queries, then per wave a V tile (reused for the wave's o at the end), its
+// probabilities, and its rescale factors and (m, l).
+template <typename KVT, int DH>
+struct AttnLds {
+  static constexpr int kWaves = kWG / 64;
+  static constexpr size_t kQ = (size_t)kAttnMaxQ * DH * 4;
+  static constexpr size_t kTile = (size_t)kAttnWaveKeys * DH * sizeof(KVT);
+  static constexpr size_t kO = (size_t)kAttnMaxQ * DH * 4;
+  static constexpr size_t kVt = kTile > kO ? kTile : kO;
+  static constexpr size_t kP = (size_t)kAttnMaxQ * kAttnWaveKeys * 4;
+  static constexpr size_t kA = (size_t)kAttnMaxQ * 4 * 3;  // alpha, m, l
+  static constexpr size_t kWave = kVt + kP + kA;
+  static constexpr size_t kTotal = kQ + kWaves * kWave;
+};
 
 template <typename KVT, int DH>
 constexpr size_t attn_split_lds() {
-  return (size_t)kAttnMaxQ * DH * 4 + (size_t)kAttnMaxQ * kAttnPass * 4 + (size_t)kAttnPass * DH * sizeof(KVT) +
-         (size_t)2 * kMaxSplits * kAttnMaxQ * 4;
+  return AttnLds<KVT, DH>::kTotal;
 }
 
 // 16 bytes (16-byte aligned) with device-scope loads.
@@ -35,7 +58,7 @@ __device__ __forceinline__ uint4 ldg16_coherent(const void* p) {
   return make_uint4((uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32));
 }
 
-// KV cache reads. Ordinary loads: a pass's keys come back faster than with the non-temporal hint.
+// KV cache reads. Ordinary loads: a round's keys come back faster than with the non-temporal hint.
 __device__ __forceinline__ uint4 ldkv16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 
 __device__ __forceinline__ void st_dev2f(float* p, float x, float y) {  // p 8-byte aligned
@@ -43,172 +66,288 @@ __device__ __forceinline__ void st_dev2f(float* p, float x, float y) {  // p 8-b
   __hip_atomic_store((unsigned long long*)p, u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// One split. COH: the query and the newest key (pos0) were written by the same launch (device-scope
-// loads) and the output goes to a tile of the same launch (device-scope stores). kv: the layer's
-// cache; q: the G rotated query rows of this head group; out: their G output rows; rec: the
-// (o[8][DH], m[8], l[8]) records of this (stage, head), one per split; cnt: its split ticket (zero at
-// rest); page0: the physical page of this thread's key in the first pass (requested by the caller
-// before anything else). Returns true when this workgroup wrote the final output.
-template <typename KVT, int DH, bool COH>
-__device__ bool attn_split(const Ctx& C, const KVT* kvb, const float* q, float* out, float* rec_base, int* cnt, int g,
-                           int split, int nsplit, int k0, int k1, int pos0, int page0, float* lds) {
+// Sum over the four lanes of a quad (DPP quad permutes); all four lanes get the same bits.
+__device__ __forceinline__ float quad_sum(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));  // lane ^ 1
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));  // lane ^ 2
+  return v;
+}
+
+// Max / sum over the 16 lanes of a wave that share lane mod 4; every such lane gets the same bits.
+__device__ __forceinline__ float key_max(float v) {
+#pragma unroll
+  for (int m = 4; m < 64; m <<= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  return v;
+}
+__device__ __forceinline__ float key_sum(float v) {
+#pragma unroll
+  for (int m = 4; m < 64; m <<= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
+// Orders the wave's LDS writes before its later LDS reads of other lanes' data (one wave executes
+// its LDS operations in order; this keeps the compiler from moving them).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// N consecutive KV elements from LDS as floats (N * sizeof(T): 8 bytes or a multiple of 16, aligned).
+template <typename T, int N>
+__device__ __forceinline__ void lds_row(const T* p, float* o) {
+  constexpr int BYTES = N * (int)sizeof(T);
+  if constexpr (BYTES % 16 == 0) {
+#pragma unroll
+    for (int c = 0; c < BYTES / 16; c++)
+      unpack16<T>(reinterpret_cast<const uint4*>(p)[c], o + c * (16 / (int)sizeof(T)));
+  } else {
+    static_assert(BYTES == 8, "row of 8 bytes or a multiple of 16");
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    if constexpr (sizeof(T) == 2) {
+      o[0] = bf_lo(u.x);
+      o[1] = bf_hi(u.x);
+      o[2] = bf_lo(u.y);
+      o[3] = bf_hi(u.y);
+    } else {
+      o[0] = __uint_as_float(u.x);
+      o[1] = __uint_as_float(u.y);
+    }
+  }
+}
+
+// One split with GP head slots (4: G <= 4, 8: G <= 8). Arguments as for attn_split.
+template <typename KVT, int DH, bool COH, int GP>
+__device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float* out, float* rec_base, int* cnt,
+                             int g, int split, int nsplit, int k0, int k1, int pos0, int page0, float* lds) {
   constexpr int TPK = kAttnTPK, NE = DH / TPK, VE = Elt<KVT>::VE, KCH = NE / VE;
-  constexpr int MAXQ = kAttnMaxQ, PASS = kAttnPass;
+  constexpr int WK = kAttnWaveKeys, PASS = kAttnPass, MAXQ = kAttnMaxQ, NJ = GP / 4;
+  constexpr int LPH = 64 / GP, DPL = DH / LPH;  // P.V: lanes per head, dimensions per lane
+  constexpr int KUNR = DPL > 8 ? 2 : 4;          // P.V keys in flight
   constexpr int RS = MAXQ * (DH + 2);
-  float* qs = lds;                                         // [MAXQ][DH] pre-scaled queries
-  float* sc = qs + MAXQ * DH;                              // [MAXQ][PASS] scores, then probabilities
-  KVT* vs = reinterpret_cast<KVT*>(sc + MAXQ * PASS);      // [PASS][DH] V tile
-  float* s_pw = reinterpret_cast<float*>(vs + PASS * DH);  // merge: m of each split, then its weight
-  float* s_pl = s_pw + kMaxSplits * MAXQ;
-  __shared__ float s_m[MAXQ], s_l[MAXQ], s_al[MAXQ];
+  using LA = AttnLds<KVT, DH>;
   __shared__ int s_last;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  const int kk = tid / TPK, qq = tid % TPK;
+  const int kk = lane / TPK, qq = lane % TPK;
   const int G = C.G;
+  char* const lbase = reinterpret_cast<char*>(lds);
+  float* qs = lds;                                                  // [MAXQ][DH] pre-scaled queries
+  char* wbase = lbase + LA::kQ + (size_t)w * LA::kWave;
+  KVT* vt = reinterpret_cast<KVT*>(wbase);                          // [WK][DH] V tile, then o [MAXQ][DH]
+  float* pt = reinterpret_cast<float*>(wbase + LA::kVt);            // [MAXQ][WK] probabilities
+  float* at = reinterpret_cast<float*>(wbase + LA::kVt + LA::kP);   // alpha[MAXQ], m[MAXQ], l[MAXQ]
   const size_t page_elems = (size_t)2 * C.hkv * C.page * DH;
   const size_t head_off = (size_t)g * C.page * DH;
   const size_t voff = (size_t)C.hkv * C.page * DH;
-  uint4 kraw[KCH], vraw[KCH];
-  auto issue = [&](int kp, int page) {
-    const int key = kp + kk;
+  const int R = (k1 - k0 + PASS - 1) / PASS;  // rounds
+  const int my = w * WK + kk;                 // this lane's key within a round
+
+  // queries first, then the page of round 1, then rounds 0 and 1 (no wait below waits for later loads)
+  constexpr int QPT = (MAXQ * DH + kWG - 1) / kWG;
+  float qv[QPT];
+#pragma unroll
+  for (int i = 0; i < QPT; i++) {
+    const int e = tid + i * kWG;
+    qv[i] = e < G * DH ? (COH ? ld_dev(q + e) : q[e]) : 0.f;
+  }
+  auto page_of = [&](int r) { return C.page_table[min(k0 + r * PASS + my, k1 - 1) / C.page]; };
+  int pg_next = R > 1 ? page_of(1) : 0;
+  uint4 kb0[KCH], vb0[KCH], kb1[KCH], vb1[KCH];
+  auto issue = [&](int r, int page, uint4* kr, uint4* vr) {
+    const int key = k0 + r * PASS + my;
     if (key < k1) {
       const KVT* base = kvb + (size_t)page * page_elems + head_off + (size_t)(key % C.page) * DH + qq * NE;
       if (COH && key == pos0) {
 #pragma unroll
-        for (int c4 = 0; c4 < KCH; c4++) kraw[c4] = ldg16_coherent(reinterpret_cast<const uint4*>(base) + c4);
+        for (int c = 0; c < KCH; c++) kr[c] = ldg16_coherent(reinterpret_cast<const uint4*>(base) + c);
 #pragma unroll
-        for (int c4 = 0; c4 < KCH; c4++) vraw[c4] = ldg16_coherent(reinterpret_cast<const uint4*>(base + voff) + c4);
+        for (int c = 0; c < KCH; c++) vr[c] = ldg16_coherent(reinterpret_cast<const uint4*>(base + voff) + c);
       } else {
 #pragma unroll
-        for (int c4 = 0; c4 < KCH; c4++) kraw[c4] = ldkv16(reinterpret_cast<const uint4*>(base) + c4);
+        for (int c = 0; c < KCH; c++) kr[c] = ldkv16(reinterpret_cast<const uint4*>(base) + c);
 #pragma unroll
-        for (int c4 = 0; c4 < KCH; c4++) vraw[c4] = ldkv16(reinterpret_cast<const uint4*>(base + voff) + c4);
+        for (int c = 0; c < KCH; c++) vr[c] = ldkv16(reinterpret_cast<const uint4*>(base + voff) + c);
       }
+    } else {  // past the split: zeros, so the tile row holds finite values
+#pragma unroll
+      for (int c = 0; c < KCH; c++) kr[c] = vr[c] = make_uint4(0u, 0u, 0u, 0u);
     }
   };
-  issue(k0, page0);
-  for (int e = tid; e < G * DH; e += kWG) qs[e] = (COH ? ld_dev(q + e) : q[e]) * C.scale;
-  if (tid < MAXQ) {
-    s_m[tid] = -INFINITY;
-    s_l[tid] = 0.f;
+  issue(0, page0, kb0, vb0);
+  if (R > 1) {
+    const int pg1 = pg_next;
+    pg_next = R > 2 ? page_of(2) : 0;
+    issue(1, pg1, kb1, vb1);
   }
-  constexpr int npair = DH >> 1;
-  constexpr int NG = kWG / npair;
-  constexpr int MAXU = (MAXQ + NG - 1) / NG;
-  const int dp = tid % npair, qg = tid / npair;
-  float o0[MAXU], o1[MAXU];
 #pragma unroll
-  for (int u = 0; u < MAXU; u++) o0[u] = o1[u] = 0.f;
-  for (int kp = k0; kp < k1; kp += PASS) {
-    const int nk = min(PASS, k1 - kp);
-    float kr[NE];
-    if (kk < nk) {
+  for (int i = 0; i < QPT; i++) {
+    const int e = tid + i * kWG;
+    if (e < G * DH) qs[e] = qv[i] * C.scale;
+  }
+  __syncthreads();  // queries staged
+
+  float m_run[NJ], l_run[NJ];
 #pragma unroll
-      for (int c4 = 0; c4 < KCH; c4++) reinterpret_cast<uint4*>(vs + kk * DH + qq * NE)[c4] = vraw[c4];
+  for (int j = 0; j < NJ; j++) {
+    m_run[j] = -INFINITY;
+    l_run[j] = 0.f;
+  }
+  const int ph = lane / LPH, pd = (lane % LPH) * DPL;  // P.V: head slot and first dimension
+  float o[DPL];
 #pragma unroll
-      for (int c4 = 0; c4 < KCH; c4++) unpack16<KVT>(kraw[c4], kr + c4 * VE);
+  for (int e = 0; e < DPL; e++) o[e] = 0.f;
+
+  auto round = [&](int r, uint4* kr_raw, uint4* vr_raw) {
+    const int kbase = k0 + r * PASS + w * WK;  // the wave's first key in this round
+    const int nkw = min(WK, k1 - kbase);       // wave-uniform
+    float kf[NE];
+#pragma unroll
+    for (int c = 0; c < KCH; c++) unpack16<KVT>(kr_raw[c], kf + c * VE);
+#pragma unroll
+    for (int c = 0; c < KCH; c++) reinterpret_cast<uint4*>(vt + kk * DH + qq * NE)[c] = vr_raw[c];
+    if (r + 2 < R) {  // the buffers are free again: round r + 2, and the page of round r + 3
+      const int pg = pg_next;
+      pg_next = r + 3 < R ? page_of(r + 3) : 0;
+      issue(r + 2, pg, kr_raw, vr_raw);
     }
-    if (kp + PASS < k1) {  // the next pass's keys are in flight while this one is computed
-      const int nkey = kp + PASS + kk;
-      issue(kp + PASS, C.page_table[min(nkey, k1 - 1) / C.page]);
-    }
-    __syncthreads();  // q staged (first pass), V tile written
-    for (int qi = 0; qi < G; qi++) {
-      float dsum = 0.f;
-      if (kk < nk) {
-        const float* qv = qs + qi * DH + qq * NE;
+    if (nkw > 0) {  // else the wave has no key in this round
+      const bool valid = kk < nkw;
+      float sel[NJ];
 #pragma unroll
-        for (int e = 0; e < NE; e += 4) {
-          const float4 q4 = *reinterpret_cast<const float4*>(qv + e);
-          dsum = fmaf(q4.x, kr[e], dsum);
-          dsum = fmaf(q4.y, kr[e + 1], dsum);
-          dsum = fmaf(q4.z, kr[e + 2], dsum);
-          dsum = fmaf(q4.w, kr[e + 3], dsum);
-        }
-      }
-      dsum += __shfl_xor(dsum, 1, 64);
-      dsum += __shfl_xor(dsum, 2, 64);
-      if (qq == 0 && kk < nk) sc[qi * PASS + kk] = dsum;
-    }
-    __syncthreads();
-    for (int qi = w; qi < G; qi += kWG / 64) {  // online softmax, one wave per query head
-      const float sv = lane < nk ? sc[qi * PASS + lane] : -INFINITY;
-      const float mx = wave_max(sv);
-      const float mo = s_m[qi];
-      const float mn = fmaxf(mo, mx);
-      const float p = lane < nk ? expf(sv - mn) : 0.f;
-      if (lane < nk) sc[qi * PASS + lane] = p;
-      const float ps = wave_sum(p);
-      if (lane == 0) {
-        const float al = (mo == -INFINITY) ? 0.f : expf(mo - mn);
-        s_al[qi] = al;
-        s_l[qi] = s_l[qi] * al + ps;
-        s_m[qi] = mn;
-      }
-    }
-    __syncthreads();
+      for (int j = 0; j < NJ; j++) sel[j] = -INFINITY;
 #pragma unroll
-    for (int u = 0; u < MAXU; u++) {
-      const int qi = qg + u * NG;
-      if (qi < G) {
-        const float al = s_al[qi];
-        o0[u] *= al;
-        o1[u] *= al;
-      }
-    }
-    // P.V: eight keys' V pairs and probabilities are read from LDS together (rows >= nk of the
-    // tile hold stale values and are skipped), then accumulated in key order
-    for (int k2 = 0; k2 < nk; k2 += 8) {
-      float2 vv[8];
-#pragma unroll
-      for (int j = 0; j < 8; j++) vv[j] = ld2<KVT>(vs + (size_t)(k2 + j) * DH + 2 * dp);
-#pragma unroll
-      for (int u = 0; u < MAXU; u++) {
-        const int qi = qg + u * NG;
+      for (int qi = 0; qi < GP; qi++) {
         if (qi < G) {
-          float pp[8];
+          const float* qp = qs + qi * DH + qq * NE;
+          float dsum = 0.f;
 #pragma unroll
-          for (int j = 0; j < 8; j++) pp[j] = sc[qi * PASS + k2 + j];
-#pragma unroll
-          for (int j = 0; j < 8; j++) {
-            if (k2 + j < nk) {
-              o0[u] = fmaf(pp[j], vv[j].x, o0[u]);
-              o1[u] = fmaf(pp[j], vv[j].y, o1[u]);
-            }
+          for (int e = 0; e < NE; e += 4) {
+            const float4 q4 = *reinterpret_cast<const float4*>(qp + e);
+            dsum = fmaf(q4.x, kf[e], dsum);
+            dsum = fmaf(q4.y, kf[e + 1], dsum);
+            dsum = fmaf(q4.z, kf[e + 2], dsum);
+            dsum = fmaf(q4.w, kf[e + 3], dsum);
           }
+          dsum = quad_sum(dsum);
+          if ((qi & 3) == qq) sel[qi >> 2] = valid ? dsum : -INFINITY;
+        }
+      }
+      // online softmax of head qq + 4j over the wave's keys (key 0 of the round is valid, so mn is
+      // finite for every head h < G)
+#pragma unroll
+      for (int j = 0; j < NJ; j++) {
+        const int h = qq + 4 * j;
+        const float mx = key_max(sel[j]);
+        const float mn = fmaxf(m_run[j], mx);
+        const float al = m_run[j] == -INFINITY ? 0.f : expf(m_run[j] - mn);
+        const float p = valid && h < G ? expf(sel[j] - mn) : 0.f;
+        const float ps = key_sum(p);
+        l_run[j] = l_run[j] * al + ps;
+        m_run[j] = mn;
+        if (h < G) {
+          pt[h * WK + kk] = p;
+          if (kk == 0) at[h] = al;
+        }
+      }
+      wave_lds_sync();
+      if (ph < G) {
+        const float al = at[ph];
+#pragma unroll
+        for (int e = 0; e < DPL; e++) o[e] *= al;
+        const float* pp = pt + ph * WK;
+#pragma unroll KUNR
+        for (int k = 0; k < WK; k++) {
+          float v[DPL];
+          lds_row<KVT, DPL>(vt + k * DH + pd, v);
+          const float pk = pp[k];
+#pragma unroll
+          for (int e = 0; e < DPL; e++) o[e] = fmaf(pk, v[e], o[e]);
         }
       }
     }
-    __syncthreads();
+    wave_lds_sync();  // the tile and probabilities are rewritten next round
+  };
+  for (int r = 0; r < R; r += 2) {
+    round(r, kb0, vb0);
+    if (r + 1 < R) round(r + 1, kb1, vb1);
+  }
+
+  // the wave's (m, l, o) to LDS; o reuses the V tile
+  float* ow = reinterpret_cast<float*>(vt);
+#pragma unroll
+  for (int j = 0; j < NJ; j++) {
+    const int h = qq + 4 * j;
+    if (kk == 0 && h < G) {
+      at[MAXQ + h] = m_run[j];
+      at[2 * MAXQ + h] = l_run[j];
+    }
+  }
+  if (ph < G) {
+#pragma unroll
+    for (int e = 0; e < DPL; e++) ow[ph * DH + pd + e] = o[e];
+  }
+  __syncthreads();
+
+  // combine the waves in wave order: (A, M, L) of the split per (head, dimension pair); a wave with
+  // no key has m = -inf and weight 0 (wave 0 always has key k0, so M is finite)
+  constexpr int NW = LA::kWaves;
+  constexpr int NPAIR = MAXQ * DH / 2;
+  constexpr int PPT = (NPAIR + kWG - 1) / kWG;
+  float A0[PPT], A1[PPT], Ms[PPT], Ls[PPT];
+#pragma unroll
+  for (int i = 0; i < PPT; i++) {
+    const int e = tid + i * kWG, qi = e / (DH / 2), dp = e % (DH / 2);
+    A0[i] = A1[i] = Ms[i] = Ls[i] = 0.f;
+    if (qi < G) {
+      float M = -INFINITY;
+#pragma unroll
+      for (int wv = 0; wv < NW; wv++)
+        M = fmaxf(M, reinterpret_cast<const float*>(lbase + LA::kQ + (size_t)wv * LA::kWave + LA::kVt + LA::kP)[MAXQ + qi]);
+      float L = 0.f, a0 = 0.f, a1 = 0.f;
+#pragma unroll
+      for (int wv = 0; wv < NW; wv++) {
+        const char* wb = lbase + LA::kQ + (size_t)wv * LA::kWave;
+        const float* aw = reinterpret_cast<const float*>(wb + LA::kVt + LA::kP);
+        const float mw = aw[MAXQ + qi];
+        if (mw != -INFINITY) {
+          const float f = expf(mw - M);
+          L = fmaf(aw[2 * MAXQ + qi], f, L);
+          const float2 ov = *reinterpret_cast<const float2*>(reinterpret_cast<const float*>(wb) + qi * DH + 2 * dp);
+          a0 = fmaf(ov.x, f, a0);
+          a1 = fmaf(ov.y, f, a1);
+        }
+      }
+      A0[i] = a0;
+      A1[i] = a1;
+      Ms[i] = M;
+      Ls[i] = L;
+    }
   }
   if (nsplit == 1) {
 #pragma unroll
-    for (int u = 0; u < MAXU; u++) {
-      const int qi = qg + u * NG;
+    for (int i = 0; i < PPT; i++) {
+      const int e = tid + i * kWG, qi = e / (DH / 2), dp = e % (DH / 2);
       if (qi < G) {
-        const float inv = 1.0f / s_l[qi];
-        if (COH) {
-          st_dev2f(out + qi * DH + 2 * dp, o0[u] * inv, o1[u] * inv);
-        } else {
-          out[qi * DH + 2 * dp] = o0[u] * inv;
-          out[qi * DH + 2 * dp + 1] = o1[u] * inv;
-        }
+        const float inv = 1.0f / Ls[i];
+        if (COH)
+          st_dev2f(out + qi * DH + 2 * dp, A0[i] * inv, A1[i] * inv);
+        else
+          *reinterpret_cast<float2*>(out + qi * DH + 2 * dp) = make_float2(A0[i] * inv, A1[i] * inv);
       }
     }
     return true;
   }
   float* rec = rec_base + (size_t)split * RS;
 #pragma unroll
-  for (int u = 0; u < MAXU; u++) {
-    const int qi = qg + u * NG;
+  for (int i = 0; i < PPT; i++) {
+    const int e = tid + i * kWG, qi = e / (DH / 2), dp = e % (DH / 2);
     if (qi < G) {
-      st_dev(rec + qi * DH + 2 * dp, o0[u]);
-      st_dev(rec + qi * DH + 2 * dp + 1, o1[u]);
+      st_dev2f(rec + qi * DH + 2 * dp, A0[i], A1[i]);
+      if (dp == 0) {
+        st_dev(rec + MAXQ * DH + qi, Ms[i]);
+        st_dev(rec + MAXQ * DH + MAXQ + qi, Ls[i]);
+      }
     }
-  }
-  if (tid < G) {
-    st_dev(rec + MAXQ * DH + tid, s_m[tid]);
-    st_dev(rec + MAXQ * DH + MAXQ + tid, s_l[tid]);
   }
   wait_own_stores();
   __syncthreads();
@@ -218,55 +357,73 @@ __device__ bool attn_split(const Ctx& C, const KVT* kvb, const float* q, float* 
   }
   __syncthreads();
   if (!s_last) return false;
-  for (int e = tid; e < nsplit * G; e += kWG) {  // every split has >= 1 key, so m is finite
-    const int sp = e / G, qi = e % G;
-    s_pw[sp * MAXQ + qi] = ld_dev(rec_base + (size_t)sp * RS + MAXQ * DH + qi);
-    s_pl[sp * MAXQ + qi] = ld_dev(rec_base + (size_t)sp * RS + MAXQ * DH + MAXQ + qi);
-  }
-  __syncthreads();
-  if (tid < G) {  // split order, fixed
-    float M = -INFINITY;
-    for (int sp = 0; sp < nsplit; sp++) M = fmaxf(M, s_pw[sp * MAXQ + tid]);
-    float Ls = 0.f;
-    for (int sp = 0; sp < nsplit; sp++) Ls = fmaf(s_pl[sp * MAXQ + tid], expf(s_pw[sp * MAXQ + tid] - M), Ls);
-    s_m[tid] = M;
-    s_l[tid] = 1.0f / Ls;
-  }
-  __syncthreads();
-  for (int e = tid; e < nsplit * G; e += kWG) {
-    const int sp = e / G, qi = e % G;
-    s_pw[sp * MAXQ + qi] = expf(s_pw[sp * MAXQ + qi] - s_m[qi]) * s_l[qi];
-  }
-  __syncthreads();
+
+  // merge every split in split order (every split has a key, so each m is finite)
 #pragma unroll
-  for (int u = 0; u < MAXU; u++) {
-    const int qi = qg + u * NG;
+  for (int i = 0; i < PPT; i++) {
+    const int e = tid + i * kWG, qi = e / (DH / 2), dp = e % (DH / 2);
     if (qi < G) {
-      float A0 = 0.f, A1 = 0.f;
-      for (int sp0 = 0; sp0 < nsplit; sp0 += 8) {
-        float2 v[8];
+      float M = -INFINITY, L = 0.f, a0 = 0.f, a1 = 0.f;
+      for (int sp0 = 0; sp0 < nsplit; sp0 += kAttnMergeBatch) {
+        float mb[kAttnMergeBatch], lb[kAttnMergeBatch];
+        float2 ob[kAttnMergeBatch];
 #pragma unroll
-        for (int j = 0; j < 8; j++)
-          v[j] = sp0 + j < nsplit ? ld_dev2(rec_base + (size_t)(sp0 + j) * RS + qi * DH + 2 * dp) : make_float2(0.f, 0.f);
-#pragma unroll
-        for (int j = 0; j < 8; j++) {
+        for (int j = 0; j < kAttnMergeBatch; j++) {
+          const float* rj = rec_base + (size_t)(sp0 + j) * RS;
           if (sp0 + j < nsplit) {
-            const float f = s_pw[(sp0 + j) * MAXQ + qi];
-            A0 = fmaf(v[j].x, f, A0);
-            A1 = fmaf(v[j].y, f, A1);
+            ob[j] = ld_dev2(rj + qi * DH + 2 * dp);
+            mb[j] = ld_dev(rj + MAXQ * DH + qi);
+            lb[j] = ld_dev(rj + MAXQ * DH + MAXQ + qi);
+          } else {
+            ob[j] = make_float2(0.f, 0.f);
+            mb[j] = -INFINITY;
+            lb[j] = 0.f;
           }
         }
+        float Mn = M;
+#pragma unroll
+        for (int j = 0; j < kAttnMergeBatch; j++) Mn = fmaxf(Mn, mb[j]);
+        if (M != -INFINITY) {
+          const float sc = expf(M - Mn);
+          L *= sc;
+          a0 *= sc;
+          a1 *= sc;
+        }
+#pragma unroll
+        for (int j = 0; j < kAttnMergeBatch; j++) {
+          if (sp0 + j < nsplit) {
+            const float f = expf(mb[j] - Mn);
+            L = fmaf(lb[j], f, L);
+            a0 = fmaf(ob[j].x, f, a0);
+            a1 = fmaf(ob[j].y, f, a1);
+          }
+        }
+        M = Mn;
       }
-      if (COH) {
-        st_dev2f(out + qi * DH + 2 * dp, A0, A1);
-      } else {
-        out[qi * DH + 2 * dp] = A0;
-        out[qi * DH + 2 * dp + 1] = A1;
-      }
+      const float inv = 1.0f / L;
+      if (COH)
+        st_dev2f(out + qi * DH + 2 * dp, a0 * inv, a1 * inv);
+      else
+        *reinterpret_cast<float2*>(out + qi * DH + 2 * dp) = make_float2(a0 * inv, a1 * inv);
     }
   }
   if (tid == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   return true;
+}
+
+// One split. COH: the query and the newest key (pos0) were written by the same launch (device-scope
+// loads) and the output goes to a tile of the same launch (device-scope stores). kvb: the layer's
+// cache; q: the G rotated query rows of this head group; out: their G output rows; rec_base: the
+// (o[8][DH], m[8], l[8]) records of this (stage, head), one per split; cnt: its split ticket (zero at
+// rest); page0: the physical page of this thread's key in the first round (key k0 + threadIdx.x / 4,
+// clamped; requested by the caller before anything else). Returns true when this workgroup wrote the
+// final output.
+template <typename KVT, int DH, bool COH>
+__device__ bool attn_split(const Ctx& C, const KVT* kvb, const float* q, float* out, float* rec_base, int* cnt, int g,
+                           int split, int nsplit, int k0, int k1, int pos0, int page0, float* lds) {
+  if (C.G <= 4)
+    return attn_split_g<KVT, DH, COH, 4>(C, kvb, q, out, rec_base, cnt, g, split, nsplit, k0, k1, pos0, page0, lds);
+  return attn_split_g<KVT, DH, COH, 8>(C, kvb, q, out, rec_base, cnt, g, split, nsplit, k0, k1, pos0, page0, lds);
 }
 
 }  // namespace spd

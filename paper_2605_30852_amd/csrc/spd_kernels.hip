@@ -924,7 +924,8 @@ __global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
 // Decode attention of a stage launch. Grid: x = key split, y = KV head, z = stage of the launch.
 // The page of this thread's first key and the device state are requested together at entry; the
 // split itself is attn_split (shared with the persistent step kernel).
-template <typename KVT, int DH>
+// GP: head slots of the split (4 or 8), or 0 to choose from C.G at run time.
+template <typename KVT, int DH, int GP = 0>
 __device__ __forceinline__ void attn_part(const Ctx& C, int s, int slot, const KVT* kv, int set, int g, int split) {
   extern __shared__ __align__(16) float lds[];
   const int k0 = split * C.chunk;
@@ -939,15 +940,20 @@ __device__ __forceinline__ void attn_part(const Ctx& C, int s, int slot, const K
   const BufSet& B = C.b[set];
   const int cidx = s * C.hkv + g;
   constexpr int RS = kAttnMaxQ * (DH + 2);
-  attn_split<KVT, DH, false>(C, kv, B.q + (size_t)s * C.qdim + g * C.G * DH, B.ao + (size_t)s * C.qdim + g * C.G * DH,
-                             B.part + (size_t)cidx * C.max_splits * RS, B.cnt + cidx, g, split, nsplit, k0, k1, pos0,
-                             page0, lds);
+  const float* q = B.q + (size_t)s * C.qdim + g * C.G * DH;
+  float* out = B.ao + (size_t)s * C.qdim + g * C.G * DH;
+  float* rec = B.part + (size_t)cidx * C.max_splits * RS;
+  if constexpr (GP == 0)
+    attn_split<KVT, DH, false>(C, kv, q, out, rec, B.cnt + cidx, g, split, nsplit, k0, k1, pos0, page0, lds);
+  else
+    attn_split_g<KVT, DH, false, GP>(C, kv, q, out, rec, B.cnt + cidx, g, split, nsplit, k0, k1, pos0, page0, lds);
 }
 
-template <typename KVT, int DH>
+// The stage launch is instantiated per head-slot count, so its registers are those of one variant.
+template <typename KVT, int DH, int GP>
 __global__ __launch_bounds__(kWG) void k_attn_stage(Ctx C, Rows R) {
   const int s = R.stage0 + blockIdx.z;
-  attn_part<KVT, DH>(C, s, R.slot, (const KVT*)R.ld[s].kv, R.set, blockIdx.y, blockIdx.x);
+  attn_part<KVT, DH, GP>(C, s, R.slot, (const KVT*)R.ld[s].kv, R.set, blockIdx.y, blockIdx.x);
 }
 
 // ---------------------------------------------------------------------------- mixed launches
@@ -1349,10 +1355,18 @@ template <typename WT>
 void Launch<WT>::attn(const Ctx& c, const Rows& r, void* s) {
   if (r.kind == 0) {
     const dim3 grid(c.max_splits, c.hkv, r.nst);
-    if (c.dh == 128)
-      launch_timed((k_attn_stage<WT, 128>), grid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
-    else
-      launch_timed((k_attn_stage<WT, 64>), grid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
+    const bool g4 = c.G <= 4;
+    if (c.dh == 128) {
+      if (g4)
+        launch_timed((k_attn_stage<WT, 128, 4>), grid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
+      else
+        launch_timed((k_attn_stage<WT, 128, 8>), grid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
+    } else {
+      if (g4)
+        launch_timed((k_attn_stage<WT, 64, 4>), grid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
+      else
+        launch_timed((k_attn_stage<WT, 64, 8>), grid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
+    }
     return;
   }
   if (c.dh == 128)

@@ -290,8 +290,8 @@ size_t step_lds_bytes(const Ctx& c, int bf16) {
   int kmax = std::max(std::max(c.d, c.qdim), c.F);
   kmax = (kmax + blk - 1) / blk * blk;
   const size_t gemv = (size_t)kmax * sizeof(float);
-  const size_t attn = (size_t)kAttnMaxQ * c.dh * 4 + (size_t)kAttnMaxQ * kAttnPass * 4 +
-                      (size_t)kAttnPass * c.dh * (bf16 ? 2 : 4) + (size_t)2 * kMaxSplits * kAttnMaxQ * 4;
+  const size_t attn = bf16 ? (c.dh == 128 ? attn_split_lds<uint16_t, 128>() : attn_split_lds<uint16_t, 64>())
+                           : (c.dh == 128 ? attn_split_lds<float, 128>() : attn_split_lds<float, 64>());
   return std::max(gemv, attn);
 }
 
