@@ -163,6 +163,9 @@ def main():
                          "independent sublayers of different stages, 4 one persistent launch with a group of "
                          "workgroups per stage")
     ap.add_argument("--step-grid", type=int, default=0, help="workgroups of the persistent step launch (0: default)")
+    ap.add_argument("--stage-groups", type=int, default=0, help="mode 2: stage streams (0: the library default)")
+    ap.add_argument("--pdm-place", type=int, default=0, choices=[0, 1, 2, 3],
+                    help="PDM launches: own stream, main before the stages, first group before/after")
     ap.add_argument("--attn-chunk", type=int, default=0, help="keys per attention split (0: the workload's default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (the known-size kernel for HBM counter scaling)")
@@ -215,7 +218,8 @@ def main():
     fused = not args.separate_head
     mode = args.step_mode
     ar = Engine(weights, max_tokens=max_tokens, n=1, attn_chunk=attn_chunk, fused_head=fused)
-    ar.spd_set_step_kernel(mode, args.step_grid)
+    ar.spd_set_step_kernel(mode, args.step_grid, args.stage_groups if mode == 2 else -1)
+    ar.spd_set_pdm_placement(args.pdm_place)
     ar.spd_set_graph(not args.no_graph)
     first = ar.spd_prefill(prompt)
     log(f"[bench] AR prefill {P} tokens in {time.time() - t0:.1f}s")
@@ -233,8 +237,10 @@ def main():
     # SPD handle, all drafts forced to the greedy tokens: every step after the fill is a full step
     t0 = time.time()
     eng = Engine(weights, max_tokens=max_tokens, n=n, attn_chunk=attn_chunk, fused_head=fused)
-    eng.spd_set_step_kernel(mode, args.step_grid)
+    eng.spd_set_step_kernel(mode, args.step_grid, args.stage_groups if mode == 2 else -1)
+    eng.spd_set_pdm_placement(args.pdm_place)
     eng.spd_set_graph(not args.no_graph)
+    groups = B.spd_step_plan_info(eng.h)["stage_groups"]
     f2 = eng.spd_prefill(prompt)
     assert f2 == first
     log(f"[bench] SPD prefill {P} tokens in {time.time() - t0:.1f}s")
@@ -297,7 +303,7 @@ def main():
         else:
             lb = launch_bytes(sh, n, cm, esz)[kname]
         if mode == 2 and kname not in ("head", "step"):
-            lb = lb / n  # each launch covers one stage
+            lb = lb / groups  # each launch covers one group's stages (n / groups on average)
         us = 1e3 * ms / max(1, nl)
         kernels[kname] = {"us_per_launch": round(us, 2), "timed_launches_per_step": nl / steps,
                           "bytes_per_launch": int(lb), "GBps": round(lb / (us * 1e-6) / 1e9, 1)}
@@ -370,10 +376,14 @@ def main():
                    "step_graph": not args.no_graph,
                    "stage_compute": {0: "five launches per layer slot covering all stages",
                                      1: "one persistent launch per step",
-                                     2: "one stream per stage, five launches per layer slot",
+                                     2: f"{groups} stage groups on their own streams, five launches per layer slot "
+                                        f"each covering the group's stages",
                                      3: "skewed schedule: 5J+n-1 launches, launch L runs sublayer L-s of stage s",
                                      4: "one persistent launch per step, a group of workgroups per stage"}[mode],
-                   "step_grid": args.step_grid or None},
+                   "step_grid": args.step_grid or None,
+                   "pdm_placement": {0: "own stream", 1: "main stream before the stages",
+                                     2: "first stage group's stream, before its stages",
+                                     3: "first stage group's stream, after its stages"}[args.pdm_place]},
         "bytes_per_step": int(bytes_step),
         "step_GBps": round(gbs, 1),
         "step_roofline_frac": round(gbs / PEAK_HBM_GBS, 4),
@@ -381,13 +391,14 @@ def main():
                      "frac": round(dk["GBps"] / PEAK_HBM_GBS, 4), "traffic": traffic_from_profile(dominant),
                      "kernel": {0: "k_sgemv gate/up: grouped gate/up GEMV + SwiGLU over the n stages",
                                 1: "k_step: the persistent launch running every layer slot of all n stages",
-                                2: "k_sgemv gate/up of one stage (stage streams run concurrently)",
+                                2: f"k_sgemv gate/up of one stage group (n/{groups} stages; the groups' streams "
+                                   f"run concurrently)",
                                 3: "k_mix: the skewed launches of the stage compute (all layers' weights and KV; "
                                    "bytes and time summed over the launches of a step)",
                                 4: "k_pstep: the persistent launch running every layer slot of all n stages, "
                                    "one group of workgroups per stage"}[mode],
                      "bytes_per_launch": dk["bytes_per_launch"], "us_per_launch": dk["us_per_launch"],
-                     "timing": f"dispatch-recorded HIP events on the main stream, layer slots >= {first_slot} of "
+                     "timing": f"dispatch-recorded HIP events on the launching stream, layer slots >= {first_slot} of "
                                f"{L_slots}, {K_GU} steady-state steps"},
         "kernels": kernels,
         "pdm_overlap": spans,

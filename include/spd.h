@@ -185,7 +185,13 @@ spd_status spd_sync(spd_handle* h, spd_step_result* last);
  *                        staged, end) in the first 4*nitems. Grouped kernel: 3 per workgroup and sublayer
  *                        (wait start, wait end, end) at ((workgroup * 5J) + sublayer) * 3; workgroups
  *                        whose stamps would not fit record none.
- * bytes must equal the size listed (nitems and ntrace from spd_step_plan_info). */
+ *   SPD_DBG_KTRACE:      nkslots x 2 uint64 wall-clock stamps of the last step run with
+ *                        spd_set_kernel_trace on: per slot the first workgroup's start and the
+ *                        latest workgroup end (both 0: nothing ran). Slot (j*5 + k)*n + s
+ *                        is sublayer k (QKV, attention, O-proj, gate/up, down) of layer slot j of stage
+ *                        s (stage launches, modes 0 and 2); slots 5*J*n + 0, 1, 2 are the LM head,
+ *                        verify and the PDM feature projection.
+ * bytes must equal the size listed (nitems, ntrace and nkslots from spd_step_plan_info). */
 enum {
   SPD_DBG_RESID = 1,
   SPD_DBG_ANCHORS = 2,
@@ -195,7 +201,8 @@ enum {
   SPD_DBG_TOKENS = 6,
   SPD_DBG_STATE = 7,
   SPD_DBG_STEP_ITEMS = 8,
-  SPD_DBG_STEP_TRACE = 9
+  SPD_DBG_STEP_TRACE = 9,
+  SPD_DBG_KTRACE = 10
 };
 spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes);
 
@@ -219,9 +226,11 @@ spd_status spd_set_graph(spd_handle* h, int32_t on);
  *           the stages' sublayers in lockstep, k > 0 staggers stage s by k*s sublayers, -1 keeps the
  *           current order. If a wait ever timed out, the next call that reads the step result returns
  *           SPD_E_HIP.
- *   mode 2 (default): stage s runs its own chain of five launches per layer slot on its own stream
- *           (the library's, default priority), forked from and joined to main_stream, so that one
- *           stage's attention and launch tails can overlap the other stages' weight streaming.
+ *   mode 2 (default): the stages are spread over G groups of consecutive stages (skew = G, at most
+ *           n; 0: the default, 2; -1 keeps the current G); each group runs its own chain of five launches
+ *           per layer slot, each covering the group's stages, on its own stream (the library's,
+ *           default priority), forked from and joined to main_stream, so that one group's attention
+ *           and launch tails can overlap the other groups' weight streaming.
  *   mode 3: a skewed schedule on main_stream: launch L runs sublayer L - s (in the order
  *           QKV, attention, O-proj, gate/up, down of each layer slot) of every stage s, 5J + n - 1
  *           launches per step. The parts of a launch belong to different stages and are independent,
@@ -240,13 +249,26 @@ spd_status spd_set_graph(spd_handle* h, int32_t on);
  * classes time modes 0 and 2. */
 spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t skew);
 
+/* Where the Pipeline Draft Module's launches go within a step (it reads only pre-step features, so
+ * any placement gives the same results): 0 (default): its own stream, forked from main_stream;
+ * 1: main_stream, before the stage compute; 2 and 3 (mode 2 only; otherwise 0): the first stage
+ * group's stream, before (2) or after (3) that group's stage launches. */
+spd_status spd_set_pdm_placement(spd_handle* h, int32_t place);
+
 /* Tracing of the persistent step launch: while on, every tile records four wall-clock stamps (for
  * SPD_DBG_STEP_TRACE; each step overwrites them). Costs a few stores per tile. */
 spd_status spd_set_step_trace(spd_handle* h, int32_t on);
 
-/* info (host, 10 int32): number of tickets of one step, layer slots J, tiles per stage of QKV,
+/* Launch trace: while on, every step first resets the trace and its stage launches, LM head, verify
+ * and PDM projection record their wall-clock start and end in it (SPD_DBG_KTRACE). One store per
+ * launch and one device atomic per workgroup that nothing waits for; for measurement only. */
+spd_status spd_set_kernel_trace(spd_handle* h, int32_t on);
+
+/* info (host, 16 int32): number of tickets of one step, layer slots J, tiles per stage of QKV,
  * attention, O-proj, gate/up and down, the wall-clock rate of the trace stamps in kHz, the stamps the
- * trace buffer holds (ntrace) and the grouped kernel's grid (0 until mode 4 is chosen). */
+ * trace buffer holds (ntrace), the grouped kernel's grid (0 until mode 4 is chosen), the launch-trace
+ * slots (nkslots), the SPD width n, the stage groups in effect (1 outside mode 2), the PDM placement,
+ * and two zeros. */
 spd_status spd_step_plan_info(spd_handle* h, int32_t* info);
 
 /* 1: every LM-head pass also writes its full logits (for SPD_DBG_*_LOGITS). */

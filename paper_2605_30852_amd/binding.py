@@ -17,7 +17,7 @@ SPD_F32, SPD_BF16 = 0, 1
 SPD_NONE, SPD_ACCEPT, SPD_REJECT = 0, 1, 2
 SPD_DBG_RESID, SPD_DBG_ANCHORS, SPD_DBG_PDM_HIDDEN = 1, 2, 3
 SPD_DBG_EXIT_LOGITS, SPD_DBG_PDM_LOGITS, SPD_DBG_TOKENS, SPD_DBG_STATE = 4, 5, 6, 7
-SPD_DBG_STEP_ITEMS, SPD_DBG_STEP_TRACE = 8, 9
+SPD_DBG_STEP_ITEMS, SPD_DBG_STEP_TRACE, SPD_DBG_KTRACE = 8, 9, 10
 SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD, SPD_K_SPANS, SPD_K_STEP = 1, 2, 3, 4, 5, 6, 7, 8
 SPD_K_MIX = 9
 
@@ -60,7 +60,7 @@ EXPORTS = [
     "spd_set_forced_drafts", "spd_clear_forced_drafts", "spd_run_steps", "spd_sync", "spd_read_debug",
     "spd_read_kv", "spd_set_debug", "spd_destroy", "spd_status_str", "spd_last_error",
     "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing", "spd_set_step_kernel",
-    "spd_set_step_trace", "spd_step_plan_info",
+    "spd_set_step_trace", "spd_step_plan_info", "spd_set_kernel_trace", "spd_set_pdm_placement",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -100,6 +100,8 @@ def lib() -> ct.CDLL:
             "spd_set_graph": (I, [P, I]),
             "spd_set_step_kernel": (I, [P, I, I, I]),
             "spd_set_step_trace": (I, [P, I]),
+            "spd_set_kernel_trace": (I, [P, I]),
+            "spd_set_pdm_placement": (I, [P, I]),
             "spd_step_plan_info": (I, [P, ct.POINTER(ct.c_int32)]),
             "spd_kernel_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
             "spd_span_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_double),
@@ -243,10 +245,28 @@ def spd_set_step_trace(h: int, on: bool) -> None:
 
 
 def spd_step_plan_info(h: int) -> dict:
-    info = (ct.c_int32 * 10)()
+    info = (ct.c_int32 * 16)()
     _check("spd_step_plan_info", lib().spd_step_plan_info(h, info), h)
     return {"nitems": info[0], "J": info[1], "tiles": list(info[2:7]), "clock_khz": info[7],
-            "ntrace": info[8], "pstep_grid": info[9]}
+            "ntrace": info[8], "pstep_grid": info[9], "nkslots": info[10], "n": info[11],
+            "stage_groups": info[12], "pdm_place": info[13]}
+
+
+def spd_set_pdm_placement(h: int, place: int) -> None:
+    _check("spd_set_pdm_placement", lib().spd_set_pdm_placement(h, place), h)
+
+
+def spd_set_kernel_trace(h: int, on: bool) -> None:
+    _check("spd_set_kernel_trace", lib().spd_set_kernel_trace(h, 1 if on else 0), h)
+
+
+def spd_kernel_trace(h: int) -> dict:
+    """The last traced step's launch spans (see SPD_DBG_KTRACE): `stage` [J][5][n][2] and `extra`
+    [4][2] wall-clock stamps (start, end; both 0 where nothing ran)."""
+    info = spd_step_plan_info(h)
+    J, n, ns = info["J"], info["n"], info["nkslots"]
+    raw = spd_read_debug(h, SPD_DBG_KTRACE, 2 * ns, np.uint64).reshape(ns, 2)
+    return {"stage": raw[: 5 * J * n].reshape(J, 5, n, 2), "extra": raw[5 * J * n:], **info}
 
 
 def spd_step_trace(h: int) -> dict:

@@ -25,9 +25,9 @@ enum HState { H_INIT = 0, H_READY = 1, H_PENDING = 2 };
 struct Layout {
   size_t kv, pkv, pt, rope, state, tok, forced, log, resid, anch, pdmx, pfx, pfanch, dbg, lay;
   size_t q[2], ao[2], act[2], part[2], cnt[2], hkey[2];
-  size_t items, sync, dctx, trace;
+  size_t items, sync, dctx, trace, ktrace;
   size_t total;
-  int num_pages, chunk, max_splits, J, nitems, nsync, ntrace;
+  int num_pages, chunk, max_splits, J, nitems, nsync, ntrace, nkslots;
   int tiles[5];
   size_t kv_layer_bytes;
 };
@@ -130,6 +130,8 @@ Layout make_layout(const spd_config& c) {
   L.dctx = take(sizeof(Ctx));
   L.ntrace = std::max(4 * L.nitems, 2048 * 5 * L.J * 3);
   L.trace = take(sizeof(unsigned long long) * (size_t)L.ntrace);
+  L.nkslots = 5 * L.J * n + 4;
+  L.ktrace = take(sizeof(unsigned long long) * 2 * (size_t)L.nkslots);
   L.total = o;
   return L;
 }
@@ -185,6 +187,8 @@ struct spd_handle {
   int step_mode = kStepModeDefault;
   int step_grid = kStepGridDefault;
   int step_skew = kStepSkewDefault;
+  int stage_groups = 0;  // mode 2: streams the stages are spread over (0: kStageGroupsDefault)
+  int pdm_place = 0;     // where the PDM's launches go (spd_set_pdm_placement)
   int pstep_grid = 0;  // mode 4: workgroups, at most what the GPU holds at once
   hipGraphExec_t gexec = nullptr;
   // kernel timing
@@ -284,18 +288,33 @@ template <typename WT>
 static spd_status enqueue_step(spd_handle* h, int forced_override) {
   const Ctx& C = h->ctx;
   hipEvent_t* sp = span_events(h);
+  if (C.ktrace) launch_ktrace_reset(C, h->lay.nkslots, h->main);
   if (sp) HIPC(hipEventRecord(sp[0], h->main));
-  HIPC(hipEventRecord(h->ev_fork, h->main));
-  HIPC(hipStreamWaitEvent(h->pdm, h->ev_fork, 0));
-  // Pipeline Draft Module on its own stream: pre-step features only (Section 3.3)
-  Launch<WT>::pdm_fc(C, 0, 0, h->pdm);
-  for (int i = 0; i < h->cfg.pdm_layers; i++)
-    enqueue_layer<WT>(C, rows_block(h->cfg.n_layers + i, -1, -1, C.pdm_x, nullptr, -1, 1), h->pdm);
   const bool fused = h->cfg.fused_head != 0;
-  h->cur_slot = 0;
-  if (!fused) Launch<WT>::head(C, 1, 0, h->pdm);
-  if (sp) HIPC(hipEventRecord(sp[1], h->pdm));
-  HIPC(hipEventRecord(h->ev_join, h->pdm));
+  // Pipeline Draft Module: pre-step features only (Section 3.3), so it can run beside the stage
+  // compute; it ends by recording ev_join, which the LM head waits for.
+  auto enqueue_pdm = [&](hipStream_t s) -> spd_status {
+    h->cur_slot = 0;
+    Launch<WT>::pdm_fc(C, 0, 0, s);
+    for (int i = 0; i < h->cfg.pdm_layers; i++)
+      enqueue_layer<WT>(C, rows_block(h->cfg.n_layers + i, -1, -1, C.pdm_x, nullptr, -1, 1), s);
+    if (!fused) Launch<WT>::head(C, 1, 0, s);
+    if (sp) HIPC(hipEventRecord(sp[1], s));
+    HIPC(hipEventRecord(h->ev_join, s));
+    return SPD_OK;
+  };
+  const bool stage_streams = h->step_mode == 2;
+  const int place = stage_streams ? h->pdm_place : (h->pdm_place == 1 ? 1 : 0);
+  if (place == 1) {  // on main_stream, before the stage compute
+    spd_status st = enqueue_pdm(h->main);
+    if (st != SPD_OK) return st;
+  }
+  HIPC(hipEventRecord(h->ev_fork, h->main));
+  if (place == 0) {  // its own stream
+    HIPC(hipStreamWaitEvent(h->pdm, h->ev_fork, 0));
+    spd_status st = enqueue_pdm(h->pdm);
+    if (st != SPD_OK) return st;
+  }
   // every active stage advances its token by one layer per slot (Section 3.1)
   if (h->step_mode == 1) {
     h->cur_slot = 0;
@@ -369,16 +388,23 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     }
     (void)esz;
   } else {
-    // mode 0: every launch covers all stages, on main_stream. mode 2: stage s runs its own chain of
-    // launches on its own stream, forked from and joined to main_stream, so that one stage's
-    // latency-bound attention and launch tails overlap the other stages' weight streaming.
+    // mode 0: every launch covers all stages, on main_stream. mode 2: the stages are spread over G
+    // groups of consecutive stages, each group running its own chain of launches (covering its
+    // stages) on its own stream, forked from and joined to main_stream, so that one group's
+    // latency-bound attention and launch tails overlap the other groups' weight streaming.
     const int n = h->cfg.n_stages;
-    const int groups = h->step_mode == 2 ? n : 1;
+    const int groups =
+        h->step_mode == 2 ? std::min(h->stage_groups > 0 ? h->stage_groups : kStageGroupsDefault, n) : 1;
     for (int gi = 0; gi < groups; gi++) {
+      const int s0 = gi * n / groups, s1 = (gi + 1) * n / groups;
       hipStream_t s = h->main;
       if (h->step_mode == 2) {
         s = h->sst[gi];
         HIPC(hipStreamWaitEvent(s, h->ev_fork, 0));
+      }
+      if (gi == 0 && place == 2) {  // first group's stream, before its stage launches
+        spd_status st = enqueue_pdm(s);
+        if (st != SPD_OK) return st;
       }
       for (int j = 0; j < h->J; j++) {
         h->cur_slot = j;
@@ -386,8 +412,8 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
         std::memset(&r, 0, sizeof(Rows));
         r.kind = 0;
         r.slot = j;
-        r.stage0 = h->step_mode == 2 ? gi : 0;
-        r.nst = h->step_mode == 2 ? 1 : n;
+        r.stage0 = s0;
+        r.nst = s1 - s0;
         r.nrows = 1;
         r.cap = -1;
         bool any = false;
@@ -401,6 +427,10 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
           }
         }
         if (any) enqueue_layer<WT>(C, r, s, h);
+      }
+      if (gi == 0 && place == 3) {  // first group's stream, after its stage launches
+        spd_status st = enqueue_pdm(s);
+        if (st != SPD_OK) return st;
       }
       if (h->step_mode == 2) {
         HIPC(hipEventRecord(h->ev_st[gi], s));
@@ -713,7 +743,9 @@ spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_
     h->step_grid = grid ? grid : kStepGridDefault;
   else if (mode != 4)
     h->ctx.stream_wgs = grid;  // 0: default
-  if (skew >= 0 && skew != h->step_skew) {
+  if (mode == 2) {
+    if (skew >= 0) h->stage_groups = skew;
+  } else if (skew >= 0 && skew != h->step_skew) {
     HIPC(hipSetDevice(h->dev));
     HIPC(hipStreamSynchronize(h->pdm));
     HIPC(hipStreamSynchronize(h->main));
@@ -737,6 +769,24 @@ spd_status spd_set_step_trace(spd_handle* h, int32_t on) {
   return SPD_OK;
 }
 
+spd_status spd_set_pdm_placement(spd_handle* h, int32_t place) {
+  if (!h || place < 0 || place > 3) return SPD_E_INVAL;
+  h->pdm_place = place;
+  drop_graph(h);  // the captured launches change
+  return SPD_OK;
+}
+
+spd_status spd_set_kernel_trace(spd_handle* h, int32_t on) {
+  if (!h) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->pdm));
+  HIPC(hipStreamSynchronize(h->main));
+  h->ctx.ktrace = on ? (unsigned long long*)(h->ws + h->lay.ktrace) : nullptr;
+  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
+  drop_graph(h);  // kernel arguments changed
+  return SPD_OK;
+}
+
 spd_status spd_step_plan_info(spd_handle* h, int32_t* info) {
   if (!h || !info) return SPD_E_INVAL;
   info[0] = h->lay.nitems;
@@ -747,6 +797,13 @@ spd_status spd_step_plan_info(spd_handle* h, int32_t* info) {
   info[7] = khz;
   info[8] = h->lay.ntrace;
   info[9] = h->pstep_grid;
+  info[10] = h->lay.nkslots;
+  info[11] = h->cfg.n_stages;
+  info[12] = h->step_mode == 2 ? std::min(h->stage_groups > 0 ? h->stage_groups : kStageGroupsDefault,
+                                          h->cfg.n_stages)
+                               : 1;
+  info[13] = h->pdm_place;
+  info[14] = info[15] = 0;
   return SPD_OK;
 }
 
@@ -959,6 +1016,10 @@ spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes)
     case SPD_DBG_TOKENS: src = h->ctx.tok; need = sizeof(int32_t) * c.max_tokens; break;
     case SPD_DBG_STATE: src = nullptr; need = sizeof(int32_t) * 4; break;
     case SPD_DBG_STEP_ITEMS: src = h->ctx.plan.items; need = sizeof(uint32_t) * (size_t)h->lay.nitems; break;
+    case SPD_DBG_KTRACE:
+      src = h->ws + h->lay.ktrace;
+      need = sizeof(unsigned long long) * 2 * (size_t)h->lay.nkslots;
+      break;
     case SPD_DBG_STEP_TRACE:
       src = h->ws + h->lay.trace;
       need = sizeof(unsigned long long) * (size_t)h->lay.ntrace;

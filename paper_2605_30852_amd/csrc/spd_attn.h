@@ -17,7 +17,7 @@
 // Each wave keeps its own running (m, l, o); the four are combined in wave order at the end of the
 // split (one barrier). With one split the workgroup writes the output; otherwise the split that
 // finishes last (a ticket per stage and head) merges every split in split order, its loads for up to
-// 16 splits issued at once. The split size is a function of the configuration only, so a token's
+// 32 splits issued at once. The split size is a function of the configuration only, so a token's
 // result never depends on how many stages run.
 #pragma once
 #include "spd_devfn.h"
@@ -28,7 +28,7 @@ constexpr int kAttnTPK = 4;                   // lanes per key
 constexpr int kAttnWaveKeys = 64 / kAttnTPK;  // keys per wave per round
 constexpr int kAttnPass = kWG / kAttnTPK;     // keys per round
 constexpr int kAttnMaxQ = 8;                  // query heads per KV head
-constexpr int kAttnMergeBatch = 16;           // splits whose records the merge loads at once
+constexpr int kAttnMergeBatch = 32;           // splits whose partial outputs the merge loads at once
 
 // LDS: pre-scaled queries, then per wave a V tile (reused for the wave's o at the end), its
 // probabilities, and its rescale factors and (m, l).
@@ -142,48 +142,43 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
   const int R = (k1 - k0 + PASS - 1) / PASS;  // rounds
   const int my = w * WK + kk;                 // this lane's key within a round
 
-  // queries first, then the page of round 1, then rounds 0 and 1 (no wait below waits for later loads)
+  // Every global load below is unconditional (keys past the split read key k1 - 1 and are masked
+  // later), so the count of loads issued after any given load is the same on every path and each
+  // wait covers exactly the loads it needs: queries first, then the page of round 1, round 0, the
+  // page of round 2, round 1.
   constexpr int QPT = (MAXQ * DH + kWG - 1) / kWG;
   float qv[QPT];
 #pragma unroll
   for (int i = 0; i < QPT; i++) {
-    const int e = tid + i * kWG;
-    qv[i] = e < G * DH ? (COH ? ld_dev(q + e) : q[e]) : 0.f;
+    const int e = min(tid + i * kWG, G * DH - 1);
+    qv[i] = COH ? ld_dev(q + e) : q[e];
   }
   auto page_of = [&](int r) { return C.page_table[min(k0 + r * PASS + my, k1 - 1) / C.page]; };
-  int pg_next = R > 1 ? page_of(1) : 0;
+  int pg_next = page_of(1);
   uint4 kb0[KCH], vb0[KCH], kb1[KCH], vb1[KCH];
   auto issue = [&](int r, int page, uint4* kr, uint4* vr) {
-    const int key = k0 + r * PASS + my;
-    if (key < k1) {
-      const KVT* base = kvb + (size_t)page * page_elems + head_off + (size_t)(key % C.page) * DH + qq * NE;
-      if (COH && key == pos0) {
+    const int key = min(k0 + r * PASS + my, k1 - 1);
+    const KVT* base = kvb + (size_t)page * page_elems + head_off + (size_t)(key % C.page) * DH + qq * NE;
+    if (COH) {  // the newest key was written by this launch
 #pragma unroll
-        for (int c = 0; c < KCH; c++) kr[c] = ldg16_coherent(reinterpret_cast<const uint4*>(base) + c);
+      for (int c = 0; c < KCH; c++) kr[c] = ldg16_coherent(reinterpret_cast<const uint4*>(base) + c);
 #pragma unroll
-        for (int c = 0; c < KCH; c++) vr[c] = ldg16_coherent(reinterpret_cast<const uint4*>(base + voff) + c);
-      } else {
+      for (int c = 0; c < KCH; c++) vr[c] = ldg16_coherent(reinterpret_cast<const uint4*>(base + voff) + c);
+    } else {
 #pragma unroll
-        for (int c = 0; c < KCH; c++) kr[c] = ldkv16(reinterpret_cast<const uint4*>(base) + c);
+      for (int c = 0; c < KCH; c++) kr[c] = ldkv16(reinterpret_cast<const uint4*>(base) + c);
 #pragma unroll
-        for (int c = 0; c < KCH; c++) vr[c] = ldkv16(reinterpret_cast<const uint4*>(base + voff) + c);
-      }
-    } else {  // past the split: zeros, so the tile row holds finite values
-#pragma unroll
-      for (int c = 0; c < KCH; c++) kr[c] = vr[c] = make_uint4(0u, 0u, 0u, 0u);
+      for (int c = 0; c < KCH; c++) vr[c] = ldkv16(reinterpret_cast<const uint4*>(base + voff) + c);
     }
   };
   issue(0, page0, kb0, vb0);
-  if (R > 1) {
+  {
     const int pg1 = pg_next;
-    pg_next = R > 2 ? page_of(2) : 0;
+    pg_next = page_of(2);
     issue(1, pg1, kb1, vb1);
   }
 #pragma unroll
-  for (int i = 0; i < QPT; i++) {
-    const int e = tid + i * kWG;
-    if (e < G * DH) qs[e] = qv[i] * C.scale;
-  }
+  for (int i = 0; i < QPT; i++) qs[tid + i * kWG] = qv[i] * C.scale;  // slots >= G: unused
   __syncthreads();  // queries staged
 
   float m_run[NJ], l_run[NJ];
@@ -205,9 +200,9 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
     for (int c = 0; c < KCH; c++) unpack16<KVT>(kr_raw[c], kf + c * VE);
 #pragma unroll
     for (int c = 0; c < KCH; c++) reinterpret_cast<uint4*>(vt + kk * DH + qq * NE)[c] = vr_raw[c];
-    if (r + 2 < R) {  // the buffers are free again: round r + 2, and the page of round r + 3
+    {  // the buffers are free again: round r + 2, and the page of round r + 3 (past the end: key k1 - 1)
       const int pg = pg_next;
-      pg_next = r + 3 < R ? page_of(r + 3) : 0;
+      pg_next = page_of(r + 3);
       issue(r + 2, pg, kr_raw, vr_raw);
     }
     if (nkw > 0) {  // else the wave has no key in this round
@@ -267,9 +262,9 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
     }
     wave_lds_sync();  // the tile and probabilities are rewritten next round
   };
-  for (int r = 0; r < R; r += 2) {
+  for (int r = 0; r < R; r += 2) {  // an odd count ends with a round that has no key
     round(r, kb0, vb0);
-    if (r + 1 < R) round(r + 1, kb1, vb1);
+    round(r + 1, kb1, vb1);
   }
 
   // the wave's (m, l, o) to LDS; o reuses the V tile
@@ -358,47 +353,56 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
   __syncthreads();
   if (!s_last) return false;
 
-  // merge every split in split order (every split has a key, so each m is finite)
+  // merge every split in split order (every split has a key, so each m is finite). All (m, l) pairs
+  // are requested first, then the first batch of partial outputs (split indices clamped, so the loads
+  // are unconditional), then the (m, l) pairs go to LDS.
+  constexpr int MB = kAttnMergeBatch;
+  constexpr int MLT = (kMaxSplits * MAXQ + kWG - 1) / kWG;
+  float* sm = reinterpret_cast<float*>(lbase + LA::kQ);  // [split][MAXQ] m, then l (the wave areas are free)
+  float* sl = sm + kMaxSplits * MAXQ;
+  float mlm[MLT], mll[MLT];
 #pragma unroll
+  for (int i = 0; i < MLT; i++) {
+    const int t = min(tid + i * kWG, nsplit * G - 1), sp = t / G, qi = t % G;
+    mlm[i] = ld_dev(rec_base + (size_t)sp * RS + MAXQ * DH + qi);
+    mll[i] = ld_dev(rec_base + (size_t)sp * RS + MAXQ * DH + MAXQ + qi);
+  }
+  const int qi0 = tid / (DH / 2), dp0 = tid % (DH / 2);
+  const int qc0 = min(qi0, G - 1);
+  float2 ob[MB];
+#pragma unroll
+  for (int j = 0; j < MB; j++) ob[j] = ld_dev2(rec_base + (size_t)min(j, nsplit - 1) * RS + qc0 * DH + 2 * dp0);
+#pragma unroll
+  for (int i = 0; i < MLT; i++) {
+    const int t = tid + i * kWG;
+    if (t < nsplit * G) {
+      sm[(t / G) * MAXQ + t % G] = mlm[i];
+      sl[(t / G) * MAXQ + t % G] = mll[i];
+    }
+  }
+  __syncthreads();
+#pragma unroll 1
   for (int i = 0; i < PPT; i++) {
     const int e = tid + i * kWG, qi = e / (DH / 2), dp = e % (DH / 2);
     if (qi < G) {
-      float M = -INFINITY, L = 0.f, a0 = 0.f, a1 = 0.f;
-      for (int sp0 = 0; sp0 < nsplit; sp0 += kAttnMergeBatch) {
-        float mb[kAttnMergeBatch], lb[kAttnMergeBatch];
-        float2 ob[kAttnMergeBatch];
+      float M = -INFINITY;
+      for (int sp = 0; sp < nsplit; sp++) M = fmaxf(M, sm[sp * MAXQ + qi]);
+      float L = 0.f, a0 = 0.f, a1 = 0.f;
+      for (int sp0 = 0; sp0 < nsplit; sp0 += MB) {
+        if (i > 0 || sp0 > 0) {
 #pragma unroll
-        for (int j = 0; j < kAttnMergeBatch; j++) {
-          const float* rj = rec_base + (size_t)(sp0 + j) * RS;
-          if (sp0 + j < nsplit) {
-            ob[j] = ld_dev2(rj + qi * DH + 2 * dp);
-            mb[j] = ld_dev(rj + MAXQ * DH + qi);
-            lb[j] = ld_dev(rj + MAXQ * DH + MAXQ + qi);
-          } else {
-            ob[j] = make_float2(0.f, 0.f);
-            mb[j] = -INFINITY;
-            lb[j] = 0.f;
-          }
-        }
-        float Mn = M;
-#pragma unroll
-        for (int j = 0; j < kAttnMergeBatch; j++) Mn = fmaxf(Mn, mb[j]);
-        if (M != -INFINITY) {
-          const float sc = expf(M - Mn);
-          L *= sc;
-          a0 *= sc;
-          a1 *= sc;
+          for (int j = 0; j < MB; j++)
+            ob[j] = ld_dev2(rec_base + (size_t)min(sp0 + j, nsplit - 1) * RS + qi * DH + 2 * dp);
         }
 #pragma unroll
-        for (int j = 0; j < kAttnMergeBatch; j++) {
+        for (int j = 0; j < MB; j++) {
           if (sp0 + j < nsplit) {
-            const float f = expf(mb[j] - Mn);
-            L = fmaf(lb[j], f, L);
+            const float f = expf(sm[(sp0 + j) * MAXQ + qi] - M);
+            L = fmaf(sl[(sp0 + j) * MAXQ + qi], f, L);
             a0 = fmaf(ob[j].x, f, a0);
             a1 = fmaf(ob[j].y, f, a1);
           }
         }
-        M = Mn;
       }
       const float inv = 1.0f / L;
       if (COH)

@@ -67,6 +67,9 @@ constexpr int kDRows = 8;    // down item: 8 rows (1 row pair per wave)
 constexpr int kStepGridDefault = 512;
 constexpr int kStepSkewDefault = 0;
 constexpr int kStepModeDefault = 2;
+// mode 2: stage groups (streams). With the PDM's stream, more than four parallel chains per step make
+// the runtime run one chain after another; two groups keep every chain running from the fork.
+constexpr int kStageGroupsDefault = 2;
 constexpr int kStreamWGs = 768;  // workgroups of one streaming stage launch (all its stages)
 __host__ __device__ inline uint32_t step_item(int p, int s, int t) {
   return ((uint32_t)p << 19) | ((uint32_t)s << 16) | (uint32_t)t;
@@ -124,6 +127,7 @@ struct Ctx {
   int debug;
   BufSet b[2];      // 0: target stream, 1: PDM stream
   StepPlan plan;    // persistent step kernel
+  unsigned long long* ktrace;  // null, or the launch trace: per slot (first start, last end) wall clock
   int stream_wgs;   // workgroups of one streaming stage launch (all its stages)
   int J;            // layer slots per step (longest stage)
 };
@@ -191,6 +195,7 @@ void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* stream,
 // Every layer slot of every active stage of one step in one persistent launch (spd_step.hip).
 // dev_ctx: a device copy of c.
 void launch_step(const Ctx& c, const Ctx* dev_ctx, int grid, void* stream, int bf16);
+void launch_ktrace_reset(const Ctx& c, int nslots, void* stream);
 size_t step_lds_bytes(const Ctx& c, int bf16);
 // Events (hipEvent_t) that the next launches of this host thread record at their own start and end;
 // nullptr turns it off.

@@ -211,6 +211,22 @@ static __device__ __noinline__ void wait_count_sum(int* sync, int idx, int parts
   }
 }
 
+// Launch trace (debugging and measurement): slot (j * 5 + k) * n + s is sublayer k of layer slot j
+// of stage s; then the LM head, verify and the PDM's feature projection. The launch's first
+// workgroup (dispatched first) stores the start; every workgroup folds its end time into the slot
+// with a maximum that nothing waits for, so the trace barely moves the schedule it measures.
+enum KTraceExtra { KT_HEAD = 0, KT_VERIFY = 1, KT_PDM = 2, KT_EXTRA = 4 };
+__device__ __forceinline__ int ktrace_slot(const Ctx& C, int j, int k, int s) { return (j * 5 + k) * C.n + s; }
+__device__ __forceinline__ int ktrace_extra(const Ctx& C, int e) { return 5 * C.J * C.n + e; }
+__device__ __forceinline__ void ktrace_start(const Ctx& C, int slot, bool first) {
+  if (C.ktrace != nullptr && first && threadIdx.x == 0) C.ktrace[2 * slot] = (unsigned long long)wall_clock64();
+}
+__device__ __forceinline__ void ktrace_end(const Ctx& C, int slot) {
+  if (C.ktrace != nullptr && threadIdx.x == 0)
+    __hip_atomic_fetch_max(C.ktrace + 2 * slot + 1, (unsigned long long)wall_clock64(), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // A KV-cache element with a device-scope store.
 template <typename T>
 __device__ __forceinline__ void st_kv_dev(T* p, float v);

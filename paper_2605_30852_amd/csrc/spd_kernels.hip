@@ -555,7 +555,10 @@ template <typename WT, int KIND>
 __global__ __launch_bounds__(kWG) void k_sgemv(Ctx C, Rows R) {
   const Grp gr = resolve(C, R, blockIdx.y);
   if (!gr.active) return;
+  const int ts = ktrace_slot(C, R.slot, KIND, gr.s);
+  ktrace_start(C, ts, blockIdx.x == 0);
   sgemv_part<WT, KIND, false>(C, gr, R.ld[gr.s], R.set, blockIdx.x, gridDim.x, [] {});  // stage launches carry their layers
+  ktrace_end(C, ts);
 }
 
 // ---------------------------------------------------------------------- PDM feature projection
@@ -563,7 +566,7 @@ __global__ __launch_bounds__(kWG) void k_sgemv(Ctx C, Rows R) {
 // one projection whose column block j serves anchor j). prefill = 1: rows of the prefill chunk
 // at full depth; else the a in-flight rows, row i at depth a-1-i. Tile = 8 outputs (2 per wave).
 template <typename WT>
-__global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_arg) {
+__device__ __forceinline__ void pdm_fc_body(const Ctx& C, int prefill, int nrows_arg) {
   extern __shared__ __align__(16) float lds[];
   constexpr int NV = kMaxRows;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -607,6 +610,13 @@ __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_ar
   }
 }
 
+template <typename WT>
+__global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_arg) {
+  ktrace_start(C, ktrace_extra(C, KT_PDM), blockIdx.x == 0 && blockIdx.y == 0);
+  pdm_fc_body<WT>(C, prefill, nrows_arg);
+  ktrace_end(C, ktrace_extra(C, KT_PDM));
+}
+
 // ---------------------------------------------------------------------------- LM head + argmax
 // Tile = kHeadRows vocabulary rows, kHeadRows/4 per wave in pairs. Each workgroup writes its best
 // (value, index), the lowest index winning ties; the single-workgroup kernel that follows on the
@@ -617,7 +627,7 @@ __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_ar
 // 2: prefill row `row`; 3: the exit row and the PDM's last row together (rows 0 and 1), one pass over
 // W_lm serving both heads. Row results go to the partials of set 0 (target) or set 1 (PDM).
 template <typename WT, int NV>
-__global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row) {
+__device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
   extern __shared__ __align__(16) float lds[];
   __shared__ float s_v[NV][4];
   __shared__ int s_i[NV][4];
@@ -728,6 +738,13 @@ __global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row) {
     // the maximum is order-independent, so the result does not depend on which tile lands last
     __hip_atomic_fetch_max(C.b[set[v]].hkey, argmax_key(fv, fi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+}
+
+template <typename WT, int NV>
+__global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row) {
+  ktrace_start(C, ktrace_extra(C, KT_HEAD), blockIdx.x == 0 && blockIdx.y == 0);
+  head_body<WT, NV>(C, src, row);
+  ktrace_end(C, ktrace_extra(C, KT_HEAD));
 }
 
 // The LM-head argmax of one stream's row, read (and reset to zero for the next pass) by the single
@@ -953,7 +970,22 @@ __device__ __forceinline__ void attn_part(const Ctx& C, int s, int slot, const K
 template <typename KVT, int DH, int GP>
 __global__ __launch_bounds__(kWG) void k_attn_stage(Ctx C, Rows R) {
   const int s = R.stage0 + blockIdx.z;
+  const int ts = ktrace_slot(C, R.slot, SK_ATTN, s);
+  ktrace_start(C, ts, blockIdx.x == 0 && blockIdx.y == 0);
   attn_part<KVT, DH, GP>(C, s, R.slot, (const KVT*)R.ld[s].kv, R.set, blockIdx.y, blockIdx.x);
+  ktrace_end(C, ts);
+}
+
+// Launch trace reset.
+__global__ __launch_bounds__(kWG) void k_ktrace_reset(Ctx C, int nslots) {
+  for (int i = blockIdx.x * kWG + threadIdx.x; i < nslots; i += gridDim.x * kWG) {
+    C.ktrace[2 * i] = 0ull;
+    C.ktrace[2 * i + 1] = 0ull;
+  }
+}
+
+void launch_ktrace_reset(const Ctx& c, int nslots, void* stream) {
+  hipLaunchKernelGGL(k_ktrace_reset, dim3((nslots + kWG - 1) / kWG), dim3(kWG), 0, (hipStream_t)stream, c, nslots);
 }
 
 // ---------------------------------------------------------------------------- mixed launches
@@ -1159,7 +1191,7 @@ __device__ __forceinline__ void reset_step_sync(const Ctx& C) {
 // Greedy streaming verification (Section 3.4) and the pipeline state update; single workgroup,
 // last kernel of a step.
 template <typename WT>
-__global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int auto_rb) {
+__device__ __forceinline__ void verify_body(const Ctx& C, int forced_override, int auto_rb) {
   __shared__ int s_tok, s_pos;
   DevState* st = C.st;
   const int y_all = (st->a == C.n) ? take_head(C.b[0], C.V) : -1;
@@ -1231,6 +1263,13 @@ __global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int 
     const int row = s_pos % C.n;
     push_embedding<WT>(C, s_tok, C.resid + (size_t)row * C.d, C.anchors + (size_t)row * C.n * C.d);
   }
+}
+
+template <typename WT>
+__global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int auto_rb) {
+  ktrace_start(C, ktrace_extra(C, KT_VERIFY), blockIdx.x == 0 && blockIdx.y == 0);
+  verify_body<WT>(C, forced_override, auto_rb);
+  ktrace_end(C, ktrace_extra(C, KT_VERIFY));
 }
 
 // Rollback / first placement: c := keep, one token in flight at position keep (tok < 0: the value

@@ -158,6 +158,9 @@ class Engine:
     def spd_set_step_kernel(self, mode: int, grid: int = 0, skew: int = -1) -> None:
         B.spd_set_step_kernel(self.h, mode, grid, skew)
 
+    def spd_set_pdm_placement(self, place: int) -> None:
+        B.spd_set_pdm_placement(self.h, place)
+
     def spd_set_debug(self, on: bool) -> None:
         B.spd_set_debug(self.h, on)
 

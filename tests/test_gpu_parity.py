@@ -229,21 +229,28 @@ def test_graph_replay_matches_eager(mid_w):
         e.close()
 
 
-@pytest.mark.parametrize("which,n,mode,grid,skew", [
-    ("mid", 3, 1, 0, 0), ("mid", 3, 1, 1, 0), ("mid", 3, 1, 37, 1), ("mid", 1, 1, 5, 0), ("tiny", 2, 1, 0, 2),
-    ("tiny", 4, 1, 3, 1), ("mid", 3, 2, 0, -1), ("tiny", 4, 2, 0, -1), ("mid", 1, 2, 0, -1),
-    ("mid", 3, 3, 0, -1), ("mid", 3, 3, 7, -1), ("tiny", 4, 3, 0, -1), ("tiny", 3, 3, 0, -1), ("mid", 1, 3, 0, -1),
-    ("mid", 3, 4, 0, -1), ("mid", 3, 4, 24, -1), ("tiny", 4, 4, 0, -1), ("tiny", 3, 4, 16, -1), ("mid", 1, 4, 0, -1)])
-def test_step_modes_bit_identical_to_sublayer_launches(tiny_w, mid_w, which, n, mode, grid, skew):
+@pytest.mark.parametrize("which,n,mode,grid,skew,place", [
+    ("mid", 3, 1, 0, 0, 0), ("mid", 3, 1, 1, 0, 0), ("mid", 3, 1, 37, 1, 0), ("mid", 1, 1, 5, 0, 0),
+    ("tiny", 2, 1, 0, 2, 0), ("tiny", 4, 1, 3, 1, 0),
+    ("mid", 3, 2, 0, -1, 0), ("tiny", 4, 2, 0, -1, 0), ("mid", 1, 2, 0, -1, 0), ("mid", 3, 2, 0, 3, 0),
+    ("tiny", 4, 2, 0, 4, 0), ("tiny", 4, 2, 0, 3, 0), ("mid", 3, 2, 0, 1, 0),
+    ("tiny", 4, 2, 0, 2, 1), ("mid", 3, 2, 0, 2, 2), ("tiny", 4, 2, 0, 4, 3), ("mid", 3, 0, 0, -1, 1),
+    ("mid", 3, 3, 0, -1, 0), ("mid", 3, 3, 7, -1, 0), ("tiny", 4, 3, 0, -1, 0), ("tiny", 3, 3, 0, -1, 0),
+    ("mid", 1, 3, 0, -1, 0),
+    ("mid", 3, 4, 0, -1, 0), ("mid", 3, 4, 24, -1, 0), ("tiny", 4, 4, 0, -1, 0), ("tiny", 3, 4, 16, -1, 0),
+    ("mid", 1, 4, 0, -1, 0)])
+def test_step_modes_bit_identical_to_sublayer_launches(tiny_w, mid_w, which, n, mode, grid, skew, place):
     """Every way of launching the stage compute gives the same bits as five launches per layer slot
     covering all stages: decisions, tokens, in-flight residual streams and anchors after every step.
     Mode 1 is the persistent step kernel (tiles taken from a ticket counter, data handed between
     workgroups inside the launch; small grids make few workgroups walk the whole tile order, grid 1
-    strictly in ticket order, with the stages in lockstep or staggered); mode 2 runs each stage's
-    launches on its own stream; mode 3 is the skewed schedule of mixed launches (grid 7: few
-    workgroups per weight-streaming part); mode 4 is the persistent launch with one group of
-    workgroups per stage (small grids: few workgroups per group, so each walks many rows)."""
-    _say(f"[step mode {mode} vs sublayer launches {which} n={n} grid={grid} skew={skew}]")
+    strictly in ticket order, with the stages in lockstep or staggered); mode 2 runs groups of stages
+    on their own streams (skew = the number of groups; -1: the default) with the draft module on its
+    own stream, on main_stream before the stages, or on the first group's stream before or after its
+    stages (place 0-3); mode 3 is the skewed schedule of mixed launches (grid 7: few workgroups per
+    weight-streaming part); mode 4 is the persistent launch with one group of workgroups per stage
+    (small grids: few workgroups per group, so each walks many rows)."""
+    _say(f"[step mode {mode} vs sublayer launches {which} n={n} grid={grid} skew={skew} pdm place={place}]")
     w = tiny_w if which == "tiny" else mid_w
     sh = w.shape
     prompt = synth.prompt(sh, SEED + 7, 41)
@@ -256,7 +263,9 @@ def test_step_modes_bit_identical_to_sublayer_launches(tiny_w, mid_w, which, n, 
     engs = []
     for m in (0, mode):
         e = _engine(w, n, max_tokens=200, attn_chunk=32)
-        e.spd_set_step_kernel(m, grid if m in (1, 4) else 0, skew if m == 1 else -1)
+        e.spd_set_step_kernel(m, grid if m in (1, 4) else 0, skew if m == mode and m in (1, 2) else -1)
+        if m == mode:
+            e.spd_set_pdm_placement(place)
         assert e.spd_prefill(prompt) == first
         e.spd_set_forced_drafts(arr, len(prompt))
         engs.append(e)
