@@ -164,12 +164,16 @@ def main():
                          "workgroups per stage")
     ap.add_argument("--step-grid", type=int, default=0, help="workgroups of the persistent step launch (0: default)")
     ap.add_argument("--stage-groups", type=int, default=0, help="mode 2: stage streams (0: the library default)")
-    ap.add_argument("--pdm-place", type=int, default=0, choices=[0, 1, 2, 3],
-                    help="PDM launches: own stream, main before the stages, first group before/after")
+    ap.add_argument("--pdm-grid", type=int, default=0, help="workgroups per PDM GEMV launch (0: the default)")
+    ap.add_argument("--pdm-place", type=int, default=0, choices=[0, 1, 2, 3, 4],
+                    help="PDM launches: own stream, main before the stages, first group before/after, "
+                         "spread over the groups")
     ap.add_argument("--attn-chunk", type=int, default=0, help="keys per attention split (0: the workload's default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (the known-size kernel for HBM counter scaling)")
     args = ap.parse_args()
+    if args.pdm_place == 4 and not args.no_graph:
+        sys.exit("--pdm-place 4 (spread over the stage streams) runs with issued launches only: add --no-graph")
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the SPD step here is the single-GPU stage-batched "
               "form; multi-GPU sharding is not built", file=sys.stderr)
@@ -239,6 +243,7 @@ def main():
     eng = Engine(weights, max_tokens=max_tokens, n=n, attn_chunk=attn_chunk, fused_head=fused)
     eng.spd_set_step_kernel(mode, args.step_grid, args.stage_groups if mode == 2 else -1)
     eng.spd_set_pdm_placement(args.pdm_place)
+    eng.spd_set_pdm_grid(args.pdm_grid)
     eng.spd_set_graph(not args.no_graph)
     groups = B.spd_step_plan_info(eng.h)["stage_groups"]
     f2 = eng.spd_prefill(prompt)
@@ -383,7 +388,8 @@ def main():
                    "step_grid": args.step_grid or None,
                    "pdm_placement": {0: "own stream", 1: "main stream before the stages",
                                      2: "first stage group's stream, before its stages",
-                                     3: "first stage group's stream, after its stages"}[args.pdm_place]},
+                                     3: "first stage group's stream, after its stages",
+                                     4: "spread over the stage groups' streams"}[args.pdm_place]},
         "bytes_per_step": int(bytes_step),
         "step_GBps": round(gbs, 1),
         "step_roofline_frac": round(gbs / PEAK_HBM_GBS, 4),

@@ -252,8 +252,15 @@ spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_
 /* Where the Pipeline Draft Module's launches go within a step (it reads only pre-step features, so
  * any placement gives the same results): 0 (default): its own stream, forked from main_stream;
  * 1: main_stream, before the stage compute; 2 and 3 (mode 2 only; otherwise 0): the first stage
- * group's stream, before (2) or after (3) that group's stage launches. */
+ * group's stream, before (2) or after (3) that group's stage launches; 4 (mode 2 only; otherwise 0):
+ * spread over the groups' streams, PDM launch i on group i mod G after its layer slot min(i, J-1),
+ * each PDM launch ordered after the previous one by an event (no extra stream); issued launches only:
+ * SPD_E_INVAL while graph mode is on, and spd_set_graph(h, 1) fails while placement 4 is set. */
 spd_status spd_set_pdm_placement(spd_handle* h, int32_t place);
+
+/* Workgroups of each of the PDM's GEMV launches in a step (0: the default, 32). The PDM runs beside
+ * the stage compute, so its launches are kept small enough to leave most CUs to the stages. */
+spd_status spd_set_pdm_grid(spd_handle* h, int32_t wgs);
 
 /* Tracing of the persistent step launch: while on, every tile records four wall-clock stamps (for
  * SPD_DBG_STEP_TRACE; each step overwrites them). Costs a few stores per tile. */

@@ -61,6 +61,7 @@ EXPORTS = [
     "spd_read_kv", "spd_set_debug", "spd_destroy", "spd_status_str", "spd_last_error",
     "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing", "spd_set_step_kernel",
     "spd_set_step_trace", "spd_step_plan_info", "spd_set_kernel_trace", "spd_set_pdm_placement",
+    "spd_set_pdm_grid",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -102,6 +103,7 @@ def lib() -> ct.CDLL:
             "spd_set_step_trace": (I, [P, I]),
             "spd_set_kernel_trace": (I, [P, I]),
             "spd_set_pdm_placement": (I, [P, I]),
+            "spd_set_pdm_grid": (I, [P, I]),
             "spd_step_plan_info": (I, [P, ct.POINTER(ct.c_int32)]),
             "spd_kernel_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
             "spd_span_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_double),
@@ -254,6 +256,10 @@ def spd_step_plan_info(h: int) -> dict:
 
 def spd_set_pdm_placement(h: int, place: int) -> None:
     _check("spd_set_pdm_placement", lib().spd_set_pdm_placement(h, place), h)
+
+
+def spd_set_pdm_grid(h: int, wgs: int) -> None:
+    _check("spd_set_pdm_grid", lib().spd_set_pdm_grid(h, wgs), h)
 
 
 def spd_set_kernel_trace(h: int, on: bool) -> None:

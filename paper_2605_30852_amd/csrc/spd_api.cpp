@@ -168,6 +168,7 @@ struct spd_handle {
   int J = 0;  // layer slots per step = longest stage
   hipStream_t main = nullptr, pdm = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  std::vector<hipEvent_t> ev_pdm;  // placement 4: one per PDM launch
   // step-kernel mode 2: one stream and one completion event per stage (default priority)
   hipStream_t sst[kMaxStages] = {};
   hipEvent_t ev_st[kMaxStages] = {};
@@ -293,15 +294,28 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
   const bool fused = h->cfg.fused_head != 0;
   // Pipeline Draft Module: pre-step features only (Section 3.3), so it can run beside the stage
   // compute; it ends by recording ev_join, which the LM head waits for.
-  auto enqueue_pdm = [&](hipStream_t s) -> spd_status {
-    h->cur_slot = 0;
-    Launch<WT>::pdm_fc(C, 0, 0, s);
-    for (int i = 0; i < h->cfg.pdm_layers; i++)
-      enqueue_layer<WT>(C, rows_block(h->cfg.n_layers + i, -1, -1, C.pdm_x, nullptr, -1, 1), s);
-    if (!fused) Launch<WT>::head(C, 1, 0, s);
+  // its launches, in order: the feature projection, five per PDM layer, the draft head if not fused
+  const int npdm = 1 + 5 * h->cfg.pdm_layers + (fused ? 0 : 1);
+  auto pdm_op = [&](int i, hipStream_t s) {
+    if (i == 0) {
+      Launch<WT>::pdm_fc(C, 0, 0, s);
+    } else if (i <= 5 * h->cfg.pdm_layers) {
+      const int l = (i - 1) / 5, k = (i - 1) % 5;
+      Launch<WT>::rows_sublayer(C, rows_block(h->cfg.n_layers + l, -1, -1, C.pdm_x, nullptr, -1, 1),
+                                h->cfg.n_stages, k, s);
+    } else {
+      Launch<WT>::head(C, 1, 0, s);
+    }
+  };
+  auto pdm_end = [&](hipStream_t s) -> spd_status {
     if (sp) HIPC(hipEventRecord(sp[1], s));
     HIPC(hipEventRecord(h->ev_join, s));
     return SPD_OK;
+  };
+  auto enqueue_pdm = [&](hipStream_t s) -> spd_status {
+    h->cur_slot = 0;
+    for (int i = 0; i < npdm; i++) pdm_op(i, s);
+    return pdm_end(s);
   };
   const bool stage_streams = h->step_mode == 2;
   const int place = stage_streams ? h->pdm_place : (h->pdm_place == 1 ? 1 : 0);
@@ -395,18 +409,38 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     const int n = h->cfg.n_stages;
     const int groups =
         h->step_mode == 2 ? std::min(h->stage_groups > 0 ? h->stage_groups : kStageGroupsDefault, n) : 1;
+    hipStream_t gs[kMaxStages];
     for (int gi = 0; gi < groups; gi++) {
-      const int s0 = gi * n / groups, s1 = (gi + 1) * n / groups;
-      hipStream_t s = h->main;
-      if (h->step_mode == 2) {
-        s = h->sst[gi];
-        HIPC(hipStreamWaitEvent(s, h->ev_fork, 0));
+      gs[gi] = h->step_mode == 2 ? h->sst[gi] : h->main;
+      if (h->step_mode == 2) HIPC(hipStreamWaitEvent(gs[gi], h->ev_fork, 0));
+    }
+    if (place == 2) {  // first group's stream, before its stage launches
+      spd_status st = enqueue_pdm(gs[0]);
+      if (st != SPD_OK) return st;
+    }
+    // Placement 4 spreads the PDM over the groups' streams: launch i runs on group i mod G after that
+    // group's layer slot min(i, J - 1), ordered after launch i - 1 by an event; a layer slot takes
+    // much longer than one PDM launch, so no group waits. Launches are enqueued slot by slot across
+    // the groups, so each event is recorded before it is waited for.
+    int pi = 0;
+    auto spread = [&](int j, int gi) -> spd_status {
+      while (place == 4 && pi < npdm && pi % groups == gi && std::min(pi, h->J - 1) <= j) {
+        if (pi > 0) HIPC(hipStreamWaitEvent(gs[gi], h->ev_pdm[pi - 1], 0));
+        const int keep = h->cur_slot;
+        h->cur_slot = 0;  // not a timed stage launch
+        pdm_op(pi, gs[gi]);
+        h->cur_slot = keep;
+        HIPC(hipEventRecord(h->ev_pdm[pi], gs[gi]));
+        if (++pi == npdm) {
+          spd_status st = pdm_end(gs[gi]);
+          if (st != SPD_OK) return st;
+        }
       }
-      if (gi == 0 && place == 2) {  // first group's stream, before its stage launches
-        spd_status st = enqueue_pdm(s);
-        if (st != SPD_OK) return st;
-      }
-      for (int j = 0; j < h->J; j++) {
+      return SPD_OK;
+    };
+    for (int j = 0; j < h->J; j++) {
+      for (int gi = 0; gi < groups; gi++) {
+        const int s0 = gi * n / groups, s1 = (gi + 1) * n / groups;
         h->cur_slot = j;
         Rows r;
         std::memset(&r, 0, sizeof(Rows));
@@ -426,14 +460,22 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
             std::memset(&r.ld[st], 0, sizeof(LayerDesc));
           }
         }
-        if (any) enqueue_layer<WT>(C, r, s, h);
-      }
-      if (gi == 0 && place == 3) {  // first group's stream, after its stage launches
-        spd_status st = enqueue_pdm(s);
+        if (any) enqueue_layer<WT>(C, r, gs[gi], h);
+        spd_status st = spread(j, gi);
         if (st != SPD_OK) return st;
       }
-      if (h->step_mode == 2) {
-        HIPC(hipEventRecord(h->ev_st[gi], s));
+    }
+    for (int guard = 0; place == 4 && pi < npdm && guard < npdm * kMaxStages; guard++) {  // leftovers
+      spd_status st = spread(h->J - 1, pi % groups);
+      if (st != SPD_OK) return st;
+    }
+    if (place == 3) {  // first group's stream, after its stage launches
+      spd_status st = enqueue_pdm(gs[0]);
+      if (st != SPD_OK) return st;
+    }
+    if (h->step_mode == 2) {
+      for (int gi = 0; gi < groups; gi++) {
+        HIPC(hipEventRecord(h->ev_st[gi], gs[gi]));
         HIPC(hipStreamWaitEvent(h->main, h->ev_st[gi], 0));
       }
     }
@@ -580,6 +622,8 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
     HIPI(hipStreamCreateWithFlags(&h->sst[st], hipStreamNonBlocking));
     HIPI(hipEventCreateWithFlags(&h->ev_st[st], hipEventDisableTiming));
   }
+  h->ev_pdm.assign(2 + 5 * (size_t)cfg->pdm_layers, nullptr);
+  for (hipEvent_t& e : h->ev_pdm) HIPI(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   HIPI(hipHostMalloc((void**)&h->pinned, sizeof(spd_step_result) * (kLogCap + 1), hipHostMallocDefault));
 
   const spd_config& c = *cfg;
@@ -598,6 +642,7 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   C.ls = c.pdm_layers;
   C.page = c.page_size;
   C.chunk = lay.chunk;
+  C.rows_wgs = kRowsWGsDefault;
   C.max_pages = lay.num_pages;
   C.max_splits = lay.max_splits;
   C.max_tokens = c.max_tokens;
@@ -770,9 +815,20 @@ spd_status spd_set_step_trace(spd_handle* h, int32_t on) {
 }
 
 spd_status spd_set_pdm_placement(spd_handle* h, int32_t place) {
-  if (!h || place < 0 || place > 3) return SPD_E_INVAL;
+  if (!h || place < 0 || place > 4) return SPD_E_INVAL;
+  if (place == 4 && h->use_graph) {
+    h->err = "PDM placement 4 is not captured into the step graph (turn graph mode off first)";
+    return SPD_E_INVAL;
+  }
   h->pdm_place = place;
   drop_graph(h);  // the captured launches change
+  return SPD_OK;
+}
+
+spd_status spd_set_pdm_grid(spd_handle* h, int32_t wgs) {
+  if (!h || wgs < 0 || wgs > 65535) return SPD_E_INVAL;
+  h->ctx.rows_wgs = wgs > 0 ? wgs : kRowsWGsDefault;
+  drop_graph(h);  // kernel arguments changed
   return SPD_OK;
 }
 
@@ -915,6 +971,10 @@ static spd_status run_one_step(spd_handle* h, int forced_override) {
 
 spd_status spd_set_graph(spd_handle* h, int32_t on) {
   if (!h) return SPD_E_INVAL;
+  if (on && h->pdm_place == 4) {
+    h->err = "PDM placement 4 is not captured into the step graph (choose another placement first)";
+    return SPD_E_INVAL;
+  }
   h->use_graph = on ? 1 : 0;
   if (!on) drop_graph(h);
   return SPD_OK;
@@ -1133,6 +1193,8 @@ void spd_destroy(spd_handle* h) {
     if (h->ev_st[st]) (void)hipEventDestroy(h->ev_st[st]);
     if (h->sst[st]) (void)hipStreamDestroy(h->sst[st]);
   }
+  for (hipEvent_t e : h->ev_pdm)
+    if (e) (void)hipEventDestroy(e);
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_join) (void)hipEventDestroy(h->ev_join);
   if (h->pinned) (void)hipHostFree(h->pinned);

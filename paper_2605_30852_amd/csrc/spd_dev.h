@@ -70,7 +70,10 @@ constexpr int kStepModeDefault = 2;
 // mode 2: stage groups (streams). With the PDM's stream, more than four parallel chains per step make
 // the runtime run one chain after another; two groups keep every chain running from the fork.
 constexpr int kStageGroupsDefault = 2;
-constexpr int kStreamWGs = 768;  // workgroups of one streaming stage launch (all its stages)
+constexpr int kStreamWGs = 1024;  // workgroups of one streaming stage launch (all its stages)
+// PDM row-block GEMV launches run beside the stage compute: a few workgroups, so that most CUs (and
+// their LDS) stay with the stage launches.
+constexpr int kRowsWGsDefault = 32;
 __host__ __device__ inline uint32_t step_item(int p, int s, int t) {
   return ((uint32_t)p << 19) | ((uint32_t)s << 16) | (uint32_t)t;
 }
@@ -129,6 +132,7 @@ struct Ctx {
   StepPlan plan;    // persistent step kernel
   unsigned long long* ktrace;  // null, or the launch trace: per slot (first start, last end) wall clock
   int stream_wgs;   // workgroups of one streaming stage launch (all its stages)
+  int rows_wgs;     // at most this many workgroups per row-block (PDM) GEMV launch (0: no cap)
   int J;            // layer slots per step (longest stage)
 };
 
@@ -177,6 +181,12 @@ struct Launch {
   static void oproj(const Ctx& c, const Rows& r, void* stream);
   static void gateup(const Ctx& c, const Rows& r, void* stream);
   static void down(const Ctx& c, const Rows& r, void* stream);
+  // One decoder layer of a row block whose rows share the layer (the PDM's rows in a step; at most
+  // max_rows rows, r.anch unused): streaming GEMVs applying each weight pair to all rows, and the
+  // rows' decode attention. Five launches.
+  static void rows_layer(const Ctx& c, const Rows& r, int max_rows, void* stream);
+  // sublayer k (0 QKV, 1 attention, 2 O-proj, 3 gate/up, 4 down) of rows_layer
+  static void rows_sublayer(const Ctx& c, const Rows& r, int max_rows, int k, void* stream);
   // PDM feature projection; prefill = 1: nrows rows of pf_anch at full depth.
   static void pdm_fc(const Ctx& c, int prefill, int nrows, void* stream);
   // LM head + argmax partials. src: 0 = target exit row (skipped unless a == n), 1 = PDM last row,

@@ -144,6 +144,83 @@ __device__ __forceinline__ void stream_run(const RowFn& rowptr, const DoneFn& do
 }
 
 
+// Several rows against the same weights: a wave streams its row pairs once and multiplies every
+// block by the nr (<= NR) vectors staged in LDS (vector r at lds + r * ldsK), each row keeping its
+// own accumulators in the single-row FMA order; when a pair's last group is done every lane calls
+// done(pair, s0, s1) with the nr rows' two dot products (entries >= nr are zero).
+template <typename WT, int NR, typename DoneFn>
+__device__ __forceinline__ void rgemv_comp(int nb, int ng, int u, int lane, const float* lds, int ldsK, int nr,
+                                           const uint4 (&b)[2][kU], float (&a0)[NR], float (&a1)[NR],
+                                           const DoneFn& done) {
+  constexpr int VE = Elt<WT>::VE;
+  constexpr int BLK = 64 * VE;
+  const int rp = u / ng, gi = u - rp * ng, g0 = gi * kU;
+#pragma unroll
+  for (int uu = 0; uu < kU; uu++) {
+    const int blk = g0 + uu;
+    if (blk < nb) {
+      float w0[VE], w1[VE];
+      unpack16<WT>(b[0][uu], w0);
+      unpack16<WT>(b[1][uu], w1);
+#pragma unroll
+      for (int r = 0; r < NR; r++) {
+        if (r < nr) {
+          float x[VE];
+          const float* xb = lds + (size_t)r * ldsK + blk * BLK;
+          const float4 x0 = *reinterpret_cast<const float4*>(xb + lane * 4);
+          x[0] = x0.x;
+          x[1] = x0.y;
+          x[2] = x0.z;
+          x[3] = x0.w;
+          if constexpr (VE == 8) {
+            const float4 x1 = *reinterpret_cast<const float4*>(xb + 256 + lane * 4);
+            x[4] = x1.x;
+            x[5] = x1.y;
+            x[6] = x1.z;
+            x[7] = x1.w;
+          }
+#pragma unroll
+          for (int e = 0; e < VE; e++) a0[r] = fmaf(w0[e], x[e], a0[r]);
+#pragma unroll
+          for (int e = 0; e < VE; e++) a1[r] = fmaf(w1[e], x[e], a1[r]);
+        }
+      }
+    }
+  }
+  if (gi == ng - 1) {
+    float s0[NR], s1[NR];
+#pragma unroll
+    for (int r = 0; r < NR; r++) {
+      s0[r] = r < nr ? wave_sum(a0[r]) : 0.f;
+      s1[r] = r < nr ? wave_sum(a1[r]) : 0.f;
+      a0[r] = 0.f;
+      a1[r] = 0.f;
+    }
+    done(rp, s0, s1);
+  }
+}
+
+template <typename WT, int NR, typename RowFn, typename DoneFn>
+__device__ __forceinline__ void rstream_run(const RowFn& rowptr, const DoneFn& done, int count, int K, int lane,
+                                            const float* lds, int ldsK, int nr, uint4 (&bA)[2][kU],
+                                            uint4 (&bB)[2][kU]) {
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  const int nb = (K + BLK - 1) / BLK;
+  const int ng = (nb + kU - 1) / kU;
+  const int NU = count * ng;
+  float a0[NR], a1[NR];
+#pragma unroll
+  for (int r = 0; r < NR; r++) a0[r] = a1[r] = 0.f;
+  for (int u = 0; u < NU; u += 2) {
+    rgemv_comp<WT, NR>(nb, ng, u, lane, lds, ldsK, nr, bA, a0, a1, done);
+    if (u + 2 < NU) gemv_load<WT>(rowptr, K, ng, u + 2, lane, bA);
+    if (u + 1 < NU) {
+      rgemv_comp<WT, NR>(nb, ng, u + 1, lane, lds, ldsK, nr, bB, a0, a1, done);
+      if (u + 3 < NU) gemv_load<WT>(rowptr, K, ng, u + 3, lane, bB);
+    }
+  }
+}
+
 // Stage src[0, K) into LDS in the xidx layout (COH: device-scope loads, for values written earlier in
 // the same launch; else ordinary loads), zero padded to the block multiple, times gain[k] when a gain
 // is given. Returns the workgroup's sum of squares of src when a

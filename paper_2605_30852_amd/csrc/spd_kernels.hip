@@ -561,6 +561,133 @@ __global__ __launch_bounds__(kWG) void k_sgemv(Ctx C, Rows R) {
   ktrace_end(C, ts);
 }
 
+// ----------------------------------------------------------- row-block streaming GEMVs (PDM)
+// A sublayer of a row block whose rows all use the same layer (the PDM's decoder layer over its a
+// rows, row i at position pos0 + i): the weights are streamed as in the stage launches, but every
+// pair is applied to up to nrp rows staged together in LDS (nrp fits the rows' input vectors in the
+// workgroup's LDS; more rows take further passes over the weights). Epilogues as in sgemv_part, row
+// r's handled by lane r: QKV rotates at the row's position and appends K/V to the layer's cache,
+// O-proj and down add into the row's residual stream, gate/up applies SwiGLU.
+template <typename WT, int KIND, int NR>
+__global__ __launch_bounds__(kWG) void k_rgemv(Ctx C, Rows R, int nrp) {
+  extern __shared__ __align__(16) float lds[];
+  __shared__ float red[4];
+  const Grp gr = resolve(C, R, 0);
+  if (!gr.active) return;
+  const LayerDesc Ld = C.lay[gr.layer];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int NW = gridDim.x * 4, wv = blockIdx.x * 4 + w;
+  const int d = C.d, dh = C.dh, half = C.dh >> 1;
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  const int K = KIND == SG_OPROJ ? C.qdim : (KIND == SG_DOWN ? C.F : d);
+  const int ldsK = (K + BLK - 1) / BLK * BLK;
+  const int npairs = KIND == SG_QKV ? (C.hq + 2 * C.hkv) * half : (KIND == SG_GATEUP ? C.F : (d + 1) / 2);
+  const int count = wv < npairs ? (npairs - 1 - wv) / NW + 1 : 0;  // at most 64 (the host sizes the grid)
+  auto rowptr = [&](int i, int which) -> const WT* {
+    const int q = wv + i * NW;
+    if (KIND == SG_QKV) {
+      const int head = q / half, j = q - head * half;
+      const WT* W = head < C.hq ? (const WT*)Ld.wq : (head < C.hq + C.hkv ? (const WT*)Ld.wk : (const WT*)Ld.wv);
+      const int hrow = head < C.hq ? head : (head < C.hq + C.hkv ? head - C.hq : head - C.hq - C.hkv);
+      return W + (size_t)(hrow * dh + j + which * half) * d;
+    } else if (KIND == SG_GATEUP) {
+      return (which ? (const WT*)Ld.wu : (const WT*)Ld.wg) + (size_t)q * d;
+    } else {
+      const int m = 2 * q + which;
+      const WT* W = (const WT*)(KIND == SG_OPROJ ? Ld.wo : Ld.wd);
+      return m < d ? W + (size_t)m * K : (const WT*)nullptr;
+    }
+  };
+  for (int r0 = 0; r0 < gr.nrows; r0 += nrp) {
+    const int nr = min(nrp, gr.nrows - r0);
+    if (r0 > 0) __syncthreads();  // every wave is done with the previous rows' vectors
+    uint4 bA[2][kU], bB[2][kU];
+    stream_prefetch<WT>(rowptr, count, K, lane, bA, bB);
+    // per-pair epilogue values of every row, lane i holding pair i's
+    float2 pv[NR];
+    int page[NR];
+#pragma unroll
+    for (int r = 0; r < NR; r++) {
+      pv[r] = make_float2(0.f, 0.f);
+      page[r] = 0;
+      if (r < nr) {
+        const int pos = gr.pos0 + r0 + r;
+        const float* xr = gr.x + (size_t)(r0 + r) * gr.xstride;
+        if (KIND == SG_QKV) {
+          if (lane < count) pv[r] = C.rope[(size_t)pos * half + (wv + lane * NW) % half];
+          page[r] = C.page_table[pos / C.page];
+        } else if (KIND == SG_OPROJ || KIND == SG_DOWN) {
+          if (lane < count) {
+            const int m = 2 * (wv + lane * NW);
+            pv[r].x = xr[m];
+            pv[r].y = m + 1 < d ? xr[m + 1] : 0.f;
+          }
+        }
+      }
+    }
+    float sc[NR];
+#pragma unroll
+    for (int r = 0; r < NR; r++) {
+      sc[r] = 1.f;
+      if (r < nr) {
+        if (KIND == SG_QKV || KIND == SG_GATEUP) {
+          const float ss = stage_vec<Elt<WT>::VE, false>(gr.x + (size_t)(r0 + r) * gr.xstride,
+                                                          KIND == SG_QKV ? Ld.attn_norm : Ld.mlp_norm, d,
+                                                          lds + (size_t)r * ldsK, red);
+          sc[r] = 1.0f / sqrtf(ss / (float)d + C.eps);
+        } else {
+          stage_vec<Elt<WT>::VE, false>((KIND == SG_OPROJ ? C.b[R.set].ao : C.b[R.set].act) +
+                                            (size_t)(gr.brow0 + r0 + r) * K,
+                                        nullptr, K, lds + (size_t)r * ldsK, red);
+        }
+      }
+    }
+    auto done = [&](int i, const float (&s0)[NR], const float (&s1)[NR]) {
+      float2 v[NR];
+#pragma unroll
+      for (int r = 0; r < NR; r++) v[r] = make_float2(__shfl(pv[r].x, i, 64), __shfl(pv[r].y, i, 64));
+      const int q = wv + i * NW;
+#pragma unroll
+      for (int r = 0; r < NR; r++) {
+        if (lane != r || r >= nr) continue;
+        const int row = r0 + r, pos = gr.pos0 + row;
+        if (KIND == SG_QKV) {
+          const int head = q / half, j = q - head * half;
+          float lo = s0[r] * sc[r], hi = s1[r] * sc[r];
+          if (head < C.hq + C.hkv) {
+            const float rlo = lo * v[r].x - hi * v[r].y;
+            const float rhi = hi * v[r].x + lo * v[r].y;
+            lo = rlo;
+            hi = rhi;
+          }
+          if (head < C.hq) {
+            float* qo = C.b[R.set].q + (size_t)(gr.brow0 + row) * C.qdim + head * dh;
+            qo[j] = lo;
+            qo[j + half] = hi;
+          } else {
+            const int hk = head < C.hq + C.hkv ? head - C.hq : head - C.hq - C.hkv;
+            WT* kv = (WT*)Ld.kv;
+            const size_t off = (size_t)page[r] * (2 * C.hkv * C.page * dh) +
+                               ((size_t)hk * C.page + (pos % C.page)) * dh + j +
+                               (head < C.hq + C.hkv ? 0 : (size_t)C.hkv * C.page * dh);
+            st1<WT>(kv, off, lo);
+            st1<WT>(kv, off + half, hi);
+          }
+        } else if (KIND == SG_GATEUP) {
+          const float g = s0[r] * sc[r], u = s1[r] * sc[r];
+          C.b[R.set].act[(size_t)(gr.brow0 + row) * C.F + q] = g / (1.0f + expf(-g)) * u;
+        } else {
+          const int m = 2 * q;
+          float* xr = gr.x + (size_t)row * gr.xstride;
+          xr[m] = v[r].x + s0[r];
+          if (m + 1 < d) xr[m + 1] = v[r].y + s1[r];
+        }
+      }
+    };
+    rstream_run<WT, NR>(rowptr, done, count, K, lane, lds, ldsK, nr, bA, bB);
+  }
+}
+
 // ---------------------------------------------------------------------- PDM feature projection
 // g_q = W_in . [H^{beta_0}; ...; H^{beta_f}; 0 ...] for the rows the PDM runs (Eq. agg-main with
 // one projection whose column block j serves anchor j). prefill = 1: rows of the prefill chunk
@@ -976,6 +1103,29 @@ __global__ __launch_bounds__(kWG) void k_attn_stage(Ctx C, Rows R) {
   ktrace_end(C, ts);
 }
 
+// Decode attention of a row block (the PDM's rows: row z at position pos0 + z over the layer's own
+// cache). Grid: x = key split, y = KV head, z = row. The split is attn_split with the row's scratch.
+template <typename KVT, int DH, int GP>
+__global__ __launch_bounds__(kWG) void k_attn_rows(Ctx C, Rows R) {
+  extern __shared__ __align__(16) float lds[];
+  const int split = blockIdx.x, g = blockIdx.y, z = blockIdx.z;
+  const int k0 = split * C.chunk;
+  const int page0 = C.page_table[min((k0 + (int)threadIdx.x / kAttnTPK) / C.page, C.max_pages - 1)];
+  const Grp gr = resolve(C, R, 0);
+  if (!gr.active || z >= gr.nrows) return;
+  const int pos0 = gr.pos0 + z;
+  const int nsplit = (pos0 + C.chunk) / C.chunk;
+  if (split >= nsplit) return;
+  const int k1 = min(pos0 + 1, k0 + C.chunk);
+  const BufSet& B = C.b[R.set];
+  const int cidx = z * C.hkv + g;
+  constexpr int RS = kAttnMaxQ * (DH + 2);
+  const size_t row = (size_t)(gr.brow0 + z) * C.qdim + g * C.G * DH;
+  attn_split_g<KVT, DH, false, GP>(C, (const KVT*)C.lay[gr.layer].kv, B.q + row, B.ao + row,
+                                   B.part + (size_t)cidx * C.max_splits * RS, B.cnt + cidx, g, split, nsplit, k0,
+                                   k1, pos0, page0, lds);
+}
+
 // Launch trace reset.
 __global__ __launch_bounds__(kWG) void k_ktrace_reset(Ctx C, int nslots) {
   for (int i = blockIdx.x * kWG + threadIdx.x; i < nslots; i += gridDim.x * kWG) {
@@ -1369,6 +1519,79 @@ void Launch<WT>::down(const Ctx& c, const Rows& r, void* s) {
   }
   const dim3 grid((c.d + 7) / 8, 1);
   launch_timed((k_proj_add<WT, kMaxRows, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, kMaxRows), S(s), c, r);
+}
+
+// Rows of one row-block pass that fit the workgroup's LDS with input width K (at least 1, at most
+// max_rows and 8).
+struct DevLimits {
+  int lds_max = 0, cus = 0;
+};
+static const DevLimits& dev_limits() {
+  static DevLimits L;
+  if (L.lds_max == 0) {
+    int dev = 0, v = 0, cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      v = 65536;
+      cu = 256;
+    }
+    L.lds_max = v;
+    L.cus = cu;
+  }
+  return L;
+}
+
+template <typename WT>
+static int rows_per_pass(int K, int max_rows) {
+  const size_t row = stream_lds<WT>(K);
+  const int fit = (int)((size_t)(dev_limits().lds_max - 1024) / row);
+  return std::max(1, std::min(std::min(fit, max_rows), kMaxRows));
+}
+
+template <typename WT, int KIND>
+static void rgemv_launch(const Ctx& c, const Rows& r, int npairs, int K, int max_rows, void* s) {
+  const int nrp = rows_per_pass<WT>(K, max_rows);
+  const size_t shm = stream_lds<WT>(K) * nrp;
+  // no more workgroups than the GPU holds at once with this much LDS (a second round would double
+  // the launch), and enough waves that none streams more than 64 pairs
+  const int resident = dev_limits().cus * std::max(1, (int)((size_t)dev_limits().lds_max / (shm + 1024)));
+  int wgs = std::min(stream_grid(c, npairs, 1), resident);
+  if (c.rows_wgs > 0) wgs = std::min(wgs, c.rows_wgs);  // side work: leave most CUs to the stages
+  wgs = std::max(wgs, (npairs + 255) / 256);
+  const dim3 grid(wgs);
+  if (nrp <= 4)
+    launch_timed((k_rgemv<WT, KIND, 4>), grid, dim3(kWG), shm, S(s), c, r, nrp);
+  else
+    launch_timed((k_rgemv<WT, KIND, 8>), grid, dim3(kWG), shm, S(s), c, r, nrp);
+}
+
+template <typename WT>
+void Launch<WT>::rows_layer(const Ctx& c, const Rows& r, int max_rows, void* s) {
+  for (int k = 0; k < 5; k++) rows_sublayer(c, r, max_rows, k, s);
+}
+
+template <typename WT>
+void Launch<WT>::rows_sublayer(const Ctx& c, const Rows& r, int max_rows, int k, void* s) {
+  max_rows = std::max(1, std::min(max_rows, kMaxRows));
+  if (k == 0) rgemv_launch<WT, SG_QKV>(c, r, (c.hq + 2 * c.hkv) * (c.dh / 2), c.d, max_rows, s);
+  if (k == 2) rgemv_launch<WT, SG_OPROJ>(c, r, (c.d + 1) / 2, c.qdim, max_rows, s);
+  if (k == 3) rgemv_launch<WT, SG_GATEUP>(c, r, c.F, c.d, max_rows, s);
+  if (k == 4) rgemv_launch<WT, SG_DOWN>(c, r, (c.d + 1) / 2, c.F, max_rows, s);
+  if (k != 1) return;
+  const dim3 agrid(c.max_splits, c.hkv, max_rows);
+  const bool g4 = c.G <= 4;
+  if (c.dh == 128) {
+    if (g4)
+      launch_timed((k_attn_rows<WT, 128, 4>), agrid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
+    else
+      launch_timed((k_attn_rows<WT, 128, 8>), agrid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
+  } else {
+    if (g4)
+      launch_timed((k_attn_rows<WT, 64, 4>), agrid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
+    else
+      launch_timed((k_attn_rows<WT, 64, 8>), agrid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
+  }
 }
 
 template <typename WT>

@@ -161,6 +161,9 @@ class Engine:
     def spd_set_pdm_placement(self, place: int) -> None:
         B.spd_set_pdm_placement(self.h, place)
 
+    def spd_set_pdm_grid(self, wgs: int) -> None:
+        B.spd_set_pdm_grid(self.h, wgs)
+
     def spd_set_debug(self, on: bool) -> None:
         B.spd_set_debug(self.h, on)
 

@@ -1,0 +1,127 @@
+"""Condense rocprofv3 CSV output (``-f csv``) into the short text summaries kept with the project.
+
+    python -m paper_2605_30852_amd.profsum stats KERNEL_STATS.csv [--top N]
+    python -m paper_2605_30852_amd.profsum trace KERNEL_TRACE.csv --kernel NAME [--grid-y Y]
+    python -m paper_2605_30852_amd.profsum traffic FETCH.csv WRITE.csv --kernel NAME [--grid-y Y]
+        [--algo-bytes B] [--source FILE]
+
+`stats` prints the per-kernel table; `trace` the duration of the dispatches of one kernel (a
+substring of its name, optionally only those whose grid has Y workgroups in y, e.g. the two-stage
+group launches); `traffic` the HBM bytes per dispatch of that kernel from a FETCH_SIZE run and a
+WRITE_SIZE run, each scaled by what the same counter reads for the largest device copy in the run
+(a 1 GiB copy reads and writes 2^30 bytes), as key=value lines. Pure text processing: it reads the
+CSV files only."""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import statistics
+import sys
+
+GIB_KIB = float(1 << 20)
+
+
+def _rows(path):
+    with open(path, newline="") as f:
+        yield from csv.DictReader(f)
+
+
+def _grid_y(r):
+    for k in ("Grid_Size_Y", "Grid_Y"):
+        if k in r and r[k] not in (None, ""):
+            return int(r[k])
+    return None
+
+
+def _match(r, kernel, grid_y):
+    if kernel not in r.get("Kernel_Name", ""):
+        return False
+    return grid_y is None or _grid_y(r) == grid_y
+
+
+def stats(path, top):
+    rows = list(_rows(path))
+    out = ["| kernel | calls | average us | total ms | share |", "|---|---:|---:|---:|---:|"]
+    for r in rows[:top]:
+        out.append(f"| `{r['Name']}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                   f"{float(r['TotalDurationNs']) / 1e6:.2f} | {float(r['Percentage']):.2f}% |")
+    return "\n".join(out)
+
+
+def trace(path, kernel, grid_y):
+    d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in _rows(path) if _match(r, kernel, grid_y)]
+    if not d:
+        return f"no dispatch of {kernel!r} (grid y {grid_y})"
+    return (f"kernel={kernel}\ngrid_y={grid_y}\ndispatches={len(d)}\nmean_us={statistics.mean(d):.2f}\n"
+            f"median_us={statistics.median(d):.2f}\nmin_us={min(d):.2f}\nmax_us={max(d):.2f}")
+
+
+def _counter(path, kernel, grid_y):
+    """Values of the kernel's dispatches (grid y = grid_y when the file records grid dimensions;
+    otherwise the cluster of largest values, within 3/4 of the largest, which separates launches
+    covering more stages), the largest device copy's value, and how the dispatches were selected."""
+    vals, copies, has_y = [], [], False
+    for r in _rows(path):
+        v = float(r["Counter_Value"])
+        has_y = has_y or _grid_y(r) is not None
+        if _match(r, kernel, grid_y if _grid_y(r) is not None else None):
+            vals.append(v)
+        if "copyBuffer" in r.get("Kernel_Name", ""):
+            copies.append(v)
+    how = f"grid y = {grid_y}" if (has_y or grid_y is None) else "largest-value cluster (>= 3/4 of the largest)"
+    if grid_y is not None and not has_y and vals:
+        top = max(vals)
+        vals = [v for v in vals if v >= 0.75 * top]
+    return vals, (max(copies) if copies else None), how
+
+
+def traffic(fetch, write, kernel, grid_y, algo, source):
+    fv, fc, how = _counter(fetch, kernel, grid_y)
+    wv, wc, _ = _counter(write, kernel, grid_y)
+    if not fv or not wv or not fc or not wc:
+        return "incomplete: " + repr((len(fv), len(wv), fc, wc))
+    sf, sw = GIB_KIB / fc, GIB_KIB / wc
+    fk, wk = statistics.median(fv), statistics.median(wv)
+    hbm = (fk * sf + wk * sw) * 1024.0
+    lines = [f"kernel={kernel}", f"selection={how}", f"dispatches_fetch={len(fv)}", f"dispatches_write={len(wv)}",
+             f"fetch_kib_median={fk:.1f}", f"write_kib_median={wk:.1f}",
+             f"copy_fetch_kib={fc:.1f}", f"copy_write_kib={wc:.1f}",
+             f"scale_fetch={sf:.4f}", f"scale_write={sw:.4f}", f"hbm_bytes_per_launch={hbm:.0f}"]
+    if algo:
+        lines.append(f"algorithmic_bytes_per_launch={algo:.0f}")
+        lines.append(f"traffic_over_algorithmic={hbm / algo:.4f}")
+    if source:
+        lines.append("kernels_sha256=" + hashlib.sha256(open(source, "rb").read()).hexdigest()[:16])
+    return "\n".join(lines)
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    a = sub.add_parser("stats")
+    a.add_argument("csv")
+    a.add_argument("--top", type=int, default=24)
+    b = sub.add_parser("trace")
+    b.add_argument("csv")
+    b.add_argument("--kernel", required=True)
+    b.add_argument("--grid-y", type=int, default=None)
+    c = sub.add_parser("traffic")
+    c.add_argument("fetch")
+    c.add_argument("write")
+    c.add_argument("--kernel", required=True)
+    c.add_argument("--grid-y", type=int, default=None)
+    c.add_argument("--algo-bytes", type=float, default=None)
+    c.add_argument("--source", default=None)
+    args = ap.parse_args(argv)
+    if args.cmd == "stats":
+        print(stats(args.csv, args.top))
+    elif args.cmd == "trace":
+        print(trace(args.csv, args.kernel, args.grid_y))
+    else:
+        print(traffic(args.fetch, args.write, args.kernel, args.grid_y, args.algo_bytes, args.source))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -235,6 +235,7 @@ def test_graph_replay_matches_eager(mid_w):
     ("mid", 3, 2, 0, -1, 0), ("tiny", 4, 2, 0, -1, 0), ("mid", 1, 2, 0, -1, 0), ("mid", 3, 2, 0, 3, 0),
     ("tiny", 4, 2, 0, 4, 0), ("tiny", 4, 2, 0, 3, 0), ("mid", 3, 2, 0, 1, 0),
     ("tiny", 4, 2, 0, 2, 1), ("mid", 3, 2, 0, 2, 2), ("tiny", 4, 2, 0, 4, 3), ("mid", 3, 0, 0, -1, 1),
+    ("tiny", 4, 2, 0, 4, 4), ("mid", 3, 2, 0, 3, 4), ("mid", 3, 2, 0, 1, 4), ("tiny", 2, 2, 0, 2, 4),
     ("mid", 3, 3, 0, -1, 0), ("mid", 3, 3, 7, -1, 0), ("tiny", 4, 3, 0, -1, 0), ("tiny", 3, 3, 0, -1, 0),
     ("mid", 1, 3, 0, -1, 0),
     ("mid", 3, 4, 0, -1, 0), ("mid", 3, 4, 24, -1, 0), ("tiny", 4, 4, 0, -1, 0), ("tiny", 3, 4, 16, -1, 0),
@@ -246,8 +247,8 @@ def test_step_modes_bit_identical_to_sublayer_launches(tiny_w, mid_w, which, n, 
     workgroups inside the launch; small grids make few workgroups walk the whole tile order, grid 1
     strictly in ticket order, with the stages in lockstep or staggered); mode 2 runs groups of stages
     on their own streams (skew = the number of groups; -1: the default) with the draft module on its
-    own stream, on main_stream before the stages, or on the first group's stream before or after its
-    stages (place 0-3); mode 3 is the skewed schedule of mixed launches (grid 7: few workgroups per
+    own stream, on main_stream before the stages, on the first group's stream before or after its
+    stages, or spread over the groups' streams (place 0-4); mode 3 is the skewed schedule of mixed launches (grid 7: few workgroups per
     weight-streaming part); mode 4 is the persistent launch with one group of workgroups per stage
     (small grids: few workgroups per group, so each walks many rows)."""
     _say(f"[step mode {mode} vs sublayer launches {which} n={n} grid={grid} skew={skew} pdm place={place}]")
@@ -286,6 +287,23 @@ def test_step_modes_bit_identical_to_sublayer_launches(tiny_w, mid_w, which, n, 
     assert np.array_equal(engs[0].tokens(), engs[1].tokens())
     for e in engs:
         e.close()
+
+
+def test_spread_pdm_placement_refused_in_graph_mode(tiny_w):
+    """The spread PDM placement (4) is for issued launches only: the library refuses it while graph
+    mode is on, and refuses graph mode while it is set; other placements capture as before."""
+    from paper_2605_30852_amd import binding as B
+    e = _engine(tiny_w, 2)
+    e.spd_set_graph(True)
+    with pytest.raises(B.SPDError):
+        e.spd_set_pdm_placement(4)
+    e.spd_set_graph(False)
+    e.spd_set_pdm_placement(4)
+    with pytest.raises(B.SPDError):
+        e.spd_set_graph(True)
+    e.spd_set_pdm_placement(3)
+    e.spd_set_graph(True)
+    e.close()
 
 
 @pytest.mark.parametrize("chunk", [256, 384])
