@@ -281,11 +281,13 @@ spd_status spd_step_plan_info(spd_handle* h, int32_t* info);
 /* 1: every LM-head pass also writes its full logits (for SPD_DBG_*_LOGITS). */
 spd_status spd_set_debug(spd_handle* h, int32_t on);
 
-/* Kernel timing for roofline measurements. kernel selects one launch class of the stage compute on
- * main_stream (SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN in step-kernel mode 0;
- * SPD_K_STEP, the persistent launch, in mode 1; SPD_K_HEAD; 0 turns timing off). While on, steps issue their launches (no graph replay) and every launch of that class in layer
- * slot >= first_slot (the exit head counts as the slot after the last) hands two HIP events to its own
- * dispatch, which records the kernel's start and end on main_stream. A first_slot past the draft
+/* Kernel timing for roofline measurements. kernel selects one launch class of the stage compute
+ * (SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN in modes 0 and 2; SPD_K_STEP, the
+ * persistent launch, in modes 1 and 4; SPD_K_MIX in mode 3; SPD_K_HEAD, the LM-head pass, which
+ * with the fused two-row head also runs the step's verify; 0 turns timing off). While on, steps
+ * issue their launches (no graph replay) and every launch of that class in layer slot >= first_slot
+ * (the exit head counts as the slot after the last) hands two HIP events to its own dispatch, which
+ * records the kernel's start and end on the stream it is launched on. A first_slot past the draft
  * module's span times the kernel without the side stream competing for memory bandwidth.
  * spd_kernel_timing waits for the stream, returns the summed kernel time in milliseconds and the
  * number of timed launches, and clears both. */

@@ -486,7 +486,8 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     if (sp) HIPC(hipEventRecord(sp[2], h->main));
     HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
     TimedLaunch t(h, h->main, SPD_K_HEAD);
-    Launch<WT>::head(C, 3, 0, h->main);
+    Launch<WT>::head_verify(C, forced_override, h->cfg.auto_rollback, h->main);  // + the step's verify
+    return launch_check(h, "step");
   } else {
     {
       TimedLaunch t(h, h->main, SPD_K_HEAD);

@@ -13,7 +13,6 @@ constexpr int kMaxPdmLayers = 4;
 constexpr int kWG = 256;        // threads per workgroup in every kernel
 constexpr int kLogCap = 4096;   // step log ring
 constexpr int kMaxSplits = 64;  // attention key splits per (row, KV head)
-constexpr int kHeadRows = 32;   // LM-head vocabulary rows per workgroup (one argmax partial each)
 
 // One decoder layer as the kernels see it. KV pool of the layer: [pages][2][Hkv][page][dh].
 struct LayerDesc {
@@ -41,7 +40,8 @@ struct DevState {
   int32_t pdm_draft;   // PDM argmax of this step
   int32_t err;         // sticky: a dependency wait of the step kernel timed out
   spd_step_result res; // last step
-  int32_t pad1[6];
+  int32_t head_ticket; // workgroups of the fused LM head + verify launch that are done (zero at rest)
+  int32_t pad1[5];
 };
 
 // Scratch of one compute stream. The target path and the PDM each own one, so the two streams
@@ -193,6 +193,9 @@ struct Launch {
   // 2 = prefill row `row` of pf_x, 3 = exit row and PDM row in one pass. The kernel that follows
   // (verify / reseed) reduces the partials.
   static void head(const Ctx& c, int src, int row, void* stream);
+  // The two-row head (src 3) and the verify of the step in one launch: the workgroup that finishes
+  // the head last runs the verify.
+  static void head_verify(const Ctx& c, int forced_override, int auto_rb, void* stream);
   static void embed_rows(const Ctx& c, int t0, int nrows, void* stream);
   // one launch of the skewed schedule, nwg workgroups
   static void mix(const Ctx& c, const MixLaunch& m, int nwg, void* stream);

@@ -745,73 +745,66 @@ __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_ar
 }
 
 // ---------------------------------------------------------------------------- LM head + argmax
-// Tile = kHeadRows vocabulary rows, kHeadRows/4 per wave in pairs. Each workgroup writes its best
-// (value, index), the lowest index winning ties; the single-workgroup kernel that follows on the
-// stream reduces the partials. The (value desc, index asc) order is total, so the winner does not
-// depend on the reduction order.
+// Each workgroup folds its best (value, index), the lowest index winning ties, into a 64-bit key
+// with a device-scope maximum; the single-workgroup kernel that follows on the stream reads it. The
+// (value desc, index asc) order is total, so the winner does not depend on the order of arrival.
 
 // Rows of one LM-head pass. src 0: the exit row (skipped unless a == n); 1: the PDM's last row;
 // 2: prefill row `row`; 3: the exit row and the PDM's last row together (rows 0 and 1), one pass over
-// W_lm serving both heads. Row results go to the partials of set 0 (target) or set 1 (PDM).
+// W_lm serving both heads. The vocabulary is streamed like a stage GEMV (each workgroup stages the
+// normalised rows once, its waves stream vocabulary row pairs back to back); each row's argmax goes
+// to the argmax key of set 0 (target) or set 1 (PDM) as an order-independent maximum.
 template <typename WT, int NV>
 __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
   extern __shared__ __align__(16) float lds[];
+  __shared__ float red[4];
   __shared__ float s_v[NV][4];
   __shared__ int s_i[NV][4];
-  __shared__ float red[4];
-  constexpr int RPW = kHeadRows / 4;  // rows per wave
   const int a = C.st->a, c = C.st->c;
-  XSpec xs;
-  xs.src = XS_NORM_RESID;
+  const float* xr[NV];
+  const float* gn[NV];
   int set[NV];
   if (src == 0) {
     if (a != C.n) return;  // nothing exits while the pipeline fills
-    xs.row[0] = C.resid + (size_t)(c % C.n) * C.d;
-    xs.gain[0] = C.final_norm;
+    xr[0] = C.resid + (size_t)(c % C.n) * C.d;
+    gn[0] = C.final_norm;
     set[0] = 0;
   } else if (src == 1) {
-    xs.row[0] = C.pdm_x + (size_t)(a - 1) * C.d;
-    xs.gain[0] = C.pdm_norm;
+    xr[0] = C.pdm_x + (size_t)(a - 1) * C.d;
+    gn[0] = C.pdm_norm;
     set[0] = 1;
   } else if (src == 2) {
-    xs.row[0] = C.pf_x + (size_t)row * C.d;
-    xs.gain[0] = C.final_norm;
+    xr[0] = C.pf_x + (size_t)row * C.d;
+    gn[0] = C.final_norm;
     set[0] = 0;
   } else {
-    // while the pipeline fills the exit row is computed but unused (its partials are not read)
-    xs.row[0] = C.resid + (size_t)(c % C.n) * C.d;
-    xs.gain[0] = C.final_norm;
+    // while the pipeline fills the exit row is computed but unused (its argmax is not read)
+    xr[0] = C.resid + (size_t)(c % C.n) * C.d;
+    gn[0] = C.final_norm;
     set[0] = 0;
-    xs.row[NV - 1] = C.pdm_x + (size_t)(a - 1) * C.d;
-    xs.gain[NV - 1] = C.pdm_norm;
+    xr[NV - 1] = C.pdm_x + (size_t)(a - 1) * C.d;
+    gn[NV - 1] = C.pdm_norm;
     set[NV - 1] = 1;
   }
-  constexpr int VE = Elt<WT>::VE;
-  constexpr int BLK = 64 * VE;
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  const int d = C.d, V = C.V;
+  const int ldsK = (d + BLK - 1) / BLK * BLK;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int NW = gridDim.x * 4, wv = blockIdx.x * 4 + w;
+  const int npairs = (V + 1) / 2;
+  const int count = wv < npairs ? (npairs - 1 - wv) / NW + 1 : 0;
   const WT* W = (const WT*)C.lm_head;
-  const int mw = blockIdx.x * kHeadRows + w * RPW;  // first row of this wave
-  const int kl_pad = (C.d + BLK - 1) / BLK * BLK;  // d fits one chunk (d <= 8192)
-  const int nbk = kl_pad / BLK;
-  auto rows_of = [&](int m0, const WT* (&wr)[2]) {
-#pragma unroll
-    for (int r = 0; r < 2; r++) wr[r] = (m0 + r < C.V) ? W + (size_t)(m0 + r) * C.d : nullptr;
+  auto rowptr = [&](int i, int which) -> const WT* {
+    const int m = 2 * (wv + i * NW) + which;
+    return m < V ? W + (size_t)m * d : (const WT*)nullptr;
   };
-  uint4 wv[2][kU];
-  {
-    const WT* wr[2];
-    rows_of(mw, wr);
-    load_blocks<WT, 2>(wr, C.d, 0, nbk, lane, wv);  // weights first, then the activations
-  }
-  float ss[NV];
-#pragma unroll
-  for (int v = 0; v < NV; v++) ss[v] = 0.f;
-  stage_chunk<VE, NV>(xs, NV, 0, C.d, kl_pad, lds, kl_pad, ss);
+  uint4 bA[2][kU], bB[2][kU];
+  stream_prefetch<WT>(rowptr, count, d, lane, bA, bB);  // weights first, then the rows
   float scl[NV];
 #pragma unroll
   for (int v = 0; v < NV; v++) {
-    const float tot = block_sum(ss[v], red);  // includes the barrier that publishes the staged rows
-    scl[v] = 1.0f / sqrtf(tot / (float)C.d + C.eps);
+    const float ss = stage_vec<Elt<WT>::VE, false>(xr[v], gn[v], d, lds + (size_t)v * ldsK, red);
+    scl[v] = 1.0f / sqrtf(ss / (float)d + C.eps);
   }
   float bv[NV];
   int bi[NV];
@@ -821,30 +814,25 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
     bi[v] = 0x7fffffff;
   }
   const bool dbg_row0 = C.debug && (src != 0 && src != 3 ? true : a == C.n);
-  for (int rg = 0; rg < RPW / 2; rg++) {
-    const int m0 = mw + rg * 2;
-    const WT* wr[2];
-    rows_of(m0, wr);
-    if (rg > 0) load_blocks<WT, 2>(wr, C.d, 0, nbk, lane, wv);
-    float acc[NV][2];
-#pragma unroll
-    for (int v = 0; v < NV; v++) acc[v][0] = acc[v][1] = 0.f;
-    accum_blocks<WT, NV, 2>(wr, C.d, 0, nbk, lds, kl_pad, NV, acc, wv, lane);
+  // every lane holds the same sums, so every lane keeps the same running maximum
+  auto done = [&](int i, const float (&s0)[NV], const float (&s1)[NV]) {
+    const int m = 2 * (wv + i * NW);
 #pragma unroll
     for (int v = 0; v < NV; v++) {
-#pragma unroll
-      for (int r = 0; r < 2; r++) acc[v][r] = wave_sum(acc[v][r]) * scl[v];
-      if (C.debug && (v > 0 || dbg_row0) && lane < 2 && m0 + lane < C.V)
-        C.dbg_logits[(size_t)set[v] * C.V + m0 + lane] = lane == 0 ? acc[v][0] : acc[v][1];
-#pragma unroll
-      for (int r = 0; r < 2; r++) {
-        if (m0 + r < C.V && better(acc[v][r], m0 + r, bv[v], bi[v])) {
-          bv[v] = acc[v][r];
-          bi[v] = m0 + r;
-        }
+      const float l0 = s0[v] * scl[v], l1 = s1[v] * scl[v];
+      if (C.debug && (v > 0 || dbg_row0) && lane < 2 && m + lane < V)
+        C.dbg_logits[(size_t)set[v] * V + m + lane] = lane == 0 ? l0 : l1;
+      if (m < V && better(l0, m, bv[v], bi[v])) {
+        bv[v] = l0;
+        bi[v] = m;
+      }
+      if (m + 1 < V && better(l1, m + 1, bv[v], bi[v])) {
+        bv[v] = l1;
+        bi[v] = m + 1;
       }
     }
-  }
+  };
+  rstream_run<WT, NV>(rowptr, done, count, d, lane, lds, ldsK, NV, bA, bB);
   if (lane == 0) {
 #pragma unroll
     for (int v = 0; v < NV; v++) {
@@ -862,8 +850,9 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
         fv = s_v[v][k];
         fi = s_i[v][k];
       }
-    // the maximum is order-independent, so the result does not depend on which tile lands last
-    __hip_atomic_fetch_max(C.b[set[v]].hkey, argmax_key(fv, fi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // the maximum is order-independent, so the result does not depend on which workgroup lands last
+    if (fi != 0x7fffffff)
+      __hip_atomic_fetch_max(C.b[set[v]].hkey, argmax_key(fv, fi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -878,6 +867,10 @@ __global__ __launch_bounds__(kWG) void k_head(Ctx C, int src, int row) {
 // workgroup that follows the head on the stream.
 __device__ __forceinline__ int take_head(const BufSet& B, int V) {
   return argmax_index(*B.hkey, V);
+}
+// The same, when the key was folded in by other workgroups of the same launch (device-scope load).
+__device__ __forceinline__ int take_head_dev(const BufSet& B, int V) {
+  return argmax_index(__hip_atomic_load(B.hkey, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), V);
 }
 
 // ------------------------------------------------------------------------------- attention
@@ -1340,12 +1333,13 @@ __device__ __forceinline__ void reset_step_sync(const Ctx& C) {
 
 // Greedy streaming verification (Section 3.4) and the pipeline state update; single workgroup,
 // last kernel of a step.
-template <typename WT>
+// COH: the argmax keys were written by other workgroups of the same launch.
+template <typename WT, bool COH = false>
 __device__ __forceinline__ void verify_body(const Ctx& C, int forced_override, int auto_rb) {
   __shared__ int s_tok, s_pos;
   DevState* st = C.st;
-  const int y_all = (st->a == C.n) ? take_head(C.b[0], C.V) : -1;
-  const int pd_all = take_head(C.b[1], C.V);
+  const int y_all = (st->a == C.n) ? (COH ? take_head_dev(C.b[0], C.V) : take_head(C.b[0], C.V)) : -1;
+  const int pd_all = COH ? take_head_dev(C.b[1], C.V) : take_head(C.b[1], C.V);
   const int step_err = C.plan.sync != nullptr ? C.plan.sync[sync_err()] : 0;
   __syncthreads();  // every thread has read the argmax keys and the timeout flag
   reset_step_sync(C);
@@ -1419,6 +1413,33 @@ template <typename WT>
 __global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int auto_rb) {
   ktrace_start(C, ktrace_extra(C, KT_VERIFY), blockIdx.x == 0 && blockIdx.y == 0);
   verify_body<WT>(C, forced_override, auto_rb);
+  ktrace_end(C, ktrace_extra(C, KT_VERIFY));
+}
+
+// The fused exit + draft head and verify: every workgroup streams its share of the vocabulary and
+// folds its argmax into the keys; once its own key updates have completed it takes a ticket, and the
+// workgroup with the last ticket (every other one has finished) runs the verify and resets the
+// ticket. Saves the launch of the single-workgroup verify after the head.
+template <typename WT>
+__global__ __launch_bounds__(kWG) void k_head_verify(Ctx C, int forced_override, int auto_rb) {
+  __shared__ int s_last;
+  ktrace_start(C, ktrace_extra(C, KT_HEAD), blockIdx.x == 0);
+  head_body<WT, 2>(C, 3, 0);
+  // the argmax updates are device-scope atomics: once this thread has seen its own complete, the
+  // ticket (relaxed, no cache-wide fence) can follow; the last workgroup reads the keys with
+  // device-scope loads
+  wait_own_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int t = __hip_atomic_fetch_add(&C.st->head_ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (t == (int)gridDim.x - 1);
+  }
+  __syncthreads();
+  ktrace_end(C, ktrace_extra(C, KT_HEAD));
+  if (!s_last) return;
+  ktrace_start(C, ktrace_extra(C, KT_VERIFY), true);
+  verify_body<WT, true>(C, forced_override, auto_rb);
+  if (threadIdx.x == 0) __hip_atomic_store(&C.st->head_ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   ktrace_end(C, ktrace_extra(C, KT_VERIFY));
 }
 
@@ -1680,15 +1701,40 @@ void Launch<WT>::pdm_fc(const Ctx& c, int prefill, int nrows, void* s) {
   launch_timed((k_pdm_fc<WT>), grid, dim3(kWG), gemv_lds<WT>(c.n * c.d, kMaxRows), S(s), c, prefill, nrows);
 }
 
+// Workgroups of `fn` (with `lds` bytes of dynamic LDS) that the GPU holds at once.
+static int resident_wgs(const void* fn, size_t lds) {
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kWG, lds) != hipSuccess || per_cu < 1) per_cu = 1;
+  return per_cu * dev_limits().cus;
+}
+
 template <typename WT>
 void Launch<WT>::head(const Ctx& c, int src, int row, void* s) {
-  const dim3 grid((c.V + kHeadRows - 1) / kHeadRows);
+  // a wave streams its vocabulary pairs back to back; no more workgroups than the GPU holds at once,
+  // since the head runs alone and a second round of workgroups would only add a tail
   constexpr int BLK = 64 * Elt<WT>::VE;
   const size_t kl_pad = (size_t)(c.d + BLK - 1) / BLK * BLK;
-  if (src == 3)
-    launch_timed((k_head<WT, 2>), grid, dim3(kWG), 2 * kl_pad * sizeof(float), S(s), c, src, row);
-  else
-    launch_timed((k_head<WT, 1>), grid, dim3(kWG), kl_pad * sizeof(float), S(s), c, src, row);
+  const int np = (c.V + 1) / 2;
+  if (src == 3) {
+    const size_t shm = 2 * kl_pad * sizeof(float);
+    const int res = resident_wgs((const void*)k_head<WT, 2>, shm);
+    const dim3 grid(std::max(std::min(stream_grid(c, np, 1), res), 1));
+    launch_timed((k_head<WT, 2>), grid, dim3(kWG), shm, S(s), c, src, row);
+  } else {
+    const size_t shm = kl_pad * sizeof(float);
+    const int res = resident_wgs((const void*)k_head<WT, 1>, shm);
+    const dim3 grid(std::max(std::min(stream_grid(c, np, 1), res), 1));
+    launch_timed((k_head<WT, 1>), grid, dim3(kWG), shm, S(s), c, src, row);
+  }
+}
+
+template <typename WT>
+void Launch<WT>::head_verify(const Ctx& c, int forced_override, int auto_rb, void* s) {
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  const size_t shm = 2 * (size_t)(c.d + BLK - 1) / BLK * BLK * sizeof(float);
+  const int res = resident_wgs((const void*)k_head_verify<WT>, shm);
+  const dim3 grid(std::max(std::min(stream_grid(c, (c.V + 1) / 2, 1), res), 1));
+  launch_timed((k_head_verify<WT>), grid, dim3(kWG), shm, S(s), c, forced_override, auto_rb);
 }
 
 template <typename WT>
