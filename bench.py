@@ -195,7 +195,7 @@ def main():
     esz = 2 if sh.dtype == "bf16" else 4
     K_GU, K_CLS, K_SPAN = 64, 16, 64
     # greedy reference long enough for every forced-accept phase below
-    n_ref = W + K + K_GU + 5 * K_CLS + K_SPAN + 2 * n + 16
+    n_ref = W + K + K_GU + 5 * K_CLS + 3 * K_SPAN + 2 * n + 16
     # capacity and attention split size depend on the workload only (not on --steps), so that a
     # profiled run with fewer steps launches exactly the kernels the timed run launches
     max_tokens = P + max(1024, n_ref + 4 * n + 64)
@@ -323,6 +323,30 @@ def main():
     spans = {"stage_us": round(1e3 * st_ms / ns, 1), "pdm_us": round(1e3 * pd_ms / ns, 1),
              "verify_wait_us": round(1e3 * late_ms / ns, 2), "steps": ns,
              "pdm_hidden": late_ms == 0.0}
+    # hidden fraction 1 - (T_with - T_without) / T_pdm: the step without the PDM's launches (drafts
+    # are forced anyway), and the PDM alone (its launches on the main stream before the stages,
+    # timed from the step start to their end)
+    if True:
+        B.spd_set_pdm_enabled(eng.h, False)
+        eng.spd_run_steps(4)
+        eng.spd_sync()
+        torch.cuda.synchronize()
+        ts = time.perf_counter()
+        eng.spd_run_steps(K_SPAN)
+        eng.spd_sync()
+        t_without = 1e6 * (time.perf_counter() - ts) / K_SPAN
+        B.spd_set_pdm_enabled(eng.h, True)
+        B.spd_set_pdm_placement(eng.h, 1)
+        B.spd_set_kernel_timing(eng.h, B.SPD_K_SPANS)
+        eng.spd_run_steps(K_SPAN // 2)
+        _, pd_alone_ms, _, na = B.spd_span_timing(eng.h)
+        B.spd_set_kernel_timing(eng.h, 0)
+        B.spd_set_pdm_placement(eng.h, args.pdm_place)
+        t_pdm = 1e3 * pd_alone_ms / na
+        spans.update({"step_us_without_pdm": round(t_without, 1), "pdm_alone_us": round(t_pdm, 1),
+                      "hidden_fraction": round(1.0 - (us_step - t_without) / t_pdm, 3)})
+        ca, aa, _, _ = eng.state()
+        assert aa == n, "PDM hiding measurement left the steady state"
     log(f"[bench] spans: {spans}")
 
     # tokens/s at a seeded Bernoulli acceptance pattern (rollback and refill exercised)
@@ -349,6 +373,19 @@ def main():
             assert r["decision"] == (B.SPD_ACCEPT if mask[r["verified_pos"]] else B.SPD_REJECT)
     log(f"[bench] p={p}: alpha={alpha:.3f}, {spd_tok_s:.0f} tok/s (AR {ar_tok_s:.0f} tok/s)")
     eng.close()
+
+    # achievable HBM read bandwidth for context: a plain 16-byte non-temporal streaming read of 1 GiB
+    # (past the 256 MB last-level cache), through the library's probe kernel
+    pbuf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    psink = torch.empty(4096, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    pms = B.spd_probe_hbm_read(pbuf.data_ptr(), pbuf.numel(), psink.data_ptr(), 10,
+                               torch.cuda.current_stream().cuda_stream)
+    probe = {"GBps": round(pbuf.numel() / (pms * 1e-3) / 1e9, 1), "bytes": pbuf.numel(),
+             "frac": round(pbuf.numel() / (pms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+             "kernel": "k_read_probe: 2048 workgroups, 16-byte non-temporal loads, 8 in flight per thread"}
+    del pbuf, psink
+    log(f"[bench] HBM read probe: {probe['GBps']} GB/s")
     del weights
     torch.cuda.empty_cache()
 
@@ -408,6 +445,7 @@ def main():
                                f"{L_slots}, {K_GU} steady-state steps"},
         "kernels": kernels,
         "pdm_overlap": spans,
+        "hbm_read_probe": probe,
         "tokens_per_s": {"spd_forced_p": p, "alpha": round(alpha, 4), "spd": round(spd_tok_s, 1),
                          "ar_same_gpu": round(ar_tok_s, 1)},
         "cpu_baseline": cpu,

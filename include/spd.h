@@ -249,6 +249,17 @@ spd_status spd_set_graph(spd_handle* h, int32_t on);
  * classes time modes 0 and 2. */
 spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t skew);
 
+/* 0: steps skip the Pipeline Draft Module's launches (feature projection and decoder layers; the
+ * two-row LM head still runs), for measuring how much of the PDM the stage compute hides; drafts
+ * should then come from spd_set_forced_drafts. 1 (default): the PDM runs. */
+spd_status spd_set_pdm_enabled(spd_handle* h, int32_t on);
+
+/* Achievable-bandwidth probe (no handle): reads `bytes` (16-byte aligned, at least 16) of device
+ * memory at buf with 16-byte non-temporal loads from 2048 workgroups, `reps` times on `stream`
+ * after one warm-up pass, and returns the mean time of one pass in *ms. sink: device memory for 2048
+ * floats (written). */
+spd_status spd_probe_hbm_read(const void* buf, size_t bytes, float* sink, int32_t reps, void* stream, double* ms);
+
 /* Where the Pipeline Draft Module's launches go within a step (it reads only pre-step features, so
  * any placement gives the same results): 0 (default): its own stream, forked from main_stream;
  * 1: main_stream, before the stage compute; 2 and 3 (mode 2 only; otherwise 0): the first stage

@@ -61,7 +61,7 @@ EXPORTS = [
     "spd_read_kv", "spd_set_debug", "spd_destroy", "spd_status_str", "spd_last_error",
     "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing", "spd_set_step_kernel",
     "spd_set_step_trace", "spd_step_plan_info", "spd_set_kernel_trace", "spd_set_pdm_placement",
-    "spd_set_pdm_grid",
+    "spd_set_pdm_grid", "spd_set_pdm_enabled", "spd_probe_hbm_read",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -104,6 +104,8 @@ def lib() -> ct.CDLL:
             "spd_set_kernel_trace": (I, [P, I]),
             "spd_set_pdm_placement": (I, [P, I]),
             "spd_set_pdm_grid": (I, [P, I]),
+            "spd_set_pdm_enabled": (I, [P, I]),
+            "spd_probe_hbm_read": (I, [P, ct.c_size_t, P, I, P, ct.POINTER(ct.c_double)]),
             "spd_step_plan_info": (I, [P, ct.POINTER(ct.c_int32)]),
             "spd_kernel_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
             "spd_span_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_double),
@@ -256,6 +258,17 @@ def spd_step_plan_info(h: int) -> dict:
 
 def spd_set_pdm_placement(h: int, place: int) -> None:
     _check("spd_set_pdm_placement", lib().spd_set_pdm_placement(h, place), h)
+
+
+def spd_set_pdm_enabled(h: int, on: bool) -> None:
+    _check("spd_set_pdm_enabled", lib().spd_set_pdm_enabled(h, 1 if on else 0), h)
+
+
+def spd_probe_hbm_read(buf: int, nbytes: int, sink: int, reps: int, stream: int) -> float:
+    """Mean milliseconds of one streaming read of nbytes at device address buf."""
+    ms = ct.c_double(0.0)
+    _check("spd_probe_hbm_read", lib().spd_probe_hbm_read(buf, nbytes, sink, reps, stream, ct.byref(ms)), 0)
+    return ms.value
 
 
 def spd_set_pdm_grid(h: int, wgs: int) -> None:

@@ -190,6 +190,7 @@ struct spd_handle {
   int step_skew = kStepSkewDefault;
   int stage_groups = 0;  // mode 2: streams the stages are spread over (0: kStageGroupsDefault)
   int pdm_place = 0;     // where the PDM's launches go (spd_set_pdm_placement)
+  int pdm_on = 1;        // 0: the step skips the PDM's launches (spd_set_pdm_enabled)
   int pstep_grid = 0;  // mode 4: workgroups, at most what the GPU holds at once
   hipGraphExec_t gexec = nullptr;
   // kernel timing
@@ -302,7 +303,7 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     } else if (i <= 5 * h->cfg.pdm_layers) {
       const int l = (i - 1) / 5, k = (i - 1) % 5;
       Launch<WT>::rows_sublayer(C, rows_block(h->cfg.n_layers + l, -1, -1, C.pdm_x, nullptr, -1, 1),
-                                h->cfg.n_stages, k, s);
+                                h->cfg.n_stages, k, C.rows_wgs, s);
     } else {
       Launch<WT>::head(C, 1, 0, s);
     }
@@ -318,7 +319,11 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     return pdm_end(s);
   };
   const bool stage_streams = h->step_mode == 2;
-  const int place = stage_streams ? h->pdm_place : (h->pdm_place == 1 ? 1 : 0);
+  const int place = !h->pdm_on ? -1 : stage_streams ? h->pdm_place : (h->pdm_place == 1 ? 1 : 0);
+  if (place == -1) {  // no PDM launches: the join is satisfied at the fork
+    if (sp) HIPC(hipEventRecord(sp[1], h->main));
+    HIPC(hipEventRecord(h->ev_join, h->main));
+  }
   if (place == 1) {  // on main_stream, before the stage compute
     spd_status st = enqueue_pdm(h->main);
     if (st != SPD_OK) return st;
@@ -511,12 +516,12 @@ static spd_status enqueue_prefill(spd_handle* h, int len) {
       int cap = -1;
       for (int s = 0; s + 1 <= n - 1; s++)
         if (l + 1 == C.beta[s + 1]) cap = s + 1;
-      enqueue_layer<WT>(C, rows_block(l, rc, t0, C.pf_x, C.pf_anch, cap, 0), h->main);
+      Launch<WT>::rows_layer(C, rows_block(l, rc, t0, C.pf_x, C.pf_anch, cap, 0), kMaxRows, 0, h->main);
     }
     // PDM KV over the prompt: every prompt row has full depth
     Launch<WT>::pdm_fc(C, 1, rc, h->main);
     for (int i = 0; i < h->cfg.pdm_layers; i++)
-      enqueue_layer<WT>(C, rows_block(L + i, rc, t0, C.pdm_x, nullptr, -1, 1), h->main);
+      Launch<WT>::rows_layer(C, rows_block(L + i, rc, t0, C.pdm_x, nullptr, -1, 1), kMaxRows, 0, h->main);
     if (t0 + rc == len) Launch<WT>::head(C, 2, rc - 1, h->main);
     spd_status st = launch_check(h, "prefill");
     if (st != SPD_OK) return st;
@@ -812,6 +817,32 @@ spd_status spd_set_step_trace(spd_handle* h, int32_t on) {
   if (on) HIPC(hipMemset(h->ws + h->lay.trace, 0, sizeof(unsigned long long) * (size_t)h->lay.ntrace));
   HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
   drop_graph(h);
+  return SPD_OK;
+}
+
+spd_status spd_set_pdm_enabled(spd_handle* h, int32_t on) {
+  if (!h) return SPD_E_INVAL;
+  h->pdm_on = on ? 1 : 0;
+  drop_graph(h);  // the captured launches change
+  return SPD_OK;
+}
+
+spd_status spd_probe_hbm_read(const void* buf, size_t bytes, float* sink, int32_t reps, void* stream, double* ms) {
+  if (!buf || !sink || !ms || bytes < 16 || reps < 1 || ((uintptr_t)buf & 15)) return SPD_E_INVAL;
+  hipStream_t s = (hipStream_t)stream;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return SPD_E_HIP;
+  launch_read_probe(buf, bytes / 16, sink, s);  // warm-up
+  (void)hipEventRecord(e0, s);
+  for (int i = 0; i < reps; i++) launch_read_probe(buf, bytes / 16, sink, s);
+  (void)hipEventRecord(e1, s);
+  hipError_t e = hipEventSynchronize(e1);
+  float t = 0.f;
+  if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (e != hipSuccess) return SPD_E_HIP;
+  *ms = (double)t / reps;
   return SPD_OK;
 }
 

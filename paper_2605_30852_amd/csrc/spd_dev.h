@@ -181,12 +181,14 @@ struct Launch {
   static void oproj(const Ctx& c, const Rows& r, void* stream);
   static void gateup(const Ctx& c, const Rows& r, void* stream);
   static void down(const Ctx& c, const Rows& r, void* stream);
-  // One decoder layer of a row block whose rows share the layer (the PDM's rows in a step; at most
-  // max_rows rows, r.anch unused): streaming GEMVs applying each weight pair to all rows, and the
-  // rows' decode attention. Five launches.
-  static void rows_layer(const Ctx& c, const Rows& r, int max_rows, void* stream);
+  // One decoder layer of a row block whose rows share the layer (the PDM's rows in a step, or a
+  // prefill chunk; at most max_rows rows): streaming GEMVs applying each weight pair to all rows
+  // (the down projection also captures the rows' anchor when r.anch and r.cap name one), and the
+  // rows' decode attention. Five launches; the GEMV launches take at most cap_wgs workgroups (0: as
+  // many as fit at once).
+  static void rows_layer(const Ctx& c, const Rows& r, int max_rows, int cap_wgs, void* stream);
   // sublayer k (0 QKV, 1 attention, 2 O-proj, 3 gate/up, 4 down) of rows_layer
-  static void rows_sublayer(const Ctx& c, const Rows& r, int max_rows, int k, void* stream);
+  static void rows_sublayer(const Ctx& c, const Rows& r, int max_rows, int k, int cap_wgs, void* stream);
   // PDM feature projection; prefill = 1: nrows rows of pf_anch at full depth.
   static void pdm_fc(const Ctx& c, int prefill, int nrows, void* stream);
   // LM head + argmax partials. src: 0 = target exit row (skipped unless a == n), 1 = PDM last row,
@@ -209,6 +211,9 @@ void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* stream,
 // dev_ctx: a device copy of c.
 void launch_step(const Ctx& c, const Ctx* dev_ctx, int grid, void* stream, int bf16);
 void launch_ktrace_reset(const Ctx& c, int nslots, void* stream);
+// Streaming read of n16 16-byte blocks (a bandwidth probe); sink gets one float per workgroup.
+void launch_read_probe(const void* buf, size_t n16, float* sink, void* stream);
+constexpr int kReadProbeWGs = 2048;
 size_t step_lds_bytes(const Ctx& c, int bf16);
 // Events (hipEvent_t) that the next launches of this host thread record at their own start and end;
 // nullptr turns it off.

@@ -642,6 +642,8 @@ __global__ __launch_bounds__(kWG) void k_rgemv(Ctx C, Rows R, int nrp) {
         }
       }
     }
+    // down of a prefill row block ending a stage: its output is also that stage's anchor of the row
+    float* cap = (KIND == SG_DOWN && R.anch != nullptr && R.cap >= 0) ? R.anch + (size_t)R.cap * d : nullptr;
     auto done = [&](int i, const float (&s0)[NR], const float (&s1)[NR]) {
       float2 v[NR];
 #pragma unroll
@@ -679,8 +681,14 @@ __global__ __launch_bounds__(kWG) void k_rgemv(Ctx C, Rows R, int nrp) {
         } else {
           const int m = 2 * q;
           float* xr = gr.x + (size_t)row * gr.xstride;
-          xr[m] = v[r].x + s0[r];
-          if (m + 1 < d) xr[m + 1] = v[r].y + s1[r];
+          const float n0 = v[r].x + s0[r], n1 = v[r].y + s1[r];
+          xr[m] = n0;
+          if (m + 1 < d) xr[m + 1] = n1;
+          if (cap != nullptr) {
+            float* cr = cap + (size_t)row * C.n * d;
+            cr[m] = n0;
+            if (m + 1 < d) cr[m + 1] = n1;
+          }
         }
       }
     };
@@ -1127,6 +1135,36 @@ __global__ __launch_bounds__(kWG) void k_ktrace_reset(Ctx C, int nslots) {
   }
 }
 
+// Bandwidth probe: each workgroup streams one contiguous share of the buffer, its threads reading
+// consecutive 16-byte blocks with non-temporal loads, eight in flight per thread, folded into one
+// value so that no load is dropped.
+__global__ __launch_bounds__(kWG) void k_read_probe(const uint4* p, size_t n16, float* sink) {
+  constexpr int U = 8;
+  const size_t per = (n16 + gridDim.x - 1) / gridDim.x;
+  const size_t b0 = (size_t)blockIdx.x * per, b1 = b0 + per < n16 ? b0 + per : n16;
+  uint32_t acc = 0;
+  for (size_t i0 = b0 + threadIdx.x; i0 < b1; i0 += (size_t)kWG * U) {
+    uint4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) {
+      const size_t i = i0 + (size_t)u * kWG;
+      v[u] = i < b1 ? ldg16(p + i) : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < U; u++) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  __shared__ uint32_t s_acc;
+  if (threadIdx.x == 0) s_acc = 0;
+  __syncthreads();
+  atomicXor(&s_acc, acc);
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = __uint_as_float(s_acc);
+}
+
+void launch_read_probe(const void* buf, size_t n16, float* sink, void* stream) {
+  hipLaunchKernelGGL(k_read_probe, dim3(kReadProbeWGs), dim3(kWG), 0, (hipStream_t)stream, (const uint4*)buf, n16, sink);
+}
+
 void launch_ktrace_reset(const Ctx& c, int nslots, void* stream) {
   hipLaunchKernelGGL(k_ktrace_reset, dim3((nslots + kWG - 1) / kWG), dim3(kWG), 0, (hipStream_t)stream, c, nslots);
 }
@@ -1571,14 +1609,14 @@ static int rows_per_pass(int K, int max_rows) {
 }
 
 template <typename WT, int KIND>
-static void rgemv_launch(const Ctx& c, const Rows& r, int npairs, int K, int max_rows, void* s) {
+static void rgemv_launch(const Ctx& c, const Rows& r, int npairs, int K, int max_rows, int cap_wgs, void* s) {
   const int nrp = rows_per_pass<WT>(K, max_rows);
   const size_t shm = stream_lds<WT>(K) * nrp;
   // no more workgroups than the GPU holds at once with this much LDS (a second round would double
   // the launch), and enough waves that none streams more than 64 pairs
   const int resident = dev_limits().cus * std::max(1, (int)((size_t)dev_limits().lds_max / (shm + 1024)));
   int wgs = std::min(stream_grid(c, npairs, 1), resident);
-  if (c.rows_wgs > 0) wgs = std::min(wgs, c.rows_wgs);  // side work: leave most CUs to the stages
+  if (cap_wgs > 0) wgs = std::min(wgs, cap_wgs);  // side work: leave most CUs to the stages
   wgs = std::max(wgs, (npairs + 255) / 256);
   const dim3 grid(wgs);
   if (nrp <= 4)
@@ -1588,17 +1626,17 @@ static void rgemv_launch(const Ctx& c, const Rows& r, int npairs, int K, int max
 }
 
 template <typename WT>
-void Launch<WT>::rows_layer(const Ctx& c, const Rows& r, int max_rows, void* s) {
-  for (int k = 0; k < 5; k++) rows_sublayer(c, r, max_rows, k, s);
+void Launch<WT>::rows_layer(const Ctx& c, const Rows& r, int max_rows, int cap_wgs, void* s) {
+  for (int k = 0; k < 5; k++) rows_sublayer(c, r, max_rows, k, cap_wgs, s);
 }
 
 template <typename WT>
-void Launch<WT>::rows_sublayer(const Ctx& c, const Rows& r, int max_rows, int k, void* s) {
+void Launch<WT>::rows_sublayer(const Ctx& c, const Rows& r, int max_rows, int k, int cap_wgs, void* s) {
   max_rows = std::max(1, std::min(max_rows, kMaxRows));
-  if (k == 0) rgemv_launch<WT, SG_QKV>(c, r, (c.hq + 2 * c.hkv) * (c.dh / 2), c.d, max_rows, s);
-  if (k == 2) rgemv_launch<WT, SG_OPROJ>(c, r, (c.d + 1) / 2, c.qdim, max_rows, s);
-  if (k == 3) rgemv_launch<WT, SG_GATEUP>(c, r, c.F, c.d, max_rows, s);
-  if (k == 4) rgemv_launch<WT, SG_DOWN>(c, r, (c.d + 1) / 2, c.F, max_rows, s);
+  if (k == 0) rgemv_launch<WT, SG_QKV>(c, r, (c.hq + 2 * c.hkv) * (c.dh / 2), c.d, max_rows, cap_wgs, s);
+  if (k == 2) rgemv_launch<WT, SG_OPROJ>(c, r, (c.d + 1) / 2, c.qdim, max_rows, cap_wgs, s);
+  if (k == 3) rgemv_launch<WT, SG_GATEUP>(c, r, c.F, c.d, max_rows, cap_wgs, s);
+  if (k == 4) rgemv_launch<WT, SG_DOWN>(c, r, (c.d + 1) / 2, c.F, max_rows, cap_wgs, s);
   if (k != 1) return;
   const dim3 agrid(c.max_splits, c.hkv, max_rows);
   const bool g4 = c.G <= 4;

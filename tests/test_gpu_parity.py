@@ -289,6 +289,39 @@ def test_step_modes_bit_identical_to_sublayer_launches(tiny_w, mid_w, which, n, 
         e.close()
 
 
+def test_pdm_disabled_with_forced_drafts_is_bit_identical(mid_w):
+    """With every draft forced, skipping the PDM's launches (spd_set_pdm_enabled(0), used to measure
+    how much of the PDM the stage compute hides) changes nothing on the target path: decisions,
+    tokens, residual streams and anchors match a run with the PDM, bit for bit."""
+    from paper_2605_30852_amd import binding as B
+    sh = mid_w.shape
+    prompt = synth.prompt(sh, SEED + 11, 29)
+    first, ar, _ = _gpu_stream(mid_w, 1, prompt, 24, max_tokens=200)
+    mask = synth.accept_mask(0.6, SEED + 12, 400)
+    table = forced_table(ar, mask, len(prompt), sh.vocab)
+    arr = np.full(len(table) + 8, -1, dtype=np.int32)
+    for q, t in table.items():
+        arr[q - len(prompt)] = t
+    engs = []
+    for on in (True, False):
+        e = _engine(mid_w, 3, max_tokens=200, attn_chunk=32)
+        B.spd_set_pdm_enabled(e.h, on)
+        assert e.spd_prefill(prompt) == first
+        e.spd_set_forced_drafts(arr, len(prompt))
+        engs.append(e)
+    for i in range(14):
+        logs = [e.spd_run_steps(1, want_log=True)[0] for e in engs]
+        for r in logs:
+            r.pop("pdm_draft", None)
+        assert logs[0] == logs[1], f"step {i}"
+        c, a, _, _ = engs[0].state()
+        for q in range(c, c + a):
+            assert np.array_equal(engs[0].resid()[q % 3], engs[1].resid()[q % 3])
+    assert np.array_equal(engs[0].tokens(), engs[1].tokens())
+    for e in engs:
+        e.close()
+
+
 def test_spread_pdm_placement_refused_in_graph_mode(tiny_w):
     """The spread PDM placement (4) is for issued launches only: the library refuses it while graph
     mode is on, and refuses graph mode while it is set; other placements capture as before."""
