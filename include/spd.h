@@ -269,8 +269,9 @@ spd_status spd_probe_hbm_read(const void* buf, size_t bytes, float* sink, int32_
  * SPD_E_INVAL while graph mode is on, and spd_set_graph(h, 1) fails while placement 4 is set. */
 spd_status spd_set_pdm_placement(spd_handle* h, int32_t place);
 
-/* Workgroups of each of the PDM's GEMV launches in a step (0: the default, 32). The PDM runs beside
- * the stage compute, so its launches are kept small enough to leave most CUs to the stages. */
+/* Workgroups of each of the PDM's GEMV launches in a step (0: the default, 32 per 256 MB of PDM
+ * weights). The PDM runs beside the stage compute, so its launches are kept small enough to leave
+ * most CUs to the stages while still finishing inside the stage compute. */
 spd_status spd_set_pdm_grid(spd_handle* h, int32_t wgs);
 
 /* Tracing of the persistent step launch: while on, every tile records four wall-clock stamps (for

@@ -256,6 +256,17 @@ static void enqueue_layer(const Ctx& C, const Rows& r, hipStream_t s, spd_handle
   { TimedLaunch t(h, s, SPD_K_DOWN); Launch<WT>::down(C, r, s); }
 }
 
+// PDM GEMV workgroups: kRowsWGsDefault per 256 MB of PDM weights (feature projection and decoder
+// layers), so that a larger draft module keeps finishing inside the stage compute.
+static int default_rows_wgs(const spd_config& c) {
+  const double esz = c.dtype == SPD_BF16 ? 2.0 : 4.0;
+  const double d = c.d_model, qd = (double)c.n_q_heads * c.head_dim, kvd = (double)c.n_kv_heads * c.head_dim;
+  const double layer = d * (qd + 2 * kvd) + qd * d + 3 * d * c.ffn_dim;
+  const double bytes = esz * (d * c.n_stages * d + c.pdm_layers * layer);
+  const int units = std::max(1, (int)std::lround(bytes / (256.0 * 1024 * 1024)));
+  return std::min(kRowsWGsDefault * units, 1024);
+}
+
 static Rows rows_block(int layer, int nrows, int pos0, float* x, float* anch, int cap, int set) {
   Rows r;
   std::memset(&r, 0, sizeof(Rows));
@@ -648,7 +659,7 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   C.ls = c.pdm_layers;
   C.page = c.page_size;
   C.chunk = lay.chunk;
-  C.rows_wgs = kRowsWGsDefault;
+  C.rows_wgs = default_rows_wgs(c);
   C.max_pages = lay.num_pages;
   C.max_splits = lay.max_splits;
   C.max_tokens = c.max_tokens;
@@ -859,7 +870,7 @@ spd_status spd_set_pdm_placement(spd_handle* h, int32_t place) {
 
 spd_status spd_set_pdm_grid(spd_handle* h, int32_t wgs) {
   if (!h || wgs < 0 || wgs > 65535) return SPD_E_INVAL;
-  h->ctx.rows_wgs = wgs > 0 ? wgs : kRowsWGsDefault;
+  h->ctx.rows_wgs = wgs > 0 ? wgs : default_rows_wgs(h->cfg);
   drop_graph(h);  // kernel arguments changed
   return SPD_OK;
 }
