@@ -63,13 +63,6 @@ __device__ __forceinline__ Grp resolve(const Ctx& C, const Rows& R, int g) {
   return r;
 }
 
-// The layer a group runs: from the launch's own arguments for stage launches, from the device table
-// for row blocks.
-__device__ __forceinline__ LayerDesc layer_of(const Ctx& C, const Rows& R, const Grp& gr) {
-  return R.kind == 0 ? R.ld[gr.s] : C.lay[gr.layer];
-}
-
-
 // --------------------------------------------------------------------------------- GEMV building
 
 // Load blocks [blk, min(blk + kU, blk_end)) of every row (block b = columns b*64*VE + lane*VE + 0..VE-1);
@@ -260,169 +253,6 @@ __device__ __forceinline__ void gemv_tile(const WT* const (&wr)[RL], int K, cons
   }
 }
 
-// ------------------------------------------------------------------ QKV + RoPE + KV append
-// Tile = 4 RoPE pairs of one head: wave w holds row j = 4*tile + w and its partner j + dh/2, so the
-// rotation happens in registers right after the reduction.
-template <typename WT, int NV>
-__global__ __launch_bounds__(kWG) void k_qkv(Ctx C, Rows R) {
-  extern __shared__ __align__(16) float lds[];
-  const Grp gr = resolve(C, R, blockIdx.y);
-  if (!gr.active) return;
-  const LayerDesc Ld = layer_of(C, R, gr);
-  const int dh = C.dh, half = dh >> 1, tph = half >> 2;
-  const int head = blockIdx.x / tph, pb = blockIdx.x % tph;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const WT* W;
-  int hrow;  // head index within its matrix
-  int kind;  // 0 q, 1 k, 2 v
-  if (head < C.hq) {
-    W = (const WT*)Ld.wq;
-    hrow = head;
-    kind = 0;
-  } else if (head < C.hq + C.hkv) {
-    W = (const WT*)Ld.wk;
-    hrow = head - C.hq;
-    kind = 1;
-  } else {
-    W = (const WT*)Ld.wv;
-    hrow = head - C.hq - C.hkv;
-    kind = 2;
-  }
-  const int j = pb * 4 + w;  // pair index (< half)
-  const WT* wr[2];
-  wr[0] = W + (size_t)(hrow * dh + j) * C.d;
-  wr[1] = W + (size_t)(hrow * dh + j + half) * C.d;
-  XSpec xs;
-  xs.src = XS_NORM_RESID;
-  for (int v = 0; v < NV; v++) {
-    xs.row[v] = gr.x + (size_t)v * gr.xstride;
-    xs.gain[v] = Ld.attn_norm;
-  }
-  const int KC = chunk_floats<NV>(C.d, 64 * Elt<WT>::VE);
-  float acc[NV][2];
-  gemv_tile<WT, NV, 2>(wr, C.d, xs, gr.nrows, C.eps, lds, KC, acc);
-  float* qbuf = C.b[R.set].q;
-#pragma unroll
-  for (int v = 0; v < NV; v++) {
-    if (lane == v && v < gr.nrows) {
-      const int pos = gr.pos0 + v;
-      float lo = acc[v][0], hi = acc[v][1];
-      if (kind != 2) {
-        const float2 cs = C.rope[(size_t)pos * half + j];
-        const float rlo = lo * cs.x - hi * cs.y;
-        const float rhi = hi * cs.x + lo * cs.y;
-        lo = rlo;
-        hi = rhi;
-      }
-      if (kind == 0) {
-        float* qo = qbuf + (size_t)(gr.brow0 + v) * C.qdim + hrow * dh;
-        qo[j] = lo;
-        qo[j + half] = hi;
-      } else {
-        WT* kv = (WT*)Ld.kv;
-        const size_t off = kv_off(C, pos, hrow, j) + (kind == 2 ? (size_t)C.hkv * C.page * dh : 0);
-        st1<WT>(kv, off, lo);
-        st1<WT>(kv, off + half, hi);
-      }
-    }
-  }
-}
-
-// --------------------------------------------------------------- O-proj / down-proj + residual
-// Tile = 8 output rows (2 per wave). MODE 0: o-proj (input = attention output, K = Hq*dh);
-// MODE 1: down-proj (input = SwiGLU activation, K = F), which also captures the stage output as
-// the next PDM anchor when this is a stage's last layer.
-template <typename WT, int NV, int MODE>
-__global__ __launch_bounds__(kWG) void k_proj_add(Ctx C, Rows R) {
-  extern __shared__ __align__(16) float lds[];
-  const Grp gr = resolve(C, R, blockIdx.y);
-  if (!gr.active) return;
-  const LayerDesc Ld = layer_of(C, R, gr);
-  const int K = MODE == 0 ? C.qdim : C.F;
-  const WT* W = (const WT*)(MODE == 0 ? Ld.wo : Ld.wd);
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int m0 = blockIdx.x * 8 + w * 2;
-  const WT* wr[2];
-#pragma unroll
-  for (int r = 0; r < 2; r++) wr[r] = (m0 + r < C.d) ? W + (size_t)(m0 + r) * K : nullptr;
-  XSpec xs;
-  xs.src = XS_PLAIN;
-  {
-    const float* b0 = (MODE == 0 ? C.b[R.set].ao : C.b[R.set].act) + (size_t)gr.brow0 * K;
-    for (int v = 0; v < NV; v++) xs.row[v] = b0 + (size_t)v * K;
-  }
-  const int KC = chunk_floats<NV>(K, 64 * Elt<WT>::VE);
-  float acc[NV][2];
-  gemv_tile<WT, NV, 2>(wr, K, xs, gr.nrows, 0.f, lds, KC, acc);
-  // anchor capture target
-  float* cap = nullptr;
-  size_t cap_stride = 0;
-  if (MODE == 1) {
-    if (R.kind == 0) {
-      const int s = gr.s;
-      if (gr.layer + 1 == C.beta[s + 1] && s + 1 <= C.n - 1) {
-        cap = C.anchors + ((size_t)(gr.pos0 % C.n) * C.n + (s + 1)) * C.d;
-      }
-    } else if (R.anch != nullptr && R.cap >= 0) {
-      cap = R.anch + (size_t)R.cap * C.d;
-      cap_stride = (size_t)C.n * C.d;
-    }
-  }
-#pragma unroll
-  for (int v = 0; v < NV; v++) {
-#pragma unroll
-    for (int r = 0; r < 2; r++) {
-      if (lane == v * 2 + r && v < gr.nrows && m0 + r < C.d) {
-        float* xo = gr.x + (size_t)v * gr.xstride;
-        const float nv = xo[m0 + r] + acc[v][r];
-        xo[m0 + r] = nv;
-        if (cap != nullptr) cap[(size_t)v * cap_stride + m0 + r] = nv;
-      }
-    }
-  }
-}
-
-// ------------------------------------------------------------------------- gate/up + SwiGLU
-// Tile = 4 outputs (1 per wave); each wave streams the gate and up rows of its output together.
-template <typename WT, int NV>
-__global__ __launch_bounds__(kWG) void k_gateup(Ctx C, Rows R) {
-  extern __shared__ __align__(16) float lds[];
-  const Grp gr = resolve(C, R, blockIdx.y);
-  if (!gr.active) return;
-  const LayerDesc Ld = layer_of(C, R, gr);
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int m = blockIdx.x * 4 + w;
-  const WT* wr[2];
-  wr[0] = (m < C.F) ? (const WT*)Ld.wg + (size_t)m * C.d : nullptr;
-  wr[1] = (m < C.F) ? (const WT*)Ld.wu + (size_t)m * C.d : nullptr;
-  XSpec xs;
-  xs.src = XS_NORM_RESID;
-  for (int v = 0; v < NV; v++) {
-    xs.row[v] = gr.x + (size_t)v * gr.xstride;
-    xs.gain[v] = Ld.mlp_norm;
-  }
-  const int KC = chunk_floats<NV>(C.d, 64 * Elt<WT>::VE);
-  float acc[NV][2];
-  gemv_tile<WT, NV, 2>(wr, C.d, xs, gr.nrows, C.eps, lds, KC, acc);
-  float* act = C.b[R.set].act;
-#pragma unroll
-  for (int v = 0; v < NV; v++) {
-    if (lane == v && v < gr.nrows && m < C.F) {
-      const float g = acc[v][0], u = acc[v][1];
-      act[(size_t)(gr.brow0 + v) * C.F + m] = g / (1.0f + expf(-g)) * u;
-    }
-  }
-}
-
-// ------------------------------------------------------------- streaming stage-launch GEMVs
-// One launch of a sublayer for the stages of a stage launch (grid y = stage). The launch holds a few
-// workgroups per CU; each stages the stage's input vector into LDS once (with RMSNorm for QKV and
-// gate/up) and its waves then stream their row pairs back to back: wave w of workgroup b takes pairs
-// b*4+w, b*4+w+NW, ... (NW = waves per stage), loading two units ahead across pair boundaries.
-// Values an epilogue needs from memory (RoPE cos/sin, residual entries, the token's KV page) are
-// loaded before the stream, one pair per lane, and handed over by lane shuffles, so no epilogue load
-// makes a wave wait for its own weight stream. Pairs: QKV (j, j + dh/2) of one head (RoPE partners),
-// gate/up (gate m, up m), O-proj and down (2m, 2m + 1).
 enum SKind { SG_QKV = 0, SG_OPROJ = 2, SG_GATEUP = 3, SG_DOWN = 4 };
 
 // Workgroup bx of nbx working on one stage's sublayer (gr: the stage's row, Ld: its layer, set: the
@@ -882,190 +712,6 @@ __device__ __forceinline__ int take_head_dev(const BufSet& B, int V) {
 }
 
 // ------------------------------------------------------------------------------- attention
-// Ragged paged GQA decode attention. Grid: x = key split (chunk keys each), y = KV head, z = group.
-// A group's rows sit at positions pos0..pos0+nrows-1; row i attends to keys [0, pos0+i]. The split
-// count is ceil(keys / chunk), a function of the length only. With one split the workgroup writes
-// the output; otherwise each split writes (o, m, l) and k_attn_combine merges them in split order.
-// LDS (dynamic): queries [MAXQ][DH] fp32, scores [MAXQ][PASS] fp32, V tile [PASS][DH] in the KV type.
-template <int MAXQ>
-struct AttnShape {
-  static constexpr int PASS = MAXQ <= 8 ? 64 : 32;  // keys per pass
-  static constexpr int TPK = kWG / PASS;             // threads per key in the score phase
-};
-
-template <typename KVT, int MAXQ, int DH>
-constexpr size_t attn_lds() {
-  return (size_t)MAXQ * DH * 4 + (size_t)MAXQ * AttnShape<MAXQ>::PASS * 4 +
-         (size_t)AttnShape<MAXQ>::PASS * DH * sizeof(KVT) + (size_t)3 * MAXQ * 4;
-}
-
-template <typename KVT, int MAXQ, int DH>
-__global__ __launch_bounds__(kWG) void k_attn(Ctx C, Rows R) {
-  constexpr int PASS = AttnShape<MAXQ>::PASS;
-  constexpr int TPK = AttnShape<MAXQ>::TPK;
-  constexpr int NE = DH / TPK;  // dims per thread in the score phase
-  constexpr int VE = Elt<KVT>::VE;
-  extern __shared__ __align__(16) float smem[];
-  float* qs = smem;                       // [MAXQ][DH]
-  float* sc = qs + MAXQ * DH;             // [MAXQ][PASS]
-  KVT* vs = (KVT*)(sc + MAXQ * PASS);     // [PASS][DH]
-  float* s_m = (float*)(vs + PASS * DH);  // [MAXQ]
-  float* s_l = s_m + MAXQ;
-  float* s_al = s_l + MAXQ;
-  const Grp gr = resolve(C, R, blockIdx.z);
-  if (!gr.active) return;
-  const int g = blockIdx.y, split = blockIdx.x;
-  const int G = C.G;
-  const int nkeys = gr.pos0 + gr.nrows;
-  const int nsplit = (nkeys + C.chunk - 1) / C.chunk;
-  if (split >= nsplit) return;
-  const int k0 = split * C.chunk, k1 = min(nkeys, k0 + C.chunk);
-  const int nq = gr.nrows * G;
-  const LayerDesc Ld = layer_of(C, R, gr);
-  const KVT* kvb = (const KVT*)Ld.kv;
-  const size_t voff = (size_t)C.hkv * C.page * DH;
-  const BufSet& B = C.b[R.set];
-  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-
-  // queries (already rotated), pre-scaled by 1/sqrt(dh)
-  for (int e = tid; e < nq * DH; e += kWG) {
-    const int qi = e / DH, dd = e % DH;
-    const int i = qi / G, h = g * G + (qi % G);
-    qs[qi * DH + dd] = B.q[(size_t)(gr.brow0 + i) * C.qdim + h * DH + dd] * C.scale;
-  }
-  for (int qi = tid; qi < MAXQ; qi += kWG) {
-    s_m[qi] = -INFINITY;
-    s_l[qi] = 0.f;
-  }
-  // output accumulators: thread -> (query group qg, dim pair dp)
-  constexpr int npair = DH >> 1;
-  constexpr int NG = kWG / npair;  // 4 (dh 128) or 8 (dh 64)
-  const int dp = tid % npair, qg = tid / npair;
-  constexpr int MAXU = (MAXQ + NG - 1) / NG;
-  float o0[MAXU], o1[MAXU];
-#pragma unroll
-  for (int u = 0; u < MAXU; u++) {
-    o0[u] = 0.f;
-    o1[u] = 0.f;
-  }
-  __syncthreads();
-
-  constexpr int VCH = DH * (int)sizeof(KVT) / 16;  // 16-byte chunks per V row
-  for (int kp = k0; kp < k1; kp += PASS) {
-    const int nk = min(PASS, k1 - kp);
-    // V tile -> LDS, 16-byte loads (a page holds 16 consecutive keys of one head contiguously)
-    for (int e = tid; e < nk * VCH; e += kWG) {
-      const int kk = e / VCH, ch = e % VCH;
-      const uint4* src = reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + kk, g, 0) + voff) + ch;
-      reinterpret_cast<uint4*>(vs + kk * DH)[ch] = *src;
-    }
-    // scores: thread -> (key kk, part qq of the head dimension)
-    {
-      const int kk = tid / TPK, qq = tid % TPK;
-      float kr[NE];
-      if (kk < nk) {
-        const uint4* k4 = reinterpret_cast<const uint4*>(kvb + kv_off(C, kp + kk, g, qq * NE));
-#pragma unroll
-        for (int c4 = 0; c4 < NE / VE; c4++) unpack16<KVT>(k4[c4], kr + c4 * VE);
-      } else {
-#pragma unroll
-        for (int e = 0; e < NE; e++) kr[e] = 0.f;
-      }
-      for (int qi = 0; qi < nq; qi++) {
-        float dsum = 0.f;
-        const float* qv = qs + qi * DH + qq * NE;
-#pragma unroll
-        for (int e = 0; e < NE; e += 4) {
-          const float4 q4 = *reinterpret_cast<const float4*>(qv + e);
-          dsum = fmaf(q4.x, kr[e], dsum);
-          dsum = fmaf(q4.y, kr[e + 1], dsum);
-          dsum = fmaf(q4.z, kr[e + 2], dsum);
-          dsum = fmaf(q4.w, kr[e + 3], dsum);
-        }
-#pragma unroll
-        for (int m = 1; m < TPK; m <<= 1) dsum += __shfl_xor(dsum, m, 64);
-        if (qq == 0 && kk < nk) {
-          const int lim = gr.pos0 + qi / G;
-          sc[qi * PASS + kk] = (kp + kk <= lim) ? dsum : -INFINITY;
-        }
-      }
-    }
-    __syncthreads();
-    // online softmax update per query vector (one wave per query vector)
-    for (int qi = w; qi < nq; qi += 4) {
-      const float sv = lane < nk ? sc[qi * PASS + lane] : -INFINITY;
-      const float mx = wave_max(sv);
-      const float mo = s_m[qi];
-      const float mn = fmaxf(mo, mx);
-      const float p = (sv == -INFINITY) ? 0.f : expf(sv - mn);
-      if (lane < nk) sc[qi * PASS + lane] = p;
-      const float ps = wave_sum(p);
-      if (lane == 0) {
-        const float al = (mo == -INFINITY) ? 0.f : expf(mo - mn);
-        s_al[qi] = al;
-        s_l[qi] = s_l[qi] * al + ps;
-        s_m[qi] = mn;
-      }
-    }
-    __syncthreads();
-    // o = o * alpha + P V
-#pragma unroll
-    for (int u = 0; u < MAXU; u++) {
-      const int qi = qg + u * NG;
-      if (qi < nq) {
-        const float al = s_al[qi];
-        o0[u] *= al;
-        o1[u] *= al;
-      }
-    }
-    for (int kk = 0; kk < nk; kk++) {
-      const float v0 = ld1<KVT>(vs, (size_t)kk * DH + 2 * dp);
-      const float v1 = ld1<KVT>(vs, (size_t)kk * DH + 2 * dp + 1);
-#pragma unroll
-      for (int u = 0; u < MAXU; u++) {
-        const int qi = qg + u * NG;
-        if (qi < nq) {
-          const float p = sc[qi * PASS + kk];
-          o0[u] = fmaf(p, v0, o0[u]);
-          o1[u] = fmaf(p, v1, o1[u]);
-        }
-      }
-    }
-    __syncthreads();
-  }
-
-  if (nsplit == 1) {
-#pragma unroll
-    for (int u = 0; u < MAXU; u++) {
-      const int qi = qg + u * NG;
-      if (qi < nq) {
-        const int i = qi / G, h = g * G + (qi % G);
-        const float inv = 1.0f / s_l[qi];
-        float* out = B.ao + (size_t)(gr.brow0 + i) * C.qdim + h * DH + 2 * dp;
-        out[0] = o0[u] * inv;
-        out[1] = o1[u] * inv;
-      }
-    }
-    return;
-  }
-  constexpr int RS = MAXQ * (DH + 2);  // partial record: o[MAXQ][DH], m[MAXQ], l[MAXQ]
-  const int cidx = blockIdx.z * C.hkv + g;
-  float* rec = B.part + ((size_t)cidx * C.max_splits + split) * RS;
-#pragma unroll
-  for (int u = 0; u < MAXU; u++) {
-    const int qi = qg + u * NG;
-    if (qi < nq) {
-      rec[qi * DH + 2 * dp] = o0[u];
-      rec[qi * DH + 2 * dp + 1] = o1[u];
-    }
-  }
-  for (int qi = tid; qi < nq; qi += kWG) {
-    rec[MAXQ * DH + qi] = s_m[qi];
-    rec[MAXQ * DH + MAXQ + qi] = s_l[qi];
-  }
-}
-
-
 // Decode attention of a stage launch. Grid: x = key split, y = KV head, z = stage of the launch.
 // The page of this thread's first key and the device state are requested together at entry; the
 // split itself is attn_split (shared with the persistent step kernel).
@@ -1305,43 +951,6 @@ __global__ __launch_bounds__(kWG, 3) void k_pstep(const Ctx* __restrict__ Cp) {
   }
 }
 
-// Merge the splits of each (group, KV head) in split order. Grid: x = KV head, y = group.
-template <int MAXQ, int DH>
-__global__ __launch_bounds__(kWG) void k_attn_combine(Ctx C, Rows R) {
-  const Grp gr = resolve(C, R, blockIdx.y);
-  if (!gr.active) return;
-  const int g = blockIdx.x;
-  const int nkeys = gr.pos0 + gr.nrows;
-  const int nsplit = (nkeys + C.chunk - 1) / C.chunk;
-  if (nsplit == 1) return;  // the attention kernel wrote the output itself
-  const int G = C.G, nq = gr.nrows * G;
-  constexpr int RS = MAXQ * (DH + 2);
-  constexpr int npair = DH >> 1;
-  constexpr int NG = kWG / npair;
-  const int tid = threadIdx.x, dp = tid % npair, qg = tid / npair;
-  const BufSet& B = C.b[R.set];
-  const int cidx = blockIdx.y * C.hkv + g;
-  const float* base = B.part + (size_t)cidx * C.max_splits * RS;
-  for (int qi = qg; qi < nq; qi += NG) {
-    float M = -INFINITY;
-    for (int sp = 0; sp < nsplit; sp++) M = fmaxf(M, base[(size_t)sp * RS + MAXQ * DH + qi]);
-    float Ls = 0.f, A0 = 0.f, A1 = 0.f;
-    for (int sp = 0; sp < nsplit; sp++) {
-      const float* r = base + (size_t)sp * RS;
-      const float ms = r[MAXQ * DH + qi];
-      const float f = (ms == -INFINITY) ? 0.f : expf(ms - M);
-      Ls = fmaf(r[MAXQ * DH + MAXQ + qi], f, Ls);
-      A0 = fmaf(r[qi * DH + 2 * dp], f, A0);
-      A1 = fmaf(r[qi * DH + 2 * dp + 1], f, A1);
-    }
-    const int i = qi / G, h = g * G + (qi % G);
-    const float inv = 1.0f / Ls;
-    float* out = B.ao + (size_t)(gr.brow0 + i) * C.qdim + h * DH + 2 * dp;
-    out[0] = A0 * inv;
-    out[1] = A1 * inv;
-  }
-}
-
 // ------------------------------------------------------------------------- embedding / state
 template <typename WT>
 __device__ __forceinline__ void push_embedding(const Ctx& C, int tok, float* dst0, float* dst1) {
@@ -1547,37 +1156,23 @@ static inline size_t stream_lds(int K) {
   return (size_t)(K + BLK - 1) / BLK * BLK * sizeof(float);
 }
 
+// Stage launches (r.kind == 0); row blocks go through rows_layer.
 template <typename WT>
 void Launch<WT>::qkv(const Ctx& c, const Rows& r, void* s) {
-  if (r.kind == 0) {
-    const int np = (c.hq + 2 * c.hkv) * (c.dh / 2);
-    launch_timed((k_sgemv<WT, SG_QKV>), dim3(stream_grid(c, np, r.nst), r.nst), dim3(kWG), stream_lds<WT>(c.d), S(s), c, r);
-    return;
-  }
-  const dim3 grid((c.hq + 2 * c.hkv) * (c.dh / 8), 1);
-  launch_timed((k_qkv<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
+  const int np = (c.hq + 2 * c.hkv) * (c.dh / 2);
+  launch_timed((k_sgemv<WT, SG_QKV>), dim3(stream_grid(c, np, r.nst), r.nst), dim3(kWG), stream_lds<WT>(c.d), S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::oproj(const Ctx& c, const Rows& r, void* s) {
-  if (r.kind == 0) {
-    launch_timed((k_sgemv<WT, SG_OPROJ>), dim3(stream_grid(c, (c.d + 1) / 2, r.nst), r.nst), dim3(kWG),
-                 stream_lds<WT>(c.qdim), S(s), c, r);
-    return;
-  }
-  const dim3 grid((c.d + 7) / 8, 1);
-  launch_timed((k_proj_add<WT, kMaxRows, 0>), grid, dim3(kWG), gemv_lds<WT>(c.qdim, kMaxRows), S(s), c, r);
+  launch_timed((k_sgemv<WT, SG_OPROJ>), dim3(stream_grid(c, (c.d + 1) / 2, r.nst), r.nst), dim3(kWG),
+               stream_lds<WT>(c.qdim), S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::down(const Ctx& c, const Rows& r, void* s) {
-  if (r.kind == 0) {
-    launch_timed((k_sgemv<WT, SG_DOWN>), dim3(stream_grid(c, (c.d + 1) / 2, r.nst), r.nst), dim3(kWG),
-                 stream_lds<WT>(c.F), S(s), c, r);
-    return;
-  }
-  const dim3 grid((c.d + 7) / 8, 1);
-  launch_timed((k_proj_add<WT, kMaxRows, 1>), grid, dim3(kWG), gemv_lds<WT>(c.F, kMaxRows), S(s), c, r);
+  launch_timed((k_sgemv<WT, SG_DOWN>), dim3(stream_grid(c, (c.d + 1) / 2, r.nst), r.nst), dim3(kWG),
+               stream_lds<WT>(c.F), S(s), c, r);
 }
 
 // Rows of one row-block pass that fit the workgroup's LDS with input width K (at least 1, at most
@@ -1655,45 +1250,25 @@ void Launch<WT>::rows_sublayer(const Ctx& c, const Rows& r, int max_rows, int k,
 
 template <typename WT>
 void Launch<WT>::gateup(const Ctx& c, const Rows& r, void* s) {
-  if (r.kind == 0) {
-    launch_timed((k_sgemv<WT, SG_GATEUP>), dim3(stream_grid(c, c.F, r.nst), r.nst), dim3(kWG), stream_lds<WT>(c.d),
-                 S(s), c, r);
-    return;
-  }
-  const dim3 grid((c.F + 3) / 4, 1);
-  launch_timed((k_gateup<WT, kMaxRows>), grid, dim3(kWG), gemv_lds<WT>(c.d, kMaxRows), S(s), c, r);
-}
-
-template <typename WT, int MAXQ, int DH>
-static void attn_launch(const Ctx& c, const Rows& r, void* s) {
-  const dim3 grid(c.max_splits, c.hkv, r.kind == 0 ? r.nst : 1);
-  launch_timed((k_attn<WT, MAXQ, DH>), grid, dim3(kWG), (attn_lds<WT, MAXQ, DH>()), S(s), c, r);
-  const dim3 cgrid(c.hkv, r.kind == 0 ? r.nst : 1);
-  launch_timed((k_attn_combine<MAXQ, DH>), cgrid, dim3(kWG), 0, S(s), c, r);
+  launch_timed((k_sgemv<WT, SG_GATEUP>), dim3(stream_grid(c, c.F, r.nst), r.nst), dim3(kWG), stream_lds<WT>(c.d),
+               S(s), c, r);
 }
 
 template <typename WT>
 void Launch<WT>::attn(const Ctx& c, const Rows& r, void* s) {
-  if (r.kind == 0) {
-    const dim3 grid(c.max_splits, c.hkv, r.nst);
-    const bool g4 = c.G <= 4;
-    if (c.dh == 128) {
-      if (g4)
-        launch_timed((k_attn_stage<WT, 128, 4>), grid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
-      else
-        launch_timed((k_attn_stage<WT, 128, 8>), grid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
-    } else {
-      if (g4)
-        launch_timed((k_attn_stage<WT, 64, 4>), grid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
-      else
-        launch_timed((k_attn_stage<WT, 64, 8>), grid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
-    }
-    return;
+  const dim3 grid(c.max_splits, c.hkv, r.nst);
+  const bool g4 = c.G <= 4;
+  if (c.dh == 128) {
+    if (g4)
+      launch_timed((k_attn_stage<WT, 128, 4>), grid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
+    else
+      launch_timed((k_attn_stage<WT, 128, 8>), grid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
+  } else {
+    if (g4)
+      launch_timed((k_attn_stage<WT, 64, 4>), grid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
+    else
+      launch_timed((k_attn_stage<WT, 64, 8>), grid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
   }
-  if (c.dh == 128)
-    attn_launch<WT, 64, 128>(c, r, s);
-  else
-    attn_launch<WT, 64, 64>(c, r, s);
 }
 
 template <typename WT>
