@@ -220,6 +220,24 @@ def ar_greedy(model: Model, prompt, n_new: int, return_logits: bool = False):
     return (out, logs) if return_logits else out
 
 
+def ar_sample(model: Model, prompt, n_new: int, dist_of, draw):
+    """Plain autoregressive sampling: token i after the prompt is draw(dist_of(logits), position).
+    dist_of and draw are the sampling rule (oracle/sampling.py); returns the n_new tokens."""
+    caches = new_caches(model.shape, model.shape.n_layers)
+    h = None
+    for p, t in enumerate(prompt):
+        h, _ = run_token(model, caches, int(t), p)
+    out = []
+    pos = len(prompt)
+    while True:
+        x = draw(dist_of(lm_logits(model, h)), pos)
+        out.append(x)
+        if len(out) == n_new:
+            return out
+        h, _ = run_token(model, caches, x, pos)
+        pos += 1
+
+
 def forward_full(model: Model, tokens, layers_out=None, free_layers: bool = False) -> Dict[int, np.ndarray]:
     """Brute force without any cache: full causal attention over all rows at every layer.
 

@@ -25,6 +25,11 @@ What it follows:
     target's own argmax is reseeded at depth 0. With n = 1 the judged token is this step's own
     draft, so the step is ordinary greedy decoding. While a < n (warm-up or refill) nothing exits
     and the draft is pushed unconditionally.
+  * Sampled decoding (Section 3.4 under sampling, Section 4.1's top-k setting; oracle/sampling.py):
+    the draft is drawn from the PDM's top-k distribution q with the draft position's u_draft, and q
+    is kept with the in-flight token; the exit's top-k distribution p judges the successor by
+    rejection sampling with the successor's u_accept / u_resample, and a reject reseeds the residual
+    draw. A forced draft carries q = delta. The prompt's first token is drawn from p with u_resample.
 """
 from __future__ import annotations
 
@@ -35,6 +40,7 @@ import numpy as np
 
 import synth
 from .model import (LayerCache, Model, argmax_first, decoder_layer, embed, lm_logits, new_caches)
+from . import sampling as smp
 
 NONE, ACCEPT, REJECT = 0, 1, 2
 
@@ -59,9 +65,9 @@ def eligible_anchors(k: int, anchors: Sequence[int], n_layers: int, n: int) -> i
 @dataclasses.dataclass
 class StepResult:
     decision: int
-    target_argmax: int  # y (or -1 when nothing exited)
+    target_argmax: int  # y, the token committed at verified_pos (or -1 when nothing exited)
     draft: int  # the token the PDM proposed (after any forced override)
-    pdm_draft: int  # the PDM's own argmax
+    pdm_draft: int  # the PDM's own argmax (sampled decoding: its own draw)
     exited_pos: int
     verified_pos: int
     verified_token: int
@@ -71,12 +77,16 @@ class StepResult:
     pdm_logits: Optional[np.ndarray] = None
     pdm_hidden: Optional[Dict[int, np.ndarray]] = None
     depths: Optional[Dict[int, int]] = None  # pre-step depth of every row the PDM read
+    pdm_dist: Optional[smp.Dist] = None  # sampled decoding: the PDM's top-k distribution
+    exit_dist: Optional[smp.Dist] = None  # sampled decoding: the exit's top-k distribution
+    accepted_by_ratio: Optional[bool] = None  # sampled decoding: outcome of the acceptance test
 
 
 class SPDOracle:
     """SPD state for one sequence: target KV per layer, PDM KV per PDM layer, in-flight tokens."""
 
-    def __init__(self, model: Model, n: Optional[int] = None, pdm_layers: Optional[int] = None):
+    def __init__(self, model: Model, n: Optional[int] = None, pdm_layers: Optional[int] = None,
+                 sampling: Optional[smp.Sampling] = None):
         model = model.for_width(model.shape.n_stages if n is None else n, pdm_layers)
         sh = model.shape
         self.m = model
@@ -96,6 +106,23 @@ class SPDOracle:
         self.prompt_len = 0
         self.steps = 0
         self.verified = 0  # N: prefill token + one per exit
+        self.sampling = sampling
+        self.qdist: Dict[int, smp.Dist] = {}  # sampled decoding: q of each in-flight token
+
+    def clone(self) -> "SPDOracle":
+        """An independent copy of the decoding state (the model is shared)."""
+        o = object.__new__(SPDOracle)
+        o.__dict__.update(self.__dict__)
+        o.caches = [cc.clone() for cc in self.caches]
+        o.pdm_caches = [cc.clone() for cc in self.pdm_caches]
+        o.toks = list(self.toks)
+        o.hidden = {q: h.copy() for q, h in self.hidden.items()}
+        o.anch = {q: [x.copy() for x in v] for q, v in self.anch.items()}
+        o.qdist = dict(self.qdist)
+        return o
+
+    def _target_dist(self, lg: np.ndarray) -> smp.Dist:
+        return smp.top_k_dist(lg, self.sampling.top_k, self.sampling.temperature)
 
     # ------------------------------------------------------------------ PDM pieces
     def w_in(self) -> np.ndarray:
@@ -129,7 +156,9 @@ class SPDOracle:
         for p, t in enumerate(prompt):
             h, kept = self._run_stage_range(embed(self.m, t), p, 0, self.n, capture=True)
             self.pdm_row(self.feature(kept, self.n), p)
-        x = argmax_first(lm_logits(self.m, h))
+        lg = lm_logits(self.m, h)
+        x = argmax_first(lg) if self.sampling is None else smp.sample(
+            self._target_dist(lg), self.sampling.u(P, smp.U_RESAMPLE))
         self.toks = prompt + [x]
         self.prompt_len = P
         self.c = P
@@ -174,8 +203,15 @@ class SPDOracle:
             g = self.feature(self.anch[q], a - 1 - i)
             pdm_h[q] = self.pdm_row(g, q)
         pdm_lg = lm_logits(self.m, pdm_h[c + a - 1], "pdm.norm")
-        pdm_draft = argmax_first(pdm_lg)
+        dpos = c + a  # the draft's position
+        if self.sampling is None:
+            qd = None
+            pdm_draft = argmax_first(pdm_lg)
+        else:
+            qd = self._target_dist(pdm_lg)
+            pdm_draft = smp.sample(qd, self.sampling.u(dpos, smp.U_DRAFT))
         draft = pdm_draft if forced_draft is None else int(forced_draft)
+        q_draft = None if qd is None else (qd if forced_draft is None else smp.point_mass(draft))
 
         # --- target: the token at depth s runs stage s
         for i in range(a):
@@ -187,13 +223,23 @@ class SPDOracle:
 
         self.steps += 1
         res = StepResult(NONE, -1, draft, pdm_draft, -1, -1, -1, 0, 0, depths=depths,
-                         pdm_hidden=pdm_h)
+                         pdm_hidden=pdm_h, pdm_dist=qd)
         if want_logits:
             res.pdm_logits = pdm_lg
+        if q_draft is not None:
+            self.qdist[dpos] = q_draft  # kept with the token while it is in flight
         if a == n:
             lg = lm_logits(self.m, self.hidden[c])
-            y = argmax_first(lg)
             succ = self.toks[c + 1] if n >= 2 else draft
+            if self.sampling is None:
+                y = argmax_first(lg)
+            else:
+                pd = self._target_dist(lg)
+                ok, y = smp.rejection_verify(pd, self.qdist[c + 1], succ,
+                                             self.sampling.u(c + 1, smp.U_ACCEPT),
+                                             self.sampling.u(c + 1, smp.U_RESAMPLE))
+                res.exit_dist, res.accepted_by_ratio = pd, ok
+                del self.qdist[c + 1]  # judged once; committed from here on
             res.target_argmax, res.exited_pos, res.verified_pos, res.verified_token = y, c, c + 1, y
             if want_logits:
                 res.exit_logits = lg
@@ -234,6 +280,8 @@ class SPDOracle:
             pc.truncate(min(pc.n, keep))
         for q in [q for q in self.hidden if q >= keep]:
             del self.hidden[q], self.anch[q]
+        for q in [q for q in self.qdist if q >= keep]:
+            del self.qdist[q]
         del self.toks[keep:]
 
     def rollback(self, keep_len: int, reseed: int) -> None:
@@ -259,11 +307,12 @@ class SPDOracle:
 
 
 def run_spd(model: Model, prompt, n_tokens: int, n: Optional[int] = None,
-            draft_for: Optional[Callable[[int], Optional[int]]] = None, max_steps: int = 100000):
+            draft_for: Optional[Callable[[int], Optional[int]]] = None, max_steps: int = 100000,
+            sampling: Optional[smp.Sampling] = None):
     """Run SPD until n_tokens generated tokens are verified. draft_for(position) may force drafts.
 
     Returns (oracle, list of StepResult)."""
-    o = SPDOracle(model, n=n)
+    o = SPDOracle(model, n=n, sampling=sampling)
     o.prefill(prompt)
     results = []
     while o.verified < n_tokens and len(results) < max_steps:
