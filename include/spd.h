@@ -161,6 +161,23 @@ spd_status spd_rollback(spd_handle* h, int32_t keep_len, int32_t reseed_token);
 spd_status spd_set_forced_drafts(spd_handle* h, const int32_t* table, int32_t first_pos, int32_t len);
 spd_status spd_clear_forced_drafts(spd_handle* h);
 
+/* Sampled decoding (Section 3.4 under sampling; Section 4.1 samples at temperature 1 with top-k 50
+ * and top-p 1.0). Every distribution is the softmax at `temperature` of the top_k largest logits
+ * (lower index first among equal logits). The PDM's draft is drawn from its distribution q; when the
+ * exiting token's distribution p judges the in-flight successor x, x is kept iff
+ * u_accept * q(x) < p(x) (probability min(1, p(x)/q(x))), else the committed token is drawn from
+ * max(0, p - q) normalised (from p if that has no mass) and reseeded, so the output follows p. A forced
+ * draft has q = delta. The prompt's first token is drawn from p. Draws take the inverse CDF in
+ * value-descending order: the first i with u * sum < cumsum_i.
+ * uniforms: host float[3 * positions], positions == max_tokens; entry 3*pos + j is position pos's
+ * u_draft (j = 0), u_accept (1) and u_resample (2), each in [0, 1); copied during the call.
+ * top_k in [1, 64] turns sampling on (needs fused_head = 1), top_k = 0 back to greedy decoding
+ * (uniforms may be NULL). Legal only before spd_prefill (SPD_E_STATE afterwards). In a sampled step
+ * spd_step_result.target_argmax and verified_token hold the committed token and pdm_draft the
+ * PDM's own draw. */
+spd_status spd_set_sampling(spd_handle* h, int32_t top_k, float temperature, const float* uniforms,
+                            int32_t positions);
+
 /* Enqueue `count` steps without host synchronisation (needs auto_rollback = 1). If log is not
  * NULL (host, count entries) the call waits and fills it with each step's result; otherwise it
  * returns once the work is enqueued and spd_sync() waits. */
@@ -191,6 +208,9 @@ spd_status spd_sync(spd_handle* h, spd_step_result* last);
  *                        is sublayer k (QKV, attention, O-proj, gate/up, down) of layer slot j of stage
  *                        s (stage launches, modes 0 and 2); slots 5*J*n + 0, 1, 2 are the LM head,
  *                        verify and the PDM feature projection.
+ *   SPD_DBG_QDIST:       sampled decoding: the draft distribution q kept with each in-flight token,
+ *                        row r = position mod n: n int32 entry counts, then [n][64] int32 ids, then
+ *                        [n][64] fp32 probabilities (value-descending order)
  * bytes must equal the size listed (nitems, ntrace and nkslots from spd_step_plan_info). */
 enum {
   SPD_DBG_RESID = 1,
@@ -202,7 +222,8 @@ enum {
   SPD_DBG_STATE = 7,
   SPD_DBG_STEP_ITEMS = 8,
   SPD_DBG_STEP_TRACE = 9,
-  SPD_DBG_KTRACE = 10
+  SPD_DBG_KTRACE = 10,
+  SPD_DBG_QDIST = 11
 };
 spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes);
 

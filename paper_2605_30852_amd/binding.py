@@ -17,7 +17,8 @@ SPD_F32, SPD_BF16 = 0, 1
 SPD_NONE, SPD_ACCEPT, SPD_REJECT = 0, 1, 2
 SPD_DBG_RESID, SPD_DBG_ANCHORS, SPD_DBG_PDM_HIDDEN = 1, 2, 3
 SPD_DBG_EXIT_LOGITS, SPD_DBG_PDM_LOGITS, SPD_DBG_TOKENS, SPD_DBG_STATE = 4, 5, 6, 7
-SPD_DBG_STEP_ITEMS, SPD_DBG_STEP_TRACE, SPD_DBG_KTRACE = 8, 9, 10
+SPD_DBG_STEP_ITEMS, SPD_DBG_STEP_TRACE, SPD_DBG_KTRACE, SPD_DBG_QDIST = 8, 9, 10, 11
+MAX_TOP_K = 64
 SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD, SPD_K_SPANS, SPD_K_STEP = 1, 2, 3, 4, 5, 6, 7, 8
 SPD_K_MIX = 9
 
@@ -61,7 +62,7 @@ EXPORTS = [
     "spd_read_kv", "spd_set_debug", "spd_destroy", "spd_status_str", "spd_last_error",
     "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing", "spd_set_step_kernel",
     "spd_set_step_trace", "spd_step_plan_info", "spd_set_kernel_trace", "spd_set_pdm_placement",
-    "spd_set_pdm_grid", "spd_set_pdm_enabled", "spd_probe_hbm_read",
+    "spd_set_pdm_grid", "spd_set_pdm_enabled", "spd_probe_hbm_read", "spd_set_sampling",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -105,6 +106,7 @@ def lib() -> ct.CDLL:
             "spd_set_pdm_placement": (I, [P, I]),
             "spd_set_pdm_grid": (I, [P, I]),
             "spd_set_pdm_enabled": (I, [P, I]),
+            "spd_set_sampling": (I, [P, I, ct.c_float, ct.POINTER(ct.c_float), I]),
             "spd_probe_hbm_read": (I, [P, ct.c_size_t, P, I, P, ct.POINTER(ct.c_double)]),
             "spd_step_plan_info": (I, [P, ct.POINTER(ct.c_int32)]),
             "spd_kernel_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
@@ -262,6 +264,17 @@ def spd_set_pdm_placement(h: int, place: int) -> None:
 
 def spd_set_pdm_enabled(h: int, on: bool) -> None:
     _check("spd_set_pdm_enabled", lib().spd_set_pdm_enabled(h, 1 if on else 0), h)
+
+
+def spd_set_sampling(h: int, top_k: int, temperature: float = 1.0, uniforms=None) -> None:
+    """uniforms: float[max_tokens, 3] (u_draft, u_accept, u_resample per position); top_k 0 = greedy."""
+    if uniforms is None:
+        _check("spd_set_sampling", lib().spd_set_sampling(h, int(top_k), float(temperature), None, 0), h)
+        return
+    u = np.ascontiguousarray(uniforms, dtype=np.float32)
+    assert u.ndim == 2 and u.shape[1] == 3
+    _check("spd_set_sampling", lib().spd_set_sampling(h, int(top_k), float(temperature),
+                                                      u.ctypes.data_as(ct.POINTER(ct.c_float)), u.shape[0]), h)
 
 
 def spd_probe_hbm_read(buf: int, nbytes: int, sink: int, reps: int, stream: int) -> float:

@@ -26,7 +26,9 @@ struct Layout {
   size_t kv, pkv, pt, rope, state, tok, forced, log, resid, anch, pdmx, pfx, pfanch, dbg, lay;
   size_t q[2], ao[2], act[2], part[2], cnt[2], hkey[2];
   size_t items, sync, dctx, trace, ktrace;
+  size_t su, swlog, swgmax, sqids, sqp, sqcnt;  // sampled decoding
   size_t total;
+  int wlog_stride;
   int num_pages, chunk, max_splits, J, nitems, nsync, ntrace, nkslots;
   int tiles[5];
   size_t kv_layer_bytes;
@@ -132,6 +134,14 @@ Layout make_layout(const spd_config& c) {
   L.trace = take(sizeof(unsigned long long) * (size_t)L.ntrace);
   L.nkslots = 5 * L.J * n + 4;
   L.ktrace = take(sizeof(unsigned long long) * 2 * (size_t)L.nkslots);
+  // sampled decoding: the head's wave regions cover at most V + 2 * (4 * kSampleWGs) floats per row
+  L.wlog_stride = (int)align_up((size_t)c.vocab + 8 * kSampleWGs, 64);
+  L.su = take(sizeof(float) * 3 * (size_t)c.max_tokens);
+  L.swlog = take(sizeof(float) * 2 * (size_t)L.wlog_stride);
+  L.swgmax = take(sizeof(unsigned long long) * 2 * kSampleWGs);
+  L.sqids = take(sizeof(int32_t) * n * kMaxTopK);
+  L.sqp = take(sizeof(float) * n * kMaxTopK);
+  L.sqcnt = take(sizeof(int32_t) * n);
   L.total = o;
   return L;
 }
@@ -502,7 +512,10 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     if (sp) HIPC(hipEventRecord(sp[2], h->main));
     HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
     TimedLaunch t(h, h->main, SPD_K_HEAD);
-    Launch<WT>::head_verify(C, forced_override, h->cfg.auto_rollback, h->main);  // + the step's verify
+    if (C.sam.top_k > 0)  // + top-k distributions, the draft's draw and the rejection-sampling verify
+      Launch<WT>::head_sample(C, 3, 0, 0, forced_override, h->cfg.auto_rollback, h->main);
+    else
+      Launch<WT>::head_verify(C, forced_override, h->cfg.auto_rollback, h->main);  // + the step's verify
     return launch_check(h, "step");
   } else {
     {
@@ -533,7 +546,12 @@ static spd_status enqueue_prefill(spd_handle* h, int len) {
     Launch<WT>::pdm_fc(C, 1, rc, h->main);
     for (int i = 0; i < h->cfg.pdm_layers; i++)
       Launch<WT>::rows_layer(C, rows_block(L + i, rc, t0, C.pdm_x, nullptr, -1, 1), kMaxRows, 0, h->main);
-    if (t0 + rc == len) Launch<WT>::head(C, 2, rc - 1, h->main);
+    if (t0 + rc == len) {
+      if (C.sam.top_k > 0)  // the first token is drawn from the top-k distribution
+        Launch<WT>::head_sample(C, 2, rc - 1, len, -1, 0, h->main);
+      else
+        Launch<WT>::head(C, 2, rc - 1, h->main);
+    }
     spd_status st = launch_check(h, "prefill");
     if (st != SPD_OK) return st;
   }
@@ -699,6 +717,15 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
     B.cnt = (int32_t*)(ws + lay.cnt[s]);
     B.hkey = (unsigned long long*)(ws + lay.hkey[s]);
   }
+  C.sam.top_k = 0;
+  C.sam.inv_temp = 1.0f;
+  C.sam.u = (const float*)(ws + lay.su);
+  C.sam.wlog = (float*)(ws + lay.swlog);
+  C.sam.wlog_stride = lay.wlog_stride;
+  C.sam.wgmax = (unsigned long long*)(ws + lay.swgmax);
+  C.sam.q_ids = (int32_t*)(ws + lay.sqids);
+  C.sam.q_p = (float*)(ws + lay.sqp);
+  C.sam.q_cnt = (int32_t*)(ws + lay.sqcnt);
   C.plan.items = (const uint32_t*)(ws + lay.items);
   C.plan.nitems = lay.nitems;
   C.plan.sync = (int32_t*)(ws + lay.sync);
@@ -759,6 +786,7 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   for (int s = 0; s < 2; s++) HIPI(hipMemsetAsync(ws + lay.hkey[s], 0, sizeof(unsigned long long), h->main));
   HIPI(hipMemcpyAsync(ws + lay.items, items.data(), sizeof(uint32_t) * items.size(), hipMemcpyHostToDevice, h->main));
   HIPI(hipMemsetAsync(ws + lay.sync, 0, sizeof(int32_t) * lay.nsync, h->main));
+  HIPI(hipMemsetAsync(ws + lay.sqcnt, 0, sizeof(int32_t) * c.n_stages, h->main));
   // the persistent step kernel reads the context from device memory
   HIPI(hipMemcpyAsync(ws + lay.dctx, &C, sizeof(Ctx), hipMemcpyHostToDevice, h->main));
   HIPI(hipStreamSynchronize(h->main));
@@ -828,6 +856,37 @@ spd_status spd_set_step_trace(spd_handle* h, int32_t on) {
   if (on) HIPC(hipMemset(h->ws + h->lay.trace, 0, sizeof(unsigned long long) * (size_t)h->lay.ntrace));
   HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
   drop_graph(h);
+  return SPD_OK;
+}
+
+static spd_status refuse(spd_handle* h, const char* why) {
+  h->err = why;
+  return SPD_E_INVAL;
+}
+
+spd_status spd_set_sampling(spd_handle* h, int32_t top_k, float temperature, const float* uniforms,
+                            int32_t positions) {
+  if (!h) return SPD_E_INVAL;
+  if (h->hstate != H_INIT) return SPD_E_STATE;
+  if (top_k == 0) {
+    h->ctx.sam.top_k = 0;
+    drop_graph(h);
+    return SPD_OK;
+  }
+  if (top_k < 0 || top_k > kMaxTopK) return refuse(h, "top_k must be in [0, 64]");
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return refuse(h, "temperature must be > 0");
+  if (!h->cfg.fused_head) return refuse(h, "sampled decoding needs fused_head = 1");
+  if (!uniforms || positions != h->cfg.max_tokens)
+    return refuse(h, "uniforms must hold 3 * max_tokens values");
+  for (size_t i = 0; i < (size_t)3 * positions; i++)
+    if (!(uniforms[i] >= 0.f && uniforms[i] < 1.f)) return refuse(h, "uniforms must lie in [0, 1)");
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->main));
+  HIPC(hipMemcpy(h->ws + h->lay.su, uniforms, sizeof(float) * 3 * (size_t)positions, hipMemcpyHostToDevice));
+  h->ctx.sam.top_k = top_k;
+  h->ctx.sam.inv_temp = 1.0f / temperature;
+  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
+  drop_graph(h);  // the captured launches change
   return SPD_OK;
 }
 
@@ -1118,6 +1177,7 @@ spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes)
     case SPD_DBG_PDM_LOGITS: src = h->ctx.dbg_logits + c.vocab; need = sizeof(float) * c.vocab; break;
     case SPD_DBG_TOKENS: src = h->ctx.tok; need = sizeof(int32_t) * c.max_tokens; break;
     case SPD_DBG_STATE: src = nullptr; need = sizeof(int32_t) * 4; break;
+    case SPD_DBG_QDIST: src = nullptr; need = sizeof(int32_t) * c.n_stages * (1 + 2 * kMaxTopK); break;
     case SPD_DBG_STEP_ITEMS: src = h->ctx.plan.items; need = sizeof(uint32_t) * (size_t)h->lay.nitems; break;
     case SPD_DBG_KTRACE:
       src = h->ws + h->lay.ktrace;
@@ -1141,6 +1201,15 @@ spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes)
     o[1] = s.a;
     o[2] = s.prompt_len;
     o[3] = s.nsteps;
+    return SPD_OK;
+  }
+  if (what == SPD_DBG_QDIST) {
+    const int n = c.n_stages;
+    char* o = (char*)host;
+    HIPC(hipMemcpy(o, h->ctx.sam.q_cnt, sizeof(int32_t) * n, hipMemcpyDeviceToHost));
+    HIPC(hipMemcpy(o + sizeof(int32_t) * n, h->ctx.sam.q_ids, sizeof(int32_t) * n * kMaxTopK, hipMemcpyDeviceToHost));
+    HIPC(hipMemcpy(o + sizeof(int32_t) * n * (1 + kMaxTopK), h->ctx.sam.q_p, sizeof(float) * n * kMaxTopK,
+                   hipMemcpyDeviceToHost));
     return SPD_OK;
   }
   HIPC(hipMemcpy(host, src, need, hipMemcpyDeviceToHost));

@@ -74,6 +74,12 @@ constexpr int kStreamWGs = 1024;  // workgroups of one streaming stage launch (a
 // PDM row-block GEMV launches run beside the stage compute: a few workgroups, so that most CUs (and
 // their LDS) stay with the stage launches.
 constexpr int kRowsWGsDefault = 32;
+// Sampled decoding (top-k, temperature): at most this many tokens per distribution; a sampled
+// LM-head launch has at most kSampleWGs workgroups (each leaves one maximum per row), and its
+// selection keeps up to kSelCap candidates in LDS (more go through a slower pass over memory).
+constexpr int kMaxTopK = 64;
+constexpr int kSampleWGs = 1024;
+constexpr int kSelCap = 1024;
 __host__ __device__ inline uint32_t step_item(int p, int s, int t) {
   return ((uint32_t)p << 19) | ((uint32_t)s << 16) | (uint32_t)t;
 }
@@ -88,6 +94,22 @@ __host__ __device__ inline int sync_done(int p, int s, int n) { return (2 + p * 
 // grouped persistent kernel: stage s's arrival counters, kBarParts of them (one line each)
 constexpr int kBarParts = 8;
 __host__ __device__ inline int sync_bar(int s) { return (2 + s * kBarParts) * kSyncStride; }
+
+// Sampled decoding state. The sampled LM-head launch leaves every logit of its rows in wlog, one
+// region of cmax = 2*ceil(pairs / waves) floats per wave (entry i of wave w is vocabulary row
+// 2*(w + (i/2)*waves) + i%2), and each workgroup's best key per row in wgmax; q_* hold the draft
+// distribution of every in-flight token (row = position mod n) until its acceptance test.
+struct Sampler {
+  int top_k;                  // 0: greedy decoding
+  float inv_temp;             // 1 / temperature
+  const float* u;             // [max_tokens][3]: u_draft, u_accept, u_resample of each position
+  float* wlog;                // [2][wlog_stride]: row 0 the exit (or prefill) row, row 1 the PDM row
+  int wlog_stride;            // floats per row, >= V + 8 * kSampleWGs
+  unsigned long long* wgmax;  // [2][kSampleWGs]
+  int32_t* q_ids;             // [n][kMaxTopK]
+  float* q_p;                 // [n][kMaxTopK]
+  int32_t* q_cnt;             // [n]
+};
 
 struct StepPlan {
   const uint32_t* items;  // ticket -> item
@@ -134,6 +156,7 @@ struct Ctx {
   int stream_wgs;   // workgroups of one streaming stage launch (all its stages)
   int rows_wgs;     // at most this many workgroups per row-block (PDM) GEMV launch (0: no cap)
   int J;            // layer slots per step (longest stage)
+  Sampler sam;      // sampled decoding (sam.top_k == 0: greedy)
 };
 
 // Which rows a launch works on.
@@ -198,6 +221,12 @@ struct Launch {
   // The two-row head (src 3) and the verify of the step in one launch: the workgroup that finishes
   // the head last runs the verify.
   static void head_verify(const Ctx& c, int forced_override, int auto_rb, void* stream);
+  // Sampled decoding (c.sam.top_k > 0). src 3: the two-row head, then the top-k distributions, the
+  // draft's draw and the rejection-sampling verify of the step, in one launch; src 2: prefill row
+  // `row` and the draw of the token at position pos (published as the row's argmax key, which the
+  // reseed that follows reads).
+  static void head_sample(const Ctx& c, int src, int row, int pos, int forced_override, int auto_rb,
+                          void* stream);
   static void embed_rows(const Ctx& c, int t0, int nrows, void* stream);
   // one launch of the skewed schedule, nwg workgroups
   static void mix(const Ctx& c, const MixLaunch& m, int nwg, void* stream);

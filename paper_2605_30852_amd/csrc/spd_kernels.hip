@@ -18,6 +18,7 @@
 #include "spd_devfn.h"
 #include "spd_gemv.h"
 #include "spd_attn.h"
+#include "spd_sample.h"
 
 namespace spd {
 
@@ -592,7 +593,10 @@ __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_ar
 // W_lm serving both heads. The vocabulary is streamed like a stage GEMV (each workgroup stages the
 // normalised rows once, its waves stream vocabulary row pairs back to back); each row's argmax goes
 // to the argmax key of set 0 (target) or set 1 (PDM) as an order-independent maximum.
-template <typename WT, int NV>
+// SAMP: sampled decoding; every logit also goes to the wave's region of C.sam.wlog and the
+// workgroup's best key per row to C.sam.wgmax (device-scope stores, read by the launch's last
+// workgroup).
+template <typename WT, int NV, bool SAMP = false>
 __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
   extern __shared__ __align__(16) float lds[];
   __shared__ float red[4];
@@ -652,6 +656,7 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
     bi[v] = 0x7fffffff;
   }
   const bool dbg_row0 = C.debug && (src != 0 && src != 3 ? true : a == C.n);
+  const int cmax = 2 * ((npairs + NW - 1) / NW);  // SAMP: floats per wave region
   // every lane holds the same sums, so every lane keeps the same running maximum
   auto done = [&](int i, const float (&s0)[NV], const float (&s1)[NV]) {
     const int m = 2 * (wv + i * NW);
@@ -660,6 +665,9 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
       const float l0 = s0[v] * scl[v], l1 = s1[v] * scl[v];
       if (C.debug && (v > 0 || dbg_row0) && lane < 2 && m + lane < V)
         C.dbg_logits[(size_t)set[v] * V + m + lane] = lane == 0 ? l0 : l1;
+      if (SAMP && lane < 2 && m + lane < V)
+        st_dev(C.sam.wlog + (size_t)set[v] * C.sam.wlog_stride + (size_t)wv * cmax + 2 * i + lane,
+               lane == 0 ? l0 : l1);
       if (m < V && better(l0, m, bv[v], bi[v])) {
         bv[v] = l0;
         bi[v] = m;
@@ -691,6 +699,9 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
     // the maximum is order-independent, so the result does not depend on which workgroup lands last
     if (fi != 0x7fffffff)
       __hip_atomic_fetch_max(C.b[set[v]].hkey, argmax_key(fv, fi), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (SAMP)
+      __hip_atomic_store(C.sam.wgmax + (size_t)set[v] * kSampleWGs + blockIdx.x,
+                         fi != 0x7fffffff ? argmax_key(fv, fi) : 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -978,17 +989,13 @@ __device__ __forceinline__ void reset_step_sync(const Ctx& C) {
     for (int i = threadIdx.x; i < C.plan.nsync; i += kWG) C.plan.sync[i] = 0;
 }
 
-// Greedy streaming verification (Section 3.4) and the pipeline state update; single workgroup,
-// last kernel of a step.
-// COH: the argmax keys were written by other workgroups of the same launch.
-template <typename WT, bool COH = false>
-__device__ __forceinline__ void verify_body(const Ctx& C, int forced_override, int auto_rb) {
+// The state update of a step once the target's token y_all (-1 if nothing exits) and the PDM's own
+// draft pd_all are known; every thread has read what reset_step_sync clears.
+template <typename WT>
+__device__ __forceinline__ void verify_update(const Ctx& C, int y_all, int pd_all, int step_err, int forced_override,
+                                              int auto_rb) {
   __shared__ int s_tok, s_pos;
   DevState* st = C.st;
-  const int y_all = (st->a == C.n) ? (COH ? take_head_dev(C.b[0], C.V) : take_head(C.b[0], C.V)) : -1;
-  const int pd_all = COH ? take_head_dev(C.b[1], C.V) : take_head(C.b[1], C.V);
-  const int step_err = C.plan.sync != nullptr ? C.plan.sync[sync_err()] : 0;
-  __syncthreads();  // every thread has read the argmax keys and the timeout flag
   reset_step_sync(C);
   if (threadIdx.x == 0) {
     if (step_err) st->err = 1;
@@ -1056,6 +1063,19 @@ __device__ __forceinline__ void verify_body(const Ctx& C, int forced_override, i
   }
 }
 
+// Greedy streaming verification (Section 3.4) and the pipeline state update; single workgroup,
+// last kernel of a step.
+// COH: the argmax keys were written by other workgroups of the same launch.
+template <typename WT, bool COH = false>
+__device__ __forceinline__ void verify_body(const Ctx& C, int forced_override, int auto_rb) {
+  DevState* st = C.st;
+  const int y_all = (st->a == C.n) ? (COH ? take_head_dev(C.b[0], C.V) : take_head(C.b[0], C.V)) : -1;
+  const int pd_all = COH ? take_head_dev(C.b[1], C.V) : take_head(C.b[1], C.V);
+  const int step_err = C.plan.sync != nullptr ? C.plan.sync[sync_err()] : 0;
+  __syncthreads();  // every thread has read the argmax keys and the timeout flag
+  verify_update<WT>(C, y_all, pd_all, step_err, forced_override, auto_rb);
+}
+
 template <typename WT>
 __global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int auto_rb) {
   ktrace_start(C, ktrace_extra(C, KT_VERIFY), blockIdx.x == 0 && blockIdx.y == 0);
@@ -1086,6 +1106,104 @@ __global__ __launch_bounds__(kWG) void k_head_verify(Ctx C, int forced_override,
   if (!s_last) return;
   ktrace_start(C, ktrace_extra(C, KT_VERIFY), true);
   verify_body<WT, true>(C, forced_override, auto_rb);
+  if (threadIdx.x == 0) __hip_atomic_store(&C.st->head_ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  ktrace_end(C, ktrace_extra(C, KT_VERIFY));
+}
+
+// Sampled decoding (Section 3.4 under sampling, Section 4.1's top-k setting): one workgroup, after
+// select_top_k has filled S for the PDM row (and the exit row when a == n). The draft is drawn from
+// the PDM's distribution q with the draft position's u_draft (a forced draft has q = delta) and q is
+// kept with the token; the exit's distribution p judges the successor: it is kept iff
+// u_accept * q(x) < p(x), else the token is drawn from max(0, p - q) (from p if that has no mass)
+// with u_resample. Then the ordinary state update runs with that token as the target's.
+template <typename WT>
+__device__ __forceinline__ void sampled_verify(const Ctx& C, SelLds& S, int kq, int kp, int forced_override,
+                                               int auto_rb) {
+  DevState* st = C.st;
+  const int step_err = C.plan.sync != nullptr ? C.plan.sync[sync_err()] : 0;
+  if (threadIdx.x == 0) {
+    const int c = st->c, a = st->a, n = C.n;
+    const float* u = C.sam.u;
+    const int dpos = c + a;
+    int fd = forced_override;
+    if (fd < 0 && dpos < C.max_tokens) fd = C.forced[dpos];
+    const int pd = S.ids[1][dpos < C.max_tokens ? draw_index(S.p[1], kq, u[3 * dpos + 0]) : 0];
+    const int draft = fd >= 0 ? fd : pd;
+    {
+      const int r = dpos % n;
+      int* qi = C.sam.q_ids + (size_t)r * kMaxTopK;
+      float* qp = C.sam.q_p + (size_t)r * kMaxTopK;
+      if (fd >= 0) {
+        qi[0] = fd;
+        qp[0] = 1.0f;
+        C.sam.q_cnt[r] = 1;
+      } else {
+        for (int j = 0; j < kq; j++) {
+          qi[j] = S.ids[1][j];
+          qp[j] = S.p[1][j];
+        }
+        C.sam.q_cnt[r] = kq;
+      }
+    }
+    int y = -1;
+    if (a == n) {
+      const int succ = n >= 2 ? C.tok[c + 1] : draft;
+      const int r = (c + 1) % n;  // n == 1: the slot just written
+      const int* qi = C.sam.q_ids + (size_t)r * kMaxTopK;
+      const float* qp = C.sam.q_p + (size_t)r * kMaxTopK;
+      const int qn = C.sam.q_cnt[r];
+      const float px = prob_in(S.ids[0], S.p[0], kp, succ), qx = prob_in(qi, qp, qn, succ);
+      if (u[3 * (c + 1) + 1] * qx < px) {
+        y = succ;
+      } else {
+        float mass = 0.f;
+        for (int j = 0; j < kp; j++) mass += fmaxf(0.f, S.p[0][j] - prob_in(qi, qp, qn, S.ids[0][j]));
+        if (mass > 0.f)
+          for (int j = 0; j < kp; j++) S.p[0][j] = fmaxf(0.f, S.p[0][j] - prob_in(qi, qp, qn, S.ids[0][j]));
+        y = S.ids[0][draw_index(S.p[0], kp, u[3 * (c + 1) + 2])];
+      }
+    }
+    S.out[0] = y;
+    S.out[1] = pd;
+  }
+  __syncthreads();
+  const int y = S.out[0], pd = S.out[1];
+  __syncthreads();
+  verify_update<WT>(C, y, pd, step_err, forced_override, auto_rb);
+}
+
+// The sampled LM head: head_body with the logits kept, then (last workgroup, as in k_head_verify)
+// the top-k selection and the step's sampled verify (NV 2, src 3) or the prefill draw (NV 1, src 2:
+// the token at position pos goes to the argmax key of set 0, which the reseed reads).
+template <typename WT, int NV>
+__global__ __launch_bounds__(kWG) void k_head_sample(Ctx C, int src, int row, int pos, int forced_override,
+                                                     int auto_rb) {
+  extern __shared__ __align__(16) float lds[];
+  __shared__ int s_last;
+  ktrace_start(C, ktrace_extra(C, KT_HEAD), blockIdx.x == 0);
+  head_body<WT, NV, true>(C, src, row);
+  wait_own_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int t = __hip_atomic_fetch_add(&C.st->head_ticket, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (t == (int)gridDim.x - 1);
+  }
+  __syncthreads();
+  ktrace_end(C, ktrace_extra(C, KT_HEAD));
+  if (!s_last) return;
+  ktrace_start(C, ktrace_extra(C, KT_VERIFY), true);
+  SelLds& S = *reinterpret_cast<SelLds*>(lds);  // the staged rows are no longer needed
+  if (NV == 2) {
+    const int kq = select_top_k(C, 1, S);
+    const int kp = C.st->a == C.n ? select_top_k(C, 0, S) : 0;
+    sampled_verify<WT>(C, S, kq, kp, forced_override, auto_rb);
+  } else {
+    const int k = select_top_k(C, 0, S);
+    if (threadIdx.x == 0) {
+      const int x = S.ids[0][draw_index(S.p[0], k, C.sam.u[3 * pos + 2])];
+      __hip_atomic_store(C.b[0].hkey, argmax_key(0.0f, x), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
   if (threadIdx.x == 0) __hip_atomic_store(&C.st->head_ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   ktrace_end(C, ktrace_extra(C, KT_VERIFY));
 }
@@ -1348,6 +1466,25 @@ void Launch<WT>::head_verify(const Ctx& c, int forced_override, int auto_rb, voi
   const int res = resident_wgs((const void*)k_head_verify<WT>, shm);
   const dim3 grid(std::max(std::min(stream_grid(c, (c.V + 1) / 2, 1), res), 1));
   launch_timed((k_head_verify<WT>), grid, dim3(kWG), shm, S(s), c, forced_override, auto_rb);
+}
+
+template <typename WT>
+void Launch<WT>::head_sample(const Ctx& c, int src, int row, int pos, int forced_override, int auto_rb, void* s) {
+  // dynamic LDS: the staged rows during the pass, the selection's state afterwards
+  constexpr int BLK = 64 * Elt<WT>::VE;
+  const size_t kl_pad = (size_t)(c.d + BLK - 1) / BLK * BLK;
+  const int np = (c.V + 1) / 2;
+  if (src == 3) {
+    const size_t shm = std::max(2 * kl_pad * sizeof(float), sizeof(SelLds));
+    const int res = resident_wgs((const void*)k_head_sample<WT, 2>, shm);
+    const dim3 grid(std::max(std::min({stream_grid(c, np, 1), res, kSampleWGs}), 1));
+    launch_timed((k_head_sample<WT, 2>), grid, dim3(kWG), shm, S(s), c, src, row, pos, forced_override, auto_rb);
+  } else {
+    const size_t shm = std::max(kl_pad * sizeof(float), sizeof(SelLds));
+    const int res = resident_wgs((const void*)k_head_sample<WT, 1>, shm);
+    const dim3 grid(std::max(std::min({stream_grid(c, np, 1), res, kSampleWGs}), 1));
+    launch_timed((k_head_sample<WT, 1>), grid, dim3(kWG), shm, S(s), c, src, row, pos, forced_override, auto_rb);
+  }
 }
 
 template <typename WT>

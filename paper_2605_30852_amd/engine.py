@@ -161,6 +161,9 @@ class Engine:
     def spd_set_pdm_placement(self, place: int) -> None:
         B.spd_set_pdm_placement(self.h, place)
 
+    def spd_set_sampling(self, top_k: int, temperature: float = 1.0, uniforms=None) -> None:
+        B.spd_set_sampling(self.h, top_k, temperature, uniforms)
+
     def spd_set_pdm_grid(self, wgs: int) -> None:
         B.spd_set_pdm_grid(self.h, wgs)
 
@@ -183,6 +186,16 @@ class Engine:
 
     def pdm_logits(self) -> np.ndarray:
         return B.spd_read_debug(self.h, B.SPD_DBG_PDM_LOGITS, self.shape.vocab)
+
+    def qdist(self, pos: int):
+        """Sampled decoding: (ids, probs) of the draft distribution kept for in-flight position pos."""
+        n, K = self.n, B.MAX_TOP_K
+        raw = B.spd_read_debug(self.h, B.SPD_DBG_QDIST, n * (1 + 2 * K), np.int32)
+        r = pos % n
+        cnt = int(raw[r])
+        ids = raw[n:n + n * K].reshape(n, K)[r, :cnt].astype(np.int64)
+        probs = raw[n + n * K:].view(np.float32).reshape(n, K)[r, :cnt].astype(np.float64)
+        return ids, probs
 
     def tokens(self) -> np.ndarray:
         return B.spd_read_debug(self.h, B.SPD_DBG_TOKENS, self.cfg.max_tokens, np.int32)
