@@ -374,6 +374,11 @@ def main():
     log(f"[bench] p={p}: alpha={alpha:.3f}, {spd_tok_s:.0f} tok/s (AR {ar_tok_s:.0f} tok/s)")
     eng.close()
 
+    sampled = None
+    if fused:
+        sampled = sampled_phase(args, sh, weights, prompt, ref, first, mask, max_tokens, attn_chunk, K, W, n,
+                                us_step, kernels.get("head"))
+
     # achievable HBM read bandwidth for context: a plain 16-byte non-temporal streaming read of 1 GiB
     # (past the 256 MB last-level cache), through the library's probe kernel
     pbuf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
@@ -448,9 +453,86 @@ def main():
         "hbm_read_probe": probe,
         "tokens_per_s": {"spd_forced_p": p, "alpha": round(alpha, 4), "spd": round(spd_tok_s, 1),
                          "ar_same_gpu": round(ar_tok_s, 1)},
+        "sampled": sampled,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def sampled_phase(args, sh, weights, prompt, ref, first, mask, max_tokens, attn_chunk, K, W, n, greedy_us,
+                  greedy_head):
+    """Sampled decoding at top-k 50, temperature 1 (the paper's sampling setting). With u_accept = 0 a
+    judged draft is kept iff the target gives it mass, and with u_resample = 0 a draw takes the most
+    likely token, so with the drafts forced to the greedy tokens every step keeps its draft and the
+    stream is greedy decoding's while every step still runs the top-50 selection of both rows, the
+    draws and the rejection-sampling verify. Then the Bernoulli(p) draft pattern: a wrong draft (a
+    token outside the top 50) is rejected and the residual draw commits the greedy token."""
+    import numpy as np
+    import torch
+
+    from paper_2605_30852_amd import binding as B
+    from paper_2605_30852_amd.engine import Engine
+
+    P = len(prompt)
+    top_k, temp = 50, 1.0
+    U = np.random.default_rng([args.seed, 4]).random((max_tokens, 3))
+    U[:, 1] = 0.0
+    U[:, 2] = 0.0
+    sam = Engine(weights, max_tokens=max_tokens, n=n, attn_chunk=attn_chunk, fused_head=True)
+    sam.spd_set_step_kernel(args.step_mode, args.step_grid, args.stage_groups if args.step_mode == 2 else -1)
+    sam.spd_set_pdm_placement(args.pdm_place)
+    sam.spd_set_pdm_grid(args.pdm_grid)
+    sam.spd_set_sampling(top_k, temp, U)
+    sam.spd_set_graph(not args.no_graph)
+    assert sam.spd_prefill(prompt) == first, "the first sampled token at u = 0 is not the greedy token"
+    sam.spd_set_forced_drafts(ref.astype(np.int32), P)
+    sam.spd_run_steps(W)
+    c0, a0, _, _ = sam.state()
+    assert a0 == n, "sampled pipeline not full after warm-up"
+    torch.cuda.synchronize()
+    ts = time.perf_counter()
+    sam.spd_run_steps(K)
+    sam.spd_sync()
+    el = time.perf_counter() - ts
+    c1, a1, _, _ = sam.state()
+    assert c1 - c0 == K and a1 == n, "sampled forced-accept run left the steady state"
+    toks = sam.tokens()[P: c1 + 1]
+    assert np.array_equal(toks, ref[: len(toks)]), "sampled stream at u = 0 differs from greedy decoding"
+    us = 1e6 * el / K
+    B.spd_set_kernel_timing(sam.h, B.SPD_K_HEAD, 0)
+    sam.spd_run_steps(16)
+    sam.spd_sync()
+    ms, nl = B.spd_kernel_timing(sam.h)
+    B.spd_set_kernel_timing(sam.h, 0)
+    head_us = 1e3 * ms / max(1, nl)
+    # Bernoulli(p) draft pattern
+    sam.spd_rollback(P, int(first))
+    table = np.full(len(ref), -1, dtype=np.int32)
+    for i in range(1, len(ref)):
+        table[i] = ref[i] if mask[P + i] else (ref[i] + 1) % sh.vocab
+    sam.spd_clear_forced_drafts()
+    sam.spd_set_forced_drafts(table, P)
+    torch.cuda.synchronize()
+    ts = time.perf_counter()
+    logp = sam.spd_run_steps(K, want_log=True)
+    elp = time.perf_counter() - ts
+    committed = logp[-1]["committed_len"] - P
+    agree = sum(1 for r in logp if r["decision"] != B.SPD_NONE
+                and r["decision"] == (B.SPD_ACCEPT if mask[r["verified_pos"]] else B.SPD_REJECT))
+    exits = sum(1 for r in logp if r["decision"] != B.SPD_NONE)
+    sam.close()
+    out = {"top_k": top_k, "temperature": temp, "us_per_step": round(us, 1),
+           "over_greedy_us": round(us - greedy_us, 1),
+           "head_verify_us_per_launch": round(head_us, 2),
+           "greedy_head_verify_us_per_launch": greedy_head["us_per_launch"] if greedy_head else None,
+           "p_run": {"alpha": round(committed / K, 4), "tok_s": round(committed / elp, 1),
+                     "decisions_matching_mask": f"{agree}/{exits}"},
+           "uniforms": "u_accept = u_resample = 0 (keep iff the target gives mass; draws take the most likely "
+                       "token); u_draft seeded uniform"}
+    log(f"[bench] sampled top-{top_k} T={temp}: {us:.1f} us/step ({us - greedy_us:+.1f} over greedy), "
+        f"head+verify {head_us:.1f} us/launch; p-run alpha {committed / K:.3f}, {committed / elp:.0f} tok/s, "
+        f"decisions matching the mask {agree}/{exits}")
+    return out
 
 
 def traffic_from_profile(dominant):

@@ -595,9 +595,11 @@ __global__ __launch_bounds__(kWG) void k_pdm_fc(Ctx C, int prefill, int nrows_ar
 // to the argmax key of set 0 (target) or set 1 (PDM) as an order-independent maximum.
 // SAMP: sampled decoding; every logit also goes to the wave's region of C.sam.wlog and the
 // workgroup's best key per row to C.sam.wgmax (device-scope stores, read by the launch's last
-// workgroup).
+// workgroup). The logits gather in LDS after the staged rows (lcap floats per wave and row) while
+// the vocabulary streams, and each wave writes its region out once at the end, so that no store
+// sits between the weight loads; a region over lcap floats is stored as it is produced.
 template <typename WT, int NV, bool SAMP = false>
-__device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
+__device__ __forceinline__ void head_body(const Ctx& C, int src, int row, int lcap = 0) {
   extern __shared__ __align__(16) float lds[];
   __shared__ float red[4];
   __shared__ float s_v[NV][4];
@@ -657,6 +659,8 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
   }
   const bool dbg_row0 = C.debug && (src != 0 && src != 3 ? true : a == C.n);
   const int cmax = 2 * ((npairs + NW - 1) / NW);  // SAMP: floats per wave region
+  const bool lbuf = SAMP && cmax <= lcap;
+  float* lg = lds + (size_t)NV * ldsK + (size_t)w * NV * lcap;  // lbuf: [NV][lcap] of this wave
   // every lane holds the same sums, so every lane keeps the same running maximum
   auto done = [&](int i, const float (&s0)[NV], const float (&s1)[NV]) {
     const int m = 2 * (wv + i * NW);
@@ -665,9 +669,13 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
       const float l0 = s0[v] * scl[v], l1 = s1[v] * scl[v];
       if (C.debug && (v > 0 || dbg_row0) && lane < 2 && m + lane < V)
         C.dbg_logits[(size_t)set[v] * V + m + lane] = lane == 0 ? l0 : l1;
-      if (SAMP && lane < 2 && m + lane < V)
-        st_dev(C.sam.wlog + (size_t)set[v] * C.sam.wlog_stride + (size_t)wv * cmax + 2 * i + lane,
-               lane == 0 ? l0 : l1);
+      if (SAMP && lane < 2 && m + lane < V) {
+        if (lbuf)
+          lg[v * lcap + 2 * i + lane] = lane == 0 ? l0 : l1;
+        else
+          st_dev(C.sam.wlog + (size_t)set[v] * C.sam.wlog_stride + (size_t)wv * cmax + 2 * i + lane,
+                 lane == 0 ? l0 : l1);
+      }
       if (m < V && better(l0, m, bv[v], bi[v])) {
         bv[v] = l0;
         bi[v] = m;
@@ -679,6 +687,13 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row) {
     }
   };
   rstream_run<WT, NV>(rowptr, done, count, d, lane, lds, ldsK, NV, bA, bB);
+  if (lbuf) {  // the wave reads back only what its own lanes wrote (in order within the wave)
+#pragma unroll
+    for (int v = 0; v < NV; v++)
+      for (int e = lane; e < 2 * count; e += 64)
+        if (2 * (wv + (e >> 1) * NW) + (e & 1) < V)
+          st_dev(C.sam.wlog + (size_t)set[v] * C.sam.wlog_stride + (size_t)wv * cmax + e, lg[v * lcap + e]);
+  }
   if (lane == 0) {
 #pragma unroll
     for (int v = 0; v < NV; v++) {
@@ -1115,56 +1130,95 @@ __global__ __launch_bounds__(kWG) void k_head_verify(Ctx C, int forced_override,
 // the PDM's distribution q with the draft position's u_draft (a forced draft has q = delta) and q is
 // kept with the token; the exit's distribution p judges the successor: it is kept iff
 // u_accept * q(x) < p(x), else the token is drawn from max(0, p - q) (from p if that has no mass)
-// with u_resample. Then the ordinary state update runs with that token as the target's.
+// with u_resample. Then the ordinary state update runs with that token as the target's. The lookups
+// run on wave 0, one distribution entry per lane (k <= 64); the inverse-CDF draws on its lane 0.
 template <typename WT>
 __device__ __forceinline__ void sampled_verify(const Ctx& C, SelLds& S, int kq, int kp, int forced_override,
                                                int auto_rb) {
   DevState* st = C.st;
   const int step_err = C.plan.sync != nullptr ? C.plan.sync[sync_err()] : 0;
-  if (threadIdx.x == 0) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
     const int c = st->c, a = st->a, n = C.n;
     const float* u = C.sam.u;
     const int dpos = c + a;
     int fd = forced_override;
     if (fd < 0 && dpos < C.max_tokens) fd = C.forced[dpos];
-    const int pd = S.ids[1][dpos < C.max_tokens ? draw_index(S.p[1], kq, u[3 * dpos + 0]) : 0];
+    int pd = S.ids[1][0];
+    if (lane == 0 && dpos < C.max_tokens) pd = S.ids[1][draw_index(S.p[1], kq, u[3 * dpos + 0])];
+    pd = __shfl(pd, 0, 64);
     const int draft = fd >= 0 ? fd : pd;
-    {
+    // the judged token's q: the slot of position c + 1 (n == 1: the distribution just drawn from)
+    int qn = 0;
+    if (a == n) {
+      if (n >= 2) {
+        const int r = (c + 1) % n;
+        qn = C.sam.q_cnt[r];
+        if (lane < qn) {
+          S.qj_ids[lane] = C.sam.q_ids[(size_t)r * kMaxTopK + lane];
+          S.qj_p[lane] = C.sam.q_p[(size_t)r * kMaxTopK + lane];
+        }
+      } else if (fd >= 0) {
+        qn = 1;
+        if (lane == 0) {
+          S.qj_ids[0] = fd;
+          S.qj_p[0] = 1.0f;
+        }
+      } else {
+        qn = kq;
+        if (lane < kq) {
+          S.qj_ids[lane] = S.ids[1][lane];
+          S.qj_p[lane] = S.p[1][lane];
+        }
+      }
+    }
+    {  // keep the new token's q (row dpos mod n; for n >= 2 not the judged row)
       const int r = dpos % n;
       int* qi = C.sam.q_ids + (size_t)r * kMaxTopK;
       float* qp = C.sam.q_p + (size_t)r * kMaxTopK;
       if (fd >= 0) {
-        qi[0] = fd;
-        qp[0] = 1.0f;
-        C.sam.q_cnt[r] = 1;
-      } else {
-        for (int j = 0; j < kq; j++) {
-          qi[j] = S.ids[1][j];
-          qp[j] = S.p[1][j];
+        if (lane == 0) {
+          qi[0] = fd;
+          qp[0] = 1.0f;
+          C.sam.q_cnt[r] = 1;
         }
-        C.sam.q_cnt[r] = kq;
+      } else {
+        if (lane < kq) {
+          qi[lane] = S.ids[1][lane];
+          qp[lane] = S.p[1][lane];
+        }
+        if (lane == 0) C.sam.q_cnt[r] = kq;
       }
     }
+    __builtin_amdgcn_wave_barrier();
     int y = -1;
     if (a == n) {
       const int succ = n >= 2 ? C.tok[c + 1] : draft;
-      const int r = (c + 1) % n;  // n == 1: the slot just written
-      const int* qi = C.sam.q_ids + (size_t)r * kMaxTopK;
-      const float* qp = C.sam.q_p + (size_t)r * kMaxTopK;
-      const int qn = C.sam.q_cnt[r];
-      const float px = prob_in(S.ids[0], S.p[0], kp, succ), qx = prob_in(qi, qp, qn, succ);
+      const unsigned long long mp = __ballot(lane < kp && S.ids[0][lane] == succ);
+      const unsigned long long mq = __ballot(lane < qn && S.qj_ids[lane] == succ);
+      const float px = mp ? S.p[0][__ffsll((long long)mp) - 1] : 0.f;
+      const float qx = mq ? S.qj_p[__ffsll((long long)mq) - 1] : 0.f;
       if (u[3 * (c + 1) + 1] * qx < px) {
         y = succ;
       } else {
-        float mass = 0.f;
-        for (int j = 0; j < kp; j++) mass += fmaxf(0.f, S.p[0][j] - prob_in(qi, qp, qn, S.ids[0][j]));
-        if (mass > 0.f)
-          for (int j = 0; j < kp; j++) S.p[0][j] = fmaxf(0.f, S.p[0][j] - prob_in(qi, qp, qn, S.ids[0][j]));
-        y = S.ids[0][draw_index(S.p[0], kp, u[3 * (c + 1) + 2])];
+        float res = 0.f;
+        if (lane < kp) {
+          const int id = S.ids[0][lane];
+          float qv = 0.f;
+          for (int j = 0; j < qn; j++)
+            if (S.qj_ids[j] == id) qv = S.qj_p[j];
+          res = fmaxf(0.f, S.p[0][lane] - qv);
+        }
+        const float mass = wave_sum(res);
+        if (mass > 0.f && lane < kp) S.p[0][lane] = res;
+        __builtin_amdgcn_wave_barrier();
+        if (lane == 0) y = S.ids[0][draw_index(S.p[0], kp, u[3 * (c + 1) + 2])];
       }
     }
-    S.out[0] = y;
-    S.out[1] = pd;
+    if (lane == 0) {
+      S.out[0] = y;
+      S.out[1] = pd;
+    }
   }
   __syncthreads();
   const int y = S.out[0], pd = S.out[1];
@@ -1177,11 +1231,11 @@ __device__ __forceinline__ void sampled_verify(const Ctx& C, SelLds& S, int kq, 
 // the token at position pos goes to the argmax key of set 0, which the reseed reads).
 template <typename WT, int NV>
 __global__ __launch_bounds__(kWG) void k_head_sample(Ctx C, int src, int row, int pos, int forced_override,
-                                                     int auto_rb) {
+                                                     int auto_rb, int lcap) {
   extern __shared__ __align__(16) float lds[];
   __shared__ int s_last;
   ktrace_start(C, ktrace_extra(C, KT_HEAD), blockIdx.x == 0);
-  head_body<WT, NV, true>(C, src, row);
+  head_body<WT, NV, true>(C, src, row, lcap);
   wait_own_stores();
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -1470,21 +1524,30 @@ void Launch<WT>::head_verify(const Ctx& c, int forced_override, int auto_rb, voi
 
 template <typename WT>
 void Launch<WT>::head_sample(const Ctx& c, int src, int row, int pos, int forced_override, int auto_rb, void* s) {
-  // dynamic LDS: the staged rows during the pass, the selection's state afterwards
+  // dynamic LDS: the staged rows and the waves' logit regions during the pass, the selection's state
+  // afterwards; a smaller grid (fewer resident workgroups) means larger regions, so settle both
   constexpr int BLK = 64 * Elt<WT>::VE;
   const size_t kl_pad = (size_t)(c.d + BLK - 1) / BLK * BLK;
   const int np = (c.V + 1) / 2;
-  if (src == 3) {
-    const size_t shm = std::max(2 * kl_pad * sizeof(float), sizeof(SelLds));
-    const int res = resident_wgs((const void*)k_head_sample<WT, 2>, shm);
-    const dim3 grid(std::max(std::min({stream_grid(c, np, 1), res, kSampleWGs}), 1));
-    launch_timed((k_head_sample<WT, 2>), grid, dim3(kWG), shm, S(s), c, src, row, pos, forced_override, auto_rb);
-  } else {
-    const size_t shm = std::max(kl_pad * sizeof(float), sizeof(SelLds));
-    const int res = resident_wgs((const void*)k_head_sample<WT, 1>, shm);
-    const dim3 grid(std::max(std::min({stream_grid(c, np, 1), res, kSampleWGs}), 1));
-    launch_timed((k_head_sample<WT, 1>), grid, dim3(kWG), shm, S(s), c, src, row, pos, forced_override, auto_rb);
+  const int nv = src == 3 ? 2 : 1;
+  const void* fn = src == 3 ? (const void*)k_head_sample<WT, 2> : (const void*)k_head_sample<WT, 1>;
+  int grid = std::max(std::min(stream_grid(c, np, 1), kSampleWGs), 1);
+  int lcap = 0;
+  size_t shm = 0;
+  for (int it = 0; it < 4; it++) {
+    lcap = 2 * ((np + 4 * grid - 1) / (4 * grid));
+    shm = std::max(((size_t)nv * kl_pad + (size_t)nv * 4 * lcap) * sizeof(float), sizeof(SelLds));
+    const int res = resident_wgs(fn, shm);
+    if (res >= grid) break;
+    grid = std::max(res, 1);
   }
+  // lcap is the region each launch's wave needs; the kernel stores directly if its region exceeds it
+  if (src == 3)
+    launch_timed((k_head_sample<WT, 2>), dim3(grid), dim3(kWG), shm, S(s), c, src, row, pos, forced_override,
+                 auto_rb, lcap);
+  else
+    launch_timed((k_head_sample<WT, 1>), dim3(grid), dim3(kWG), shm, S(s), c, src, row, pos, forced_override,
+                 auto_rb, lcap);
 }
 
 template <typename WT>

@@ -5,25 +5,33 @@
 // Selection runs in the last workgroup of the launch. Keys are the 64-bit argmax keys (logit
 // descending, then index ascending), so every key is distinct and "the k largest keys" is exactly
 // the top-k with ties broken towards the lower index. Each workgroup of the head left its best key
-// per row; the k-th largest of those maxima, t_lo, is a lower bound of the k-th largest logit key
-// overall (k workgroups each hold a key >= t_lo). Only workgroups whose maximum reaches t_lo can
-// hold a top-k key, and only their entries >= t_lo are candidates: typically little more than k.
-// A radix select (8-bit digits, most significant first) finds the k-th largest candidate key T, and
-// the k keys >= T are sorted by rank.
+// per row; each thread takes the largest of up to four of those maxima, and the k-th largest of the
+// threads' values, t_lo, is a lower bound of the k-th largest logit key overall (k threads each saw
+// a distinct key >= t_lo). Only workgroups whose maximum reaches t_lo can hold a top-k key, and only
+// their entries >= t_lo are candidates: typically little more than k. Each candidate's rank is the
+// number of candidates above it, so the top-k land in rank order with no further passes. (Over
+// kSelCap candidates a radix select over memory, 8-bit digits most significant first, finds the
+// k-th largest key instead.)
 #pragma once
 #include "spd_dev.h"
 #include "spd_devfn.h"
 
 namespace spd {
 
+static_assert(kSampleWGs % kWG == 0 && kSampleWGs / kWG <= 4, "workgroup maxima per selection thread");
+
 struct SelLds {
   unsigned long long keys[kSelCap];  // workgroup maxima, then candidates
   unsigned long long top[kMaxTopK];
+  unsigned long long gmax[kWG];      // each thread's largest workgroup maximum
   int sel[kSampleWGs];               // workgroups whose maximum reaches t_lo
   unsigned hist[256];
   int misc[4];
+  unsigned long long tlo;
   int ids[2][kMaxTopK];              // [0]: target row, [1]: PDM row (value-descending order)
   float p[2][kMaxTopK];
+  int qj_ids[kMaxTopK];              // the draft distribution of the token being judged
+  float qj_p[kMaxTopK];
   int out[2];
 };
 
@@ -90,22 +98,46 @@ __device__ unsigned long long select_kth(Visit visit, int k, SelLds& S) {
 }
 
 // Every logit key of row `set` in the regions of the workgroups listed in S.sel[0..nsel) that is
-// >= tlo, handed to f (each thread its share). The region geometry is the head's (see Sampler).
+// >= tlo, handed to f (each thread its share). The region geometry is the head's (see Sampler): a
+// workgroup's four wave regions are consecutive, 4 * cmax floats (cmax even), so the entries go as
+// 8-byte pairs, eight device-scope loads in flight per thread before any is looked at.
 template <typename F>
 __device__ void visit_regions(const Ctx& C, int set, const SelLds& S, int nsel, unsigned long long tlo, F f) {
   const int V = C.V, NW = (int)gridDim.x * 4, npairs = (V + 1) / 2;
   const int cmax = 2 * ((npairs + NW - 1) / NW);
-  const int per = 4 * cmax;
-  const int total = nsel * per;
-  const float* base = C.sam.wlog + (size_t)set * C.sam.wlog_stride;
-  for (int e = threadIdx.x; e < total; e += kWG) {
-    const int off = e % per;
-    const int wv = S.sel[e / per] * 4 + off / cmax, i = off % cmax;
-    const int cnt = wv < npairs ? (npairs - 1 - wv) / NW + 1 : 0;
-    const int m = 2 * (wv + (i >> 1) * NW) + (i & 1);
-    if (i >= 2 * cnt || m >= V) continue;
-    const unsigned long long key = argmax_key(ld_dev(base + (size_t)wv * cmax + i), m);
-    if (key >= tlo) f(key);
+  const int per2 = 2 * cmax;  // pairs per workgroup
+  const int total = nsel * per2;
+  const unsigned long long* base =
+      reinterpret_cast<const unsigned long long*>(C.sam.wlog + (size_t)set * C.sam.wlog_stride);
+  constexpr int kB = 8;
+  for (int e0 = threadIdx.x; e0 < total; e0 += kB * kWG) {
+    unsigned long long raw[kB];
+    int wg[kB], off[kB];
+#pragma unroll
+    for (int j = 0; j < kB; j++) {
+      const int e = e0 + j * kWG;
+      raw[j] = 0ull;
+      wg[j] = -1;
+      if (e < total) {
+        wg[j] = S.sel[e / per2];
+        off[j] = e % per2;
+        raw[j] = ld_dev_u64(base + (size_t)wg[j] * per2 + off[j]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kB; j++) {
+      if (wg[j] < 0) continue;
+      const int wv = wg[j] * 4 + (2 * off[j]) / cmax, i = (2 * off[j]) % cmax;  // i even
+      const int cnt = wv < npairs ? (npairs - 1 - wv) / NW + 1 : 0;
+      if (i >= 2 * cnt) continue;
+      const int m = 2 * (wv + (i >> 1) * NW);
+      const unsigned long long k0 = argmax_key(__uint_as_float((uint32_t)raw[j]), m);
+      if (m < V && k0 >= tlo) f(k0);
+      if (m + 1 < V) {
+        const unsigned long long k1 = argmax_key(__uint_as_float((uint32_t)(raw[j] >> 32)), m + 1);
+        if (k1 >= tlo) f(k1);
+      }
+    }
   }
 }
 
@@ -113,20 +145,37 @@ __device__ void visit_regions(const Ctx& C, int set, const SelLds& S, int nsel, 
 // V) largest logits, value descending (lower index first among equal values), and their softmax at
 // temperature 1/inv_temp (max-subtracted, fp32). Whole workgroup; returns k.
 __device__ int select_top_k(const Ctx& C, int set, SelLds& S) {
-  const int tid = threadIdx.x, G = (int)gridDim.x, V = C.V;
+  const int tid = threadIdx.x, lane = tid & 63, G = (int)gridDim.x, V = C.V;
   const int k = min(C.sam.top_k, V);
-  for (int i = tid; i < G; i += kWG) S.keys[i] = ld_dev_u64(C.sam.wgmax + (size_t)set * kSampleWGs + i);
-  __syncthreads();
-  unsigned long long tlo = 1ull;  // every real key is >= 1
-  if (G >= k) {
-    const unsigned long long t = select_kth([&](auto f) { for (int i = tid; i < G; i += kWG) f(S.keys[i]); }, k, S);
-    tlo = t > 1ull ? t : 1ull;
+  unsigned long long gm = 0ull;  // G <= kSampleWGs = 4 * kWG: at most four maxima per thread
+  {
+    unsigned long long x[kSampleWGs / kWG];
+#pragma unroll
+    for (int j = 0; j < kSampleWGs / kWG; j++) {
+      const int i = tid + j * kWG;
+      x[j] = i < G ? ld_dev_u64(C.sam.wgmax + (size_t)set * kSampleWGs + i) : 0ull;
+    }
+#pragma unroll
+    for (int j = 0; j < kSampleWGs / kWG; j++) {
+      const int i = tid + j * kWG;
+      if (i < G) S.keys[i] = x[j];
+      gm = x[j] > gm ? x[j] : gm;
+    }
   }
+  S.gmax[tid] = gm;
   if (tid == 0) {
     S.misc[2] = 0;
     S.misc[3] = 0;
+    S.tlo = 1ull;  // every real key is >= 1; stays if fewer than k threads saw a key
   }
   __syncthreads();
+  if (gm != 0ull) {  // nonzero values are distinct keys of different vocabulary rows
+    int r = 0;
+    for (int j = 0; j < kWG; j++) r += S.gmax[j] > gm;
+    if (r == k - 1) S.tlo = gm;
+  }
+  __syncthreads();
+  const unsigned long long tlo = S.tlo;
   for (int i = tid; i < G; i += kWG)
     if (S.keys[i] >= tlo) S.sel[atomicAdd(&S.misc[2], 1)] = i;
   __syncthreads();
@@ -136,45 +185,43 @@ __device__ int select_top_k(const Ctx& C, int set, SelLds& S) {
     if (at < kSelCap) S.keys[at] = key;
   });
   __syncthreads();
-  const int ncand = S.misc[3];
-  const bool in_lds = ncand <= kSelCap;
-  auto cands = [&](auto f) {
-    if (in_lds) {
-      for (int i = tid; i < ncand; i += kWG) f(S.keys[i]);
-    } else {
-      visit_regions(C, set, S, nsel, tlo, f);
+  const int ncand = S.misc[3];  // >= k: every top-k key is a candidate
+  if (ncand <= kSelCap) {
+    for (int i = tid; i < ncand; i += kWG) {
+      const unsigned long long x = S.keys[i];
+      int r = 0;
+      for (int j = 0; j < ncand; j++) r += S.keys[j] > x;
+      if (r < k) {
+        S.ids[set][r] = argmax_index(x, V);
+        S.p[set][r] = key_value(x);
+      }
     }
-  };
-  const unsigned long long T = select_kth(cands, k, S);
-  if (tid == 0) S.misc[2] = 0;
-  __syncthreads();
-  cands([&](unsigned long long key) {
-    if (key >= T) {
-      const int at = atomicAdd(&S.misc[2], 1);
-      if (at < kMaxTopK) S.top[at] = key;
+  } else {
+    const unsigned long long T =
+        select_kth([&](auto f) { visit_regions(C, set, S, nsel, tlo, f); }, k, S);
+    if (tid == 0) S.misc[2] = 0;
+    __syncthreads();
+    visit_regions(C, set, S, nsel, tlo, [&](unsigned long long key) {
+      if (key >= T) {
+        const int at = atomicAdd(&S.misc[2], 1);
+        if (at < kMaxTopK) S.top[at] = key;
+      }
+    });
+    __syncthreads();
+    if (tid < k) {  // exactly k distinct keys are >= T
+      const unsigned long long x = S.top[tid];
+      int r = 0;
+      for (int j = 0; j < k; j++) r += S.top[j] > x;
+      S.ids[set][r] = argmax_index(x, V);
+      S.p[set][r] = key_value(x);
     }
-  });
-  __syncthreads();
-  // exactly k distinct keys are >= T; each one's rank is its place in value-descending order
-  unsigned long long mine = 0ull;
-  int rank = 0;
-  if (tid < k) {
-    mine = S.top[tid];
-    for (int j = 0; j < k; j++) rank += S.top[j] > mine;
-    S.ids[set][rank] = argmax_index(mine, V);
-    S.p[set][rank] = key_value(mine);
   }
   __syncthreads();
-  const float top = S.p[set][0];
-  const float w = tid < k ? expf((S.p[set][tid] - top) * C.sam.inv_temp) : 0.f;
-  __syncthreads();
-  if (tid < k) S.p[set][tid] = w;
-  __syncthreads();
-  if (tid == 0) {
-    float sum = 0.f;
-    for (int j = 0; j < k; j++) sum += S.p[set][j];
-    const float inv = 1.0f / sum;
-    for (int j = 0; j < k; j++) S.p[set][j] *= inv;
+  if (tid < 64) {  // k <= 64: one wave
+    const float top = S.p[set][0];
+    const float w = lane < k ? expf((S.p[set][lane] - top) * C.sam.inv_temp) : 0.f;
+    const float inv = 1.0f / wave_sum(w);
+    if (lane < k) S.p[set][lane] = w * inv;
   }
   __syncthreads();
   return k;
@@ -192,12 +239,6 @@ __device__ __forceinline__ int draw_index(const float* w, int m, float u) {
     if (t < cs) return i;
   }
   return m - 1;
-}
-
-__device__ __forceinline__ float prob_in(const int* ids, const float* p, int m, int tok) {
-  for (int j = 0; j < m; j++)
-    if (ids[j] == tok) return p[j];
-  return 0.f;
 }
 
 }  // namespace spd
