@@ -30,6 +30,10 @@ What it follows:
     is kept with the in-flight token; the exit's top-k distribution p judges the successor by
     rejection sampling with the successor's u_accept / u_resample, and a reject reseeds the residual
     draw. A forced draft carries q = delta. The prompt's first token is drawn from p with u_resample.
+  * Post-step schedule (the ablation of Section 4.4 against Section 3.3's pre-step choice): the PDM
+    waits for the stage compute and reads the post-step features, every in-flight token one stage
+    deeper (the newest contributes g^1 instead of g^0); drafting is then serial behind the step.
+    Everything else (rows rewritten, the draft's position, verify) is as in the pre-step schedule.
 """
 from __future__ import annotations
 
@@ -86,7 +90,9 @@ class SPDOracle:
     """SPD state for one sequence: target KV per layer, PDM KV per PDM layer, in-flight tokens."""
 
     def __init__(self, model: Model, n: Optional[int] = None, pdm_layers: Optional[int] = None,
-                 sampling: Optional[smp.Sampling] = None):
+                 sampling: Optional[smp.Sampling] = None, schedule: str = "pre"):
+        """schedule: "pre" (the PDM reads pre-step features, Section 3.3) or "post" (it reads the
+        features after the step's stage compute)."""
         model = model.for_width(model.shape.n_stages if n is None else n, pdm_layers)
         sh = model.shape
         self.m = model
@@ -108,6 +114,8 @@ class SPDOracle:
         self.verified = 0  # N: prefill token + one per exit
         self.sampling = sampling
         self.qdist: Dict[int, smp.Dist] = {}  # sampled decoding: q of each in-flight token
+        assert schedule in ("pre", "post")
+        self.schedule = schedule
 
     def clone(self) -> "SPDOracle":
         """An independent copy of the decoding state (the model is shared)."""
@@ -194,14 +202,31 @@ class SPDOracle:
         c, a, n = self.c, self.a, self.n
         depths = {q: self.depth(q) for q in range(0, c + a)}
 
-        # --- PDM on pre-step features: rows c..c+a-1 rewritten, rows < c kept
-        for pc in self.pdm_caches:
-            pc.truncate(c)
-        pdm_h = {}
-        for i in range(a):
-            q = c + i
-            g = self.feature(self.anch[q], a - 1 - i)
-            pdm_h[q] = self.pdm_row(g, q)
+        def run_pdm(shift):
+            # rows c..c+a-1 rewritten at depth (pre-step depth + shift), rows < c kept
+            for pc in self.pdm_caches:
+                pc.truncate(c)
+            out = {}
+            for i in range(a):
+                q = c + i
+                out[q] = self.pdm_row(self.feature(self.anch[q], a - 1 - i + shift), q)
+            return out
+
+        def run_target():
+            # the token at depth s runs stage s
+            for i in range(a):
+                q = c + i
+                s = a - 1 - i
+                h, kept = self._run_stage_range(self.hidden[q], q, s, s + 1, capture=True, anchors=self.anch[q])
+                self.hidden[q] = h
+                self.anch[q] = kept
+
+        if self.schedule == "pre":  # the PDM reads only pre-step features (Section 3.3)
+            pdm_h = run_pdm(0)
+            run_target()
+        else:  # post-step: every in-flight token one stage deeper
+            run_target()
+            pdm_h = run_pdm(1)
         pdm_lg = lm_logits(self.m, pdm_h[c + a - 1], "pdm.norm")
         dpos = c + a  # the draft's position
         if self.sampling is None:
@@ -212,14 +237,6 @@ class SPDOracle:
             pdm_draft = smp.sample(qd, self.sampling.u(dpos, smp.U_DRAFT))
         draft = pdm_draft if forced_draft is None else int(forced_draft)
         q_draft = None if qd is None else (qd if forced_draft is None else smp.point_mass(draft))
-
-        # --- target: the token at depth s runs stage s
-        for i in range(a):
-            q = c + i
-            s = a - 1 - i
-            h, kept = self._run_stage_range(self.hidden[q], q, s, s + 1, capture=True, anchors=self.anch[q])
-            self.hidden[q] = h
-            self.anch[q] = kept
 
         self.steps += 1
         res = StepResult(NONE, -1, draft, pdm_draft, -1, -1, -1, 0, 0, depths=depths,
@@ -308,11 +325,11 @@ class SPDOracle:
 
 def run_spd(model: Model, prompt, n_tokens: int, n: Optional[int] = None,
             draft_for: Optional[Callable[[int], Optional[int]]] = None, max_steps: int = 100000,
-            sampling: Optional[smp.Sampling] = None):
+            sampling: Optional[smp.Sampling] = None, schedule: str = "pre"):
     """Run SPD until n_tokens generated tokens are verified. draft_for(position) may force drafts.
 
     Returns (oracle, list of StepResult)."""
-    o = SPDOracle(model, n=n, sampling=sampling)
+    o = SPDOracle(model, n=n, sampling=sampling, schedule=schedule)
     o.prefill(prompt)
     results = []
     while o.verified < n_tokens and len(results) < max_steps:
