@@ -195,7 +195,7 @@ def main():
     esz = 2 if sh.dtype == "bf16" else 4
     K_GU, K_CLS, K_SPAN = 64, 16, 64
     # greedy reference long enough for every forced-accept phase below
-    n_ref = W + K + K_GU + 5 * K_CLS + 3 * K_SPAN + 2 * n + 16
+    n_ref = W + K + K_GU + 5 * K_CLS + 4 * K_SPAN + 2 * n + 24
     # capacity and attention split size depend on the workload only (not on --steps), so that a
     # profiled run with fewer steps launches exactly the kernels the timed run launches
     max_tokens = P + max(1024, n_ref + 4 * n + 64)
@@ -345,6 +345,16 @@ def main():
         t_pdm = 1e3 * pd_alone_ms / na
         spans.update({"step_us_without_pdm": round(t_without, 1), "pdm_alone_us": round(t_pdm, 1),
                       "hidden_fraction": round(1.0 - (us_step - t_without) / t_pdm, 3)})
+        # the post-step schedule (the PDM after the stage compute, on deeper features): serial
+        B.spd_set_pdm_schedule(eng.h, True)
+        eng.spd_run_steps(4)
+        eng.spd_sync()
+        torch.cuda.synchronize()
+        ts = time.perf_counter()
+        eng.spd_run_steps(K_SPAN)
+        eng.spd_sync()
+        spans["post_step_us_per_step"] = round(1e6 * (time.perf_counter() - ts) / K_SPAN, 1)
+        B.spd_set_pdm_schedule(eng.h, False)
         ca, aa, _, _ = eng.state()
         assert aa == n, "PDM hiding measurement left the steady state"
     log(f"[bench] spans: {spans}")

@@ -178,6 +178,14 @@ spd_status spd_clear_forced_drafts(spd_handle* h);
 spd_status spd_set_sampling(spd_handle* h, int32_t top_k, float temperature, const float* uniforms,
                             int32_t positions);
 
+/* Draft-module schedule (Section 3.3's choice against the ablation of Section 4.4). post_step = 0
+ * (default): the PDM reads the pre-step features and runs beside the stage compute. post_step = 1:
+ * it runs after the step's stage compute on main_stream, before the exit head, and reads every
+ * in-flight token one stage deeper (the newest token's anchors 0 and 1 instead of its embedding);
+ * drafting is then serial behind the step. Rows recomputed, the draft's position and the verify are
+ * unchanged. Legal in any state; SPD_E_INVAL for other values. */
+spd_status spd_set_pdm_schedule(spd_handle* h, int32_t post_step);
+
 /* Enqueue `count` steps without host synchronisation (needs auto_rollback = 1). If log is not
  * NULL (host, count entries) the call waits and fills it with each step's result; otherwise it
  * returns once the work is enqueued and spd_sync() waits. */

@@ -340,7 +340,8 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     return pdm_end(s);
   };
   const bool stage_streams = h->step_mode == 2;
-  const int place = !h->pdm_on ? -1 : stage_streams ? h->pdm_place : (h->pdm_place == 1 ? 1 : 0);
+  // post-step schedule: the PDM waits for the stage compute (placement 5, on main_stream after it)
+  const int place = !h->pdm_on ? -1 : C.post_step ? 5 : stage_streams ? h->pdm_place : (h->pdm_place == 1 ? 1 : 0);
   if (place == -1) {  // no PDM launches: the join is satisfied at the fork
     if (sp) HIPC(hipEventRecord(sp[1], h->main));
     HIPC(hipEventRecord(h->ev_join, h->main));
@@ -505,6 +506,11 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
         HIPC(hipStreamWaitEvent(h->main, h->ev_st[gi], 0));
       }
     }
+  }
+  if (place == 5) {  // post-step features: after every stage of this step, before the exit head
+    h->cur_slot = 0;
+    spd_status st = enqueue_pdm(h->main);
+    if (st != SPD_OK) return st;
   }
   h->cur_slot = h->J;
   if (fused) {
@@ -717,6 +723,7 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
     B.cnt = (int32_t*)(ws + lay.cnt[s]);
     B.hkey = (unsigned long long*)(ws + lay.hkey[s]);
   }
+  C.post_step = 0;
   C.sam.top_k = 0;
   C.sam.inv_temp = 1.0f;
   C.sam.u = (const float*)(ws + lay.su);
@@ -885,6 +892,16 @@ spd_status spd_set_sampling(spd_handle* h, int32_t top_k, float temperature, con
   HIPC(hipMemcpy(h->ws + h->lay.su, uniforms, sizeof(float) * 3 * (size_t)positions, hipMemcpyHostToDevice));
   h->ctx.sam.top_k = top_k;
   h->ctx.sam.inv_temp = 1.0f / temperature;
+  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
+  drop_graph(h);  // the captured launches change
+  return SPD_OK;
+}
+
+spd_status spd_set_pdm_schedule(spd_handle* h, int32_t post_step) {
+  if (!h || (post_step != 0 && post_step != 1)) return SPD_E_INVAL;
+  HIPC(hipSetDevice(h->dev));
+  HIPC(hipStreamSynchronize(h->main));
+  h->ctx.post_step = post_step;
   HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
   drop_graph(h);  // the captured launches change
   return SPD_OK;

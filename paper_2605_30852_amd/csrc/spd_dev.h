@@ -157,6 +157,7 @@ struct Ctx {
   int rows_wgs;     // at most this many workgroups per row-block (PDM) GEMV launch (0: no cap)
   int J;            // layer slots per step (longest stage)
   Sampler sam;      // sampled decoding (sam.top_k == 0: greedy)
+  int post_step;    // 1: the PDM reads the features after the step's stage compute (one stage deeper)
 };
 
 // Which rows a launch works on.

@@ -552,7 +552,8 @@ __device__ __forceinline__ void pdm_fc_body(const Ctx& C, int prefill, int nrows
     for (int i = 0; i < kMaxRows; i++) {
       // in-flight position c+i keeps its anchors in ring row (c+i) mod n
       xs.row[i] = C.anchors + (size_t)((c + i) % C.n) * C.n * C.d;
-      const int depth = a - 1 - i;
+      // pre-step depth a - 1 - i; the post-step schedule runs after the stage compute, one deeper
+      const int depth = a - 1 - i + C.post_step;
       const int f = depth < C.n - 1 ? depth : C.n - 1;
       xs.nelig[i] = (f + 1) * C.d;
     }

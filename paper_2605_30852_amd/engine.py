@@ -161,6 +161,9 @@ class Engine:
     def spd_set_pdm_placement(self, place: int) -> None:
         B.spd_set_pdm_placement(self.h, place)
 
+    def spd_set_pdm_schedule(self, post_step: bool) -> None:
+        B.spd_set_pdm_schedule(self.h, post_step)
+
     def spd_set_sampling(self, top_k: int, temperature: float = 1.0, uniforms=None) -> None:
         B.spd_set_sampling(self.h, top_k, temperature, uniforms)
 

@@ -47,9 +47,11 @@ def compare_state(eng, ora, tag, worst):
             assert r <= REL_HIDDEN, f"{tag}: anchor {j} of position {q} rel L2 {r:.3e}"
 
 
-def run_lockstep(eng, model, prompt, n_steps, draft_for=None, check_pdm=True, log=None):
-    """eng: paper_2605_30852_amd.engine.Engine with debug on. Returns worst errors seen."""
-    ora = osp.SPDOracle(model, n=eng.n)
+def run_lockstep(eng, model, prompt, n_steps, draft_for=None, check_pdm=True, log=None, schedule="pre"):
+    """eng: paper_2605_30852_amd.engine.Engine with debug on. Returns worst errors seen. schedule:
+    the PDM's ("pre" or "post"); the engine is set to the same one."""
+    ora = osp.SPDOracle(model, n=eng.n, schedule=schedule)
+    eng.spd_set_pdm_schedule(schedule == "post")
     worst = {"hidden": 0.0, "logit": 0.0, "pdm_hidden": 0.0, "pdm_logit": 0.0, "steps": 0, "near_tie": 0}
     eng.spd_set_debug(True)
     xg = eng.spd_prefill(prompt)
