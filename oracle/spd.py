@@ -30,6 +30,9 @@ What it follows:
     is kept with the in-flight token; the exit's top-k distribution p judges the successor by
     rejection sampling with the successor's u_accept / u_resample, and a reject reseeds the residual
     draw. A forced draft carries q = delta. The prompt's first token is drawn from p with u_resample.
+  * The PDM's LM head (Section 4.1): shared with the target, or its own head over a smaller vocabulary
+    (initialised from the target's rows of that subset); a draft id i then stands for target token
+    map[i], map ascending, so ties still go to the lower target id.
   * Post-step schedule (the ablation of Section 4.4 against Section 3.3's pre-step choice): the PDM
     waits for the stage compute and reads the post-step features, every in-flight token one stage
     deeper (the newest contributes g^1 instead of g^0); drafting is then serial behind the step.
@@ -43,7 +46,7 @@ from typing import Callable, Dict, List, Optional, Sequence
 import numpy as np
 
 import synth
-from .model import (LayerCache, Model, argmax_first, decoder_layer, embed, lm_logits, new_caches)
+from .model import (LayerCache, Model, argmax_first, decoder_layer, embed, lm_logits, new_caches, rms_norm)
 from . import sampling as smp
 
 NONE, ACCEPT, REJECT = 0, 1, 2
@@ -116,6 +119,8 @@ class SPDOracle:
         self.qdist: Dict[int, smp.Dist] = {}  # sampled decoding: q of each in-flight token
         assert schedule in ("pre", "post")
         self.schedule = schedule
+        # the PDM's own vocabulary (target ids of its draft ids), or None: the shared head
+        self.pdm_ids = synth.pdm_vocab_map(sh, model.seed) if sh.pdm_vocab else None
 
     def clone(self) -> "SPDOracle":
         """An independent copy of the decoding state (the model is shared)."""
@@ -146,6 +151,15 @@ class SPDOracle:
         for j in range(f + 1):
             z[j * d:(j + 1) * d] = anchors[j]
         return self.w_in() @ z
+
+    def pdm_logits(self, h: np.ndarray) -> np.ndarray:
+        """The PDM's head over its last row: the shared W_lm, or its own head (draft ids)."""
+        if self.pdm_ids is None:
+            return lm_logits(self.m, h, "pdm.norm")
+        return self.m.w("pdm.lm_head") @ rms_norm(h, self.m.w("pdm.norm"), self.sh.rms_eps)
+
+    def pdm_token(self, i: int) -> int:
+        return int(i) if self.pdm_ids is None else int(self.pdm_ids[int(i)])
 
     def pdm_row(self, g: np.ndarray, pos: int) -> np.ndarray:
         h = g
@@ -227,13 +241,14 @@ class SPDOracle:
         else:  # post-step: every in-flight token one stage deeper
             run_target()
             pdm_h = run_pdm(1)
-        pdm_lg = lm_logits(self.m, pdm_h[c + a - 1], "pdm.norm")
+        pdm_lg = self.pdm_logits(pdm_h[c + a - 1])
         dpos = c + a  # the draft's position
         if self.sampling is None:
             qd = None
-            pdm_draft = argmax_first(pdm_lg)
+            pdm_draft = self.pdm_token(argmax_first(pdm_lg))
         else:
-            qd = self._target_dist(pdm_lg)
+            ids, probs = self._target_dist(pdm_lg)  # over draft ids, then as target tokens
+            qd = (np.array([self.pdm_token(i) for i in ids], dtype=np.int64), probs)
             pdm_draft = smp.sample(qd, self.sampling.u(dpos, smp.U_DRAFT))
         draft = pdm_draft if forced_draft is None else int(forced_draft)
         q_draft = None if qd is None else (qd if forced_draft is None else smp.point_mass(draft))

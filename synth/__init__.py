@@ -35,6 +35,7 @@ class ModelShape:
     rms_eps: float = 1e-6
     rope_base: float = 10000.0
     page_size: int = 16
+    pdm_vocab: int = 0  # 0: the PDM shares the target's LM head; else its own head over this many tokens
 
     def with_(self, **kw) -> "ModelShape":
         return dataclasses.replace(self, **kw)
@@ -75,6 +76,8 @@ class ModelShape:
             for k, s in self.layer_shapes().items():
                 out[f"pdm.layer.{l}.{k}"] = s
         out["pdm.norm"] = (d,)
+        if self.pdm_vocab:
+            out["pdm.lm_head"] = (self.pdm_vocab, d)
         return out
 
     def param_bytes(self, names: Optional[List[str]] = None) -> int:
@@ -129,10 +132,13 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
 def tensor(shape: ModelShape, seed: int, name: str) -> np.ndarray:
     """One named tensor as float32 values (already rounded to bf16 for bf16 workloads).
 
-    Norm gains are 1.0; every other tensor is N(0, 0.02^2)."""
+    Norm gains are 1.0; the PDM's own LM head is initialised from the target's, the rows of its
+    vocabulary subset (pdm_vocab_map); every other tensor is N(0, 0.02^2)."""
     s = shape.tensor_shapes()[name]
     if is_norm(name):
         return np.ones(s, dtype=np.float32)
+    if name == "pdm.lm_head":
+        return tensor(shape, seed, "lm_head")[pdm_vocab_map(shape, seed)]
     x = _stream(seed, name).standard_normal(s, dtype=np.float32)
     x *= np.float32(WEIGHT_STD)
     if shape.dtype == "bf16":
@@ -145,11 +151,21 @@ def tensor_storage(shape: ModelShape, seed: int, name: str) -> np.ndarray:
     s = shape.tensor_shapes()[name]
     if is_norm(name):
         return np.ones(s, dtype=np.float32)
+    if name == "pdm.lm_head":
+        return np.ascontiguousarray(tensor_storage(shape, seed, "lm_head")[pdm_vocab_map(shape, seed)])
     x = _stream(seed, name).standard_normal(s, dtype=np.float32)
     x *= np.float32(WEIGHT_STD)
     if shape.dtype == "bf16":
         return bf16_bits(x).reshape(s)
     return x
+
+
+def pdm_vocab_map(shape: ModelShape, seed: int) -> np.ndarray:
+    """The PDM vocabulary: pdm_vocab distinct target token ids, ascending (draft id i is target token
+    map[i]), drawn uniformly from the target vocabulary."""
+    assert 0 < shape.pdm_vocab <= shape.vocab
+    ids = np.random.default_rng([int(seed), 13]).choice(shape.vocab, size=shape.pdm_vocab, replace=False)
+    return np.sort(ids).astype(np.int32)
 
 
 def iter_storage(shape: ModelShape, seed: int, threads: int = 8) -> Iterator[Tuple[str, np.ndarray]]:
