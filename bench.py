@@ -384,6 +384,8 @@ def main():
     log(f"[bench] p={p}: alpha={alpha:.3f}, {spd_tok_s:.0f} tok/s (AR {ar_tok_s:.0f} tok/s)")
     eng.close()
 
+    own_head = own_head_phase(args, weights, prompt, ref, max_tokens, attn_chunk, K, W, n, us_step)
+
     sampled = None
     if fused:
         sampled = sampled_phase(args, sh, weights, prompt, ref, first, mask, max_tokens, attn_chunk, K, W, n,
@@ -463,10 +465,58 @@ def main():
         "hbm_read_probe": probe,
         "tokens_per_s": {"spd_forced_p": p, "alpha": round(alpha, 4), "spd": round(spd_tok_s, 1),
                          "ar_same_gpu": round(ar_tok_s, 1)},
+        "pdm_own_head": own_head,
         "sampled": sampled,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def own_head_phase(args, weights, prompt, ref, max_tokens, attn_chunk, K, W, n, shared_us, vocab=32768):
+    """The PDM with its own LM head over a smaller vocabulary (initialised from the target's rows of
+    that subset): its head runs on the PDM's stream, the exit row alone on the main stream. Steady
+    state with drafts forced to the greedy tokens (the stream is checked), and the PDM's span."""
+    import numpy as np
+    import torch
+
+    from paper_2605_30852_amd import binding as B
+    from paper_2605_30852_amd.engine import Engine
+
+    P = len(prompt)
+    wv = weights.with_pdm_vocab(vocab)
+    eng = Engine(wv, max_tokens=max_tokens, n=n, attn_chunk=attn_chunk)
+    eng.spd_set_step_kernel(args.step_mode, args.step_grid, args.stage_groups if args.step_mode == 2 else -1)
+    eng.spd_set_pdm_placement(args.pdm_place)
+    eng.spd_set_pdm_grid(args.pdm_grid)
+    eng.spd_set_graph(not args.no_graph)
+    eng.spd_prefill(prompt)
+    eng.spd_set_forced_drafts(ref.astype(np.int32), P)
+    eng.spd_run_steps(W)
+    c0, a0, _, _ = eng.state()
+    assert a0 == n, "own-head pipeline not full after warm-up"
+    torch.cuda.synchronize()
+    ts = time.perf_counter()
+    eng.spd_run_steps(K)
+    eng.spd_sync()
+    el = time.perf_counter() - ts
+    c1, a1, _, _ = eng.state()
+    assert c1 - c0 == K and a1 == n, "own-head forced-accept run left the steady state"
+    toks = eng.tokens()[P: c1 + 1]
+    assert np.array_equal(toks, ref[: len(toks)]), "own-head SPD stream differs from greedy decoding"
+    B.spd_set_kernel_timing(eng.h, B.SPD_K_SPANS)
+    eng.spd_run_steps(32)
+    st_ms, pd_ms, late_ms, ns = B.spd_span_timing(eng.h)
+    B.spd_set_kernel_timing(eng.h, 0)
+    eng.close()
+    del wv
+    us = 1e6 * el / K
+    out = {"pdm_vocab": vocab, "us_per_step": round(us, 1), "over_shared_fused_us": round(us - shared_us, 1),
+           "stage_us": round(1e3 * st_ms / ns, 1), "pdm_us": round(1e3 * pd_ms / ns, 1),
+           "verify_wait_us": round(1e3 * late_ms / ns, 2),
+           "head_bytes": int(vocab * weights.shape.d_model * (2 if weights.shape.dtype == "bf16" else 4))}
+    log(f"[bench] own PDM head ({vocab} tokens): {us:.1f} us/step ({us - shared_us:+.1f} over the shared fused "
+        f"head), PDM span {out['pdm_us']} us, verify wait {out['verify_wait_us']} us")
+    return out
 
 
 def sampled_phase(args, sh, weights, prompt, ref, first, mask, max_tokens, attn_chunk, K, W, n, greedy_us,

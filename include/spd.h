@@ -76,6 +76,10 @@ typedef struct spd_config {
                             vocabulary (one two-row pass on main_stream after the draft module's
                             layers join); 0: the draft module runs its own pass on pdm_stream.
                             Both give the same draft. */
+  int32_t pdm_vocab;     /* 0: the draft module shares the target's lm_head. > 0: it has its own LM
+                            head over this many tokens (Section 4.1: smaller vocabulary), in
+                            spd_weights.pdm_lm_head / pdm_vocab_map; at most vocab; needs
+                            fused_head = 0 (the two heads stream different weights) */
 } spd_config;
 
 /* One decoder layer's weights, all device pointers, row-major [out x in]:
@@ -96,7 +100,11 @@ typedef struct spd_layer_weights {
 /* All weights. `layers` and `pdm_layers` are HOST arrays (n_layers and pdm_layers entries) of device
  * pointers; they are copied during spd_init. embed, lm_head: [V x d]; final_norm, pdm_norm: fp32 [d];
  * pdm_in: [d x n*d], the PDM's feature projection (Eq. agg-main): column block j multiplies the
- * anchor H^{beta_j} (the input of stage j). The PDM shares the target's lm_head. */
+ * anchor H^{beta_j} (the input of stage j). With spd_config.pdm_vocab = 0 the PDM shares the target's
+ * lm_head and the last two pointers are ignored; otherwise pdm_lm_head is [pdm_vocab x d] (the
+ * config's dtype) and pdm_vocab_map device int32 [pdm_vocab]: draft id i stands for target token
+ * pdm_vocab_map[i], each in [0, vocab) (checked at spd_init; SPD_E_INVAL otherwise). The PDM's
+ * draft is pdm_vocab_map[argmax] (lowest draft id on ties). */
 typedef struct spd_weights {
   const void* embed;
   const spd_layer_weights* layers;
@@ -105,6 +113,8 @@ typedef struct spd_weights {
   const void* pdm_in;
   const spd_layer_weights* pdm_layers;
   const void* pdm_norm;
+  const void* pdm_lm_head;
+  const int32_t* pdm_vocab_map;
 } spd_weights;
 
 /* Result of one step. Positions are 0-based. committed_len = c, the number of positions that have
@@ -171,7 +181,8 @@ spd_status spd_clear_forced_drafts(spd_handle* h);
  * value-descending order: the first i with u * sum < cumsum_i.
  * uniforms: host float[3 * positions], positions == max_tokens; entry 3*pos + j is position pos's
  * u_draft (j = 0), u_accept (1) and u_resample (2), each in [0, 1); copied during the call.
- * top_k in [1, 64] turns sampling on (needs fused_head = 1), top_k = 0 back to greedy decoding
+ * top_k in [1, 64] turns sampling on (needs fused_head = 1, so the shared head), top_k = 0 back to
+ * greedy decoding
  * (uniforms may be NULL). Legal only before spd_prefill (SPD_E_STATE afterwards). In a sampled step
  * spd_step_result.target_argmax and verified_token hold the committed token and pdm_draft the
  * PDM's own draw. */

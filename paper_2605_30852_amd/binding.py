@@ -31,6 +31,7 @@ class spd_config(ct.Structure):
         ("dtype", ct.c_int32), ("n_stages", ct.c_int32), ("pdm_layers", ct.c_int32),
         ("page_size", ct.c_int32), ("max_tokens", ct.c_int32), ("auto_rollback", ct.c_int32),
         ("attn_chunk", ct.c_int32), ("page_seed", ct.c_uint64), ("fused_head", ct.c_int32),
+        ("pdm_vocab", ct.c_int32),
     ]
 
 
@@ -44,6 +45,7 @@ class spd_weights(ct.Structure):
         ("embed", ct.c_void_p), ("layers", ct.POINTER(spd_layer_weights)),
         ("final_norm", ct.c_void_p), ("lm_head", ct.c_void_p), ("pdm_in", ct.c_void_p),
         ("pdm_layers", ct.POINTER(spd_layer_weights)), ("pdm_norm", ct.c_void_p),
+        ("pdm_lm_head", ct.c_void_p), ("pdm_vocab_map", ct.c_void_p),
     ]
 
 

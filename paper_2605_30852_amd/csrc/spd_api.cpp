@@ -65,6 +65,8 @@ spd_status check_config(const spd_config* c, std::string* why) {
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f)) return bad("rms_eps must be > 0 and rope_base > 1");
   if (c->auto_rollback != 0 && c->auto_rollback != 1) return bad("auto_rollback must be 0 or 1");
   if (c->fused_head != 0 && c->fused_head != 1) return bad("fused_head must be 0 or 1");
+  if (c->pdm_vocab < 0 || c->pdm_vocab > c->vocab) return bad("pdm_vocab must be in [0, vocab]");
+  if (c->pdm_vocab > 0 && c->fused_head) return bad("an own PDM head (pdm_vocab > 0) needs fused_head = 0");
   if (c->d_model > 8192) return bad("d_model must be at most 8192");
   return SPD_OK;
 }
@@ -521,17 +523,15 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     if (C.sam.top_k > 0)  // + top-k distributions, the draft's draw and the rejection-sampling verify
       Launch<WT>::head_sample(C, 3, 0, 0, forced_override, h->cfg.auto_rollback, h->main);
     else
-      Launch<WT>::head_verify(C, forced_override, h->cfg.auto_rollback, h->main);  // + the step's verify
+      Launch<WT>::head_verify(C, 1, forced_override, h->cfg.auto_rollback, h->main);  // + the step's verify
     return launch_check(h, "step");
-  } else {
-    {
-      TimedLaunch t(h, h->main, SPD_K_HEAD);
-      Launch<WT>::head(C, 0, 0, h->main);  // exit row, only when the pipeline is full
-    }
-    if (sp) HIPC(hipEventRecord(sp[2], h->main));
-    HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
   }
-  launch_verify(C, forced_override, h->cfg.auto_rollback, h->main, h->bf16);
+  // the draft module's own head pass has left its draft: the exit row alone, with the verify in the
+  // launch's last workgroup (the draft module ends well inside the stage compute)
+  if (sp) HIPC(hipEventRecord(sp[2], h->main));
+  HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
+  TimedLaunch t(h, h->main, SPD_K_HEAD);
+  Launch<WT>::head_verify(C, 0, forced_override, h->cfg.auto_rollback, h->main);
   return launch_check(h, "step");
 }
 
@@ -610,6 +610,10 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   if (!w || !w->embed || !w->layers || !w->final_norm || !w->lm_head || !w->pdm_in || !w->pdm_layers ||
       !w->pdm_norm) {
     g_init_error = "weights: NULL pointer";
+    return SPD_E_INVAL;
+  }
+  if (cfg->pdm_vocab > 0 && (!w->pdm_lm_head || !w->pdm_vocab_map)) {
+    g_init_error = "weights: pdm_vocab > 0 needs pdm_lm_head and pdm_vocab_map";
     return SPD_E_INVAL;
   }
   for (int l = 0; l < cfg->n_layers; l++)
@@ -698,6 +702,18 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   C.lay = (const LayerDesc*)(ws + lay.lay);
   C.embed = w->embed;
   C.lm_head = w->lm_head;
+  C.pdm_V = cfg->pdm_vocab;
+  C.pdm_head = cfg->pdm_vocab > 0 ? w->pdm_lm_head : w->lm_head;
+  C.pdm_map = cfg->pdm_vocab > 0 ? w->pdm_vocab_map : nullptr;
+  if (cfg->pdm_vocab > 0) {  // every draft id must name a target token (it is embedded when pushed)
+    std::vector<int32_t> map(cfg->pdm_vocab);
+    HIPI(hipMemcpy(map.data(), w->pdm_vocab_map, sizeof(int32_t) * map.size(), hipMemcpyDeviceToHost));
+    for (int32_t t : map)
+      if (t < 0 || t >= cfg->vocab) {
+        h->err = "weights: pdm_vocab_map holds an id outside [0, vocab)";
+        return fail(SPD_E_INVAL);
+      }
+  }
   C.w_in = w->pdm_in;
   C.final_norm = (const float*)w->final_norm;
   C.pdm_norm = (const float*)w->pdm_norm;
@@ -883,6 +899,7 @@ spd_status spd_set_sampling(spd_handle* h, int32_t top_k, float temperature, con
   if (top_k < 0 || top_k > kMaxTopK) return refuse(h, "top_k must be in [0, 64]");
   if (!(temperature > 0.f) || !std::isfinite(temperature)) return refuse(h, "temperature must be > 0");
   if (!h->cfg.fused_head) return refuse(h, "sampled decoding needs fused_head = 1");
+  if (h->cfg.pdm_vocab > 0) return refuse(h, "sampled decoding needs the shared PDM head");
   if (!uniforms || positions != h->cfg.max_tokens)
     return refuse(h, "uniforms must hold 3 * max_tokens values");
   for (size_t i = 0; i < (size_t)3 * positions; i++)
@@ -1191,7 +1208,10 @@ spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes)
     case SPD_DBG_ANCHORS: src = h->ctx.anchors; need = sizeof(float) * c.n_stages * c.n_stages * c.d_model; break;
     case SPD_DBG_PDM_HIDDEN: src = h->ctx.pdm_x; need = sizeof(float) * kMaxRows * c.d_model; break;
     case SPD_DBG_EXIT_LOGITS: src = h->ctx.dbg_logits; need = sizeof(float) * c.vocab; break;
-    case SPD_DBG_PDM_LOGITS: src = h->ctx.dbg_logits + c.vocab; need = sizeof(float) * c.vocab; break;
+    case SPD_DBG_PDM_LOGITS:
+      src = h->ctx.dbg_logits + c.vocab;
+      need = sizeof(float) * (c.pdm_vocab > 0 ? c.pdm_vocab : c.vocab);
+      break;
     case SPD_DBG_TOKENS: src = h->ctx.tok; need = sizeof(int32_t) * c.max_tokens; break;
     case SPD_DBG_STATE: src = nullptr; need = sizeof(int32_t) * 4; break;
     case SPD_DBG_QDIST: src = nullptr; need = sizeof(int32_t) * c.n_stages * (1 + 2 * kMaxTopK); break;

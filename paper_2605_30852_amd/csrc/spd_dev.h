@@ -135,6 +135,9 @@ struct Ctx {
   const void* w_in;
   const float* final_norm;
   const float* pdm_norm;
+  const void* pdm_head;      // the PDM's own LM head [pdm_V x d], or the shared lm_head (pdm_V == 0)
+  const int32_t* pdm_map;    // pdm_V > 0: target token of each draft id
+  int pdm_V;                 // 0: shared head
   const int32_t* page_table;
   const float2* rope;     // [max_tokens][dh/2] (cos, sin)
   // state
@@ -221,7 +224,8 @@ struct Launch {
   static void head(const Ctx& c, int src, int row, void* stream);
   // The two-row head (src 3) and the verify of the step in one launch: the workgroup that finishes
   // the head last runs the verify.
-  static void head_verify(const Ctx& c, int forced_override, int auto_rb, void* stream);
+  // two_rows 0: the exit row alone (src 0), the PDM's draft already left by its own head pass.
+  static void head_verify(const Ctx& c, int two_rows, int forced_override, int auto_rb, void* stream);
   // Sampled decoding (c.sam.top_k > 0). src 3: the two-row head, then the top-k distributions, the
   // draft's draw and the rejection-sampling verify of the step, in one launch; src 2: prefill row
   // `row` and the draw of the token at position pos (published as the row's argmax key, which the
@@ -236,7 +240,6 @@ struct Launch {
   static size_t pstep_lds(const Ctx& c);
   static const void* pstep_fn(const Ctx& c);
 };
-void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* stream, int bf16);
 // Every layer slot of every active stage of one step in one persistent launch (spd_step.hip).
 // dev_ctx: a device copy of c.
 void launch_step(const Ctx& c, const Ctx* dev_ctx, int grid, void* stream, int bf16);

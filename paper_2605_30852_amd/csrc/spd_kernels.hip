@@ -632,13 +632,15 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row, int lc
     set[NV - 1] = 1;
   }
   constexpr int BLK = 64 * Elt<WT>::VE;
-  const int d = C.d, V = C.V;
+  // the PDM's row alone (src 1) goes through its own head when it has one; V counts that head's rows
+  const bool own = src == 1 && C.pdm_V > 0;
+  const int d = C.d, V = own ? C.pdm_V : C.V;
   const int ldsK = (d + BLK - 1) / BLK * BLK;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int NW = gridDim.x * 4, wv = blockIdx.x * 4 + w;
   const int npairs = (V + 1) / 2;
   const int count = wv < npairs ? (npairs - 1 - wv) / NW + 1 : 0;
-  const WT* W = (const WT*)C.lm_head;
+  const WT* W = (const WT*)(own ? C.pdm_head : C.lm_head);
   auto rowptr = [&](int i, int which) -> const WT* {
     const int m = 2 * (wv + i * NW) + which;
     return m < V ? W + (size_t)m * d : (const WT*)nullptr;
@@ -669,7 +671,7 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row, int lc
     for (int v = 0; v < NV; v++) {
       const float l0 = s0[v] * scl[v], l1 = s1[v] * scl[v];
       if (C.debug && (v > 0 || dbg_row0) && lane < 2 && m + lane < V)
-        C.dbg_logits[(size_t)set[v] * V + m + lane] = lane == 0 ? l0 : l1;
+        C.dbg_logits[(size_t)set[v] * C.V + m + lane] = lane == 0 ? l0 : l1;
       if (SAMP && lane < 2 && m + lane < V) {
         if (lbuf)
           lg[v * lcap + 2 * i + lane] = lane == 0 ? l0 : l1;
@@ -737,6 +739,9 @@ __device__ __forceinline__ int take_head(const BufSet& B, int V) {
 __device__ __forceinline__ int take_head_dev(const BufSet& B, int V) {
   return argmax_index(__hip_atomic_load(B.hkey, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), V);
 }
+// Rows of the PDM's head, and the target token of its argmax (a draft id with an own head).
+__device__ __forceinline__ int pdm_rows(const Ctx& C) { return C.pdm_V > 0 ? C.pdm_V : C.V; }
+__device__ __forceinline__ int pdm_token(const Ctx& C, int i) { return C.pdm_V > 0 ? C.pdm_map[i] : i; }
 
 // ------------------------------------------------------------------------------- attention
 // Decode attention of a stage launch. Grid: x = key split, y = KV head, z = stage of the launch.
@@ -1079,35 +1084,31 @@ __device__ __forceinline__ void verify_update(const Ctx& C, int y_all, int pd_al
   }
 }
 
-// Greedy streaming verification (Section 3.4) and the pipeline state update; single workgroup,
-// last kernel of a step.
-// COH: the argmax keys were written by other workgroups of the same launch.
-template <typename WT, bool COH = false>
+// Greedy streaming verification (Section 3.4) and the pipeline state update, run by the last
+// workgroup of the LM-head launch: the argmax keys were folded in by the launch's other workgroups
+// (and by the draft module's own head pass, if it has one), so they are read with device-scope loads.
+template <typename WT>
 __device__ __forceinline__ void verify_body(const Ctx& C, int forced_override, int auto_rb) {
   DevState* st = C.st;
-  const int y_all = (st->a == C.n) ? (COH ? take_head_dev(C.b[0], C.V) : take_head(C.b[0], C.V)) : -1;
-  const int pd_all = COH ? take_head_dev(C.b[1], C.V) : take_head(C.b[1], C.V);
+  const int y_all = (st->a == C.n) ? take_head_dev(C.b[0], C.V) : -1;
+  const int pd_all = pdm_token(C, take_head_dev(C.b[1], pdm_rows(C)));
   const int step_err = C.plan.sync != nullptr ? C.plan.sync[sync_err()] : 0;
   __syncthreads();  // every thread has read the argmax keys and the timeout flag
   verify_update<WT>(C, y_all, pd_all, step_err, forced_override, auto_rb);
 }
 
-template <typename WT>
-__global__ __launch_bounds__(kWG) void k_verify(Ctx C, int forced_override, int auto_rb) {
-  ktrace_start(C, ktrace_extra(C, KT_VERIFY), blockIdx.x == 0 && blockIdx.y == 0);
-  verify_body<WT>(C, forced_override, auto_rb);
-  ktrace_end(C, ktrace_extra(C, KT_VERIFY));
-}
 
 // The fused exit + draft head and verify: every workgroup streams its share of the vocabulary and
 // folds its argmax into the keys; once its own key updates have completed it takes a ticket, and the
 // workgroup with the last ticket (every other one has finished) runs the verify and resets the
 // ticket. Saves the launch of the single-workgroup verify after the head.
-template <typename WT>
+// NV 2: the two-row head (src 3); NV 1: the exit row alone (src 0), when the PDM's own pass has left
+// its argmax key before this launch.
+template <typename WT, int NV>
 __global__ __launch_bounds__(kWG) void k_head_verify(Ctx C, int forced_override, int auto_rb) {
   __shared__ int s_last;
   ktrace_start(C, ktrace_extra(C, KT_HEAD), blockIdx.x == 0);
-  head_body<WT, 2>(C, 3, 0);
+  head_body<WT, NV>(C, NV == 2 ? 3 : 0, 0);
   // the argmax updates are device-scope atomics: once this thread has seen its own complete, the
   // ticket (relaxed, no cache-wide fence) can follow; the last workgroup reads the keys with
   // device-scope loads
@@ -1121,7 +1122,7 @@ __global__ __launch_bounds__(kWG) void k_head_verify(Ctx C, int forced_override,
   ktrace_end(C, ktrace_extra(C, KT_HEAD));
   if (!s_last) return;
   ktrace_start(C, ktrace_extra(C, KT_VERIFY), true);
-  verify_body<WT, true>(C, forced_override, auto_rb);
+  verify_body<WT>(C, forced_override, auto_rb);
   if (threadIdx.x == 0) __hip_atomic_store(&C.st->head_ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   ktrace_end(C, ktrace_extra(C, KT_VERIFY));
 }
@@ -1500,7 +1501,7 @@ void Launch<WT>::head(const Ctx& c, int src, int row, void* s) {
   // since the head runs alone and a second round of workgroups would only add a tail
   constexpr int BLK = 64 * Elt<WT>::VE;
   const size_t kl_pad = (size_t)(c.d + BLK - 1) / BLK * BLK;
-  const int np = (c.V + 1) / 2;
+  const int np = ((src == 1 && c.pdm_V > 0 ? c.pdm_V : c.V) + 1) / 2;
   if (src == 3) {
     const size_t shm = 2 * kl_pad * sizeof(float);
     const int res = resident_wgs((const void*)k_head<WT, 2>, shm);
@@ -1515,12 +1516,17 @@ void Launch<WT>::head(const Ctx& c, int src, int row, void* s) {
 }
 
 template <typename WT>
-void Launch<WT>::head_verify(const Ctx& c, int forced_override, int auto_rb, void* s) {
+void Launch<WT>::head_verify(const Ctx& c, int two_rows, int forced_override, int auto_rb, void* s) {
   constexpr int BLK = 64 * Elt<WT>::VE;
-  const size_t shm = 2 * (size_t)(c.d + BLK - 1) / BLK * BLK * sizeof(float);
-  const int res = resident_wgs((const void*)k_head_verify<WT>, shm);
+  const int nv = two_rows ? 2 : 1;
+  const size_t shm = nv * (size_t)(c.d + BLK - 1) / BLK * BLK * sizeof(float);
+  const void* fn = two_rows ? (const void*)k_head_verify<WT, 2> : (const void*)k_head_verify<WT, 1>;
+  const int res = resident_wgs(fn, shm);
   const dim3 grid(std::max(std::min(stream_grid(c, (c.V + 1) / 2, 1), res), 1));
-  launch_timed((k_head_verify<WT>), grid, dim3(kWG), shm, S(s), c, forced_override, auto_rb);
+  if (two_rows)
+    launch_timed((k_head_verify<WT, 2>), grid, dim3(kWG), shm, S(s), c, forced_override, auto_rb);
+  else
+    launch_timed((k_head_verify<WT, 1>), grid, dim3(kWG), shm, S(s), c, forced_override, auto_rb);
 }
 
 template <typename WT>
@@ -1558,13 +1564,6 @@ void Launch<WT>::embed_rows(const Ctx& c, int t0, int nrows, void* s) {
 
 template struct Launch<float>;
 template struct Launch<uint16_t>;
-
-void launch_verify(const Ctx& c, int forced_override, int auto_rb, void* s, int bf16) {
-  if (bf16)
-    launch_timed((k_verify<uint16_t>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
-  else
-    launch_timed((k_verify<float>), dim3(1), dim3(kWG), 0, S(s), c, forced_override, auto_rb);
-}
 
 void launch_reseed(const Ctx& c, int keep, int tok, int prompt_len, void* s, int bf16) {
   if (bf16)

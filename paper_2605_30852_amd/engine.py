@@ -36,6 +36,7 @@ def make_config(shape: synth.ModelShape, max_tokens: int, n: Optional[int] = Non
     c.attn_chunk = attn_chunk
     c.page_seed = page_seed
     c.fused_head = 1 if fused_head else 0
+    c.pdm_vocab = shape.pdm_vocab
     return c
 
 
@@ -51,6 +52,8 @@ class DeviceWeights:
             if overrides and name in overrides:
                 arr = self._storage(overrides[name], name)
             self.t[name] = self._upload(arr, device)
+        if shape.pdm_vocab:
+            self.t["pdm.vocab_map"] = self._upload(synth.pdm_vocab_map(shape, seed), device)
 
     def _storage(self, values: np.ndarray, name: str) -> np.ndarray:
         v = np.asarray(values, dtype=np.float32)
@@ -79,6 +82,20 @@ class DeviceWeights:
         for name in other.shape.tensor_shapes():
             if name.startswith("pdm."):
                 other.t[name] = self._upload(synth.tensor_storage(other.shape, self.seed, name), device)
+        if "pdm.vocab_map" in self.t:
+            other.t["pdm.vocab_map"] = self.t["pdm.vocab_map"]
+        return other
+
+    def with_pdm_vocab(self, pdm_vocab: int, device="cuda") -> "DeviceWeights":
+        """A view whose PDM has its own LM head over pdm_vocab tokens (initialised from the target's
+        rows of that vocabulary); every other tensor is shared."""
+        other = DeviceWeights.__new__(DeviceWeights)
+        other.shape = self.shape.with_(pdm_vocab=pdm_vocab)
+        other.seed = self.seed
+        other.t = {k: v for k, v in self.t.items() if k not in ("pdm.lm_head", "pdm.vocab_map")}
+        if pdm_vocab:
+            other.t["pdm.lm_head"] = self._upload(synth.tensor_storage(other.shape, self.seed, "pdm.lm_head"), device)
+            other.t["pdm.vocab_map"] = self._upload(synth.pdm_vocab_map(other.shape, self.seed), device)
         return other
 
     def struct(self):
@@ -100,6 +117,9 @@ class DeviceWeights:
         w.pdm_in = self.ptr("pdm.in")
         w.pdm_layers = ct.cast(pdm, ct.POINTER(B.spd_layer_weights))
         w.pdm_norm = self.ptr("pdm.norm")
+        if sh.pdm_vocab:
+            w.pdm_lm_head = self.ptr("pdm.lm_head")
+            w.pdm_vocab_map = self.ptr("pdm.vocab_map")
         return w, (layers, pdm)
 
 
@@ -108,12 +128,15 @@ class Engine:
 
     def __init__(self, weights: DeviceWeights, max_tokens: int, n: Optional[int] = None,
                  pdm_layers: Optional[int] = None, auto_rollback: bool = True, attn_chunk: int = 0,
-                 page_seed: int = 0, fused_head: bool = True, device="cuda"):
+                 page_seed: int = 0, fused_head: Optional[bool] = None, device="cuda"):
+        """fused_head: None picks the two-row pass when the PDM shares the target's head."""
         if not torch.cuda.is_available():
             raise RuntimeError("Engine needs a GPU: the SPD step has no CPU path")
         n = weights.shape.n_stages if n is None else n
         self.w = weights.pdm_for_width(n, pdm_layers, device)
         self.shape = self.w.shape
+        if fused_head is None:
+            fused_head = self.shape.pdm_vocab == 0
         self.cfg = make_config(self.shape, max_tokens, n=n, auto_rollback=auto_rollback,
                                attn_chunk=attn_chunk, page_seed=page_seed, fused_head=fused_head)
         self.n = n
@@ -188,7 +211,7 @@ class Engine:
         return B.spd_read_debug(self.h, B.SPD_DBG_EXIT_LOGITS, self.shape.vocab)
 
     def pdm_logits(self) -> np.ndarray:
-        return B.spd_read_debug(self.h, B.SPD_DBG_PDM_LOGITS, self.shape.vocab)
+        return B.spd_read_debug(self.h, B.SPD_DBG_PDM_LOGITS, self.shape.pdm_vocab or self.shape.vocab)
 
     def qdist(self, pos: int):
         """Sampled decoding: (ids, probs) of the draft distribution kept for in-flight position pos."""
