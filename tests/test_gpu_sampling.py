@@ -295,3 +295,58 @@ def test_fullsize_4b_sampled_step_selection():
             assert r["verified_token"] in top
     eng.close()
     _say(f"[fullsize 4b sampled] {exits} exits checked")
+
+
+def _pit(ids, probs, tok, w):
+    """A point w of the way through token tok's interval of the inverse CDF in the listed order; U(0, 1)
+    over draws when tok follows (ids, probs) and w is an independent uniform."""
+    probs = np.asarray(probs, dtype=np.float64)
+    probs = probs / probs.sum()
+    hit = np.nonzero(np.asarray(ids) == tok)[0]
+    assert hit.size == 1, f"token {tok} outside the distribution"
+    j = int(hit[0])
+    return float(probs[:j].sum() + w * probs[j])
+
+
+def test_fullsize_4b_sampled_tokens_follow_their_distributions():
+    """Any size: under sampled decoding (top-50, T = 1) with the PDM's own draws, each committed
+    token follows the exit's top-50 distribution p (the rejection-sampling guarantee) and each draw of
+    the PDM follows its q. With p and q built from the HIP path's own logits, the randomised
+    probability-integral transform of every committed token and every draft is uniform (KS test),
+    at the 4B-class size in the benchmark's launch form (stage groups, step graph)."""
+    from scipy import stats
+
+    from paper_2605_30852_amd.engine import DeviceWeights, Engine
+
+    sh = synth.B4
+    n, P, rows, steps = 2, 24, 400, 300
+    prompt = synth.prompt(sh, 0, P)
+    _say("[fullsize 4b PIT] uploading weights")
+    W = DeviceWeights(sh, 0, threads=16)
+    U = np.random.default_rng(9).random((rows, 3))
+    eng = Engine(W, max_tokens=rows, n=n)
+    eng.spd_set_sampling(50, 1.0, U)
+    eng.spd_set_graph(True)
+    eng.spd_set_debug(True)
+    eng.spd_prefill(prompt)
+    rng = np.random.default_rng(21)
+    pit_p, pit_q, accepts = [], [], 0
+    for i in range(steps):
+        r = eng.spd_run_steps(1, want_log=True)[0]
+        if r["decision"] != osp.NONE:
+            el = eng.exit_logits().astype(np.float64)
+            order = np.lexsort((np.arange(len(el)), -el))[:50]
+            z = el[order]
+            pit_p.append(_pit(order, np.exp(z - z[0]), r["verified_token"], rng.random()))
+            accepts += r["decision"] == osp.ACCEPT
+        if r["decision"] != osp.REJECT:  # the newest token is the PDM's draw, kept with its q
+            c, a, _, _ = eng.state()
+            ids, probs = eng.qdist(c + a - 1)
+            pit_q.append(_pit(ids, probs, r["pdm_draft"], rng.random()))
+    eng.close()
+    ks_p = stats.kstest(pit_p, "uniform")
+    ks_q = stats.kstest(pit_q, "uniform")
+    _say(f"[fullsize 4b PIT] {len(pit_p)} exits ({accepts} accepts), KS p = {ks_p.pvalue:.3f}; "
+         f"{len(pit_q)} drafts, KS p = {ks_q.pvalue:.3f}")
+    assert len(pit_p) >= 100 and len(pit_q) >= 100
+    assert ks_p.pvalue > 1e-3 and ks_q.pvalue > 1e-3
