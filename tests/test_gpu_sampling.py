@@ -83,10 +83,10 @@ def _settle(u, uses):
     return float(np.float32(v))
 
 
-def _oracle_run(model, prompt, n, k, temp, U, steps, draft_for, nudge):
+def _oracle_run(model, prompt, n, k, temp, U, steps, draft_for, nudge, schedule="pre"):
     """One oracle run; with nudge, every uniform the run draws with is settled clear of its decision
     boundaries (in place; see _settle). Returns (results, near-tie positions, moved?)."""
-    ora = osp.SPDOracle(model, n=n, sampling=smp.Sampling(k, temp, U))
+    ora = osp.SPDOracle(model, n=n, sampling=smp.Sampling(k, temp, U), schedule=schedule)
     ties = set()
     uses = {}
     P = len(prompt)
@@ -129,10 +129,10 @@ def _oracle_run(model, prompt, n, k, temp, U, steps, draft_for, nudge):
     return out, ties, moved
 
 
-def _clear_uniforms(model, prompt, n, k, temp, rows, steps, draft_for, seed):
+def _clear_uniforms(model, prompt, n, k, temp, rows, steps, draft_for, seed, schedule="pre"):
     U = np.random.default_rng([seed, 3]).random((rows, 3)).astype(np.float32).astype(np.float64)
     for _ in range(20):
-        _, _, moved = _oracle_run(model, prompt, n, k, temp, U, steps, draft_for, nudge=True)
+        _, _, moved = _oracle_run(model, prompt, n, k, temp, U, steps, draft_for, nudge=True, schedule=schedule)
         U = U.astype(np.float32).astype(np.float64)  # the values the GPU sees
         U[U >= 1.0] = float(np.nextafter(np.float32(1.0), np.float32(0.0)))
         if not moved:
@@ -145,10 +145,11 @@ def _kth_gap(logits, k):
     return s[k - 1] - s[k] if k < len(s) else np.inf
 
 
-@pytest.mark.parametrize("n,k,temp,forced", [(1, 8, 1.0, False), (2, 8, 0.5, True), (2, 64, 1.0, False),
-                                             (3, 16, 0.2, True), (4, 50, 0.7, False)])
-def test_sampled_lockstep_matches_oracle(tiny_w, n, k, temp, forced):
-    _say(f"[sampled lockstep n={n} k={k} T={temp} forced={forced}]")
+@pytest.mark.parametrize("n,k,temp,forced,schedule", [(1, 8, 1.0, False, "pre"), (2, 8, 0.5, True, "pre"),
+                                                      (2, 64, 1.0, False, "pre"), (3, 16, 0.2, True, "pre"),
+                                                      (4, 50, 0.7, False, "pre"), (3, 16, 0.5, False, "post")])
+def test_sampled_lockstep_matches_oracle(tiny_w, n, k, temp, forced, schedule):
+    _say(f"[sampled lockstep n={n} k={k} T={temp} forced={forced} schedule={schedule}]")
     sh = synth.TINY
     model = om.Model(sh, SEED)
     prompt = synth.prompt(sh, SEED, 21)
@@ -159,10 +160,11 @@ def test_sampled_lockstep_matches_oracle(tiny_w, n, k, temp, forced):
         mask = synth.accept_mask(0.7, SEED + n, rows + 8)
         table = {P + i: (int(t) if mask[P + i] else int((t + 1) % sh.vocab)) for i, t in enumerate(ref)}
         draft_for = table.get
-    U = _clear_uniforms(model, prompt, n, k, temp, rows, steps, draft_for, seed=100 * n + k)
-    _, ties, _ = _oracle_run(model, prompt, n, k, temp, U, steps, draft_for, nudge=False)
-    ora = osp.SPDOracle(model, n=n, sampling=smp.Sampling(k, temp, U))
+    U = _clear_uniforms(model, prompt, n, k, temp, rows, steps, draft_for, seed=100 * n + k, schedule=schedule)
+    _, ties, _ = _oracle_run(model, prompt, n, k, temp, U, steps, draft_for, nudge=False, schedule=schedule)
+    ora = osp.SPDOracle(model, n=n, sampling=smp.Sampling(k, temp, U), schedule=schedule)
     eng = _engine(tiny_w, n, rows)
+    eng.spd_set_pdm_schedule(schedule == "post")
     eng.spd_set_sampling(k, temp, U)
     eng.spd_set_debug(True)
     assert eng.spd_prefill(prompt) == ora.prefill(prompt)
