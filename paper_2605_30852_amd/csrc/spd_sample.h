@@ -109,7 +109,7 @@ __device__ void visit_regions(const Ctx& C, int set, const SelLds& S, int nsel, 
   const int total = nsel * per2;
   const unsigned long long* base =
       reinterpret_cast<const unsigned long long*>(C.sam.wlog + (size_t)set * C.sam.wlog_stride);
-  constexpr int kB = 8;
+  constexpr int kB = 8;  // more in flight raises the kernel's registers and slows the head's stream
   for (int e0 = threadIdx.x; e0 < total; e0 += kB * kWG) {
     unsigned long long raw[kB];
     int wg[kB], off[kB];
