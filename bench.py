@@ -169,6 +169,9 @@ def main():
                     help="PDM launches: own stream, main before the stages, first group before/after, "
                          "spread over the groups")
     ap.add_argument("--attn-chunk", type=int, default=0, help="keys per attention split (0: the workload's default)")
+    ap.add_argument("--extra-phases", choices=["auto", "on", "off"], default="auto",
+                    help="the PDM's own head and sampled decoding, each on a handle of its own (auto: on "
+                         "for prompts up to 4096 tokens; each needs its own prefill)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (the known-size kernel for HBM counter scaling)")
     args = ap.parse_args()
@@ -384,10 +387,13 @@ def main():
     log(f"[bench] p={p}: alpha={alpha:.3f}, {spd_tok_s:.0f} tok/s (AR {ar_tok_s:.0f} tok/s)")
     eng.close()
 
-    own_head = own_head_phase(args, weights, prompt, ref, max_tokens, attn_chunk, K, W, n, us_step)
+    extra = args.extra_phases == "on" or (args.extra_phases == "auto" and P <= 4096)
+    if not extra:
+        log(f"[bench] own-head and sampled phases skipped (--extra-phases {args.extra_phases}, prompt {P})")
+    own_head = own_head_phase(args, weights, prompt, ref, max_tokens, attn_chunk, K, W, n, us_step) if extra else None
 
     sampled = None
-    if fused:
+    if fused and extra:
         sampled = sampled_phase(args, sh, weights, prompt, ref, first, mask, max_tokens, attn_chunk, K, W, n,
                                 us_step, kernels.get("head"))
 
