@@ -783,11 +783,18 @@ __global__ __launch_bounds__(kWG) void k_attn_stage(Ctx C, Rows R) {
 }
 
 // Decode attention of a row block (the PDM's rows: row z at position pos0 + z over the layer's own
-// cache). Grid: x = key split, y = KV head, z = row. The split is attn_split with the row's scratch.
+// cache). The split is attn_split with the row's scratch. The rows of one (key split, KV head) group
+// read the same pages, so they run back to back on one XCD and share its L2: workgroups go to the
+// XCDs in turn (workgroup b to XCD b mod 8), and the b-th workgroup of an XCD takes row j mod nrg of
+// group (j / nrg) * 8 + xcd, j = b / 8. One-dimensional grid of ceil(groups / 8) * 8 * nrg
+// workgroups (groups = max_splits * hkv); the padding groups return at once.
 template <typename KVT, int DH, int GP>
-__global__ __launch_bounds__(kWG) void k_attn_rows(Ctx C, Rows R) {
+__global__ __launch_bounds__(kWG) void k_attn_rows(Ctx C, Rows R, int nrg) {
   extern __shared__ __align__(16) float lds[];
-  const int split = blockIdx.x, g = blockIdx.y, z = blockIdx.z;
+  const int xcd = (int)blockIdx.x & 7, j = (int)blockIdx.x >> 3;
+  const int z = j % nrg, grp = (j / nrg) * 8 + xcd;
+  if (grp >= C.max_splits * C.hkv) return;
+  const int split = grp % C.max_splits, g = grp / C.max_splits;
   const int k0 = split * C.chunk;
   const int page0 = C.page_table[min((k0 + (int)threadIdx.x / kAttnTPK) / C.page, C.max_pages - 1)];
   const Grp gr = resolve(C, R, 0);
@@ -1407,18 +1414,19 @@ void Launch<WT>::rows_sublayer(const Ctx& c, const Rows& r, int max_rows, int k,
   if (k == 3) rgemv_launch<WT, SG_GATEUP>(c, r, c.F, c.d, max_rows, cap_wgs, s);
   if (k == 4) rgemv_launch<WT, SG_DOWN>(c, r, (c.d + 1) / 2, c.F, max_rows, cap_wgs, s);
   if (k != 1) return;
-  const dim3 agrid(c.max_splits, c.hkv, max_rows);
+  const int groups8 = (c.max_splits * c.hkv + 7) / 8 * 8;  // see k_attn_rows: XCD-aware order
+  const dim3 agrid(groups8 * max_rows);
   const bool g4 = c.G <= 4;
   if (c.dh == 128) {
     if (g4)
-      launch_timed((k_attn_rows<WT, 128, 4>), agrid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
+      launch_timed((k_attn_rows<WT, 128, 4>), agrid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r, max_rows);
     else
-      launch_timed((k_attn_rows<WT, 128, 8>), agrid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r);
+      launch_timed((k_attn_rows<WT, 128, 8>), agrid, dim3(kWG), attn_split_lds<WT, 128>(), S(s), c, r, max_rows);
   } else {
     if (g4)
-      launch_timed((k_attn_rows<WT, 64, 4>), agrid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
+      launch_timed((k_attn_rows<WT, 64, 4>), agrid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r, max_rows);
     else
-      launch_timed((k_attn_rows<WT, 64, 8>), agrid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
+      launch_timed((k_attn_rows<WT, 64, 8>), agrid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r, max_rows);
   }
 }
 
