@@ -46,6 +46,23 @@ def step_bytes(sh, n, ls, c, esz, pdm_head=True):
     return target, pdm
 
 
+def step_bytes_active(sh, n, ls, c, a, esz):
+    """Algorithmic HBM bytes of a step (fused head) that starts with c committed positions and a
+    in-flight tokens: stages 0..a-1 run (the token at depth s runs stage s), the two-row head pass
+    runs every step, the PDM rewrites the a rows."""
+    d, V, L = sh.d_model, sh.vocab, sh.n_layers
+    kv_tok = 2 * sh.kv_dim * esz
+    layer_w = layer_bytes(sh, esz)
+    beta = [s * L // n for s in range(n + 1)]
+    target = V * d * esz
+    for s in range(a):
+        pos = c + a - 1 - s
+        nl = beta[s + 1] - beta[s]
+        target += nl * (layer_w + (pos + 1) * kv_tok + kv_tok)
+    pdm_kv = sum((c + i + 1) for i in range(a)) * ls * kv_tok + a * ls * kv_tok
+    return target + d * n * d * esz + ls * layer_w + pdm_kv
+
+
 def layer_bytes(sh, esz):
     d, F, qd, kvd = sh.d_model, sh.ffn_dim, sh.q_dim, sh.kv_dim
     return (qd * d + 2 * kvd * d + d * qd + 3 * F * d) * esz + 2 * d * 4
@@ -384,7 +401,15 @@ def main():
     for r in logp:
         if r["decision"] != B.SPD_NONE:
             assert r["decision"] == (B.SPD_ACCEPT if mask[r["verified_pos"]] else B.SPD_REJECT)
-    log(f"[bench] p={p}: alpha={alpha:.3f}, {spd_tok_s:.0f} tok/s (AR {ar_tok_s:.0f} tok/s)")
+    # run mean over every step of the pattern (fill and refill steps stream only the active stages)
+    run_bytes, c_pre, a_pre = 0, P, 1
+    for r in logp:
+        run_bytes += step_bytes_active(sh, n, sh.pdm_layers, c_pre, a_pre, esz)
+        c_pre, a_pre = r["committed_len"], r["inflight"]
+    run_mean = {"us_per_step": round(1e6 * elp / K, 1), "GB_per_step": round(run_bytes / K / 1e9, 3),
+                "GBps": round(run_bytes / elp / 1e9, 1),
+                "frac": round(run_bytes / elp / 1e9 / PEAK_HBM_GBS, 4)} if fused else None
+    log(f"[bench] p={p}: alpha={alpha:.3f}, {spd_tok_s:.0f} tok/s (AR {ar_tok_s:.0f} tok/s); run mean {run_mean}")
     eng.close()
 
     extra = args.extra_phases == "on" or (args.extra_phases == "auto" and P <= 4096)
@@ -470,7 +495,7 @@ def main():
         "pdm_overlap": spans,
         "hbm_read_probe": probe,
         "tokens_per_s": {"spd_forced_p": p, "alpha": round(alpha, 4), "spd": round(spd_tok_s, 1),
-                         "ar_same_gpu": round(ar_tok_s, 1)},
+                         "ar_same_gpu": round(ar_tok_s, 1), "run_mean": run_mean},
         "pdm_own_head": own_head,
         "sampled": sampled,
         "cpu_baseline": cpu,
