@@ -92,3 +92,41 @@ def test_init_rejects_null_arguments_before_touching_the_gpu():
     assert B.lib().spd_step(None, None, None) == B.SPD_E_INVAL
     assert B.lib().spd_rollback(None, 0, 0) == B.SPD_E_INVAL
     assert B.lib().spd_prefill(None, None, 0, None) == B.SPD_E_INVAL
+
+
+def test_pdm_vocab_config_rules():
+    """The PDM's own head: pdm_vocab in [0, vocab], and an own head needs fused_head = 0 (the exit
+    row and the PDM's row then stream different weights)."""
+    sh = synth.TINY.with_(pdm_vocab=300)
+    assert B.spd_workspace_size(make_config(sh, 128, fused_head=False)) > 0
+    for cfg in (make_config(sh, 128, fused_head=True),
+                make_config(synth.TINY.with_(pdm_vocab=synth.TINY.vocab + 1), 128, fused_head=False),
+                make_config(synth.TINY.with_(pdm_vocab=-1), 128, fused_head=False)):
+        with pytest.raises(B.SPDError) as e:
+            B.spd_workspace_size(cfg)
+        assert e.value.status == B.SPD_E_INVAL
+
+
+def test_init_needs_the_own_head_pointers_before_touching_the_gpu():
+    import ctypes as ct
+    sh = synth.TINY.with_(pdm_vocab=300)
+    cfg = make_config(sh, 128, fused_head=False)
+    fake = 4096  # never dereferenced: the call fails on its argument checks first
+    lw = B.spd_layer_weights(*([fake] * 9))
+    layers = (B.spd_layer_weights * sh.n_layers)(*([lw] * sh.n_layers))
+    pdm = (B.spd_layer_weights * sh.pdm_layers)(*([lw] * sh.pdm_layers))
+    w = B.spd_weights()
+    for f in ("embed", "final_norm", "lm_head", "pdm_in", "pdm_norm"):
+        setattr(w, f, fake)
+    w.layers = ct.cast(layers, ct.POINTER(B.spd_layer_weights))
+    w.pdm_layers = ct.cast(pdm, ct.POINTER(B.spd_layer_weights))
+    h = ct.c_void_p(0)
+    st = B.lib().spd_init(ct.byref(cfg), ct.byref(w), ct.c_void_p(0), 0, ct.c_void_p(1), ct.c_void_p(2),
+                          ct.byref(h))
+    assert st == B.SPD_E_INVAL and h.value is None
+    assert "pdm_lm_head" in B.lib().spd_last_error(None).decode()
+
+
+def test_new_setters_check_their_handle():
+    assert B.lib().spd_set_sampling(None, 8, 1.0, None, 0) == B.SPD_E_INVAL
+    assert B.lib().spd_set_pdm_schedule(None, 1) == B.SPD_E_INVAL
