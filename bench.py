@@ -215,7 +215,7 @@ def main():
     esz = 2 if sh.dtype == "bf16" else 4
     K_GU, K_CLS, K_SPAN = 64, 16, 64
     # greedy reference long enough for every forced-accept phase below
-    n_ref = W + K + K_GU + 5 * K_CLS + 4 * K_SPAN + 2 * n + 24
+    n_ref = W + K + K_GU + 6 * K_CLS + 4 * K_SPAN + 2 * n + 32
     # capacity and attention split size depend on the workload only (not on --steps), so that a
     # profiled run with fewer steps launches exactly the kernels the timed run launches
     max_tokens = P + max(1024, n_ref + 4 * n + 64)
@@ -334,6 +334,20 @@ def main():
                           "bytes_per_launch": int(lb), "GBps": round(lb / (us * 1e-6) / 1e9, 1)}
     log(f"[bench] kernels: {kernels}")
     dk = kernels[dominant]
+    # the same kernel with nothing beside it: one stage group, so each gate/up launch covers all n
+    # stages and no other launch shares the GPU (context for the concurrent figure above)
+    isolated = None
+    if mode == 2:
+        eng.spd_set_step_kernel(2, args.step_grid, 1)
+        eng.spd_run_steps(2)
+        ms, nl, cm = time_class(B.SPD_K_GATEUP, K_CLS)
+        lb = launch_bytes(sh, n, cm, esz)["gateup"]
+        us = 1e3 * ms / max(1, nl)
+        isolated = {"stage_groups": 1, "bytes_per_launch": int(lb), "us_per_launch": round(us, 2),
+                    "GBps": round(lb / (us * 1e-6) / 1e9, 1), "frac": round(lb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        eng.spd_set_step_kernel(2, args.step_grid, args.stage_groups)
+        eng.spd_run_steps(2)
+        log(f"[bench] gate/up with one stage group: {isolated}")
 
     # PDM overlap: step start -> end of the stage compute (main) and -> end of the PDM (side stream)
     B.spd_set_kernel_timing(eng.h, B.SPD_K_SPANS)
@@ -490,7 +504,8 @@ def main():
                                    "one group of workgroups per stage"}[mode],
                      "bytes_per_launch": dk["bytes_per_launch"], "us_per_launch": dk["us_per_launch"],
                      "timing": f"dispatch-recorded HIP events on the launching stream, layer slots >= {first_slot} of "
-                               f"{L_slots}, {K_GU} steady-state steps"},
+                               f"{L_slots}, {K_GU} steady-state steps",
+                     "isolated": isolated},
         "kernels": kernels,
         "pdm_overlap": spans,
         "hbm_read_probe": probe,
