@@ -181,7 +181,9 @@ spd_status spd_clear_forced_drafts(spd_handle* h);
  * value-descending order: the first i with u * sum < cumsum_i.
  * uniforms: host float[3 * positions], positions == max_tokens; entry 3*pos + j is position pos's
  * u_draft (j = 0), u_accept (1) and u_resample (2), each in [0, 1); copied during the call.
- * top_k in [1, 64] turns sampling on (needs fused_head = 1, so the shared head); top_k = 0 returns
+ * top_k in [1, 64] turns sampling on, with either head form: the two-row pass selects both
+ * distributions in its last workgroup; otherwise the draft module's own pass (shared or own head)
+ * selects q and leaves it for the exit row's pass, which selects p and verifies. top_k = 0 returns
  * to greedy decoding (uniforms may then be NULL). Legal only before spd_prefill (SPD_E_STATE
  * afterwards); SPD_E_INVAL for other top_k, a temperature that is not finite and > 0, a uniforms
  * array of another length or a value outside [0, 1). In a sampled step

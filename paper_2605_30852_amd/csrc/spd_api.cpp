@@ -26,7 +26,7 @@ struct Layout {
   size_t kv, pkv, pt, rope, state, tok, forced, log, resid, anch, pdmx, pfx, pfanch, dbg, lay;
   size_t q[2], ao[2], act[2], part[2], cnt[2], hkey[2];
   size_t items, sync, dctx, trace, ktrace;
-  size_t su, swlog, swgmax, sqids, sqp, sqcnt;  // sampled decoding
+  size_t su, swlog, swgmax, sqids, sqp, sqcnt, spq;  // sampled decoding
   size_t total;
   int wlog_stride;
   int num_pages, chunk, max_splits, J, nitems, nsync, ntrace, nkslots;
@@ -144,6 +144,7 @@ Layout make_layout(const spd_config& c) {
   L.sqids = take(sizeof(int32_t) * n * kMaxTopK);
   L.sqp = take(sizeof(float) * n * kMaxTopK);
   L.sqcnt = take(sizeof(int32_t) * n);
+  L.spq = take((sizeof(int32_t) + sizeof(float)) * kMaxTopK + sizeof(int32_t));
   L.total = o;
   return L;
 }
@@ -327,6 +328,8 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
       const int l = (i - 1) / 5, k = (i - 1) % 5;
       Launch<WT>::rows_sublayer(C, rows_block(h->cfg.n_layers + l, -1, -1, C.pdm_x, nullptr, -1, 1),
                                 h->cfg.n_stages, k, C.rows_wgs, s);
+    } else if (C.sam.top_k > 0) {  // the draft module's distribution, left for the exit row's pass
+      Launch<WT>::head_sample(C, 1, 0, 0, -1, 0, s);
     } else {
       Launch<WT>::head(C, 1, 0, s);
     }
@@ -531,7 +534,10 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
   if (sp) HIPC(hipEventRecord(sp[2], h->main));
   HIPC(hipStreamWaitEvent(h->main, h->ev_join, 0));
   TimedLaunch t(h, h->main, SPD_K_HEAD);
-  Launch<WT>::head_verify(C, 0, forced_override, h->cfg.auto_rollback, h->main);
+  if (C.sam.top_k > 0)  // + the exit row's distribution, the draft's draw and the sampled verify
+    Launch<WT>::head_sample(C, 0, 0, 0, forced_override, h->cfg.auto_rollback, h->main);
+  else
+    Launch<WT>::head_verify(C, 0, forced_override, h->cfg.auto_rollback, h->main);
   return launch_check(h, "step");
 }
 
@@ -749,6 +755,9 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   C.sam.q_ids = (int32_t*)(ws + lay.sqids);
   C.sam.q_p = (float*)(ws + lay.sqp);
   C.sam.q_cnt = (int32_t*)(ws + lay.sqcnt);
+  C.sam.pq_ids = (int32_t*)(ws + lay.spq);
+  C.sam.pq_p = (float*)(ws + lay.spq + sizeof(int32_t) * kMaxTopK);
+  C.sam.pq_cnt = (int32_t*)(ws + lay.spq + (sizeof(int32_t) + sizeof(float)) * kMaxTopK);
   C.plan.items = (const uint32_t*)(ws + lay.items);
   C.plan.nitems = lay.nitems;
   C.plan.sync = (int32_t*)(ws + lay.sync);
@@ -810,6 +819,7 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   HIPI(hipMemcpyAsync(ws + lay.items, items.data(), sizeof(uint32_t) * items.size(), hipMemcpyHostToDevice, h->main));
   HIPI(hipMemsetAsync(ws + lay.sync, 0, sizeof(int32_t) * lay.nsync, h->main));
   HIPI(hipMemsetAsync(ws + lay.sqcnt, 0, sizeof(int32_t) * c.n_stages, h->main));
+  HIPI(hipMemsetAsync(ws + lay.spq, 0, (sizeof(int32_t) + sizeof(float)) * kMaxTopK + sizeof(int32_t), h->main));
   // the persistent step kernel reads the context from device memory
   HIPI(hipMemcpyAsync(ws + lay.dctx, &C, sizeof(Ctx), hipMemcpyHostToDevice, h->main));
   HIPI(hipStreamSynchronize(h->main));
@@ -898,8 +908,6 @@ spd_status spd_set_sampling(spd_handle* h, int32_t top_k, float temperature, con
   }
   if (top_k < 0 || top_k > kMaxTopK) return refuse(h, "top_k must be in [0, 64]");
   if (!(temperature > 0.f) || !std::isfinite(temperature)) return refuse(h, "temperature must be > 0");
-  if (!h->cfg.fused_head) return refuse(h, "sampled decoding needs fused_head = 1");
-  if (h->cfg.pdm_vocab > 0) return refuse(h, "sampled decoding needs the shared PDM head");
   if (!uniforms || positions != h->cfg.max_tokens)
     return refuse(h, "uniforms must hold 3 * max_tokens values");
   for (size_t i = 0; i < (size_t)3 * positions; i++)

@@ -109,6 +109,10 @@ struct Sampler {
   int32_t* q_ids;             // [n][kMaxTopK]
   float* q_p;                 // [n][kMaxTopK]
   int32_t* q_cnt;             // [n]
+  // the draft module's top-k distribution when its row has its own head pass (target ids)
+  int32_t* pq_ids;            // [kMaxTopK]
+  float* pq_p;                // [kMaxTopK]
+  int32_t* pq_cnt;            // [1]
 };
 
 struct StepPlan {

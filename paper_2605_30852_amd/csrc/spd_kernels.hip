@@ -1260,6 +1260,24 @@ __global__ __launch_bounds__(kWG) void k_head_sample(Ctx C, int src, int row, in
     const int kq = select_top_k(C, 1, S);
     const int kp = C.st->a == C.n ? select_top_k(C, 0, S) : 0;
     sampled_verify<WT>(C, S, kq, kp, forced_override, auto_rb);
+  } else if (src == 1) {  // the draft module's own pass: leave q (as target tokens) for the exit row's
+    const int kq = select_top_k(C, 1, S);
+    for (int j = threadIdx.x; j < kq; j += kWG) {
+      const int id = S.ids[1][j];
+      __hip_atomic_store(C.sam.pq_ids + j, C.pdm_V > 0 ? C.pdm_map[id] : id, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      st_dev(C.sam.pq_p + j, S.p[1][j]);
+    }
+    if (threadIdx.x == 0) __hip_atomic_store(C.sam.pq_cnt, kq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  } else if (src == 0) {  // the exit row's pass after the draft module's: p, the left q, the verify
+    const int kp = C.st->a == C.n ? select_top_k(C, 0, S) : 0;
+    const int kq = min(max(ld_dev_i(C.sam.pq_cnt), 1), kMaxTopK);
+    for (int j = threadIdx.x; j < kq; j += kWG) {  // (ids kept inside the vocabulary: they are embedded)
+      S.ids[1][j] = min(max(ld_dev_i(C.sam.pq_ids + j), 0), C.V - 1);
+      S.p[1][j] = ld_dev(C.sam.pq_p + j);
+    }
+    __syncthreads();
+    sampled_verify<WT>(C, S, kq, kp, forced_override, auto_rb);
   } else {
     const int k = select_top_k(C, 0, S);
     if (threadIdx.x == 0) {
@@ -1543,7 +1561,7 @@ void Launch<WT>::head_sample(const Ctx& c, int src, int row, int pos, int forced
   // afterwards; a smaller grid (fewer resident workgroups) means larger regions, so settle both
   constexpr int BLK = 64 * Elt<WT>::VE;
   const size_t kl_pad = (size_t)(c.d + BLK - 1) / BLK * BLK;
-  const int np = (c.V + 1) / 2;
+  const int np = ((src == 1 && c.pdm_V > 0 ? c.pdm_V : c.V) + 1) / 2;
   const int nv = src == 3 ? 2 : 1;
   const void* fn = src == 3 ? (const void*)k_head_sample<WT, 2> : (const void*)k_head_sample<WT, 1>;
   int grid = std::max(std::min(stream_grid(c, np, 1), kSampleWGs), 1);

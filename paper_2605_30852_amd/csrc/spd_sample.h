@@ -97,13 +97,18 @@ __device__ unsigned long long select_kth(Visit visit, int k, SelLds& S) {
   return prefix;
 }
 
+// Vocabulary rows of a set's head: the draft module's own head for set 1 when it has one.
+__device__ __forceinline__ int set_rows(const Ctx& C, int set) {
+  return set == 1 && C.pdm_V > 0 ? C.pdm_V : C.V;
+}
+
 // Every logit key of row `set` in the regions of the workgroups listed in S.sel[0..nsel) that is
 // >= tlo, handed to f (each thread its share). The region geometry is the head's (see Sampler): a
 // workgroup's four wave regions are consecutive, 4 * cmax floats (cmax even), so the entries go as
 // 8-byte pairs, eight device-scope loads in flight per thread before any is looked at.
 template <typename F>
 __device__ void visit_regions(const Ctx& C, int set, const SelLds& S, int nsel, unsigned long long tlo, F f) {
-  const int V = C.V, NW = (int)gridDim.x * 4, npairs = (V + 1) / 2;
+  const int V = set_rows(C, set), NW = (int)gridDim.x * 4, npairs = (V + 1) / 2;
   const int cmax = 2 * ((npairs + NW - 1) / NW);
   const int per2 = 2 * cmax;  // pairs per workgroup
   const int total = nsel * per2;
@@ -145,7 +150,7 @@ __device__ void visit_regions(const Ctx& C, int set, const SelLds& S, int nsel, 
 // V) largest logits, value descending (lower index first among equal values), and their softmax at
 // temperature 1/inv_temp (max-subtracted, fp32). Whole workgroup; returns k.
 __device__ int select_top_k(const Ctx& C, int set, SelLds& S) {
-  const int tid = threadIdx.x, lane = tid & 63, G = (int)gridDim.x, V = C.V;
+  const int tid = threadIdx.x, lane = tid & 63, G = (int)gridDim.x, V = set_rows(C, set);
   const int k = min(C.sam.top_k, V);
   unsigned long long gm = 0ull;  // G <= kSampleWGs = 4 * kWG: at most four maxima per thread
   {

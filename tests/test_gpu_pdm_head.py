@@ -3,7 +3,8 @@
 Lockstep against the oracle's own-head PDM (its logits over the draft vocabulary, drafts mapped to
 target tokens, and everything the pre-step lockstep checks), a 4B-class run in the benchmark's launch
 form whose drafts are the mapped argmax of the HIP path's own PDM logits and whose stream is greedy
-decoding bit for bit, and the argument checks at spd_init and spd_set_sampling."""
+decoding bit for bit, and the argument checks at spd_init. (Sampled decoding with the own head is in
+tests/test_gpu_sampling.py.)"""
 import sys
 
 import numpy as np
@@ -79,10 +80,6 @@ def test_own_head_argument_checks(tiny_w):
     bad.t["pdm.vocab_map"] = m
     with pytest.raises(SPDError):
         _engine(bad, 2)
-    eng = _engine(w, 2)
-    with pytest.raises(SPDError):
-        eng.spd_set_sampling(8, 1.0, np.random.default_rng(0).random((160, 3)))
-    eng.close()
 
 
 def test_fullsize_4b_own_head_drafts_and_lossless():

@@ -145,12 +145,16 @@ def _kth_gap(logits, k):
     return s[k - 1] - s[k] if k < len(s) else np.inf
 
 
-@pytest.mark.parametrize("n,k,temp,forced,schedule", [(1, 8, 1.0, False, "pre"), (2, 8, 0.5, True, "pre"),
-                                                      (2, 64, 1.0, False, "pre"), (3, 16, 0.2, True, "pre"),
-                                                      (4, 50, 0.7, False, "pre"), (3, 16, 0.5, False, "post")])
-def test_sampled_lockstep_matches_oracle(tiny_w, n, k, temp, forced, schedule):
-    _say(f"[sampled lockstep n={n} k={k} T={temp} forced={forced} schedule={schedule}]")
-    sh = synth.TINY
+@pytest.mark.parametrize("n,k,temp,forced,schedule,head", [
+    (1, 8, 1.0, False, "pre", "fused"), (2, 8, 0.5, True, "pre", "fused"), (2, 64, 1.0, False, "pre", "fused"),
+    (3, 16, 0.2, True, "pre", "fused"), (4, 50, 0.7, False, "pre", "fused"), (3, 16, 0.5, False, "post", "fused"),
+    (2, 16, 0.5, False, "pre", "unfused"), (2, 16, 0.5, False, "pre", "own"), (3, 8, 0.3, True, "post", "own")])
+def test_sampled_lockstep_matches_oracle(tiny_w, n, k, temp, forced, schedule, head):
+    """head: the two-row pass ("fused"), the PDM's own pass over the shared head ("unfused") or over
+    its own 300-token head ("own"); the last two select q in the PDM's pass and p in the exit row's."""
+    _say(f"[sampled lockstep n={n} k={k} T={temp} forced={forced} schedule={schedule} head={head}]")
+    w = tiny_w.with_pdm_vocab(300) if head == "own" else tiny_w
+    sh = w.shape
     model = om.Model(sh, SEED)
     prompt = synth.prompt(sh, SEED, 21)
     P, steps, rows = len(prompt), 28, 96
@@ -163,7 +167,7 @@ def test_sampled_lockstep_matches_oracle(tiny_w, n, k, temp, forced, schedule):
     U = _clear_uniforms(model, prompt, n, k, temp, rows, steps, draft_for, seed=100 * n + k, schedule=schedule)
     _, ties, _ = _oracle_run(model, prompt, n, k, temp, U, steps, draft_for, nudge=False, schedule=schedule)
     ora = osp.SPDOracle(model, n=n, sampling=smp.Sampling(k, temp, U), schedule=schedule)
-    eng = _engine(tiny_w, n, rows)
+    eng = _engine(w, n, rows, fused_head=head == "fused")
     eng.spd_set_pdm_schedule(schedule == "post")
     eng.spd_set_sampling(k, temp, U)
     eng.spd_set_debug(True)
@@ -242,10 +246,6 @@ def test_sampling_setter_rules(tiny_w):
     with pytest.raises(SPDError):
         eng.spd_set_sampling(0)  # only before prefill
     eng.close()
-    unfused = _engine(tiny_w, 2, rows, fused_head=False)
-    with pytest.raises(SPDError):
-        unfused.spd_set_sampling(8, 1.0, U)
-    unfused.close()
 
 
 def test_fullsize_4b_sampled_step_selection():
