@@ -1,7 +1,8 @@
 """Parity at the full 4B-class size (36 layers, d 2560, 32/8 heads of 128, FFN 9728, vocabulary 151936,
-bf16 weights and KV, SPD width n = 4, one-layer draft module) in the launch configuration the benchmark
-times: stage compute on one stream per stage, every step replayed from the captured step graph, the
-exit and draft LM heads sharing one pass over the vocabulary.
+bf16 weights and KV, SPD width n = 4, one-layer draft module) and the full 9B-class size (d 4096, FFN
+12288, otherwise alike) in the launch configuration the benchmark times: the stage compute in stage
+groups on their own streams, every step replayed from the captured step graph, the exit and draft LM
+heads sharing one pass over the vocabulary.
 
 The prompt is short so that the float64 oracle can recompute every sampled output one by one: the GPU's
 in-flight residual streams and PDM anchors after each step, and the exit token's full-vocabulary logits,
@@ -28,15 +29,16 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def test_fullsize_4b_step_parity():
+@pytest.mark.parametrize("which", ["4b", "9b"])
+def test_fullsize_step_parity(which):
     from paper_2605_30852_amd.engine import DeviceWeights, Engine
 
-    sh = synth.B4
+    sh = {"4b": synth.B4, "9b": synth.B9}[which]
     n, L, P, seed = sh.n_stages, sh.n_layers, 20, 0
     prompt = synth.prompt(sh, seed, P)
     chunk = max(64, (P // 16 + 63) // 64 * 64)  # the benchmark's split size for this prompt length
     t0 = time.time()
-    _say("[fullsize 4b] uploading weights")
+    _say(f"[fullsize {which}] uploading weights")
     W = DeviceWeights(sh, seed, threads=16)
     ar = Engine(W, max_tokens=P + 64, n=1, attn_chunk=chunk)
     ar.spd_set_graph(True)
@@ -60,13 +62,13 @@ def test_fullsize_4b_step_parity():
     eng.close()
     del W
     torch.cuda.empty_cache()
-    _say(f"[fullsize 4b] GPU done in {time.time() - t0:.0f}s; oracle forward over the same tokens")
+    _say(f"[fullsize {which}] GPU done in {time.time() - t0:.0f}s; oracle forward over the same tokens")
     last = max(c + a for _, c, a, _, _, _ in snaps)
     tokens = np.concatenate([prompt, ref[: last - P]])
     model = om.Model(sh, seed)
     beta = osp.stage_bounds(L, n)
     full = om.forward_full(model, tokens, free_layers=True)
-    _say(f"[fullsize 4b] oracle done in {time.time() - t0:.0f}s")
+    _say(f"[fullsize {which}] oracle done in {time.time() - t0:.0f}s")
 
     lg = om.lm_logits(model, full[L][P - 1])
     if om.argmax_first(lg) != first:
@@ -93,5 +95,5 @@ def test_fullsize_4b_step_parity():
             if r["target_argmax"] != om.argmax_first(lo):
                 assert margin(lo) < TIE_MARGIN, f"step {i}: target argmax differs"
                 break
-    _say(f"[fullsize 4b] worst hidden rel L2 {worst_h:.2e}, worst logit abs {worst_l:.2e}, {exits} exits")
+    _say(f"[fullsize {which}] worst hidden rel L2 {worst_h:.2e}, worst logit abs {worst_l:.2e}, {exits} exits")
     assert exits >= 4
