@@ -2,7 +2,8 @@
 bf16 weights and KV, SPD width n = 4, one-layer draft module) and the full 9B-class size (d 4096, FFN
 12288, otherwise alike) in the launch configuration the benchmark times: the stage compute in stage
 groups on their own streams, every step replayed from the captured step graph, the exit and draft LM
-heads sharing one pass over the vocabulary.
+heads sharing one pass over the vocabulary. The long-context configuration's shape (9B-class, n = 8
+with stages of 4-5 layers, two-layer draft module) runs with a short prompt as well.
 
 The prompt is short so that the float64 oracle can recompute every sampled output one by one: the GPU's
 in-flight residual streams and PDM anchors after each step, and the exit token's full-vocabulary logits,
@@ -29,11 +30,11 @@ def _say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-@pytest.mark.parametrize("which", ["4b", "9b"])
+@pytest.mark.parametrize("which", ["4b", "9b", "9b-n8"])
 def test_fullsize_step_parity(which):
     from paper_2605_30852_amd.engine import DeviceWeights, Engine
 
-    sh = {"4b": synth.B4, "9b": synth.B9}[which]
+    sh = {"4b": synth.B4, "9b": synth.B9, "9b-n8": synth.B9_LONG}[which]
     n, L, P, seed = sh.n_stages, sh.n_layers, 20, 0
     prompt = synth.prompt(sh, seed, P)
     chunk = max(64, (P // 16 + 63) // 64 * 64)  # the benchmark's split size for this prompt length
@@ -43,9 +44,11 @@ def test_fullsize_step_parity(which):
     ar = Engine(W, max_tokens=P + 64, n=1, attn_chunk=chunk)
     ar.spd_set_graph(True)
     first = ar.spd_prefill(prompt)
-    ar.spd_run_steps(12)
+    steps = 8 if n <= 4 else 2 * n + 4  # the pipeline fills in n - 1 steps, then one exit per step
+    nref = steps + n + 4
+    ar.spd_run_steps(nref - 1)
     ar.spd_sync()
-    ref = ar.tokens()[P:P + 13].astype(np.int32)
+    ref = ar.tokens()[P:P + nref].astype(np.int32)
     ar.close()
     assert ref[0] == first
     eng = Engine(W, max_tokens=P + 64, n=n, attn_chunk=chunk)
@@ -54,7 +57,7 @@ def test_fullsize_step_parity(which):
     assert eng.spd_prefill(prompt) == first
     eng.spd_set_forced_drafts(ref, P)
     snaps = []
-    for i in range(8):
+    for i in range(steps):
         r = eng.spd_run_steps(1, want_log=True)[0]
         c, a, _, _ = eng.state()
         snaps.append((r, c, a, eng.resid().copy(), eng.anchors().copy(),
