@@ -58,9 +58,8 @@ def trace(path, kernel, grid_y):
 
 
 def _counter(path, kernel, grid_y):
-    """Values of the kernel's dispatches (grid y = grid_y when the file records grid dimensions;
-    otherwise the cluster of largest values, within 3/4 of the largest, which separates launches
-    covering more stages), the largest device copy's value, and how the dispatches were selected."""
+    """Values of the kernel's dispatches in dispatch order (only grid y = grid_y when the file records
+    grid dimensions), whether it does, and the largest device copy's value."""
     vals, copies, has_y = [], [], False
     for r in _rows(path):
         v = float(r["Counter_Value"])
@@ -69,19 +68,30 @@ def _counter(path, kernel, grid_y):
             vals.append(v)
         if "copyBuffer" in r.get("Kernel_Name", ""):
             copies.append(v)
-    how = f"grid y = {grid_y}" if (has_y or grid_y is None) else "largest-value cluster (>= 3/4 of the largest)"
-    if grid_y is not None and not has_y and vals:
-        top = max(vals)
-        vals = [v for v in vals if v >= 0.75 * top]
-    return vals, (max(copies) if copies else None), how
+    return vals, has_y, (max(copies) if copies else None)
 
 
 def traffic(fetch, write, kernel, grid_y, algo, source):
-    fv, fc, how = _counter(fetch, kernel, grid_y)
-    wv, wc, _ = _counter(write, kernel, grid_y)
+    fv, has_y, fc = _counter(fetch, kernel, grid_y)
+    wv, _, wc = _counter(write, kernel, grid_y)
     if not fv or not wv or not fc or not wc:
         return "incomplete: " + repr((len(fv), len(wv), fc, wc))
     sf, sw = GIB_KIB / fc, GIB_KIB / wc
+    how = f"grid y = {grid_y}"
+    if grid_y is not None and not has_y:
+        # no grid shape in the file: launches covering other stage counts read other amounts, so keep
+        # the dispatches whose fetch is within 1/4 of the algorithmic bytes (else the largest-value
+        # cluster), and the same dispatch ordinals of the write run (both runs issue the same sequence)
+        if algo:
+            keep = [i for i, v in enumerate(fv) if 0.75 * algo <= v * sf * 1024.0 <= 1.25 * algo]
+            how = "fetch within 1/4 of the algorithmic bytes"
+        else:
+            top = max(fv)
+            keep = [i for i, v in enumerate(fv) if v >= 0.75 * top]
+            how = "largest-value cluster (>= 3/4 of the largest)"
+        if len(wv) != len(fv) or not keep:
+            return "incomplete: " + repr((len(fv), len(wv), len(keep)))
+        fv, wv = [fv[i] for i in keep], [wv[i] for i in keep]
     fk, wk = statistics.median(fv), statistics.median(wv)
     hbm = (fk * sf + wk * sw) * 1024.0
     lines = [f"kernel={kernel}", f"selection={how}", f"dispatches_fetch={len(fv)}", f"dispatches_write={len(wv)}",
