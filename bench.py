@@ -186,6 +186,7 @@ def main():
                     help="PDM launches: own stream, main before the stages, first group before/after, "
                          "spread over the groups")
     ap.add_argument("--attn-chunk", type=int, default=0, help="keys per attention split (0: the workload's default)")
+    ap.add_argument("--graph-steps", type=int, default=1, help="steps per replayed graph in batched runs")
     ap.add_argument("--extra-phases", choices=["auto", "on", "off"], default="auto",
                     help="the PDM's own head and sampled decoding, each on a handle of its own (auto: on "
                          "for prompts up to 4096 tokens; each needs its own prefill)")
@@ -265,6 +266,7 @@ def main():
     eng.spd_set_pdm_placement(args.pdm_place)
     eng.spd_set_pdm_grid(args.pdm_grid)
     eng.spd_set_graph(not args.no_graph)
+    eng.spd_set_graph_steps(args.graph_steps)
     groups = B.spd_step_plan_info(eng.h)["stage_groups"]
     f2 = eng.spd_prefill(prompt)
     assert f2 == first

@@ -200,6 +200,12 @@ spd_status spd_set_sampling(spd_handle* h, int32_t top_k, float temperature, con
  * unchanged. Legal in any state; SPD_E_INVAL for other values. */
 spd_status spd_set_pdm_schedule(spd_handle* h, int32_t post_step);
 
+/* Steps per replayed graph in spd_run_steps (graph mode): `steps` consecutive steps are captured into
+ * one graph, so the device runs them with no host launch between them; a remainder below `steps`
+ * replays the one-step graph. steps in [1, 16] (default 1); SPD_E_INVAL otherwise. Results are
+ * identical for every value. */
+spd_status spd_set_graph_steps(spd_handle* h, int32_t steps);
+
 /* Enqueue `count` steps without host synchronisation (needs auto_rollback = 1). If log is not
  * NULL (host, count entries) the call waits and fills it with each step's result; otherwise it
  * returns once the work is enqueued and spd_sync() waits. */

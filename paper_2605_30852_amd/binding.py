@@ -65,7 +65,7 @@ EXPORTS = [
     "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing", "spd_set_step_kernel",
     "spd_set_step_trace", "spd_step_plan_info", "spd_set_kernel_trace", "spd_set_pdm_placement",
     "spd_set_pdm_grid", "spd_set_pdm_enabled", "spd_probe_hbm_read", "spd_set_sampling",
-    "spd_set_pdm_schedule",
+    "spd_set_pdm_schedule", "spd_set_graph_steps",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -110,6 +110,7 @@ def lib() -> ct.CDLL:
             "spd_set_pdm_grid": (I, [P, I]),
             "spd_set_pdm_enabled": (I, [P, I]),
             "spd_set_pdm_schedule": (I, [P, I]),
+            "spd_set_graph_steps": (I, [P, I]),
             "spd_set_sampling": (I, [P, I, ct.c_float, ct.POINTER(ct.c_float), I]),
             "spd_probe_hbm_read": (I, [P, ct.c_size_t, P, I, P, ct.POINTER(ct.c_double)]),
             "spd_step_plan_info": (I, [P, ct.POINTER(ct.c_int32)]),
@@ -268,6 +269,10 @@ def spd_set_pdm_placement(h: int, place: int) -> None:
 
 def spd_set_pdm_enabled(h: int, on: bool) -> None:
     _check("spd_set_pdm_enabled", lib().spd_set_pdm_enabled(h, 1 if on else 0), h)
+
+
+def spd_set_graph_steps(h: int, steps: int) -> None:
+    _check("spd_set_graph_steps", lib().spd_set_graph_steps(h, int(steps)), h)
 
 
 def spd_set_pdm_schedule(h: int, post_step: bool) -> None:

@@ -206,6 +206,8 @@ struct spd_handle {
   int pdm_on = 1;        // 0: the step skips the PDM's launches (spd_set_pdm_enabled)
   int pstep_grid = 0;  // mode 4: workgroups, at most what the GPU holds at once
   hipGraphExec_t gexec = nullptr;
+  hipGraphExec_t gexec_multi = nullptr;  // graph_steps steps in one graph (spd_run_steps)
+  int graph_steps = 1;
   // kernel timing
   int timed_kernel = 0;
   int timed_first_slot = 0;
@@ -1083,7 +1085,36 @@ spd_status spd_step(spd_handle* h, const int32_t* forced_draft, spd_step_result*
 
 static void drop_graph(spd_handle* h) {
   if (h->gexec) (void)hipGraphExecDestroy(h->gexec);
+  if (h->gexec_multi) (void)hipGraphExecDestroy(h->gexec_multi);
   h->gexec = nullptr;
+  h->gexec_multi = nullptr;
+}
+
+// Capture `steps` consecutive steps (each the launches of enqueue_step) into one executable graph.
+// Nothing a step enqueues depends on host state, so the steps chain on the device alone.
+static spd_status capture_steps(spd_handle* h, int steps, hipGraphExec_t* out) {
+  hipGraph_t g = nullptr;
+  HIPC(hipStreamBeginCapture(h->main, hipStreamCaptureModeRelaxed));
+  spd_status st = SPD_OK;
+  for (int i = 0; i < steps && st == SPD_OK; i++)
+    st = h->bf16 ? enqueue_step<uint16_t>(h, -1) : enqueue_step<float>(h, -1);
+  hipError_t e = hipStreamEndCapture(h->main, &g);
+  if (st != SPD_OK) {
+    if (g) (void)hipGraphDestroy(g);
+    return st;
+  }
+  if (e != hipSuccess) {
+    h->err = std::string("hipStreamEndCapture: ") + hipGetErrorString(e);
+    return SPD_E_HIP;
+  }
+  e = hipGraphInstantiate(out, g, nullptr, nullptr, 0);
+  (void)hipGraphDestroy(g);
+  if (e != hipSuccess) {
+    *out = nullptr;
+    h->err = std::string("hipGraphInstantiate: ") + hipGetErrorString(e);
+    return SPD_E_HIP;
+  }
+  return SPD_OK;
 }
 
 // One step: a replay of the captured step graph when graph mode is on (and no per-step override or
@@ -1092,24 +1123,17 @@ static spd_status run_one_step(spd_handle* h, int forced_override) {
   const bool graph = h->use_graph && forced_override < 0 && h->timed_kernel == 0;
   if (!graph) return h->bf16 ? enqueue_step<uint16_t>(h, forced_override) : enqueue_step<float>(h, forced_override);
   if (!h->gexec) {
-    hipGraph_t g = nullptr;
-    HIPC(hipStreamBeginCapture(h->main, hipStreamCaptureModeRelaxed));
-    spd_status st = h->bf16 ? enqueue_step<uint16_t>(h, -1) : enqueue_step<float>(h, -1);
-    hipError_t e = hipStreamEndCapture(h->main, &g);
+    spd_status st = capture_steps(h, 1, &h->gexec);
     if (st != SPD_OK) return st;
-    if (e != hipSuccess) {
-      h->err = std::string("hipStreamEndCapture: ") + hipGetErrorString(e);
-      return SPD_E_HIP;
-    }
-    e = hipGraphInstantiate(&h->gexec, g, nullptr, nullptr, 0);
-    (void)hipGraphDestroy(g);
-    if (e != hipSuccess) {
-      h->gexec = nullptr;
-      h->err = std::string("hipGraphInstantiate: ") + hipGetErrorString(e);
-      return SPD_E_HIP;
-    }
   }
   HIPC(hipGraphLaunch(h->gexec, h->main));
+  return SPD_OK;
+}
+
+spd_status spd_set_graph_steps(spd_handle* h, int32_t steps) {
+  if (!h || steps < 1 || steps > 16) return SPD_E_INVAL;
+  h->graph_steps = steps;
+  drop_graph(h);
   return SPD_OK;
 }
 
@@ -1130,7 +1154,17 @@ spd_status spd_run_steps(spd_handle* h, int32_t count, spd_step_result* log) {
   if (count > kLogCap && log) return SPD_E_INVAL;
   if (h->bound + count > h->cfg.max_tokens) return SPD_E_CAPACITY;
   HIPC(hipSetDevice(h->dev));
-  for (int i = 0; i < count; i++) {
+  int i = 0;
+  if (h->use_graph && h->timed_kernel == 0 && h->graph_steps > 1) {  // whole multi-step graphs first
+    for (; i + h->graph_steps <= count; i += h->graph_steps) {
+      if (!h->gexec_multi) {
+        spd_status st = capture_steps(h, h->graph_steps, &h->gexec_multi);
+        if (st != SPD_OK) return st;
+      }
+      HIPC(hipGraphLaunch(h->gexec_multi, h->main));
+    }
+  }
+  for (; i < count; i++) {
     spd_status st = run_one_step(h, -1);
     if (st != SPD_OK) return st;
   }

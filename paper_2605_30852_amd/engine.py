@@ -184,6 +184,9 @@ class Engine:
     def spd_set_pdm_placement(self, place: int) -> None:
         B.spd_set_pdm_placement(self.h, place)
 
+    def spd_set_graph_steps(self, steps: int) -> None:
+        B.spd_set_graph_steps(self.h, steps)
+
     def spd_set_pdm_schedule(self, post_step: bool) -> None:
         B.spd_set_pdm_schedule(self.h, post_step)
 

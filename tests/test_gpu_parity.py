@@ -196,10 +196,12 @@ def test_rollback_api_and_state_errors(tiny_w):
     eng.close()
 
 
-def test_graph_replay_matches_eager(mid_w):
-    """Steps replayed from the captured step graph give the same bits as launched steps, on every
-    replay, with eager work and synchronisation between the replays."""
-    _say("[graph replay]")
+@pytest.mark.parametrize("graph_steps", [1, 4])
+def test_graph_replay_matches_eager(mid_w, graph_steps):
+    """Steps replayed from the captured step graph (graph_steps steps per graph, and the one-step
+    graph for the remainder) give the same bits as launched steps, on every replay, with eager work
+    and synchronisation between the replays."""
+    _say(f"[graph replay, {graph_steps} steps per graph]")
     sh = mid_w.shape
     prompt = synth.prompt(sh, SEED + 6, 33)
     first, ar, _ = _gpu_stream(mid_w, 1, prompt, 30, max_tokens=200)
@@ -214,6 +216,8 @@ def test_graph_replay_matches_eager(mid_w):
         e.spd_prefill(prompt)
         e.spd_set_forced_drafts(arr, len(prompt))
         e.spd_set_graph(graph)
+        if graph:
+            e.spd_set_graph_steps(graph_steps)
         engs.append(e)
     for chunk in range(4):
         logs = [e.spd_run_steps(6, want_log=True) for e in engs]
