@@ -1,0 +1,43 @@
+"""The benchmark's byte accounting (CPU only): the algorithmic bytes the roofline figures divide by.
+
+A full-pipeline step (a = n) streams every layer's weights once, reads each stage token's keys, writes
+one K/V row per layer, makes one two-row pass over the LM head and runs the PDM over n rows; a step
+with a < n in-flight tokens streams only stages 0..a-1. These are checked against sums written out
+here from the shapes, independently of how bench.py arranges them."""
+import pytest
+
+import bench
+import synth
+
+
+def _layer(sh, esz):
+    d, F = sh.d_model, sh.ffn_dim
+    return (sh.q_dim * d + 2 * sh.kv_dim * d + d * sh.q_dim + 3 * F * d) * esz + 2 * d * 4
+
+
+@pytest.mark.parametrize("sh,n,c", [(synth.B4, 4, 2300), (synth.B9, 4, 4200), (synth.B4, 8, 8300)])
+def test_full_step_bytes_agree(sh, n, c):
+    esz = 2
+    tgt, pdm = bench.step_bytes(sh, n, sh.pdm_layers, c, esz, pdm_head=False)
+    active = bench.step_bytes_active(sh, n, sh.pdm_layers, c, n, esz)
+    assert abs((tgt + pdm) - active) <= sh.d_model * esz  # step_bytes also counts the exit row itself
+
+
+def test_one_token_step_is_stage_zero_plus_head_and_pdm():
+    sh, n, c, esz = synth.B4, 4, 2048, 2
+    kv_tok = 2 * sh.kv_dim * esz
+    stage0 = sh.n_layers // n  # beta_1 = floor(L / n)
+    expect = stage0 * (_layer(sh, esz) + (c + 1) * kv_tok + kv_tok)  # keys 0..c read, one row written
+    expect += sh.vocab * sh.d_model * esz  # the two-row head pass runs every step
+    expect += sh.d_model * n * sh.d_model * esz + sh.pdm_layers * _layer(sh, esz)  # PDM projection, layer
+    expect += sh.pdm_layers * ((c + 1) * kv_tok + kv_tok)  # PDM KV of its one row
+    assert bench.step_bytes_active(sh, n, sh.pdm_layers, c, 1, esz) == expect
+
+
+def test_steady_step_bytes_at_the_headline_size():
+    """4B-class n = 4 at 2300 committed positions: 7.267 GB of layer weights, 0.778 GB of LM head,
+    about 0.37 GB of keys and values, 0.26 GB for the PDM."""
+    sh, esz = synth.B4, 2
+    total = bench.step_bytes_active(sh, 4, 1, 2300, 4, esz)
+    assert 8.6e9 < total < 8.75e9
+    assert abs(sh.n_layers * _layer(sh, esz) - 7.267e9) < 5e6
