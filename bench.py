@@ -522,8 +522,9 @@ def main():
 
 def own_head_phase(args, weights, prompt, ref, max_tokens, attn_chunk, K, W, n, shared_us, vocab=32768):
     """The PDM with its own LM head over a smaller vocabulary (initialised from the target's rows of
-    that subset): its head runs on the PDM's stream, the exit row alone on the main stream. Steady
-    state with drafts forced to the greedy tokens (the stream is checked), and the PDM's span."""
+    that subset; at most half the target's): its head runs on the PDM's stream, the exit row alone on
+    the main stream. Steady state with drafts forced to the greedy tokens (the stream is checked), and
+    the PDM's span."""
     import numpy as np
     import torch
 
@@ -531,6 +532,7 @@ def own_head_phase(args, weights, prompt, ref, max_tokens, attn_chunk, K, W, n, 
     from paper_2605_30852_amd.engine import Engine
 
     P = len(prompt)
+    vocab = min(vocab, weights.shape.vocab // 2)
     wv = weights.with_pdm_vocab(vocab)
     eng = Engine(wv, max_tokens=max_tokens, n=n, attn_chunk=attn_chunk)
     eng.spd_set_step_kernel(args.step_mode, args.step_grid, args.stage_groups if args.step_mode == 2 else -1)
