@@ -245,6 +245,9 @@ def main():
     ar = Engine(weights, max_tokens=max_tokens, n=1, attn_chunk=attn_chunk, fused_head=fused)
     ar.spd_set_step_kernel(mode, args.step_grid, args.stage_groups if mode == 2 else -1)
     ar.spd_set_pdm_placement(args.pdm_place)
+    # plain decoding needs no draft module: at n = 1 a step commits the target's token whatever the
+    # draft, so the draft module's launches are left out of the reference and its tokens/s
+    B.spd_set_pdm_enabled(ar.h, False)
     ar.spd_set_graph(not args.no_graph)
     first = ar.spd_prefill(prompt)
     log(f"[bench] AR prefill {P} tokens in {time.time() - t0:.1f}s")
