@@ -216,7 +216,8 @@ def main():
     esz = 2 if sh.dtype == "bf16" else 4
     K_GU, K_CLS, K_SPAN = 64, 16, 64
     # greedy reference long enough for every forced-accept phase below
-    n_ref = W + K + K_GU + 6 * K_CLS + 4 * K_SPAN + 2 * n + 32
+    K_P50 = 64
+    n_ref = W + K + K_GU + 6 * K_CLS + 4 * K_SPAN + K_P50 + 2 * n + 40
     # capacity and attention split size depend on the workload only (not on --steps), so that a
     # profiled run with fewer steps launches exactly the kernels the timed run launches
     max_tokens = P + max(1024, n_ref + 4 * n + 64)
@@ -295,6 +296,20 @@ def main():
     gbs = bytes_step / (us_step * 1e-6) / 1e9
     log(f"[bench] SPD n={n}: {us_step:.1f} us/step, {bytes_step / 1e9:.3f} GB/step, {gbs:.0f} GB/s "
         f"({100 * gbs / PEAK_HBM_GBS:.1f}% of {PEAK_HBM_GBS:.0f})")
+    # per-step durations: events on the handle's main stream between single-step replays (no host
+    # synchronisation between the steps)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K_P50 + 1)]
+    evs[0].record(eng.main)
+    for i in range(K_P50):
+        eng.spd_run_steps(1)
+        evs[i + 1].record(eng.main)
+    eng.spd_sync()
+    torch.cuda.synchronize()
+    per_step = sorted(1e3 * evs[i].elapsed_time(evs[i + 1]) for i in range(K_P50))
+    step_dist = {"steps": K_P50, "p50_us": round(per_step[K_P50 // 2], 1),
+                 "p90_us": round(per_step[(9 * K_P50) // 10], 1), "min_us": round(per_step[0], 1),
+                 "mean_us": round(sum(per_step) / K_P50, 1)}
+    log(f"[bench] per-step durations: {step_dist}")
 
     # per-kernel HIP-event timing on the main stream, steady state (every step accepts). With
     # sublayer launches only the slots after the draft module's span are timed, so that a kernel is
@@ -497,6 +512,7 @@ def main():
         "bytes_per_step": int(bytes_step),
         "step_GBps": round(gbs, 1),
         "step_roofline_frac": round(gbs / PEAK_HBM_GBS, 4),
+        "step_us_distribution": step_dist,
         "roofline": {"bound": "hbm", "achieved": dk["GBps"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(dk["GBps"] / PEAK_HBM_GBS, 4), "traffic": traffic_from_profile(dominant),
                      "kernel": {0: "k_sgemv gate/up: grouped gate/up GEMV + SwiGLU over the n stages",
