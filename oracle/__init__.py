@@ -25,8 +25,8 @@ Pins (what ties each function to something other than itself) are in tests/test_
   spd.speedup_*                              -> Table 3's printed speedups (tests/golden/)
 Parity unpinned: the PDM's draft quality (it has random weights); only its definition is pinned.
 """
-from .model import (LayerCache, Model, ar_greedy, ar_sample, argmax_first, attend, decoder_layer, embed,
-                    forward_full, lm_logits, rms_norm, rope, rope_angles, round_bf16, silu)
+from .model import (LayerCache, Model, ar_greedy, argmax_first, attend, decoder_layer, embed,
+                    forward_full, forward_rows, lm_logits, rms_norm, rope, rope_angles, round_bf16, silu)
 from .sampling import (Sampling, point_mass, prob_of, rejection_verify, sample, sample_index,
                        top_k_dist)
 from .spd import (ACCEPT, NONE, REJECT, SPDOracle, StepResult, eligible_anchors, l_max, run_spd,

@@ -220,40 +220,33 @@ def ar_greedy(model: Model, prompt, n_new: int, return_logits: bool = False):
     return (out, logs) if return_logits else out
 
 
-def ar_sample(model: Model, prompt, n_new: int, dist_of, draw):
-    """Plain autoregressive sampling: token i after the prompt is draw(dist_of(logits), position).
-    dist_of and draw are the sampling rule (oracle/sampling.py); returns the n_new tokens."""
-    caches = new_caches(model.shape, model.shape.n_layers)
-    h = None
-    for p, t in enumerate(prompt):
-        h, _ = run_token(model, caches, int(t), p)
-    out = []
-    pos = len(prompt)
-    while True:
-        x = draw(dist_of(lm_logits(model, h)), pos)
-        out.append(x)
-        if len(out) == n_new:
-            return out
-        h, _ = run_token(model, caches, x, pos)
-        pos += 1
-
-
 def forward_full(model: Model, tokens, layers_out=None, free_layers: bool = False) -> Dict[int, np.ndarray]:
     """Brute force without any cache: full causal attention over all rows at every layer.
 
     Returns {l: H^l [T, d]} for l in layers_out (default: every l in 0..L). free_layers drops each
     layer's weights once the layer is done (same arithmetic; for full-size models, whose float64
     weights do not all fit in memory at once)."""
-    sh = model.shape
-    L, dh = sh.n_layers, sh.head_dim
-    T = len(tokens)
-    layers_out = list(range(L + 1)) if layers_out is None else list(layers_out)
     H = model.w("embed")[np.asarray(tokens, dtype=np.int64)].copy()
+    return forward_rows(model, H, "layer", model.shape.n_layers, layers_out, free_layers)
+
+
+def forward_rows(model: Model, H0: np.ndarray, prefix: str, n_layers: int, layers_out=None,
+                 free_layers: bool = False, caches: Optional[List[LayerCache]] = None) -> Dict[int, np.ndarray]:
+    """Layers 0..n_layers-1 named `prefix` ("layer": the target, "pdm.layer": the draft module's)
+    over the rows H0 [T, d], row t at position t, each attending causally to rows 0..t, without any
+    cache. Returns {l: H^l [T, d]} for l in layers_out (default every l in 0..n_layers; H^0 = H0).
+    caches: empty per-layer caches that receive each layer's keys and values of the T rows (as a
+    token-by-token pass would have appended them)."""
+    sh = model.shape
+    dh = sh.head_dim
+    H = np.array(H0, dtype=np.float64)
+    T = H.shape[0]
+    layers_out = list(range(n_layers + 1)) if layers_out is None else list(layers_out)
     res = {0: H.copy()} if 0 in layers_out else {}
     grp = sh.n_q_heads // sh.n_kv_heads
     causal = np.tril(np.ones((T, T), dtype=bool))
-    for l in range(L):
-        lw = model.layer(l)
+    for l in range(n_layers):
+        lw = model.layer(l, prefix)
         U = rms_norm(H, lw["attn_norm"], sh.rms_eps)
         Q = (U @ lw["wq"].T).reshape(T, sh.n_q_heads, dh)
         K = (U @ lw["wk"].T).reshape(T, sh.n_kv_heads, dh)
@@ -261,6 +254,9 @@ def forward_full(model: Model, tokens, layers_out=None, free_layers: bool = Fals
         Q = np.stack([rope(Q[t], t, sh.rope_base) for t in range(T)])
         K = round_kv(np.stack([rope(K[t], t, sh.rope_base) for t in range(T)]), sh.dtype)
         V = round_kv(V, sh.dtype)
+        if caches is not None:
+            for t in range(T):
+                caches[l].append(t, K[t], V[t])
         O = np.zeros((T, sh.n_q_heads, dh))
         for h in range(sh.n_q_heads):
             kv = h // grp
@@ -277,5 +273,5 @@ def forward_full(model: Model, tokens, layers_out=None, free_layers: bool = Fals
             res[l + 1] = H.copy()
         if free_layers:
             del lw
-            model.drop(f"layer.{l}.")
+            model.drop(f"{prefix}.{l}.")
     return res

@@ -33,7 +33,7 @@ What it follows:
   * The PDM's LM head (Section 4.1): shared with the target, or its own head over a smaller vocabulary
     (initialised from the target's rows of that subset); a draft id i then stands for target token
     map[i], map ascending, so ties still go to the lower target id.
-  * Post-step schedule (the ablation of Section 4.4 against Section 3.3's pre-step choice): the PDM
+  * Post-step schedule (the ablation of Section 4.5 against Section 3.3's pre-step choice): the PDM
     waits for the stage compute and reads the post-step features, every in-flight token one stage
     deeper (the newest contributes g^1 instead of g^0); drafting is then serial behind the step.
     Everything else (rows rewritten, the draft's position, verify) is as in the pre-step schedule.
@@ -46,7 +46,8 @@ from typing import Callable, Dict, List, Optional, Sequence
 import numpy as np
 
 import synth
-from .model import (LayerCache, Model, argmax_first, decoder_layer, embed, lm_logits, new_caches, rms_norm)
+from .model import (LayerCache, Model, argmax_first, decoder_layer, embed, forward_rows, lm_logits, new_caches,
+                    rms_norm)
 from . import sampling as smp
 
 NONE, ACCEPT, REJECT = 0, 1, 2
@@ -168,16 +169,28 @@ class SPDOracle:
         return h
 
     # ------------------------------------------------------------------ prefill
-    def prefill(self, prompt) -> int:
+    def prefill(self, prompt, batched: bool = False) -> int:
         """Process the prompt through the target (keeping the anchors), build the PDM KV over it
-        with full-depth features, and place the target's first token in flight at depth 0."""
+        with full-depth features, and place the target's first token in flight at depth 0.
+
+        batched: the same causal forward over the whole prompt at once (every layer as one matrix
+        product over the prompt's rows, causal attention over the row block), for long prompts; the
+        caches receive the same keys and values a token-by-token pass appends."""
         prompt = [int(t) for t in prompt]
         P = len(prompt)
         assert P >= 1
         h = None
-        for p, t in enumerate(prompt):
-            h, kept = self._run_stage_range(embed(self.m, t), p, 0, self.n, capture=True)
-            self.pdm_row(self.feature(kept, self.n), p)
+        if batched:
+            H0 = self.m.w("embed")[np.asarray(prompt, dtype=np.int64)]
+            full = forward_rows(self.m, H0, "layer", self.L, layers_out=sorted(set(self.anchor_layers) | {self.L}),
+                                caches=self.caches)
+            G = np.stack([self.feature([full[b][p] for b in self.anchor_layers], self.n) for p in range(P)])
+            forward_rows(self.m, G, "pdm.layer", self.ls, layers_out=[], caches=self.pdm_caches)
+            h = full[self.L][P - 1]
+        else:
+            for p, t in enumerate(prompt):
+                h, kept = self._run_stage_range(embed(self.m, t), p, 0, self.n, capture=True)
+                self.pdm_row(self.feature(kept, self.n), p)
         lg = lm_logits(self.m, h)
         x = argmax_first(lg) if self.sampling is None else smp.sample(
             self._target_dist(lg), self.sampling.u(P, smp.U_RESAMPLE))

@@ -1,6 +1,6 @@
 """Pins for the oracle's post-step schedule (CPU only).
 
-Under the post-step schedule (the ablation of Section 4.4) the PDM reads the features left after the
+Under the post-step schedule (the ablation of Section 4.5) the PDM reads the features left after the
 step's stage compute, so every in-flight token is one stage deeper than under the pre-step schedule
 of Section 3.3. What fixes it independently of the pipelined code: with W_in selecting one anchor
 block and the PDM layers reduced to the identity, each PDM row must equal that anchor of its token as

@@ -278,3 +278,47 @@ def test_simulator_closed_form_alpha():
         N = 200000
         K = osp.simulate_steps(n, N, lambda q: bool(bits[q]), 0)
         assert abs(N / K - 1 / (p + (1 - p) * n)) < 0.01
+
+
+@pytest.mark.parametrize("shape", [synth.TINY, synth.MID])
+def test_batched_prefill_equals_token_by_token(shape):
+    """The batched prefill (the whole prompt's causal forward as matrix products over its rows) and
+    the token-by-token prefill fill the target and draft-module caches with the same keys and values,
+    pick the same first token and continue identically (fp32 tiny, and the bf16 mid shape whose keys
+    and values are rounded to bf16 as they are written)."""
+    m = om.Model(shape, SEED)
+    prompt = synth.prompt(shape, SEED, 23)
+    a, b = osp.SPDOracle(m), osp.SPDOracle(m)
+    assert a.prefill(prompt) == b.prefill(prompt, batched=True)
+    for ca, cb in zip(a.caches + a.pdm_caches, b.caches + b.pdm_caches):
+        assert ca.n == cb.n == len(prompt)
+        np.testing.assert_allclose(cb.k[: cb.n], ca.k[: ca.n], rtol=1e-9, atol=1e-12)
+        np.testing.assert_allclose(cb.v[: cb.n], ca.v[: ca.n], rtol=1e-9, atol=1e-12)
+    for _ in range(8):
+        ra, rb = a.step(want_logits=True), b.step(want_logits=True)
+        assert (ra.decision, ra.target_argmax, ra.pdm_draft, ra.c, ra.a) == \
+               (rb.decision, rb.target_argmax, rb.pdm_draft, rb.c, rb.a)
+        np.testing.assert_allclose(rb.pdm_logits, ra.pdm_logits, rtol=1e-7, atol=1e-9)
+    for q in range(a.c, a.c + a.a):
+        np.testing.assert_allclose(b.hidden[q], a.hidden[q], rtol=1e-8, atol=1e-10)
+
+
+def test_inflight_states_equal_brute_force_bf16():
+    """The brute-force pin of in-flight states on the bf16 mid shape (keys and values rounded to bf16
+    as the cache stores them, on both sides), with ragged stages (6 layers, n = 4)."""
+    m = om.Model(synth.MID, SEED)
+    prompt = synth.prompt(synth.MID, SEED, 17)
+    ref = om.ar_greedy(m, prompt, 20)
+    mask = synth.accept_mask(0.6, 19, 80)
+    table = {len(prompt) + i: (t if mask[len(prompt) + i] else (t + 1) % synth.MID.vocab) for i, t in enumerate(ref)}
+    o = osp.SPDOracle(m, n=4)
+    o.prefill(prompt)
+    beta = o.beta
+    for _ in range(9):
+        o.step(forced_draft=table.get(o.c + o.a))
+        full = om.forward_full(m, o.toks[: o.c + o.a])
+        for q in range(o.c, o.c + o.a):
+            k = o.depth(q)
+            np.testing.assert_allclose(o.hidden[q], full[beta[k]][q], rtol=1e-9, atol=1e-11)
+            for j, an in enumerate(o.anch[q]):
+                np.testing.assert_allclose(an, full[beta[j]][q], rtol=1e-9, atol=1e-11)
