@@ -9,8 +9,10 @@ every stage's 9 layers, the exit LM head and verification.
 Timed region: K back-to-back steps with drafts forced to the target's own greedy tokens (every step
 accepts, so every step is a full-pipeline step), bracketed by device synchronisation. Reported:
 us per step, algorithmic HBM bytes per step and GB/s against 8 TB/s, the dominant kernel's
-roofline (HIP events around each launch), tokens/s at a Bernoulli(0.7) acceptance pattern next to
-plain greedy decoding on the same GPU, and the CPU oracle's time per step on the host cores.
+roofline (HIP events around each launch of it when it runs alone), tokens/s at a Bernoulli(0.7)
+acceptance pattern next to plain greedy decoding on the same GPU, the CPU oracle's time per step on
+the host cores, and the 9B-class workloads (n = 4 at 4096 tokens; n = 8 with a two-layer PDM at 32768
+tokens) with their step time, bandwidth and PDM hiding.
 """
 import argparse
 import json
@@ -29,20 +31,27 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def pdm_kv_bytes(sh, ls, c, a, esz):
+    """The draft module's keys and values in a step with c committed positions and a in-flight rows:
+    its rows at positions c..c+a-1 attend over one shared cache, so each PDM layer's keys and values
+    0..c+a-1 are read once, and the a rows are written."""
+    kv_tok = 2 * sh.kv_dim * esz
+    return ls * ((c + a) * kv_tok + a * kv_tok)
+
+
 def step_bytes(sh, n, ls, c, esz, pdm_head=True):
-    """Algorithmic HBM bytes of one full-pipeline step that starts with c committed positions."""
-    d, F, V, L = sh.d_model, sh.ffn_dim, sh.vocab, sh.n_layers
-    qd, kvd = sh.q_dim, sh.kv_dim
-    layer_w = (qd * d + 2 * kvd * d + d * qd + 3 * F * d) * esz + 2 * d * 4
-    kv_tok = 2 * kvd * esz
+    """Algorithmic HBM bytes of one full-pipeline step that starts with c committed positions:
+    (target, PDM). pdm_head: the PDM streams its own pass over the LM head."""
+    d, V, L = sh.d_model, sh.vocab, sh.n_layers
+    kv_tok = 2 * sh.kv_dim * esz
     beta = [s * L // n for s in range(n + 1)]
     kv_read = 0
     for s in range(n):
-        pos = c + n - 1 - s  # token of stage s attends to pos+1 keys
+        pos = c + n - 1 - s  # token of stage s attends to pos+1 keys of its own layers
         kv_read += (beta[s + 1] - beta[s]) * (pos + 1) * kv_tok
-    target = L * layer_w + kv_read + L * kv_tok + V * d * esz + d * esz
-    pdm_kv = sum((c + i + 1) for i in range(n)) * ls * kv_tok + n * ls * kv_tok
-    pdm = d * n * d * esz + ls * layer_w + pdm_kv + (V * d * esz if pdm_head else 0)
+    target = L * layer_bytes(sh, esz) + kv_read + L * kv_tok + V * d * esz + d * esz
+    pdm = d * n * d * esz + ls * layer_bytes(sh, esz) + pdm_kv_bytes(sh, ls, c, n, esz) + \
+        (V * d * esz if pdm_head else 0)
     return target, pdm
 
 
@@ -59,27 +68,12 @@ def step_bytes_active(sh, n, ls, c, a, esz):
         pos = c + a - 1 - s
         nl = beta[s + 1] - beta[s]
         target += nl * (layer_w + (pos + 1) * kv_tok + kv_tok)
-    pdm_kv = sum((c + i + 1) for i in range(a)) * ls * kv_tok + a * ls * kv_tok
-    return target + d * n * d * esz + ls * layer_w + pdm_kv
+    return target + d * n * d * esz + ls * layer_w + pdm_kv_bytes(sh, ls, c, a, esz)
 
 
 def layer_bytes(sh, esz):
     d, F, qd, kvd = sh.d_model, sh.ffn_dim, sh.q_dim, sh.kv_dim
     return (qd * d + 2 * kvd * d + d * qd + 3 * F * d) * esz + 2 * d * 4
-
-
-def step_kernel_bytes(sh, n, c, esz):
-    """Algorithmic bytes of one steady-state persistent step launch (all n stages active, the step
-    starting with c committed positions): every layer's weights and norm gains once, each stage's KV
-    read over its own length, the new K/V written, and the activations each sublayer reads and writes
-    (per stage and layer: x in/out for the two norms and two residual adds, q, attention output and
-    the SwiGLU activation, all fp32)."""
-    d, F, qd, kvd, L = sh.d_model, sh.ffn_dim, sh.q_dim, sh.kv_dim, sh.n_layers
-    kv_tok = 2 * kvd * esz
-    beta = [s * L // n for s in range(n + 1)]
-    kv_read = sum((beta[s + 1] - beta[s]) * (c + n - s) * kv_tok for s in range(n))
-    act = L * 4 * (6 * d + 2 * qd + 2 * F)
-    return L * layer_bytes(sh, esz) + kv_read + L * kv_tok + act
 
 
 def launch_bytes(sh, n, c, esz):
@@ -97,7 +91,6 @@ def launch_bytes(sh, n, c, esz):
         "gateup": n * (2 * F * d * esz + 2 * d * 4 + F * 4),
         "down": n * (d * F * esz + F * 4 + 2 * d * 4),
         "head": V * d * esz + 2 * d * 4,  # one pass; the fused form adds only a second activation row
-        "step": step_kernel_bytes(sh, n, c, esz),
         "_beta": beta,
     }
 
@@ -152,13 +145,25 @@ def cpu_baseline(sh, n, ctx, seed, budget_s=12.0):
     return {
         "value": round(1e6 * step, 1), "unit": "us/step", "cores": threads or len(os.sched_getaffinity(0)),
         "kind": "oracle",
-        "sample": (f"float64 oracle on the host: decoder_layer of one {sh.name} layer at context {ctx} "
-                   f"x{r_layer}, lm_logits over {sh.vocab} tokens x{r_head}, PDM feature projection "
-                   f"({n}*{sh.d_model} -> {sh.d_model}) x{r_fc}; scaled to one full-pipeline step = "
+        "sample": (f"extrapolated from timed oracle calls, not a timed oracle step: float64 decoder_layer of one "
+                   f"{sh.name} layer at context {ctx} x{r_layer}, lm_logits over {sh.vocab} tokens x{r_head}, PDM "
+                   f"feature projection ({n}*{sh.d_model} -> {sh.d_model}) x{r_fc}; one full-pipeline step = "
                    f"{sh.n_layers} target layers + {n} rows x {sh.pdm_layers} PDM layer(s) + {n} "
                    f"projections + 2 LM heads"),
+        "cpu_model": cpu_model(),
         "per_layer_s": round(t_layer, 5), "head_s": round(t_head, 5), "fc_s": round(t_fc, 5),
     }
+
+
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), or None."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
@@ -174,27 +179,25 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="issue every launch instead of replaying the step graph")
     ap.add_argument("--separate-head", action="store_true",
                     help="the draft module runs its own LM-head pass on its stream instead of sharing the exit pass")
-    ap.add_argument("--step-mode", type=int, default=2, choices=[0, 1, 2, 3, 4],
-                    help="stage compute: 0 five launches per layer slot covering all stages, 1 one persistent "
-                         "launch per step, 2 (default) one stream per stage, 3 skewed launches, each mixing "
-                         "independent sublayers of different stages, 4 one persistent launch with a group of "
-                         "workgroups per stage")
-    ap.add_argument("--step-grid", type=int, default=0, help="workgroups of the persistent step launch (0: default)")
+    ap.add_argument("--step-mode", type=int, default=2, choices=[0, 2],
+                    help="stage compute: 0 five launches per layer slot covering all stages on one stream, "
+                         "2 (default) stage groups, each on its own stream")
+    ap.add_argument("--step-grid", type=int, default=0, help="workgroups of one stage launch (0: default)")
     ap.add_argument("--stage-groups", type=int, default=0, help="mode 2: stage streams (0: the library default)")
     ap.add_argument("--pdm-grid", type=int, default=0, help="workgroups per PDM GEMV launch (0: the default)")
-    ap.add_argument("--pdm-place", type=int, default=0, choices=[0, 1, 2, 3, 4],
-                    help="PDM launches: own stream, main before the stages, first group before/after, "
-                         "spread over the groups")
+    ap.add_argument("--pdm-place", type=int, default=0, choices=[0, 1, 2, 3],
+                    help="PDM launches: own stream, main before the stages, first group before/after")
     ap.add_argument("--attn-chunk", type=int, default=0, help="keys per attention split (0: the workload's default)")
     ap.add_argument("--graph-steps", type=int, default=1, help="steps per replayed graph in batched runs")
     ap.add_argument("--extra-phases", choices=["auto", "on", "off"], default="auto",
                     help="the PDM's own head and sampled decoding, each on a handle of its own (auto: on "
                          "for prompts up to 4096 tokens; each needs its own prefill)")
+    ap.add_argument("--extra-workloads", choices=["auto", "on", "off"], default="auto",
+                    help="the 9B-class workloads (n = 4 at 4096 tokens; n = 8, two-layer PDM at 32768 tokens) after "
+                         "the main one (auto: with the default 4B workload)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (the known-size kernel for HBM counter scaling)")
     args = ap.parse_args()
-    if args.pdm_place == 4 and not args.no_graph:
-        sys.exit("--pdm-place 4 (spread over the stage streams) runs with issued launches only: add --no-graph")
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the SPD step here is the single-GPU stage-batched "
               "form; multi-GPU sharding is not built", file=sys.stderr)
@@ -311,11 +314,11 @@ def main():
                  "mean_us": round(sum(per_step) / K_P50, 1)}
     log(f"[bench] per-step durations: {step_dist}")
 
-    # per-kernel HIP-event timing on the main stream, steady state (every step accepts). With
-    # sublayer launches only the slots after the draft module's span are timed, so that a kernel is
-    # timed without the side stream sharing HBM; the persistent launch covers the whole step.
+    # per-kernel HIP-event timing on the launching stream, steady state (every step accepts). Only the
+    # slots after the draft module's span are timed, so that a kernel is timed without the side
+    # stream sharing HBM.
     L_slots = max(sh.n_layers // n + (1 if sh.n_layers % n else 0), 1)
-    first_slot = L_slots // 2 if mode in (0, 2) else 0
+    first_slot = L_slots // 2
 
     def time_class(kid, steps):
         B.spd_set_kernel_timing(eng.h, kid, first_slot if kid != B.SPD_K_HEAD else 0)
@@ -329,45 +332,37 @@ def main():
         assert nl > 0, "no launch of the timed class"
         return ms, nl, (ca + cb) // 2
 
+    # Every sublayer class in the timed launch form. With stage groups a launch's events also hold the
+    # time it waits for the compute units another group's launch occupies, so these are not kernel
+    # durations; they show where the step's time goes.
     kernels = {}
-    if mode in (1, 4):
-        classes = (("step", B.SPD_K_STEP), ("head", B.SPD_K_HEAD))
-        dominant = "step"
-    elif mode == 3:
-        classes = (("mix", B.SPD_K_MIX), ("head", B.SPD_K_HEAD))
-        dominant = "mix"
-    else:
-        classes = (("qkv", B.SPD_K_QKV), ("attn", B.SPD_K_ATTN), ("oproj", B.SPD_K_OPROJ),
-                   ("gateup", B.SPD_K_GATEUP), ("down", B.SPD_K_DOWN), ("head", B.SPD_K_HEAD))
-        dominant = "gateup"
+    classes = (("qkv", B.SPD_K_QKV), ("attn", B.SPD_K_ATTN), ("oproj", B.SPD_K_OPROJ),
+               ("gateup", B.SPD_K_GATEUP), ("down", B.SPD_K_DOWN), ("head", B.SPD_K_HEAD))
     for kname, kid in classes:
-        steps = K_GU if kname == dominant else K_CLS
-        ms, nl, cm = time_class(kid, steps)
-        if kname == "mix":  # the launches of a step together stream what one persistent launch does
-            lb = launch_bytes(sh, n, cm, esz)["step"] / (nl / steps)
-        else:
-            lb = launch_bytes(sh, n, cm, esz)[kname]
-        if mode == 2 and kname not in ("head", "step"):
+        ms, nl, cm = time_class(kid, K_CLS)
+        lb = launch_bytes(sh, n, cm, esz)[kname]
+        if mode == 2 and kname != "head":
             lb = lb / groups  # each launch covers one group's stages (n / groups on average)
         us = 1e3 * ms / max(1, nl)
-        kernels[kname] = {"us_per_launch": round(us, 2), "timed_launches_per_step": nl / steps,
+        kernels[kname] = {"us_per_launch": round(us, 2), "timed_launches_per_step": nl / K_CLS,
                           "bytes_per_launch": int(lb), "GBps": round(lb / (us * 1e-6) / 1e9, 1)}
-    log(f"[bench] kernels: {kernels}")
-    dk = kernels[dominant]
-    # the same kernel with nothing beside it: one stage group, so each gate/up launch covers all n
-    # stages and no other launch shares the GPU (context for the concurrent figure above)
-    isolated = None
-    if mode == 2:
-        eng.spd_set_step_kernel(2, args.step_grid, 1)
-        eng.spd_run_steps(2)
-        ms, nl, cm = time_class(B.SPD_K_GATEUP, K_CLS)
-        lb = launch_bytes(sh, n, cm, esz)["gateup"]
-        us = 1e3 * ms / max(1, nl)
-        isolated = {"stage_groups": 1, "bytes_per_launch": int(lb), "us_per_launch": round(us, 2),
-                    "GBps": round(lb / (us * 1e-6) / 1e9, 1), "frac": round(lb / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
-        eng.spd_set_step_kernel(2, args.step_grid, args.stage_groups)
-        eng.spd_run_steps(2)
-        log(f"[bench] gate/up with one stage group: {isolated}")
+    log(f"[bench] kernels (concurrent launch form): {kernels}")
+    # The dominant kernel (most bytes per step: the gate/up GEMV) with nothing beside it, so that its
+    # event interval is its own execution: one stage group (every launch covers all n stages) and the
+    # draft module's launches off (drafts are forced). The kernel trace of the same command times the
+    # same launches (grid y = n).
+    eng.spd_set_step_kernel(mode, args.step_grid, 1)
+    B.spd_set_pdm_enabled(eng.h, False)
+    eng.spd_run_steps(2)
+    ms, nl, cm = time_class(B.SPD_K_GATEUP, K_GU)
+    lb = launch_bytes(sh, n, cm, esz)["gateup"]
+    dom_us = 1e3 * ms / max(1, nl)
+    dom = {"bytes_per_launch": int(lb), "us_per_launch": round(dom_us, 2), "launches": nl,
+           "GBps": round(lb / (dom_us * 1e-6) / 1e9, 1)}
+    B.spd_set_pdm_enabled(eng.h, True)
+    eng.spd_set_step_kernel(mode, args.step_grid, args.stage_groups)
+    eng.spd_run_steps(2)
+    log(f"[bench] gate/up alone (one stage group, no PDM): {dom}")
 
     # PDM overlap: step start -> end of the stage compute (main) and -> end of the PDM (side stream)
     B.spd_set_kernel_timing(eng.h, B.SPD_K_SPANS)
@@ -471,6 +466,22 @@ def main():
     del weights
     torch.cuda.empty_cache()
 
+    workloads = None
+    if args.extra_workloads == "on" or (args.extra_workloads == "auto" and args.workload == "4b"
+                                        and args.prompt is None and args.n is None):
+        t0 = time.time()
+        log(f"[bench] generating and uploading 9b weights ({synth.B9.param_bytes() / 1e9:.2f} GB)")
+        w9 = DeviceWeights(synth.B9, args.seed, threads=16)
+        torch.cuda.synchronize()
+        log(f"[bench] 9b weights ready in {time.time() - t0:.1f}s")
+        workloads = {}
+        workloads["9b_n4_4096"] = extra_workload("9b n=4, 4096-token prompt", w9, 4, 1, 4096, 0.7, args.seed)
+        wl8 = w9.pdm_for_width(8, 2)
+        workloads["9b_n8_32768"] = extra_workload("9b n=8, two-layer PDM, 32768-token prompt", wl8, 8, 2, 32768, 0.6,
+                                                  args.seed)
+        del wl8, w9
+        torch.cuda.empty_cache()
+
     cpu = None
     if not args.no_cpu_baseline:
         t0 = time.time()
@@ -499,44 +510,136 @@ def main():
                    "lm_head": "one two-row pass shared by exit and draft" if fused else "separate passes",
                    "step_graph": not args.no_graph,
                    "stage_compute": {0: "five launches per layer slot covering all stages",
-                                     1: "one persistent launch per step",
                                      2: f"{groups} stage groups on their own streams, five launches per layer slot "
-                                        f"each covering the group's stages",
-                                     3: "skewed schedule: 5J+n-1 launches, launch L runs sublayer L-s of stage s",
-                                     4: "one persistent launch per step, a group of workgroups per stage"}[mode],
+                                        f"each covering the group's stages"}[mode],
                    "step_grid": args.step_grid or None,
                    "pdm_placement": {0: "own stream", 1: "main stream before the stages",
                                      2: "first stage group's stream, before its stages",
-                                     3: "first stage group's stream, after its stages",
-                                     4: "spread over the stage groups' streams"}[args.pdm_place]},
+                                     3: "first stage group's stream, after its stages"}[args.pdm_place]},
         "bytes_per_step": int(bytes_step),
         "step_GBps": round(gbs, 1),
         "step_roofline_frac": round(gbs / PEAK_HBM_GBS, 4),
         "step_us_distribution": step_dist,
-        "roofline": {"bound": "hbm", "achieved": dk["GBps"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                     "frac": round(dk["GBps"] / PEAK_HBM_GBS, 4), "traffic": traffic_from_profile(dominant),
-                     "kernel": {0: "k_sgemv gate/up: grouped gate/up GEMV + SwiGLU over the n stages",
-                                1: "k_step: the persistent launch running every layer slot of all n stages",
-                                2: f"k_sgemv gate/up of one stage group (n/{groups} stages; the groups' streams "
-                                   f"run concurrently)",
-                                3: "k_mix: the skewed launches of the stage compute (all layers' weights and KV; "
-                                   "bytes and time summed over the launches of a step)",
-                                4: "k_pstep: the persistent launch running every layer slot of all n stages, "
-                                   "one group of workgroups per stage"}[mode],
-                     "bytes_per_launch": dk["bytes_per_launch"], "us_per_launch": dk["us_per_launch"],
+        "roofline": {"bound": "hbm", "achieved": dom["GBps"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(dom["GBps"] / PEAK_HBM_GBS, 4),
+                     "traffic": traffic_from_profile("gateup_4b_n4_traffic.txt") if sh.name == "4b" and n == 4 else None,
+                     "kernel": f"k_sgemv gate/up GEMV + SwiGLU, one launch over all {n} stages (grid y = {n}) with "
+                               f"nothing beside it: one stage group, the PDM's launches off",
+                     "bytes_per_launch": dom["bytes_per_launch"], "us_per_launch": dom["us_per_launch"],
                      "timing": f"dispatch-recorded HIP events on the launching stream, layer slots >= {first_slot} of "
-                               f"{L_slots}, {K_GU} steady-state steps",
-                     "isolated": isolated},
+                               f"{L_slots}, {K_GU} steady-state steps ({dom['launches']} launches)",
+                     "concurrent": {"us_per_launch": kernels["gateup"]["us_per_launch"],
+                                    "bytes_per_launch": kernels["gateup"]["bytes_per_launch"],
+                                    "note": f"the timed launch form ({groups} stage groups): a launch's events also "
+                                            f"hold its wait for the compute units the other group's launch occupies"}},
         "kernels": kernels,
         "pdm_overlap": spans,
         "hbm_read_probe": probe,
         "tokens_per_s": {"spd_forced_p": p, "alpha": round(alpha, 4), "spd": round(spd_tok_s, 1),
-                         "ar_same_gpu": round(ar_tok_s, 1), "run_mean": run_mean},
+                         "ar_same_gpu": round(ar_tok_s, 1), "run_mean": run_mean,
+                         "note": "context, not a target: on one GPU an SPD step streams about the bytes of one "
+                                 "plain decoding step, and plain decoding through this library (n = 1, one "
+                                 "chain of small launches per token) is launch-bound; neither figure is a "
+                                 "property of the method"},
+        "workloads": workloads,
         "pdm_own_head": own_head,
         "sampled": sampled,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def extra_workload(label, weights, n, ls, P, p, seed, steps=32, warmup=4, k_span=16, n_bern=96):
+    """One more workload on one handle: prefill, the greedy reference from the handle's own decoding
+    with the PDM's drafts (lossless, so its committed stream is greedy decoding), then steady-state
+    steps with the drafts forced to it (us/step, algorithmic bytes, GB/s), the PDM's hiding (the
+    step without the PDM's launches and the PDM alone), and a Bernoulli(p) draft pattern."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2605_30852_amd import binding as B
+    from paper_2605_30852_amd.engine import Engine
+
+    sh = weights.shape
+    esz = 2 if sh.dtype == "bf16" else 4
+    max_tokens = P + 2048
+    prompt = synth.prompt(sh, seed, P)
+    eng = Engine(weights, max_tokens=max_tokens, n=n, pdm_layers=ls)
+    eng.spd_set_graph(True)
+    t0 = time.time()
+    log(f"[bench] {label}: prefill")
+    first = eng.spd_prefill(prompt)
+    log(f"[bench] {label}: prefill {P} tokens in {time.time() - t0:.1f}s")
+    need = warmup + steps + 3 * k_span + 16 + 4 * n + 16
+    while eng.state()[0] - P < need:
+        eng.spd_run_steps(256)
+        eng.spd_sync()
+    c, _, _, _ = eng.state()
+    ref = eng.tokens()[P: c + 1].astype(np.int64)
+    log(f"[bench] {label}: {len(ref)} greedy reference tokens from the PDM's own drafts")
+    eng.spd_rollback(P, int(first))
+    eng.spd_set_forced_drafts(ref.astype(np.int32), P)
+    eng.spd_run_steps(warmup)
+    c0, a0, _, _ = eng.state()
+    assert a0 == n
+    torch.cuda.synchronize()
+    ts = time.perf_counter()
+    eng.spd_run_steps(steps)
+    eng.spd_sync()
+    us = 1e6 * (time.perf_counter() - ts) / steps
+    c1, a1, _, _ = eng.state()
+    assert c1 - c0 == steps and a1 == n
+    tb, pb = step_bytes(sh, n, ls, (c0 + c1) // 2, esz, pdm_head=False)
+    B.spd_set_kernel_timing(eng.h, B.SPD_K_SPANS)
+    eng.spd_run_steps(k_span)
+    st_ms, pd_ms, late_ms, ns = B.spd_span_timing(eng.h)
+    B.spd_set_kernel_timing(eng.h, 0)
+    B.spd_set_pdm_enabled(eng.h, False)
+    eng.spd_run_steps(4)
+    eng.spd_sync()
+    ts = time.perf_counter()
+    eng.spd_run_steps(k_span)
+    eng.spd_sync()
+    t_without = 1e6 * (time.perf_counter() - ts) / k_span
+    B.spd_set_pdm_enabled(eng.h, True)
+    B.spd_set_pdm_placement(eng.h, 1)
+    B.spd_set_kernel_timing(eng.h, B.SPD_K_SPANS)
+    eng.spd_run_steps(k_span)
+    _, pd_alone_ms, _, na = B.spd_span_timing(eng.h)
+    B.spd_set_kernel_timing(eng.h, 0)
+    B.spd_set_pdm_placement(eng.h, 0)
+    t_pdm = 1e3 * pd_alone_ms / na
+    toks = eng.tokens()[P: eng.state()[0] + 1]
+    assert np.array_equal(toks, ref[: len(toks)]), f"{label}: SPD stream differs from greedy decoding"
+    # the Bernoulli(p) draft pattern: rollback, refill, tokens per second
+    eng.spd_rollback(P, int(first))
+    mask = synth.accept_mask(p, seed, max_tokens)
+    table = np.array([ref[i] if mask[P + i] else (ref[i] + 1) % sh.vocab for i in range(len(ref))], dtype=np.int32)
+    eng.spd_clear_forced_drafts()
+    eng.spd_set_forced_drafts(table, P)
+    steps_b = min(n_bern, len(ref) - 2 * n)
+    torch.cuda.synchronize()
+    ts = time.perf_counter()
+    logp = eng.spd_run_steps(steps_b, want_log=True)
+    elp = time.perf_counter() - ts
+    committed = logp[-1]["committed_len"] - P
+    exits = [r for r in logp if r["decision"] != B.SPD_NONE]
+    agree = sum(1 for r in exits if r["decision"] == (B.SPD_ACCEPT if mask[r["verified_pos"]] else B.SPD_REJECT))
+    toks = eng.tokens()[P: logp[-1]["committed_len"] + 1]
+    assert np.array_equal(toks, ref[: len(toks)]), f"{label}: SPD stream differs from greedy decoding (p run)"
+    eng.close()
+    out = {"workload": f"{sh.name}-class dense decoder (d {sh.d_model}, FFN {sh.ffn_dim}), n={n}, {ls}-layer PDM, "
+                       f"{P}-token prompt", "n": n, "pdm_layers": ls, "prompt": P, "steps": steps,
+           "us_per_step": round(us, 1), "bytes_per_step": int(tb + pb),
+           "GBps": round((tb + pb) / (us * 1e-6) / 1e9, 1), "frac": round((tb + pb) / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+           "pdm": {"stage_us": round(1e3 * st_ms / ns, 1), "pdm_us": round(1e3 * pd_ms / ns, 1),
+                   "verify_wait_us": round(1e3 * late_ms / ns, 2), "step_us_without_pdm": round(t_without, 1),
+                   "pdm_alone_us": round(t_pdm, 1), "hidden_fraction": round(1.0 - (us - t_without) / t_pdm, 3)},
+           "bernoulli": {"p": p, "steps": steps_b, "alpha": round(committed / steps_b, 4),
+                         "tok_s": round(committed / elp, 1), "decisions_matching_mask": f"{agree}/{len(exits)}"}}
+    log(f"[bench] {label}: {out}")
+    return out
 
 
 def own_head_phase(args, weights, prompt, ref, max_tokens, attn_chunk, K, W, n, shared_us, vocab=32768):
@@ -664,13 +767,13 @@ def sampled_phase(args, sh, weights, prompt, ref, first, mask, max_tokens, attn_
     return out
 
 
-def traffic_from_profile(dominant):
-    """HBM bytes per launch of the dominant kernel from committed rocprofv3 counter runs, or None
-    when the counters were taken on other kernel sources than the ones built now."""
+def traffic_from_profile(name):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter summary
+    profiles/<name>, or None when the counters were taken on other kernel sources than the ones built
+    now."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", f"{dominant}_4b_n4_traffic.txt")
-    src = os.path.join(ROOT, "paper_2605_30852_amd", "csrc",
-                       "spd_step.hip" if dominant == "step" else "spd_kernels.hip")
+    path = os.path.join(ROOT, "profiles", name)
+    src = os.path.join(ROOT, "paper_2605_30852_amd", "csrc", "spd_kernels.hip")
     if not os.path.exists(path):
         return None
     kv = {}

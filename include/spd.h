@@ -125,6 +125,7 @@ typedef struct spd_step_result {
   int32_t draft;          /* token pushed at depth 0 (the PDM's draft unless forced); -1 on REJECT */
   int32_t pdm_draft;      /* the PDM's own argmax */
   int32_t exited_pos;     /* position that left the last stage, -1 if none */
+  int32_t exited_token;   /* token at exited_pos (committed in an earlier step), -1 if none */
   int32_t verified_pos;   /* position judged this step, -1 if none */
   int32_t verified_token; /* token now committed at verified_pos (equals target_argmax) */
   int32_t committed_len;  /* c after the step */
@@ -192,7 +193,7 @@ spd_status spd_clear_forced_drafts(spd_handle* h);
 spd_status spd_set_sampling(spd_handle* h, int32_t top_k, float temperature, const float* uniforms,
                             int32_t positions);
 
-/* Draft-module schedule (Section 3.3's choice against the ablation of Section 4.4). post_step = 0
+/* Draft-module schedule (Section 3.3's choice against the ablation of Section 4.5). post_step = 0
  * (default): the PDM reads the pre-step features and runs beside the stage compute. post_step = 1:
  * it runs after the step's stage compute on main_stream, before the exit head, and reads every
  * in-flight token one stage deeper (the newest token's anchors 0 and 1 instead of its embedding);
@@ -222,24 +223,16 @@ spd_status spd_sync(spd_handle* h, spd_step_result* last);
  *   SPD_DBG_PDM_LOGITS:  V fp32, the PDM's logits of the last step (needs spd_set_debug)
  *   SPD_DBG_TOKENS:      max_tokens int32, token id per position
  *   SPD_DBG_STATE:       4 int32: c, a, prompt_len, steps
- *   SPD_DBG_STEP_ITEMS:  nitems uint32, the persistent step launch's tile of each ticket:
- *                        phase p = item >> 19 (layer slot p / 5, sublayer p % 5 in the order QKV,
- *                        attention, O-proj, gate/up, down), stage (item >> 16) & 7, tile item & 0xffff
- *   SPD_DBG_STEP_TRACE:  ntrace uint64 wall-clock stamps of the last traced step (spd_set_step_trace;
- *                        0: not reached). Ticket-queue kernel: 4 per ticket (start, inputs ready, input
- *                        staged, end) in the first 4*nitems. Grouped kernel: 3 per workgroup and sublayer
- *                        (wait start, wait end, end) at ((workgroup * 5J) + sublayer) * 3; workgroups
- *                        whose stamps would not fit record none.
  *   SPD_DBG_KTRACE:      nkslots x 2 uint64 wall-clock stamps of the last step run with
  *                        spd_set_kernel_trace on: per slot the first workgroup's start and the
  *                        latest workgroup end (both 0: nothing ran). Slot (j*5 + k)*n + s
  *                        is sublayer k (QKV, attention, O-proj, gate/up, down) of layer slot j of stage
- *                        s (stage launches, modes 0 and 2); slots 5*J*n + 0, 1, 2 are the LM head,
+ *                        s (stage launches); slots 5*J*n + 0, 1, 2 are the LM head,
  *                        verify and the PDM feature projection.
  *   SPD_DBG_QDIST:       sampled decoding: the draft distribution q kept with each in-flight token,
  *                        row r = position mod n: n int32 entry counts, then [n][64] int32 ids, then
  *                        [n][64] fp32 probabilities (value-descending order)
- * bytes must equal the size listed (nitems, ntrace and nkslots from spd_step_plan_info). */
+ * bytes must equal the size listed (nkslots from spd_step_plan_info). */
 enum {
   SPD_DBG_RESID = 1,
   SPD_DBG_ANCHORS = 2,
@@ -248,8 +241,6 @@ enum {
   SPD_DBG_PDM_LOGITS = 5,
   SPD_DBG_TOKENS = 6,
   SPD_DBG_STATE = 7,
-  SPD_DBG_STEP_ITEMS = 8,
-  SPD_DBG_STEP_TRACE = 9,
   SPD_DBG_KTRACE = 10,
   SPD_DBG_QDIST = 11
 };
@@ -266,37 +257,18 @@ spd_status spd_read_kv(spd_handle* h, int32_t pdm, int32_t layer, int32_t pos0, 
 spd_status spd_set_graph(spd_handle* h, int32_t on);
 
 /* How the stage compute of a step is launched (Section 3.1: every active stage advances its token by
- * one stage). All modes give bit-identical results (the per-row arithmetic is the same).
+ * one stage). Both modes give bit-identical results (the per-row arithmetic is the same).
  *   mode 0: five launches per layer slot (QKV, attention, O-proj, gate/up, down) on main_stream, each
  *           covering all stages.
- *   mode 1: one persistent launch per step runs every layer slot of every stage; its `grid`
- *           workgroups (0: 512) take tiles from a ticket counter in a fixed order and each tile waits
- *           (bounded) only for the previous sublayer of its own stage. skew orders the tiles: 0 keeps
- *           the stages' sublayers in lockstep, k > 0 staggers stage s by k*s sublayers, -1 keeps the
- *           current order. If a wait ever timed out, the next call that reads the step result returns
- *           SPD_E_HIP.
- *   mode 2 (default): the stages are spread over G groups of consecutive stages (skew = G, at most
- *           n; 0: the default, 2; -1 keeps the current G); each group runs its own chain of five launches
- *           per layer slot, each covering the group's stages, on its own stream (the library's,
- *           default priority), forked from and joined to main_stream, so that one group's attention
- *           and launch tails can overlap the other groups' weight streaming.
- *   mode 3: a skewed schedule on main_stream: launch L runs sublayer L - s (in the order
- *           QKV, attention, O-proj, gate/up, down of each layer slot) of every stage s, 5J + n - 1
- *           launches per step. The parts of a launch belong to different stages and are independent,
- *           so one stage's latency-bound attention runs under the others' weight streaming and every
- *           launch streams several stages' worth of weights.
- *   mode 4: one persistent launch per step in which every active stage has its own group of
- *           workgroups (`grid` in all, 0: 512, at most what the GPU holds at once); a group walks its
- *           stage's sublayers in order, each workgroup streaming a contiguous share of each sublayer
- *           and waiting (bounded) for its group only before reading what the previous sublayer wrote,
- *           with its first weights for that sublayer already requested. Stages never wait for each
- *           other. SPD_E_INVAL if the GPU cannot hold enough workgroups for the configuration.
- * In modes 0, 2 and 3 `grid` sets the workgroups of one sublayer launch, or of the weight-streaming
- * parts of one mixed launch (0: the default): each stages its input vector once and its waves stream
- * their weight rows back to back.
- * SPD_K_STEP times the persistent launch (modes 1 and 4), SPD_K_MIX the launches of mode 3; the per-sublayer timing
- * classes time modes 0 and 2. */
-spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t skew);
+ *   mode 2 (default): the stages are spread over `groups` groups of consecutive stages (at most n;
+ *           0: the default, 2; -1 keeps the current value); each group runs its own chain of five
+ *           launches per layer slot, each covering the group's stages, on its own stream (the
+ *           library's, default priority), forked from and joined to main_stream, so that one group's
+ *           attention and launch tails can overlap the other groups' weight streaming.
+ * `grid` sets the workgroups of one sublayer launch (0: the default): each stages its input vector
+ * once and its waves stream their weight rows back to back. SPD_E_INVAL for another mode, a grid
+ * above 65535 or groups outside [-1, 8]. */
+spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t groups);
 
 /* 0: steps skip the Pipeline Draft Module's launches (feature projection and decoder layers; the
  * two-row LM head still runs), for measuring how much of the PDM the stage compute hides; drafts
@@ -312,10 +284,7 @@ spd_status spd_probe_hbm_read(const void* buf, size_t bytes, float* sink, int32_
 /* Where the Pipeline Draft Module's launches go within a step (it reads only pre-step features, so
  * any placement gives the same results): 0 (default): its own stream, forked from main_stream;
  * 1: main_stream, before the stage compute; 2 and 3 (mode 2 only; otherwise 0): the first stage
- * group's stream, before (2) or after (3) that group's stage launches; 4 (mode 2 only; otherwise 0):
- * spread over the groups' streams, PDM launch i on group i mod G after its layer slot min(i, J-1),
- * each PDM launch ordered after the previous one by an event (no extra stream); issued launches only:
- * SPD_E_INVAL while graph mode is on, and spd_set_graph(h, 1) fails while placement 4 is set. */
+ * group's stream, before (2) or after (3) that group's stage launches. SPD_E_INVAL otherwise. */
 spd_status spd_set_pdm_placement(spd_handle* h, int32_t place);
 
 /* Workgroups of each of the PDM's GEMV launches in a step (0: the default, 32 per 256 MB of PDM
@@ -323,28 +292,21 @@ spd_status spd_set_pdm_placement(spd_handle* h, int32_t place);
  * most CUs to the stages while still finishing inside the stage compute. */
 spd_status spd_set_pdm_grid(spd_handle* h, int32_t wgs);
 
-/* Tracing of the persistent step launch: while on, every tile records four wall-clock stamps (for
- * SPD_DBG_STEP_TRACE; each step overwrites them). Costs a few stores per tile. */
-spd_status spd_set_step_trace(spd_handle* h, int32_t on);
-
 /* Launch trace: while on, every step first resets the trace and its stage launches, LM head, verify
  * and PDM projection record their wall-clock start and end in it (SPD_DBG_KTRACE). One store per
  * launch and one device atomic per workgroup that nothing waits for; for measurement only. */
 spd_status spd_set_kernel_trace(spd_handle* h, int32_t on);
 
-/* info (host, 16 int32): number of tickets of one step, layer slots J, tiles per stage of QKV,
- * attention, O-proj, gate/up and down, the wall-clock rate of the trace stamps in kHz, the stamps the
- * trace buffer holds (ntrace), the grouped kernel's grid (0 until mode 4 is chosen), the launch-trace
- * slots (nkslots), the SPD width n, the stage groups in effect (1 outside mode 2), the PDM placement,
- * and two zeros. */
+/* info (host, 8 int32): layer slots J, the wall-clock rate of the launch-trace stamps in kHz, the
+ * launch-trace slots (nkslots), the SPD width n, the stage groups in effect (1 in mode 0), the PDM
+ * placement, and two zeros. */
 spd_status spd_step_plan_info(spd_handle* h, int32_t* info);
 
 /* 1: every LM-head pass also writes its full logits (for SPD_DBG_*_LOGITS). */
 spd_status spd_set_debug(spd_handle* h, int32_t on);
 
 /* Kernel timing for roofline measurements. kernel selects one launch class of the stage compute
- * (SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN in modes 0 and 2; SPD_K_STEP, the
- * persistent launch, in modes 1 and 4; SPD_K_MIX in mode 3; SPD_K_HEAD, the LM-head pass, which
+ * (SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN; SPD_K_HEAD, the LM-head pass, which
  * with the fused two-row head also runs the step's verify; 0 turns timing off). While on, steps
  * issue their launches (no graph replay) and every launch of that class in layer slot >= first_slot
  * (the exit head counts as the slot after the last) hands two HIP events to its own dispatch, which
@@ -353,7 +315,7 @@ spd_status spd_set_debug(spd_handle* h, int32_t on);
  * spd_kernel_timing waits for the stream, returns the summed kernel time in milliseconds and the
  * number of timed launches, and clears both. */
 enum { SPD_K_QKV = 1, SPD_K_ATTN = 2, SPD_K_OPROJ = 3, SPD_K_GATEUP = 4, SPD_K_DOWN = 5, SPD_K_HEAD = 6,
-       SPD_K_SPANS = 7, SPD_K_STEP = 8, SPD_K_MIX = 9 };
+       SPD_K_SPANS = 7 };
 spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel, int32_t first_slot);
 spd_status spd_kernel_timing(spd_handle* h, double* total_ms, int32_t* launches);
 

@@ -17,10 +17,9 @@ SPD_F32, SPD_BF16 = 0, 1
 SPD_NONE, SPD_ACCEPT, SPD_REJECT = 0, 1, 2
 SPD_DBG_RESID, SPD_DBG_ANCHORS, SPD_DBG_PDM_HIDDEN = 1, 2, 3
 SPD_DBG_EXIT_LOGITS, SPD_DBG_PDM_LOGITS, SPD_DBG_TOKENS, SPD_DBG_STATE = 4, 5, 6, 7
-SPD_DBG_STEP_ITEMS, SPD_DBG_STEP_TRACE, SPD_DBG_KTRACE, SPD_DBG_QDIST = 8, 9, 10, 11
+SPD_DBG_KTRACE, SPD_DBG_QDIST = 10, 11
 MAX_TOP_K = 64
-SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD, SPD_K_SPANS, SPD_K_STEP = 1, 2, 3, 4, 5, 6, 7, 8
-SPD_K_MIX = 9
+SPD_K_QKV, SPD_K_ATTN, SPD_K_OPROJ, SPD_K_GATEUP, SPD_K_DOWN, SPD_K_HEAD, SPD_K_SPANS = 1, 2, 3, 4, 5, 6, 7
 
 
 class spd_config(ct.Structure):
@@ -51,7 +50,7 @@ class spd_weights(ct.Structure):
 
 class spd_step_result(ct.Structure):
     _fields_ = [(k, ct.c_int32) for k in
-                ("decision", "target_argmax", "draft", "pdm_draft", "exited_pos", "verified_pos",
+                ("decision", "target_argmax", "draft", "pdm_draft", "exited_pos", "exited_token", "verified_pos",
                  "verified_token", "committed_len", "inflight", "step_index")]
 
     def as_dict(self):
@@ -63,7 +62,7 @@ EXPORTS = [
     "spd_set_forced_drafts", "spd_clear_forced_drafts", "spd_run_steps", "spd_sync", "spd_read_debug",
     "spd_read_kv", "spd_set_debug", "spd_destroy", "spd_status_str", "spd_last_error",
     "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing", "spd_set_step_kernel",
-    "spd_set_step_trace", "spd_step_plan_info", "spd_set_kernel_trace", "spd_set_pdm_placement",
+    "spd_step_plan_info", "spd_set_kernel_trace", "spd_set_pdm_placement",
     "spd_set_pdm_grid", "spd_set_pdm_enabled", "spd_probe_hbm_read", "spd_set_sampling",
     "spd_set_pdm_schedule", "spd_set_graph_steps",
 ]
@@ -104,7 +103,6 @@ def lib() -> ct.CDLL:
             "spd_set_kernel_timing": (I, [P, I, I]),
             "spd_set_graph": (I, [P, I]),
             "spd_set_step_kernel": (I, [P, I, I, I]),
-            "spd_set_step_trace": (I, [P, I]),
             "spd_set_kernel_trace": (I, [P, I]),
             "spd_set_pdm_placement": (I, [P, I]),
             "spd_set_pdm_grid": (I, [P, I]),
@@ -247,20 +245,15 @@ def spd_set_graph(h: int, on: bool) -> None:
     _check("spd_set_graph", lib().spd_set_graph(h, 1 if on else 0), h)
 
 
-def spd_set_step_kernel(h: int, mode: int, grid: int = 0, skew: int = -1) -> None:
-    _check("spd_set_step_kernel", lib().spd_set_step_kernel(h, int(mode), int(grid), int(skew)), h)
-
-
-def spd_set_step_trace(h: int, on: bool) -> None:
-    _check("spd_set_step_trace", lib().spd_set_step_trace(h, 1 if on else 0), h)
+def spd_set_step_kernel(h: int, mode: int, grid: int = 0, groups: int = -1) -> None:
+    _check("spd_set_step_kernel", lib().spd_set_step_kernel(h, int(mode), int(grid), int(groups)), h)
 
 
 def spd_step_plan_info(h: int) -> dict:
-    info = (ct.c_int32 * 16)()
+    info = (ct.c_int32 * 8)()
     _check("spd_step_plan_info", lib().spd_step_plan_info(h, info), h)
-    return {"nitems": info[0], "J": info[1], "tiles": list(info[2:7]), "clock_khz": info[7],
-            "ntrace": info[8], "pstep_grid": info[9], "nkslots": info[10], "n": info[11],
-            "stage_groups": info[12], "pdm_place": info[13]}
+    return {"J": info[0], "clock_khz": info[1], "nkslots": info[2], "n": info[3],
+            "stage_groups": info[4], "pdm_place": info[5]}
 
 
 def spd_set_pdm_placement(h: int, place: int) -> None:
@@ -313,16 +306,6 @@ def spd_kernel_trace(h: int) -> dict:
     J, n, ns = info["J"], info["n"], info["nkslots"]
     raw = spd_read_debug(h, SPD_DBG_KTRACE, 2 * ns, np.uint64).reshape(ns, 2)
     return {"stage": raw[: 5 * J * n].reshape(J, 5, n, 2), "extra": raw[5 * J * n:], **info}
-
-
-def spd_step_trace(h: int) -> dict:
-    """The last traced step: tile items and their wall-clock stamps (see SPD_DBG_STEP_TRACE)."""
-    info = spd_step_plan_info(h)
-    n = info["nitems"]
-    items = spd_read_debug(h, SPD_DBG_STEP_ITEMS, n, np.uint32)
-    raw = spd_read_debug(h, SPD_DBG_STEP_TRACE, info["ntrace"], np.uint64)
-    stamps = raw[: 4 * n].reshape(n, 4)
-    return {"items": items, "stamps": stamps, "raw": raw, **info}
 
 
 def spd_destroy(h: int) -> None:

@@ -25,12 +25,11 @@ enum HState { H_INIT = 0, H_READY = 1, H_PENDING = 2 };
 struct Layout {
   size_t kv, pkv, pt, rope, state, tok, forced, log, resid, anch, pdmx, pfx, pfanch, dbg, lay;
   size_t q[2], ao[2], act[2], part[2], cnt[2], hkey[2];
-  size_t items, sync, dctx, trace, ktrace;
+  size_t ktrace;
   size_t su, swlog, swgmax, sqids, sqp, sqcnt, spq;  // sampled decoding
   size_t total;
   int wlog_stride;
-  int num_pages, chunk, max_splits, J, nitems, nsync, ntrace, nkslots;
-  int tiles[5];
+  int num_pages, chunk, max_splits, J, nkslots;
   size_t kv_layer_bytes;
 };
 
@@ -85,18 +84,10 @@ Layout make_layout(const spd_config& c) {
     L.chunk = c.attn_chunk ? c.attn_chunk : std::max(64, ch);
   }
   L.max_splits = (c.max_tokens + L.chunk - 1) / L.chunk;
-  // persistent step kernel: tiles per stage per sublayer, and the ticket table of one step
+  // layer slots per step: the longest stage
   L.J = 0;
   for (int s = 0; s < n; s++)
     L.J = std::max(L.J, (int)((long long)(s + 1) * c.n_layers / n) - (int)((long long)s * c.n_layers / n));
-  L.tiles[SK_QKV] = (c.n_q_heads + 2 * hkv) * (dh / 2 / kQPairs);
-  L.tiles[SK_ATTN] = hkv * L.max_splits;
-  L.tiles[SK_OPROJ] = (d + kORows - 1) / kORows;
-  L.tiles[SK_GATEUP] = (c.ffn_dim + kGOut - 1) / kGOut;
-  L.tiles[SK_DOWN] = (d + kDRows - 1) / kDRows;
-  L.nitems = 0;
-  for (int k = 0; k < 5; k++) L.nitems += L.J * n * L.tiles[k];
-  L.nsync = (2 + std::max(5 * L.J * n, kMaxStages * kBarParts)) * kSyncStride;
   L.kv_layer_bytes = (size_t)L.num_pages * 2 * hkv * c.page_size * dh * esz;
   size_t o = 0;
   auto take = [&](size_t bytes) {
@@ -129,11 +120,6 @@ Layout make_layout(const spd_config& c) {
     L.cnt[s] = take(sizeof(int32_t) * kMaxStages * hkv);
     L.hkey[s] = take(sizeof(unsigned long long));
   }
-  L.items = take(sizeof(uint32_t) * (size_t)L.nitems);
-  L.sync = take(sizeof(int32_t) * (size_t)L.nsync);
-  L.dctx = take(sizeof(Ctx));
-  L.ntrace = std::max(4 * L.nitems, 2048 * 5 * L.J * 3);
-  L.trace = take(sizeof(unsigned long long) * (size_t)L.ntrace);
   L.nkslots = 5 * L.J * n + 4;
   L.ktrace = take(sizeof(unsigned long long) * 2 * (size_t)L.nkslots);
   // sampled decoding: the head's wave regions cover at most V + 2 * (4 * kSampleWGs) floats per row
@@ -153,23 +139,6 @@ void stage_bounds(int L, int n, int* beta) {
   for (int s = 0; s <= n; s++) beta[s] = (int)((long long)s * L / n);
 }
 
-// Ticket order of the persistent step kernel. Super-phase P holds phase P - skew*s of every stage s
-// (stage by stage); skew 0 keeps the stages in lockstep, skew k > 0 staggers them by k sublayers so
-// that one stage's latency-bound sublayer (attention) overlaps other stages' weight streaming. In
-// every order a tile comes after the whole previous phase of its stage, which is all it waits for.
-std::vector<uint32_t> step_items(const Layout& L, int n, int skew) {
-  std::vector<uint32_t> v;
-  v.reserve(L.nitems);
-  const int NP = 5 * L.J;
-  for (int P = 0; P < NP + skew * (n - 1); P++)
-    for (int s = 0; s < n; s++) {
-      const int p = P - skew * s;
-      if (p < 0 || p >= NP) continue;
-      for (int t = 0; t < L.tiles[p % 5]; t++) v.push_back(step_item(p, s, t));
-    }
-  return v;
-}
-
 }  // namespace
 
 struct spd_handle {
@@ -181,8 +150,7 @@ struct spd_handle {
   int J = 0;  // layer slots per step = longest stage
   hipStream_t main = nullptr, pdm = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
-  std::vector<hipEvent_t> ev_pdm;  // placement 4: one per PDM launch
-  // step-kernel mode 2: one stream and one completion event per stage (default priority)
+  // stage groups (step-kernel mode 2): one stream and one completion event per group (default priority)
   hipStream_t sst[kMaxStages] = {};
   hipEvent_t ev_st[kMaxStages] = {};
   char* ws = nullptr;
@@ -196,15 +164,12 @@ struct spd_handle {
   std::string err;
   // step graph (fork/join of both streams captured once, replayed per step)
   int use_graph = 0;
-  // stage compute: 0 = five launches per layer slot, 1 = one persistent launch per step, 2 = one
-  // stream per stage
-  int step_mode = kStepModeDefault;
-  int step_grid = kStepGridDefault;
-  int step_skew = kStepSkewDefault;
+  // stage compute: 0 = five launches per layer slot on main_stream, 2 = stage groups on their own
+  // streams
+  int step_mode = 2;
   int stage_groups = 0;  // mode 2: streams the stages are spread over (0: kStageGroupsDefault)
   int pdm_place = 0;     // where the PDM's launches go (spd_set_pdm_placement)
   int pdm_on = 1;        // 0: the step skips the PDM's launches (spd_set_pdm_enabled)
-  int pstep_grid = 0;  // mode 4: workgroups, at most what the GPU holds at once
   hipGraphExec_t gexec = nullptr;
   hipGraphExec_t gexec_multi = nullptr;  // graph_steps steps in one graph (spd_run_steps)
   int graph_steps = 1;
@@ -320,31 +285,23 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
   if (sp) HIPC(hipEventRecord(sp[0], h->main));
   const bool fused = h->cfg.fused_head != 0;
   // Pipeline Draft Module: pre-step features only (Section 3.3), so it can run beside the stage
-  // compute; it ends by recording ev_join, which the LM head waits for.
-  // its launches, in order: the feature projection, five per PDM layer, the draft head if not fused
-  const int npdm = 1 + 5 * h->cfg.pdm_layers + (fused ? 0 : 1);
-  auto pdm_op = [&](int i, hipStream_t s) {
-    if (i == 0) {
-      Launch<WT>::pdm_fc(C, 0, 0, s);
-    } else if (i <= 5 * h->cfg.pdm_layers) {
-      const int l = (i - 1) / 5, k = (i - 1) % 5;
-      Launch<WT>::rows_sublayer(C, rows_block(h->cfg.n_layers + l, -1, -1, C.pdm_x, nullptr, -1, 1),
-                                h->cfg.n_stages, k, C.rows_wgs, s);
-    } else if (C.sam.top_k > 0) {  // the draft module's distribution, left for the exit row's pass
-      Launch<WT>::head_sample(C, 1, 0, 0, -1, 0, s);
-    } else {
-      Launch<WT>::head(C, 1, 0, s);
+  // compute; it ends by recording ev_join, which the LM head waits for. Its launches, in order: the
+  // feature projection, five per PDM layer, the draft head if not fused.
+  auto enqueue_pdm = [&](hipStream_t s) -> spd_status {
+    h->cur_slot = 0;
+    Launch<WT>::pdm_fc(C, 0, 0, s);
+    for (int l = 0; l < h->cfg.pdm_layers; l++)
+      Launch<WT>::rows_layer(C, rows_block(h->cfg.n_layers + l, -1, -1, C.pdm_x, nullptr, -1, 1),
+                             h->cfg.n_stages, C.rows_wgs, s);
+    if (!fused) {
+      if (C.sam.top_k > 0)  // the draft module's distribution, left for the exit row's pass
+        Launch<WT>::head_sample(C, 1, 0, 0, -1, 0, s);
+      else
+        Launch<WT>::head(C, 1, 0, s);
     }
-  };
-  auto pdm_end = [&](hipStream_t s) -> spd_status {
     if (sp) HIPC(hipEventRecord(sp[1], s));
     HIPC(hipEventRecord(h->ev_join, s));
     return SPD_OK;
-  };
-  auto enqueue_pdm = [&](hipStream_t s) -> spd_status {
-    h->cur_slot = 0;
-    for (int i = 0; i < npdm; i++) pdm_op(i, s);
-    return pdm_end(s);
   };
   const bool stage_streams = h->step_mode == 2;
   // post-step schedule: the PDM waits for the stage compute (placement 5, on main_stream after it)
@@ -363,155 +320,56 @@ static spd_status enqueue_step(spd_handle* h, int forced_override) {
     spd_status st = enqueue_pdm(h->pdm);
     if (st != SPD_OK) return st;
   }
-  // every active stage advances its token by one layer per slot (Section 3.1)
-  if (h->step_mode == 1) {
-    h->cur_slot = 0;
-    TimedLaunch t(h, h->main, SPD_K_STEP);
-    launch_step(C, (const Ctx*)(h->ws + h->lay.dctx), h->step_grid, h->main, h->bf16);
-  } else if (h->step_mode == 4) {
-    h->cur_slot = 0;
-    TimedLaunch t(h, h->main, SPD_K_STEP);
-    Launch<WT>::pstep(C, (const Ctx*)(h->ws + h->lay.dctx), h->pstep_grid, h->main);
-  } else if (h->step_mode == 3) {
-    // skewed schedule: launch L runs sublayer L - s of every stage s (Section 3.1's stages advance
-    // independently within a step), so each launch mixes independent sublayers of different stages
-    const int n = h->cfg.n_stages, NP = 5 * h->J;
-    const size_t esz = h->bf16 ? 2 : 4;
-    const int total = C.stream_wgs > 0 ? C.stream_wgs : kStreamWGs;
-    for (int L = 0; L < NP + n - 1; L++) {
-      MixLaunch m;
-      std::memset(&m, 0, sizeof(m));
-      struct G { int kind, s, slot; double bytes; int npairs; };
-      std::vector<G> gem;
-      int wg = 0;
-      for (int pass = 0; pass < 2; pass++) {  // attention parts first, then the weight-streaming ones
-        for (int st = 0; st < n; st++) {
-          const int p = L - st;
-          if (p < 0 || p >= NP) continue;
-          const int slot = p / 5, kind = p % 5, layer = C.beta[st] + slot;
-          if (layer >= C.beta[st + 1]) continue;
-          if ((kind == SK_ATTN) != (pass == 0)) continue;
-          if (kind == SK_ATTN) {
-            MixPart& P = m.p[m.nparts++];
-            P.kind = kind;
-            P.stage = st;
-            P.slot = slot;
-            P.ld = h->layer_desc[layer];
-            P.wg0 = wg;
-            P.nwg = C.hkv * C.max_splits;
-            wg += P.nwg;
-          } else {
-            G g;
-            g.kind = kind;
-            g.s = st;
-            g.slot = slot;
-            const double d = C.d, F = C.F, qd = C.qdim;
-            g.bytes = kind == SK_QKV ? (C.hq + 2 * C.hkv) * C.dh * d : kind == SK_OPROJ ? d * qd
-                      : kind == SK_GATEUP ? 2 * F * d : d * F;
-            g.npairs = kind == SK_QKV ? (C.hq + 2 * C.hkv) * (C.dh / 2) : kind == SK_GATEUP ? C.F : (C.d + 1) / 2;
-            gem.push_back(g);
-          }
-        }
-      }
-      double tot = 0;
-      for (const G& g : gem) tot += g.bytes;
-      for (const G& g : gem) {
-        int nwg = (int)std::lround(total * g.bytes / tot);
-        nwg = std::max(nwg, (g.npairs + 255) / 256);  // a wave streams at most 64 pairs
-        nwg = std::min(nwg, (g.npairs + 3) / 4);
-        nwg = std::max(nwg, 1);
-        MixPart& P = m.p[m.nparts++];
-        P.kind = g.kind;
-        P.stage = g.s;
-        P.slot = g.slot;
-        P.ld = h->layer_desc[C.beta[g.s] + g.slot];
-        P.wg0 = wg;
-        P.nwg = nwg;
-        wg += nwg;
-      }
-      if (m.nparts == 0) continue;
-      h->cur_slot = L / 5;
-      TimedLaunch t(h, h->main, SPD_K_MIX);
-      Launch<WT>::mix(C, m, wg, h->main);
-    }
-    (void)esz;
-  } else {
-    // mode 0: every launch covers all stages, on main_stream. mode 2: the stages are spread over G
-    // groups of consecutive stages, each group running its own chain of launches (covering its
-    // stages) on its own stream, forked from and joined to main_stream, so that one group's
-    // latency-bound attention and launch tails overlap the other groups' weight streaming.
-    const int n = h->cfg.n_stages;
-    const int groups =
-        h->step_mode == 2 ? std::min(h->stage_groups > 0 ? h->stage_groups : kStageGroupsDefault, n) : 1;
-    hipStream_t gs[kMaxStages];
+  // every active stage advances its token by one layer per slot (Section 3.1). mode 0: every launch
+  // covers all stages, on main_stream. mode 2: the stages are spread over G groups of consecutive
+  // stages, each group running its own chain of launches (covering its stages) on its own stream,
+  // forked from and joined to main_stream, so that one group's latency-bound attention and launch
+  // tails overlap the other groups' weight streaming.
+  const int n = h->cfg.n_stages;
+  const int groups =
+      h->step_mode == 2 ? std::min(h->stage_groups > 0 ? h->stage_groups : kStageGroupsDefault, n) : 1;
+  hipStream_t gs[kMaxStages];
+  for (int gi = 0; gi < groups; gi++) {
+    gs[gi] = h->step_mode == 2 ? h->sst[gi] : h->main;
+    if (h->step_mode == 2) HIPC(hipStreamWaitEvent(gs[gi], h->ev_fork, 0));
+  }
+  if (place == 2) {  // first group's stream, before its stage launches
+    spd_status st = enqueue_pdm(gs[0]);
+    if (st != SPD_OK) return st;
+  }
+  for (int j = 0; j < h->J; j++) {
     for (int gi = 0; gi < groups; gi++) {
-      gs[gi] = h->step_mode == 2 ? h->sst[gi] : h->main;
-      if (h->step_mode == 2) HIPC(hipStreamWaitEvent(gs[gi], h->ev_fork, 0));
-    }
-    if (place == 2) {  // first group's stream, before its stage launches
-      spd_status st = enqueue_pdm(gs[0]);
-      if (st != SPD_OK) return st;
-    }
-    // Placement 4 spreads the PDM over the groups' streams: launch i runs on group i mod G after that
-    // group's layer slot min(i, J - 1), ordered after launch i - 1 by an event; a layer slot takes
-    // much longer than one PDM launch, so no group waits. Launches are enqueued slot by slot across
-    // the groups, so each event is recorded before it is waited for.
-    int pi = 0;
-    auto spread = [&](int j, int gi) -> spd_status {
-      while (place == 4 && pi < npdm && pi % groups == gi && std::min(pi, h->J - 1) <= j) {
-        if (pi > 0) HIPC(hipStreamWaitEvent(gs[gi], h->ev_pdm[pi - 1], 0));
-        const int keep = h->cur_slot;
-        h->cur_slot = 0;  // not a timed stage launch
-        pdm_op(pi, gs[gi]);
-        h->cur_slot = keep;
-        HIPC(hipEventRecord(h->ev_pdm[pi], gs[gi]));
-        if (++pi == npdm) {
-          spd_status st = pdm_end(gs[gi]);
-          if (st != SPD_OK) return st;
+      const int s0 = gi * n / groups, s1 = (gi + 1) * n / groups;
+      h->cur_slot = j;
+      Rows r;
+      std::memset(&r, 0, sizeof(Rows));
+      r.kind = 0;
+      r.slot = j;
+      r.stage0 = s0;
+      r.nst = s1 - s0;
+      r.nrows = 1;
+      r.cap = -1;
+      bool any = false;
+      for (int st = 0; st < kMaxStages; st++) {
+        const int l = (st >= r.stage0 && st < r.stage0 + r.nst) ? C.beta[st] + j : -1;
+        if (l >= 0 && l < C.beta[st + 1]) {
+          r.ld[st] = h->layer_desc[l];
+          any = true;
+        } else {
+          std::memset(&r.ld[st], 0, sizeof(LayerDesc));
         }
       }
-      return SPD_OK;
-    };
-    for (int j = 0; j < h->J; j++) {
-      for (int gi = 0; gi < groups; gi++) {
-        const int s0 = gi * n / groups, s1 = (gi + 1) * n / groups;
-        h->cur_slot = j;
-        Rows r;
-        std::memset(&r, 0, sizeof(Rows));
-        r.kind = 0;
-        r.slot = j;
-        r.stage0 = s0;
-        r.nst = s1 - s0;
-        r.nrows = 1;
-        r.cap = -1;
-        bool any = false;
-        for (int st = 0; st < kMaxStages; st++) {
-          const int l = (st >= r.stage0 && st < r.stage0 + r.nst) ? C.beta[st] + j : -1;
-          if (l >= 0 && l < C.beta[st + 1]) {
-            r.ld[st] = h->layer_desc[l];
-            any = true;
-          } else {
-            std::memset(&r.ld[st], 0, sizeof(LayerDesc));
-          }
-        }
-        if (any) enqueue_layer<WT>(C, r, gs[gi], h);
-        spd_status st = spread(j, gi);
-        if (st != SPD_OK) return st;
-      }
+      if (any) enqueue_layer<WT>(C, r, gs[gi], h);
     }
-    for (int guard = 0; place == 4 && pi < npdm && guard < npdm * kMaxStages; guard++) {  // leftovers
-      spd_status st = spread(h->J - 1, pi % groups);
-      if (st != SPD_OK) return st;
-    }
-    if (place == 3) {  // first group's stream, after its stage launches
-      spd_status st = enqueue_pdm(gs[0]);
-      if (st != SPD_OK) return st;
-    }
-    if (h->step_mode == 2) {
-      for (int gi = 0; gi < groups; gi++) {
-        HIPC(hipEventRecord(h->ev_st[gi], gs[gi]));
-        HIPC(hipStreamWaitEvent(h->main, h->ev_st[gi], 0));
-      }
+  }
+  if (place == 3) {  // first group's stream, after its stage launches
+    spd_status st = enqueue_pdm(gs[0]);
+    if (st != SPD_OK) return st;
+  }
+  if (h->step_mode == 2) {
+    for (int gi = 0; gi < groups; gi++) {
+      HIPC(hipEventRecord(h->ev_st[gi], gs[gi]));
+      HIPC(hipStreamWaitEvent(h->main, h->ev_st[gi], 0));
     }
   }
   if (place == 5) {  // post-step features: after every stage of this step, before the exit head
@@ -675,8 +533,6 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
     HIPI(hipStreamCreateWithFlags(&h->sst[st], hipStreamNonBlocking));
     HIPI(hipEventCreateWithFlags(&h->ev_st[st], hipEventDisableTiming));
   }
-  h->ev_pdm.assign(2 + 5 * (size_t)cfg->pdm_layers, nullptr);
-  for (hipEvent_t& e : h->ev_pdm) HIPI(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   HIPI(hipHostMalloc((void**)&h->pinned, sizeof(spd_step_result) * (kLogCap + 1), hipHostMallocDefault));
 
   const spd_config& c = *cfg;
@@ -760,14 +616,6 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   C.sam.pq_ids = (int32_t*)(ws + lay.spq);
   C.sam.pq_p = (float*)(ws + lay.spq + sizeof(int32_t) * kMaxTopK);
   C.sam.pq_cnt = (int32_t*)(ws + lay.spq + (sizeof(int32_t) + sizeof(float)) * kMaxTopK);
-  C.plan.items = (const uint32_t*)(ws + lay.items);
-  C.plan.nitems = lay.nitems;
-  C.plan.sync = (int32_t*)(ws + lay.sync);
-  C.plan.nsync = lay.nsync;
-  for (int k = 0; k < 5; k++) C.plan.tiles[k] = lay.tiles[k];
-  C.plan.trace = nullptr;
-  C.plan.ntrace = lay.ntrace;
-  const std::vector<uint32_t> items = step_items(lay, c.n_stages, kStepSkewDefault);
 
   // layer table
   std::vector<LayerDesc> ld(c.n_layers + c.pdm_layers);
@@ -818,12 +666,8 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   HIPI(hipMemsetAsync(ws + lay.forced, 0xff, sizeof(int32_t) * (c.max_tokens + 8), h->main));
   for (int s = 0; s < 2; s++) HIPI(hipMemsetAsync(ws + lay.cnt[s], 0, sizeof(int32_t) * kMaxStages * c.n_kv_heads, h->main));
   for (int s = 0; s < 2; s++) HIPI(hipMemsetAsync(ws + lay.hkey[s], 0, sizeof(unsigned long long), h->main));
-  HIPI(hipMemcpyAsync(ws + lay.items, items.data(), sizeof(uint32_t) * items.size(), hipMemcpyHostToDevice, h->main));
-  HIPI(hipMemsetAsync(ws + lay.sync, 0, sizeof(int32_t) * lay.nsync, h->main));
   HIPI(hipMemsetAsync(ws + lay.sqcnt, 0, sizeof(int32_t) * c.n_stages, h->main));
   HIPI(hipMemsetAsync(ws + lay.spq, 0, (sizeof(int32_t) + sizeof(float)) * kMaxTopK + sizeof(int32_t), h->main));
-  // the persistent step kernel reads the context from device memory
-  HIPI(hipMemcpyAsync(ws + lay.dctx, &C, sizeof(Ctx), hipMemcpyHostToDevice, h->main));
   HIPI(hipStreamSynchronize(h->main));
 #undef HIPI
   *out = h;
@@ -833,64 +677,13 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
 static void drop_graph(spd_handle* h);
 static spd_status run_one_step(spd_handle* h, int forced_override);
 
-// Workgroups of the grouped persistent step kernel: the requested number (0: kStepGridDefault),
-// at most what the GPU holds at once (its per-stage waits need every workgroup resident), and at least
-// enough per stage that no wave streams more than 64 row pairs.
-static spd_status size_pstep(spd_handle* h, int grid) {
-  const Ctx& C = h->ctx;
-  int per_cu = 0, cus = 0;
-  const void* fn = h->bf16 ? Launch<uint16_t>::pstep_fn(C) : Launch<float>::pstep_fn(C);
-  const size_t lds = h->bf16 ? Launch<uint16_t>::pstep_lds(C) : Launch<float>::pstep_lds(C);
-  HIPC(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kWG, lds));
-  HIPC(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, h->dev));
-  const int cap = per_cu * cus;
-  int g = std::min(grid > 0 ? grid : kStepGridDefault, cap);
-  const int npmax = std::max(std::max(C.F, (C.hq + 2 * C.hkv) * (C.dh / 2)), (C.d + 1) / 2);
-  const int need = h->cfg.n_stages * ((npmax + 255) / 256);
-  if (g < need) {
-    h->err = "grouped step kernel: the GPU holds " + std::to_string(cap) + " workgroups, " + std::to_string(need) +
-             " are needed";
+spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t groups) {
+  if (!h || (mode != 0 && mode != 2) || grid < 0 || grid > 65535 || groups < -1 || groups > kMaxStages)
     return SPD_E_INVAL;
-  }
-  h->pstep_grid = g;
-  return SPD_OK;
-}
-
-spd_status spd_set_step_kernel(spd_handle* h, int32_t mode, int32_t grid, int32_t skew) {
-  if (!h || mode < 0 || mode > 4 || grid < 0 || grid > 65535 || skew < -1 || skew > 16) return SPD_E_INVAL;
-  if (mode == 4) {
-    HIPC(hipSetDevice(h->dev));
-    spd_status st = size_pstep(h, grid);
-    if (st != SPD_OK) return st;
-  }
   h->step_mode = mode;
-  if (mode == 1)
-    h->step_grid = grid ? grid : kStepGridDefault;
-  else if (mode != 4)
-    h->ctx.stream_wgs = grid;  // 0: default
-  if (mode == 2) {
-    if (skew >= 0) h->stage_groups = skew;
-  } else if (skew >= 0 && skew != h->step_skew) {
-    HIPC(hipSetDevice(h->dev));
-    HIPC(hipStreamSynchronize(h->pdm));
-    HIPC(hipStreamSynchronize(h->main));
-    const std::vector<uint32_t> items = step_items(h->lay, h->cfg.n_stages, skew);
-    HIPC(hipMemcpy(h->ws + h->lay.items, items.data(), sizeof(uint32_t) * items.size(), hipMemcpyHostToDevice));
-    h->step_skew = skew;
-  }
+  h->ctx.stream_wgs = grid;  // 0: default
+  if (mode == 2 && groups >= 0) h->stage_groups = groups;
   drop_graph(h);  // the captured launches change
-  return SPD_OK;
-}
-
-spd_status spd_set_step_trace(spd_handle* h, int32_t on) {
-  if (!h) return SPD_E_INVAL;
-  HIPC(hipSetDevice(h->dev));
-  HIPC(hipStreamSynchronize(h->pdm));
-  HIPC(hipStreamSynchronize(h->main));
-  h->ctx.plan.trace = on ? (unsigned long long*)(h->ws + h->lay.trace) : nullptr;
-  if (on) HIPC(hipMemset(h->ws + h->lay.trace, 0, sizeof(unsigned long long) * (size_t)h->lay.ntrace));
-  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
-  drop_graph(h);
   return SPD_OK;
 }
 
@@ -919,7 +712,6 @@ spd_status spd_set_sampling(spd_handle* h, int32_t top_k, float temperature, con
   HIPC(hipMemcpy(h->ws + h->lay.su, uniforms, sizeof(float) * 3 * (size_t)positions, hipMemcpyHostToDevice));
   h->ctx.sam.top_k = top_k;
   h->ctx.sam.inv_temp = 1.0f / temperature;
-  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
   drop_graph(h);  // the captured launches change
   return SPD_OK;
 }
@@ -929,7 +721,6 @@ spd_status spd_set_pdm_schedule(spd_handle* h, int32_t post_step) {
   HIPC(hipSetDevice(h->dev));
   HIPC(hipStreamSynchronize(h->main));
   h->ctx.post_step = post_step;
-  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
   drop_graph(h);  // the captured launches change
   return SPD_OK;
 }
@@ -961,11 +752,7 @@ spd_status spd_probe_hbm_read(const void* buf, size_t bytes, float* sink, int32_
 }
 
 spd_status spd_set_pdm_placement(spd_handle* h, int32_t place) {
-  if (!h || place < 0 || place > 4) return SPD_E_INVAL;
-  if (place == 4 && h->use_graph) {
-    h->err = "PDM placement 4 is not captured into the step graph (turn graph mode off first)";
-    return SPD_E_INVAL;
-  }
+  if (!h || place < 0 || place > 3) return SPD_E_INVAL;
   h->pdm_place = place;
   drop_graph(h);  // the captured launches change
   return SPD_OK;
@@ -984,28 +771,23 @@ spd_status spd_set_kernel_trace(spd_handle* h, int32_t on) {
   HIPC(hipStreamSynchronize(h->pdm));
   HIPC(hipStreamSynchronize(h->main));
   h->ctx.ktrace = on ? (unsigned long long*)(h->ws + h->lay.ktrace) : nullptr;
-  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
   drop_graph(h);  // kernel arguments changed
   return SPD_OK;
 }
 
 spd_status spd_step_plan_info(spd_handle* h, int32_t* info) {
   if (!h || !info) return SPD_E_INVAL;
-  info[0] = h->lay.nitems;
-  info[1] = h->lay.J;
-  for (int k = 0; k < 5; k++) info[2 + k] = h->lay.tiles[k];
+  for (int i = 0; i < 8; i++) info[i] = 0;
+  info[0] = h->lay.J;
   int khz = 0;
   HIPC(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->dev));
-  info[7] = khz;
-  info[8] = h->lay.ntrace;
-  info[9] = h->pstep_grid;
-  info[10] = h->lay.nkslots;
-  info[11] = h->cfg.n_stages;
-  info[12] = h->step_mode == 2 ? std::min(h->stage_groups > 0 ? h->stage_groups : kStageGroupsDefault,
-                                          h->cfg.n_stages)
-                               : 1;
-  info[13] = h->pdm_place;
-  info[14] = info[15] = 0;
+  info[1] = khz;
+  info[2] = h->lay.nkslots;
+  info[3] = h->cfg.n_stages;
+  info[4] = h->step_mode == 2 ? std::min(h->stage_groups > 0 ? h->stage_groups : kStageGroupsDefault,
+                                         h->cfg.n_stages)
+                              : 1;
+  info[5] = h->pdm_place;
   return SPD_OK;
 }
 
@@ -1015,19 +797,13 @@ spd_status spd_set_debug(spd_handle* h, int32_t on) {
   HIPC(hipStreamSynchronize(h->pdm));
   HIPC(hipStreamSynchronize(h->main));
   h->ctx.debug = on ? 1 : 0;
-  HIPC(hipMemcpy(h->ws + h->lay.dctx, &h->ctx, sizeof(Ctx), hipMemcpyHostToDevice));
   drop_graph(h);  // kernel arguments changed
   return SPD_OK;
 }
 
 static spd_status fetch_state(spd_handle* h) {
   HIPC(hipMemcpyAsync(h->pinned, &h->ctx.st->res, sizeof(spd_step_result), hipMemcpyDeviceToHost, h->main));
-  HIPC(hipMemcpyAsync(&h->pinned[1].decision, &h->ctx.st->err, sizeof(int32_t), hipMemcpyDeviceToHost, h->main));
   HIPC(hipStreamSynchronize(h->main));
-  if (h->pinned[1].decision != 0) {
-    h->err = "step kernel: a dependency wait timed out; the step's results are invalid";
-    return SPD_E_HIP;
-  }
   const spd_step_result& r = h->pinned[0];
   h->c = r.committed_len;
   h->a = r.inflight;
@@ -1139,10 +915,6 @@ spd_status spd_set_graph_steps(spd_handle* h, int32_t steps) {
 
 spd_status spd_set_graph(spd_handle* h, int32_t on) {
   if (!h) return SPD_E_INVAL;
-  if (on && h->pdm_place == 4) {
-    h->err = "PDM placement 4 is not captured into the step graph (choose another placement first)";
-    return SPD_E_INVAL;
-  }
   h->use_graph = on ? 1 : 0;
   if (!on) drop_graph(h);
   return SPD_OK;
@@ -1257,14 +1029,9 @@ spd_status spd_read_debug(spd_handle* h, int32_t what, void* host, size_t bytes)
     case SPD_DBG_TOKENS: src = h->ctx.tok; need = sizeof(int32_t) * c.max_tokens; break;
     case SPD_DBG_STATE: src = nullptr; need = sizeof(int32_t) * 4; break;
     case SPD_DBG_QDIST: src = nullptr; need = sizeof(int32_t) * c.n_stages * (1 + 2 * kMaxTopK); break;
-    case SPD_DBG_STEP_ITEMS: src = h->ctx.plan.items; need = sizeof(uint32_t) * (size_t)h->lay.nitems; break;
     case SPD_DBG_KTRACE:
       src = h->ws + h->lay.ktrace;
       need = sizeof(unsigned long long) * 2 * (size_t)h->lay.nkslots;
-      break;
-    case SPD_DBG_STEP_TRACE:
-      src = h->ws + h->lay.trace;
-      need = sizeof(unsigned long long) * (size_t)h->lay.ntrace;
       break;
     default: return SPD_E_INVAL;
   }
@@ -1328,7 +1095,7 @@ spd_status spd_read_kv(spd_handle* h, int32_t pdm, int32_t layer, int32_t pos0, 
 }
 
 spd_status spd_set_kernel_timing(spd_handle* h, int32_t kernel, int32_t first_slot) {
-  if (!h || kernel < 0 || kernel > SPD_K_MIX || first_slot < 0) return SPD_E_INVAL;
+  if (!h || kernel < 0 || kernel > SPD_K_SPANS || first_slot < 0) return SPD_E_INVAL;
   h->timed_kernel = kernel;
   h->timed_first_slot = first_slot;
   return SPD_OK;
@@ -1384,8 +1151,6 @@ void spd_destroy(spd_handle* h) {
     if (h->ev_st[st]) (void)hipEventDestroy(h->ev_st[st]);
     if (h->sst[st]) (void)hipStreamDestroy(h->sst[st]);
   }
-  for (hipEvent_t e : h->ev_pdm)
-    if (e) (void)hipEventDestroy(e);
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_join) (void)hipEventDestroy(h->ev_join);
   if (h->pinned) (void)hipHostFree(h->pinned);

@@ -1,6 +1,5 @@
-// Decode attention of one stage's token over one KV head's paged cache, one key split per workgroup
-// (the stage launches, the mixed launches and the persistent step kernels share it, so all compute
-// the same bits).
+// Decode attention of one token over one KV head's paged cache, one key split per workgroup (the
+// stage launches and the row-block launches share it, so both compute the same bits).
 //
 // The token at position pos0 attends to keys 0..pos0 of its own layer (Section 3.1: each stage's
 // token reads the cache of the layer it is on). Its G query heads share KV head g (grouped-query
@@ -48,14 +47,6 @@ struct AttnLds {
 template <typename KVT, int DH>
 constexpr size_t attn_split_lds() {
   return AttnLds<KVT, DH>::kTotal;
-}
-
-// 16 bytes (16-byte aligned) with device-scope loads.
-__device__ __forceinline__ uint4 ldg16_coherent(const void* p) {
-  unsigned long long* q = (unsigned long long*)const_cast<void*>(p);
-  const unsigned long long a = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const unsigned long long b = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return make_uint4((uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32));
 }
 
 // KV cache reads. Ordinary loads: a round's keys come back faster than with the non-temporal hint.
@@ -117,7 +108,7 @@ __device__ __forceinline__ void lds_row(const T* p, float* o) {
 }
 
 // One split with GP head slots (4: G <= 4, 8: G <= 8). Arguments as for attn_split.
-template <typename KVT, int DH, bool COH, int GP>
+template <typename KVT, int DH, int GP>
 __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float* out, float* rec_base, int* cnt,
                              int g, int split, int nsplit, int k0, int k1, int pos0, int page0, float* lds) {
   constexpr int TPK = kAttnTPK, NE = DH / TPK, VE = Elt<KVT>::VE, KCH = NE / VE;
@@ -151,7 +142,7 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
 #pragma unroll
   for (int i = 0; i < QPT; i++) {
     const int e = min(tid + i * kWG, G * DH - 1);
-    qv[i] = COH ? ld_dev(q + e) : q[e];
+    qv[i] = q[e];
   }
   auto page_of = [&](int r) { return C.page_table[min(k0 + r * PASS + my, k1 - 1) / C.page]; };
   int pg_next = page_of(1);
@@ -159,17 +150,10 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
   auto issue = [&](int r, int page, uint4* kr, uint4* vr) {
     const int key = min(k0 + r * PASS + my, k1 - 1);
     const KVT* base = kvb + (size_t)page * page_elems + head_off + (size_t)(key % C.page) * DH + qq * NE;
-    if (COH) {  // the newest key was written by this launch
 #pragma unroll
-      for (int c = 0; c < KCH; c++) kr[c] = ldg16_coherent(reinterpret_cast<const uint4*>(base) + c);
+    for (int c = 0; c < KCH; c++) kr[c] = ldkv16(reinterpret_cast<const uint4*>(base) + c);
 #pragma unroll
-      for (int c = 0; c < KCH; c++) vr[c] = ldg16_coherent(reinterpret_cast<const uint4*>(base + voff) + c);
-    } else {
-#pragma unroll
-      for (int c = 0; c < KCH; c++) kr[c] = ldkv16(reinterpret_cast<const uint4*>(base) + c);
-#pragma unroll
-      for (int c = 0; c < KCH; c++) vr[c] = ldkv16(reinterpret_cast<const uint4*>(base + voff) + c);
-    }
+    for (int c = 0; c < KCH; c++) vr[c] = ldkv16(reinterpret_cast<const uint4*>(base + voff) + c);
   };
   issue(0, page0, kb0, vb0);
   {
@@ -324,10 +308,7 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
       const int e = tid + i * kWG, qi = e / (DH / 2), dp = e % (DH / 2);
       if (qi < G) {
         const float inv = 1.0f / Ls[i];
-        if (COH)
-          st_dev2f(out + qi * DH + 2 * dp, A0[i] * inv, A1[i] * inv);
-        else
-          *reinterpret_cast<float2*>(out + qi * DH + 2 * dp) = make_float2(A0[i] * inv, A1[i] * inv);
+        *reinterpret_cast<float2*>(out + qi * DH + 2 * dp) = make_float2(A0[i] * inv, A1[i] * inv);
       }
     }
     return true;
@@ -405,29 +386,25 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
         }
       }
       const float inv = 1.0f / L;
-      if (COH)
-        st_dev2f(out + qi * DH + 2 * dp, a0 * inv, a1 * inv);
-      else
-        *reinterpret_cast<float2*>(out + qi * DH + 2 * dp) = make_float2(a0 * inv, a1 * inv);
+      *reinterpret_cast<float2*>(out + qi * DH + 2 * dp) = make_float2(a0 * inv, a1 * inv);
     }
   }
   if (tid == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   return true;
 }
 
-// One split. COH: the query and the newest key (pos0) were written by the same launch (device-scope
-// loads) and the output goes to a tile of the same launch (device-scope stores). kvb: the layer's
+// One split. kvb: the layer's
 // cache; q: the G rotated query rows of this head group; out: their G output rows; rec_base: the
 // (o[8][DH], m[8], l[8]) records of this (stage, head), one per split; cnt: its split ticket (zero at
 // rest); page0: the physical page of this thread's key in the first round (key k0 + threadIdx.x / 4,
 // clamped; requested by the caller before anything else). Returns true when this workgroup wrote the
 // final output.
-template <typename KVT, int DH, bool COH>
+template <typename KVT, int DH>
 __device__ bool attn_split(const Ctx& C, const KVT* kvb, const float* q, float* out, float* rec_base, int* cnt, int g,
                            int split, int nsplit, int k0, int k1, int pos0, int page0, float* lds) {
   if (C.G <= 4)
-    return attn_split_g<KVT, DH, COH, 4>(C, kvb, q, out, rec_base, cnt, g, split, nsplit, k0, k1, pos0, page0, lds);
-  return attn_split_g<KVT, DH, COH, 8>(C, kvb, q, out, rec_base, cnt, g, split, nsplit, k0, k1, pos0, page0, lds);
+    return attn_split_g<KVT, DH, 4>(C, kvb, q, out, rec_base, cnt, g, split, nsplit, k0, k1, pos0, page0, lds);
+  return attn_split_g<KVT, DH, 8>(C, kvb, q, out, rec_base, cnt, g, split, nsplit, k0, k1, pos0, page0, lds);
 }
 
 }  // namespace spd

@@ -38,7 +38,6 @@ struct DevState {
   int32_t nsteps;
   int32_t y;           // target argmax of this step's exiting token
   int32_t pdm_draft;   // PDM argmax of this step
-  int32_t err;         // sticky: a dependency wait of the step kernel timed out
   spd_step_result res; // last step
   int32_t head_ticket; // workgroups of the fused LM head + verify launch that are done (zero at rest)
   int32_t pad1[5];
@@ -57,18 +56,11 @@ struct BufSet {
   unsigned long long* hkey;
 };
 
-// Work items of the persistent step kernel. One step is 5J phases (layer slot j = p / 5, sublayer
-// p % 5); every active stage has a fixed number of tiles per phase. An item is (phase, stage, tile).
+// Sublayers of a layer slot, in launch order (the launch trace's slot index uses the same order).
 enum StepKind { SK_QKV = 0, SK_ATTN = 1, SK_OPROJ = 2, SK_GATEUP = 3, SK_DOWN = 4 };
-constexpr int kQPairs = 16;  // QKV item: 16 RoPE pairs of one head (32 weight rows, 4 pairs per wave)
-constexpr int kORows = 16;   // O-proj item: 16 rows (2 row pairs per wave)
-constexpr int kGOut = 16;    // gate/up item: 16 outputs = 32 weight rows (4 per wave)
-constexpr int kDRows = 8;    // down item: 8 rows (1 row pair per wave)
-constexpr int kStepGridDefault = 512;
-constexpr int kStepSkewDefault = 0;
-constexpr int kStepModeDefault = 2;
-// mode 2: stage groups (streams). With the PDM's stream, more than four parallel chains per step make
-// the runtime run one chain after another; two groups keep every chain running from the fork.
+// Stage groups: the stages of a step are spread over this many streams (groups of consecutive
+// stages). With the PDM's stream, more than four parallel chains per step make the runtime run one
+// chain after another; two groups keep every chain running from the fork.
 constexpr int kStageGroupsDefault = 2;
 constexpr int kStreamWGs = 1024;  // workgroups of one streaming stage launch (all its stages)
 // PDM row-block GEMV launches run beside the stage compute: a few workgroups, so that most CUs (and
@@ -80,21 +72,6 @@ constexpr int kRowsWGsDefault = 32;
 constexpr int kMaxTopK = 64;
 constexpr int kSampleWGs = 1024;
 constexpr int kSelCap = 1024;
-__host__ __device__ inline uint32_t step_item(int p, int s, int t) {
-  return ((uint32_t)p << 19) | ((uint32_t)s << 16) | (uint32_t)t;
-}
-
-// Counters of the persistent step kernel, each on its own 128-byte line so that polls of one do not
-// contend with atomics on another: the ticket counter, the timeout flag, and per (phase, stage) the
-// number of finished units.
-constexpr int kSyncStride = 32;  // ints per line
-__host__ __device__ inline int sync_ticket() { return 0; }
-__host__ __device__ inline int sync_err() { return kSyncStride; }
-__host__ __device__ inline int sync_done(int p, int s, int n) { return (2 + p * n + s) * kSyncStride; }
-// grouped persistent kernel: stage s's arrival counters, kBarParts of them (one line each)
-constexpr int kBarParts = 8;
-__host__ __device__ inline int sync_bar(int s) { return (2 + s * kBarParts) * kSyncStride; }
-
 // Sampled decoding state. The sampled LM-head launch leaves every logit of its rows in wlog, one
 // region of cmax = 2*ceil(pairs / waves) floats per wave (entry i of wave w is vocabulary row
 // 2*(w + (i/2)*waves) + i%2), and each workgroup's best key per row in wgmax; q_* hold the draft
@@ -113,17 +90,6 @@ struct Sampler {
   int32_t* pq_ids;            // [kMaxTopK]
   float* pq_p;                // [kMaxTopK]
   int32_t* pq_cnt;            // [1]
-};
-
-struct StepPlan {
-  const uint32_t* items;  // ticket -> item
-  int nitems;
-  int* sync;              // counters (sync_ticket, sync_err, sync_done)
-  int nsync;              // ints in sync ((2 + 5J*n) * kSyncStride)
-  int tiles[5];           // tiles per stage per sublayer kind (attention: Hkv * max_splits)
-  unsigned long long* trace;  // null, or per ticket 4 wall-clock stamps: start, inputs ready, staged, end
-                              // (grouped kernel: per workgroup and sublayer 3 stamps: wait start, wait end, end)
-  int ntrace;                 // stamps the trace buffer holds
 };
 
 struct Ctx {
@@ -158,7 +124,6 @@ struct Ctx {
   float* dbg_logits;// [2][V]
   int debug;
   BufSet b[2];      // 0: target stream, 1: PDM stream
-  StepPlan plan;    // persistent step kernel
   unsigned long long* ktrace;  // null, or the launch trace: per slot (first start, last end) wall clock
   int stream_wgs;   // workgroups of one streaming stage launch (all its stages)
   int rows_wgs;     // at most this many workgroups per row-block (PDM) GEMV launch (0: no cap)
@@ -187,21 +152,6 @@ struct Rows {
   // kind 0: layer beta_s + slot of every stage s, passed with the launch so that weight loads need
   // no table lookup (all pointers null for a stage with no layer in this slot)
   LayerDesc ld[kMaxStages];
-};
-
-// One launch of the skewed schedule (step-kernel mode 3): part i is sublayer `kind` (StepKind) of
-// stage `stage` in layer slot `slot`, on workgroups [wg0, wg0 + nwg) of the launch.
-struct MixPart {
-  int kind;
-  int stage;
-  int slot;
-  int wg0;
-  int nwg;
-  LayerDesc ld;
-};
-struct MixLaunch {
-  int nparts;
-  MixPart p[kMaxStages];
 };
 
 // Launchers (spd_kernels.hip). All are asynchronous on `stream`.
@@ -237,21 +187,11 @@ struct Launch {
   static void head_sample(const Ctx& c, int src, int row, int pos, int forced_override, int auto_rb,
                           void* stream);
   static void embed_rows(const Ctx& c, int t0, int nrows, void* stream);
-  // one launch of the skewed schedule, nwg workgroups
-  static void mix(const Ctx& c, const MixLaunch& m, int nwg, void* stream);
-  // the grouped persistent step kernel (dev_ctx: a device copy of c), its LDS bytes and function
-  static void pstep(const Ctx& c, const Ctx* dev_ctx, int grid, void* stream);
-  static size_t pstep_lds(const Ctx& c);
-  static const void* pstep_fn(const Ctx& c);
 };
-// Every layer slot of every active stage of one step in one persistent launch (spd_step.hip).
-// dev_ctx: a device copy of c.
-void launch_step(const Ctx& c, const Ctx* dev_ctx, int grid, void* stream, int bf16);
 void launch_ktrace_reset(const Ctx& c, int nslots, void* stream);
 // Streaming read of n16 16-byte blocks (a bandwidth probe); sink gets one float per workgroup.
 void launch_read_probe(const void* buf, size_t n16, float* sink, void* stream);
 constexpr int kReadProbeWGs = 2048;
-size_t step_lds_bytes(const Ctx& c, int bf16);
 // Events (hipEvent_t) that the next launches of this host thread record at their own start and end;
 // nullptr turns it off.
 void set_launch_events(void* start, void* stop);

@@ -169,46 +169,8 @@ __device__ __forceinline__ void wait_own_stores() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-constexpr int kSpinLimit = 1 << 20;
-
 __device__ __forceinline__ int ld_dev_i(const int* p) {
   return __hip_atomic_load(const_cast<int*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Thread 0 of a workgroup: wait until sync[idx] reaches target. Bounded: after kSpinLimit polls
-// (roughly a second) the launch's timeout flag is raised, which the host reports as an error, and every
-// later wait of the launch returns at once, so the grid always drains. The timeout flag
-// is looked at every 64 polls only, to keep polls off its line.
-static __device__ __noinline__ void wait_count(int* sync, int idx, int target) {
-  int spins = 0;
-  while (ld_dev_i(sync + idx) < target) {
-    ++spins;
-    if ((spins & 63) == 0 && ld_dev_i(sync + sync_err()) != 0) return;
-    if (spins > kSpinLimit) {
-      __hip_atomic_store(sync + sync_err(), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return;
-    }
-    __builtin_amdgcn_s_sleep(2);
-  }
-}
-
-// Thread 0 of a workgroup: wait until the sum of the `parts` counters sync[idx + i * kSyncStride]
-// reaches target (same bound and timeout behaviour as wait_count). Arrivals spread over several
-// counters (each on its own line) contend less than arrivals on one.
-static __device__ __noinline__ void wait_count_sum(int* sync, int idx, int parts, int target) {
-  int spins = 0;
-  for (;;) {
-    int tot = 0;
-    for (int i = 0; i < parts; i++) tot += ld_dev_i(sync + idx + i * kSyncStride);
-    if (tot >= target) return;
-    ++spins;
-    if ((spins & 15) == 0 && ld_dev_i(sync + sync_err()) != 0) return;
-    if (spins > kSpinLimit) {
-      __hip_atomic_store(sync + sync_err(), 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return;
-    }
-    __builtin_amdgcn_s_sleep(8);
-  }
 }
 
 // Launch trace (debugging and measurement): slot (j * 5 + k) * n + s is sublayer k of layer slot j
@@ -225,18 +187,6 @@ __device__ __forceinline__ void ktrace_end(const Ctx& C, int slot) {
   if (C.ktrace != nullptr && threadIdx.x == 0)
     __hip_atomic_fetch_max(C.ktrace + 2 * slot + 1, (unsigned long long)wall_clock64(), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// A KV-cache element with a device-scope store.
-template <typename T>
-__device__ __forceinline__ void st_kv_dev(T* p, float v);
-template <>
-__device__ __forceinline__ void st_kv_dev<float>(float* p, float v) {
-  st_dev(p, v);
-}
-template <>
-__device__ __forceinline__ void st_kv_dev<uint16_t>(uint16_t* p, float v) {
-  __hip_atomic_store(p, f2bf(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ float2 ld_dev2(const float* p) {  // p 8-byte aligned

@@ -221,13 +221,12 @@ __device__ __forceinline__ void rstream_run(const RowFn& rowptr, const DoneFn& d
   }
 }
 
-// Stage src[0, K) into LDS in the xidx layout (COH: device-scope loads, for values written earlier in
-// the same launch; else ordinary loads), zero padded to the block multiple, times gain[k] when a gain
-// is given. Returns the workgroup's sum of squares of src when a
+// Stage src[0, K) into LDS in the xidx layout, zero padded to the block multiple, times gain[k] when a
+// gain is given. Returns the workgroup's sum of squares of src when a
 // gain is given: each thread sums its float4 groups in the same order as the per-sublayer kernels'
 // staging, then the fixed block reduction, so both launch modes compute the same norm bit for bit.
 // Ends with a barrier, so the vector is visible to all waves.
-template <int VE, bool COH>
+template <int VE>
 __device__ __forceinline__ float stage_vec(const float* src, const float* gain, int K, float* lds, float* red) {
   constexpr int BLK = 64 * VE;
   constexpr int RND = 4;
@@ -239,10 +238,7 @@ __device__ __forceinline__ float stage_vec(const float* src, const float* gain, 
     for (int j = 0; j < RND; j++) {
       const int k = (k40 + j * kWG) * 4;
       const bool ok = k < K;  // K is a multiple of 4
-      if (ok && COH) {
-        const float2 lo = ld_dev2(src + k), hi = ld_dev2(src + k + 2);
-        v[j] = make_float4(lo.x, lo.y, hi.x, hi.y);
-      } else if (ok) {
+      if (ok) {
         v[j] = *reinterpret_cast<const float4*>(src + k);
       } else {
         v[j] = make_float4(0.f, 0.f, 0.f, 0.f);

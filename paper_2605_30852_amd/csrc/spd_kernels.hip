@@ -257,12 +257,11 @@ __device__ __forceinline__ void gemv_tile(const WT* const (&wr)[RL], int K, cons
 enum SKind { SG_QKV = 0, SG_OPROJ = 2, SG_GATEUP = 3, SG_DOWN = 4 };
 
 // Workgroup bx of nbx working on one stage's sublayer (gr: the stage's row, Ld: its layer, set: the
-// scratch set). wait_inputs runs after the first weight units are requested and before anything the
-// previous sublayer wrote is read. COH: the inputs were written, and the outputs are read, by other
-// workgroups of the same launch (device-scope loads and stores).
-template <typename WT, int KIND, bool COH, typename WaitFn>
+// scratch set). The first weight units are requested before anything the previous sublayer wrote is
+// read.
+template <typename WT, int KIND>
 __device__ __forceinline__ void sgemv_part(const Ctx& C, const Grp& gr, const LayerDesc& Ld, int set, int bx,
-                                           int nbx, const WaitFn& wait_inputs) {
+                                           int nbx) {
   extern __shared__ __align__(16) float lds[];
   __shared__ float red[4];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -300,20 +299,19 @@ __device__ __forceinline__ void sgemv_part(const Ctx& C, const Grp& gr, const La
     }
     page = C.page_table[pos / C.page];
   }
-  wait_inputs();
   if (KIND == SG_OPROJ || KIND == SG_DOWN) {
     if (lane < count) {
       const int m = 2 * (wv + lane * NW);
-      pv.x = COH ? ld_dev(x + m) : x[m];
-      pv.y = m + 1 < d ? (COH ? ld_dev(x + m + 1) : x[m + 1]) : 0.f;
+      pv.x = x[m];
+      pv.y = m + 1 < d ? x[m + 1] : 0.f;
     }
   }
   float sc = 1.f;
   if (KIND == SG_QKV || KIND == SG_GATEUP) {
-    const float ss = stage_vec<Elt<WT>::VE, COH>(x, KIND == SG_QKV ? Ld.attn_norm : Ld.mlp_norm, d, lds, red);
+    const float ss = stage_vec<Elt<WT>::VE>(x, KIND == SG_QKV ? Ld.attn_norm : Ld.mlp_norm, d, lds, red);
     sc = 1.0f / sqrtf(ss / (float)d + C.eps);
   } else {
-    stage_vec<Elt<WT>::VE, COH>((KIND == SG_OPROJ ? C.b[set].ao : C.b[set].act) + (size_t)gr.brow0 * K,
+    stage_vec<Elt<WT>::VE>((KIND == SG_OPROJ ? C.b[set].ao : C.b[set].act) + (size_t)gr.brow0 * K,
                                 nullptr, K, lds, red);
   }
   float* cap = nullptr;
@@ -334,47 +332,28 @@ __device__ __forceinline__ void sgemv_part(const Ctx& C, const Grp& gr, const La
       }
       if (head < C.hq) {
         float* qo = C.b[set].q + (size_t)gr.brow0 * C.qdim + head * dh;
-        if (COH) {
-          st_dev(qo + j, lo);
-          st_dev(qo + j + half, hi);
-        } else {
-          qo[j] = lo;
-          qo[j + half] = hi;
-        }
+        qo[j] = lo;
+        qo[j + half] = hi;
       } else {
         const int hk = head < C.hq + C.hkv ? head - C.hq : head - C.hq - C.hkv;
         WT* kv = (WT*)Ld.kv;
         const size_t off = (size_t)page * (2 * C.hkv * C.page * dh) + ((size_t)hk * C.page + (pos % C.page)) * dh + j +
                            (head < C.hq + C.hkv ? 0 : (size_t)C.hkv * C.page * dh);
-        if (COH) {
-          st_kv_dev<WT>(kv + off, lo);
-          st_kv_dev<WT>(kv + off + half, hi);
-        } else {
-          st1<WT>(kv, off, lo);
-          st1<WT>(kv, off + half, hi);
-        }
+        st1<WT>(kv, off, lo);
+        st1<WT>(kv, off + half, hi);
       }
     } else if (KIND == SG_GATEUP) {
       const float g = s0 * sc, u = s1 * sc;
       float* ao = C.b[set].act + (size_t)gr.brow0 * C.F + q;
-      if (COH)
-        st_dev(ao, g / (1.0f + expf(-g)) * u);
-      else
-        *ao = g / (1.0f + expf(-g)) * u;
+      *ao = g / (1.0f + expf(-g)) * u;
     } else {
       const int m = 2 * q;
       const float n0 = v.x + s0;
-      if (COH)
-        st_dev(x + m, n0);
-      else
-        x[m] = n0;
+      x[m] = n0;
       if (cap != nullptr) cap[m] = n0;
       if (m + 1 < d) {
         const float n1 = v.y + s1;
-        if (COH)
-          st_dev(x + m + 1, n1);
-        else
-          x[m + 1] = n1;
+        x[m + 1] = n1;
         if (cap != nullptr) cap[m + 1] = n1;
       }
     }
@@ -388,7 +367,7 @@ __global__ __launch_bounds__(kWG) void k_sgemv(Ctx C, Rows R) {
   if (!gr.active) return;
   const int ts = ktrace_slot(C, R.slot, KIND, gr.s);
   ktrace_start(C, ts, blockIdx.x == 0);
-  sgemv_part<WT, KIND, false>(C, gr, R.ld[gr.s], R.set, blockIdx.x, gridDim.x, [] {});  // stage launches carry their layers
+  sgemv_part<WT, KIND>(C, gr, R.ld[gr.s], R.set, blockIdx.x, gridDim.x);  // stage launches carry their layers
   ktrace_end(C, ts);
 }
 
@@ -462,12 +441,12 @@ __global__ __launch_bounds__(kWG) void k_rgemv(Ctx C, Rows R, int nrp) {
       sc[r] = 1.f;
       if (r < nr) {
         if (KIND == SG_QKV || KIND == SG_GATEUP) {
-          const float ss = stage_vec<Elt<WT>::VE, false>(gr.x + (size_t)(r0 + r) * gr.xstride,
+          const float ss = stage_vec<Elt<WT>::VE>(gr.x + (size_t)(r0 + r) * gr.xstride,
                                                           KIND == SG_QKV ? Ld.attn_norm : Ld.mlp_norm, d,
                                                           lds + (size_t)r * ldsK, red);
           sc[r] = 1.0f / sqrtf(ss / (float)d + C.eps);
         } else {
-          stage_vec<Elt<WT>::VE, false>((KIND == SG_OPROJ ? C.b[R.set].ao : C.b[R.set].act) +
+          stage_vec<Elt<WT>::VE>((KIND == SG_OPROJ ? C.b[R.set].ao : C.b[R.set].act) +
                                             (size_t)(gr.brow0 + r0 + r) * K,
                                         nullptr, K, lds + (size_t)r * ldsK, red);
         }
@@ -650,7 +629,7 @@ __device__ __forceinline__ void head_body(const Ctx& C, int src, int row, int lc
   float scl[NV];
 #pragma unroll
   for (int v = 0; v < NV; v++) {
-    const float ss = stage_vec<Elt<WT>::VE, false>(xr[v], gn[v], d, lds + (size_t)v * ldsK, red);
+    const float ss = stage_vec<Elt<WT>::VE>(xr[v], gn[v], d, lds + (size_t)v * ldsK, red);
     scl[v] = 1.0f / sqrtf(ss / (float)d + C.eps);
   }
   float bv[NV];
@@ -767,9 +746,9 @@ __device__ __forceinline__ void attn_part(const Ctx& C, int s, int slot, const K
   float* out = B.ao + (size_t)s * C.qdim + g * C.G * DH;
   float* rec = B.part + (size_t)cidx * C.max_splits * RS;
   if constexpr (GP == 0)
-    attn_split<KVT, DH, false>(C, kv, q, out, rec, B.cnt + cidx, g, split, nsplit, k0, k1, pos0, page0, lds);
+    attn_split<KVT, DH>(C, kv, q, out, rec, B.cnt + cidx, g, split, nsplit, k0, k1, pos0, page0, lds);
   else
-    attn_split_g<KVT, DH, false, GP>(C, kv, q, out, rec, B.cnt + cidx, g, split, nsplit, k0, k1, pos0, page0, lds);
+    attn_split_g<KVT, DH, GP>(C, kv, q, out, rec, B.cnt + cidx, g, split, nsplit, k0, k1, pos0, page0, lds);
 }
 
 // The stage launch is instantiated per head-slot count, so its registers are those of one variant.
@@ -807,7 +786,7 @@ __global__ __launch_bounds__(kWG) void k_attn_rows(Ctx C, Rows R, int nrg) {
   const int cidx = z * C.hkv + g;
   constexpr int RS = kAttnMaxQ * (DH + 2);
   const size_t row = (size_t)(gr.brow0 + z) * C.qdim + g * C.G * DH;
-  attn_split_g<KVT, DH, false, GP>(C, (const KVT*)C.lay[gr.layer].kv, B.q + row, B.ao + row,
+  attn_split_g<KVT, DH, GP>(C, (const KVT*)C.lay[gr.layer].kv, B.q + row, B.ao + row,
                                    B.part + (size_t)cidx * C.max_splits * RS, B.cnt + cidx, g, split, nsplit, k0,
                                    k1, pos0, page0, lds);
 }
@@ -854,142 +833,6 @@ void launch_ktrace_reset(const Ctx& c, int nslots, void* stream) {
   hipLaunchKernelGGL(k_ktrace_reset, dim3((nslots + kWG - 1) / kWG), dim3(kWG), 0, (hipStream_t)stream, c, nslots);
 }
 
-// ---------------------------------------------------------------------------- mixed launches
-// One launch of the skewed schedule: up to n independent parts, part i being sublayer kind of
-// stage s in layer slot `slot`, on workgroups [wg0, wg0 + nwg). Parts never depend on each other
-// (different stages), so a latency-bound part (attention) runs under the weight streaming of the
-// others, and every launch streams several stages' worth of weights.
-template <typename WT, int DH>
-__global__ __launch_bounds__(kWG) void k_mix(Ctx C, MixLaunch M) {
-  int i = 0;
-  while (i + 1 < M.nparts && (int)blockIdx.x >= M.p[i + 1].wg0) i++;
-  const MixPart& P = M.p[i];
-  const int b = blockIdx.x - P.wg0;
-  if (P.kind == SK_ATTN) {
-    attn_part<WT, DH>(C, P.stage, P.slot, (const WT*)P.ld.kv, 0, b / C.max_splits, b % C.max_splits);
-    return;
-  }
-  Rows R;
-  R.kind = 0;
-  R.slot = P.slot;
-  R.stage0 = P.stage;
-  R.nst = 1;
-  const Grp gr = resolve(C, R, 0);
-  if (!gr.active) return;
-  switch (P.kind) {
-    case SK_QKV: sgemv_part<WT, SG_QKV, false>(C, gr, P.ld, 0, b, P.nwg, [] {}); break;
-    case SK_OPROJ: sgemv_part<WT, SG_OPROJ, false>(C, gr, P.ld, 0, b, P.nwg, [] {}); break;
-    case SK_GATEUP: sgemv_part<WT, SG_GATEUP, false>(C, gr, P.ld, 0, b, P.nwg, [] {}); break;
-    default: sgemv_part<WT, SG_DOWN, false>(C, gr, P.ld, 0, b, P.nwg, [] {}); break;
-  }
-}
-
-// ----------------------------------------------------------------- grouped persistent step kernel
-// Every layer slot of every active stage in one launch, each active stage on its own group of
-// workgroups (workgroup b works for stage b mod a). A group walks its stage's sublayers in order; a
-// workgroup streams a contiguous share of each sublayer's weight rows (or of its attention splits)
-// and then counts itself on the stage's counter. Before it reads anything the previous sublayer
-// wrote, it waits until every workgroup of its group has counted that sublayer, but its first
-// weight units for the sublayer are requested before that wait, so the stream goes on while it
-// waits. Stages never wait for each other, so one stage's attention and waits overlap the other
-// stages' weight streaming. Values handed between workgroups use device-scope stores and loads.
-//
-// The per-stage waits need every workgroup of the launch to be resident at once: the host sizes the
-// grid to what the GPU holds, and every wait is bounded (a timeout raises the launch's flag, which
-// the host reports, and lets the grid drain).
-// One attention tile of the grouped kernel, kept out of line: it runs a few times per workgroup and
-// step, and inlining it would add its registers to the weight-streaming sublayers'.
-template <typename WT, int DH>
-__device__ __noinline__ void pstep_attn_tile(const Ctx& C, const void* kv, int s, int g, int split, int nsplit,
-                                             int pos0) {
-  extern __shared__ __align__(16) float lds[];
-  constexpr int RS = kAttnMaxQ * (DH + 2);
-  const int k0 = split * C.chunk, k1 = min(pos0 + 1, k0 + C.chunk);
-  const int page0 = C.page_table[min((k0 + (int)threadIdx.x / kAttnTPK) / C.page, C.max_pages - 1)];
-  const int cidx = s * C.hkv + g;
-  const BufSet& B = C.b[0];
-  attn_split<WT, DH, true>(C, (const WT*)kv, B.q + (size_t)s * C.qdim + g * C.G * DH,
-                           B.ao + (size_t)s * C.qdim + g * C.G * DH, B.part + (size_t)cidx * C.max_splits * RS,
-                           B.cnt + cidx, g, split, nsplit, k0, k1, pos0, page0, lds);
-}
-
-// The weight-streaming sublayers of the grouped kernel, each out of line for the same reason.
-template <typename WT, int KIND>
-__device__ __noinline__ void pstep_gemv(const Ctx& C, const Grp& gr, const LayerDesc& Ld, int bx, int nb, int* sync,
-                                        int bar, int target, unsigned long long* tr) {
-  sgemv_part<WT, KIND, true>(C, gr, Ld, 0, bx, nb, [&] {
-    if (tr != nullptr && threadIdx.x == 0) tr[0] = (unsigned long long)wall_clock64();
-    if (threadIdx.x == 0 && target > 0) wait_count_sum(sync, bar, kBarParts, target);
-    __syncthreads();
-    if (tr != nullptr && threadIdx.x == 0) tr[1] = (unsigned long long)wall_clock64();
-  });
-}
-
-template <typename WT, int DH>
-__global__ __launch_bounds__(kWG, 3) void k_pstep(const Ctx* __restrict__ Cp) {
-  extern __shared__ __align__(16) float lds[];
-  const Ctx& C = *Cp;
-  const int a = C.st->a, c = C.st->c;  // pre-step state; only the verify kernel changes it
-  if (a <= 0) return;
-  const int s = blockIdx.x % a, bx = blockIdx.x / a;
-  const int nb = ((int)gridDim.x - 1 - s) / a + 1;  // workgroups of this stage's group
-  int* sync = C.plan.sync;
-  const int bar = sync_bar(s);
-  int phase = 0;  // sublayers this group has finished
-  // tracing: per workgroup and sublayer, wall-clock stamps at wait start, wait end and sublayer end
-  auto trp = [&](int ph) -> unsigned long long* {
-    const size_t at = ((size_t)blockIdx.x * 5 * C.J + ph) * 3;
-    return C.plan.trace != nullptr && at + 3 <= (size_t)C.plan.ntrace ? C.plan.trace + at : nullptr;
-  };
-  auto arrive = [&]() {
-    wait_own_stores();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      __hip_atomic_fetch_add(sync + bar + (bx % kBarParts) * kSyncStride, 1, __ATOMIC_RELAXED,
-                             __HIP_MEMORY_SCOPE_AGENT);
-      unsigned long long* t = trp(phase);
-      if (t != nullptr) t[2] = (unsigned long long)wall_clock64();
-    }
-    phase++;
-  };
-  auto wait_prev = [&]() {
-    unsigned long long* t = trp(phase);
-    if (t != nullptr && threadIdx.x == 0) t[0] = (unsigned long long)wall_clock64();
-    if (threadIdx.x == 0 && phase > 0) wait_count_sum(sync, bar, kBarParts, phase * nb);
-    __syncthreads();
-    if (t != nullptr && threadIdx.x == 0) t[1] = (unsigned long long)wall_clock64();
-  };
-  Rows R;
-  R.kind = 0;
-  R.stage0 = s;
-  R.nst = 1;
-  for (int j = 0; j < C.J; j++) {
-    R.slot = j;
-    const Grp gr = resolve(C, R, 0);
-    if (!gr.active) break;  // a shorter stage has no layer in this slot
-    const LayerDesc& Ld = C.lay[gr.layer];
-    pstep_gemv<WT, SG_QKV>(C, gr, Ld, bx, nb, sync, bar, phase * nb, trp(phase));
-    arrive();
-    {  // attention: the stage's (KV head, split) tiles, shared out over the group
-      const int pos0 = gr.pos0;
-      const int nsplit = (pos0 + C.chunk) / C.chunk;
-      const int ntile = C.hkv * nsplit;
-      wait_prev();
-      for (int t = bx; t < ntile; t += nb) {
-        pstep_attn_tile<WT, DH>(C, Ld.kv, s, t / nsplit, t % nsplit, nsplit, pos0);
-        __syncthreads();  // LDS free for the next tile
-      }
-      arrive();
-    }
-    pstep_gemv<WT, SG_OPROJ>(C, gr, Ld, bx, nb, sync, bar, phase * nb, trp(phase));
-    arrive();
-    pstep_gemv<WT, SG_GATEUP>(C, gr, Ld, bx, nb, sync, bar, phase * nb, trp(phase));
-    arrive();
-    pstep_gemv<WT, SG_DOWN>(C, gr, Ld, bx, nb, sync, bar, phase * nb, trp(phase));
-    arrive();
-  }
-}
-
 // ------------------------------------------------------------------------- embedding / state
 template <typename WT>
 __device__ __forceinline__ void push_embedding(const Ctx& C, int tok, float* dst0, float* dst1) {
@@ -1009,24 +852,21 @@ __global__ __launch_bounds__(kWG) void k_embed_rows(Ctx C, int t0, int nrows) {
   push_embedding<WT>(C, tok, C.pf_x + (size_t)i * C.d, C.pf_anch + (size_t)i * C.n * C.d);
 }
 
-// Zero what the next step's kernels count from: both argmax keys and the step kernel's ticket,
-// timeout flag and per-(phase, stage) counters. Plain stores: the next launch sees them.
+// Zero what the next step's kernels count from: both argmax keys. Plain stores: the next launch
+// sees them.
 __device__ __forceinline__ void reset_step_sync(const Ctx& C) {
   if (threadIdx.x < 2) *C.b[threadIdx.x].hkey = 0ull;
-  if (C.plan.sync != nullptr)
-    for (int i = threadIdx.x; i < C.plan.nsync; i += kWG) C.plan.sync[i] = 0;
 }
 
 // The state update of a step once the target's token y_all (-1 if nothing exits) and the PDM's own
 // draft pd_all are known; every thread has read what reset_step_sync clears.
 template <typename WT>
-__device__ __forceinline__ void verify_update(const Ctx& C, int y_all, int pd_all, int step_err, int forced_override,
+__device__ __forceinline__ void verify_update(const Ctx& C, int y_all, int pd_all, int forced_override,
                                               int auto_rb) {
   __shared__ int s_tok, s_pos;
   DevState* st = C.st;
   reset_step_sync(C);
   if (threadIdx.x == 0) {
-    if (step_err) st->err = 1;
     const int c = st->c, a = st->a, n = C.n;
     const int pd = pd_all;
     st->pdm_draft = pd;
@@ -1041,6 +881,7 @@ __device__ __forceinline__ void verify_update(const Ctx& C, int y_all, int pd_al
     r.draft = draft;
     r.pdm_draft = pd;
     r.exited_pos = -1;
+    r.exited_token = -1;
     r.verified_pos = -1;
     r.verified_token = -1;
     int ptok = -1, ppos = -1;
@@ -1049,6 +890,7 @@ __device__ __forceinline__ void verify_update(const Ctx& C, int y_all, int pd_al
       const int succ = n >= 2 ? C.tok[c + 1] : draft;
       r.target_argmax = y;
       r.exited_pos = c;
+      r.exited_token = C.tok[c];
       r.verified_pos = c + 1;
       r.verified_token = y;
       st->c = c + 1;
@@ -1099,9 +941,8 @@ __device__ __forceinline__ void verify_body(const Ctx& C, int forced_override, i
   DevState* st = C.st;
   const int y_all = (st->a == C.n) ? take_head_dev(C.b[0], C.V) : -1;
   const int pd_all = pdm_token(C, take_head_dev(C.b[1], pdm_rows(C)));
-  const int step_err = C.plan.sync != nullptr ? C.plan.sync[sync_err()] : 0;
-  __syncthreads();  // every thread has read the argmax keys and the timeout flag
-  verify_update<WT>(C, y_all, pd_all, step_err, forced_override, auto_rb);
+  __syncthreads();  // every thread has read the argmax keys
+  verify_update<WT>(C, y_all, pd_all, forced_override, auto_rb);
 }
 
 
@@ -1145,7 +986,6 @@ template <typename WT>
 __device__ __forceinline__ void sampled_verify(const Ctx& C, SelLds& S, int kq, int kp, int forced_override,
                                                int auto_rb) {
   DevState* st = C.st;
-  const int step_err = C.plan.sync != nullptr ? C.plan.sync[sync_err()] : 0;
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
     const int c = st->c, a = st->a, n = C.n;
@@ -1232,7 +1072,7 @@ __device__ __forceinline__ void sampled_verify(const Ctx& C, SelLds& S, int kq, 
   __syncthreads();
   const int y = S.out[0], pd = S.out[1];
   __syncthreads();
-  verify_update<WT>(C, y, pd, step_err, forced_override, auto_rb);
+  verify_update<WT>(C, y, pd, forced_override, auto_rb);
 }
 
 // The sampled LM head: head_body with the logits kept, then (last workgroup, as in k_head_verify)
@@ -1469,43 +1309,6 @@ void Launch<WT>::attn(const Ctx& c, const Rows& r, void* s) {
     else
       launch_timed((k_attn_stage<WT, 64, 8>), grid, dim3(kWG), attn_split_lds<WT, 64>(), S(s), c, r);
   }
-}
-
-template <typename WT>
-void Launch<WT>::mix(const Ctx& c, const MixLaunch& m, int nwg, void* s) {
-  constexpr int BLK = 64 * Elt<WT>::VE;
-  int kmax = std::max(std::max(c.d, c.qdim), c.F);
-  kmax = (kmax + BLK - 1) / BLK * BLK;
-  size_t shm = (size_t)kmax * sizeof(float);
-  if (c.dh == 128) {
-    shm = std::max(shm, attn_split_lds<WT, 128>());
-    launch_timed((k_mix<WT, 128>), dim3(nwg), dim3(kWG), shm, S(s), c, m);
-  } else {
-    shm = std::max(shm, attn_split_lds<WT, 64>());
-    launch_timed((k_mix<WT, 64>), dim3(nwg), dim3(kWG), shm, S(s), c, m);
-  }
-}
-
-template <typename WT>
-size_t Launch<WT>::pstep_lds(const Ctx& c) {
-  constexpr int BLK = 64 * Elt<WT>::VE;
-  int kmax = std::max(std::max(c.d, c.qdim), c.F);
-  kmax = (kmax + BLK - 1) / BLK * BLK;
-  const size_t attn = c.dh == 128 ? attn_split_lds<WT, 128>() : attn_split_lds<WT, 64>();
-  return std::max((size_t)kmax * sizeof(float), attn);
-}
-
-template <typename WT>
-const void* Launch<WT>::pstep_fn(const Ctx& c) {
-  return c.dh == 128 ? (const void*)k_pstep<WT, 128> : (const void*)k_pstep<WT, 64>;
-}
-
-template <typename WT>
-void Launch<WT>::pstep(const Ctx& c, const Ctx* dev_ctx, int grid, void* s) {
-  if (c.dh == 128)
-    launch_timed((k_pstep<WT, 128>), dim3(grid), dim3(kWG), pstep_lds(c), S(s), dev_ctx);
-  else
-    launch_timed((k_pstep<WT, 64>), dim3(grid), dim3(kWG), pstep_lds(c), S(s), dev_ctx);
 }
 
 template <typename WT>

@@ -178,8 +178,8 @@ class Engine:
     def spd_set_graph(self, on: bool) -> None:
         B.spd_set_graph(self.h, on)
 
-    def spd_set_step_kernel(self, mode: int, grid: int = 0, skew: int = -1) -> None:
-        B.spd_set_step_kernel(self.h, mode, grid, skew)
+    def spd_set_step_kernel(self, mode: int, grid: int = 0, groups: int = -1) -> None:
+        B.spd_set_step_kernel(self.h, mode, grid, groups)
 
     def spd_set_pdm_placement(self, place: int) -> None:
         B.spd_set_pdm_placement(self.h, place)

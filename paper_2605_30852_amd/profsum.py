@@ -3,14 +3,16 @@
     python -m paper_2605_30852_amd.profsum stats KERNEL_STATS.csv [--top N]
     python -m paper_2605_30852_amd.profsum trace KERNEL_TRACE.csv --kernel NAME [--grid-y Y]
     python -m paper_2605_30852_amd.profsum traffic FETCH.csv WRITE.csv --kernel NAME [--grid-y Y]
-        [--algo-bytes B] [--source FILE]
+        [--fetch-trace KT.csv --write-trace KT.csv] [--algo-bytes B] [--source FILE]
 
 `stats` prints the per-kernel table; `trace` the duration of the dispatches of one kernel (a
 substring of its name, optionally only those whose grid has Y workgroups in y, e.g. the two-stage
 group launches); `traffic` the HBM bytes per dispatch of that kernel from a FETCH_SIZE run and a
 WRITE_SIZE run, each scaled by what the same counter reads for the largest device copy in the run
-(a 1 GiB copy reads and writes 2^30 bytes), as key=value lines. Pure text processing: it reads the
-CSV files only."""
+(a 1 GiB copy reads and writes 2^30 bytes), as key=value lines. The counter files record only the
+total grid size, so a grid-y selection takes the dispatch ids of the matching dispatches from a
+kernel trace of the same run (rocprofv3 --pmc ... --kernel-trace writes both). Pure text
+processing: it reads the CSV files only."""
 from __future__ import annotations
 
 import argparse
@@ -57,41 +59,44 @@ def trace(path, kernel, grid_y):
             f"median_us={statistics.median(d):.2f}\nmin_us={min(d):.2f}\nmax_us={max(d):.2f}")
 
 
-def _counter(path, kernel, grid_y):
-    """Values of the kernel's dispatches in dispatch order (only grid y = grid_y when the file records
-    grid dimensions), whether it does, and the largest device copy's value."""
+def _dispatch_ids(trace_path, kernel, grid_y):
+    """Dispatch ids of the kernel's dispatches with grid_y workgroups in y, from a kernel trace."""
+    return {r["Dispatch_Id"] for r in _rows(trace_path) if _match(r, kernel, grid_y)}
+
+
+def _counter(path, kernel, grid_y, ids=None):
+    """Values of the kernel's dispatches in dispatch order and the largest device copy's value. With
+    ids (dispatch ids from a kernel trace of the same run) only those dispatches count; otherwise the
+    grid-y selection needs grid dimensions in the file itself (None if it has none)."""
     vals, copies, has_y = [], [], False
     for r in _rows(path):
         v = float(r["Counter_Value"])
         has_y = has_y or _grid_y(r) is not None
-        if _match(r, kernel, grid_y if _grid_y(r) is not None else None):
+        if ids is not None:
+            if kernel in r.get("Kernel_Name", "") and r["Dispatch_Id"] in ids:
+                vals.append(v)
+        elif _match(r, kernel, grid_y if _grid_y(r) is not None else None):
             vals.append(v)
         if "copyBuffer" in r.get("Kernel_Name", ""):
             copies.append(v)
-    return vals, has_y, (max(copies) if copies else None)
+    if grid_y is not None and ids is None and not has_y:
+        return None, (max(copies) if copies else None)
+    return vals, (max(copies) if copies else None)
 
 
-def traffic(fetch, write, kernel, grid_y, algo, source):
-    fv, has_y, fc = _counter(fetch, kernel, grid_y)
-    wv, _, wc = _counter(write, kernel, grid_y)
+def traffic(fetch, write, kernel, grid_y, algo, source, fetch_trace=None, write_trace=None):
+    fids = _dispatch_ids(fetch_trace, kernel, grid_y) if fetch_trace else None
+    wids = _dispatch_ids(write_trace, kernel, grid_y) if write_trace else None
+    fv, fc = _counter(fetch, kernel, grid_y, fids)
+    wv, wc = _counter(write, kernel, grid_y, wids)
+    if fv is None or wv is None:
+        return "incomplete: the counter files hold no grid shape; give the kernel traces of the same runs"
     if not fv or not wv or not fc or not wc:
         return "incomplete: " + repr((len(fv), len(wv), fc, wc))
     sf, sw = GIB_KIB / fc, GIB_KIB / wc
-    how = f"grid y = {grid_y}"
-    if grid_y is not None and not has_y:
-        # no grid shape in the file: launches covering other stage counts read other amounts, so keep
-        # the dispatches whose fetch is within 1/4 of the algorithmic bytes (else the largest-value
-        # cluster), and the same dispatch ordinals of the write run (both runs issue the same sequence)
-        if algo:
-            keep = [i for i, v in enumerate(fv) if 0.75 * algo <= v * sf * 1024.0 <= 1.25 * algo]
-            how = "fetch within 1/4 of the algorithmic bytes"
-        else:
-            top = max(fv)
-            keep = [i for i, v in enumerate(fv) if v >= 0.75 * top]
-            how = "largest-value cluster (>= 3/4 of the largest)"
-        if len(wv) != len(fv) or not keep:
-            return "incomplete: " + repr((len(fv), len(wv), len(keep)))
-        fv, wv = [fv[i] for i in keep], [wv[i] for i in keep]
+    how = "all dispatches" if grid_y is None else (
+        f"grid y = {grid_y}, by dispatch id from the kernel trace of each counter run" if fids is not None
+        else f"grid y = {grid_y}")
     fk, wk = statistics.median(fv), statistics.median(wv)
     hbm = (fk * sf + wk * sw) * 1024.0
     lines = [f"kernel={kernel}", f"selection={how}", f"dispatches_fetch={len(fv)}", f"dispatches_write={len(wv)}",
@@ -121,6 +126,8 @@ def main(argv=None):
     c.add_argument("write")
     c.add_argument("--kernel", required=True)
     c.add_argument("--grid-y", type=int, default=None)
+    c.add_argument("--fetch-trace", default=None, help="kernel trace CSV of the FETCH_SIZE run")
+    c.add_argument("--write-trace", default=None, help="kernel trace CSV of the WRITE_SIZE run")
     c.add_argument("--algo-bytes", type=float, default=None)
     c.add_argument("--source", default=None)
     args = ap.parse_args(argv)
@@ -129,7 +136,8 @@ def main(argv=None):
     elif args.cmd == "trace":
         print(trace(args.csv, args.kernel, args.grid_y))
     else:
-        print(traffic(args.fetch, args.write, args.kernel, args.grid_y, args.algo_bytes, args.source))
+        print(traffic(args.fetch, args.write, args.kernel, args.grid_y, args.algo_bytes, args.source,
+                      args.fetch_trace, args.write_trace))
     return 0
 
 

@@ -104,6 +104,11 @@ B9_LONG = B9.with_(name="9b-long", n_stages=8, pdm_layers=2)
 # A mid-size bf16 model for parity: several GEMV/attention tiles per launch and ragged tails
 # (ffn 1000 and vocab 3001 are not multiples of any tile height).
 MID = ModelShape("mid", 6, 384, 8, 2, 64, 1000, 3001, "bf16", n_stages=3, pdm_layers=1)
+# A bf16 model with the full-size head shape (heads of 128, 4 query heads per KV head) for parity at
+# long contexts and wide pipelines: 10 layers split into 5, 6 or 8 ragged stages, a two-layer draft
+# module whose feature projection reads n * 1024 anchors, and an FFN of 5120 (eight rows of its down
+# projection input do not fit one workgroup's LDS at once).
+WIDE = ModelShape("wide", 10, 1024, 8, 2, 128, 5120, 4096, "bf16", n_stages=8, pdm_layers=2)
 
 WORKLOADS = {
     "tiny": dict(shape=TINY, prompt_len=64, steps=32, p_accept=None),

@@ -2,7 +2,8 @@
 
 A full-pipeline step (a = n) streams every layer's weights once, reads each stage token's keys, writes
 one K/V row per layer, makes one two-row pass over the LM head and runs the PDM over n rows; a step
-with a < n in-flight tokens streams only stages 0..a-1. These are checked against sums written out
+with a < n in-flight tokens streams only stages 0..a-1. The PDM's rows share one cache, so its keys
+and values are read once per step (through the newest row's position), not once per row. These are checked against sums written out
 here from the shapes, independently of how bench.py arranges them."""
 import pytest
 
@@ -41,3 +42,16 @@ def test_steady_step_bytes_at_the_headline_size():
     total = bench.step_bytes_active(sh, 4, 1, 2300, 4, esz)
     assert 8.6e9 < total < 8.75e9
     assert abs(sh.n_layers * _layer(sh, esz) - 7.267e9) < 5e6
+
+
+@pytest.mark.parametrize("n,ls,c", [(4, 1, 2048), (8, 2, 32768)])
+def test_pdm_kv_is_read_once_per_step(n, ls, c):
+    """The a = n rows at positions c..c+n-1 all read one shared cache: keys and values 0..c+n-1 of each
+    PDM layer once, plus the n rows written; the PDM's other bytes are its weights."""
+    sh, esz = synth.B9, 2
+    kv_tok = 2 * sh.kv_dim * esz
+    _, pdm = bench.step_bytes(sh, n, ls, c, esz, pdm_head=False)
+    weights = sh.d_model * n * sh.d_model * esz + ls * _layer(sh, esz)
+    assert pdm - weights == ls * (c + n) * kv_tok + ls * n * kv_tok
+    # a per-row count would have read sum_i (c + i + 1) keys per layer instead
+    assert pdm - weights < ls * sum(c + i + 1 for i in range(n)) * kv_tok

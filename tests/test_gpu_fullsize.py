@@ -7,7 +7,12 @@ with stages of 4-5 layers, two-layer draft module) runs with a short prompt as w
 
 The prompt is short so that the float64 oracle can recompute every sampled output one by one: the GPU's
 in-flight residual streams and PDM anchors after each step, and the exit token's full-vocabulary logits,
-against the oracle's cache-free forward pass over the same tokens. Drafts are forced to the GPU's own
+against the oracle's cache-free forward pass over the same tokens; and the draft module's rows and
+logits of every step against a cache-free forward of its layers over the feature sequence of that step
+(Eq. input-seq: every committed position with all n anchors, the in-flight token at depth k with
+anchors 0..min(k, n-1), projected by W_in as in Eq. agg-main). At these sizes the feature projection
+reads n * d = 10240 (4B) and 32768 (9B, n = 8) anchors, more than one LDS chunk, and the n = 8 draft
+module's 8 rows of the 12288-wide down projection input take several LDS passes through its two layers. Drafts are forced to the GPU's own
 plain greedy decode (n = 1) so that every step after the fill accepts and a token exits each step.
 Tolerances: hidden states rel L2 <= 2e-2, logits max abs <= 5e-2, top-1 identical unless the oracle's
 top-2 margin is below 1e-2."""
@@ -56,12 +61,14 @@ def test_fullsize_step_parity(which):
     eng.spd_set_debug(True)
     assert eng.spd_prefill(prompt) == first
     eng.spd_set_forced_drafts(ref, P)
-    snaps = []
+    snaps, pdm_snaps = [], []
     for i in range(steps):
+        c0, a0, _, _ = eng.state()
         r = eng.spd_run_steps(1, want_log=True)[0]
         c, a, _, _ = eng.state()
         snaps.append((r, c, a, eng.resid().copy(), eng.anchors().copy(),
                       eng.exit_logits().copy() if r["decision"] != 0 else None))
+        pdm_snaps.append((c0, a0, eng.pdm_hidden()[:a0].copy(), eng.pdm_logits().copy(), r["pdm_draft"]))
     eng.close()
     del W
     torch.cuda.empty_cache()
@@ -98,5 +105,31 @@ def test_fullsize_step_parity(which):
             if r["target_argmax"] != om.argmax_first(lo):
                 assert margin(lo) < TIE_MARGIN, f"step {i}: target argmax differs"
                 break
-    _say(f"[fullsize {which}] worst hidden rel L2 {worst_h:.2e}, worst logit abs {worst_l:.2e}, {exits} exits")
-    assert exits >= 4
+    # the draft module: a cache-free forward of its layers over each step's feature sequence
+    d = sh.d_model
+    w_in = model.w("pdm.in")
+    worst_ph, worst_pl, pdm_checked = 0.0, 0.0, 0
+    for i, (c0, a0, ph, pl, pdraft) in enumerate(pdm_snaps):
+        T = c0 + a0
+        G = np.zeros((T, d))
+        for q in range(T):
+            k = n if q < c0 else a0 - 1 - (q - c0)
+            z = np.zeros(n * d)
+            for j in range(min(k, n - 1) + 1):
+                z[j * d:(j + 1) * d] = full[beta[j]][q]
+            G[q] = w_in @ z
+        Hp = om.forward_rows(model, G, "pdm.layer", sh.pdm_layers, layers_out=[sh.pdm_layers])[sh.pdm_layers]
+        for r_ in range(a0):
+            e = rel_l2(ph[r_], Hp[c0 + r_])
+            worst_ph = max(worst_ph, e)
+            assert e <= REL_HIDDEN, f"step {i}: PDM row {c0 + r_} rel L2 {e:.3e}"
+        lo = model.w("lm_head") @ om.rms_norm(Hp[T - 1], model.w("pdm.norm"), sh.rms_eps)
+        e = float(np.max(np.abs(pl - lo)))
+        worst_pl = max(worst_pl, e)
+        assert e <= ABS_LOGIT, f"step {i}: PDM logits max abs {e:.3e}"
+        if pdraft != om.argmax_first(lo):
+            assert margin(lo) < TIE_MARGIN, f"step {i}: PDM draft {pdraft} != {om.argmax_first(lo)}"
+        pdm_checked += 1
+    _say(f"[fullsize {which}] worst hidden rel L2 {worst_h:.2e}, worst logit abs {worst_l:.2e}, {exits} exits; "
+         f"PDM rows rel L2 {worst_ph:.2e}, PDM logits abs {worst_pl:.2e} over {pdm_checked} steps")
+    assert exits >= 4 and pdm_checked == steps

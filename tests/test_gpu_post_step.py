@@ -1,4 +1,4 @@
-"""GPU parity of the post-step PDM schedule (the ablation of Section 4.4) through the C ABI.
+"""GPU parity of the post-step PDM schedule (the ablation of Section 4.5) through the C ABI.
 
 The PDM then runs after the step's stage compute and reads every in-flight token one stage deeper.
 Lockstep against the oracle's post-step schedule (PDM rows, PDM logits, drafts, exit logits and
@@ -55,7 +55,7 @@ def test_tiny_post_step_lockstep(tiny_w, n, forced):
     eng = _engine(tiny_w, n)
     w = run_lockstep(eng, model, prompt, 20, draft_for=draft_for, schedule="post")
     eng.close()
-    assert w["steps"] >= 10 or w["near_tie"]
+    assert w["steps"] == 20, w
     assert w["hidden"] < 1e-4 and w["pdm_hidden"] < 1e-4  # fp32 weights and KV
 
 
@@ -68,7 +68,7 @@ def test_mid_bf16_post_step_lockstep(mid_w, fused):
     eng = _engine(mid_w, 3, fused_head=fused)
     w = run_lockstep(eng, model, prompt, 14, schedule="post")
     eng.close()
-    assert w["steps"] >= 8 or w["near_tie"]
+    assert w["steps"] == 14, w
 
 
 def test_n1_post_step_bit_identical_to_pre_step(mid_w):

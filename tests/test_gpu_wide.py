@@ -1,0 +1,125 @@
+"""GPU parity at head_dim 128 with many key splits, the draft module at full width with two layers, and
+wide pipelines, against the float64 oracle step by step, and bit-exact against the GPU's own greedy
+decoding.
+
+Shape (synth.WIDE): 10 layers, d 1024, 8/2 heads of 128, FFN 5120, vocabulary 4096, bf16 weights and
+KV, a two-layer draft module. It exercises what the small parity shapes do not reach:
+  * decode attention over 2048 keys in 128-key splits (17 splits: the benchmark's split size at that
+    context), in 512-key splits (8 rounds per split, like the 32K-token benchmark's long splits) and
+    over 2000 keys in 32-key splits (63 splits: the split merge runs more than one batch of 32), for
+    the stage launches and for the draft module's row attention;
+  * the draft module at n = 8: its feature projection reads 8 * 1024 anchors (several LDS chunks)
+    and its 8 rows do not fit one LDS pass of the 5120-wide down projection input;
+  * n = 5, 6 and 8 over 10 layers (ragged stages, two stage groups), with Bernoulli rejections,
+    rollback, KV truncation and refill.
+The oracle's prefill is its batched causal forward over the prompt (pinned against the token-by-token
+prefill on the CPU). Tolerances: hidden states rel L2 <= 2e-2, logits max abs <= 5e-2, top-1 identical
+unless the oracle's top-2 margin is below 1e-2 (the runs are then re-synchronised and go on)."""
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import model as om
+from oracle import spd as osp
+from tests.lockstep import forced_table, run_lockstep
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+SEED = 13
+SH = synth.WIDE
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def wide_w():
+    from paper_2605_30852_amd.engine import DeviceWeights
+    return DeviceWeights(SH, SEED, threads=16)
+
+
+@pytest.fixture(scope="module")
+def model():
+    return om.Model(SH, SEED)
+
+
+def _oracle_greedy(model, prompt, count):
+    """Plain greedy decoding through the oracle (n = 1 steps after its batched prefill)."""
+    o = osp.SPDOracle(model, n=1)
+    toks = [o.prefill(prompt, batched=True)]
+    while len(toks) < count:
+        toks.append(o.step().verified_token)
+    return toks
+
+
+@pytest.mark.parametrize("n,P,chunk,p,steps", [
+    (8, 2048, 128, 0.6, 24),    # 17 splits of 128 keys, full-width two-layer PDM, ragged n = 8, rejections
+    (4, 2048, 512, None, 16),   # natural drafts; 5 splits of 512 keys (8 rounds each, as at 32K tokens)
+    (6, 2000, 32, 0.7, 20),     # 63 splits of 32 keys: two merge batches, waves with no key in a round
+    (5, 300, 0, 0.7, 20),       # n = 5, the default split size
+])
+def test_wide_lockstep(wide_w, model, n, P, chunk, p, steps):
+    from paper_2605_30852_amd.engine import Engine
+    _say(f"[wide lockstep n={n} prompt={P} chunk={chunk} p={p}]")
+    prompt = synth.prompt(SH, SEED, P)
+    draft_for = None
+    if p is not None:
+        ref = _oracle_greedy(model, prompt, steps + 2)
+        mask = synth.accept_mask(p, SEED + n, P + steps + 64)
+        tab = forced_table(ref, mask, P, SH.vocab)
+        draft_for = tab.get
+    max_tokens = P + steps + n + 16
+    eng = Engine(wide_w, max_tokens=max_tokens, n=n, attn_chunk=chunk, page_seed=7)
+    if chunk:
+        _say(f"  key splits of the newest row: {(P + steps + n + chunk - 1) // chunk}")
+    w = run_lockstep(eng, model, prompt, steps, draft_for=draft_for, batched_prefill=True)
+    eng.close()
+    _say(f"  worst {w}")
+    assert w["steps"] == steps, w
+
+
+def _gpu_stream(w, n, prompt, steps, table=None):
+    from paper_2605_30852_amd.engine import Engine
+    eng = Engine(w, max_tokens=len(prompt) + steps + n + 8, n=n, page_seed=3)
+    first = eng.spd_prefill(prompt)
+    if table is not None:
+        arr = np.full(steps + 16, -1, dtype=np.int32)
+        for q, t in table.items():
+            if 0 <= q - len(prompt) < len(arr):
+                arr[q - len(prompt)] = t
+        eng.spd_set_forced_drafts(arr, len(prompt))
+    eng.spd_set_graph(True)
+    log = eng.spd_run_steps(steps, want_log=True)
+    toks = eng.tokens()
+    c = log[-1]["committed_len"]
+    eng.close()
+    return first, [int(t) for t in toks[len(prompt): c + 1]], log
+
+
+@pytest.mark.parametrize("n,p", [(5, 0.7), (6, 0.6), (8, 0.7), (8, None)])
+def test_wide_lossless_gpu_spd_equals_gpu_greedy(wide_w, n, p):
+    """Token ids and decisions of the GPU's SPD run at n = 5, 6, 8 (step graph, stage groups) are
+    bit-exact against the GPU's plain greedy decode (n = 1), under Bernoulli masks (decisions equal
+    the mask bits; the step count equals the pipeline timing simulator's) and natural drafts."""
+    prompt = synth.prompt(SH, SEED + 1, 200)
+    steps = 64
+    _say(f"[wide lossless n={n} p={p}]")
+    first, ar, _ = _gpu_stream(wide_w, 1, prompt, steps)
+    table = mask = None
+    if p is not None:
+        mask = synth.accept_mask(p, SEED + 10 * n, 400)
+        table = forced_table(ar, mask, len(prompt), SH.vocab)
+    f2, toks, log = _gpu_stream(wide_w, n, prompt, steps, table)
+    assert f2 == first == ar[0]
+    m = len(toks)
+    assert m >= 2 and toks == ar[:m], f"n={n}: SPD stream differs from greedy decoding"
+    if p is not None:
+        exits = [r for r in log if r["decision"] != 0]
+        assert exits and all(r["decision"] == (1 if mask[r["verified_pos"]] else 2) for r in exits)
+        assert any(r["decision"] == 2 for r in exits) and any(r["decision"] == 1 for r in exits)
+        assert len(log) == osp.simulate_steps(n, m, lambda q: bool(mask[q]), len(prompt)) or \
+            log[-1]["inflight"] != n  # the run may end inside a refill

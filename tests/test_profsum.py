@@ -1,17 +1,17 @@
 """The rocprofv3 summariser that writes the traffic figures under profiles/ (CPU only, synthetic CSVs).
 
-Counter files record no grid shape, so launches of one kernel that cover different stage counts are
-told apart by how much they fetch: the dispatches kept are those within 1/4 of the algorithmic bytes
-(scaled by the device copy's reading of the same counter), and the write run's dispatches at the same
-ordinals. Kernel traces do record grid shapes and select by grid y."""
+Counter files record only a dispatch's total grid size, which is the same for a stage launch over one,
+two or four stages (every stage launch has the same number of workgroups), so a selection by grid y
+takes the dispatch ids of the matching dispatches from the kernel trace of the same counter run, which
+records the grid shape. Nothing is selected by the measured values themselves."""
 import csv
-import os
 
 import pytest
 
 from paper_2605_30852_amd import profsum as ps
 
 K = "k_sgemv<unsigned short, 3>"
+NAME = f"void spd::{K}(spd::Ctx, spd::Rows)"
 
 
 def _csv(path, rows, header):
@@ -23,49 +23,58 @@ def _csv(path, rows, header):
     return str(path)
 
 
-def _counters(tmp_path, fetch_kib, write_kib):
-    hdr = ["Kernel_Name", "Counter_Name", "Counter_Value"]
-    f = _csv(tmp_path / "f.csv", [["__amd_rocclr_copyBuffer", "FETCH_SIZE", 524288.0]] +
-             [[f"void spd::{K}(spd::Ctx, spd::Rows)", "FETCH_SIZE", v] for v in fetch_kib], hdr)
-    w = _csv(tmp_path / "w.csv", [["__amd_rocclr_copyBuffer", "WRITE_SIZE", 1048576.0]] +
-             [[f"void spd::{K}(spd::Ctx, spd::Rows)", "WRITE_SIZE", v] for v in write_kib], hdr)
-    return f, w
+def _run(tmp_path, tag, counter, copy_value, dispatches):
+    """dispatches: (dispatch id, grid y, counter value) of the kernel; returns (counter csv, trace csv)."""
+    hdr = ["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    rows = [[1, 1 << 28, "__amd_rocclr_copyBuffer", counter, copy_value]]
+    rows += [[i, 1024 * 256, NAME, counter, v] for i, _, v in dispatches]
+    c = _csv(tmp_path / f"{tag}_counter.csv", rows, hdr)
+    thdr = ["Dispatch_Id", "Kernel_Name", "Grid_Size_X", "Grid_Size_Y", "Grid_Size_Z", "Start_Timestamp",
+            "End_Timestamp"]
+    trows = [[1, "__amd_rocclr_copyBuffer", 1 << 28, 1, 1, 0, 10]]
+    trows += [[i, NAME, 1024 * 256 // y, y, 1, 0, 10] for i, y, _ in dispatches]
+    t = _csv(tmp_path / f"{tag}_trace.csv", trows, thdr)
+    return c, t
 
 
 def _kv(text):
     return dict(line.split("=", 1) for line in text.splitlines() if "=" in line)
 
 
-def test_traffic_keeps_the_launches_near_the_algorithmic_bytes(tmp_path):
-    # two-stage launches (~97500 KiB fetched), one-stage (half) and four-stage (double) launches mixed
-    fetch = [97500, 48750, 97510, 195000, 97490]
-    write = [150, 75, 152, 300, 154]
-    f, w = _counters(tmp_path, fetch, write)
-    algo = 2 * 97500 * 1024  # the copy reads 512 MiB for 1 GiB: fetch scale 2
-    out = _kv(ps.traffic(f, w, K, 2, algo, None))
+def test_traffic_selects_dispatches_by_id_from_the_same_runs_trace(tmp_path):
+    # four-stage (grid y 4), two-stage and one-stage launches mixed; the fetch run and the write run
+    # issue their dispatches under different ids
+    f, ft = _run(tmp_path, "f", "FETCH_SIZE", 524288.0,
+                 [(10, 4, 195000), (11, 2, 97500), (12, 4, 195010), (13, 1, 48000), (14, 4, 194990)])
+    w, wt = _run(tmp_path, "w", "WRITE_SIZE", 1048576.0,
+                 [(20, 4, 300), (21, 2, 150), (22, 4, 302), (23, 1, 75), (24, 4, 304)])
+    algo = 2 * 195000 * 1024
+    out = _kv(ps.traffic(f, w, K, 4, algo, None, ft, wt))
     assert out["dispatches_fetch"] == "3" and out["dispatches_write"] == "3"
-    assert float(out["fetch_kib_median"]) == 97500 and float(out["write_kib_median"]) == 152
-    assert float(out["scale_fetch"]) == pytest.approx(2.0)
-    assert float(out["hbm_bytes_per_launch"]) == pytest.approx((97500 * 2 + 152) * 1024)
+    assert float(out["fetch_kib_median"]) == 195000 and float(out["write_kib_median"]) == 302
+    assert float(out["scale_fetch"]) == pytest.approx(2.0) and float(out["scale_write"]) == pytest.approx(1.0)
+    assert float(out["hbm_bytes_per_launch"]) == pytest.approx((195000 * 2 + 302) * 1024)
+    assert "dispatch id" in out["selection"]
 
 
-def test_traffic_without_algorithmic_bytes_takes_the_largest_cluster(tmp_path):
-    f, w = _counters(tmp_path, [100, 98, 50, 99], [1, 2, 3, 4])
-    out = _kv(ps.traffic(f, w, K, 2, None, None))
-    assert out["selection"].startswith("largest-value cluster")
-    assert out["dispatches_fetch"] == "3" and float(out["write_kib_median"]) == 2
+def test_traffic_refuses_a_grid_selection_without_traces(tmp_path):
+    f, _ = _run(tmp_path, "f", "FETCH_SIZE", 524288.0, [(10, 4, 195000), (11, 2, 97500)])
+    w, _ = _run(tmp_path, "w", "WRITE_SIZE", 1048576.0, [(20, 4, 300), (21, 2, 150)])
+    assert ps.traffic(f, w, K, 4, None, None).startswith("incomplete")
 
 
-def test_traffic_reports_mismatched_runs(tmp_path):
-    f, w = _counters(tmp_path, [100, 98], [1])
-    assert ps.traffic(f, w, K, 2, 100 * 2 * 1024, None).startswith("incomplete")
+def test_traffic_of_every_dispatch(tmp_path):
+    f, _ = _run(tmp_path, "f", "FETCH_SIZE", 524288.0, [(10, 1, 100), (11, 1, 98), (12, 1, 99)])
+    w, _ = _run(tmp_path, "w", "WRITE_SIZE", 1048576.0, [(20, 1, 1), (21, 1, 2), (22, 1, 3)])
+    out = _kv(ps.traffic(f, w, K, None, None, None))
+    assert out["selection"] == "all dispatches" and out["dispatches_fetch"] == "3"
+    assert float(out["write_kib_median"]) == 2
 
 
 def test_trace_selects_by_grid_y(tmp_path):
     hdr = ["Kernel_Name", "Grid_Size_X", "Grid_Size_Y", "Grid_Size_Z", "Workgroup_Size_X",
            "Start_Timestamp", "End_Timestamp"]
-    rows = [[f"void spd::{K}(spd::Ctx, spd::Rows)", 1024 * 256, y, 1, 256, 0, d * 1000]
-            for y, d in [(2, 40), (2, 42), (4, 73), (1, 20)]]
+    rows = [[NAME, 1024 * 256, y, 1, 256, 0, d * 1000] for y, d in [(2, 40), (2, 42), (4, 73), (1, 20)]]
     t = _csv(tmp_path / "t.csv", rows, hdr)
     out = _kv(ps.trace(t, K, 2))
     assert out["dispatches"] == "2" and float(out["mean_us"]) == pytest.approx(41.0)
