@@ -571,7 +571,7 @@ def extra_workload(label, weights, n, ls, P, p, seed, steps=32, warmup=4, k_span
     log(f"[bench] {label}: prefill")
     first = eng.spd_prefill(prompt)
     log(f"[bench] {label}: prefill {P} tokens in {time.time() - t0:.1f}s")
-    need = warmup + steps + 3 * k_span + 16 + 4 * n + 16
+    need = warmup + steps + 3 * k_span + 16 + 6 * n + 16
     while eng.state()[0] - P < need:
         eng.spd_run_steps(256)
         eng.spd_sync()
@@ -580,9 +580,9 @@ def extra_workload(label, weights, n, ls, P, p, seed, steps=32, warmup=4, k_span
     log(f"[bench] {label}: {len(ref)} greedy reference tokens from the PDM's own drafts")
     eng.spd_rollback(P, int(first))
     eng.spd_set_forced_drafts(ref.astype(np.int32), P)
-    eng.spd_run_steps(warmup)
+    eng.spd_run_steps(warmup + n)  # the pipeline fills in n - 1 steps
     c0, a0, _, _ = eng.state()
-    assert a0 == n
+    assert a0 == n, f"{label}: pipeline not full after warm-up"
     torch.cuda.synchronize()
     ts = time.perf_counter()
     eng.spd_run_steps(steps)

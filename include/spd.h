@@ -328,6 +328,29 @@ spd_status spd_kernel_timing(spd_handle* h, double* total_ms, int32_t* launches)
  * end), i.e. time the verification waited for the draft), and the number of steps; then clears them. */
 spd_status spd_span_timing(spd_handle* h, double* stage_ms, double* pdm_ms, double* late_ms, int32_t* steps);
 
+/* Ragged paged decode attention (Section 3.1: every in-flight token attends, at its own position, over
+ * the cache of the layer it is on) for up to 8 query rows of one layer, as a call of its own. It runs
+ * the step's attention split code: one workgroup per (key split, KV head, row), the last split of a
+ * (row, head) to finish merging its splits in split order.
+ *   q: device fp32 [nrows][n_q_heads][head_dim], the rows' rotated queries (query head h reads KV
+ *      head h / (n_q_heads / n_kv_heads)); scores are scaled by 1/sqrt(head_dim).
+ *   kv: device, one layer's pool [num_pages][K, V][n_kv_heads][16 keys][head_dim] of dtype.
+ *   page_table: device int32 [num_pages]: logical page i (keys 16i..16i+15) is at physical page
+ *      page_table[i], each in [0, num_pages).
+ *   lens: host int32 [nrows], row i attends keys [0, lens[i]); 1 <= lens[i] <= 16 * num_pages.
+ *   out: device fp32 [nrows][n_q_heads][head_dim].
+ *   chunk: keys per split, a positive multiple of 16, with ceil(max lens / chunk) <= 64 splits.
+ *   workspace: device, 256-byte aligned, scratch for the split records and tickets: at least
+ *      ceil256(4 * nrows * n_kv_heads * splits * 8 * (head_dim + 2)) + 4 * nrows * n_kv_heads bytes.
+ * Limits: head_dim 64 or 128; n_q_heads / n_kv_heads in {1, 2, 4, 8}; 1 <= nrows <= 8. The caller owns
+ * every buffer. Asynchronous on stream (a hipStream_t). SPD_E_INVAL for other arguments (checked on the
+ * host before anything is launched), SPD_E_CAPACITY for a workspace too small, SPD_E_HIP if the launch
+ * fails; spd_last_error(NULL) has the message. */
+spd_status spd_decode_attention(const float* q, const void* kv, const int32_t* page_table, int32_t num_pages,
+                                const int32_t* lens, int32_t nrows, int32_t n_q_heads, int32_t n_kv_heads,
+                                int32_t head_dim, int32_t dtype, int32_t chunk, float* out, void* workspace,
+                                size_t ws_bytes, void* stream);
+
 /* Release the handle's events and host buffers (not the caller's memory). NULL is ignored. */
 void spd_destroy(spd_handle* h);
 

@@ -64,7 +64,7 @@ EXPORTS = [
     "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing", "spd_set_step_kernel",
     "spd_step_plan_info", "spd_set_kernel_trace", "spd_set_pdm_placement",
     "spd_set_pdm_grid", "spd_set_pdm_enabled", "spd_probe_hbm_read", "spd_set_sampling",
-    "spd_set_pdm_schedule", "spd_set_graph_steps",
+    "spd_set_pdm_schedule", "spd_set_graph_steps", "spd_decode_attention",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -115,6 +115,8 @@ def lib() -> ct.CDLL:
             "spd_kernel_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
             "spd_span_timing": (I, [P, ct.POINTER(ct.c_double), ct.POINTER(ct.c_double),
                                     ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
+            "spd_decode_attention": (I, [P, P, P, I, ct.POINTER(ct.c_int32), I, I, I, I, I, I, P, P, ct.c_size_t,
+                                         P]),
             "spd_destroy": (None, [P]),
             "spd_status_str": (ct.c_char_p, [I]),
             "spd_last_error": (ct.c_char_p, [P]),
@@ -306,6 +308,24 @@ def spd_kernel_trace(h: int) -> dict:
     J, n, ns = info["J"], info["n"], info["nkslots"]
     raw = spd_read_debug(h, SPD_DBG_KTRACE, 2 * ns, np.uint64).reshape(ns, 2)
     return {"stage": raw[: 5 * J * n].reshape(J, 5, n, 2), "extra": raw[5 * J * n:], **info}
+
+
+def decode_attention_workspace_bytes(nrows: int, n_kv_heads: int, head_dim: int, lens, chunk: int) -> int:
+    """Workspace bytes spd_decode_attention needs (the formula its declaration states)."""
+    splits = (max(int(x) for x in lens) + chunk - 1) // chunk
+    rec = 4 * nrows * n_kv_heads * splits * 8 * (head_dim + 2)
+    return (rec + 255) // 256 * 256 + 4 * nrows * n_kv_heads
+
+
+def spd_decode_attention(q: int, kv: int, page_table: int, num_pages: int, lens, n_q_heads: int, n_kv_heads: int,
+                         head_dim: int, dtype: int, chunk: int, out: int, workspace: int, ws_bytes: int,
+                         stream: int) -> None:
+    """Device pointers as ints; lens: host ints (one per row)."""
+    ln = np.ascontiguousarray(lens, dtype=np.int32)
+    _check("spd_decode_attention",
+           lib().spd_decode_attention(q, kv, page_table, int(num_pages), ln.ctypes.data_as(ct.POINTER(ct.c_int32)),
+                                      len(ln), int(n_q_heads), int(n_kv_heads), int(head_dim), int(dtype), int(chunk),
+                                      out, workspace, int(ws_bytes), stream), None)
 
 
 def spd_destroy(h: int) -> None:

@@ -7,7 +7,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 LIB = os.path.join(PKG, "libspd.so")
-SOURCES = [os.path.join(PKG, "csrc", f) for f in ("spd_kernels.hip", "spd_api.cpp")]
+SOURCES = [os.path.join(PKG, "csrc", f) for f in ("spd_kernels.hip", "spd_decode.hip", "spd_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -141,6 +141,11 @@ void stage_bounds(int L, int n, int* beta) {
 
 }  // namespace
 
+namespace spd {
+// The message spd_last_error(NULL) returns, for calls that have no handle.
+void set_call_error(const std::string& msg) { g_init_error = msg; }
+}  // namespace spd
+
 struct spd_handle {
   spd_config cfg;
   Layout lay;

@@ -130,3 +130,34 @@ def test_init_needs_the_own_head_pointers_before_touching_the_gpu():
 def test_new_setters_check_their_handle():
     assert B.lib().spd_set_sampling(None, 8, 1.0, None, 0) == B.SPD_E_INVAL
     assert B.lib().spd_set_pdm_schedule(None, 1) == B.SPD_E_INVAL
+
+
+def _attn_args(**kw):
+    a = dict(q=256, kv=512, page_table=768, num_pages=8, lens=[20, 19], n_q_heads=8, n_kv_heads=2, head_dim=128,
+             dtype=B.SPD_BF16, chunk=32, out=1024, workspace=4096, ws_bytes=1 << 20, stream=0)
+    a.update(kw)
+    return a
+
+
+@pytest.mark.parametrize("field,value", [
+    ("head_dim", 96), ("n_q_heads", 6), ("chunk", 24), ("chunk", 0), ("lens", [0]), ("lens", [129]),
+    ("lens", [1] * 9), ("dtype", 5), ("workspace", 4100), ("q", 0), ("num_pages", 0),
+])
+def test_decode_attention_argument_checks(field, value):
+    """spd_decode_attention checks its arguments on the host before it launches anything (the pointers
+    here are never dereferenced): SPD_E_INVAL for bad shapes, lengths beyond the pages, a misaligned
+    workspace or a NULL pointer."""
+    with pytest.raises(B.SPDError) as e:
+        B.spd_decode_attention(**_attn_args(**{field: value}))
+    assert e.value.status == B.SPD_E_INVAL
+
+
+def test_decode_attention_workspace_capacity():
+    need = B.decode_attention_workspace_bytes(2, 2, 128, [20, 19], 32)
+    with pytest.raises(B.SPDError) as e:
+        B.spd_decode_attention(**_attn_args(ws_bytes=need - 1))
+    assert e.value.status == B.SPD_E_CAPACITY
+    assert str(need) in str(e.value)
+    with pytest.raises(B.SPDError) as e:  # 69 splits of 16 keys: more than 64
+        B.spd_decode_attention(**_attn_args(lens=[1100], chunk=16, num_pages=80, ws_bytes=1 << 30))
+    assert e.value.status == B.SPD_E_INVAL

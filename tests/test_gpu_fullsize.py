@@ -25,7 +25,7 @@ import pytest
 import synth
 from oracle import model as om
 from oracle import spd as osp
-from tests.lockstep import ABS_LOGIT, REL_HIDDEN, TIE_MARGIN, margin, rel_l2
+from tests.lockstep import ABS_LOGIT, REL_HIDDEN, TIE_MARGIN, margin, rel_l2, top1_explained
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -103,12 +103,12 @@ def test_fullsize_step_parity(which):
             worst_l = max(worst_l, e)
             assert e <= ABS_LOGIT, f"step {i}: exit logits max abs {e:.3e}"
             if r["target_argmax"] != om.argmax_first(lo):
-                assert margin(lo) < TIE_MARGIN, f"step {i}: target argmax differs"
+                assert top1_explained(lo, el, r["target_argmax"]), f"step {i}: target argmax differs"
                 break
     # the draft module: a cache-free forward of its layers over each step's feature sequence
     d = sh.d_model
     w_in = model.w("pdm.in")
-    worst_ph, worst_pl, pdm_checked = 0.0, 0.0, 0
+    worst_ph, worst_pl, pdm_checked, flips = 0.0, 0.0, 0, []
     for i, (c0, a0, ph, pl, pdraft) in enumerate(pdm_snaps):
         T = c0 + a0
         G = np.zeros((T, d))
@@ -128,8 +128,11 @@ def test_fullsize_step_parity(which):
         worst_pl = max(worst_pl, e)
         assert e <= ABS_LOGIT, f"step {i}: PDM logits max abs {e:.3e}"
         if pdraft != om.argmax_first(lo):
-            assert margin(lo) < TIE_MARGIN, f"step {i}: PDM draft {pdraft} != {om.argmax_first(lo)}"
+            flips.append((i, margin(lo), e, float(lo.max() - lo[pdraft])))
+            assert top1_explained(lo, pl, pdraft), \
+                f"step {i}: PDM draft {pdraft} != {om.argmax_first(lo)} (margin {margin(lo):.3e}, logit error {e:.3e})"
         pdm_checked += 1
     _say(f"[fullsize {which}] worst hidden rel L2 {worst_h:.2e}, worst logit abs {worst_l:.2e}, {exits} exits; "
-         f"PDM rows rel L2 {worst_ph:.2e}, PDM logits abs {worst_pl:.2e} over {pdm_checked} steps")
+         f"PDM rows rel L2 {worst_ph:.2e}, PDM logits abs {worst_pl:.2e} over {pdm_checked} steps; "
+         f"draft flips (step, oracle margin, logit error, gap of the GPU's choice): {flips}")
     assert exits >= 4 and pdm_checked == steps

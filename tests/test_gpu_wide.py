@@ -84,10 +84,11 @@ def test_wide_lockstep(wide_w, model, n, P, chunk, p, steps):
 
 def _gpu_stream(w, n, prompt, steps, table=None):
     from paper_2605_30852_amd.engine import Engine
-    eng = Engine(w, max_tokens=len(prompt) + steps + n + 8, n=n, page_seed=3)
+    max_tokens = len(prompt) + steps + n + 8
+    eng = Engine(w, max_tokens=max_tokens, n=n, page_seed=3)
     first = eng.spd_prefill(prompt)
     if table is not None:
-        arr = np.full(steps + 16, -1, dtype=np.int32)
+        arr = np.full(max_tokens - len(prompt), -1, dtype=np.int32)
         for q, t in table.items():
             if 0 <= q - len(prompt) < len(arr):
                 arr[q - len(prompt)] = t
