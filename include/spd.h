@@ -351,6 +351,20 @@ spd_status spd_decode_attention(const float* q, const void* kv, const int32_t* p
                                 int32_t head_dim, int32_t dtype, int32_t chunk, float* out, void* workspace,
                                 size_t ws_bytes, void* stream);
 
+/* spd_decode_attention for callers that cannot allocate: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation. The same arguments and results without the workspace: the
+ * split records and tickets live in a static device array of the library, 8.5 MB (2048 split records
+ * of head_dim 128, plus 8 KiB of tickets) on each GPU the library runs on, held until the process
+ * ends. The call allocates nothing (no hipMalloc, no library allocation); it clears the tickets with a
+ * fill kernel before the attention, so a captured call replays correctly. Every call on a GPU uses that
+ * GPU's one array and leaves its contents there: calls that overlap on one GPU (other streams, other
+ * threads) race, so the caller serializes them. SPD_E_CAPACITY (before anything is launched) when
+ * nrows * n_kv_heads * ceil(max lens / chunk) exceeds 2048; otherwise as spd_decode_attention. */
+spd_status spd_decode_attention_noalloc(const float* q, const void* kv, const int32_t* page_table,
+                                        int32_t num_pages, const int32_t* lens, int32_t nrows, int32_t n_q_heads,
+                                        int32_t n_kv_heads, int32_t head_dim, int32_t dtype, int32_t chunk,
+                                        float* out, void* stream);
+
 /* Release the handle's events and host buffers (not the caller's memory). NULL is ignored. */
 void spd_destroy(spd_handle* h);
 

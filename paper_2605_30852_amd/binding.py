@@ -64,7 +64,7 @@ EXPORTS = [
     "spd_set_kernel_timing", "spd_kernel_timing", "spd_set_graph", "spd_span_timing", "spd_set_step_kernel",
     "spd_step_plan_info", "spd_set_kernel_trace", "spd_set_pdm_placement",
     "spd_set_pdm_grid", "spd_set_pdm_enabled", "spd_probe_hbm_read", "spd_set_sampling",
-    "spd_set_pdm_schedule", "spd_set_graph_steps", "spd_decode_attention",
+    "spd_set_pdm_schedule", "spd_set_graph_steps", "spd_decode_attention", "spd_decode_attention_noalloc",
 ]
 
 _lib: Optional[ct.CDLL] = None
@@ -117,6 +117,7 @@ def lib() -> ct.CDLL:
                                     ct.POINTER(ct.c_double), ct.POINTER(ct.c_int32)]),
             "spd_decode_attention": (I, [P, P, P, I, ct.POINTER(ct.c_int32), I, I, I, I, I, I, P, P, ct.c_size_t,
                                          P]),
+            "spd_decode_attention_noalloc": (I, [P, P, P, I, ct.POINTER(ct.c_int32), I, I, I, I, I, I, P, P]),
             "spd_destroy": (None, [P]),
             "spd_status_str": (ct.c_char_p, [I]),
             "spd_last_error": (ct.c_char_p, [P]),
@@ -326,6 +327,17 @@ def spd_decode_attention(q: int, kv: int, page_table: int, num_pages: int, lens,
            lib().spd_decode_attention(q, kv, page_table, int(num_pages), ln.ctypes.data_as(ct.POINTER(ct.c_int32)),
                                       len(ln), int(n_q_heads), int(n_kv_heads), int(head_dim), int(dtype), int(chunk),
                                       out, workspace, int(ws_bytes), stream), None)
+
+
+def spd_decode_attention_noalloc(q: int, kv: int, page_table: int, num_pages: int, lens, n_q_heads: int,
+                                 n_kv_heads: int, head_dim: int, dtype: int, chunk: int, out: int, stream: int) -> None:
+    """spd_decode_attention with the library's static scratch (no workspace, no allocation)."""
+    ln = np.ascontiguousarray(lens, dtype=np.int32)
+    _check("spd_decode_attention_noalloc",
+           lib().spd_decode_attention_noalloc(q, kv, page_table, int(num_pages),
+                                              ln.ctypes.data_as(ct.POINTER(ct.c_int32)), len(ln), int(n_q_heads),
+                                              int(n_kv_heads), int(head_dim), int(dtype), int(chunk), out, stream),
+           None)
 
 
 def spd_destroy(h: int) -> None:

@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "spd_dev.h"
@@ -144,6 +145,41 @@ spd_status run(const Request& r, const float* q, const void* kv, float* out, flo
 
 size_t rec_bytes(const Request& r) { return (r.rec_floats * sizeof(float) + 255) / 256 * 256; }
 
+// Scratch of spd_decode_attention_noalloc: the split records of at most kNoAllocRecords (row, KV head,
+// split) triples at head_dim 128, then one ticket per (row, KV head). Each GPU the library runs on holds
+// its own copy until the process ends; host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device (the array's name is a host-side stand-in).
+constexpr int kNoAllocRecords = 2048;
+constexpr size_t kNoAllocRecBytes = (size_t)kNoAllocRecords * kAttnMaxQ * (128 + 2) * sizeof(float);
+constexpr size_t kNoAllocBytes = kNoAllocRecBytes + sizeof(int) * (size_t)kNoAllocRecords;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up once per device with that device current.
+spd_status scratch_of_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    set_call_error(std::string("decode attention (no allocation): hipGetDevice: ") + hipGetErrorString(e));
+    return SPD_E_HIP;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      set_call_error(std::string("decode attention (no allocation): hipGetSymbolAddress: ") + hipGetErrorString(e));
+      return SPD_E_HIP;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SPD_OK;
+}
+
 }  // namespace
 }  // namespace spd
 
@@ -170,3 +206,23 @@ extern "C" spd_status spd_decode_attention(const float* q, const void* kv, const
   return run(r, q, kv, out, (float*)ws, (int*)(ws + rec_bytes(r)), stream);
 }
 
+extern "C" spd_status spd_decode_attention_noalloc(const float* q, const void* kv, const int32_t* page_table,
+                                                   int32_t num_pages, const int32_t* lens, int32_t nrows,
+                                                   int32_t n_q_heads, int32_t n_kv_heads, int32_t head_dim,
+                                                   int32_t dtype, int32_t chunk, float* out, void* stream) {
+  Request r;
+  spd_status st = check(q, kv, page_table, num_pages, lens, nrows, n_q_heads, n_kv_heads, head_dim, dtype, chunk, out,
+                        &r);
+  if (st != SPD_OK) return st;
+  const size_t records = (size_t)r.nrows * r.C.hkv * r.smax;
+  if (records > (size_t)kNoAllocRecords) {
+    set_call_error("decode attention (no allocation): nrows * n_kv_heads * splits = " + std::to_string(records) +
+                   " exceeds the " + std::to_string(kNoAllocRecords) + " split records of the static scratch");
+    return SPD_E_CAPACITY;
+  }
+  void* base = nullptr;
+  st = scratch_of_current_device(&base);
+  if (st != SPD_OK) return st;
+  char* ws = (char*)base;
+  return run(r, q, kv, out, (float*)ws, (int*)(ws + kNoAllocRecBytes), stream);
+}
