@@ -35,12 +35,14 @@ __device__ __forceinline__ void gemv_load(const RowFn& rowptr, int K, int ng, in
   }
 }
 
-template <typename WT, typename DoneFn>
-__device__ __forceinline__ void gemv_comp(int nb, int ng, int u, int lane, const float* lds, const uint4 (&b)[2][kU],
-                                          float& a0, float& a1, const DoneFn& done) {
+// The FMAs of unit u (the pair's blocks of group gi against the staged vector) into a0, a1.
+template <typename WT>
+__device__ __forceinline__ void gemv_acc(int nb, int ng, int u, int lane, const float* lds, const uint4 (&b)[2][kU],
+                                         float& a0, float& a1) {
   constexpr int VE = Elt<WT>::VE;
   constexpr int BLK = 64 * VE;
   const int rp = u / ng, gi = u - rp * ng, g0 = gi * kU;
+  (void)rp;
 #pragma unroll
   for (int uu = 0; uu < kU; uu++) {
     const int blk = g0 + uu;
@@ -68,47 +70,18 @@ __device__ __forceinline__ void gemv_comp(int nb, int ng, int u, int lane, const
       for (int e = 0; e < VE; e++) a1 = fmaf(w1[e], x[e], a1);
     }
   }
-  if (gi == ng - 1) {  // the pair's last group: reduce across the wave (fixed butterfly)
+}
+
+// After unit u's FMAs: if it was the pair's last group, reduce across the wave (fixed butterfly) and
+// hand the pair's two dot products to done.
+template <typename DoneFn>
+__device__ __forceinline__ void gemv_fin(int ng, int u, float& a0, float& a1, const DoneFn& done) {
+  const int rp = u / ng, gi = u - rp * ng;
+  if (gi == ng - 1) {
     const float s0 = wave_sum(a0), s1 = wave_sum(a1);
     done(rp, s0, s1);
     a0 = 0.f;
     a1 = 0.f;
-  }
-}
-
-// The first two units (0 in bA, 1 in bB) are requested by gemv_prefetch before the tile waits for
-// its inputs, since weights depend on nothing; gemv_run then keeps one unit in flight while it
-// multiplies the other.
-template <typename WT, int NP, typename RowFn>
-__device__ __forceinline__ void gemv_prefetch(const RowFn& rowptr, int K, int lane, uint4 (&bA)[2][kU],
-                                              uint4 (&bB)[2][kU]) {
-  constexpr int BLK = 64 * Elt<WT>::VE;
-  const int ng = ((K + BLK - 1) / BLK + kU - 1) / kU;
-  gemv_load<WT>(rowptr, K, ng, 0, lane, bA);
-  if (NP * ng > 1) gemv_load<WT>(rowptr, K, ng, 1, lane, bB);
-}
-
-template <typename WT, int NP, typename RowFn>
-__device__ __forceinline__ void gemv_run(const RowFn& rowptr, int K, int lane, const float* lds, uint4 (&bA)[2][kU],
-                                         uint4 (&bB)[2][kU], float& r0, float& r1) {
-  constexpr int BLK = 64 * Elt<WT>::VE;
-  const int nb = (K + BLK - 1) / BLK;
-  const int ng = (nb + kU - 1) / kU;
-  const int NU = NP * ng;
-  float a0 = 0.f, a1 = 0.f;
-  auto done = [&](int rp, float s0, float s1) {
-    if (lane == rp) {
-      r0 = s0;
-      r1 = s1;
-    }
-  };
-  for (int u = 0; u < NU; u += 2) {
-    gemv_comp<WT>(nb, ng, u, lane, lds, bA, a0, a1, done);
-    if (u + 2 < NU) gemv_load<WT>(rowptr, K, ng, u + 2, lane, bA);
-    if (u + 1 < NU) {
-      gemv_comp<WT>(nb, ng, u + 1, lane, lds, bB, a0, a1, done);
-      if (u + 3 < NU) gemv_load<WT>(rowptr, K, ng, u + 3, lane, bB);
-    }
   }
 }
 
@@ -133,12 +106,16 @@ __device__ __forceinline__ void stream_run(const RowFn& rowptr, const DoneFn& do
   const int ng = (nb + kU - 1) / kU;
   const int NU = count * ng;
   float a0 = 0.f, a1 = 0.f;
+  // each buffer is refilled as soon as its unit's FMAs have read it, before that unit's reduction and
+  // epilogue (whose stores the compiler would otherwise keep ahead of the next loads)
   for (int u = 0; u < NU; u += 2) {
-    gemv_comp<WT>(nb, ng, u, lane, lds, bA, a0, a1, done);
+    gemv_acc<WT>(nb, ng, u, lane, lds, bA, a0, a1);
     if (u + 2 < NU) gemv_load<WT>(rowptr, K, ng, u + 2, lane, bA);
+    gemv_fin(ng, u, a0, a1, done);
     if (u + 1 < NU) {
-      gemv_comp<WT>(nb, ng, u + 1, lane, lds, bB, a0, a1, done);
+      gemv_acc<WT>(nb, ng, u + 1, lane, lds, bB, a0, a1);
       if (u + 3 < NU) gemv_load<WT>(rowptr, K, ng, u + 3, lane, bB);
+      gemv_fin(ng, u + 1, a0, a1, done);
     }
   }
 }
@@ -148,13 +125,12 @@ __device__ __forceinline__ void stream_run(const RowFn& rowptr, const DoneFn& do
 // block by the nr (<= NR) vectors staged in LDS (vector r at lds + r * ldsK), each row keeping its
 // own accumulators in the single-row FMA order; when a pair's last group is done every lane calls
 // done(pair, s0, s1) with the nr rows' two dot products (entries >= nr are zero).
-template <typename WT, int NR, typename DoneFn>
-__device__ __forceinline__ void rgemv_comp(int nb, int ng, int u, int lane, const float* lds, int ldsK, int nr,
-                                           const uint4 (&b)[2][kU], float (&a0)[NR], float (&a1)[NR],
-                                           const DoneFn& done) {
+template <typename WT, int NR>
+__device__ __forceinline__ void rgemv_acc(int nb, int ng, int u, int lane, const float* lds, int ldsK, int nr,
+                                          const uint4 (&b)[2][kU], float (&a0)[NR], float (&a1)[NR]) {
   constexpr int VE = Elt<WT>::VE;
   constexpr int BLK = 64 * VE;
-  const int rp = u / ng, gi = u - rp * ng, g0 = gi * kU;
+  const int gi = u % ng, g0 = gi * kU;
 #pragma unroll
   for (int uu = 0; uu < kU; uu++) {
     const int blk = g0 + uu;
@@ -187,6 +163,11 @@ __device__ __forceinline__ void rgemv_comp(int nb, int ng, int u, int lane, cons
       }
     }
   }
+}
+
+template <int NR, typename DoneFn>
+__device__ __forceinline__ void rgemv_fin(int ng, int u, int nr, float (&a0)[NR], float (&a1)[NR], const DoneFn& done) {
+  const int rp = u / ng, gi = u - rp * ng;
   if (gi == ng - 1) {
     float s0[NR], s1[NR];
 #pragma unroll
@@ -212,11 +193,13 @@ __device__ __forceinline__ void rstream_run(const RowFn& rowptr, const DoneFn& d
 #pragma unroll
   for (int r = 0; r < NR; r++) a0[r] = a1[r] = 0.f;
   for (int u = 0; u < NU; u += 2) {
-    rgemv_comp<WT, NR>(nb, ng, u, lane, lds, ldsK, nr, bA, a0, a1, done);
+    rgemv_acc<WT, NR>(nb, ng, u, lane, lds, ldsK, nr, bA, a0, a1);
     if (u + 2 < NU) gemv_load<WT>(rowptr, K, ng, u + 2, lane, bA);
+    rgemv_fin<NR>(ng, u, nr, a0, a1, done);
     if (u + 1 < NU) {
-      rgemv_comp<WT, NR>(nb, ng, u + 1, lane, lds, ldsK, nr, bB, a0, a1, done);
+      rgemv_acc<WT, NR>(nb, ng, u + 1, lane, lds, ldsK, nr, bB, a0, a1);
       if (u + 3 < NU) gemv_load<WT>(rowptr, K, ng, u + 3, lane, bB);
+      rgemv_fin<NR>(ng, u + 1, nr, a0, a1, done);
     }
   }
 }
