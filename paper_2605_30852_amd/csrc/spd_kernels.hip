@@ -791,6 +791,22 @@ __global__ __launch_bounds__(kWG) void k_attn_rows(Ctx C, Rows R, int nrg) {
                                    k1, pos0, page0, lds);
 }
 
+// Row-block attention on matrix cores (bf16 caches, rows * G <= 32 queries): one workgroup per (key
+// split, KV head) serves every row of the block (attn_rows_mfma). Grid: x = key split, y = KV head;
+// splits past the block's last key return at once.
+template <int DH>
+__global__ __launch_bounds__(kWG) void k_attn_rows_mfma(Ctx C, Rows R) {
+  extern __shared__ __align__(16) float lds[];
+  const Grp gr = resolve(C, R, 0);
+  if (!gr.active) return;
+  const int split = blockIdx.x, g = blockIdx.y;
+  if (split * C.chunk >= gr.pos0 + gr.nrows) return;
+  const BufSet& B = C.b[R.set];
+  const size_t row0 = (size_t)gr.brow0 * C.qdim;
+  attn_rows_mfma<DH>(C, (const uint16_t*)C.lay[gr.layer].kv, B.q + row0, B.ao + row0, B.part, B.cnt, g, split,
+                     gr.nrows, gr.pos0, lds);
+}
+
 // Launch trace reset.
 __global__ __launch_bounds__(kWG) void k_ktrace_reset(Ctx C, int nslots) {
   for (int i = blockIdx.x * kWG + threadIdx.x; i < nslots; i += gridDim.x * kWG) {
@@ -1272,6 +1288,16 @@ void Launch<WT>::rows_sublayer(const Ctx& c, const Rows& r, int max_rows, int k,
   if (k == 3) rgemv_launch<WT, SG_GATEUP>(c, r, c.F, c.d, max_rows, cap_wgs, s);
   if (k == 4) rgemv_launch<WT, SG_DOWN>(c, r, (c.d + 1) / 2, c.F, max_rows, cap_wgs, s);
   if (k != 1) return;
+  if constexpr (std::is_same<WT, uint16_t>::value) {
+    if (max_rows * c.G <= 32 && (c.dh == 64 || c.dh == 128)) {  // every query of the block in one MFMA tile
+      const dim3 grid(c.max_splits, c.hkv);
+      if (c.dh == 128)
+        launch_timed((k_attn_rows_mfma<128>), grid, dim3(kWG), attn_rows_mfma_lds<128>(), S(s), c, r);
+      else
+        launch_timed((k_attn_rows_mfma<64>), grid, dim3(kWG), attn_rows_mfma_lds<64>(), S(s), c, r);
+      return;
+    }
+  }
   const int groups8 = (c.max_splits * c.hkv + 7) / 8 * 8;  // see k_attn_rows: XCD-aware order
   const dim3 agrid(groups8 * max_rows);
   const bool g4 = c.G <= 4;

@@ -196,12 +196,15 @@ def test_rollback_api_and_state_errors(tiny_w):
     eng.close()
 
 
-@pytest.mark.parametrize("graph_steps", [1, 4])
-def test_graph_replay_matches_eager(mid_w, graph_steps):
+@pytest.mark.parametrize("mode,groups,place,post,graph_steps", [
+    (2, -1, 0, False, 1), (2, -1, 0, False, 4), (2, 3, 0, False, 1), (2, 2, 1, False, 1), (2, 2, 2, False, 1),
+    (2, 2, 3, False, 1), (0, -1, 0, False, 1), (0, -1, 1, False, 1), (2, -1, 0, True, 1)])
+def test_graph_replay_matches_eager(mid_w, mode, groups, place, post, graph_steps):
     """Steps replayed from the captured step graph (graph_steps steps per graph, and the one-step
-    graph for the remainder) give the same bits as launched steps, on every replay, with eager work
-    and synchronisation between the replays."""
-    _say(f"[graph replay, {graph_steps} steps per graph]")
+    graph for the remainder; the stage groups' and the draft module's streams as its branches,
+    wherever the draft module is placed) give the same bits as launched steps, on every replay, with
+    eager work and synchronisation between the replays; under the post-step schedule too."""
+    _say(f"[graph replay mode={mode} groups={groups} pdm place={place} post_step={post} steps/graph={graph_steps}]")
     sh = mid_w.shape
     prompt = synth.prompt(sh, SEED + 6, 33)
     first, ar, _ = _gpu_stream(mid_w, 1, prompt, 30, max_tokens=200)
@@ -213,22 +216,30 @@ def test_graph_replay_matches_eager(mid_w, graph_steps):
     engs = []
     for graph in (False, True):
         e = _engine(mid_w, 3, max_tokens=200)
-        e.spd_prefill(prompt)
+        e.spd_set_step_kernel(mode, 0, groups if mode == 2 else -1)
+        e.spd_set_pdm_placement(place)
+        e.spd_set_pdm_schedule(post)
+        assert e.spd_prefill(prompt) == first
         e.spd_set_forced_drafts(arr, len(prompt))
         e.spd_set_graph(graph)
         if graph:
             e.spd_set_graph_steps(graph_steps)
         engs.append(e)
+    steps = 0
     for chunk in range(4):
         logs = [e.spd_run_steps(6, want_log=True) for e in engs]
         assert logs[0] == logs[1], f"replay chunk {chunk} differs"
+        steps += 6
         r0, r1 = engs[0].resid(), engs[1].resid()
         assert np.array_equal(r0, r1)
+        assert np.array_equal(engs[0].pdm_hidden(), engs[1].pdm_hidden())
         # one launched (non-graph) step on the graph engine in between replays
         if chunk == 1:
             for e in engs:
                 e.spd_step(int(table.get(e.state()[0] + e.state()[1], 0)))
+            steps += 1
     assert np.array_equal(engs[0].tokens(), engs[1].tokens())
+    assert engs[0].state() == engs[1].state() and engs[0].state()[3] == steps
     for e in engs:
         e.close()
 
