@@ -412,23 +412,23 @@ def main():
         assert aa == n, "PDM hiding measurement left the steady state"
     log(f"[bench] spans: {spans}")
 
-    # tokens/s at a seeded Bernoulli acceptance pattern (rollback and refill exercised)
+    # tokens/s at a seeded Bernoulli acceptance pattern (rollback and refill exercised): one untimed
+    # pass over the pattern, then the timed pass over the same steps
     p = wl.get("p_accept") or 0.7
-    eng.spd_rollback(P, int(first))
     mask = synth.accept_mask(p, args.seed, max_tokens)
     table = np.full(len(ref), -1, dtype=np.int32)
     for i in range(1, len(ref)):
         q = P + i
         table[i] = ref[i] if mask[q] else (ref[i] + 1) % sh.vocab
-    eng.spd_clear_forced_drafts()
-    eng.spd_set_forced_drafts(table, P)
-    torch.cuda.synchronize()
-    ts = time.perf_counter()
-    logp = eng.spd_run_steps(1, want_log=True)
-    t_first = time.perf_counter() - ts
-    logp += eng.spd_run_steps(K - 1, want_log=True)
-    elp = time.perf_counter() - ts
-    log(f"[bench] p-run: first step {1e3 * t_first:.2f} ms, the other {K - 1} steps {1e3 * (elp - t_first):.2f} ms")
+    for timed_pass in (False, True):
+        eng.spd_rollback(P, int(first))
+        eng.spd_clear_forced_drafts()
+        eng.spd_set_forced_drafts(table, P)
+        torch.cuda.synchronize()
+        ts = time.perf_counter()
+        logp = eng.spd_run_steps(K, want_log=True)
+        elp = time.perf_counter() - ts
+        log(f"[bench] p-run ({'timed' if timed_pass else 'warm-up'}): {K} steps in {1e3 * elp:.2f} ms")
     committed = logp[-1]["committed_len"] - P
     spd_tok_s = committed / elp
     alpha = committed / K
@@ -621,17 +621,19 @@ def extra_workload(label, weights, n, ls, P, p, seed, steps=32, warmup=4, k_span
     t_pdm = 1e3 * pd_alone_ms / na
     toks = eng.tokens()[P: eng.state()[0] + 1]
     assert np.array_equal(toks, ref[: len(toks)]), f"{label}: SPD stream differs from greedy decoding"
-    # the Bernoulli(p) draft pattern: rollback, refill, tokens per second
-    eng.spd_rollback(P, int(first))
+    # the Bernoulli(p) draft pattern: rollback, refill, tokens per second (an untimed pass over the
+    # pattern, then the timed pass over the same steps)
     mask = synth.accept_mask(p, seed, max_tokens)
     table = np.array([ref[i] if mask[P + i] else (ref[i] + 1) % sh.vocab for i in range(len(ref))], dtype=np.int32)
-    eng.spd_clear_forced_drafts()
-    eng.spd_set_forced_drafts(table, P)
     steps_b = min(n_bern, len(ref) - 2 * n)
-    torch.cuda.synchronize()
-    ts = time.perf_counter()
-    logp = eng.spd_run_steps(steps_b, want_log=True)
-    elp = time.perf_counter() - ts
+    for _ in range(2):
+        eng.spd_rollback(P, int(first))
+        eng.spd_clear_forced_drafts()
+        eng.spd_set_forced_drafts(table, P)
+        torch.cuda.synchronize()
+        ts = time.perf_counter()
+        logp = eng.spd_run_steps(steps_b, want_log=True)
+        elp = time.perf_counter() - ts
     committed = logp[-1]["committed_len"] - P
     exits = [r for r in logp if r["decision"] != B.SPD_NONE]
     agree = sum(1 for r in exits if r["decision"] == (B.SPD_ACCEPT if mask[r["verified_pos"]] else B.SPD_REJECT))

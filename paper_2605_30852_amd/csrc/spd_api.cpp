@@ -951,14 +951,17 @@ spd_status spd_run_steps(spd_handle* h, int32_t count, spd_step_result* log) {
     spd_status st = fetch_state(h);
     if (st != SPD_OK) return st;
     const int last = h->pinned[0].step_index;
-    // copy the ring entries of the last `count` steps
-    for (int i = 0; i < count; i++) {
-      const int idx = (last - count + i) % kLogCap;
-      HIPC(hipMemcpyAsync(&h->pinned[1 + i % kLogCap], h->ctx.log + idx, sizeof(spd_step_result),
+    // the ring entries of the last `count` steps: one contiguous run, or two where it wraps
+    const int start = (last - count) % kLogCap;
+    const int n1 = std::min(count, kLogCap - start);
+    if (n1 > 0)
+      HIPC(hipMemcpyAsync(&h->pinned[1], h->ctx.log + start, sizeof(spd_step_result) * n1, hipMemcpyDeviceToHost,
+                          h->main));
+    if (count > n1)
+      HIPC(hipMemcpyAsync(&h->pinned[1 + n1], h->ctx.log, sizeof(spd_step_result) * (count - n1),
                           hipMemcpyDeviceToHost, h->main));
-    }
     HIPC(hipStreamSynchronize(h->main));
-    for (int i = 0; i < count; i++) log[i] = h->pinned[1 + i % kLogCap];
+    for (int i = 0; i < count; i++) log[i] = h->pinned[1 + i];
   }
   return SPD_OK;
 }
