@@ -196,7 +196,8 @@ def main():
                     help="the 9B-class workloads (n = 4 at 4096 tokens; n = 8, two-layer PDM at 32768 tokens) after "
                          "the main one (auto: with the default 4B workload)")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="also run a 1 GiB device copy (the known-size kernel for HBM counter scaling)")
+                    help="profiling runs: a 1 GiB device copy (the known-size kernel for HBM counter scaling) "
+                         "and marker dispatches around the measured phases")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the SPD step here is the single-GPU stage-batched "
@@ -284,12 +285,14 @@ def main():
     eng.spd_run_steps(W)
     c0, a0, _, _ = eng.state()
     assert a0 == n, "pipeline not full after warm-up"
+    phase_marker(args)  # phase 0: the steady-state timed run
     torch.cuda.synchronize()
     ts = time.perf_counter()
     eng.spd_run_steps(K)
     eng.spd_sync()
     torch.cuda.synchronize()
     el = time.perf_counter() - ts
+    phase_marker(args)
     c1, a1, _, _ = eng.state()
     assert c1 - c0 == K and a1 == n, "forced-accept run left the steady state"
     toks = eng.tokens()[P: c1 + 1]
@@ -356,7 +359,10 @@ def main():
     eng.spd_set_step_kernel(mode, args.step_grid, 1)
     B.spd_set_pdm_enabled(eng.h, False)
     eng.spd_run_steps(2)
+    eng.spd_sync()
+    phase_marker(args)  # phase 1: the dominant kernel alone
     ms, nl, cm = time_class(B.SPD_K_GATEUP, K_GU)
+    phase_marker(args)
     lb = launch_bytes(sh, n, cm, esz)["gateup"]
     dom_us = 1e3 * ms / max(1, nl)
     dom = {"bytes_per_launch": int(lb), "us_per_launch": round(dom_us, 2), "launches": nl,
@@ -778,13 +784,29 @@ def sampled_phase(args, sh, weights, prompt, ref, first, mask, max_tokens, attn_
     return out
 
 
+def phase_marker(args):
+    """Profiling runs (--copy-calibration): two dispatches of the library's read-probe kernel on a
+    1 MiB buffer, with the GPU idle before and after, at the start and at the end of each measured
+    phase. A counter file records kernel names and dispatch order but not grid shapes, so these
+    markers are how its dispatches are assigned to phases (phase k between markers 2k and 2k+1;
+    the probe kernel runs nowhere else before the closing bandwidth probe)."""
+    if not args.copy_calibration:
+        return
+    import torch
+    from paper_2605_30852_amd import binding as B
+    torch.cuda.synchronize()
+    buf = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(4096, dtype=torch.float32, device="cuda")
+    B.spd_probe_hbm_read(buf.data_ptr(), buf.numel(), sink.data_ptr(), 1, torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+
+
 def traffic_from_profile(name):
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3 counter summary
-    profiles/<name>, or None when the counters were taken on other kernel sources than the ones built
-    now."""
-    import hashlib
+    profiles/<name>, or None when the counters were taken on other kernel sources (any .hip or .h file
+    of csrc) than the ones built now."""
+    from paper_2605_30852_amd.profsum import kernel_sources_digest
     path = os.path.join(ROOT, "profiles", name)
-    src = os.path.join(ROOT, "paper_2605_30852_amd", "csrc", "spd_kernels.hip")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -792,7 +814,7 @@ def traffic_from_profile(name):
         if "=" in line and not line.startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    digest = kernel_sources_digest(os.path.join(ROOT, "paper_2605_30852_amd", "csrc"))
     if kv.get("kernels_sha256") != digest or "hbm_bytes_per_launch" not in kv:
         return None
     return int(float(kv["hbm_bytes_per_launch"]))

@@ -2,22 +2,25 @@
 
     python -m paper_2605_30852_amd.profsum stats KERNEL_STATS.csv [--top N]
     python -m paper_2605_30852_amd.profsum trace KERNEL_TRACE.csv --kernel NAME [--grid-y Y]
-    python -m paper_2605_30852_amd.profsum traffic FETCH.csv WRITE.csv --kernel NAME [--grid-y Y]
-        [--fetch-trace KT.csv --write-trace KT.csv] [--algo-bytes B] [--source FILE]
+    python -m paper_2605_30852_amd.profsum traffic FETCH.csv WRITE.csv --kernel NAME
+        [--phase K | --grid-y Y --fetch-trace KT.csv --write-trace KT.csv] [--algo-bytes B] [--source CSRC_DIR]
 
 `stats` prints the per-kernel table; `trace` the duration of the dispatches of one kernel (a
 substring of its name, optionally only those whose grid has Y workgroups in y, e.g. the two-stage
 group launches); `traffic` the HBM bytes per dispatch of that kernel from a FETCH_SIZE run and a
 WRITE_SIZE run, each scaled by what the same counter reads for the largest device copy in the run
 (a 1 GiB copy reads and writes 2^30 bytes), as key=value lines. The counter files record only the
-total grid size, so a grid-y selection takes the dispatch ids of the matching dispatches from a
-kernel trace of the same run (rocprofv3 --pmc ... --kernel-trace writes both). Pure text
-processing: it reads the CSV files only."""
+total grid size, which is the same for a stage launch over one, two or four stages, so dispatches
+are selected by identity: `--phase K` keeps those of the run's K-th measured phase, which a
+profiling run of bench.py brackets with marker dispatches of the library's read-probe kernel; a
+grid-y selection takes the dispatch ids from a kernel trace of the same run. Pure text processing:
+it reads the CSV files only."""
 from __future__ import annotations
 
 import argparse
 import csv
 import hashlib
+import os
 import statistics
 import sys
 
@@ -84,9 +87,48 @@ def _counter(path, kernel, grid_y, ids=None):
     return vals, (max(copies) if copies else None)
 
 
-def traffic(fetch, write, kernel, grid_y, algo, source, fetch_trace=None, write_trace=None):
-    fids = _dispatch_ids(fetch_trace, kernel, grid_y) if fetch_trace else None
-    wids = _dispatch_ids(write_trace, kernel, grid_y) if write_trace else None
+MARKER = "k_read_probe"
+
+
+def _phase_ids(path, phase):
+    """Dispatch ids between the run's phase markers: the dispatches of the library's read-probe kernel
+    that a profiling run issues around each measured phase (one group of consecutive probe dispatches
+    before the phase, one after). Phase k lies between marker groups 2k and 2k + 1, in dispatch
+    order; the selection depends on dispatch order and kernel names only."""
+    rows = sorted(_rows(path), key=lambda r: int(r["Dispatch_Id"]))
+    groups, cur = [], None  # (first index, last index) of each run of marker dispatches
+    for i, r in enumerate(rows):
+        if MARKER in r.get("Kernel_Name", ""):
+            if cur is not None and cur[1] == i - 1:
+                cur[1] = i
+            else:
+                cur = [i, i]
+                groups.append(cur)
+    if len(groups) < 2 * phase + 2:
+        return None
+    lo, hi = groups[2 * phase][1], groups[2 * phase + 1][0]
+    return {rows[i]["Dispatch_Id"] for i in range(lo + 1, hi)}
+
+
+def kernel_sources_digest(csrc):
+    """First 16 hex digits of the SHA-256 over the device sources in directory csrc (every .hip and .h
+    file, in name order): the counters describe these sources only."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic(fetch, write, kernel, grid_y, algo, source, fetch_trace=None, write_trace=None, phase=None):
+    if phase is not None:
+        fids, wids = _phase_ids(fetch, phase), _phase_ids(write, phase)
+        if fids is None or wids is None:
+            return f"incomplete: fewer than {2 * phase + 2} phase markers in a counter file"
+    else:
+        fids = _dispatch_ids(fetch_trace, kernel, grid_y) if fetch_trace else None
+        wids = _dispatch_ids(write_trace, kernel, grid_y) if write_trace else None
     fv, fc = _counter(fetch, kernel, grid_y, fids)
     wv, wc = _counter(write, kernel, grid_y, wids)
     if fv is None or wv is None:
@@ -94,9 +136,12 @@ def traffic(fetch, write, kernel, grid_y, algo, source, fetch_trace=None, write_
     if not fv or not wv or not fc or not wc:
         return "incomplete: " + repr((len(fv), len(wv), fc, wc))
     sf, sw = GIB_KIB / fc, GIB_KIB / wc
-    how = "all dispatches" if grid_y is None else (
-        f"grid y = {grid_y}, by dispatch id from the kernel trace of each counter run" if fids is not None
-        else f"grid y = {grid_y}")
+    if phase is not None:
+        how = f"phase {phase}: the dispatches between the run's phase markers {2 * phase} and {2 * phase + 1}"
+    else:
+        how = "all dispatches" if grid_y is None else (
+            f"grid y = {grid_y}, by dispatch id from the kernel trace of each counter run" if fids is not None
+            else f"grid y = {grid_y}")
     fk, wk = statistics.median(fv), statistics.median(wv)
     hbm = (fk * sf + wk * sw) * 1024.0
     lines = [f"kernel={kernel}", f"selection={how}", f"dispatches_fetch={len(fv)}", f"dispatches_write={len(wv)}",
@@ -107,7 +152,7 @@ def traffic(fetch, write, kernel, grid_y, algo, source, fetch_trace=None, write_
         lines.append(f"algorithmic_bytes_per_launch={algo:.0f}")
         lines.append(f"traffic_over_algorithmic={hbm / algo:.4f}")
     if source:
-        lines.append("kernels_sha256=" + hashlib.sha256(open(source, "rb").read()).hexdigest()[:16])
+        lines.append("kernels_sha256=" + kernel_sources_digest(source))
     return "\n".join(lines)
 
 
@@ -129,7 +174,9 @@ def main(argv=None):
     c.add_argument("--fetch-trace", default=None, help="kernel trace CSV of the FETCH_SIZE run")
     c.add_argument("--write-trace", default=None, help="kernel trace CSV of the WRITE_SIZE run")
     c.add_argument("--algo-bytes", type=float, default=None)
-    c.add_argument("--source", default=None)
+    c.add_argument("--source", default=None, help="the kernel source directory (csrc)")
+    c.add_argument("--phase", type=int, default=None,
+                   help="only the dispatches of measured phase k (between phase markers 2k and 2k+1)")
     args = ap.parse_args(argv)
     if args.cmd == "stats":
         print(stats(args.csv, args.top))
@@ -137,7 +184,7 @@ def main(argv=None):
         print(trace(args.csv, args.kernel, args.grid_y))
     else:
         print(traffic(args.fetch, args.write, args.kernel, args.grid_y, args.algo_bytes, args.source,
-                      args.fetch_trace, args.write_trace))
+                      args.fetch_trace, args.write_trace, args.phase))
     return 0
 
 

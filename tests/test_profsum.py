@@ -3,7 +3,9 @@
 Counter files record only a dispatch's total grid size, which is the same for a stage launch over one,
 two or four stages (every stage launch has the same number of workgroups), so a selection by grid y
 takes the dispatch ids of the matching dispatches from the kernel trace of the same counter run, which
-records the grid shape. Nothing is selected by the measured values themselves."""
+records the grid shape, or keeps the dispatches of one measured phase, which a profiling run brackets
+with marker dispatches of the read-probe kernel. Nothing is selected by the measured values
+themselves."""
 import csv
 
 import pytest
@@ -78,3 +80,29 @@ def test_trace_selects_by_grid_y(tmp_path):
     t = _csv(tmp_path / "t.csv", rows, hdr)
     out = _kv(ps.trace(t, K, 2))
     assert out["dispatches"] == "2" and float(out["mean_us"]) == pytest.approx(41.0)
+
+
+def test_traffic_selects_a_phase_between_markers(tmp_path):
+    """Phase k lies between marker groups 2k and 2k+1 (runs of consecutive read-probe dispatches):
+    same-named dispatches before, between and after the phases are left out, whatever their values."""
+    hdr = ["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    probe = "void spd::k_read_probe(uint4 const*, unsigned long, float*)"
+
+    def run(tag, counter, copy_value, scale):
+        rows = [[1, 1 << 28, "__amd_rocclr_copyBuffer", counter, copy_value]]
+        seq = [("k", 50), ("m", 0), ("m", 0), ("k", 100), ("k", 102), ("m", 0), ("m", 0), ("k", 7),
+               ("m", 0), ("m", 0), ("k", 400), ("k", 404), ("k", 399), ("m", 0), ("m", 0), ("k", 50),
+               ("m", 0), ("m", 0)]  # the last pair: the closing probe
+        for i, (what, v) in enumerate(seq):
+            rows.append([10 + i, 1024 * 256, NAME if what == "k" else probe, counter, v * scale])
+        rows.reverse()  # the file's row order is not the dispatch order
+        return _csv(tmp_path / f"{tag}.csv", rows, hdr)
+
+    f = run("f", "FETCH_SIZE", 524288.0, 1000)
+    w = run("w", "WRITE_SIZE", 1048576.0, 1)
+    out0 = _kv(ps.traffic(f, w, K, None, None, None, phase=0))
+    assert out0["dispatches_fetch"] == "2" and float(out0["fetch_kib_median"]) == 101000
+    out1 = _kv(ps.traffic(f, w, K, None, None, None, phase=1))
+    assert out1["dispatches_write"] == "3" and float(out1["write_kib_median"]) == 400
+    assert "phase 1" in out1["selection"]
+    assert ps.traffic(f, w, K, None, None, None, phase=2).startswith("incomplete")
