@@ -95,6 +95,22 @@ def launch_bytes(sh, n, c, esz):
     }
 
 
+def timed_stages_per_launch(L, n, groups, first_slot):
+    """Mean number of active stages in the stage launches of layer slots >= first_slot (the launches
+    the kernel timing covers), with the stages spread over `groups` groups of consecutive stages. A
+    stage with fewer layers than the longest is idle in the last slots (beta_{s+1} - beta_s < J), and a
+    group launch with no active stage is not issued."""
+    beta = [s * L // n for s in range(n + 1)]
+    J = max(beta[s + 1] - beta[s] for s in range(n))
+    counts = []
+    for j in range(first_slot, J):
+        for gi in range(groups):
+            k = sum(1 for s in range(gi * n // groups, (gi + 1) * n // groups) if beta[s] + j < beta[s + 1])
+            if k:
+                counts.append(k)
+    return sum(counts) / len(counts)
+
+
 def cpu_baseline(sh, n, ctx, seed, budget_s=12.0):
     """Time the float64 CPU oracle on a bounded sample of the same step and scale it to one step.
 
@@ -343,11 +359,12 @@ def main():
     kernels = {}
     classes = (("qkv", B.SPD_K_QKV), ("attn", B.SPD_K_ATTN), ("oproj", B.SPD_K_OPROJ),
                ("gateup", B.SPD_K_GATEUP), ("down", B.SPD_K_DOWN), ("head", B.SPD_K_HEAD))
+    stages_timed = timed_stages_per_launch(sh.n_layers, n, groups if mode == 2 else 1, first_slot)
     for kname, kid in classes:
         ms, nl, cm = time_class(kid, K_CLS)
         lb = launch_bytes(sh, n, cm, esz)[kname]
-        if mode == 2 and kname != "head":
-            lb = lb / groups  # each launch covers one group's stages (n / groups on average)
+        if kname != "head":
+            lb = lb / n * stages_timed  # per stage, times the stages a timed launch covers on average
         us = 1e3 * ms / max(1, nl)
         kernels[kname] = {"us_per_launch": round(us, 2), "timed_launches_per_step": nl / K_CLS,
                           "bytes_per_launch": int(lb), "GBps": round(lb / (us * 1e-6) / 1e9, 1)}
@@ -363,7 +380,7 @@ def main():
     phase_marker(args)  # phase 1: the dominant kernel alone
     ms, nl, cm = time_class(B.SPD_K_GATEUP, K_GU)
     phase_marker(args)
-    lb = launch_bytes(sh, n, cm, esz)["gateup"]
+    lb = launch_bytes(sh, n, cm, esz)["gateup"] / n * timed_stages_per_launch(sh.n_layers, n, 1, first_slot)
     dom_us = 1e3 * ms / max(1, nl)
     dom = {"bytes_per_launch": int(lb), "us_per_launch": round(dom_us, 2), "launches": nl,
            "GBps": round(lb / (dom_us * 1e-6) / 1e9, 1)}

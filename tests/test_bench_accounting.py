@@ -55,3 +55,16 @@ def test_pdm_kv_is_read_once_per_step(n, ls, c):
     assert pdm - weights == ls * (c + n) * kv_tok + ls * n * kv_tok
     # a per-row count would have read sum_i (c + i + 1) keys per layer instead
     assert pdm - weights < ls * sum(c + i + 1 for i in range(n)) * kv_tok
+
+
+@pytest.mark.parametrize("L,n,groups,first_slot,expect", [
+    (36, 4, 2, 4, 2.0),            # 9 layers per stage: every timed launch covers its group's 2 stages
+    (36, 4, 1, 4, 4.0),
+    (36, 8, 1, 2, (8 + 8 + 4) / 3),  # stages of 4 or 5 layers: slot 4 has only the four 5-layer stages
+    (36, 8, 2, 2, 10 / 3),         # per group (4 stages): 4, 4, 2 in slots 2, 3, 4
+    (36, 6, 2, 3, 3.0),
+])
+def test_timed_stage_launches_count_only_active_stages(L, n, groups, first_slot, expect):
+    """The per-launch bytes of the kernel timing divide by launches of layer slots >= first_slot; a
+    stage shorter than the longest is idle in the last slot and moves nothing there."""
+    assert bench.timed_stages_per_launch(L, n, groups, first_slot) == pytest.approx(expect)
