@@ -95,6 +95,13 @@ def launch_bytes(sh, n, c, esz):
     }
 
 
+def default_attn_chunk(prompt_len):
+    """Keys per attention split in the bench's workloads: about 16 splits over the prompt, in multiples
+    of 64 keys (128 at the 2048-token headline size; 2048 at 32768 tokens, where fewer and longer
+    splits share the GPU better with the other stage group than the library default's ~40)."""
+    return max(64, (prompt_len // 16 + 63) // 64 * 64)
+
+
 def timed_stages_per_launch(L, n, groups, first_slot):
     """Mean number of active stages in the stage launches of layer slots >= first_slot (the launches
     the kernel timing covers), with the stages spread over `groups` groups of consecutive stages. A
@@ -241,7 +248,7 @@ def main():
     # capacity and attention split size depend on the workload only (not on --steps), so that a
     # profiled run with fewer steps launches exactly the kernels the timed run launches
     max_tokens = P + max(1024, n_ref + 4 * n + 64)
-    attn_chunk = args.attn_chunk or max(64, (P // 16 + 63) // 64 * 64)
+    attn_chunk = args.attn_chunk or default_attn_chunk(P)
 
     if args.copy_calibration:
         src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
@@ -595,7 +602,7 @@ def extra_workload(label, weights, n, ls, P, p, seed, steps=32, warmup=4, k_span
     esz = 2 if sh.dtype == "bf16" else 4
     max_tokens = P + 2048
     prompt = synth.prompt(sh, seed, P)
-    eng = Engine(weights, max_tokens=max_tokens, n=n, pdm_layers=ls)
+    eng = Engine(weights, max_tokens=max_tokens, n=n, pdm_layers=ls, attn_chunk=default_attn_chunk(P))
     eng.spd_set_graph(True)
     t0 = time.time()
     log(f"[bench] {label}: prefill")
@@ -665,6 +672,7 @@ def extra_workload(label, weights, n, ls, P, p, seed, steps=32, warmup=4, k_span
     eng.close()
     out = {"workload": f"{sh.name}-class dense decoder (d {sh.d_model}, FFN {sh.ffn_dim}), n={n}, {ls}-layer PDM, "
                        f"{P}-token prompt", "n": n, "pdm_layers": ls, "prompt": P, "steps": steps,
+           "attn_chunk": default_attn_chunk(P),
            "us_per_step": round(us, 1), "bytes_per_step": int(tb + pb),
            "GBps": round((tb + pb) / (us * 1e-6) / 1e9, 1), "frac": round((tb + pb) / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
            "pdm": {"stage_us": round(1e3 * st_ms / ns, 1), "pdm_us": round(1e3 * pd_ms / ns, 1),

@@ -2,6 +2,7 @@
 
     python -m paper_2605_30852_amd.profsum stats KERNEL_STATS.csv [--top N]
     python -m paper_2605_30852_amd.profsum trace KERNEL_TRACE.csv --kernel NAME [--grid-y Y]
+    python -m paper_2605_30852_amd.profsum counters COUNTERS.csv --kernel NAME [--phase K] [--simds N]
     python -m paper_2605_30852_amd.profsum traffic FETCH.csv WRITE.csv --kernel NAME
         [--phase K | --grid-y Y --fetch-trace KT.csv --write-trace KT.csv] [--algo-bytes B] [--source CSRC_DIR]
 
@@ -110,6 +111,38 @@ def _phase_ids(path, phase):
     return {rows[i]["Dispatch_Id"] for i in range(lo + 1, hi)}
 
 
+def counters(path, kernel, phase=None, simds=None):
+    """Median per dispatch of every counter in a counter file, over the kernel's dispatches (those of
+    measured phase k with phase=k). With simds (the GPU's SIMD count), SQ_VALU_MFMA_BUSY_CYCLES is also
+    given as a share of the dispatch's GRBM_GUI_ACTIVE cycles on every SIMD, and the MFMA floating
+    point operations from the MOPS counters (each counts 512 operations)."""
+    ids = _phase_ids(path, phase) if phase is not None else None
+    if phase is not None and ids is None:
+        return f"incomplete: fewer than {2 * phase + 2} phase markers"
+    per = {}
+    for r in _rows(path):
+        if kernel not in r.get("Kernel_Name", "") or (ids is not None and r["Dispatch_Id"] not in ids):
+            continue
+        per.setdefault(r["Counter_Name"], {}).setdefault(r["Dispatch_Id"], 0.0)
+        per[r["Counter_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
+    if not per:
+        return f"no dispatch of {kernel!r}"
+    lines = [f"kernel={kernel}", "selection=" + (f"phase {phase}" if phase is not None else "all dispatches")]
+    for name in sorted(per):
+        v = list(per[name].values())
+        lines.append(f"{name}_dispatches={len(v)}")
+        lines.append(f"{name}_median={statistics.median(v):.1f}")
+    if simds and "SQ_VALU_MFMA_BUSY_CYCLES" in per and "GRBM_GUI_ACTIVE" in per:
+        util = [per["SQ_VALU_MFMA_BUSY_CYCLES"][i] / (per["GRBM_GUI_ACTIVE"][i] * simds)
+                for i in per["SQ_VALU_MFMA_BUSY_CYCLES"] if per["GRBM_GUI_ACTIVE"].get(i)]
+        lines.append(f"mfma_busy_share_median={statistics.median(util):.4f}")
+    for name in sorted(per):
+        if name.startswith("SQ_INSTS_VALU_MFMA_MOPS_"):
+            lines.append(f"{name[len('SQ_INSTS_VALU_MFMA_MOPS_'):].lower()}_mfma_flop_median="
+                         f"{512 * statistics.median(per[name].values()):.0f}")
+    return "\n".join(lines)
+
+
 def kernel_sources_digest(csrc):
     """First 16 hex digits of the SHA-256 over the device sources in directory csrc (every .hip and .h
     file, in name order): the counters describe these sources only."""
@@ -166,6 +199,11 @@ def main(argv=None):
     b.add_argument("csv")
     b.add_argument("--kernel", required=True)
     b.add_argument("--grid-y", type=int, default=None)
+    m = sub.add_parser("counters")
+    m.add_argument("csv")
+    m.add_argument("--kernel", required=True)
+    m.add_argument("--phase", type=int, default=None)
+    m.add_argument("--simds", type=int, default=None, help="SIMDs of the GPU (MI355X: 1024)")
     c = sub.add_parser("traffic")
     c.add_argument("fetch")
     c.add_argument("write")
@@ -182,6 +220,8 @@ def main(argv=None):
         print(stats(args.csv, args.top))
     elif args.cmd == "trace":
         print(trace(args.csv, args.kernel, args.grid_y))
+    elif args.cmd == "counters":
+        print(counters(args.csv, args.kernel, args.phase, args.simds))
     else:
         print(traffic(args.fetch, args.write, args.kernel, args.grid_y, args.algo_bytes, args.source,
                       args.fetch_trace, args.write_trace, args.phase))

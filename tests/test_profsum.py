@@ -106,3 +106,20 @@ def test_traffic_selects_a_phase_between_markers(tmp_path):
     assert out1["dispatches_write"] == "3" and float(out1["write_kib_median"]) == 400
     assert "phase 1" in out1["selection"]
     assert ps.traffic(f, w, K, None, None, None, phase=2).startswith("incomplete")
+
+
+def test_counters_summary_with_mfma_share(tmp_path):
+    """Several counters per dispatch (one row each): medians per counter, the MFMA busy share of the
+    dispatch's active cycles on every SIMD, and the MOPS counter scaled to operations."""
+    hdr = ["Dispatch_Id", "Grid_Size", "Kernel_Name", "Counter_Name", "Counter_Value"]
+    rows = []
+    for i, (busy, active, mops) in enumerate([(400, 10, 100), (600, 10, 300), (500, 10, 200)]):
+        for name, v in (("SQ_VALU_MFMA_BUSY_CYCLES", busy), ("GRBM_GUI_ACTIVE", active),
+                        ("SQ_INSTS_VALU_MFMA_MOPS_F32", mops)):
+            rows.append([100 + i, 256, NAME, name, v])
+    rows.append([200, 256, "other", "GRBM_GUI_ACTIVE", 1])
+    c = _csv(tmp_path / "m.csv", rows, hdr)
+    out = _kv(ps.counters(c, K, None, 100))
+    assert out["GRBM_GUI_ACTIVE_dispatches"] == "3"
+    assert float(out["mfma_busy_share_median"]) == pytest.approx(0.5)
+    assert float(out["f32_mfma_flop_median"]) == 512 * 200
