@@ -109,6 +109,10 @@ MID = ModelShape("mid", 6, 384, 8, 2, 64, 1000, 3001, "bf16", n_stages=3, pdm_la
 # module whose feature projection reads n * 1024 anchors, and an FFN of 5120 (eight rows of its down
 # projection input do not fit one workgroup's LDS at once).
 WIDE = ModelShape("wide", 10, 1024, 8, 2, 128, 5120, 4096, "bf16", n_stages=8, pdm_layers=2)
+# bf16 models with other head ratios: eight query heads per KV head (a prefill chunk's 8 rows are then
+# 64 queries per KV head) and plain multi-head attention (one query head per KV head).
+GQA8 = ModelShape("gqa8", 5, 256, 16, 2, 64, 704, 2000, "bf16", n_stages=4, pdm_layers=1)
+MHA = ModelShape("mha", 4, 256, 4, 4, 64, 704, 2000, "bf16", n_stages=3, pdm_layers=1)
 
 WORKLOADS = {
     "tiny": dict(shape=TINY, prompt_len=64, steps=32, p_accept=None),
