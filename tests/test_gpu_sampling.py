@@ -7,7 +7,8 @@ boundaries of each draw and the acceptance ratio p(x)/q(x)), staying inside the 
 so the oracle's run is unchanged; after that the HIP path must make every decision the oracle makes:
 draft, acceptance, committed token, pipeline state, step by step. The draft distributions the HIP path
 keeps with the in-flight tokens must hold the oracle's top-k ids (the last place may differ when the
-oracle's k-th and (k+1)-th logits are closer than TIE) and its probabilities to PROB_ABS.
+oracle's k-th and (k+1)-th logits are closer than TIE), each with its probability to PROB_ABS, in the
+oracle's order except between entries whose logits lie within twice the measured logit error.
 At any size: top_k = 1 is greedy decoding, bit for bit; and at the 4B-class size the kept
 distribution is exactly the top-50 of the HIP path's own logits with their softmax."""
 import sys
@@ -135,6 +136,27 @@ def _oracle_run(model, prompt, n, k, temp, U, steps, draft_for, nudge, schedule=
     return out, ties, moved
 
 
+def _check_kept(gi, gp, ids, probs, tie, swap, p_tol, tag):
+    """The kept top-k list of one position against the oracle's. The verify reads it only as a map
+    from ids to probabilities (q(x) and max(0, p - q) per id), so each id's probability is compared
+    by id. The order must be the oracle's except between entries whose oracle log-probabilities lie
+    within `swap` of each other (logits off by e can reorder any two closer than 2e); where the
+    oracle's k-th and (k+1)-th logits nearly tie, one id may be the oracle's (k+1)-th instead."""
+    where = {int(t): j for j, t in enumerate(ids)}
+    pos = [where.get(int(t), -1) for t in gi]
+    assert sum(j < 0 for j in pos) <= (1 if tie else 0), f"{tag}: ids {list(gi)} vs {list(ids)}"
+    assert len(set(pos)) == len(pos), f"{tag}: repeated ids {list(gi)}"
+    lp = np.log(np.asarray(probs, dtype=np.float64))
+    mine = [(j, lp[i]) for j, i in enumerate(pos) if i >= 0]
+    lowest = np.inf  # oracle log-probabilities must not rise along the kept order beyond `swap`
+    for j, v in mine:
+        assert v <= lowest + swap, f"{tag}: place {j} (id {gi[j]}) out of order beyond {swap:.2e}"
+        lowest = min(lowest, v)
+    got = np.array([gp[j] for j, _ in mine])
+    want = np.array([probs[pos[j]] for j, _ in mine])
+    np.testing.assert_allclose(got, want, atol=p_tol, err_msg=tag)
+
+
 def _clear_uniforms(model, prompt, n, k, temp, rows, steps, draft_for, seed, schedule="pre", tol_u=TOL_U):
     U = np.random.default_rng([seed, 3]).random((rows, 3)).astype(np.float32).astype(np.float64)
     for _ in range(20):
@@ -216,9 +238,7 @@ def test_sampled_lockstep_matches_oracle(tiny_w, mid_w, which, n, k, temp, force
         for q, (ids, probs) in ora.qdist.items():
             gi, gp = eng.qdist(q)
             assert len(gi) == len(ids), f"{tag}: q of position {q} has {len(gi)} entries, oracle {len(ids)}"
-            m = len(ids) - (1 if q in ties else 0)  # the last place of a near tie may differ
-            np.testing.assert_array_equal(gi[:m], ids[:m], err_msg=f"{tag}: q ids of position {q}")
-            np.testing.assert_allclose(gp[:m], probs[:m], atol=p_tol, err_msg=f"{tag}: q of position {q}")
+            _check_kept(gi, gp, ids, probs, q in ties, 2.0 * lg_err / temp, p_tol, f"{tag}: q of position {q}")
     toks = eng.tokens()
     assert list(toks[: ora.c + 1]) == ora.toks[: ora.c + 1]
     eng.close()
