@@ -31,6 +31,31 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def prefill_with_progress(eng, prompt, label, every=20.0):
+    """eng.spd_prefill(prompt) on a worker thread (the C call releases the interpreter lock), with a
+    progress line every `every` seconds while it runs: a long prompt takes over a minute."""
+    import threading
+    out = {}
+
+    def work():
+        try:
+            out["first"] = eng.spd_prefill(prompt)
+        except BaseException as e:  # re-raised on the calling thread
+            out["error"] = e
+
+    t0 = time.time()
+    th = threading.Thread(target=work, daemon=True)
+    th.start()
+    while True:
+        th.join(every)
+        if not th.is_alive():
+            break
+        log(f"[bench] {label}: prefill of {len(prompt)} tokens running, {time.time() - t0:.0f}s")
+    if "error" in out:
+        raise out["error"]
+    return out["first"]
+
+
 def pdm_kv_bytes(sh, ls, c, a, esz):
     """The draft module's keys and values in a step with c committed positions and a in-flight rows:
     its rows at positions c..c+a-1 attend over one shared cache, so each PDM layer's keys and values
@@ -606,7 +631,7 @@ def extra_workload(label, weights, n, ls, P, p, seed, steps=32, warmup=4, k_span
     eng.spd_set_graph(True)
     t0 = time.time()
     log(f"[bench] {label}: prefill")
-    first = eng.spd_prefill(prompt)
+    first = prefill_with_progress(eng, prompt, label)
     log(f"[bench] {label}: prefill {P} tokens in {time.time() - t0:.1f}s")
     need = warmup + steps + 3 * k_span + 16 + 6 * n + 16
     while eng.state()[0] - P < need:

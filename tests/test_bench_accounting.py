@@ -68,3 +68,24 @@ def test_timed_stage_launches_count_only_active_stages(L, n, groups, first_slot,
     """The per-launch bytes of the kernel timing divide by launches of layer slots >= first_slot; a
     stage shorter than the longest is idle in the last slot and moves nothing there."""
     assert bench.timed_stages_per_launch(L, n, groups, first_slot) == pytest.approx(expect)
+
+
+class _SlowPrefill:
+    def __init__(self, secs, fail=False):
+        self.secs, self.fail = secs, fail
+
+    def spd_prefill(self, prompt):
+        import time
+        time.sleep(self.secs)
+        if self.fail:
+            raise RuntimeError("prefill refused")
+        return int(prompt[-1])
+
+
+def test_prefill_progress_lines_and_result(capsys):
+    """The bench's long prefills run on a worker thread: progress lines while it runs, then the first
+    token; an error on the worker is raised on the caller."""
+    assert bench.prefill_with_progress(_SlowPrefill(0.35), [3, 9, 5], "w", every=0.1) == 5
+    assert "prefill of 3 tokens running" in capsys.readouterr().err
+    with pytest.raises(RuntimeError, match="refused"):
+        bench.prefill_with_progress(_SlowPrefill(0.05, fail=True), [1], "w", every=0.1)
