@@ -24,7 +24,7 @@ enum HState { H_INIT = 0, H_READY = 1, H_PENDING = 2 };
 
 struct Layout {
   size_t kv, pkv, pt, rope, state, tok, forced, log, resid, anch, pdmx, pfx, pfanch, dbg, lay;
-  size_t q[2], ao[2], act[2], part[2], cnt[2], hkey[2];
+  size_t q[2], ao[2], act[2], part[2], cnt[2], hkey[2], rpart[2], rtick[2];
   size_t ktrace;
   size_t su, swlog, swgmax, sqids, sqp, sqcnt, spq;  // sampled decoding
   size_t total;
@@ -68,6 +68,21 @@ spd_status check_config(const spd_config* c, std::string* why) {
   if (c->pdm_vocab > 0 && c->fused_head) return bad("an own PDM head (pdm_vocab > 0) needs fused_head = 0");
   if (c->d_model > 8192) return bad("d_model must be at most 8192");
   return SPD_OK;
+}
+
+// Floats of one set's K-split row GEMV records: the largest sublayer's chunk dot products (chunks x
+// kMaxRows rows x pairs x 2), then the sums of squares of up to kRowSplitCols columns.
+size_t rows_split_floats(const spd_config& c) {
+  const int d = c.d_model, qdim = c.n_q_heads * c.head_dim, F = c.ffn_dim;
+  auto chunks = [](int K) { return (size_t)(K + kRowSplitK - 1) / kRowSplitK; };
+  const size_t pairs_qkv = (size_t)(c.n_q_heads + 2 * c.n_kv_heads) * (c.head_dim / 2);
+  const size_t pairs_half = (size_t)(d + 1) / 2;
+  size_t rec = chunks(d) * pairs_qkv;
+  rec = std::max(rec, chunks(qdim) * pairs_half);
+  rec = std::max(rec, chunks(d) * (size_t)F);
+  rec = std::max(rec, chunks(F) * pairs_half);
+  const size_t max_chunks = std::max(chunks(d), std::max(chunks(qdim), chunks(F)));
+  return rec * kMaxRows * 2 + (size_t)kRowSplitCols * max_chunks * kMaxRows;
 }
 
 Layout make_layout(const spd_config& c) {
@@ -118,6 +133,8 @@ Layout make_layout(const spd_config& c) {
     L.act[s] = take(sizeof(float) * kMaxRows * (size_t)c.ffn_dim);
     L.part[s] = take(sizeof(float) * part_floats);
     L.cnt[s] = take(sizeof(int32_t) * kMaxStages * hkv);
+    L.rpart[s] = take(sizeof(float) * rows_split_floats(c));
+    L.rtick[s] = take(sizeof(int32_t) * kRowSplitCols);
     L.hkey[s] = take(sizeof(unsigned long long));
   }
   L.nkslots = 5 * L.J * n + 4;
@@ -606,6 +623,8 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
     B.act = (float*)(ws + lay.act[s]);
     B.part = (float*)(ws + lay.part[s]);
     B.cnt = (int32_t*)(ws + lay.cnt[s]);
+    B.rpart = (float*)(ws + lay.rpart[s]);
+    B.rtick = (int32_t*)(ws + lay.rtick[s]);
     B.hkey = (unsigned long long*)(ws + lay.hkey[s]);
   }
   C.post_step = 0;
@@ -670,6 +689,7 @@ spd_status spd_init(const spd_config* cfg, const spd_weights* w, void* workspace
   HIPI(hipMemsetAsync(ws + lay.tok, 0, sizeof(int32_t) * (c.max_tokens + 8), h->main));
   HIPI(hipMemsetAsync(ws + lay.forced, 0xff, sizeof(int32_t) * (c.max_tokens + 8), h->main));
   for (int s = 0; s < 2; s++) HIPI(hipMemsetAsync(ws + lay.cnt[s], 0, sizeof(int32_t) * kMaxStages * c.n_kv_heads, h->main));
+  for (int s = 0; s < 2; s++) HIPI(hipMemsetAsync(ws + lay.rtick[s], 0, sizeof(int32_t) * kRowSplitCols, h->main));
   for (int s = 0; s < 2; s++) HIPI(hipMemsetAsync(ws + lay.hkey[s], 0, sizeof(unsigned long long), h->main));
   HIPI(hipMemsetAsync(ws + lay.sqcnt, 0, sizeof(int32_t) * c.n_stages, h->main));
   HIPI(hipMemsetAsync(ws + lay.spq, 0, (sizeof(int32_t) + sizeof(float)) * kMaxTopK + sizeof(int32_t), h->main));

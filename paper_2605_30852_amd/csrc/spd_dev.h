@@ -9,6 +9,11 @@ namespace spd {
 
 constexpr int kMaxStages = 8;   // n
 constexpr int kMaxRows = 8;     // rows of one row-block launch (PDM rows, prefill chunk)
+// Uncapped row-block GEMVs (prefill chunks) whose rows' input vectors take more LDS than kRowLdsBudget
+// at full width run K-split: chunks of kRowSplitK inputs, at most kRowSplitCols workgroup columns.
+constexpr int kRowSplitK = 1024;
+constexpr int kRowLdsBudget = 64 * 1024;
+constexpr int kRowSplitCols = 1024;
 constexpr int kMaxPdmLayers = 4;
 constexpr int kWG = 256;        // threads per workgroup in every kernel
 constexpr int kLogCap = 4096;   // step log ring
@@ -51,6 +56,8 @@ struct BufSet {
   float* act;       // [8][F] SwiGLU activations
   float* part;      // attention split partials
   int32_t* cnt;     // per (stage, KV head) split tickets of the decode attention; zero at rest
+  float* rpart;     // K-split row GEMV records (chunk dot products, sums of squares)
+  int32_t* rtick;   // K-split row GEMV tickets, one per workgroup column; zero at rest
   // LM-head argmax of this stream's row: the maximum over the vocabulary of a 64-bit key that
   // orders (logit descending, index ascending); zero at rest (reset by its reader)
   unsigned long long* hkey;

@@ -506,6 +506,155 @@ __global__ __launch_bounds__(kWG) void k_rgemv(Ctx C, Rows R, int nrp) {
   }
 }
 
+// K-split row-block GEMV: the same sublayers as k_rgemv, for row blocks whose input vectors do not fit
+// the LDS budget at full width. Workgroup (x, y) stages chunk y (kRowSplitK inputs) of every row and
+// streams its pairs over that chunk only, in the same per-wave FMA order as k_rgemv, so each weight is
+// read once and the workgroup holds a small LDS slice, leaving room on its compute unit for other work.
+// Each chunk's dot products (and, for the normed sublayers, its sums of squares) go to split records;
+// the workgroup of column x that finishes last (a ticket per column, zero at rest) adds the chunks in
+// chunk order and runs the epilogue of the column's pairs, then resets the ticket.
+// Records: pair q of row r, chunk y at part[((y * kMaxRows + r) * npairs + q) * 2]; the sums of
+// squares of column x after them, at [(x * chunks + y) * kMaxRows + r].
+template <typename WT, int KIND, int NR>
+__global__ __launch_bounds__(kWG) void k_rgemv_ks(Ctx C, Rows R) {
+  extern __shared__ __align__(16) float lds[];
+  __shared__ float red[4];
+  __shared__ float s_sc[kMaxRows];
+  __shared__ int s_last;
+  const Grp gr = resolve(C, R, 0);
+  if (!gr.active) return;
+  const LayerDesc Ld = C.lay[gr.layer];
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int NW = gridDim.x * 4, wv = blockIdx.x * 4 + w;
+  const int d = C.d, dh = C.dh, half = C.dh >> 1;
+  const int K = KIND == SG_OPROJ ? C.qdim : (KIND == SG_DOWN ? C.F : d);
+  const int ns = gridDim.y, y = blockIdx.y;
+  const int k0 = y * kRowSplitK, KC = min(kRowSplitK, K - k0);
+  const int npairs = KIND == SG_QKV ? (C.hq + 2 * C.hkv) * half : (KIND == SG_GATEUP ? C.F : (d + 1) / 2);
+  const int count = wv < npairs ? (npairs - 1 - wv) / NW + 1 : 0;  // at most 64 (the host sizes the grid)
+  const int nr = gr.nrows;                                          // at most NR (the host checks)
+  constexpr bool NORM = KIND == SG_QKV || KIND == SG_GATEUP;
+  float* part = C.b[R.set].rpart;
+  float* ssq = part + (size_t)ns * kMaxRows * npairs * 2;
+  auto rowptr = [&](int i, int which) -> const WT* {
+    const int q = wv + i * NW;
+    const WT* p;
+    if (KIND == SG_QKV) {
+      const int head = q / half, j = q - head * half;
+      const WT* W = head < C.hq ? (const WT*)Ld.wq : (head < C.hq + C.hkv ? (const WT*)Ld.wk : (const WT*)Ld.wv);
+      const int hrow = head < C.hq ? head : (head < C.hq + C.hkv ? head - C.hq : head - C.hq - C.hkv);
+      p = W + (size_t)(hrow * dh + j + which * half) * d;
+    } else if (KIND == SG_GATEUP) {
+      p = (which ? (const WT*)Ld.wu : (const WT*)Ld.wg) + (size_t)q * d;
+    } else {
+      const int m = 2 * q + which;
+      if (m >= d) return (const WT*)nullptr;
+      p = (const WT*)(KIND == SG_OPROJ ? Ld.wo : Ld.wd) + (size_t)m * K;
+    }
+    return p + k0;
+  };
+  uint4 bA[2][kU], bB[2][kU];
+  stream_prefetch<WT>(rowptr, count, KC, lane, bA, bB);
+  float ss[NR];
+#pragma unroll
+  for (int r = 0; r < NR; r++) {
+    ss[r] = 0.f;
+    if (r < nr) {
+      if (NORM)
+        ss[r] = stage_vec<Elt<WT>::VE>(gr.x + (size_t)r * gr.xstride + k0,
+                                       (KIND == SG_QKV ? Ld.attn_norm : Ld.mlp_norm) + k0, KC,
+                                       lds + (size_t)r * kRowSplitK, red);
+      else
+        stage_vec<Elt<WT>::VE>((KIND == SG_OPROJ ? C.b[R.set].ao : C.b[R.set].act) + (size_t)(gr.brow0 + r) * K + k0,
+                               nullptr, KC, lds + (size_t)r * kRowSplitK, red);
+    }
+  }
+  auto keep = [&](int i, const float (&s0)[NR], const float (&s1)[NR]) {
+    const int q = wv + i * NW;
+#pragma unroll
+    for (int r = 0; r < NR; r++)
+      if (lane == r && r < nr) st_dev2f(part + (((size_t)y * kMaxRows + r) * npairs + q) * 2, s0[r], s1[r]);
+  };
+  rstream_run<WT, NR>(rowptr, keep, count, KC, lane, lds, kRowSplitK, nr, bA, bB);
+  if (NORM && tid < nr) {
+#pragma unroll
+    for (int r = 0; r < NR; r++)
+      if (tid == r) st_dev(ssq + ((size_t)blockIdx.x * ns + y) * kMaxRows + r, ss[r]);
+  }
+  wait_own_stores();
+  __syncthreads();
+  if (tid == 0) {
+    const int t = __hip_atomic_fetch_add(C.b[R.set].rtick + blockIdx.x, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (t == ns - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  // the column's last workgroup: the rows' RMSNorm scales, then every (pair, row) of the column
+  if (tid < kMaxRows) {
+    float sc = 1.f;
+    if (NORM && tid < nr) {
+      float t = 0.f;
+      for (int yy = 0; yy < ns; yy++) t += ld_dev(ssq + ((size_t)blockIdx.x * ns + yy) * kMaxRows + tid);
+      sc = 1.0f / sqrtf(t / (float)d + C.eps);
+    }
+    s_sc[tid] = sc;
+  }
+  __syncthreads();
+  float* cap = (KIND == SG_DOWN && R.anch != nullptr && R.cap >= 0) ? R.anch + (size_t)R.cap * d : nullptr;
+  for (int e = lane; e < count * nr; e += 64) {
+    const int i = e / nr, r = e - i * nr;
+    const int q = wv + i * NW;
+    float s0 = 0.f, s1 = 0.f;
+    for (int yy = 0; yy < ns; yy++) {
+      const float2 v = ld_dev2(part + (((size_t)yy * kMaxRows + r) * npairs + q) * 2);
+      s0 += v.x;
+      s1 += v.y;
+    }
+    const float sc = s_sc[r];
+    const int pos = gr.pos0 + r;
+    if (KIND == SG_QKV) {
+      const int head = q / half, j = q - head * half;
+      float lo = s0 * sc, hi = s1 * sc;
+      if (head < C.hq + C.hkv) {
+        const float2 v = C.rope[(size_t)pos * half + j];
+        const float rlo = lo * v.x - hi * v.y;
+        const float rhi = hi * v.x + lo * v.y;
+        lo = rlo;
+        hi = rhi;
+      }
+      if (head < C.hq) {
+        float* qo = C.b[R.set].q + (size_t)(gr.brow0 + r) * C.qdim + head * dh;
+        qo[j] = lo;
+        qo[j + half] = hi;
+      } else {
+        const int hk = head < C.hq + C.hkv ? head - C.hq : head - C.hq - C.hkv;
+        WT* kv = (WT*)Ld.kv;
+        const int page = C.page_table[pos / C.page];
+        const size_t off = (size_t)page * (2 * C.hkv * C.page * dh) + ((size_t)hk * C.page + (pos % C.page)) * dh + j +
+                           (head < C.hq + C.hkv ? 0 : (size_t)C.hkv * C.page * dh);
+        st1<WT>(kv, off, lo);
+        st1<WT>(kv, off + half, hi);
+      }
+    } else if (KIND == SG_GATEUP) {
+      const float g = s0 * sc, u = s1 * sc;
+      C.b[R.set].act[(size_t)(gr.brow0 + r) * C.F + q] = g / (1.0f + expf(-g)) * u;
+    } else {
+      const int m = 2 * q;
+      float* xr = gr.x + (size_t)r * gr.xstride;
+      const float n0 = xr[m] + s0;
+      const float n1 = m + 1 < d ? xr[m + 1] + s1 : 0.f;
+      xr[m] = n0;
+      if (m + 1 < d) xr[m + 1] = n1;
+      if (cap != nullptr) {
+        float* cr = cap + (size_t)r * C.n * d;
+        cr[m] = n0;
+        if (m + 1 < d) cr[m + 1] = n1;
+      }
+    }
+  }
+  if (tid == 0) __hip_atomic_store(C.b[R.set].rtick + blockIdx.x, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---------------------------------------------------------------------- PDM feature projection
 // g_q = W_in . [H^{beta_0}; ...; H^{beta_f}; 0 ...] for the rows the PDM runs (Eq. agg-main with
 // one projection whose column block j serves anchor j). prefill = 1: rows of the prefill chunk
@@ -1260,6 +1409,25 @@ static int rows_per_pass(int K, int max_rows) {
 
 template <typename WT, int KIND>
 static void rgemv_launch(const Ctx& c, const Rows& r, int npairs, int K, int max_rows, int cap_wgs, void* s) {
+  const int rows = std::max(1, std::min(max_rows, kMaxRows));
+  const int min_cols = (npairs + 255) / 256;  // no wave streams more than 64 pairs
+  if (cap_wgs <= 0 && stream_lds<WT>(K) * rows > (size_t)kRowLdsBudget && K > kRowSplitK &&
+      min_cols <= kRowSplitCols) {
+    // K-split (uncapped row blocks: prefill chunks): every chunk of every row in one pass over the
+    // weights, a small LDS slice per workgroup. A capped launch (side work beside the stage compute)
+    // keeps the full-width form: with few columns the split's last-arriver merges run long.
+    const int ns = (K + kRowSplitK - 1) / kRowSplitK;
+    const size_t shm = (size_t)rows * kRowSplitK * sizeof(float);
+    const int resident = dev_limits().cus * std::max(1, (int)((size_t)dev_limits().lds_max / (shm + 1024)));
+    const int cols = std::min(std::max(std::min(stream_grid(c, npairs, 1), std::max(1, resident / ns)), min_cols),
+                              kRowSplitCols);
+    const dim3 grid(cols, ns);
+    if (rows <= 4)
+      launch_timed((k_rgemv_ks<WT, KIND, 4>), grid, dim3(kWG), shm, S(s), c, r);
+    else
+      launch_timed((k_rgemv_ks<WT, KIND, 8>), grid, dim3(kWG), shm, S(s), c, r);
+    return;
+  }
   const int nrp = rows_per_pass<WT>(K, max_rows);
   const size_t shm = stream_lds<WT>(K) * nrp;
   // no more workgroups than the GPU holds at once with this much LDS (a second round would double
