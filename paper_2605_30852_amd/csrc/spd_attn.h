@@ -197,8 +197,8 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
   const int R = (k1 - k0 + PASS - 1) / PASS;  // rounds
   const int my = w * WK + kk;                 // this lane's key within a round
 
-  // Every global load below is unconditional (keys past the split read key k1 - 1 and are masked
-  // later), so the count of loads issued after any given load is the same on every path and each
+  // Every global load below is unconditional (keys past the split read the slot of key k1 - 1, in
+  // round 0 of the page their own key falls in, and are masked later), so the count of loads issued after any given load is the same on every path and each
   // wait covers exactly the loads it needs: queries first, then the page of round 1, round 0, the
   // page of round 2, round 1.
   constexpr int QPT = (MAXQ * DH + kWG - 1) / kWG;
@@ -246,8 +246,13 @@ __device__ bool attn_split_g(const Ctx& C, const KVT* kvb, const float* q, float
     float kf[NE];
 #pragma unroll
     for (int c = 0; c < KCH; c++) unpack16<KVT>(kr_raw[c], kf + c * VE);
+    // a key past the end may come from a page beyond the cache's length (round 0's page is looked up
+    // before the length is known), whose contents are arbitrary: its V row enters the tile as zeros,
+    // so that its zero probability keeps the sums exact even if those bytes are not a finite number
+    const bool kin = kk < nkw;
 #pragma unroll
-    for (int c = 0; c < KCH; c++) reinterpret_cast<uint4*>(vt + kk * DH + qq * NE)[c] = vr_raw[c];
+    for (int c = 0; c < KCH; c++)
+      reinterpret_cast<uint4*>(vt + kk * DH + qq * NE)[c] = kin ? vr_raw[c] : make_uint4(0u, 0u, 0u, 0u);
     {  // the buffers are free again: round r + 2, and the page of round r + 3 (past the end: key k1 - 1)
       const int pg = pg_next;
       pg_next = page_of(r + 3);

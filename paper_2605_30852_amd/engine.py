@@ -128,8 +128,11 @@ class Engine:
 
     def __init__(self, weights: DeviceWeights, max_tokens: int, n: Optional[int] = None,
                  pdm_layers: Optional[int] = None, auto_rollback: bool = True, attn_chunk: int = 0,
-                 page_seed: int = 0, fused_head: Optional[bool] = None, device="cuda"):
-        """fused_head: None picks the two-row pass when the PDM shares the target's head."""
+                 page_seed: int = 0, fused_head: Optional[bool] = None, device="cuda",
+                 ws_fill: Optional[int] = None):
+        """fused_head: None picks the two-row pass when the PDM shares the target's head.
+        ws_fill: a byte value written over the whole workspace before spd_init (0xFF makes every
+        float the library has not written a NaN; for tests that nothing stale is read)."""
         if not torch.cuda.is_available():
             raise RuntimeError("Engine needs a GPU: the SPD step has no CPU path")
         n = weights.shape.n_stages if n is None else n
@@ -142,6 +145,8 @@ class Engine:
         self.n = n
         nbytes = B.spd_workspace_size(self.cfg)
         self.ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+        if ws_fill is not None:
+            self.ws.fill_(int(ws_fill))
         base = self.ws.data_ptr()
         aligned = (base + 255) // 256 * 256
         # default priority streams only
