@@ -109,9 +109,9 @@ __device__ __forceinline__ void lds_row(const T* p, float* o) {
 
 // Merge of one (token, KV head)'s nsplit split records (o[8][DH], m[8], l[8]; every split has a key,
 // so each m is finite) in split order into its G output rows. Every thread of the workgroup calls it.
-// All (m, l) pairs are requested first, then the first batch of partial outputs (split indices
-// clamped, so the loads are unconditional), then the (m, l) pairs go to LDS (sm: 2 * kMaxSplits *
-// kAttnMaxQ floats).
+// All (m, l) pairs are requested first, then the first batch of partial outputs (only the entries
+// that exist: the records are read past the L2, where a repeated address costs as much as a new
+// one), then the (m, l) pairs go to LDS (sm: 2 * kMaxSplits * kAttnMaxQ floats).
 template <int DH>
 __device__ __forceinline__ void attn_merge(const float* rec_base, int nsplit, int G, float* out, float* sm) {
   constexpr int MAXQ = kAttnMaxQ, RS = MAXQ * (DH + 2);
@@ -124,15 +124,19 @@ __device__ __forceinline__ void attn_merge(const float* rec_base, int nsplit, in
   float mlm[MLT], mll[MLT];
 #pragma unroll
   for (int i = 0; i < MLT; i++) {
-    const int t = min(tid + i * kWG, nsplit * G - 1), sp = t / G, qi = t % G;
-    mlm[i] = ld_dev(rec_base + (size_t)sp * RS + MAXQ * DH + qi);
-    mll[i] = ld_dev(rec_base + (size_t)sp * RS + MAXQ * DH + MAXQ + qi);
+    const int t = tid + i * kWG, sp = t / G, qi = t % G;
+    mlm[i] = mll[i] = 0.f;
+    if (t < nsplit * G) {
+      mlm[i] = ld_dev(rec_base + (size_t)sp * RS + MAXQ * DH + qi);
+      mll[i] = ld_dev(rec_base + (size_t)sp * RS + MAXQ * DH + MAXQ + qi);
+    }
   }
   const int qi0 = tid / (DH / 2), dp0 = tid % (DH / 2);
   const int qc0 = min(qi0, G - 1);
   float2 ob[MB];
 #pragma unroll
-  for (int j = 0; j < MB; j++) ob[j] = ld_dev2(rec_base + (size_t)min(j, nsplit - 1) * RS + qc0 * DH + 2 * dp0);
+  for (int j = 0; j < MB; j++)
+    ob[j] = (j < nsplit && qi0 < G) ? ld_dev2(rec_base + (size_t)j * RS + qc0 * DH + 2 * dp0) : make_float2(0.f, 0.f);
 #pragma unroll
   for (int i = 0; i < MLT; i++) {
     const int t = tid + i * kWG;
